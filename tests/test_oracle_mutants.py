@@ -1,0 +1,93 @@
+"""The oracle's pins must catch plausible mistakes.
+
+Each case plants one mistake in a copy of the oracle's C source (a dropped
+term, an off-by-one bound, a wrong divisor, a transposed column, a wrong
+exponent bias, a flipped sign, a lost shard offset ...), builds it on the CPU
+into a temporary directory and runs the pin checks of test_oracle_pins against
+it.  At least one check must fail for every mutant; the unmodified source must
+pass them all.
+"""
+import os
+import subprocess
+
+import numpy as np
+import pytest
+
+import oracle
+import test_oracle_pins as pins
+
+SRC = os.path.join(os.path.dirname(oracle.__file__), "eb_oracle.c")
+
+MUTANTS = {
+    "drop_last_index": ("for (int64_t k = s; k < e; ++k)", "for (int64_t k = s; k + 1 < e; ++k)"),
+    "shard_hi_inclusive": ("(i < shard_hi)", "(i <= shard_hi)"),
+    "table_bound_inclusive": ("(i < rows[t])", "(i <= rows[t])"),
+    "mean_over_hits": ("acc[c] / (double)L", "acc[c] / (double)(hits ? hits : 1)"),
+    "reversed_columns": ("int64_t k = r * D + c;", "int64_t k = r * D + (D - 1 - c);"),
+    "f16_exponent_bias": ("expo - 25", "expo - 24"),
+    "f16_subnormal_scale": ("ldexp((double)frac, -24)", "ldexp((double)frac, -25)"),
+    "bf16_shift": ("(uint32_t)h << 16", "(uint32_t)h << 15"),
+    "flipped_sign": ("acc[c] += w;", "acc[c] -= w;"),
+    "lost_shard_offset": ("int64_t r = i - shard_lo;", "int64_t r = i;"),
+    "magnitude_without_abs": ("mag[c] += fabs(w);", "mag[c] += w;"),
+    "bag_end_from_start": ("e = offsets[p + 1];", "e = offsets[p] + (offsets[p + 1] > offsets[p]);"),
+    "hits_once_per_bag": ("++hits;", "hits = 1;"),
+}
+
+
+def pin_checks():
+    """(name, callable) for a compact run of the pins."""
+    checks = []
+    for reading in ("reading_A", "reading_B"):
+        for mode in (oracle.SUM, oracle.MEAN):
+            checks.append((f"worked_{reading}_{mode}",
+                           lambda r=reading, m=mode: pins.test_worked_example(r, m)))
+    for dtype in (oracle.F32, oracle.F16, oracle.BF16):
+        for mode in (oracle.SUM, oracle.MEAN):
+            for seed in range(4):
+                checks.append((f"brute_{dtype}_{mode}_{seed}",
+                               lambda d=dtype, m=mode, s=seed: pins.test_brute_force(d, m, s)))
+        if dtype != oracle.F32:
+            checks.append((f"decode_{dtype}", lambda d=dtype: pins.test_decode_all_16bit_patterns(d)))
+        checks.append((f"copies_{dtype}", lambda d=dtype: pins.test_copies_of_one_row(d)))
+    checks.append(("shards", lambda: pins.test_shard_partials_add_up(3)))
+    checks.append(("empty", pins.test_empty_bags_pool_to_zero))
+    checks.append(("malformed", pins.test_malformed_offsets))
+    checks.append(("scipy", lambda: pins.test_scipy_csr_spmm(0)))
+    return checks
+
+
+def run_checks():
+    failed = []
+    for name, fn in pin_checks():
+        try:
+            fn()
+        except (AssertionError, ValueError):
+            failed.append(name)
+    return failed
+
+
+def build_variant(tmp_path, name, old, new):
+    src = open(SRC).read()
+    assert src.count(old) == 1, f"mutation site for {name} not unique"
+    path = tmp_path / f"{name}.c"
+    path.write_text(src.replace(old, new))
+    lib = tmp_path / f"lib{name}.so"
+    subprocess.run(["gcc", "-O2", "-std=c99", "-fPIC", "-shared", "-ffp-contract=off", str(path),
+                    "-o", str(lib), "-lm"], check=True)
+    return str(lib)
+
+
+def test_unmodified_source_passes(tmp_path):
+    lib = build_variant(tmp_path, "identity", "enum { ORACLE_SUM", "enum { ORACLE_SUM")
+    with oracle.using(lib):
+        assert run_checks() == []
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_mutant_is_caught(tmp_path, name):
+    old, new = MUTANTS[name]
+    lib = build_variant(tmp_path, name, old, new)
+    with np.errstate(all="ignore"), oracle.using(lib):
+        failed = run_checks()
+    assert failed, f"no pin caught the planted mistake {name!r}"
