@@ -1,0 +1,226 @@
+"""Benchmark: pooled embedding-bag lookups on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload N] [--dim D --dtype f16]
+
+A step is one eb_forward over one batch: CSR decode, shard filter, row gather,
+fp32 pooling and the output store, all in the HIP library.  The default
+workload is 8 tables of 1,000,000 x 128 fp32 rows, 2048 bags per table of 40
+uniform ids each (655,360 lookups per step).  Several independent index
+batches are prepared and cycled, so consecutive steps gather different rows
+and the 256 MB last-level cache cannot hold them; tables, ids and offsets are
+resident in HBM before the timed region starts.
+
+Prints one JSON line: lookups/s over the timed steps, the kernel's HBM
+roofline (algorithmic bytes per launch / mean kernel time from HIP events on
+the launch stream, against 8 TB/s) and the CPU oracle's rate on the host.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+from paper_2512_05831_amd import workloads as wl  # noqa: E402
+
+METRIC = "pooled lookups/sec + effective HBM GB/s (% of MI355X peak) per config"
+HBM_PEAK_GBPS = 8000.0
+KERNEL_SRC = os.path.join(ROOT, "paper_2512_05831_amd", "csrc", "eb.hip")
+PROFILES = os.path.join(ROOT, "profiles")
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def kernel_source_hash() -> str:
+    return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()[:16]
+
+
+def algorithmic_bytes(w, local_ids: int, nnz: int, with_hits: bool) -> int:
+    """Every gathered row once, every id and offset, the fp32 output (and the
+    int32 hit counts when written)."""
+    b = local_ids * w.D * w.elem_bytes + nnz * 8 + (w.T * w.B + 1) * 8 + w.B * w.T * w.D * 4
+    if with_hits:
+        b += w.B * w.T * 4
+    return int(b)
+
+
+def measured_traffic(workload_name: str):
+    """HBM bytes per launch from committed rocprofv3 counter summaries, or None
+    when none exists for this workload or the kernel source has changed."""
+    path = os.path.join(PROFILES, f"counters_{workload_name}.txt")
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    for line in open(path):
+        if ":" in line and not line.startswith("#"):
+            k, v = line.split(":", 1)
+            kv[k.strip()] = v.strip()
+    if kv.get("kernel_source_sha256") != kernel_source_hash():
+        return None
+    try:
+        fetch = float(kv["fetch_kib_per_dispatch"]) * 1024 * float(kv["copy_fetch_factor"])
+        write = float(kv["write_kib_per_dispatch"]) * 1024 * float(kv["copy_write_factor"])
+    except (KeyError, ValueError):
+        return None
+    return fetch + write
+
+
+def pick_workload(args):
+    if args.workload == 4:
+        w = wl.config(4, D=args.dim, dtype={"f16": wl.F16, "bf16": wl.BF16}[args.dtype])
+    else:
+        w = wl.config(args.workload)
+    return w
+
+
+def cpu_baseline(w, host_tables, batches, off, budget_s: float):
+    import oracle
+
+    lookups = 0
+    passes = 0
+    t0 = time.perf_counter()
+    while True:
+        idx = batches[passes % len(batches)]
+        oracle.forward(host_tables, [w.rows] * w.T, w.D, w.dtype, idx, off, w.B, w.modes[0],
+                       w.shard_lo, w.shard_hi)
+        lookups += idx.size
+        passes += 1
+        if time.perf_counter() - t0 >= budget_s:
+            break
+    dt = time.perf_counter() - t0
+    return {"value": lookups / dt, "unit": "lookups/s", "cores": 1, "kind": "oracle",
+            "sample": f"{passes} full batch(es) of this workload ({lookups} lookups), "
+                      f"single-threaded fp64 C loop, {dt:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=400)
+    ap.add_argument("--warmup", type=int, default=40)
+    ap.add_argument("--workload", type=int, default=2, choices=[1, 2, 3, 4, 5])
+    ap.add_argument("--dim", type=int, default=128)
+    ap.add_argument("--dtype", default="f16", choices=["f16", "bf16"])
+    ap.add_argument("--batches", type=int, default=8, help="distinct index batches cycled")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
+              "(the sharded multi-GPU pipeline is not part of this library)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2512_05831_amd import eb
+
+    dev = torch.device("cuda:0")
+    w = pick_workload(args)
+    mode = w.modes[0]
+    log(f"bench: workload {w.name}, generating inputs")
+    off = w.offsets()
+    batches = [w.with_(seed=w.seed + 7919 * j).indices(off) if j else w.indices(off)
+               for j in range(args.batches)]
+    host_tables = []
+    dev_tables = []
+    tdt = {wl.F32: torch.float32, wl.F16: torch.float16, wl.BF16: torch.bfloat16}[w.dtype]
+    for t in range(w.T):
+        h = w.table(t)
+        d = torch.from_numpy(h.view(np.int16) if h.dtype == np.uint16 else h).to(dev).view(tdt)
+        host_tables.append(h)
+        dev_tables.append(d)
+    log(f"bench: tables resident ({sum(d.numel() * d.element_size() for d in dev_tables) / 1e9:.2f} GB)")
+
+    et = eb.EmbeddingBagTables(dev_tables, rows=[w.rows] * w.T, shard_lo=w.shard_lo,
+                               shard_hi=w.shard_hi)
+    stream = torch.cuda.Stream(dev)
+    d_off = torch.from_numpy(off).to(dev)
+    d_idx = [torch.from_numpy(b).to(dev) for b in batches]
+    out = torch.empty((w.B, w.T * w.D), dtype=torch.float32, device=dev)
+    hits = torch.empty((w.B, w.T), dtype=torch.int32, device=dev) if w.want_hits else None
+    calls = [et.prepare(i, d_off, w.B, mode, out, hits, stream) for i in d_idx]
+    local = [int(np.count_nonzero((b >= w.shard_lo) & (b < w.local_hi))) for b in batches]
+    nnz = [int(b.size) for b in batches]
+    torch.cuda.synchronize()
+
+    K, W = args.steps, args.warmup
+    with torch.cuda.stream(stream):
+        for i in range(W):
+            calls[i % len(calls)]()
+        torch.cuda.synchronize()
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(K)]
+        t_start = time.perf_counter()
+        for i in range(K):
+            ev[i][0].record(stream)
+            calls[i % len(calls)]()
+            ev[i][1].record(stream)
+        torch.cuda.synchronize()
+        t_end = time.perf_counter()
+    kernel_ms = np.array([a.elapsed_time(b) for a, b in ev])
+    wall_ms = (t_end - t_start) * 1e3
+    ms_per_step = wall_ms / K
+
+    steps_lookups = sum(nnz[i % len(nnz)] for i in range(K))
+    steps_bytes = sum(algorithmic_bytes(w, local[i % len(local)], nnz[i % len(nnz)], hits is not None)
+                      for i in range(K))
+    value = steps_lookups / (wall_ms / 1e3)
+    achieved = steps_bytes / (kernel_ms.sum() / 1e3) / 1e9
+    bytes_per_launch = steps_bytes / K
+    traffic = measured_traffic(w.name)
+    log(f"bench: kernel mean {kernel_ms.mean() * 1e3:.1f} us (p10 {np.percentile(kernel_ms, 10) * 1e3:.1f}, "
+        f"p90 {np.percentile(kernel_ms, 90) * 1e3:.1f}), step {ms_per_step * 1e3:.1f} us, "
+        f"{achieved:.0f} GB/s algorithmic")
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("bench: timing the CPU oracle")
+        cpu = cpu_baseline(w, host_tables, batches, off, args.cpu_seconds)
+
+    line = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "lookups/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": W,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": wl.DTYPE_NAMES[w.dtype],
+        "data": "synthetic",
+        "config": {"workload": w.name, "tables": w.T, "rows": w.rows, "D": w.D,
+                   "storage": wl.DTYPE_NAMES[w.dtype], "accumulate": "f32", "B": w.B,
+                   "lengths": (f"fixed {w.L}" if w.lengths_kind == "fixed" else
+                               f"0 w.p. {w.p_empty} else U[{w.L_lo},{w.L_hi}]"),
+                   "ids": (w.dist if w.dist == "uniform" else
+                           f"zipf({w.alpha}){' permuted' if w.permuted else ''}"),
+                   "shard": None if not w.sharded else [w.shard_lo, w.shard_hi],
+                   "mode": "sum" if mode == wl.SUM else "mean",
+                   "index_batches_cycled": len(batches)},
+        "bags_per_s": w.T * w.B / (ms_per_step / 1e3),
+        "kernel_us_mean": float(kernel_ms.mean() * 1e3),
+        "effective_GBps": achieved,
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBPS,
+                     "algorithmic_bytes_per_launch": bytes_per_launch,
+                     "traffic": traffic},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+    et.close()
+
+
+if __name__ == "__main__":
+    main()

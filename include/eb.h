@@ -1,0 +1,153 @@
+/*
+ * eb.h -- Embedding Bag forward pass for AMD Instinct MI355X (gfx950).
+ *
+ * The operation (Ambati, Ding, Diep, "Dissecting Embedding Bag Performance in
+ * DLRM Inference", arXiv 2512.05831):
+ *
+ *   Sec. 4.1  An Embedding Bag sums, for one inference, the rows of an
+ *             embedding table named by that inference's categorical ids
+ *             ("sum pooling"); the number of rows is the pooling size.
+ *   Sec. 4.2  The categorical input of one table is an array of row indices
+ *             plus an array of lengths, one length per inference of the
+ *             mini-batch; every table carries such a pair.
+ *   Sec. 4.1, 4.2, 4.3
+ *             Under row-wise parallelism each GPU stores one contiguous,
+ *             even block of every table's rows, gathers and pools only the
+ *             indices that fall in its block, and hands its partial sums to
+ *             a reduce-scatter that adds them across GPUs.
+ *
+ * This library is one GPU's share of that operator: for every (table t,
+ * bag b) it gathers the rows of t named by the bag's indices that lie in the
+ * caller's row shard [shard_lo, shard_hi), accumulates them in fp32 and
+ * writes the D-wide result.  An unsharded call passes shard_lo = 0 and
+ * shard_hi = INT64_MAX.
+ *
+ * Conventions used by every entry point
+ *   - Return value: EB_OK (0) or a negative EB_ERR_* code; eb_last_error()
+ *     then returns a message for the calling thread.  No entry point throws.
+ *   - Lengths arrive as offsets, their exclusive prefix sum (CSR form).  For
+ *     T tables and B bags per table, offsets has T*B+1 int64 entries and bag
+ *     (t, b) owns the index positions [offsets[t*B+b], offsets[t*B+b+1]),
+ *     so the indices of table 0 come first, then those of table 1, ...
+ *   - Offsets are clamped into [0, nnz]; a bag whose end precedes its start is
+ *     empty.  The bag length L (used by mean pooling) is the number of index
+ *     positions the bag owns after clamping.
+ *   - An index i of table t is gathered iff 0 <= i < rows[t] and
+ *     shard_lo <= i < shard_hi; it then reads stored row i - shard_lo.  Other
+ *     indices contribute nothing and are not counted as hits.  Duplicates
+ *     count with multiplicity.
+ *   - Device buffers are borrowed: the caller owns and frees them, and must
+ *     keep table memory alive while a handle that names it is in use.
+ */
+#ifndef EB_H
+#define EB_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Element type of the stored tables.  Accumulation and output are fp32. */
+enum { EB_F32 = 0, EB_F16 = 1, EB_BF16 = 2 };
+
+/* Pooling.  EB_MEAN divides the bag's sum by its length L (an empty bag
+ * pools to 0); with a shard, each GPU's partial means then add up to the
+ * mean over all GPUs. */
+enum { EB_SUM = 0, EB_MEAN = 1 };
+
+/* Return codes. */
+enum {
+    EB_OK = 0,
+    EB_ERR_INVALID = -1,     /* an argument violates this header's contract */
+    EB_ERR_UNSUPPORTED = -2, /* valid, but beyond a documented limit        */
+    EB_ERR_HIP = -3,         /* the HIP runtime refused a launch            */
+    EB_ERR_NOMEM = -4        /* host allocation of the handle failed        */
+};
+
+typedef struct eb_tables eb_tables;
+
+/*
+ * eb_create_tables -- describe T embedding tables resident on the device
+ * (Sec. 4.1: one table per sparse feature, rows x D; Sec. 4.2 / 4.3: a
+ * row-wise shard stores a contiguous block of each table's rows).
+ *
+ *   T            number of tables, >= 1.
+ *   table_ptrs   host array [T] of device pointers.  Table t is row-major
+ *                [stored_rows[t], D] of `dtype` elements, rows packed with
+ *                pitch D elements.  BORROWED: not copied, not freed.
+ *   stored_rows  host array [T]: rows physically present for table t
+ *                (>= 0).  Copied.
+ *   D            embedding dimension (row width in elements), >= 1.
+ *   dtype        EB_F32, EB_F16 or EB_BF16.
+ *   out_handle   receives the new handle.
+ *
+ * Touches no device state and allocates no device memory; the handle holds
+ * host copies of the pointers and row counts only.  Returns EB_ERR_INVALID
+ * for a NULL pointer, T < 1, D < 1, an unknown dtype, a negative row count,
+ * or a NULL table pointer with stored_rows > 0; EB_ERR_NOMEM if the host
+ * allocation fails.
+ */
+int eb_create_tables(int32_t T, const void *const *table_ptrs, const int64_t *stored_rows,
+                     int32_t D, int32_t dtype, eb_tables **out_handle);
+
+/*
+ * eb_forward -- pooled embedding lookups for the first T tables of a handle
+ * (Sec. 4.1 sum pooling over the Sec. 4.2 indices / lengths input, restricted
+ * to one row-wise shard as in Sec. 4.1 / 4.3).
+ *
+ *   tables     handle from eb_create_tables.
+ *   T          tables pooled by this call, 0 <= T <= the handle's T.
+ *   rows       host array [T]: logical (global) row count of table t; an
+ *              index >= rows[t] is out of range and skipped.
+ *   D, dtype   must equal the handle's.
+ *   indices    device int64 [nnz] row ids, table-major (see above).
+ *   nnz        number of entries in indices, >= 0.
+ *   offsets    device int64 [T*B+1], see above.
+ *   B          bags per table (the mini-batch size), >= 0.
+ *   mode       EB_SUM or EB_MEAN.
+ *   shard_lo, shard_hi
+ *              this GPU's row range [shard_lo, shard_hi), 0 <= lo <= hi.
+ *              For every t, stored_rows[t] must cover the rows
+ *              [shard_lo, min(shard_hi, rows[t])).
+ *   out        device fp32 [B, T*D] row-major: bag b of table t goes to
+ *              out[b*T*D + t*D + c], c < D.  Every element is written.
+ *   hits       device int32 [B, T] or NULL: hits[b*T + t] = number of the
+ *              bag's indices that were gathered here.
+ *   stream     a hipStream_t (NULL = the null stream).  The work is enqueued
+ *              on it and the call returns without waiting.
+ *
+ * No host synchronisation, no allocation.  T == 0 or B == 0 is a successful
+ * no-op.  Index and offset contents are not validated: any values are safe
+ * (the rules above keep every read in bounds) but the caller must size the
+ * buffers as stated.  Device faults surface at the caller's next
+ * synchronisation of `stream`.
+ *
+ * Errors: EB_ERR_INVALID for NULL handle/rows/offsets/out (or indices with
+ * nnz > 0), T out of range, D or dtype differing from the handle, an unknown
+ * mode, a bad shard range, negative rows[t] / nnz / B, stored rows that do
+ * not cover the shard, or B*T*D overflowing int64.  EB_ERR_UNSUPPORTED when a
+ * table's gatherable rows (min(shard_hi, rows[t]) - shard_lo) exceed
+ * 4,294,967,294.  EB_ERR_HIP when a kernel launch fails.
+ *
+ * Thread safety: the handle is read-only after creation; concurrent calls on
+ * different streams are safe.
+ */
+int eb_forward(const eb_tables *tables, int32_t T, const int64_t *rows, int32_t D, int32_t dtype,
+               const int64_t *indices, int64_t nnz, const int64_t *offsets, int64_t B,
+               int32_t mode, int64_t shard_lo, int64_t shard_hi, float *out, int32_t *hits,
+               void *stream);
+
+/* eb_destroy -- free a handle (never the tables).  NULL is a no-op. */
+void eb_destroy(eb_tables *tables);
+
+/* eb_last_error -- message for the calling thread's most recent failed call,
+ * or "" if none has failed.  Owned by the library, valid until the thread's
+ * next call into it. */
+const char *eb_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* EB_H */

@@ -1,0 +1,180 @@
+"""Python binding of the C ABI in ``include/eb.h`` (ctypes, marshalling only).
+
+The functions carry the C names and arguments; every step of the pass runs in
+the HIP library ``libeb.so``.  There is no fallback: if the library cannot be
+loaded the import of a function fails with an error.
+
+``EmbeddingBagTables`` is a thin convenience over the same calls for torch
+device tensors: it keeps the table tensors alive and passes their pointers and
+the current HIP stream.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+from . import build as _build
+
+EB_F32, EB_F16, EB_BF16 = 0, 1, 2
+EB_SUM, EB_MEAN = 0, 1
+EB_OK, EB_ERR_INVALID, EB_ERR_UNSUPPORTED, EB_ERR_HIP, EB_ERR_NOMEM = 0, -1, -2, -3, -4
+INT64_MAX = (1 << 63) - 1
+
+LIB_PATH = _build.LIB
+
+
+class EbError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"[{code}] {msg}")
+        self.code = code
+
+
+_lib = None
+
+
+def library() -> ctypes.CDLL:
+    """Load libeb.so, building it first only if it is not there."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            _build.build_library()
+        lib = ctypes.CDLL(LIB_PATH)
+        p, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+        lib.eb_create_tables.argtypes = [i32, p, p, i32, i32, ctypes.POINTER(p)]
+        lib.eb_create_tables.restype = ctypes.c_int
+        lib.eb_forward.argtypes = [p, i32, p, i32, i32, p, i64, p, i64, i32, i64, i64, p, p, p]
+        lib.eb_forward.restype = ctypes.c_int
+        lib.eb_destroy.argtypes = [p]
+        lib.eb_destroy.restype = None
+        lib.eb_last_error.argtypes = []
+        lib.eb_last_error.restype = ctypes.c_char_p
+        _lib = lib
+    return _lib
+
+
+def eb_last_error() -> str:
+    return library().eb_last_error().decode()
+
+
+def _check(rc: int) -> None:
+    if rc != EB_OK:
+        raise EbError(rc, eb_last_error())
+
+
+def _i64_array(values):
+    values = list(values)
+    return (ctypes.c_int64 * max(1, len(values)))(*values)
+
+
+def eb_create_tables(table_ptrs, stored_rows, D: int, dtype: int, T: int | None = None):
+    """Returns an opaque handle (ctypes.c_void_p).  ``table_ptrs``: device
+    addresses as ints; ``stored_rows``: rows stored per table."""
+    table_ptrs = list(table_ptrs)
+    T = len(table_ptrs) if T is None else T
+    ptrs = (ctypes.c_void_p * max(1, len(table_ptrs)))(*table_ptrs)
+    rows = _i64_array(stored_rows)
+    h = ctypes.c_void_p()
+    _check(library().eb_create_tables(T, ptrs, rows, D, dtype, ctypes.byref(h)))
+    return h
+
+
+def eb_forward(handle, T: int, rows, D: int, dtype: int, indices_ptr: int, nnz: int,
+               offsets_ptr: int, B: int, mode: int, shard_lo: int, shard_hi: int, out_ptr: int,
+               hits_ptr: int | None, stream_ptr: int | None) -> None:
+    """Enqueue the pass on ``stream_ptr`` (a hipStream_t as int).  Raises EbError."""
+    _check(library().eb_forward(handle, T, _i64_array(rows), D, dtype, indices_ptr, nnz,
+                                offsets_ptr, B, mode, shard_lo, shard_hi, out_ptr,
+                                hits_ptr or None, stream_ptr or None))
+
+
+def eb_destroy(handle) -> None:
+    library().eb_destroy(handle)
+
+
+_TORCH_DTYPE_CODES = {"torch.float32": EB_F32, "torch.float16": EB_F16, "torch.bfloat16": EB_BF16}
+
+
+class EmbeddingBagTables:
+    """Tables held as torch device tensors [stored_rows, D] of one dtype."""
+
+    def __init__(self, tables, rows=None, shard_lo: int = 0, shard_hi: int = INT64_MAX):
+        import torch  # noqa: F401  (device memory and streams only)
+
+        self.tables = list(tables)
+        if not self.tables:
+            raise ValueError("need at least one table")
+        t0 = self.tables[0]
+        self.D = int(t0.shape[1])
+        self.dtype = _TORCH_DTYPE_CODES[str(t0.dtype)]
+        for w in self.tables:
+            if w.dim() != 2 or w.shape[1] != self.D or w.dtype != t0.dtype or not w.is_cuda:
+                raise ValueError("tables must be 2-D device tensors of one dtype and width")
+            if not w.is_contiguous():
+                raise ValueError("tables must be contiguous")
+        self.T = len(self.tables)
+        self.stored_rows = [int(w.shape[0]) for w in self.tables]
+        self.rows = list(rows) if rows is not None else [shard_lo + n for n in self.stored_rows]
+        self.shard_lo, self.shard_hi = int(shard_lo), int(shard_hi)
+        self.handle = eb_create_tables([w.data_ptr() for w in self.tables], self.stored_rows,
+                                       self.D, self.dtype)
+
+    def forward(self, indices, offsets, B: int, mode: int = EB_SUM, out=None, hits=None,
+                stream=None):
+        """indices int64 [nnz], offsets int64 [T*B+1] on the device.  Returns out
+        (fp32 [B, T*D]) and hits (int32 [B, T]) when ``hits`` is True or a tensor."""
+        import torch
+
+        dev = self.tables[0].device
+        if out is None:
+            out = torch.empty((B, self.T * self.D), dtype=torch.float32, device=dev)
+        want_hits = hits is not None and hits is not False
+        if hits is True:
+            hits = torch.empty((B, self.T), dtype=torch.int32, device=dev)
+        if stream is None:
+            stream = torch.cuda.current_stream(dev)
+        for tnsr, dt in ((indices, torch.int64), (offsets, torch.int64)):
+            if tnsr.dtype != dt or not tnsr.is_contiguous():
+                raise ValueError("indices / offsets must be contiguous int64")
+        if offsets.numel() != self.T * B + 1:
+            raise ValueError("offsets must have T*B+1 entries")
+        if out.dtype != torch.float32 or not out.is_contiguous() or out.numel() < B * self.T * self.D:
+            raise ValueError("out must be contiguous fp32 [B, T*D]")
+        if want_hits and (hits.dtype != torch.int32 or hits.numel() < B * self.T):
+            raise ValueError("hits must be int32 [B, T]")
+        eb_forward(self.handle, self.T, self.rows, self.D, self.dtype, indices.data_ptr(),
+                   indices.numel(), offsets.data_ptr(), B, mode, self.shard_lo, self.shard_hi,
+                   out.data_ptr(), hits.data_ptr() if want_hits else None, stream.cuda_stream)
+        return (out, hits) if want_hits else out
+
+    def prepare(self, indices, offsets, B: int, mode: int, out, hits=None, stream=None):
+        """Marshal the arguments of one eb_forward call once; the returned
+        function enqueues that call (on ``stream``) each time it is invoked."""
+        import torch
+
+        if stream is None:
+            stream = torch.cuda.current_stream(self.tables[0].device)
+        if offsets.numel() != self.T * B + 1 or out.numel() < B * self.T * self.D:
+            raise ValueError("offsets / out do not match T, B, D")
+        lib = library()
+        args = (self.handle, self.T, _i64_array(self.rows), self.D, self.dtype,
+                indices.data_ptr(), indices.numel(), offsets.data_ptr(), B, mode, self.shard_lo,
+                self.shard_hi, out.data_ptr(), hits.data_ptr() if hits is not None else None,
+                stream.cuda_stream)
+        keep = (indices, offsets, out, hits)
+
+        def call():
+            _check(lib.eb_forward(*args))
+            return keep
+
+        return call
+
+    def close(self):
+        if getattr(self, "handle", None) is not None:
+            eb_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

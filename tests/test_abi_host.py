@@ -1,0 +1,130 @@
+"""The C-ABI library on the host: it loads, exports what include/eb.h declares,
+and rejects bad arguments with the documented codes before touching a device.
+
+No call here reaches a kernel launch: every forward below either fails
+validation or is a documented no-op (T == 0 or B == 0).
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2512_05831_amd import eb
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "eb.h")
+FAKE = 0x7F0000000000  # 16-byte aligned, never dereferenced by these tests
+I64MAX = (1 << 63) - 1
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(eb_\w+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    assert declared_functions() == ["eb_create_tables", "eb_destroy", "eb_forward", "eb_last_error"]
+
+
+def test_library_exports_every_declared_symbol():
+    lib = eb.library()
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def handle(T=2, D=16, dtype=eb.EB_F32, rows=(100, 100)):
+    return eb.eb_create_tables([FAKE] * T, list(rows), D, dtype)
+
+
+def forward(h, **kw):
+    args = dict(T=2, rows=[100, 100], D=16, dtype=eb.EB_F32, indices_ptr=FAKE, nnz=10,
+                offsets_ptr=FAKE, B=4, mode=eb.EB_SUM, shard_lo=0, shard_hi=I64MAX,
+                out_ptr=FAKE, hits_ptr=None, stream_ptr=None)
+    args.update(kw)
+    return eb.eb_forward(h, **args)
+
+
+def code_of(fn):
+    with pytest.raises(eb.EbError) as e:
+        fn()
+    return e.value.code
+
+
+def test_create_rejects_bad_arguments():
+    lib = eb.library()
+    assert lib.eb_create_tables(1, None, None, 4, 0, None) == eb.EB_ERR_INVALID
+    assert code_of(lambda: eb.eb_create_tables([FAKE], [10], 4, eb.EB_F32, T=0)) == eb.EB_ERR_INVALID
+    assert code_of(lambda: eb.eb_create_tables([FAKE], [10], 0, eb.EB_F32)) == eb.EB_ERR_INVALID
+    assert code_of(lambda: eb.eb_create_tables([FAKE], [10], 4, 3)) == eb.EB_ERR_INVALID
+    assert code_of(lambda: eb.eb_create_tables([FAKE], [-1], 4, eb.EB_F32)) == eb.EB_ERR_INVALID
+    assert code_of(lambda: eb.eb_create_tables([0], [5], 4, eb.EB_F32)) == eb.EB_ERR_INVALID
+    assert "dtype" in eb.eb_last_error() or "NULL" in eb.eb_last_error()
+    h = eb.eb_create_tables([0], [0], 4, eb.EB_BF16)  # empty table may have no memory
+    eb.eb_destroy(h)
+
+
+def test_destroy_null_is_noop():
+    eb.library().eb_destroy(None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(T=3), eb.EB_ERR_INVALID),                       # more tables than the handle
+    (dict(T=-1), eb.EB_ERR_INVALID),
+    (dict(D=8), eb.EB_ERR_INVALID),                       # differs from the handle
+    (dict(dtype=eb.EB_F16), eb.EB_ERR_INVALID),
+    (dict(mode=2), eb.EB_ERR_INVALID),
+    (dict(nnz=-1), eb.EB_ERR_INVALID),
+    (dict(B=-1), eb.EB_ERR_INVALID),
+    (dict(shard_lo=-1), eb.EB_ERR_INVALID),
+    (dict(shard_lo=10, shard_hi=5), eb.EB_ERR_INVALID),
+    (dict(offsets_ptr=None), eb.EB_ERR_INVALID),
+    (dict(out_ptr=None), eb.EB_ERR_INVALID),
+    (dict(indices_ptr=None), eb.EB_ERR_INVALID),
+    (dict(rows=[100, 101]), eb.EB_ERR_INVALID),           # stored rows do not cover table 1
+    (dict(rows=[100, -1]), eb.EB_ERR_INVALID),
+    (dict(shard_lo=50, shard_hi=200, rows=[100, 160]), eb.EB_ERR_INVALID),
+    (dict(B=1 << 62), eb.EB_ERR_INVALID),                 # B*T*D overflows
+])
+def test_forward_rejects(kw, code):
+    h = handle()
+    try:
+        assert code_of(lambda: forward(h, **kw)) == code
+        assert eb.eb_last_error()
+    finally:
+        eb.eb_destroy(h)
+
+
+def test_forward_null_handle():
+    assert code_of(lambda: forward(None)) == eb.EB_ERR_INVALID
+
+
+def test_forward_noops_touch_nothing():
+    h = handle()
+    try:
+        forward(h, B=0)
+        forward(h, T=0, rows=[])
+        forward(h, B=0, indices_ptr=None, nnz=0, offsets_ptr=None, out_ptr=None)
+    finally:
+        eb.eb_destroy(h)
+
+
+def test_forward_too_many_local_rows():
+    n = 0xFFFFFFFF  # one more than the 32-bit local-row limit
+    h = eb.eb_create_tables([FAKE], [n], 1, eb.EB_F16)
+    try:
+        assert code_of(lambda: forward(h, T=1, rows=[n], D=1, dtype=eb.EB_F16)) == eb.EB_ERR_UNSUPPORTED
+        assert "4294967294" in eb.eb_last_error()
+    finally:
+        eb.eb_destroy(h)
+
+
+def test_error_message_is_per_failure():
+    h = handle()
+    try:
+        code_of(lambda: forward(h, D=8))
+        assert "D" in eb.eb_last_error()
+        code_of(lambda: forward(h, mode=9))
+        assert "mode" in eb.eb_last_error()
+    finally:
+        eb.eb_destroy(h)
