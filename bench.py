@@ -10,9 +10,14 @@ batches are prepared and cycled, so consecutive steps gather different rows
 and the 256 MB last-level cache cannot hold them; tables, ids and offsets are
 resident in HBM before the timed region starts.
 
-Prints one JSON line: lookups/s over the timed steps, the kernel's HBM
-roofline (algorithmic bytes per launch / mean kernel time from HIP events on
-the launch stream, against 8 TB/s) and the CPU oracle's rate on the host.
+Uniform ids have no reuse, so those workloads pass the streaming cache hint
+(EB_HINT_STREAM_ROWS: rows read with non-temporal loads); skewed ids keep the
+default cached loads.  ``--rows-policy cached|stream`` overrides the choice.
+
+Prints one JSON line: lookups/s over the timed steps (wall clock between two
+device synchronisations), the kernel's HBM roofline (algorithmic bytes per
+launch / mean launch duration, from HIP events on the launch stream around the
+K back-to-back launches, against 8 TB/s) and the CPU oracle's rate on the host.
 """
 from __future__ import annotations
 
@@ -56,7 +61,7 @@ def algorithmic_bytes(w, local_ids: int, nnz: int, with_hits: bool) -> int:
 def measured_traffic(workload_name: str):
     """HBM bytes per launch from committed rocprofv3 counter summaries, or None
     when none exists for this workload or the kernel source has changed."""
-    path = os.path.join(PROFILES, f"counters_{workload_name}.txt")
+    path = os.path.join(PROFILES, f"eb_gather_team__{workload_name}__counters.txt")
     if not os.path.exists(path):
         return None
     kv = {}
@@ -102,6 +107,27 @@ def cpu_baseline(w, host_tables, batches, off, budget_s: float):
                       f"single-threaded fp64 C loop, {dt:.1f} s"}
 
 
+def copy_calibration(torch, dev, nbytes: int, steps: int):
+    """A plain elementwise copy (dst = -src, fp32) of known size: each launch
+    reads nbytes and writes nbytes.  The HBM counters read for it give the
+    factor that turns counter units into bytes."""
+    src = torch.ones(nbytes // 4, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    for _ in range(5):
+        torch.neg(src, out=dst)
+    torch.cuda.synchronize()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev0.record()
+    for _ in range(steps):
+        torch.neg(src, out=dst)
+    ev1.record()
+    torch.cuda.synchronize()
+    us = ev0.elapsed_time(ev1) * 1e3 / steps
+    print(json.dumps({"copy_bytes_read": nbytes, "copy_bytes_written": nbytes,
+                      "launches": steps + 5, "us_per_launch": us,
+                      "GBps_read_plus_write": 2 * nbytes / us / 1e3}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -113,6 +139,9 @@ def main():
     ap.add_argument("--batches", type=int, default=8, help="distinct index batches cycled")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--rows-policy", default="auto", choices=["auto", "cached", "stream"])
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
+                    help="only run a plain streaming copy of BYTES (for scaling HBM counters)")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -125,8 +154,14 @@ def main():
     from paper_2512_05831_amd import eb
 
     dev = torch.device("cuda:0")
+    if args.copy_calibration:
+        copy_calibration(torch, dev, args.copy_calibration, args.steps)
+        return
     w = pick_workload(args)
     mode = w.modes[0]
+    stream_rows = (args.rows_policy == "stream" or
+                   (args.rows_policy == "auto" and w.dist == "uniform"))
+    call_mode = mode | (eb.EB_HINT_STREAM_ROWS if stream_rows else 0)
     log(f"bench: workload {w.name}, generating inputs")
     off = w.offsets()
     batches = [w.with_(seed=w.seed + 7919 * j).indices(off) if j else w.indices(off)
@@ -148,7 +183,7 @@ def main():
     d_idx = [torch.from_numpy(b).to(dev) for b in batches]
     out = torch.empty((w.B, w.T * w.D), dtype=torch.float32, device=dev)
     hits = torch.empty((w.B, w.T), dtype=torch.int32, device=dev) if w.want_hits else None
-    calls = [et.prepare(i, d_off, w.B, mode, out, hits, stream) for i in d_idx]
+    calls = [et.prepare(i, d_off, w.B, call_mode, out, hits, stream) for i in d_idx]
     local = [int(np.count_nonzero((b >= w.shard_lo) & (b < w.local_hi))) for b in batches]
     nnz = [int(b.size) for b in batches]
     torch.cuda.synchronize()
@@ -158,16 +193,16 @@ def main():
         for i in range(W):
             calls[i % len(calls)]()
         torch.cuda.synchronize()
-        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-              for _ in range(K)]
+        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         t_start = time.perf_counter()
+        ev0.record(stream)
         for i in range(K):
-            ev[i][0].record(stream)
             calls[i % len(calls)]()
-            ev[i][1].record(stream)
+        ev1.record(stream)
         torch.cuda.synchronize()
         t_end = time.perf_counter()
-    kernel_ms = np.array([a.elapsed_time(b) for a, b in ev])
+    region_ms = ev0.elapsed_time(ev1)
+    launch_ms = region_ms / K  # mean launch duration (back-to-back launches)
     wall_ms = (t_end - t_start) * 1e3
     ms_per_step = wall_ms / K
 
@@ -175,12 +210,11 @@ def main():
     steps_bytes = sum(algorithmic_bytes(w, local[i % len(local)], nnz[i % len(nnz)], hits is not None)
                       for i in range(K))
     value = steps_lookups / (wall_ms / 1e3)
-    achieved = steps_bytes / (kernel_ms.sum() / 1e3) / 1e9
+    achieved = steps_bytes / (region_ms / 1e3) / 1e9
     bytes_per_launch = steps_bytes / K
     traffic = measured_traffic(w.name)
-    log(f"bench: kernel mean {kernel_ms.mean() * 1e3:.1f} us (p10 {np.percentile(kernel_ms, 10) * 1e3:.1f}, "
-        f"p90 {np.percentile(kernel_ms, 90) * 1e3:.1f}), step {ms_per_step * 1e3:.1f} us, "
-        f"{achieved:.0f} GB/s algorithmic")
+    log(f"bench: mean launch {launch_ms * 1e3:.1f} us over {K} back-to-back launches, "
+        f"wall step {ms_per_step * 1e3:.1f} us, {achieved:.0f} GB/s algorithmic")
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -208,9 +242,10 @@ def main():
                            f"zipf({w.alpha}){' permuted' if w.permuted else ''}"),
                    "shard": None if not w.sharded else [w.shard_lo, w.shard_hi],
                    "mode": "sum" if mode == wl.SUM else "mean",
+                   "rows_cache_policy": "stream" if stream_rows else "cached",
                    "index_batches_cycled": len(batches)},
         "bags_per_s": w.T * w.B / (ms_per_step / 1e3),
-        "kernel_us_mean": float(kernel_ms.mean() * 1e3),
+        "kernel_us_mean": launch_ms * 1e3,
         "effective_GBps": achieved,
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBPS,

@@ -56,6 +56,14 @@ enum { EB_F32 = 0, EB_F16 = 1, EB_BF16 = 2 };
  * mean over all GPUs. */
 enum { EB_SUM = 0, EB_MEAN = 1 };
 
+/* Cache hint, OR-ed into eb_forward's `mode`.  EB_HINT_STREAM_ROWS reads the
+ * embedding rows with non-temporal loads, which do not keep them in L2 or the
+ * last-level cache.  That is faster when ids have little reuse (for example
+ * drawn uniformly from tables much larger than the 256 MB last-level cache)
+ * and slower when they are skewed (hot rows then miss the caches).  It
+ * changes no result.  Rows narrower than 64 bytes ignore it. */
+enum { EB_HINT_STREAM_ROWS = 0x100 };
+
 /* Return codes. */
 enum {
     EB_OK = 0,
@@ -105,7 +113,7 @@ int eb_create_tables(int32_t T, const void *const *table_ptrs, const int64_t *st
  *   nnz        number of entries in indices, >= 0.
  *   offsets    device int64 [T*B+1], see above.
  *   B          bags per table (the mini-batch size), >= 0.
- *   mode       EB_SUM or EB_MEAN.
+ *   mode       EB_SUM or EB_MEAN, optionally | EB_HINT_STREAM_ROWS.
  *   shard_lo, shard_hi
  *              this GPU's row range [shard_lo, shard_hi), 0 <= lo <= hi.
  *              For every t, stored_rows[t] must cover the rows

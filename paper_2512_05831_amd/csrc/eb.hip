@@ -45,6 +45,9 @@
 
 namespace {
 
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
 constexpr int kWave = 64;
 constexpr int kWavesPerBlock = 4;
 constexpr int kBlock = kWave * kWavesPerBlock;
@@ -167,6 +170,26 @@ template <> struct Elem<EB_BF16> {
     __device__ static __forceinline__ float load1(const char *p) { return __uint_as_float((uint32_t)(*(const uint16_t *)p) << 16); }
 };
 
+// Row chunk load: default cache policy, or non-temporal (streamed past L2
+// and the last-level cache) when the caller hints that ids have no reuse.
+template <bool kStream>
+__device__ __forceinline__ uint4 load_chunk(const char *p)
+{
+    if constexpr (kStream) {
+        const u32x4 v = __builtin_nontemporal_load((const u32x4 *)p);
+        return make_uint4(v[0], v[1], v[2], v[3]);
+    } else {
+        return *(const uint4 *)p;
+    }
+}
+
+// Results, ids and offsets are touched once: non-temporal accesses.
+__device__ __forceinline__ void store_nt(float *p, float a, float b, float c, float d)
+{
+    const f32x4 v = {a, b, c, d};
+    __builtin_nontemporal_store(v, (f32x4 *)p);
+}
+
 __device__ __forceinline__ void clamp_bag(int64_t &s, int64_t &e, int64_t nnz)
 {
     s = s < 0 ? 0 : (s > nnz ? nnz : s);
@@ -176,7 +199,7 @@ __device__ __forceinline__ void clamp_bag(int64_t &s, int64_t &e, int64_t nnz)
 
 // ---------------------------------------------------------------------------- team gather kernel
 
-template <int DT, int R, int P, int C, int U>
+template <int DT, int R, int P, int C, int U, bool kStream>
 __global__ __launch_bounds__(kBlock) void eb_gather_team(const GatherArgs a)
 {
     constexpr int kTeam = R * P;
@@ -207,8 +230,8 @@ __global__ __launch_bounds__(kBlock) void eb_gather_team(const GatherArgs a)
     int64_t s = 0, e = 0;
     if (bag_ok) {
         const int64_t *o = a.offsets + (int64_t)t * a.B + b;
-        s = o[0];
-        e = o[1];
+        s = __builtin_nontemporal_load(o);
+        e = __builtin_nontemporal_load(o + 1);
         clamp_bag(s, e, a.nnz);
     }
 
@@ -240,7 +263,7 @@ __global__ __launch_bounds__(kBlock) void eb_gather_team(const GatherArgs a)
 #pragma unroll
         for (int q = 0; q < kQ; ++q) {
             const int k = q * kTeam + tl;
-            iv[q] = src[k < n ? k : n - 1];
+            iv[q] = __builtin_nontemporal_load(src + (k < n ? k : n - 1));
         }
 #pragma unroll
         for (int q = 0; q < kQ; ++q) {
@@ -266,7 +289,7 @@ __global__ __launch_bounds__(kBlock) void eb_gather_team(const GatherArgs a)
                 if (rr[u] != kInvalidRow) {
                     const char *p = base + (size_t)rr[u] * row_bytes;
 #pragma unroll
-                    for (int c = 0; c < C; ++c) v[u][c] = *(const uint4 *)(p + coff[c]);
+                    for (int c = 0; c < C; ++c) v[u][c] = load_chunk<kStream>(p + coff[c]);
                 }
             }
 #pragma unroll
@@ -282,7 +305,7 @@ __global__ __launch_bounds__(kBlock) void eb_gather_team(const GatherArgs a)
                 const char *p = base + (size_t)r * row_bytes;
                 uint4 v[C];
 #pragma unroll
-                for (int c = 0; c < C; ++c) v[c] = *(const uint4 *)(p + coff[c]);
+                for (int c = 0; c < C; ++c) v[c] = load_chunk<kStream>(p + coff[c]);
                 ++count;
 #pragma unroll
                 for (int c = 0; c < C; ++c) Elem<DT>::add(acc + c * kEpc, v[c]);
@@ -307,11 +330,11 @@ __global__ __launch_bounds__(kBlock) void eb_gather_team(const GatherArgs a)
 #pragma unroll
         for (int c = 0; c < C; ++c) {
             if (c * R + rl >= a.chunks) break;
-            float4 *dst = (float4 *)(o + (size_t)(c * R + rl) * kEpc);
+            float *dst = o + (size_t)(c * R + rl) * kEpc;
 #pragma unroll
             for (int h = 0; h < kEpc / 4; ++h)
-                dst[h] = make_float4(acc[c * kEpc + 4 * h], acc[c * kEpc + 4 * h + 1],
-                                     acc[c * kEpc + 4 * h + 2], acc[c * kEpc + 4 * h + 3]);
+                store_nt(dst + 4 * h, acc[c * kEpc + 4 * h], acc[c * kEpc + 4 * h + 1],
+                         acc[c * kEpc + 4 * h + 2], acc[c * kEpc + 4 * h + 3]);
         }
         if (a.hits && rl == 0) a.hits[b * a.ldh + t] = count;
     }
@@ -401,40 +424,40 @@ Shape team_shape(int rb)
     // Wide rows: one bag per wave.  Narrow rows: 16-lane teams (4 bags per
     // wave), so the group reduction stays inside a DPP row.
     s.P = s.R >= 16 ? kWave / s.R : 16 / s.R;
-    s.U = s.C >= 8 ? 1 : 8 / s.C;
+    s.U = s.C >= 6 ? 1 : 6 / s.C;
     return s;
 }
 
 using KernelFn = void (*)(GatherArgs);
 
 template <int DT, int R, int C>
-KernelFn team_kernel()
+KernelFn team_kernel(bool stream)
 {
     constexpr int P = R >= 16 ? kWave / R : 16 / R;
-    constexpr int U = C >= 8 ? 1 : 8 / C;
-    return eb_gather_team<DT, R, P, C, U>;
+    constexpr int U = C >= 6 ? 1 : 6 / C;
+    return stream ? eb_gather_team<DT, R, P, C, U, true> : eb_gather_team<DT, R, P, C, U, false>;
 }
 
 template <int DT>
-KernelFn pick_team_kernel(int R, int C)
+KernelFn pick_team_kernel(int R, int C, bool stream)
 {
     switch (R) {
-    case 1: return team_kernel<DT, 1, 1>();
-    case 2: return team_kernel<DT, 2, 1>();
-    case 4: return team_kernel<DT, 4, 1>();
-    case 8: return team_kernel<DT, 8, 1>();
-    case 16: return team_kernel<DT, 16, 1>();
-    case 32: return team_kernel<DT, 32, 1>();
+    case 1: return team_kernel<DT, 1, 1>(stream);
+    case 2: return team_kernel<DT, 2, 1>(stream);
+    case 4: return team_kernel<DT, 4, 1>(stream);
+    case 8: return team_kernel<DT, 8, 1>(stream);
+    case 16: return team_kernel<DT, 16, 1>(stream);
+    case 32: return team_kernel<DT, 32, 1>(stream);
     default:
         switch (C) {
-        case 1: return team_kernel<DT, 64, 1>();
-        case 2: return team_kernel<DT, 64, 2>();
-        case 3: return team_kernel<DT, 64, 3>();
-        case 4: return team_kernel<DT, 64, 4>();
-        case 5: return team_kernel<DT, 64, 5>();
-        case 6: return team_kernel<DT, 64, 6>();
-        case 7: return team_kernel<DT, 64, 7>();
-        case 8: return team_kernel<DT, 64, 8>();
+        case 1: return team_kernel<DT, 64, 1>(stream);
+        case 2: return team_kernel<DT, 64, 2>(stream);
+        case 3: return team_kernel<DT, 64, 3>(stream);
+        case 4: return team_kernel<DT, 64, 4>(stream);
+        case 5: return team_kernel<DT, 64, 5>(stream);
+        case 6: return team_kernel<DT, 64, 6>(stream);
+        case 7: return team_kernel<DT, 64, 7>(stream);
+        case 8: return team_kernel<DT, 64, 8>(stream);
         }
     }
     return nullptr;
@@ -510,7 +533,9 @@ int eb_forward(const eb_tables *h, int32_t T, const int64_t *rows, int32_t D, in
     if (T < 0 || T > h->T) return fail(EB_ERR_INVALID, "eb_forward: T out of range for the handle");
     if (D != h->D) return fail(EB_ERR_INVALID, "eb_forward: D differs from the handle's");
     if (dtype != h->dtype) return fail(EB_ERR_INVALID, "eb_forward: dtype differs from the handle's");
-    if (mode != EB_SUM && mode != EB_MEAN) return fail(EB_ERR_INVALID, "eb_forward: unknown mode");
+    const int32_t pool = mode & 0xFF;
+    if ((pool != EB_SUM && pool != EB_MEAN) || (mode & ~(0xFF | EB_HINT_STREAM_ROWS)) != 0)
+        return fail(EB_ERR_INVALID, "eb_forward: unknown mode or hint bits");
     if (nnz < 0 || B < 0) return fail(EB_ERR_INVALID, "eb_forward: negative nnz or B");
     if (shard_lo < 0 || shard_hi < shard_lo) return fail(EB_ERR_INVALID, "eb_forward: bad shard range");
     if (T > 0 && !rows) return fail(EB_ERR_INVALID, "eb_forward: NULL rows");
@@ -540,10 +565,12 @@ int eb_forward(const eb_tables *h, int32_t T, const int64_t *rows, int32_t D, in
     bool xcd_remap = false;
     if (team_path) {
         const Shape sh = team_shape((int)rb);
+        // Streaming loses for rows narrower than 64 bytes (several share a line).
+        const bool stream = (mode & EB_HINT_STREAM_ROWS) && rb >= 64;
         switch (dtype) {
-        case EB_F32: fn = pick_team_kernel<EB_F32>(sh.R, sh.C); break;
-        case EB_F16: fn = pick_team_kernel<EB_F16>(sh.R, sh.C); break;
-        default: fn = pick_team_kernel<EB_BF16>(sh.R, sh.C); break;
+        case EB_F32: fn = pick_team_kernel<EB_F32>(sh.R, sh.C, stream); break;
+        case EB_F16: fn = pick_team_kernel<EB_F16>(sh.R, sh.C, stream); break;
+        default: fn = pick_team_kernel<EB_BF16>(sh.R, sh.C, stream); break;
         }
         bags_per_block = (kWave / (sh.R * sh.P)) * kWavesPerBlock;
         xcd_remap = true;
@@ -565,7 +592,7 @@ int eb_forward(const eb_tables *h, int32_t T, const int64_t *rows, int32_t D, in
     a.D = D;
     a.row_bytes = team_path ? (int32_t)rb : 0;
     a.chunks = team_path ? (int32_t)(rb / 16) : 0;
-    a.mean = mode == EB_MEAN;
+    a.mean = pool == EB_MEAN;
     hipStream_t st = (hipStream_t)stream;
 
     const int64_t blocks_all_bags = (B + bags_per_block - 1) / bags_per_block;

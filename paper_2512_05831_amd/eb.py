@@ -17,6 +17,7 @@ from . import build as _build
 
 EB_F32, EB_F16, EB_BF16 = 0, 1, 2
 EB_SUM, EB_MEAN = 0, 1
+EB_HINT_STREAM_ROWS = 0x100
 EB_OK, EB_ERR_INVALID, EB_ERR_UNSUPPORTED, EB_ERR_HIP, EB_ERR_NOMEM = 0, -1, -2, -3, -4
 INT64_MAX = (1 << 63) - 1
 

@@ -74,6 +74,8 @@ def test_destroy_null_is_noop():
     (dict(D=8), eb.EB_ERR_INVALID),                       # differs from the handle
     (dict(dtype=eb.EB_F16), eb.EB_ERR_INVALID),
     (dict(mode=2), eb.EB_ERR_INVALID),
+    (dict(mode=0x200), eb.EB_ERR_INVALID),                # unknown hint bit
+    (dict(mode=2 | eb.EB_HINT_STREAM_ROWS), eb.EB_ERR_INVALID),
     (dict(nnz=-1), eb.EB_ERR_INVALID),
     (dict(B=-1), eb.EB_ERR_INVALID),
     (dict(shard_lo=-1), eb.EB_ERR_INVALID),
@@ -105,6 +107,7 @@ def test_forward_noops_touch_nothing():
         forward(h, B=0)
         forward(h, T=0, rows=[])
         forward(h, B=0, indices_ptr=None, nnz=0, offsets_ptr=None, out_ptr=None)
+        forward(h, B=0, mode=eb.EB_MEAN | eb.EB_HINT_STREAM_ROWS)
     finally:
         eb.eb_destroy(h)
 

@@ -77,6 +77,9 @@ def launch(w, dev_tables, d_idx, d_off, mode, want_hits):
 
 
 def check_sampled(w, dev_tables, host_tables, idx, off, sel, mode, device, repeat=False):
+    pool = mode
+    if w.dist == "uniform":
+        mode |= eb.EB_HINT_STREAM_ROWS
     d_idx = torch.from_numpy(idx).to(device)
     d_off = torch.from_numpy(off).to(device)
     out, hits = launch(w, dev_tables, d_idx, d_off, mode, True)
@@ -85,7 +88,7 @@ def check_sampled(w, dev_tables, host_tables, idx, off, sel, mode, device, repea
     t, b = sel // w.B, sel % w.B
     got_sel = np.stack([got[b[j], t[j] * w.D:(t[j] + 1) * w.D] for j in range(sel.size)])
     ref, ref_hits, mag = oracle.bags(host_tables, [w.rows] * w.T, w.D, w.dtype, idx, off, w.B,
-                                     sel, mode, w.shard_lo, w.shard_hi)
+                                     sel, pool, w.shard_lo, w.shard_hi)
     err = assert_parity(got_sel, ref, mag, max_bag_len(off, idx.size), w.dtype,
                         got_hits[b, t], ref_hits)
     # properties over the whole batch
@@ -103,13 +106,16 @@ def check_sampled(w, dev_tables, host_tables, idx, off, sel, mode, device, repea
 
 
 def check_full(w, mode, device):
+    """Every output; uniform ids run with the streaming hint, as benchmarked."""
+    if w.dist == "uniform":
+        mode |= eb.EB_HINT_STREAM_ROWS
     off = w.offsets()
     idx = w.indices(off)
     tables = w.tables()
     got, hits = run(tables, [w.rows] * w.T, w.D, w.dtype, idx, off, w.B, mode, w.shard_lo,
                     w.shard_hi, device=device)
-    ref, ref_hits, mag = oracle.forward(tables, [w.rows] * w.T, w.D, w.dtype, idx, off, w.B, mode,
-                                        w.shard_lo, w.shard_hi)
+    ref, ref_hits, mag = oracle.forward(tables, [w.rows] * w.T, w.D, w.dtype, idx, off, w.B,
+                                        mode & 0xFF, w.shard_lo, w.shard_hi)
     return assert_parity(got, ref, mag, max_bag_len(off, idx.size), w.dtype, hits, ref_hits)
 
 

@@ -91,6 +91,19 @@ def test_dyadic_mean_within_one_ulp(dtype):
     assert np.all(np.abs(got - ref32) <= ulp)
 
 
+@pytest.mark.parametrize("dtype", DT)
+@pytest.mark.parametrize("D", [8, 16, 32, 64, 100, 128, 256, 512, 1024, 2048])
+def test_stream_hint_changes_no_result(dtype, D):
+    tables, rows, idx, off = case(D=D, dtype=dtype, seed=300 + D, lo=100, hi=2900, dist="zipf")
+    for mode in (wl.SUM, wl.MEAN):
+        plain, h1 = run(tables, rows, D, dtype, idx, off, 37, mode, 100, 2900)
+        hinted, h2 = run(tables, rows, D, dtype, idx, off, 37, mode | eb.EB_HINT_STREAM_ROWS, 100, 2900)
+        assert np.array_equal(plain.view(np.uint32), hinted.view(np.uint32))
+        assert np.array_equal(h1, h2)
+        ref, ref_hits, mag = oracle.forward(tables, rows, D, dtype, idx, off, 37, mode, 100, 2900)
+        assert_parity(hinted, ref, mag, max_bag_len(off, idx.size), dtype, h2, ref_hits)
+
+
 # ----------------------------------------------------------------------------- bag lengths
 
 
