@@ -56,12 +56,13 @@ enum { EB_F32 = 0, EB_F16 = 1, EB_BF16 = 2 };
  * mean over all GPUs. */
 enum { EB_SUM = 0, EB_MEAN = 1 };
 
-/* Cache hint, OR-ed into eb_forward's `mode`.  EB_HINT_STREAM_ROWS reads the
- * embedding rows with non-temporal loads, which do not keep them in L2 or the
- * last-level cache.  That is faster when ids have little reuse (for example
- * drawn uniformly from tables much larger than the 256 MB last-level cache)
- * and slower when they are skewed (hot rows then miss the caches).  It
- * changes no result.  Rows narrower than 64 bytes ignore it. */
+/* Reuse hint, OR-ed into eb_forward's `mode`.  EB_HINT_STREAM_ROWS tells the
+ * library that the ids have little reuse (for example drawn uniformly from
+ * tables much larger than the 256 MB last-level cache).  It then reads rows of
+ * 128 bytes or more with non-temporal loads, which bypass L2 and the
+ * last-level cache, and gives each XCD a contiguous run of bags.  Faster for
+ * such ids, slower for skewed ones (hot rows then miss the caches); it
+ * changes no result. */
 enum { EB_HINT_STREAM_ROWS = 0x100 };
 
 /* Return codes. */

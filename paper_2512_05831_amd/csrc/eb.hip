@@ -21,12 +21,15 @@
 //   * A team stages a window of its bag's indices in LDS: the window is read
 //     with coalesced int64 loads, filtered against the shard, and rewritten as
 //     32-bit local row numbers (or an invalid marker).  The gather loop then
-//     reads them from LDS and keeps U rows per group in flight (unrolled).
+//     reads them from LDS and keeps U rows per group in flight (unrolled;
+//     U = 2 for streamed rows of 128 B or more, else 6).
 //   * Accumulation is fp32; fp16 / bf16 rows are widened exactly.
-//   * Workgroups are 4 waves.  The hardware deals workgroups to the 8 XCDs
-//     round-robin; the block id is remapped so each XCD gets a contiguous run
-//     of bags (whole tables when T >= 8), which keeps a table's hot rows in
-//     one XCD's L2 under skewed ids.
+//   * Workgroups are 4 waves, bags in table-major order.  The hardware deals
+//     workgroups to the 8 XCDs round-robin, so by default all XCDs work on
+//     the same table at a time and its hot rows share L2s and the last-level
+//     cache (best for skewed ids).  Under the no-reuse hint block ids are
+//     remapped so each XCD gets a contiguous run of bags (measured faster for
+//     uniform ids).
 // Rows whose size is not a multiple of 16 bytes, unaligned tables or outputs,
 // and rows wider than 8 KB take a plain one-wave-per-bag kernel.
 
@@ -78,6 +81,7 @@ struct GatherArgs {
     int32_t blocks_per_table;
     int32_t nblocks;        // logical blocks; the grid is padded to a multiple of 8
     int32_t mean;
+    int32_t xcd_runs;       // give each XCD a contiguous run of logical blocks
 };
 
 // ---------------------------------------------------------------------------- device helpers
@@ -211,7 +215,7 @@ __global__ __launch_bounds__(kBlock) void eb_gather_team(const GatherArgs a)
 
     __shared__ uint32_t stage[kWavesPerBlock * kStagePerWave];
 
-    const int lb = xcd_contiguous_block(blockIdx.x, gridDim.x);
+    const int lb = a.xcd_runs ? xcd_contiguous_block(blockIdx.x, gridDim.x) : (int)blockIdx.x;
     if (lb >= a.nblocks) return;
 
     const int lane = threadIdx.x & (kWave - 1);
@@ -411,7 +415,7 @@ int fail(int code, const std::string &msg)
 
 // Team shape for a row of rb bytes (rb % 16 == 0, rb <= 8192).
 struct Shape {
-    int R, P, C, U;
+    int R, P, C;
 };
 
 Shape team_shape(int rb)
@@ -424,18 +428,23 @@ Shape team_shape(int rb)
     // Wide rows: one bag per wave.  Narrow rows: 16-lane teams (4 bags per
     // wave), so the group reduction stays inside a DPP row.
     s.P = s.R >= 16 ? kWave / s.R : 16 / s.R;
-    s.U = s.C >= 6 ? 1 : 6 / s.C;
     return s;
 }
 
 using KernelFn = void (*)(GatherArgs);
 
+// Rows in flight per lane: streamed (non-temporal) rows of 128 B and more all
+// go to HBM, where two per lane saturate the random-read rate and more only
+// queue; narrower rows need more requests per byte in flight, and cached rows
+// profit from deeper overlap while hits return early.
 template <int DT, int R, int C>
 KernelFn team_kernel(bool stream)
 {
     constexpr int P = R >= 16 ? kWave / R : 16 / R;
-    constexpr int U = C >= 6 ? 1 : 6 / C;
-    return stream ? eb_gather_team<DT, R, P, C, U, true> : eb_gather_team<DT, R, P, C, U, false>;
+    constexpr int U_CACHED = C >= 6 ? 1 : 6 / C;
+    constexpr int U_STREAM = R * C >= 8 ? (C >= 2 ? 1 : 2) : U_CACHED;
+    return stream ? eb_gather_team<DT, R, P, C, U_STREAM, true>
+                  : eb_gather_team<DT, R, P, C, U_CACHED, false>;
 }
 
 template <int DT>
@@ -565,15 +574,18 @@ int eb_forward(const eb_tables *h, int32_t T, const int64_t *rows, int32_t D, in
     bool xcd_remap = false;
     if (team_path) {
         const Shape sh = team_shape((int)rb);
-        // Streaming loses for rows narrower than 64 bytes (several share a line).
-        const bool stream = (mode & EB_HINT_STREAM_ROWS) && rb >= 64;
+        // Non-temporal loads lose for rows narrower than 128 bytes.
+        const bool stream = (mode & EB_HINT_STREAM_ROWS) && rb >= 128;
         switch (dtype) {
         case EB_F32: fn = pick_team_kernel<EB_F32>(sh.R, sh.C, stream); break;
         case EB_F16: fn = pick_team_kernel<EB_F16>(sh.R, sh.C, stream); break;
         default: fn = pick_team_kernel<EB_BF16>(sh.R, sh.C, stream); break;
         }
         bags_per_block = (kWave / (sh.R * sh.P)) * kWavesPerBlock;
-        xcd_remap = true;
+        // No reuse: each XCD takes a contiguous run of bags.  Otherwise
+        // hardware order, so all XCDs work on the same table at once and its
+        // hot rows share the last-level cache.
+        xcd_remap = (mode & EB_HINT_STREAM_ROWS) != 0;
     } else {
         fn = pick_plain_kernel(dtype);
     }
@@ -593,6 +605,7 @@ int eb_forward(const eb_tables *h, int32_t T, const int64_t *rows, int32_t D, in
     a.row_bytes = team_path ? (int32_t)rb : 0;
     a.chunks = team_path ? (int32_t)(rb / 16) : 0;
     a.mean = pool == EB_MEAN;
+    a.xcd_runs = xcd_remap ? 1 : 0;
     hipStream_t st = (hipStream_t)stream;
 
     const int64_t blocks_all_bags = (B + bags_per_block - 1) / bags_per_block;

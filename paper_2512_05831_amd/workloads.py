@@ -23,8 +23,8 @@ Recipe (deterministic; any part can be regenerated alone):
     with purpose 0 = table values, 1 = lengths, 2 = indices, 3 = permutation;
   * table value (t, r, c) is a counter-based draw: SplitMix64's output
     function of r*D + c, keyed by SeedSequence([seed, 0, t]), gives two 24-bit
-    uniforms and Box-Muller one standard normal; times 0.01 (std 0.01) in fp32,
-    then rounded to nearest-even into fp16 / bf16 storage;
+    uniforms and Box-Muller (in fp32) one standard normal; times 0.01 (std
+    0.01), then rounded to nearest-even into fp16 / bf16 storage;
   * "dyadic" tables hold k * 2^-12 (k integer, |k| <= 2048; bf16: k * 2^-8,
     |k| <= 127), so every partial sum of a few hundred of them is exact in fp32;
   * bounded Zipf ranks use Hoermann and Derflinger's rejection-inversion
@@ -107,18 +107,19 @@ def _rows_values(key: np.uint64, rows: np.ndarray, D: int, dtype: int, values: s
             z *= mult
         z ^= z >> np.uint64(31)
     if values == "normal":
-        u1 = (z >> np.uint64(40)).astype(np.float64)
-        u1 += 0.5
-        u1 *= 2.0 ** -24
+        # Box-Muller in fp32: sqrt(-2 ln u1) cos(2 pi u2), u1 in (0, 1), u2 in [0, 1)
+        u1 = (z >> np.uint64(40)).astype(np.float32)
+        u1 += np.float32(0.5)
+        u1 *= np.float32(2.0 ** -24)
         np.log(u1, out=u1)
-        u1 *= -2.0
+        u1 *= np.float32(-2.0)
         np.sqrt(u1, out=u1)
-        u2 = (z & np.uint64(0xFFFFFF)).astype(np.float64)
-        u2 *= 2.0 * np.pi * 2.0 ** -24
+        u2 = (z & np.uint64(0xFFFFFF)).astype(np.float32)
+        u2 *= np.float32(2.0 * np.pi * 2.0 ** -24)
         np.cos(u2, out=u2)
         u1 *= u2
-        x = u1.astype(np.float32)
-        x *= np.float32(0.01)
+        u1 *= np.float32(0.01)
+        x = u1
     elif values == "dyadic":
         if dtype == BF16:
             k = (z % np.uint64(255)).astype(np.int64) - 127
