@@ -128,6 +128,70 @@ def copy_calibration(torch, dev, nbytes: int, steps: int):
                       "GBps_read_plus_write": 2 * nbytes / us / 1e3}), flush=True)
 
 
+def paper_sweep(torch, dev, eb):
+    """The gather shapes the paper varies (Sec. 4.3 / 4.4: 2..64 tables, batch
+    128 / 1024 / 4096, pooling 4 / 8 / 16, 128-byte rows; Sec. 5.1: one table
+    with batch 128..1024, D 32..256, pooling 4 / 8 / 16, and 1..64 tables with
+    batch 128 / 1024 / 4096, pooling 32, D 32 / 128), on one GPU with fp32
+    tables and uniform ids.  The paper leaves the row count open: 1,000,000
+    rows for the single-table sweep, 100,000 per table for the multi-table
+    ones.  One JSON line per shape: mean launch time over 200 launches."""
+    shapes = []
+    for T in (2, 4, 8, 16, 32, 64):
+        for B in (128, 1024, 4096):
+            for L in (4, 8, 16):
+                shapes.append(("sec4.3", T, 100_000, 32, B, L))
+    for B in (128, 256, 512, 1024):
+        for D in (32, 64, 128, 256):
+            for L in (4, 8, 16):
+                shapes.append(("sec5.1-single", 1, 1_000_000, D, B, L))
+    for T in (1, 2, 4, 8, 16, 32, 64):
+        for B in (128, 1024, 4096):
+            for D in (32, 128):
+                shapes.append(("sec5.1-multi", T, 100_000, D, B, 32))
+    cache = {}
+
+    def tables_for(T, rows, D):
+        key = (rows, D)
+        have = cache.setdefault(key, [])
+        while len(have) < T:
+            h = wl.table(2000 + D, len(have), D, wl.F32, 0, rows)
+            have.append(torch.from_numpy(h).to(dev))
+        return have[:T]
+
+    stream = torch.cuda.Stream(dev)
+    for tag, T, rows, D, B, L in shapes:
+        w = wl.Workload(f"{tag}-t{T}-r{rows}-d{D}-b{B}-l{L}", T=T, rows=rows, D=D, dtype=wl.F32,
+                        B=B, L=L, seed=3000)
+        off = w.offsets()
+        batches = [w.with_(seed=w.seed + j).indices(off) for j in range(4)]
+        et = eb.EmbeddingBagTables(tables_for(T, rows, D), rows=[rows] * T)
+        d_off = torch.from_numpy(off).to(dev)
+        d_idx = [torch.from_numpy(b).to(dev) for b in batches]
+        out = torch.empty((B, T * D), dtype=torch.float32, device=dev)
+        calls = [et.prepare(i, d_off, B, eb.EB_SUM | eb.EB_HINT_STREAM_ROWS, out, None, stream)
+                 for i in d_idx]
+        K = 200
+        with torch.cuda.stream(stream):
+            for i in range(20):
+                calls[i % 4]()
+            torch.cuda.synchronize()
+            ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            ev0.record(stream)
+            for i in range(K):
+                calls[i % 4]()
+            ev1.record(stream)
+            torch.cuda.synchronize()
+        us = ev0.elapsed_time(ev1) * 1e3 / K
+        nnz = T * B * L
+        by = algorithmic_bytes(w, nnz, nnz, False)
+        print(json.dumps({"sweep": tag, "tables": T, "rows": rows, "D": D, "B": B, "L": L,
+                          "us_per_launch": round(us, 2), "lookups_per_s": nnz / us * 1e6,
+                          "algorithmic_GBps": round(by / us / 1e3, 1),
+                          "frac_of_8TBps": round(by / us / 1e3 / HBM_PEAK_GBPS, 4)}), flush=True)
+        et.close()
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -140,6 +204,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--rows-policy", default="auto", choices=["auto", "cached", "stream"])
+    ap.add_argument("--sweep", choices=["paper"], default=None,
+                    help="time the paper's single-GPU gather shapes instead (one JSON line each)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run a plain streaming copy of BYTES (for scaling HBM counters)")
     args = ap.parse_args()
@@ -156,6 +222,9 @@ def main():
     dev = torch.device("cuda:0")
     if args.copy_calibration:
         copy_calibration(torch, dev, args.copy_calibration, args.steps)
+        return
+    if args.sweep == "paper":
+        paper_sweep(torch, dev, eb)
         return
     w = pick_workload(args)
     mode = w.modes[0]

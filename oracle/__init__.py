@@ -8,8 +8,10 @@ package.
 ``forward`` / ``bags`` compute, in double precision on one host thread, the
 Embedding Bag pooling of arXiv 2512.05831 (sum of rows per inference, Sec. 4.1,
 over the indices + lengths input of Sec. 4.2, one row-wise shard per Sec. 4.1 /
-4.3).  The C source states the definition and the readings taken where the
-paper is silent (mean pooling, out-of-range indices, malformed offsets).
+4.3).  ``bucketize`` and ``sum_partials`` are one GPU's parts of the row-wise
+exchange around it (Sec. 4.2, Sec. 4.3).  The C source states the definitions
+and the readings taken where the paper is silent (mean pooling, out-of-range
+indices, malformed offsets).
 """
 from __future__ import annotations
 
@@ -51,6 +53,10 @@ def load_library(path: str) -> ctypes.CDLL:
     lib.oracle_eb_bags.restype = ctypes.c_int
     lib.oracle_decode.argtypes = [i32, p, i64, p]
     lib.oracle_decode.restype = ctypes.c_int
+    lib.oracle_bucketize.argtypes = [i32, i64, i32, p, p, i64, p, p, p, p]
+    lib.oracle_bucketize.restype = ctypes.c_int
+    lib.oracle_sum_partials.argtypes = [i32, p, i64, i32, i32, p, i64, p]
+    lib.oracle_sum_partials.restype = ctypes.c_int
     return lib
 
 
@@ -153,4 +159,43 @@ def decode(dtype, bits) -> np.ndarray:
     out = np.empty(bits.size, dtype=np.float64)
     if _load().oracle_decode(dtype, bits.ctypes.data, bits.size, out.ctypes.data) != 0:
         raise ValueError("bad dtype")
+    return out
+
+
+def bucketize(bounds, indices, offsets, T: int, B: int):
+    """Destination lists of the row-wise exchange.  ``bounds``: int64 [T, G+1].
+
+    Returns (out_offsets int64 [G, T*B+1], out_indices int64 [total],
+    segments int64 [G+1])."""
+    bounds = np.ascontiguousarray(bounds, dtype=np.int64)
+    if bounds.ndim != 2 or bounds.shape[0] != T:
+        raise ValueError("bounds must be [T, G+1]")
+    G = bounds.shape[1] - 1
+    indices = np.ascontiguousarray(indices, dtype=np.int64)
+    offsets = np.ascontiguousarray(offsets, dtype=np.int64)
+    if offsets.size != T * B + 1:
+        raise ValueError("offsets must have T*B+1 entries")
+    out_off = np.zeros((G, T * B + 1), dtype=np.int64)
+    out_idx = np.zeros(max(1, indices.size), dtype=np.int64)
+    seg = np.zeros(G + 1, dtype=np.int64)
+    rc = _load().oracle_bucketize(T, B, G, bounds.ctypes.data, indices.ctypes.data, indices.size,
+                                  offsets.ctypes.data, out_off.ctypes.data, out_idx.ctypes.data,
+                                  seg.ctypes.data)
+    if rc != 0:
+        raise ValueError("oracle_bucketize rejected its arguments")
+    return out_off, out_idx[:seg[-1]].copy(), seg
+
+
+def sum_partials(partials, B: int, T: int, D: int, mean_offsets=None, nnz: int = 0):
+    """``partials``: float32 [G, B, T*D].  Returns float64 [B, T*D]."""
+    partials = np.ascontiguousarray(partials, dtype=np.float32)
+    G = partials.shape[0]
+    if partials.size != G * B * T * D:
+        raise ValueError("partials must be [G, B, T*D]")
+    out = np.zeros((B, T * D), dtype=np.float64)
+    mo = None if mean_offsets is None else np.ascontiguousarray(mean_offsets, dtype=np.int64)
+    rc = _load().oracle_sum_partials(G, partials.ctypes.data, B, T, D,
+                                     None if mo is None else mo.ctypes.data, nnz, out.ctypes.data)
+    if rc != 0:
+        raise ValueError("oracle_sum_partials rejected its arguments")
     return out

@@ -185,3 +185,81 @@ int oracle_decode(int32_t dtype, const void *bits, int64_t n, double *out)
     for (int64_t k = 0; k < n; ++k) out[k] = stored_value(bits, dtype, 1, k, 0);
     return 0;
 }
+
+/*
+ * Row-wise exchange, the parts one GPU computes (Sec. 4.2 and the first and
+ * third kernels of Sec. 4.3): before the gather, each id of a mini-batch is
+ * sent to the GPU whose block of its table's rows holds it (the permute that
+ * feeds an all-to-all); after it, the partial sums every GPU produced for
+ * this GPU's bags are added up (the reduce-scatter, which for NVSHMEM the
+ * paper builds from an all-to-all followed by a local sum).
+ */
+
+/* Destination lists.  Shard g of table t holds rows
+ * [bounds[t*(G+1)+g], bounds[t*(G+1)+g+1]) (bounds non-decreasing per table).
+ * For each destination g in turn, the ids of every bag (t, b) that fall in
+ * g's block are appended in (table, bag, position) order; ids outside
+ * [bounds[t][0], bounds[t][G]) go nowhere.  Bags follow the clamped-offset
+ * rule of pool_bag.
+ *   out_offsets [G][T*B+1]: CSR offsets of destination g's ids, from 0.
+ *   out_indices [total]:    the ids, destination g's at [segments[g], segments[g+1]).
+ *   segments    [G+1]. */
+int oracle_bucketize(int32_t T, int64_t B, int32_t G, const int64_t *bounds,
+                     const int64_t *indices, int64_t nnz, const int64_t *offsets,
+                     int64_t *out_offsets, int64_t *out_indices, int64_t *segments)
+{
+    if (T < 0 || B < 0 || G < 1 || nnz < 0) return -1;
+    int64_t TB = (int64_t)T * B;
+    int64_t pos = 0;
+    for (int32_t g = 0; g < G; ++g) {
+        segments[g] = pos;
+        for (int32_t t = 0; t < T; ++t) {
+            int64_t lo = bounds[(int64_t)t * (G + 1) + g];
+            int64_t hi = bounds[(int64_t)t * (G + 1) + g + 1];
+            for (int64_t b = 0; b < B; ++b) {
+                int64_t p = (int64_t)t * B + b;
+                out_offsets[(int64_t)g * (TB + 1) + p] = pos - segments[g];
+                int64_t s = offsets[p], e = offsets[p + 1];
+                if (s < 0) s = 0;
+                if (s > nnz) s = nnz;
+                if (e > nnz) e = nnz;
+                if (e < s) e = s;
+                for (int64_t k = s; k < e; ++k) {
+                    int64_t i = indices[k];
+                    if (i >= lo && i < hi) out_indices[pos++] = i;
+                }
+            }
+        }
+        out_offsets[(int64_t)g * (TB + 1) + TB] = pos - segments[g];
+    }
+    segments[G] = pos;
+    return 0;
+}
+
+/* Local sum of the partial results: out[b][t*D + c] = sum over s < G of
+ * partials[s][b][t*D + c], in double.  When mean_offsets is not NULL, bag
+ * (t, b) is then divided by its length under those offsets (clamped to nnz;
+ * an empty bag gives 0): the mean when every shard pooled sums. */
+int oracle_sum_partials(int32_t G, const float *partials, int64_t B, int32_t T, int32_t D,
+                        const int64_t *mean_offsets, int64_t nnz, double *out)
+{
+    if (G < 1 || B < 0 || T < 0 || D < 1 || nnz < 0) return -1;
+    int64_t width = (int64_t)T * D;
+    int64_t n = B * width;
+    for (int64_t j = 0; j < n; ++j) {
+        double acc = 0.0;
+        for (int32_t s = 0; s < G; ++s) acc += (double)partials[(int64_t)s * n + j];
+        if (mean_offsets) {
+            int64_t b = j / width, t = (j % width) / D;
+            int64_t p = t * B + b;
+            int64_t st = mean_offsets[p], e = mean_offsets[p + 1];
+            if (st < 0) st = 0;
+            if (st > nnz) st = nnz;
+            if (e > nnz) e = nnz;
+            if (e < st) e = st;
+            acc = (e > st) ? acc / (double)(e - st) : 0.0;
+        }
+        out[j] = acc;
+    }
+    return 0;
+}

@@ -14,12 +14,14 @@ import numpy as np
 import pytest
 
 import oracle
+import test_oracle_exchange as xpins
 import test_oracle_pins as pins
 
 SRC = os.path.join(os.path.dirname(oracle.__file__), "eb_oracle.c")
 
 MUTANTS = {
-    "drop_last_index": ("for (int64_t k = s; k < e; ++k)", "for (int64_t k = s; k + 1 < e; ++k)"),
+    "drop_last_index": ("for (int64_t k = s; k < e; ++k) {\n        int64_t i = indices[k];\n        int in_table",
+                        "for (int64_t k = s; k + 1 < e; ++k) {\n        int64_t i = indices[k];\n        int in_table"),
     "shard_hi_inclusive": ("(i < shard_hi)", "(i <= shard_hi)"),
     "table_bound_inclusive": ("(i < rows[t])", "(i <= rows[t])"),
     "mean_over_hits": ("acc[c] / (double)L", "acc[c] / (double)(hits ? hits : 1)"),
@@ -30,8 +32,19 @@ MUTANTS = {
     "flipped_sign": ("acc[c] += w;", "acc[c] -= w;"),
     "lost_shard_offset": ("int64_t r = i - shard_lo;", "int64_t r = i;"),
     "magnitude_without_abs": ("mag[c] += fabs(w);", "mag[c] += w;"),
-    "bag_end_from_start": ("e = offsets[p + 1];", "e = offsets[p] + (offsets[p + 1] > offsets[p]);"),
+    "bag_end_from_start": ("e = offsets[p + 1];\n    /* Offsets are clamped",
+                           "e = offsets[p] + (offsets[p + 1] > offsets[p]);\n    /* Offsets are clamped"),
+    "bucketize_drop_last_index": ("for (int64_t k = s; k < e; ++k) {\n                    int64_t i = indices[k];\n                    if (i >= lo",
+                                  "for (int64_t k = s; k + 1 < e; ++k) {\n                    int64_t i = indices[k];\n                    if (i >= lo"),
     "hits_once_per_bag": ("++hits;", "hits = 1;"),
+    "bucketize_hi_inclusive": ("if (i >= lo && i < hi) out_indices[pos++] = i;",
+                               "if (i >= lo && i <= hi) out_indices[pos++] = i;"),
+    "bucketize_absolute_offsets": ("out_offsets[(int64_t)g * (TB + 1) + p] = pos - segments[g];",
+                                   "out_offsets[(int64_t)g * (TB + 1) + p] = pos;"),
+    "partials_drop_last_source": ("for (int32_t s = 0; s < G; ++s) acc +=",
+                                  "for (int32_t s = 0; s + 1 < G; ++s) acc +="),
+    "partials_mean_over_sources": ("acc = (e > st) ? acc / (double)(e - st) : 0.0;",
+                                   "acc = (e > st) ? acc / (double)G : 0.0;"),
 }
 
 
@@ -54,6 +67,14 @@ def pin_checks():
     checks.append(("empty", pins.test_empty_bags_pool_to_zero))
     checks.append(("malformed", pins.test_malformed_offsets))
     checks.append(("scipy", lambda: pins.test_scipy_csr_spmm(0)))
+    checks.append(("x_example30", xpins.test_worked_example_two_gpus_thirty_rows))
+    checks.append(("x_example20", xpins.test_worked_example_two_gpus_twenty_rows))
+    for seed in range(3):
+        checks.append((f"x_sort_{seed}", lambda s=seed: xpins.test_bucketize_matches_stable_sort(3, s)))
+    for mode in (oracle.SUM, oracle.MEAN):
+        checks.append((f"x_pipeline_{mode}", lambda m=mode: xpins.test_row_wise_pipeline_equals_unsharded(3, m)))
+    checks.append(("x_partials", xpins.test_sum_partials_against_numpy))
+    checks.append(("x_partials_mean", xpins.test_sum_partials_mean_divides_by_bag_length))
     return checks
 
 
@@ -62,7 +83,7 @@ def run_checks():
     for name, fn in pin_checks():
         try:
             fn()
-        except (AssertionError, ValueError):
+        except (AssertionError, ValueError, IndexError):
             failed.append(name)
     return failed
 
@@ -78,16 +99,40 @@ def build_variant(tmp_path, name, old, new):
     return str(lib)
 
 
+CHILD = """
+import sys
+sys.path[:0] = {paths!r}
+import numpy as np
+import oracle
+import test_oracle_mutants as m
+with np.errstate(all="ignore"), oracle.using({lib!r}):
+    failed = m.run_checks()
+print("FAILED", len(failed), " ".join(failed))
+"""
+
+
+def run_in_child(lib):
+    """Pin checks against one build, in a child process: a mutant that writes
+    out of bounds may crash, and a crash counts as caught."""
+    import sys
+
+    here = os.path.dirname(os.path.abspath(__file__))
+    paths = [here, os.path.dirname(here)]
+    res = subprocess.run([sys.executable, "-c", CHILD.format(paths=paths, lib=lib)],
+                         capture_output=True, text=True, timeout=300)
+    line = [l for l in res.stdout.splitlines() if l.startswith("FAILED")]
+    return res.returncode, (int(line[0].split()[1]) if line else None)
+
+
 def test_unmodified_source_passes(tmp_path):
     lib = build_variant(tmp_path, "identity", "enum { ORACLE_SUM", "enum { ORACLE_SUM")
-    with oracle.using(lib):
-        assert run_checks() == []
+    rc, nfail = run_in_child(lib)
+    assert rc == 0 and nfail == 0
 
 
 @pytest.mark.parametrize("name", sorted(MUTANTS))
 def test_mutant_is_caught(tmp_path, name):
     old, new = MUTANTS[name]
     lib = build_variant(tmp_path, name, old, new)
-    with np.errstate(all="ignore"), oracle.using(lib):
-        failed = run_checks()
-    assert failed, f"no pin caught the planted mistake {name!r}"
+    rc, nfail = run_in_child(lib)
+    assert rc != 0 or nfail, f"no pin caught the planted mistake {name!r}"
