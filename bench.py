@@ -128,6 +128,76 @@ def copy_calibration(torch, dev, nbytes: int, steps: int):
                       "GBps_read_plus_write": 2 * nbytes / us / 1e3}), flush=True)
 
 
+def _time_launches(torch, stream, fn, K, W):
+    with torch.cuda.stream(stream):
+        for _ in range(W):
+            fn()
+        torch.cuda.synchronize()
+        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        ev0.record(stream)
+        for _ in range(K):
+            fn()
+        ev1.record(stream)
+        torch.cuda.synchronize()
+    return ev0.elapsed_time(ev1) * 1e3 / K
+
+
+def exchange_bench(torch, dev, eb, K, W):
+    """The row-wise exchange's local kernels at the sizes of the skewed
+    workloads split over 8 GPUs by rows.  bucketize: the 26-table,
+    16384-bag Zipf(1.05) batch (21.1 M ids) into 8 row blocks per table.
+    sum_partials: the 400M-id shard workload's bags, 65536 / 8 = 8192 per GPU,
+    D = 256, 8 partial blocks.  One JSON line each: mean launch time (HIP
+    events around K launches) and algorithmic bytes against 8 TB/s."""
+    K = min(K, 100)
+    stream = torch.cuda.Stream(dev)
+    w = wl.config(3)
+    off = w.offsets()
+    idx = w.indices(off)
+    G = 8
+    bounds = np.array([[g * w.rows // G for g in range(G + 1)]] * w.T, dtype=np.int64)
+    d_b = torch.from_numpy(bounds).to(dev)
+    d_i = torch.from_numpy(idx).to(dev)
+    d_o = torch.from_numpy(off).to(dev)
+    TB = w.T * w.B
+    out_off = torch.empty((G, TB + 1), dtype=torch.int64, device=dev)
+    out_idx = torch.empty(idx.size, dtype=torch.int64, device=dev)
+    seg = torch.empty(G + 1, dtype=torch.int64, device=dev)
+    nws = eb.eb_bucketize_workspace(w.T, w.B, G)
+    ws = torch.empty(nws, dtype=torch.uint8, device=dev)
+
+    def bucket():
+        eb.eb_bucketize(w.T, w.B, G, d_b.data_ptr(), d_i.data_ptr(), idx.size, d_o.data_ptr(),
+                        out_off.data_ptr(), out_idx.data_ptr(), seg.data_ptr(), ws.data_ptr(), nws,
+                        stream.cuda_stream)
+    us = _time_launches(torch, stream, bucket, K, W)
+    kept = int(seg[-1].item())
+    by = idx.size * 8 + (TB + 1) * 8 + bounds.size * 8 + kept * 8 + G * (TB + 1) * 8 + (G + 1) * 8
+    print(json.dumps({"kernel": "eb_bucketize", "workload": w.name + f"-to-{G}-row-blocks",
+                      "ids": int(idx.size), "bags": TB, "destinations": G,
+                      "us_per_call": round(us, 1), "ids_per_s": idx.size / us * 1e6,
+                      "algorithmic_bytes": by, "algorithmic_GBps": round(by / us / 1e3, 1),
+                      "frac_of_8TBps": round(by / us / 1e3 / HBM_PEAK_GBPS, 4),
+                      "kernels_per_call": 5}), flush=True)
+    del d_i, out_idx
+    B, T, D = 65536 // G, 1, 256
+    # six receive buffers cycled (400 MB), so the last-level cache cannot hold the input
+    parts = [torch.randn((G, B, T * D), dtype=torch.float32, device=dev) for _ in range(6)]
+    out = torch.empty((B, T * D), dtype=torch.float32, device=dev)
+    turn = [0]
+
+    def reduce():
+        p = parts[turn[0] % len(parts)]
+        turn[0] += 1
+        eb.eb_sum_partials(G, p.data_ptr(), B, T, D, None, 0, out.data_ptr(), stream.cuda_stream)
+    us = _time_launches(torch, stream, reduce, K * 4, W)
+    by = G * B * T * D * 4 + B * T * D * 4
+    print(json.dumps({"kernel": "eb_sum_partials", "workload": f"{G}x{B}x{T * D}-f32",
+                      "us_per_call": round(us, 1), "algorithmic_bytes": by,
+                      "algorithmic_GBps": round(by / us / 1e3, 1),
+                      "frac_of_8TBps": round(by / us / 1e3 / HBM_PEAK_GBPS, 4)}), flush=True)
+
+
 def paper_sweep(torch, dev, eb):
     """The gather shapes the paper varies (Sec. 4.3 / 4.4: 2..64 tables, batch
     128 / 1024 / 4096, pooling 4 / 8 / 16, 128-byte rows; Sec. 5.1: one table
@@ -204,6 +274,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--rows-policy", default="auto", choices=["auto", "cached", "stream"])
+    ap.add_argument("--exchange", action="store_true",
+                    help="time the row-wise exchange kernels instead (bucketize, sum_partials)")
     ap.add_argument("--sweep", choices=["paper"], default=None,
                     help="time the paper's single-GPU gather shapes instead (one JSON line each)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
@@ -225,6 +297,9 @@ def main():
         return
     if args.sweep == "paper":
         paper_sweep(torch, dev, eb)
+        return
+    if args.exchange:
+        exchange_bench(torch, dev, eb, args.steps, args.warmup)
         return
     w = pick_workload(args)
     mode = w.modes[0]

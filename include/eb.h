@@ -42,6 +42,7 @@
 #ifndef EB_H
 #define EB_H
 
+#include <stddef.h>
 #include <stdint.h>
 
 #ifdef __cplusplus
@@ -146,6 +147,82 @@ int eb_forward(const eb_tables *tables, int32_t T, const int64_t *rows, int32_t 
                const int64_t *indices, int64_t nnz, const int64_t *offsets, int64_t B,
                int32_t mode, int64_t shard_lo, int64_t shard_hi, float *out, int32_t *hits,
                void *stream);
+
+/*
+ * The row-wise exchange around the gather, one GPU's part (Sec. 4.2; the
+ * first and third kernels of Sec. 4.3).  Under row-wise parallelism each GPU
+ * sends every id of its mini-batch to the GPU whose block of rows holds it
+ * (a permute feeding an all-to-all), every GPU pools what it received, and
+ * the partial sums return to the GPU that owns the bags, which adds them (a
+ * reduce-scatter; in the paper an all-to-all followed by a local sum).  The
+ * collectives themselves are the caller's (for example RCCL); these calls
+ * compute their send buffers and the final local sum.
+ */
+
+/*
+ * eb_bucketize_workspace -- device workspace, in bytes, that eb_bucketize
+ * needs for T tables, B bags per table and G destinations (at least 1, at
+ * most 1024).  Returns EB_ERR_INVALID for NULL bytes or bad sizes,
+ * EB_ERR_UNSUPPORTED for G > 1024.  Touches no device state.
+ */
+int eb_bucketize_workspace(int32_t T, int64_t B, int32_t G, size_t *bytes);
+
+/*
+ * eb_bucketize -- sort a mini-batch's ids by destination GPU.
+ *
+ *   T, B         tables and bags per table of the mini-batch.
+ *   G            destinations (GPUs), 1 <= G <= 1024.
+ *   bounds       device int64 [T][G+1]: GPU g holds rows
+ *                [bounds[t][g], bounds[t][g+1]) of table t.  Each row of
+ *                bounds must be non-decreasing; ids outside
+ *                [bounds[t][0], bounds[t][G]) go to no GPU and are dropped.
+ *   indices, nnz, offsets
+ *                the mini-batch in the layout eb_forward takes (offsets
+ *                [T*B+1] clamped into [0, nnz]).
+ *   out_offsets  device int64 [G][T*B+1]: destination g's CSR offsets for
+ *                the same T*B bags, out_offsets[g][0] = 0.
+ *   out_indices  device int64 [nnz]: destination g's ids at
+ *                [segments[g], segments[g+1]), in (table, bag, position)
+ *                order.  They stay global ids: the receiving GPU pools them
+ *                with eb_forward and its own shard range.
+ *   segments     device int64 [G+1]; segments[G] = ids kept.
+ *   workspace    device scratch of at least eb_bucketize_workspace() bytes,
+ *                owned by the caller; its contents are not kept.
+ *   stream       a hipStream_t (NULL = the null stream); asynchronous.
+ *
+ * No allocation, no host synchronisation; calls that overlap on the same
+ * workspace race.  Errors: EB_ERR_INVALID for NULL buffers (indices and
+ * out_indices may be NULL when nnz == 0), negative sizes, or a workspace
+ * that is too small; EB_ERR_UNSUPPORTED for G > 1024 or a batch too large
+ * for one launch; EB_ERR_HIP when a launch fails.  With non-decreasing
+ * bounds the result equals the definition above; other bounds give an
+ * unspecified split but every access stays in bounds.
+ */
+int eb_bucketize(int32_t T, int64_t B, int32_t G, const int64_t *bounds, const int64_t *indices,
+                 int64_t nnz, const int64_t *offsets, int64_t *out_offsets, int64_t *out_indices,
+                 int64_t *segments, void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * eb_sum_partials -- add the partial results every GPU computed for this
+ * GPU's bags.
+ *
+ *   G            number of partial blocks, >= 1.
+ *   partials     device fp32 [G][B][T*D] (the all-to-all's receive buffer).
+ *   B, T, D      bags per table, tables, embedding dimension.
+ *   mean_offsets NULL to sum; else device int64 [T*B+1], the offsets of
+ *                this GPU's mini-batch: bag (t, b)'s sum is then divided by
+ *                its length (clamped into [0, nnz]; an empty bag gives 0),
+ *                giving mean pooling when every GPU pooled sums.
+ *   nnz          length of the ids those offsets index (used for clamping).
+ *   out          device fp32 [B][T*D].
+ *   stream       a hipStream_t; asynchronous.
+ *
+ * The sources are added in order s = 0 .. G-1 in fp32.  B*T*D == 0 is a
+ * no-op.  Errors: EB_ERR_INVALID for bad sizes or NULL buffers,
+ * EB_ERR_HIP when the launch fails.
+ */
+int eb_sum_partials(int32_t G, const float *partials, int64_t B, int32_t T, int32_t D,
+                    const int64_t *mean_offsets, int64_t nnz, float *out, void *stream);
 
 /* eb_destroy -- free a handle (never the tables).  NULL is a no-op. */
 void eb_destroy(eb_tables *tables);

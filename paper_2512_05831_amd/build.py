@@ -1,7 +1,8 @@
 """Build step: compile the HIP library for gfx950, in tree.
 
 ``python -m paper_2512_05831_amd.build`` (or ``build_library()``) runs hipcc on
-``csrc/eb.hip`` and writes ``libeb.so`` next to this file.
+``csrc/eb.hip`` and ``csrc/eb_exchange.hip`` and writes ``libeb.so`` next to this
+file.
 """
 from __future__ import annotations
 
@@ -11,7 +12,7 @@ import subprocess
 import sys
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-SRC = os.path.join(HERE, "csrc", "eb.hip")
+SRCS = [os.path.join(HERE, "csrc", "eb.hip"), os.path.join(HERE, "csrc", "eb_exchange.hip")]
 LIB = os.path.join(HERE, "libeb.so")
 ARCH = "gfx950"
 
@@ -32,7 +33,7 @@ def hipcc() -> str:
 def build_library(verbose: bool = False) -> str:
     """Compile libeb.so (always recompiles) and return its path."""
     tmp = LIB + ".tmp"
-    cmd = [hipcc(), *HIPCC_FLAGS, SRC, "-o", tmp]
+    cmd = [hipcc(), *HIPCC_FLAGS, *SRCS, "-o", tmp]
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         raise RuntimeError(f"hipcc failed ({res.returncode}):\n{' '.join(cmd)}\n{res.stderr}")

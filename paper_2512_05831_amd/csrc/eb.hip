@@ -45,6 +45,7 @@
 #include <vector>
 
 #include "../../include/eb.h"
+#include "eb_internal.h"
 
 namespace {
 
@@ -407,27 +408,40 @@ __global__ __launch_bounds__(kBlock) void eb_gather_plain(const GatherArgs a)
 
 thread_local std::string g_last_error;
 
-int fail(int code, const std::string &msg)
-{
-    g_last_error = msg;
-    return code;
-}
+using eb_detail::fail;
 
 // Team shape for a row of rb bytes (rb % 16 == 0, rb <= 8192).
 struct Shape {
     int R, P, C;
 };
 
-Shape team_shape(int rb)
+// Small batches.  A launch whose normal mapping has fewer waves than the GPU
+// holds (256 CUs x 32) leaves it partly idle, and each bag's chain of
+// dependent loads sets the time.  One wave per bag with 6 rows in flight per
+// lane then wins when bags are long (more than twice the rows the normal
+// mapping keeps in flight per bag) and few enough (measured over the paper's
+// single-GPU shapes: up to 1.5x faster, never slower).
+constexpr int64_t kWaveSlots = 256 * 32;
+constexpr int64_t kFewBagsMax = 2048;
+
+int rows_in_flight_per_bag(const Shape &s, bool stream)
+{
+    const int u_cached = s.C >= 6 ? 1 : 6 / s.C;
+    const int u = (stream && s.R * s.C >= 8) ? (s.C >= 2 ? 1 : 2) : u_cached;
+    return s.P * u;
+}
+
+Shape team_shape(int rb, bool few)
 {
     Shape s;
     const int chunks = rb / 16;
     s.R = 1;
     while (s.R < chunks && s.R < kWave) s.R *= 2;
     s.C = (chunks + s.R - 1) / s.R;
-    // Wide rows: one bag per wave.  Narrow rows: 16-lane teams (4 bags per
-    // wave), so the group reduction stays inside a DPP row.
-    s.P = s.R >= 16 ? kWave / s.R : 16 / s.R;
+    // Wide rows or small batches: one bag per wave.  Otherwise narrow rows
+    // get 16-lane teams (4 bags per wave), so the group reduction stays
+    // inside a DPP row.
+    s.P = (few || s.R >= 16) ? kWave / s.R : 16 / s.R;
     return s;
 }
 
@@ -436,37 +450,45 @@ using KernelFn = void (*)(GatherArgs);
 // Rows in flight per lane: streamed (non-temporal) rows of 128 B and more all
 // go to HBM, where two per lane saturate the random-read rate and more only
 // queue; narrower rows need more requests per byte in flight, and cached rows
-// profit from deeper overlap while hits return early.
-template <int DT, int R, int C>
+// profit from deeper overlap while hits return early.  A small batch (fewer
+// bags than fill the GPU) is bound by each bag's chain of dependent loads
+// instead: every bag then gets a whole wave and 6 rows in flight per lane.
+template <int DT, int R, int C, bool kFew>
 KernelFn team_kernel(bool stream)
 {
-    constexpr int P = R >= 16 ? kWave / R : 16 / R;
+    constexpr int P = (kFew || R >= 16) ? kWave / R : 16 / R;
     constexpr int U_CACHED = C >= 6 ? 1 : 6 / C;
-    constexpr int U_STREAM = R * C >= 8 ? (C >= 2 ? 1 : 2) : U_CACHED;
+    constexpr int U_STREAM = (!kFew && R * C >= 8) ? (C >= 2 ? 1 : 2) : U_CACHED;
     return stream ? eb_gather_team<DT, R, P, C, U_STREAM, true>
                   : eb_gather_team<DT, R, P, C, U_CACHED, false>;
 }
 
+template <int DT, int R, int C>
+KernelFn team_kernel(bool stream, bool few)
+{
+    return few ? team_kernel<DT, R, C, true>(stream) : team_kernel<DT, R, C, false>(stream);
+}
+
 template <int DT>
-KernelFn pick_team_kernel(int R, int C, bool stream)
+KernelFn pick_team_kernel(int R, int C, bool stream, bool few)
 {
     switch (R) {
-    case 1: return team_kernel<DT, 1, 1>(stream);
-    case 2: return team_kernel<DT, 2, 1>(stream);
-    case 4: return team_kernel<DT, 4, 1>(stream);
-    case 8: return team_kernel<DT, 8, 1>(stream);
-    case 16: return team_kernel<DT, 16, 1>(stream);
-    case 32: return team_kernel<DT, 32, 1>(stream);
+    case 1: return team_kernel<DT, 1, 1>(stream, few);
+    case 2: return team_kernel<DT, 2, 1>(stream, few);
+    case 4: return team_kernel<DT, 4, 1>(stream, few);
+    case 8: return team_kernel<DT, 8, 1>(stream, few);
+    case 16: return team_kernel<DT, 16, 1>(stream, few);
+    case 32: return team_kernel<DT, 32, 1>(stream, few);
     default:
         switch (C) {
-        case 1: return team_kernel<DT, 64, 1>(stream);
-        case 2: return team_kernel<DT, 64, 2>(stream);
-        case 3: return team_kernel<DT, 64, 3>(stream);
-        case 4: return team_kernel<DT, 64, 4>(stream);
-        case 5: return team_kernel<DT, 64, 5>(stream);
-        case 6: return team_kernel<DT, 64, 6>(stream);
-        case 7: return team_kernel<DT, 64, 7>(stream);
-        case 8: return team_kernel<DT, 64, 8>(stream);
+        case 1: return team_kernel<DT, 64, 1>(stream, few);
+        case 2: return team_kernel<DT, 64, 2>(stream, few);
+        case 3: return team_kernel<DT, 64, 3>(stream, few);
+        case 4: return team_kernel<DT, 64, 4>(stream, few);
+        case 5: return team_kernel<DT, 64, 5>(stream, few);
+        case 6: return team_kernel<DT, 64, 6>(stream, few);
+        case 7: return team_kernel<DT, 64, 7>(stream, few);
+        case 8: return team_kernel<DT, 64, 8>(stream, few);
         }
     }
     return nullptr;
@@ -484,6 +506,12 @@ KernelFn pick_plain_kernel(int dtype)
 int elem_bytes(int dtype) { return dtype == EB_F32 ? 4 : 2; }
 
 } // namespace
+
+int eb_detail::fail(int code, const std::string &msg)
+{
+    g_last_error = msg;
+    return code;
+}
 
 struct eb_tables {
     int32_t T;
@@ -573,13 +601,18 @@ int eb_forward(const eb_tables *h, int32_t T, const int64_t *rows, int32_t D, in
     int bags_per_block = kWavesPerBlock;
     bool xcd_remap = false;
     if (team_path) {
-        const Shape sh = team_shape((int)rb);
         // Non-temporal loads lose for rows narrower than 128 bytes.
         const bool stream = (mode & EB_HINT_STREAM_ROWS) && rb >= 128;
+        const Shape normal = team_shape((int)rb, false);
+        const int64_t bags = (int64_t)T * B;
+        const int64_t waves = bags / (kWave / (normal.R * normal.P));
+        const bool few = waves < kWaveSlots && bags <= kFewBagsMax &&
+                         nnz > 2 * (int64_t)rows_in_flight_per_bag(normal, stream) * bags;
+        const Shape sh = team_shape((int)rb, few);
         switch (dtype) {
-        case EB_F32: fn = pick_team_kernel<EB_F32>(sh.R, sh.C, stream); break;
-        case EB_F16: fn = pick_team_kernel<EB_F16>(sh.R, sh.C, stream); break;
-        default: fn = pick_team_kernel<EB_BF16>(sh.R, sh.C, stream); break;
+        case EB_F32: fn = pick_team_kernel<EB_F32>(sh.R, sh.C, stream, few); break;
+        case EB_F16: fn = pick_team_kernel<EB_F16>(sh.R, sh.C, stream, few); break;
+        default: fn = pick_team_kernel<EB_BF16>(sh.R, sh.C, stream, few); break;
         }
         bags_per_block = (kWave / (sh.R * sh.P)) * kWavesPerBlock;
         // No reuse: each XCD takes a contiguous run of bags.  Otherwise

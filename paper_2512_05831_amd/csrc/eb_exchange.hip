@@ -1,0 +1,631 @@
+// Row-wise exchange, the parts one GPU computes (C ABI in include/eb.h).
+//
+// Around the gather of a row-wise-parallel Embedding Bag (arXiv 2512.05831,
+// Sec. 4.2 and the three kernels of Sec. 4.3) two collectives move data
+// between GPUs: the mini-batch's ids go to the GPUs that hold their rows
+// (permute + all-to-all) and the partial sums come back (reduce-scatter, built
+// in the paper from an all-to-all followed by a local sum).  This file holds
+// the local halves:
+//
+//   eb_bucketize     sorts a mini-batch's ids by destination shard, keeping
+//                    (table, bag, position) order, and emits each
+//                    destination's CSR offsets: the send buffers and counts
+//                    of the all-to-all.
+//   eb_sum_partials  adds the G partial blocks received for this GPU's bags
+//                    (optionally dividing by the bag lengths for mean).
+//
+// Both are HBM-bound integer / streaming work; nothing here is a contraction.
+//
+// eb_bucketize runs three kernels on the caller's stream:
+//   1. count   : a wave takes 64 consecutive bags; each id's owner by binary
+//                search over the table's block bounds (staged in LDS); for
+//                ordinary CSR offsets the wave streams its whole id range in
+//                64-id chunks into a [bag][destination] histogram in LDS,
+//                else it walks the bags one at a time; counts land in
+//                out_offsets[g][p + 1] (coalesced per destination).
+//   2. scan    : inclusive scan of every destination's row of counts
+//                (reduce-then-scan over 2048-entry tiles: tile sums in the
+//                workspace, one workgroup scans them and writes segments).
+//   3. scatter : same waves; ids are written to segments[g] +
+//                out_offsets[g][p] + rank, the rank counting earlier ids of
+//                the bag with the same owner (ballots per distinct owner in
+//                each 64-id chunk), so the order is stable.  For ordinary CSR
+//                offsets one running slot per destination and wave suffices,
+//                since position order is then (bag, position) order.
+
+#include <hip/hip_runtime.h>
+
+#include <stdint.h>
+
+#include <algorithm>
+#include <cstring>
+#include <limits>
+#include <string>
+
+#include "../../include/eb.h"
+#include "eb_internal.h"
+
+namespace {
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kWave = 64;
+constexpr int kBlock = 256;
+constexpr int kWavesPerBlock = kBlock / kWave;
+constexpr int kScanTile = 2048;    // counts per scan tile
+constexpr int kMaxShards = 1024;   // destinations per call
+
+using eb_detail::fail;
+
+__device__ __forceinline__ void clamp_bag(int64_t &s, int64_t &e, int64_t nnz)
+{
+    s = s < 0 ? 0 : (s > nnz ? nnz : s);
+    e = e > nnz ? nnz : e;
+    e = e < s ? s : e;
+}
+
+// Owner of id i among G blocks [bnd[g], bnd[g+1]): the last g with
+// bnd[g] <= i, or -1 when i lies outside [bnd[0], bnd[G]).
+__device__ __forceinline__ int owner_of(const int64_t *bnd, int G, int64_t i)
+{
+    if (i < bnd[0] || i >= bnd[G]) return -1;
+    int lo = 0, hi = G; // invariant: bnd[lo] <= i < bnd[hi]
+    while (hi - lo > 1) {
+        const int mid = (lo + hi) >> 1;
+        if (bnd[mid] <= i) lo = mid; else hi = mid;
+    }
+    return lo;
+}
+
+// A wave takes 64 consecutive bags of one table; a block 4 waves.
+constexpr int kBagsPerWave = 64;
+constexpr int kBagsPerBlock = kBagsPerWave * kWavesPerBlock;
+constexpr int kFastShards = 32; // count's per-(bag, destination) histogram fits LDS up to here
+constexpr int kChunks = 4;      // 64-id chunks loaded ahead
+constexpr int kBallotShards = 8; // scatter ranks by one ballot per destination up to here
+
+struct BucketArgs {
+    const int64_t *bounds;   // [T][G+1]
+    const int64_t *indices;
+    const int64_t *offsets;  // [T*B+1]
+    int64_t *out_offsets;    // [G][T*B+1]
+    int64_t *out_indices;
+    const int64_t *segments; // [G+1] (scatter pass)
+    int64_t nnz;
+    int64_t B;
+    int64_t TB;
+    int32_t G;
+    int32_t blocks_per_table;
+};
+
+// Dynamic LDS: the table's G+1 bounds, then one area per wave.
+__host__ __device__ inline size_t count_wave_bytes(int G) { return 64 * 8 + (size_t)4 * G * (G <= kFastShards ? kBagsPerWave : 1); }
+__host__ __device__ inline size_t count_lds_bytes(int G) { return (size_t)(G + 1) * 8 + kWavesPerBlock * count_wave_bytes(G); }
+__host__ __device__ inline size_t scatter_lds_bytes(int G) { return (size_t)(G + 1) * 8 + (size_t)kWavesPerBlock * G * 8; }
+
+__device__ __forceinline__ int64_t shfl_down64(int64_t v, int d)
+{
+    const int lo = __shfl_down((int)(v & 0xFFFFFFFF), d);
+    const int hi = __shfl_down((int)(v >> 32), d);
+    return ((int64_t)hi << 32) | (uint32_t)lo;
+}
+
+__device__ __forceinline__ int64_t readlane64(int64_t v, int l)
+{
+    const int lo = __builtin_amdgcn_readlane((int)(v & 0xFFFFFFFF), l);
+    const int hi = __builtin_amdgcn_readlane((int)(v >> 32), l);
+    return ((int64_t)hi << 32) | (uint32_t)lo;
+}
+
+// The wave's bags: lane l < nb gets bag p0+l's clamped range [s, e).  Returns
+// whether those ranges tile [S, E) in bag order (ordinary CSR offsets), the
+// case where position order within the wave is (bag, position) order.
+__device__ __forceinline__ bool wave_bags(const BucketArgs &a, int64_t p0, int nb, int lane,
+                                          int64_t &s, int64_t &e, int64_t &S, int64_t &E)
+{
+    s = 0;
+    e = 0;
+    if (lane < nb) {
+        s = a.offsets[p0 + lane];
+        e = a.offsets[p0 + lane + 1];
+        clamp_bag(s, e, a.nnz);
+    }
+    const int64_t s_next = shfl_down64(s, 1);
+    const bool gap = lane + 1 < nb && e != s_next;
+    S = readlane64(s, 0);
+    E = readlane64(e, nb - 1);
+    return __ballot(gap) == 0;
+}
+
+__device__ __forceinline__ void wave_sync_lds()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+__global__ __launch_bounds__(kBlock) void eb_bucket_count(const BucketArgs a)
+{
+    extern __shared__ int64_t lds[];
+    const int G = a.G;
+    int64_t *bnd = lds;
+    const int t = blockIdx.x / a.blocks_per_table;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = threadIdx.x / kWave;
+    char *area = (char *)(lds + G + 1) + wave * count_wave_bytes(G);
+    int64_t *starts = (int64_t *)area; // 64 bag starts
+    int *hist = (int *)(area + 64 * 8);
+    for (int g = threadIdx.x; g <= G; g += kBlock) bnd[g] = a.bounds[(int64_t)t * (G + 1) + g];
+    __syncthreads();
+
+    const int64_t b0 = (int64_t)(blockIdx.x - t * a.blocks_per_table) * kBagsPerBlock + wave * kBagsPerWave;
+    if (b0 >= a.B) return; // no block-wide barrier follows
+    const int nb = (int)min<int64_t>(kBagsPerWave, a.B - b0);
+    const int64_t p0 = (int64_t)t * a.B + b0;
+    const int64_t row = a.TB + 1;
+    if (p0 == 0)
+        for (int g = lane; g < G; g += kWave) a.out_offsets[(int64_t)g * row] = 0;
+    int64_t s, e, S, E;
+    const bool contiguous = wave_bags(a, p0, nb, lane, s, e, S, E);
+
+    if (contiguous && G <= kFastShards) {
+        starts[lane] = lane < nb ? s : INT64_MAX;
+        for (int x = lane; x < kBagsPerWave * G; x += kWave) hist[x] = 0;
+        wave_sync_lds();
+        for (int64_t k0 = S; k0 < E; k0 += kChunks * kWave) {
+            int64_t id[kChunks];
+#pragma unroll
+            for (int u = 0; u < kChunks; ++u) {
+                const int64_t k = k0 + u * kWave + lane;
+                id[u] = k < E ? __builtin_nontemporal_load(a.indices + k) : 0;
+            }
+#pragma unroll
+            for (int u = 0; u < kChunks; ++u) {
+                const int64_t k = k0 + u * kWave + lane;
+                if (k < E) {
+                    int l = 0; // last bag starting at or before k
+#pragma unroll
+                    for (int step = 32; step > 0; step >>= 1)
+                        if (starts[l + step] <= k) l += step;
+                    const int g = owner_of(bnd, G, id[u]);
+                    if (g >= 0) atomicAdd(&hist[l * G + g], 1);
+                }
+            }
+        }
+        wave_sync_lds();
+        for (int g = 0; g < G; ++g)
+            if (lane < nb) a.out_offsets[(int64_t)g * row + p0 + lane + 1] = hist[lane * G + g];
+        return;
+    }
+    // Any offsets, any G: one bag at a time.
+    for (int j = 0; j < nb; ++j) {
+        const int64_t sj = readlane64(s, j), ej = readlane64(e, j);
+        for (int g = lane; g < G; g += kWave) hist[g] = 0;
+        wave_sync_lds();
+        for (int64_t k = sj + lane; k < ej; k += kWave) {
+            const int g = owner_of(bnd, G, __builtin_nontemporal_load(a.indices + k));
+            if (g >= 0) atomicAdd(&hist[g], 1);
+        }
+        wave_sync_lds();
+        for (int g = lane; g < G; g += kWave) a.out_offsets[(int64_t)g * row + p0 + j + 1] = hist[g];
+        wave_sync_lds();
+    }
+}
+
+// Wave-level inclusive scan of one int64 per lane (Hillis-Steele over 64 lanes).
+__device__ __forceinline__ int64_t wave_inclusive_scan(int64_t v, int lane)
+{
+#pragma unroll
+    for (int d = 1; d < kWave; d <<= 1) {
+        const int lo = __shfl_up((int)(v & 0xFFFFFFFF), d);
+        const int hi = __shfl_up((int)(v >> 32), d);
+        const int64_t u = ((int64_t)hi << 32) | (uint32_t)lo;
+        if (lane >= d) v += u;
+    }
+    return v;
+}
+
+// Block-level inclusive scan of kBlock values (one per thread); returns the
+// thread's inclusive prefix and the block total through *total.
+__device__ int64_t block_inclusive_scan(int64_t v, int64_t *total)
+{
+    __shared__ int64_t wsum[kWavesPerBlock];
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = threadIdx.x / kWave;
+    v = wave_inclusive_scan(v, lane);
+    if (lane == kWave - 1) wsum[wave] = v;
+    __syncthreads();
+    int64_t before = 0, all = 0;
+    for (int w = 0; w < kWavesPerBlock; ++w) {
+        if (w < wave) before += wsum[w];
+        all += wsum[w];
+    }
+    __syncthreads();
+    *total = all;
+    return v + before;
+}
+
+struct ScanArgs {
+    int64_t *rows;      // out_offsets: G rows of TB+1 entries; entries 1..TB are scanned
+    int64_t *tile_sums; // [G][ntiles]
+    int64_t *segments;  // [G+1]
+    int64_t TB;
+    int32_t G;
+    int32_t ntiles;
+};
+
+// Pass 2a: sum of every tile (entries 1 + k*kScanTile ... of row g).
+__global__ __launch_bounds__(kBlock) void eb_scan_tile_sums(const ScanArgs a)
+{
+    const int g = blockIdx.y;
+    const int k = blockIdx.x;
+    const int64_t *row = a.rows + (int64_t)g * (a.TB + 1) + 1;
+    const int64_t lo = (int64_t)k * kScanTile;
+    const int64_t hi = std::min<int64_t>(lo + kScanTile, a.TB);
+    int64_t v = 0;
+    for (int64_t i = lo + threadIdx.x; i < hi; i += kBlock) v += row[i];
+    int64_t total;
+    block_inclusive_scan(v, &total);
+    if (threadIdx.x == 0) a.tile_sums[(int64_t)g * a.ntiles + k] = total;
+}
+
+// Pass 2b: exclusive scan of the tile sums of every row (in place), and the
+// destination segments (exclusive scan of the row totals).  One workgroup.
+__global__ __launch_bounds__(kBlock) void eb_scan_tile_prefix(const ScanArgs a)
+{
+    __shared__ int64_t row_total;
+    if (a.TB == 0) // no bags: every destination's offsets are the single 0
+        for (int g = threadIdx.x; g < a.G; g += kBlock) a.rows[g] = 0;
+    int64_t seg = 0;
+    for (int g = 0; g < a.G; ++g) {
+        int64_t carry = 0;
+        int64_t *ts = a.tile_sums + (int64_t)g * a.ntiles;
+        for (int k0 = 0; k0 < a.ntiles; k0 += kBlock) {
+            const int k = k0 + threadIdx.x;
+            const int64_t v = k < a.ntiles ? ts[k] : 0;
+            int64_t total;
+            const int64_t inc = block_inclusive_scan(v, &total);
+            if (k < a.ntiles) ts[k] = carry + inc - v;
+            carry += total;
+        }
+        if (threadIdx.x == 0) {
+            a.segments[g] = seg;
+            row_total = carry;
+        }
+        __syncthreads();
+        seg += row_total;
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) a.segments[a.G] = seg;
+}
+
+// Pass 2c: scan every tile and add its prefix, in place.
+__global__ __launch_bounds__(kBlock) void eb_scan_tiles(const ScanArgs a)
+{
+    const int g = blockIdx.y;
+    const int k = blockIdx.x;
+    int64_t *row = a.rows + (int64_t)g * (a.TB + 1) + 1;
+    const int64_t lo = (int64_t)k * kScanTile;
+    const int64_t hi = std::min<int64_t>(lo + kScanTile, a.TB);
+    int64_t carry = a.tile_sums[(int64_t)g * a.ntiles + k];
+    for (int64_t i0 = lo; i0 < hi; i0 += kBlock) {
+        const int64_t i = i0 + threadIdx.x;
+        const int64_t v = i < hi ? row[i] : 0;
+        int64_t total;
+        const int64_t inc = block_inclusive_scan(v, &total);
+        if (i < hi) row[i] = carry + inc;
+        carry += total;
+    }
+}
+
+// Scatter one chunk of up to 64 ids (lanes with g < 0 hold none): every
+// distinct destination in turn, lowest lane first, so the order is stable.
+__device__ __forceinline__ void scatter_chunk(const BucketArgs &a, int64_t *next, int lane, int g, int64_t id)
+{
+    const uint64_t below = (1ull << lane) - 1;
+    uint64_t pending = __ballot(g >= 0);
+    while (pending) {
+        const int leader = __builtin_ctzll(pending);
+        const int og = __shfl(g, leader);
+        const uint64_t same = __ballot(g == og);
+        const int64_t base = next[og];
+        if (g == og) a.out_indices[base + __popcll(same & below)] = id;
+        __builtin_amdgcn_wave_barrier();
+        if (lane == leader) next[og] = base + __popcll(same);
+        wave_sync_lds();
+        pending &= ~same;
+    }
+}
+
+__global__ __launch_bounds__(kBlock) void eb_bucket_scatter(const BucketArgs a)
+{
+    extern __shared__ int64_t lds[];
+    const int G = a.G;
+    int64_t *bnd = lds;
+    const int t = blockIdx.x / a.blocks_per_table;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = threadIdx.x / kWave;
+    int64_t *next = lds + G + 1 + wave * G; // next free slot per destination
+    for (int g = threadIdx.x; g <= G; g += kBlock) bnd[g] = a.bounds[(int64_t)t * (G + 1) + g];
+    __syncthreads();
+
+    const int64_t b0 = (int64_t)(blockIdx.x - t * a.blocks_per_table) * kBagsPerBlock + wave * kBagsPerWave;
+    if (b0 >= a.B) return; // no block-wide barrier follows
+    const int nb = (int)min<int64_t>(kBagsPerWave, a.B - b0);
+    const int64_t p0 = (int64_t)t * a.B + b0;
+    const int64_t row = a.TB + 1;
+    int64_t s, e, S, E;
+    const bool contiguous = wave_bags(a, p0, nb, lane, s, e, S, E);
+    if (contiguous && G <= kBallotShards) {
+        // Contiguous bags, few destinations: one ballot per destination and
+        // chunk gives every id its rank among the chunk's ids for the same
+        // destination; a single store then places the whole chunk.  Lane g
+        // keeps destination g's output slot in a register.
+        int64_t slot = lane < G ? a.segments[lane] + a.out_offsets[(int64_t)lane * row + p0] : 0;
+        const uint64_t below = (1ull << lane) - 1;
+        for (int64_t k0 = S; k0 < E; k0 += kChunks * kWave) {
+            int64_t id[kChunks];
+#pragma unroll
+            for (int u = 0; u < kChunks; ++u) {
+                const int64_t k = k0 + u * kWave + lane;
+                id[u] = k < E ? __builtin_nontemporal_load(a.indices + k) : 0;
+            }
+#pragma unroll
+            for (int u = 0; u < kChunks; ++u) {
+                const int64_t k = k0 + u * kWave + lane;
+                const int g = k < E ? owner_of(bnd, G, id[u]) : -1;
+                uint64_t mine = 0;
+                int added = 0;
+#pragma unroll
+                for (int d = 0; d < kBallotShards; ++d) {
+                    if (d < G) {
+                        const uint64_t m = __ballot(g == d);
+                        mine = g == d ? m : mine;
+                        added = lane == d ? __popcll(m) : added;
+                    }
+                }
+                const int src = g >= 0 ? g : 0;
+                const int64_t base = ((int64_t)__shfl((int)(slot >> 32), src) << 32) |
+                                     (uint32_t)__shfl((int)(slot & 0xFFFFFFFF), src);
+                if (g >= 0) a.out_indices[base + __popcll(mine & below)] = id[u];
+                slot += added;
+            }
+        }
+        return;
+    }
+    if (contiguous && G <= kWave) {
+        // Contiguous bags: within a destination, (bag, position) order is
+        // position order, so one running slot per destination suffices;
+        // lane g keeps destination g's in a register.
+        int64_t slot = lane < G ? a.segments[lane] + a.out_offsets[(int64_t)lane * row + p0] : 0;
+        const uint64_t below = (1ull << lane) - 1;
+        for (int64_t k0 = S; k0 < E; k0 += kChunks * kWave) {
+            int64_t id[kChunks];
+#pragma unroll
+            for (int u = 0; u < kChunks; ++u) {
+                const int64_t k = k0 + u * kWave + lane;
+                id[u] = k < E ? __builtin_nontemporal_load(a.indices + k) : 0;
+            }
+#pragma unroll
+            for (int u = 0; u < kChunks; ++u) {
+                const int64_t k = k0 + u * kWave + lane;
+                const int g = k < E ? owner_of(bnd, G, id[u]) : -1;
+                uint64_t pending = __ballot(g >= 0);
+                while (pending) {
+                    const int og = __builtin_amdgcn_readlane(g, __builtin_ctzll(pending));
+                    const uint64_t same = __ballot(g == og);
+                    const int64_t base = readlane64(slot, og);
+                    if (g == og) a.out_indices[base + __popcll(same & below)] = id[u];
+                    if (lane == og) slot += __popcll(same);
+                    pending &= ~same;
+                }
+            }
+        }
+        return;
+    }
+    if (contiguous) {
+        for (int g = lane; g < G; g += kWave) next[g] = a.segments[g] + a.out_offsets[(int64_t)g * row + p0];
+        wave_sync_lds();
+        for (int64_t k0 = S; k0 < E; k0 += kChunks * kWave) {
+            int64_t id[kChunks];
+#pragma unroll
+            for (int u = 0; u < kChunks; ++u) {
+                const int64_t k = k0 + u * kWave + lane;
+                id[u] = k < E ? __builtin_nontemporal_load(a.indices + k) : 0;
+            }
+#pragma unroll
+            for (int u = 0; u < kChunks; ++u) {
+                const int64_t k = k0 + u * kWave + lane;
+                scatter_chunk(a, next, lane, k < E ? owner_of(bnd, G, id[u]) : -1, id[u]);
+            }
+        }
+        return;
+    }
+    // Any offsets: one bag at a time.
+    for (int j = 0; j < nb; ++j) {
+        const int64_t sj = readlane64(s, j), ej = readlane64(e, j);
+        for (int g = lane; g < G; g += kWave)
+            next[g] = a.segments[g] + a.out_offsets[(int64_t)g * row + p0 + j];
+        wave_sync_lds();
+        for (int64_t k0 = sj; k0 < ej; k0 += kWave) {
+            const int64_t k = k0 + lane;
+            int64_t id = 0;
+            int g = -1;
+            if (k < ej) {
+                id = __builtin_nontemporal_load(a.indices + k);
+                g = owner_of(bnd, G, id);
+            }
+            scatter_chunk(a, next, lane, g, id);
+        }
+    }
+}
+
+// out[j] = sum over s of partials[s*n + j] (then / L of its bag for mean).
+struct PartialArgs {
+    const float *partials;
+    const int64_t *mean_offsets; // or null
+    float *out;
+    int64_t n;       // B * T * D
+    int64_t B;
+    int64_t width;   // T * D
+    int64_t nnz;
+    int32_t D;
+    int32_t G;
+};
+
+__device__ __forceinline__ float bag_scale(const PartialArgs &a, int64_t j)
+{
+    const int64_t b = j / a.width;
+    const int64_t t = (j - b * a.width) / a.D;
+    const int64_t p = t * a.B + b;
+    int64_t s = a.mean_offsets[p], e = a.mean_offsets[p + 1];
+    clamp_bag(s, e, a.nnz);
+    return e > s ? (float)(e - s) : 0.0f;
+}
+
+__global__ __launch_bounds__(kBlock) void eb_sum_partials_vec4(const PartialArgs a)
+{
+    const int64_t n4 = a.n / 4;
+    const int64_t stride = (int64_t)gridDim.x * kBlock;
+    for (int64_t q = (int64_t)blockIdx.x * kBlock + threadIdx.x; q < n4; q += stride) {
+        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+        for (int s = 0; s < a.G; ++s)
+            acc += __builtin_nontemporal_load((const f32x4 *)(a.partials + (int64_t)s * a.n) + q);
+        if (a.mean_offsets) {
+            const float L = bag_scale(a, q * 4);
+            acc = L > 0.f ? acc / L : (f32x4){0.f, 0.f, 0.f, 0.f};
+        }
+        __builtin_nontemporal_store(acc, (f32x4 *)a.out + q);
+    }
+}
+
+__global__ __launch_bounds__(kBlock) void eb_sum_partials_scalar(const PartialArgs a)
+{
+    const int64_t stride = (int64_t)gridDim.x * kBlock;
+    for (int64_t j = (int64_t)blockIdx.x * kBlock + threadIdx.x; j < a.n; j += stride) {
+        float acc = 0.f;
+        for (int s = 0; s < a.G; ++s) acc += a.partials[(int64_t)s * a.n + j];
+        if (a.mean_offsets) {
+            const float L = bag_scale(a, j);
+            acc = L > 0.f ? acc / L : 0.f;
+        }
+        a.out[j] = acc;
+    }
+}
+
+int64_t scan_tiles(int64_t TB) { return std::max<int64_t>(1, (TB + kScanTile - 1) / kScanTile); }
+
+} // namespace
+
+extern "C" {
+
+int eb_bucketize_workspace(int32_t T, int64_t B, int32_t G, size_t *bytes)
+{
+    if (!bytes) return fail(EB_ERR_INVALID, "eb_bucketize_workspace: NULL bytes");
+    *bytes = 0;
+    if (T < 0 || B < 0 || G < 1) return fail(EB_ERR_INVALID, "eb_bucketize_workspace: bad T, B or G");
+    if (G > kMaxShards) return fail(EB_ERR_UNSUPPORTED, "eb_bucketize_workspace: more than 1024 shards");
+    if (T > 0 && B > std::numeric_limits<int64_t>::max() / T / G / 8)
+        return fail(EB_ERR_INVALID, "eb_bucketize_workspace: sizes overflow");
+    *bytes = (size_t)G * (size_t)scan_tiles((int64_t)T * B) * sizeof(int64_t);
+    return EB_OK;
+}
+
+int eb_bucketize(int32_t T, int64_t B, int32_t G, const int64_t *bounds, const int64_t *indices,
+                 int64_t nnz, const int64_t *offsets, int64_t *out_offsets, int64_t *out_indices,
+                 int64_t *segments, void *workspace, size_t workspace_bytes, void *stream)
+{
+    size_t need = 0;
+    const int rc = eb_bucketize_workspace(T, B, G, &need);
+    if (rc != EB_OK) return rc;
+    if (nnz < 0) return fail(EB_ERR_INVALID, "eb_bucketize: negative nnz");
+    if (!segments || !out_offsets) return fail(EB_ERR_INVALID, "eb_bucketize: NULL segments or out_offsets");
+    const int64_t TB = (int64_t)T * B;
+    if (TB > 0 && (!bounds || !offsets)) return fail(EB_ERR_INVALID, "eb_bucketize: NULL bounds or offsets");
+    if (TB > 0 && nnz > 0 && (!indices || !out_indices))
+        return fail(EB_ERR_INVALID, "eb_bucketize: NULL indices or out_indices with nnz > 0");
+    if (workspace_bytes < need || (need > 0 && !workspace))
+        return fail(EB_ERR_INVALID, "eb_bucketize: workspace smaller than eb_bucketize_workspace reports");
+    hipStream_t st = (hipStream_t)stream;
+
+    BucketArgs ba;
+    std::memset(&ba, 0, sizeof ba);
+    ba.bounds = bounds;
+    ba.indices = indices;
+    ba.offsets = offsets;
+    ba.out_offsets = out_offsets;
+    ba.out_indices = out_indices;
+    ba.segments = segments;
+    ba.nnz = nnz;
+    ba.B = B;
+    ba.TB = TB;
+    ba.G = G;
+    const int64_t bpt = (B + kBagsPerBlock - 1) / kBagsPerBlock;
+    if (TB > 0 && (int64_t)T * bpt > std::numeric_limits<int32_t>::max())
+        return fail(EB_ERR_UNSUPPORTED, "eb_bucketize: batch too large for one launch");
+    ba.blocks_per_table = (int32_t)bpt;
+
+    ScanArgs sa;
+    sa.rows = out_offsets;
+    sa.tile_sums = (int64_t *)workspace;
+    sa.segments = segments;
+    sa.TB = TB;
+    sa.G = G;
+    sa.ntiles = (int32_t)scan_tiles(TB);
+
+    if (TB > 0) {
+        void *args[] = {&ba};
+        hipError_t err = hipLaunchKernel((const void *)eb_bucket_count, dim3((unsigned)(T * bpt)),
+                                         dim3(kBlock), args, count_lds_bytes(G), st);
+        if (err != hipSuccess) return fail(EB_ERR_HIP, std::string("eb_bucketize: ") + hipGetErrorString(err));
+        void *sargs[] = {&sa};
+        err = hipLaunchKernel((const void *)eb_scan_tile_sums, dim3(sa.ntiles, G), dim3(kBlock), sargs, 0, st);
+        if (err == hipSuccess)
+            err = hipLaunchKernel((const void *)eb_scan_tile_prefix, dim3(1), dim3(kBlock), sargs, 0, st);
+        if (err == hipSuccess)
+            err = hipLaunchKernel((const void *)eb_scan_tiles, dim3(sa.ntiles, G), dim3(kBlock), sargs, 0, st);
+        if (err == hipSuccess)
+            err = hipLaunchKernel((const void *)eb_bucket_scatter, dim3((unsigned)(T * bpt)), dim3(kBlock), args,
+                                  scatter_lds_bytes(G), st);
+        if (err != hipSuccess) return fail(EB_ERR_HIP, std::string("eb_bucketize: ") + hipGetErrorString(err));
+    } else {
+        // No bags: every destination is empty.
+        sa.ntiles = 0;
+        void *sargs[] = {&sa};
+        hipError_t err = hipLaunchKernel((const void *)eb_scan_tile_prefix, dim3(1), dim3(kBlock), sargs, 0, st);
+        if (err != hipSuccess) return fail(EB_ERR_HIP, std::string("eb_bucketize: ") + hipGetErrorString(err));
+    }
+    return EB_OK;
+}
+
+int eb_sum_partials(int32_t G, const float *partials, int64_t B, int32_t T, int32_t D,
+                    const int64_t *mean_offsets, int64_t nnz, float *out, void *stream)
+{
+    if (G < 1 || B < 0 || T < 0 || D < 1 || nnz < 0)
+        return fail(EB_ERR_INVALID, "eb_sum_partials: bad G, B, T, D or nnz");
+    const int64_t kMax = std::numeric_limits<int64_t>::max();
+    if (T > 0 && B > kMax / T / D / G) return fail(EB_ERR_INVALID, "eb_sum_partials: sizes overflow");
+    const int64_t n = B * T * D;
+    if (n == 0) return EB_OK;
+    if (!partials || !out) return fail(EB_ERR_INVALID, "eb_sum_partials: NULL partials or out");
+    PartialArgs a;
+    a.partials = partials;
+    a.mean_offsets = mean_offsets;
+    a.out = out;
+    a.n = n;
+    a.B = B;
+    a.width = (int64_t)T * D;
+    a.nnz = nnz;
+    a.D = D;
+    a.G = G;
+    const bool vec = D % 4 == 0 && ((uintptr_t)partials % 16) == 0 && ((uintptr_t)out % 16) == 0;
+    const int64_t items = vec ? n / 4 : n;
+    const int64_t grid = std::max<int64_t>(1, std::min<int64_t>((items + kBlock - 1) / kBlock, 8192));
+    void *args[] = {&a};
+    hipError_t err = hipLaunchKernel(vec ? (const void *)eb_sum_partials_vec4 : (const void *)eb_sum_partials_scalar,
+                                     dim3((unsigned)grid), dim3(kBlock), args, 0, (hipStream_t)stream);
+    if (err != hipSuccess) return fail(EB_ERR_HIP, std::string("eb_sum_partials: ") + hipGetErrorString(err));
+    return EB_OK;
+}
+
+} // extern "C"

@@ -49,6 +49,12 @@ def library() -> ctypes.CDLL:
         lib.eb_destroy.restype = None
         lib.eb_last_error.argtypes = []
         lib.eb_last_error.restype = ctypes.c_char_p
+        lib.eb_bucketize_workspace.argtypes = [i32, i64, i32, ctypes.POINTER(ctypes.c_size_t)]
+        lib.eb_bucketize_workspace.restype = ctypes.c_int
+        lib.eb_bucketize.argtypes = [i32, i64, i32, p, p, i64, p, p, p, p, p, ctypes.c_size_t, p]
+        lib.eb_bucketize.restype = ctypes.c_int
+        lib.eb_sum_partials.argtypes = [i32, p, i64, i32, i32, p, i64, p, p]
+        lib.eb_sum_partials.restype = ctypes.c_int
         _lib = lib
     return _lib
 
@@ -90,6 +96,77 @@ def eb_forward(handle, T: int, rows, D: int, dtype: int, indices_ptr: int, nnz: 
 
 def eb_destroy(handle) -> None:
     library().eb_destroy(handle)
+
+
+def eb_bucketize_workspace(T: int, B: int, G: int) -> int:
+    n = ctypes.c_size_t()
+    _check(library().eb_bucketize_workspace(T, B, G, ctypes.byref(n)))
+    return n.value
+
+
+def eb_bucketize(T: int, B: int, G: int, bounds_ptr: int, indices_ptr: int | None, nnz: int,
+                 offsets_ptr: int, out_offsets_ptr: int, out_indices_ptr: int | None,
+                 segments_ptr: int, workspace_ptr: int | None, workspace_bytes: int,
+                 stream_ptr: int | None) -> None:
+    _check(library().eb_bucketize(T, B, G, bounds_ptr, indices_ptr or None, nnz, offsets_ptr,
+                                  out_offsets_ptr, out_indices_ptr or None, segments_ptr,
+                                  workspace_ptr or None, workspace_bytes, stream_ptr or None))
+
+
+def eb_sum_partials(G: int, partials_ptr: int, B: int, T: int, D: int,
+                    mean_offsets_ptr: int | None, nnz: int, out_ptr: int,
+                    stream_ptr: int | None) -> None:
+    _check(library().eb_sum_partials(G, partials_ptr, B, T, D, mean_offsets_ptr or None, nnz,
+                                     out_ptr, stream_ptr or None))
+
+
+def bucketize(bounds, indices, offsets, T: int, B: int, stream=None):
+    """Torch convenience for eb_bucketize.  ``bounds``: int64 device [T, G+1].
+    Returns (out_offsets [G, T*B+1], out_indices [nnz], segments [G+1]) on the
+    device; the ids kept are out_indices[:segments[G]]."""
+    import torch
+
+    dev = indices.device
+    G = int(bounds.shape[1]) - 1
+    for x in (bounds, indices, offsets):
+        if x.dtype != torch.int64 or not x.is_contiguous():
+            raise ValueError("bounds / indices / offsets must be contiguous int64")
+    if bounds.shape[0] != T or offsets.numel() != T * B + 1:
+        raise ValueError("bounds must be [T, G+1] and offsets [T*B+1]")
+    out_off = torch.empty((G, T * B + 1), dtype=torch.int64, device=dev)
+    out_idx = torch.empty(max(1, indices.numel()), dtype=torch.int64, device=dev)
+    seg = torch.empty(G + 1, dtype=torch.int64, device=dev)
+    nbytes = eb_bucketize_workspace(T, B, G)
+    ws = torch.empty(max(1, nbytes), dtype=torch.uint8, device=dev)
+    if stream is None:
+        stream = torch.cuda.current_stream(dev)
+    eb_bucketize(T, B, G, bounds.data_ptr(), indices.data_ptr() if indices.numel() else None,
+                 indices.numel(), offsets.data_ptr(), out_off.data_ptr(), out_idx.data_ptr(),
+                 seg.data_ptr(), ws.data_ptr(), nbytes, stream.cuda_stream)
+    return out_off, out_idx, seg, ws
+
+
+def sum_partials(partials, B: int, T: int, D: int, mean_offsets=None, nnz: int = 0, out=None,
+                 stream=None):
+    """Torch convenience for eb_sum_partials.  ``partials``: fp32 device [G, B, T*D]."""
+    import torch
+
+    if partials.dtype != torch.float32 or not partials.is_contiguous():
+        raise ValueError("partials must be contiguous fp32")
+    G = int(partials.shape[0])
+    if partials.numel() != G * B * T * D:
+        raise ValueError("partials must be [G, B, T*D]")
+    if out is None:
+        out = torch.empty((B, T * D), dtype=torch.float32, device=partials.device)
+    if mean_offsets is not None and (mean_offsets.dtype != torch.int64 or
+                                     mean_offsets.numel() != T * B + 1):
+        raise ValueError("mean_offsets must be int64 [T*B+1]")
+    if stream is None:
+        stream = torch.cuda.current_stream(partials.device)
+    eb_sum_partials(G, partials.data_ptr(), B, T, D,
+                    None if mean_offsets is None else mean_offsets.data_ptr(), nnz,
+                    out.data_ptr(), stream.cuda_stream)
+    return out
 
 
 _TORCH_DTYPE_CODES = {"torch.float32": EB_F32, "torch.float16": EB_F16, "torch.bfloat16": EB_BF16}

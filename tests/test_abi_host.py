@@ -24,7 +24,8 @@ def declared_functions():
 
 
 def test_header_declares_the_boundary():
-    assert declared_functions() == ["eb_create_tables", "eb_destroy", "eb_forward", "eb_last_error"]
+    assert declared_functions() == ["eb_bucketize", "eb_bucketize_workspace", "eb_create_tables",
+                                    "eb_destroy", "eb_forward", "eb_last_error", "eb_sum_partials"]
 
 
 def test_library_exports_every_declared_symbol():
@@ -131,3 +132,54 @@ def test_error_message_is_per_failure():
         assert "mode" in eb.eb_last_error()
     finally:
         eb.eb_destroy(h)
+
+
+def test_bucketize_workspace_sizes():
+    assert eb.eb_bucketize_workspace(26, 16384, 8) == 8 * ((26 * 16384 + 2047) // 2048) * 8
+    assert eb.eb_bucketize_workspace(0, 0, 1) == 8
+    assert code_of(lambda: eb.eb_bucketize_workspace(1, 1, 0)) == eb.EB_ERR_INVALID
+    assert code_of(lambda: eb.eb_bucketize_workspace(-1, 1, 2)) == eb.EB_ERR_INVALID
+    assert code_of(lambda: eb.eb_bucketize_workspace(1, 1, 1025)) == eb.EB_ERR_UNSUPPORTED
+    assert eb.library().eb_bucketize_workspace(1, 1, 1, None) == eb.EB_ERR_INVALID
+
+
+def bucketize(**kw):
+    args = dict(T=2, B=4, G=2, bounds_ptr=FAKE, indices_ptr=FAKE, nnz=10, offsets_ptr=FAKE,
+                out_offsets_ptr=FAKE, out_indices_ptr=FAKE, segments_ptr=FAKE, workspace_ptr=FAKE,
+                workspace_bytes=1 << 20, stream_ptr=None)
+    args.update(kw)
+    return eb.eb_bucketize(**args)
+
+
+@pytest.mark.parametrize("kw", [
+    dict(G=0), dict(T=-1), dict(B=-1), dict(nnz=-1), dict(segments_ptr=None),
+    dict(out_offsets_ptr=None), dict(bounds_ptr=None), dict(offsets_ptr=None),
+    dict(indices_ptr=None), dict(out_indices_ptr=None), dict(workspace_bytes=8),
+    dict(workspace_ptr=None),
+])
+def test_bucketize_rejects(kw):
+    assert code_of(lambda: bucketize(**kw)) == eb.EB_ERR_INVALID
+    assert "eb_bucketize" in eb.eb_last_error()
+
+
+def test_bucketize_too_many_shards():
+    assert code_of(lambda: bucketize(G=2000)) == eb.EB_ERR_UNSUPPORTED
+
+
+def sum_partials(**kw):
+    args = dict(G=2, partials_ptr=FAKE, B=4, T=2, D=8, mean_offsets_ptr=None, nnz=0,
+                out_ptr=FAKE, stream_ptr=None)
+    args.update(kw)
+    return eb.eb_sum_partials(**args)
+
+
+@pytest.mark.parametrize("kw", [dict(G=0), dict(B=-1), dict(T=-1), dict(D=0), dict(nnz=-1),
+                                dict(partials_ptr=None), dict(out_ptr=None), dict(B=1 << 62)])
+def test_sum_partials_rejects(kw):
+    assert code_of(lambda: sum_partials(**kw)) == eb.EB_ERR_INVALID
+    assert "eb_sum_partials" in eb.eb_last_error()
+
+
+def test_sum_partials_empty_is_noop():
+    sum_partials(B=0, partials_ptr=None, out_ptr=None)
+    sum_partials(T=0, partials_ptr=None, out_ptr=None)

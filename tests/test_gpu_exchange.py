@@ -1,0 +1,195 @@
+"""GPU parity of the row-wise exchange parts (eb_bucketize, eb_sum_partials)
+against the oracle, and the whole row-wise pipeline on one GPU.
+
+bucketize is integer work: offsets, ids and segments must match bit for bit.
+sum_partials adds G fp32 blocks in order: within Higham's gamma_{G-1} of the
+fp64 sum (relative to the sum of magnitudes), one more rounding for mean.
+The pipeline (bucketize -> eb_forward on every destination's shard -> sum of
+the partials) must reproduce the unsharded pooling exactly on dyadic tables.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_util import U32, gamma, to_device_table
+from paper_2512_05831_amd import eb, workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+
+def even_bounds(rows, G):
+    return np.array([[g * r // G for g in range(G + 1)] for r in rows], dtype=np.int64)
+
+
+def run_bucketize(bounds, idx, off, T, B, device):
+    d_b = torch.from_numpy(np.ascontiguousarray(bounds, dtype=np.int64)).to(device)
+    d_i = torch.from_numpy(np.ascontiguousarray(idx, dtype=np.int64)).to(device)
+    d_o = torch.from_numpy(np.ascontiguousarray(off, dtype=np.int64)).to(device)
+    out_off, out_idx, seg, ws = eb.bucketize(d_b, d_i, d_o, T, B)
+    torch.cuda.synchronize()
+    seg_h = seg.cpu().numpy()
+    return out_off.cpu().numpy(), out_idx.cpu().numpy()[:seg_h[-1]], seg_h
+
+
+def bucket_case(seed, G, T=None, B=None, maxL=40, uneven=False, oob=True):
+    g = np.random.default_rng(seed)
+    T = T or int(g.integers(1, 6))
+    B = B or int(g.integers(1, 300))
+    rows = [int(g.integers(1, 5000)) for _ in range(T)]
+    L = g.integers(0, maxL + 1, T * B)
+    off = wl.offsets_from_lengths(L)
+    idx = np.concatenate([g.integers(-7 if oob else 0, rows[t] + (7 if oob else 0),
+                                     int(off[(t + 1) * B] - off[t * B])) for t in range(T)])
+    if uneven:
+        bounds = np.sort(g.integers(0, max(rows) + 1, (T, G + 1)), axis=1)
+    else:
+        bounds = even_bounds(rows, G)
+    return T, B, idx, off, bounds
+
+
+def check_bucketize(T, B, idx, off, bounds, device):
+    got = run_bucketize(bounds, idx, off, T, B, device)
+    want = oracle.bucketize(bounds, idx, off, T, B)
+    for name, a, b in zip(("out_offsets", "out_indices", "segments"), got, want):
+        assert np.array_equal(a, b), name
+
+
+@pytest.mark.parametrize("G", [1, 2, 3, 8, 17, 64, 1024])
+@pytest.mark.parametrize("seed", range(3))
+def test_bucketize_matches_oracle(G, seed, device):
+    T, B, idx, off, bounds = bucket_case(seed * 31 + G, G, uneven=(seed == 2))
+    check_bucketize(T, B, idx, off, bounds, device)
+
+
+@pytest.mark.parametrize("B", [1, 3, 4, 5, 2047, 2048, 2049])
+def test_bucketize_batch_tails(B, device):
+    T, B, idx, off, bounds = bucket_case(B, 4, T=3, B=B, maxL=9)
+    check_bucketize(T, B, idx, off, bounds, device)
+
+
+def test_bucketize_long_bags_and_skew(device):
+    g = np.random.default_rng(9)
+    T, B, G = 2, 50, 8
+    L = g.integers(0, 700, T * B)
+    off = wl.offsets_from_lengths(L)
+    idx = wl.zipf_ranks(g, int(off[-1]), 100_000, 1.2) - 1  # most ids in the first block
+    bounds = even_bounds([100_000, 100_000], G)
+    check_bucketize(T, B, idx, off, bounds, device)
+
+
+def test_bucketize_edge_cases(device):
+    # no ids at all
+    off = np.zeros(2 * 5 + 1, dtype=np.int64)
+    got = run_bucketize(even_bounds([10, 10], 3), np.zeros(0, np.int64), off, 2, 5, device)
+    assert np.all(got[0] == 0) and got[2].tolist() == [0, 0, 0, 0]
+    # no bags
+    got = run_bucketize(np.zeros((0, 4), np.int64), np.zeros(0, np.int64), np.zeros(1, np.int64), 0, 7, device)
+    assert got[0].shape == (3, 1) and np.all(got[0] == 0) and got[2].tolist() == [0, 0, 0, 0]
+    # malformed offsets, empty and all-covering blocks, ids nobody owns
+    idx = np.array([5, -1, 9, 3, 100, 7, 0, 8], dtype=np.int64)
+    off = np.array([0, 3, 2, -4, 99], dtype=np.int64)
+    bounds = np.array([[0, 0, 4, 4, 10]], dtype=np.int64)
+    check_bucketize(1, 4, idx, off, bounds, device)
+
+
+def test_bucketize_dlrm_batch(device):
+    # the 26-table, 16384-bag, Zipf(1.05) batch, split over 8 GPUs by rows
+    w = wl.config(3)
+    off = w.offsets()
+    idx = w.indices(off)
+    bounds = even_bounds([w.rows] * w.T, 8)
+    check_bucketize(w.T, w.B, idx, off, bounds, device)
+
+
+def run_sum_partials(parts, B, T, D, mean_off, nnz, device, out=None):
+    d_p = torch.from_numpy(np.ascontiguousarray(parts, dtype=np.float32)).to(device)
+    d_m = None if mean_off is None else torch.from_numpy(np.asarray(mean_off, np.int64)).to(device)
+    res = eb.sum_partials(d_p, B, T, D, d_m, nnz, out=out)
+    torch.cuda.synchronize()
+    return res.cpu().numpy()
+
+
+def partial_tolerance(G):
+    return gamma(max(G - 1, 0)) + U32
+
+
+@pytest.mark.parametrize("G", [1, 2, 8, 64])
+@pytest.mark.parametrize("D", [3, 8, 128])
+@pytest.mark.parametrize("mean", [False, True])
+def test_sum_partials_matches_oracle(G, D, mean, device):
+    g = np.random.default_rng(G * 1000 + D)
+    B, T = 37, 3
+    parts = g.standard_normal((G, B, T * D)).astype(np.float32)
+    L = g.integers(0, 5, T * B)
+    off = wl.offsets_from_lengths(L)
+    mo = off if mean else None
+    got = run_sum_partials(parts, B, T, D, mo, int(off[-1]), device)
+    ref = oracle.sum_partials(parts, B, T, D, mo, int(off[-1]))
+    mag = oracle.sum_partials(np.abs(parts), B, T, D, mo, int(off[-1]))
+    zero = mag == 0
+    assert np.all(got[zero] == 0)
+    err = np.abs(got[~zero] - ref[~zero]) / mag[~zero]
+    assert err.max(initial=0) <= partial_tolerance(G)
+
+
+def test_sum_partials_unaligned_output(device):
+    G, B, T, D = 4, 9, 2, 16
+    parts = np.random.default_rng(1).standard_normal((G, B, T * D)).astype(np.float32)
+    buf = torch.full((B * T * D + 1,), float("nan"), device=device)
+    out = buf[1:].view(B, T * D)
+    got = run_sum_partials(parts, B, T, D, None, 0, device, out=out)
+    ref = oracle.sum_partials(parts, B, T, D)
+    mag = oracle.sum_partials(np.abs(parts), B, T, D)
+    assert np.max(np.abs(got - ref) / mag) <= partial_tolerance(G)
+    assert torch.isnan(buf[0]).item()
+
+
+def test_sum_partials_dyadic_exact(device):
+    G, B, T, D = 8, 100, 4, 32
+    parts = (np.random.default_rng(2).integers(-4096, 4097, (G, B, T * D)) * 2.0 ** -12).astype(np.float32)
+    got = run_sum_partials(parts, B, T, D, None, 0, device)
+    assert np.array_equal(got.astype(np.float64), oracle.sum_partials(parts, B, T, D))
+
+
+@pytest.mark.parametrize("G", [2, 8])
+@pytest.mark.parametrize("mode", [eb.EB_SUM, eb.EB_MEAN])
+def test_row_wise_pipeline_on_one_gpu(G, mode, device):
+    """bucketize -> eb_forward per destination shard -> eb_sum_partials."""
+    g = np.random.default_rng(G + 10 * mode)
+    T, B, D = 3, 300, 64
+    rows = [20_000, 7_000, 513]
+    L = g.integers(0, 60, T * B)
+    off = wl.offsets_from_lengths(L)
+    idx = np.concatenate([g.integers(0, rows[t], int(off[(t + 1) * B] - off[t * B]))
+                          for t in range(T)])
+    tables = [wl.table(5, t, D, wl.F16, 0, rows[t], values="dyadic") for t in range(T)]
+    bounds = even_bounds(rows, G)
+    out_off, out_idx, seg = run_bucketize(bounds, idx, off, T, B, device)
+    partials = torch.empty((G, B, T * D), dtype=torch.float32, device=device)
+    keep = []
+    for d in range(G):
+        ids_d = torch.from_numpy(np.ascontiguousarray(out_idx[seg[d]:seg[d + 1]])).to(device)
+        for t in range(T):
+            lo, hi = int(bounds[t][d]), int(bounds[t][d + 1])
+            off_t = out_off[d, t * B:(t + 1) * B + 1]
+            ids_t = ids_d[int(off_t[0]):int(off_t[-1])].contiguous()
+            d_off_t = torch.from_numpy(off_t - off_t[0]).to(device)
+            shard = to_device_table(np.ascontiguousarray(tables[t][lo:hi]), wl.F16, device)
+            et = eb.EmbeddingBagTables([shard], rows=[rows[t]], shard_lo=lo, shard_hi=hi)
+            out_t = torch.empty((B, D), dtype=torch.float32, device=device)
+            et.forward(ids_t, d_off_t, B, mode=eb.EB_SUM, out=out_t)
+            partials[d, :, t * D:(t + 1) * D] = out_t
+            keep.append((et, ids_t, d_off_t, shard))
+    torch.cuda.synchronize()
+    mean_off = torch.from_numpy(off).to(device) if mode == eb.EB_MEAN else None
+    got = eb.sum_partials(partials, B, T, D, mean_off, idx.size)
+    torch.cuda.synchronize()
+    ref, _, _ = oracle.forward(tables, rows, D, wl.F16, idx, off, B, mode)
+    if mode == eb.EB_SUM:
+        assert np.array_equal(got.cpu().numpy().astype(np.float64), ref)
+    else:
+        ref32 = ref.astype(np.float32)
+        assert np.all(np.abs(got.cpu().numpy() - ref32) <= np.spacing(np.abs(ref32)))
+    for et, *_ in keep:
+        et.close()
