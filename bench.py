@@ -274,6 +274,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--rows-policy", default="auto", choices=["auto", "cached", "stream"])
+    ap.add_argument("--graph", action="store_true",
+                    help="replay the steps from a captured HIP graph (launch-bound workloads)")
     ap.add_argument("--exchange", action="store_true",
                     help="time the row-wise exchange kernels instead (bucketize, sum_partials)")
     ap.add_argument("--sweep", choices=["paper"], default=None,
@@ -333,15 +335,29 @@ def main():
     torch.cuda.synchronize()
 
     K, W = args.steps, args.warmup
+    step_fns = calls
+    if args.graph:
+        # one graph per index batch; a step replays one of them
+        with torch.cuda.stream(stream):
+            for c in calls:
+                c()
+        torch.cuda.synchronize()
+        graphs = []
+        for c in calls:
+            gph = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(gph, stream=stream):
+                c()
+            graphs.append(gph)
+        step_fns = [gph.replay for gph in graphs]
     with torch.cuda.stream(stream):
         for i in range(W):
-            calls[i % len(calls)]()
+            step_fns[i % len(step_fns)]()
         torch.cuda.synchronize()
         ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         t_start = time.perf_counter()
         ev0.record(stream)
         for i in range(K):
-            calls[i % len(calls)]()
+            step_fns[i % len(step_fns)]()
         ev1.record(stream)
         torch.cuda.synchronize()
         t_end = time.perf_counter()
@@ -387,7 +403,8 @@ def main():
                    "shard": None if not w.sharded else [w.shard_lo, w.shard_hi],
                    "mode": "sum" if mode == wl.SUM else "mean",
                    "rows_cache_policy": "stream" if stream_rows else "cached",
-                   "index_batches_cycled": len(batches)},
+                   "index_batches_cycled": len(batches),
+                   "launch": "hip graph replay" if args.graph else "eb_forward per step"},
         "bags_per_s": w.T * w.B / (ms_per_step / 1e3),
         "kernel_us_mean": launch_ms * 1e3,
         "effective_GBps": achieved,
