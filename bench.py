@@ -49,10 +49,11 @@ def kernel_source_hash() -> str:
     return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()[:16]
 
 
-def algorithmic_bytes(w, local_ids: int, nnz: int, with_hits: bool) -> int:
-    """Every gathered row once, every id and offset, the fp32 output (and the
-    int32 hit counts when written)."""
-    b = local_ids * w.D * w.elem_bytes + nnz * 8 + (w.T * w.B + 1) * 8 + w.B * w.T * w.D * 4
+def algorithmic_bytes(w, local_ids: int, nnz: int, with_hits: bool, index_bytes: int = 8) -> int:
+    """Every gathered row once, every id and offset (index_bytes each), the
+    fp32 output (and the int32 hit counts when written)."""
+    b = (local_ids * w.D * w.elem_bytes + (nnz + w.T * w.B + 1) * index_bytes +
+         w.B * w.T * w.D * 4)
     if with_hits:
         b += w.B * w.T * 4
     return int(b)
@@ -198,14 +199,17 @@ def exchange_bench(torch, dev, eb, K, W):
                       "frac_of_8TBps": round(by / us / 1e3 / HBM_PEAK_GBPS, 4)}), flush=True)
 
 
-def paper_sweep(torch, dev, eb):
+def paper_sweep(torch, dev, eb, index_type="i64"):
     """The gather shapes the paper varies (Sec. 4.3 / 4.4: 2..64 tables, batch
     128 / 1024 / 4096, pooling 4 / 8 / 16, 128-byte rows; Sec. 5.1: one table
     with batch 128..1024, D 32..256, pooling 4 / 8 / 16, and 1..64 tables with
     batch 128 / 1024 / 4096, pooling 32, D 32 / 128), on one GPU with fp32
     tables and uniform ids.  The paper leaves the row count open: 1,000,000
     rows for the single-table sweep, 100,000 per table for the multi-table
-    ones.  One JSON line per shape: mean launch time over 200 launches."""
+    ones.  One JSON line per shape: mean launch time over 200 launches.
+    ``index_type`` "i32" passes the ids and offsets as int32."""
+    idt = torch.int32 if index_type == "i32" else torch.int64
+    ib = 4 if index_type == "i32" else 8
     shapes = []
     for T in (2, 4, 8, 16, 32, 64):
         for B in (128, 1024, 4096):
@@ -236,8 +240,8 @@ def paper_sweep(torch, dev, eb):
         off = w.offsets()
         batches = [w.with_(seed=w.seed + j).indices(off) for j in range(4)]
         et = eb.EmbeddingBagTables(tables_for(T, rows, D), rows=[rows] * T)
-        d_off = torch.from_numpy(off).to(dev)
-        d_idx = [torch.from_numpy(b).to(dev) for b in batches]
+        d_off = torch.from_numpy(off).to(dev).to(idt)
+        d_idx = [torch.from_numpy(b).to(dev).to(idt) for b in batches]
         out = torch.empty((B, T * D), dtype=torch.float32, device=dev)
         calls = [et.prepare(i, d_off, B, eb.EB_SUM | eb.EB_HINT_STREAM_ROWS, out, None, stream)
                  for i in d_idx]
@@ -254,8 +258,9 @@ def paper_sweep(torch, dev, eb):
             torch.cuda.synchronize()
         us = ev0.elapsed_time(ev1) * 1e3 / K
         nnz = T * B * L
-        by = algorithmic_bytes(w, nnz, nnz, False)
-        print(json.dumps({"sweep": tag, "tables": T, "rows": rows, "D": D, "B": B, "L": L,
+        by = algorithmic_bytes(w, nnz, nnz, False, ib)
+        print(json.dumps({"sweep": tag, "index_type": index_type, "tables": T, "rows": rows,
+                          "D": D, "B": B, "L": L,
                           "us_per_launch": round(us, 2), "lookups_per_s": nnz / us * 1e6,
                           "algorithmic_GBps": round(by / us / 1e3, 1),
                           "frac_of_8TBps": round(by / us / 1e3 / HBM_PEAK_GBPS, 4)}), flush=True)
@@ -274,6 +279,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--rows-policy", default="auto", choices=["auto", "cached", "stream"])
+    ap.add_argument("--index-type", default="i64", choices=["i64", "i32"],
+                    help="integer type of the ids and offsets handed to the library")
     ap.add_argument("--graph", action="store_true",
                     help="replay the steps from a captured HIP graph (launch-bound workloads)")
     ap.add_argument("--exchange", action="store_true",
@@ -298,7 +305,7 @@ def main():
         copy_calibration(torch, dev, args.copy_calibration, args.steps)
         return
     if args.sweep == "paper":
-        paper_sweep(torch, dev, eb)
+        paper_sweep(torch, dev, eb, args.index_type)
         return
     if args.exchange:
         exchange_bench(torch, dev, eb, args.steps, args.warmup)
@@ -325,8 +332,13 @@ def main():
     et = eb.EmbeddingBagTables(dev_tables, rows=[w.rows] * w.T, shard_lo=w.shard_lo,
                                shard_hi=w.shard_hi)
     stream = torch.cuda.Stream(dev)
-    d_off = torch.from_numpy(off).to(dev)
-    d_idx = [torch.from_numpy(b).to(dev) for b in batches]
+    i32 = args.index_type == "i32"
+    if i32 and (int(off[-1]) > np.iinfo(np.int32).max or w.rows > np.iinfo(np.int32).max):
+        raise SystemExit("this workload's ids or offsets do not fit int32")
+    idt = torch.int32 if i32 else torch.int64
+    index_bytes = 4 if i32 else 8
+    d_off = torch.from_numpy(off).to(dev).to(idt)
+    d_idx = [torch.from_numpy(b).to(dev).to(idt) for b in batches]
     out = torch.empty((w.B, w.T * w.D), dtype=torch.float32, device=dev)
     hits = torch.empty((w.B, w.T), dtype=torch.int32, device=dev) if w.want_hits else None
     calls = [et.prepare(i, d_off, w.B, call_mode, out, hits, stream) for i in d_idx]
@@ -367,12 +379,12 @@ def main():
     ms_per_step = wall_ms / K
 
     steps_lookups = sum(nnz[i % len(nnz)] for i in range(K))
-    steps_bytes = sum(algorithmic_bytes(w, local[i % len(local)], nnz[i % len(nnz)], hits is not None)
-                      for i in range(K))
+    steps_bytes = sum(algorithmic_bytes(w, local[i % len(local)], nnz[i % len(nnz)], hits is not None,
+                                        index_bytes) for i in range(K))
     value = steps_lookups / (wall_ms / 1e3)
     achieved = steps_bytes / (region_ms / 1e3) / 1e9
     bytes_per_launch = steps_bytes / K
-    traffic = measured_traffic(w.name)
+    traffic = measured_traffic(w.name + ("-i32" if i32 else ""))
     log(f"bench: mean launch {launch_ms * 1e3:.1f} us over {K} back-to-back launches, "
         f"wall step {ms_per_step * 1e3:.1f} us, {achieved:.0f} GB/s algorithmic")
 
@@ -403,6 +415,7 @@ def main():
                    "shard": None if not w.sharded else [w.shard_lo, w.shard_hi],
                    "mode": "sum" if mode == wl.SUM else "mean",
                    "rows_cache_policy": "stream" if stream_rows else "cached",
+                   "index_type": "int32" if i32 else "int64",
                    "index_batches_cycled": len(batches),
                    "launch": "hip graph replay" if args.graph else "eb_forward per step"},
         "bags_per_s": w.T * w.B / (ms_per_step / 1e3),

@@ -66,6 +66,11 @@ enum { EB_SUM = 0, EB_MEAN = 1 };
  * changes no result. */
 enum { EB_HINT_STREAM_ROWS = 0x100 };
 
+/* Integer type of eb_forward_ex's indices and offsets (both the same).
+ * int32 ids save 4 bytes of HBM traffic per lookup; values are widened to
+ * int64 by sign extension, so every rule above applies unchanged. */
+enum { EB_IDX_I64 = 0, EB_IDX_I32 = 1 };
+
 /* Return codes. */
 enum {
     EB_OK = 0,
@@ -147,6 +152,48 @@ int eb_forward(const eb_tables *tables, int32_t T, const int64_t *rows, int32_t 
                const int64_t *indices, int64_t nnz, const int64_t *offsets, int64_t B,
                int32_t mode, int64_t shard_lo, int64_t shard_hi, float *out, int32_t *hits,
                void *stream);
+
+/*
+ * eb_forward_ex -- eb_forward with a choice of index width and of where each
+ * table's result lands in the output.  The pooling is exactly eb_forward's.
+ *
+ * The output layout serves the other two sharding schemes of Sec. 4.1 as well
+ * as row-wise shards: under column-wise parallelism a GPU stores columns
+ * [c0, c0+D) of every row of a table (a handle of width D over those
+ * columns) and writes its D-wide result at column t*D_full + c0 of the full
+ * output; under table-wise parallelism a GPU holds whole tables and writes
+ * each at that table's place in the full output.
+ *
+ *   tables ... B     as eb_forward, except:
+ *   index_type       EB_IDX_I64: indices and offsets are device int64;
+ *                    EB_IDX_I32: both are device int32.
+ *   mode, shard_lo, shard_hi
+ *                    as eb_forward.
+ *   out              device fp32 [B, ldo]: bag b of table t goes to
+ *                    out[b*ldo + out_cols[t] + c], c < D.  Only those
+ *                    elements are written; the other columns keep their
+ *                    contents.
+ *   ldo              output row stride in floats, >= 1.
+ *   out_cols         host array [T] or NULL (then out_cols[t] = t*D).  Every
+ *                    range [out_cols[t], out_cols[t] + D) must lie inside
+ *                    [0, ldo) and no two may overlap.  Copied before return.
+ *   hits             device int32 [B, ldh] or NULL: hits[b*ldh + t].
+ *   ldh              hits row stride, >= T when hits is not NULL.
+ *   stream           as eb_forward.
+ *
+ * eb_forward(...) is eb_forward_ex with EB_IDX_I64, ldo = T*D,
+ * out_cols = NULL and ldh = T.  Rows take the 16-byte vector path only when
+ * out, ldo and every out_cols[t] keep each output row 16-byte aligned; other
+ * layouts are correct but slower.
+ *
+ * Errors: those of eb_forward, and EB_ERR_INVALID for an unknown index_type,
+ * ldo < 1, a table's columns outside [0, ldo), overlapping tables, ldh < T
+ * with hits, or B*ldo / B*ldh overflowing int64.
+ */
+int eb_forward_ex(const eb_tables *tables, int32_t T, const int64_t *rows, int32_t D, int32_t dtype,
+                  int32_t index_type, const void *indices, int64_t nnz, const void *offsets, int64_t B,
+                  int32_t mode, int64_t shard_lo, int64_t shard_hi, float *out, int64_t ldo,
+                  const int64_t *out_cols, int32_t *hits, int64_t ldh, void *stream);
 
 /*
  * The row-wise exchange around the gather, one GPU's part (Sec. 4.2; the

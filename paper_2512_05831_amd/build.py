@@ -18,7 +18,7 @@ ARCH = "gfx950"
 
 # Packed fp32 instructions are disabled for all device code.
 HIPCC_FLAGS = [
-    f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-shared",
+    f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
 ]
 
@@ -31,15 +31,31 @@ def hipcc() -> str:
 
 
 def build_library(verbose: bool = False) -> str:
-    """Compile libeb.so (always recompiles) and return its path."""
-    tmp = LIB + ".tmp"
-    cmd = [hipcc(), *HIPCC_FLAGS, *SRCS, "-o", tmp]
-    res = subprocess.run(cmd, capture_output=True, text=True)
-    if res.returncode != 0:
-        raise RuntimeError(f"hipcc failed ({res.returncode}):\n{' '.join(cmd)}\n{res.stderr}")
-    if verbose and res.stderr:
-        sys.stderr.write(res.stderr)
-    os.replace(tmp, LIB)
+    """Compile libeb.so (always recompiles) and return its path.  The sources
+    are compiled to objects in parallel, then linked."""
+    import tempfile
+
+    with tempfile.TemporaryDirectory(prefix="ebbuild") as tmpdir:
+        procs = []
+        for src in SRCS:
+            obj = os.path.join(tmpdir, os.path.basename(src) + ".o")
+            cmd = [hipcc(), *HIPCC_FLAGS, "-c", src, "-o", obj]
+            procs.append((cmd, obj, subprocess.Popen(cmd, stdout=subprocess.PIPE,
+                                                     stderr=subprocess.PIPE, text=True)))
+        objs = []
+        for cmd, obj, proc in procs:
+            _, err = proc.communicate()
+            if proc.returncode != 0:
+                raise RuntimeError(f"hipcc failed ({proc.returncode}):\n{' '.join(cmd)}\n{err}")
+            if verbose and err:
+                sys.stderr.write(err)
+            objs.append(obj)
+        tmp = LIB + ".tmp"
+        cmd = [hipcc(), *HIPCC_FLAGS, "-shared", *objs, "-o", tmp]
+        res = subprocess.run(cmd, capture_output=True, text=True)
+        if res.returncode != 0:
+            raise RuntimeError(f"hipcc link failed ({res.returncode}):\n{' '.join(cmd)}\n{res.stderr}")
+        os.replace(tmp, LIB)
     return LIB
 
 

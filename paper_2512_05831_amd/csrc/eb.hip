@@ -42,6 +42,7 @@
 #include <limits>
 #include <new>
 #include <string>
+#include <utility>
 #include <vector>
 
 #include "../../include/eb.h"
@@ -66,9 +67,10 @@ constexpr uint64_t kMaxLocalRows = 0xFFFFFFFEull; // local rows must fit below t
 struct GatherArgs {
     const char *base[kMaxTablesPerLaunch]; // stored table (local row 0 = global row shard_lo)
     uint64_t nlocal[kMaxTablesPerLaunch];  // gatherable local rows of each table
-    const int64_t *indices;
-    const int64_t *offsets; // bag (t, b) of this launch at offsets[t*B + b]
-    float *out;             // element (b, t, c) at out[b*ldo + t*D + c]
+    int64_t col[kMaxTablesPerLaunch];      // output column of each table's first element
+    const void *indices;    // int64 or int32 (the kernel's index type)
+    const void *offsets;    // bag (t, b) of this launch at offsets[t*B + b]
+    float *out;             // element (b, t, c) at out[b*ldo + col[t] + c]
     int32_t *hits;          // hits[b*ldh + t], or null
     int64_t nnz;
     int64_t B;
@@ -204,7 +206,7 @@ __device__ __forceinline__ void clamp_bag(int64_t &s, int64_t &e, int64_t nnz)
 
 // ---------------------------------------------------------------------------- team gather kernel
 
-template <int DT, int R, int P, int C, int U, bool kStream>
+template <typename IT, int DT, int R, int P, int C, int U, bool kStream>
 __global__ __launch_bounds__(kBlock) void eb_gather_team(const GatherArgs a)
 {
     constexpr int kTeam = R * P;
@@ -234,7 +236,7 @@ __global__ __launch_bounds__(kBlock) void eb_gather_team(const GatherArgs a)
 
     int64_t s = 0, e = 0;
     if (bag_ok) {
-        const int64_t *o = a.offsets + (int64_t)t * a.B + b;
+        const IT *o = (const IT *)a.offsets + (int64_t)t * a.B + b;
         s = __builtin_nontemporal_load(o);
         e = __builtin_nontemporal_load(o + 1);
         clamp_bag(s, e, a.nnz);
@@ -259,11 +261,11 @@ __global__ __launch_bounds__(kBlock) void eb_gather_team(const GatherArgs a)
 
     for (int64_t w0 = s; w0 < e; w0 += kStage) {
         const int n = (int)((e - w0) < kStage ? (e - w0) : kStage);
-        // Stage: coalesced int64 index loads, all issued before the first is
+        // Stage: coalesced index loads, all issued before the first is
         // used (positions past the window re-read its last entry), then
         // rewritten as 32-bit local rows or the marker.
         constexpr int kQ = kStage / kTeam;
-        const int64_t *src = a.indices + w0;
+        const IT *src = (const IT *)a.indices + w0;
         int64_t iv[kQ];
 #pragma unroll
         for (int q = 0; q < kQ; ++q) {
@@ -331,7 +333,7 @@ __global__ __launch_bounds__(kBlock) void eb_gather_team(const GatherArgs a)
 #pragma unroll
             for (int j = 0; j < C * kEpc; ++j) acc[j] = L > 0 ? acc[j] / fl : 0.f;
         }
-        float *o = a.out + b * a.ldo + (int64_t)t * a.D;
+        float *o = a.out + b * a.ldo + a.col[t];
 #pragma unroll
         for (int c = 0; c < C; ++c) {
             if (c * R + rl >= a.chunks) break;
@@ -348,7 +350,7 @@ __global__ __launch_bounds__(kBlock) void eb_gather_team(const GatherArgs a)
 // ---------------------------------------------------------------------------- plain kernel
 
 // One wave per bag, lanes striding over the columns; any D, any alignment.
-template <int DT>
+template <typename IT, int DT>
 __global__ __launch_bounds__(kBlock) void eb_gather_plain(const GatherArgs a)
 {
     constexpr int kEs = DT == EB_F32 ? 4 : 2;
@@ -363,7 +365,7 @@ __global__ __launch_bounds__(kBlock) void eb_gather_plain(const GatherArgs a)
 
     int64_t s, e;
     {
-        const int64_t *o = a.offsets + (int64_t)t * a.B + b;
+        const IT *o = (const IT *)a.offsets + (int64_t)t * a.B + b;
         s = o[0];
         e = o[1];
         clamp_bag(s, e, a.nnz);
@@ -373,7 +375,7 @@ __global__ __launch_bounds__(kBlock) void eb_gather_plain(const GatherArgs a)
     const uint64_t shard_lo = (uint64_t)a.shard_lo;
     const int D = a.D;
     const size_t pitch = (size_t)D * kEs;
-    float *o = a.out + b * a.ldo + (int64_t)t * D;
+    float *o = a.out + b * a.ldo + a.col[t];
     int count = 0;
 
     for (int c0 = 0; c0 < D; c0 += kWave * kCols) {
@@ -381,7 +383,7 @@ __global__ __launch_bounds__(kBlock) void eb_gather_plain(const GatherArgs a)
 #pragma unroll
         for (int j = 0; j < kCols; ++j) acc[j] = 0.f;
         for (int64_t k = s; k < e; ++k) {
-            const uint64_t r = (uint64_t)a.indices[k] - shard_lo;
+            const uint64_t r = (uint64_t)(int64_t)((const IT *)a.indices)[k] - shard_lo;
             if (r >= nlocal) continue;
             if (c0 == 0) ++count;
             const char *p = base + r * pitch;
@@ -453,53 +455,64 @@ using KernelFn = void (*)(GatherArgs);
 // profit from deeper overlap while hits return early.  A small batch (fewer
 // bags than fill the GPU) is bound by each bag's chain of dependent loads
 // instead: every bag then gets a whole wave and 6 rows in flight per lane.
-template <int DT, int R, int C, bool kFew>
+template <typename IT, int DT, int R, int C, bool kFew>
 KernelFn team_kernel(bool stream)
 {
     constexpr int P = (kFew || R >= 16) ? kWave / R : 16 / R;
     constexpr int U_CACHED = C >= 6 ? 1 : 6 / C;
     constexpr int U_STREAM = (!kFew && R * C >= 8) ? (C >= 2 ? 1 : 2) : U_CACHED;
-    return stream ? eb_gather_team<DT, R, P, C, U_STREAM, true>
-                  : eb_gather_team<DT, R, P, C, U_CACHED, false>;
+    return stream ? eb_gather_team<IT, DT, R, P, C, U_STREAM, true>
+                  : eb_gather_team<IT, DT, R, P, C, U_CACHED, false>;
 }
 
-template <int DT, int R, int C>
+template <typename IT, int DT, int R, int C>
 KernelFn team_kernel(bool stream, bool few)
 {
-    return few ? team_kernel<DT, R, C, true>(stream) : team_kernel<DT, R, C, false>(stream);
+    return few ? team_kernel<IT, DT, R, C, true>(stream) : team_kernel<IT, DT, R, C, false>(stream);
 }
 
-template <int DT>
+template <typename IT, int DT>
 KernelFn pick_team_kernel(int R, int C, bool stream, bool few)
 {
     switch (R) {
-    case 1: return team_kernel<DT, 1, 1>(stream, few);
-    case 2: return team_kernel<DT, 2, 1>(stream, few);
-    case 4: return team_kernel<DT, 4, 1>(stream, few);
-    case 8: return team_kernel<DT, 8, 1>(stream, few);
-    case 16: return team_kernel<DT, 16, 1>(stream, few);
-    case 32: return team_kernel<DT, 32, 1>(stream, few);
+    case 1: return team_kernel<IT, DT, 1, 1>(stream, few);
+    case 2: return team_kernel<IT, DT, 2, 1>(stream, few);
+    case 4: return team_kernel<IT, DT, 4, 1>(stream, few);
+    case 8: return team_kernel<IT, DT, 8, 1>(stream, few);
+    case 16: return team_kernel<IT, DT, 16, 1>(stream, few);
+    case 32: return team_kernel<IT, DT, 32, 1>(stream, few);
     default:
         switch (C) {
-        case 1: return team_kernel<DT, 64, 1>(stream, few);
-        case 2: return team_kernel<DT, 64, 2>(stream, few);
-        case 3: return team_kernel<DT, 64, 3>(stream, few);
-        case 4: return team_kernel<DT, 64, 4>(stream, few);
-        case 5: return team_kernel<DT, 64, 5>(stream, few);
-        case 6: return team_kernel<DT, 64, 6>(stream, few);
-        case 7: return team_kernel<DT, 64, 7>(stream, few);
-        case 8: return team_kernel<DT, 64, 8>(stream, few);
+        case 1: return team_kernel<IT, DT, 64, 1>(stream, few);
+        case 2: return team_kernel<IT, DT, 64, 2>(stream, few);
+        case 3: return team_kernel<IT, DT, 64, 3>(stream, few);
+        case 4: return team_kernel<IT, DT, 64, 4>(stream, few);
+        case 5: return team_kernel<IT, DT, 64, 5>(stream, few);
+        case 6: return team_kernel<IT, DT, 64, 6>(stream, few);
+        case 7: return team_kernel<IT, DT, 64, 7>(stream, few);
+        case 8: return team_kernel<IT, DT, 64, 8>(stream, few);
         }
     }
     return nullptr;
 }
 
+template <typename IT>
+KernelFn pick_team_kernel(int dtype, int R, int C, bool stream, bool few)
+{
+    switch (dtype) {
+    case EB_F32: return pick_team_kernel<IT, EB_F32>(R, C, stream, few);
+    case EB_F16: return pick_team_kernel<IT, EB_F16>(R, C, stream, few);
+    default: return pick_team_kernel<IT, EB_BF16>(R, C, stream, few);
+    }
+}
+
+template <typename IT>
 KernelFn pick_plain_kernel(int dtype)
 {
     switch (dtype) {
-    case EB_F32: return eb_gather_plain<EB_F32>;
-    case EB_F16: return eb_gather_plain<EB_F16>;
-    default: return eb_gather_plain<EB_BF16>;
+    case EB_F32: return eb_gather_plain<IT, EB_F32>;
+    case EB_F16: return eb_gather_plain<IT, EB_F16>;
+    default: return eb_gather_plain<IT, EB_BF16>;
     }
 }
 
@@ -521,6 +534,142 @@ struct eb_tables {
     std::vector<const char *> ptrs;
     std::vector<int64_t> stored_rows;
 };
+
+namespace {
+
+// Both forward entry points.  out_cols == nullptr means table t at column t*D.
+int forward_impl(const char *who, const eb_tables *h, int32_t T, const int64_t *rows, int32_t D,
+                 int32_t dtype, int32_t index_type, const void *indices, int64_t nnz, const void *offsets,
+                 int64_t B, int32_t mode, int64_t shard_lo, int64_t shard_hi, float *out, int64_t ldo,
+                 const int64_t *out_cols, int32_t *hits, int64_t ldh, void *stream)
+{
+    const std::string fn_name(who);
+    auto invalid = [&](const std::string &msg) { return fail(EB_ERR_INVALID, fn_name + ": " + msg); };
+    if (!h) return invalid("NULL handle");
+    if (T < 0 || T > h->T) return invalid("T out of range for the handle");
+    if (D != h->D) return invalid("D differs from the handle's");
+    if (dtype != h->dtype) return invalid("dtype differs from the handle's");
+    if (index_type != EB_IDX_I64 && index_type != EB_IDX_I32) return invalid("unknown index_type");
+    const int32_t pool = mode & 0xFF;
+    if ((pool != EB_SUM && pool != EB_MEAN) || (mode & ~(0xFF | EB_HINT_STREAM_ROWS)) != 0)
+        return invalid("unknown mode or hint bits");
+    if (nnz < 0 || B < 0) return invalid("negative nnz or B");
+    if (shard_lo < 0 || shard_hi < shard_lo) return invalid("bad shard range");
+    if (T > 0 && !rows) return invalid("NULL rows");
+    if (T == 0 || B == 0) return EB_OK;
+    if (!offsets || !out) return invalid("NULL offsets or out");
+    if (nnz > 0 && !indices) return invalid("NULL indices with nnz > 0");
+    const int64_t kMax = std::numeric_limits<int64_t>::max();
+    if (B > kMax / T || B * T > kMax / D) return invalid("B*T*D overflows");
+
+    // Output layout: every table's D columns inside [0, ldo), no two tables
+    // sharing a column, B rows of ldo floats addressable.
+    std::vector<int64_t> cols(T);
+    for (int32_t t = 0; t < T; ++t) cols[t] = out_cols ? out_cols[t] : (int64_t)t * D;
+    if (ldo < 1 || B > kMax / ldo) return invalid("bad ldo (must be >= 1 with B*ldo in int64)");
+    {
+        std::vector<std::pair<int64_t, int64_t>> spans(T);
+        for (int32_t t = 0; t < T; ++t) {
+            if (cols[t] < 0 || cols[t] > ldo - D)
+                return invalid("output columns of table " + std::to_string(t) + " leave [0, ldo)");
+            spans[t] = {cols[t], cols[t] + D};
+        }
+        std::sort(spans.begin(), spans.end());
+        for (int32_t t = 1; t < T; ++t)
+            if (spans[t].first < spans[t - 1].second) return invalid("two tables share output columns");
+    }
+    if (hits && (ldh < T || B > kMax / ldh)) return invalid("bad ldh (must be >= T with B*ldh in int64)");
+
+    std::vector<uint64_t> nlocal(T);
+    for (int32_t t = 0; t < T; ++t) {
+        if (rows[t] < 0) return invalid("negative rows[t]");
+        const int64_t hi = std::min(shard_hi, rows[t]);
+        const int64_t n = hi > shard_lo ? hi - shard_lo : 0;
+        if (n > h->stored_rows[t])
+            return invalid("stored rows of table " + std::to_string(t) +
+                           " do not cover [shard_lo, min(shard_hi, rows[t]))");
+        if ((uint64_t)n > kMaxLocalRows)
+            return fail(EB_ERR_UNSUPPORTED, fn_name + ": more than 4294967294 gatherable rows in a table");
+        nlocal[t] = (uint64_t)n;
+    }
+
+    const int64_t rb = (int64_t)D * elem_bytes(dtype);
+    // 16-byte stores need every (bag, table) output row start 16-byte aligned.
+    bool out_aligned = ((uintptr_t)out) % 16 == 0 && ldo % 4 == 0;
+    for (int32_t t = 0; t < T; ++t) out_aligned = out_aligned && cols[t] % 4 == 0;
+    const bool team_path = rb % 16 == 0 && rb <= 8192 && h->aligned16 && out_aligned;
+    const bool i32 = index_type == EB_IDX_I32;
+    KernelFn fn = nullptr;
+    int bags_per_block = kWavesPerBlock;
+    bool xcd_remap = false;
+    if (team_path) {
+        // Non-temporal loads lose for rows narrower than 128 bytes.
+        const bool stream = (mode & EB_HINT_STREAM_ROWS) && rb >= 128;
+        const Shape normal = team_shape((int)rb, false);
+        const int64_t bags = (int64_t)T * B;
+        const int64_t waves = bags / (kWave / (normal.R * normal.P));
+        const bool few = waves < kWaveSlots && bags <= kFewBagsMax &&
+                         nnz > 2 * (int64_t)rows_in_flight_per_bag(normal, stream) * bags;
+        const Shape sh = team_shape((int)rb, few);
+        fn = i32 ? pick_team_kernel<int32_t>(dtype, sh.R, sh.C, stream, few)
+                 : pick_team_kernel<int64_t>(dtype, sh.R, sh.C, stream, few);
+        bags_per_block = (kWave / (sh.R * sh.P)) * kWavesPerBlock;
+        // No reuse: each XCD takes a contiguous run of bags.  Otherwise
+        // hardware order, so all XCDs work on the same table at once and its
+        // hot rows share the last-level cache.
+        xcd_remap = (mode & EB_HINT_STREAM_ROWS) != 0;
+    } else {
+        fn = i32 ? pick_plain_kernel<int32_t>(dtype) : pick_plain_kernel<int64_t>(dtype);
+    }
+    if (!fn) return fail(EB_ERR_UNSUPPORTED, fn_name + ": no kernel for this row shape");
+
+    // Launch in pieces of at most 64 tables and a bounded grid.
+    const int64_t kMaxBlocks = (int64_t)1 << 22;
+    const size_t ies = i32 ? 4 : 8;
+    GatherArgs a;
+    std::memset(&a, 0, sizeof a);
+    a.indices = indices;
+    a.nnz = nnz;
+    a.B = B;
+    a.shard_lo = shard_lo;
+    a.out = out;
+    a.ldo = ldo;
+    a.ldh = ldh;
+    a.D = D;
+    a.row_bytes = team_path ? (int32_t)rb : 0;
+    a.chunks = team_path ? (int32_t)(rb / 16) : 0;
+    a.mean = pool == EB_MEAN;
+    a.xcd_runs = xcd_remap ? 1 : 0;
+    hipStream_t st = (hipStream_t)stream;
+
+    const int64_t blocks_all_bags = (B + bags_per_block - 1) / bags_per_block;
+    for (int32_t t0 = 0; t0 < T; t0 += kMaxTablesPerLaunch) {
+        const int32_t nt = std::min<int32_t>(kMaxTablesPerLaunch, T - t0);
+        for (int32_t j = 0; j < nt; ++j) {
+            a.base[j] = h->ptrs[t0 + j];
+            a.nlocal[j] = nlocal[t0 + j];
+            a.col[j] = cols[t0 + j];
+        }
+        a.offsets = (const char *)offsets + (size_t)t0 * B * ies;
+        a.hits = hits ? hits + t0 : nullptr;
+        // Bag ranges per launch keep nt * blocks_per_table within the grid bound.
+        const int64_t bpt_max = std::max<int64_t>(1, kMaxBlocks / nt);
+        for (int64_t blk0 = 0; blk0 < blocks_all_bags; blk0 += bpt_max) {
+            const int64_t bpt = std::min(bpt_max, blocks_all_bags - blk0);
+            a.bag_begin = blk0 * bags_per_block;
+            a.blocks_per_table = (int32_t)bpt;
+            a.nblocks = (int32_t)(bpt * nt);
+            const int64_t grid = xcd_remap ? (a.nblocks + kXcds - 1) / kXcds * kXcds : a.nblocks;
+            void *args[] = {&a};
+            hipError_t err = hipLaunchKernel((const void *)fn, dim3((unsigned)grid), dim3(kBlock), args, 0, st);
+            if (err != hipSuccess)
+                return fail(EB_ERR_HIP, fn_name + ": kernel launch failed: " + hipGetErrorString(err));
+        }
+    }
+    return EB_OK;
+}
+
+} // namespace
 
 extern "C" {
 
@@ -566,106 +715,18 @@ int eb_forward(const eb_tables *h, int32_t T, const int64_t *rows, int32_t D, in
                const int64_t *indices, int64_t nnz, const int64_t *offsets, int64_t B, int32_t mode,
                int64_t shard_lo, int64_t shard_hi, float *out, int32_t *hits, void *stream)
 {
-    if (!h) return fail(EB_ERR_INVALID, "eb_forward: NULL handle");
-    if (T < 0 || T > h->T) return fail(EB_ERR_INVALID, "eb_forward: T out of range for the handle");
-    if (D != h->D) return fail(EB_ERR_INVALID, "eb_forward: D differs from the handle's");
-    if (dtype != h->dtype) return fail(EB_ERR_INVALID, "eb_forward: dtype differs from the handle's");
-    const int32_t pool = mode & 0xFF;
-    if ((pool != EB_SUM && pool != EB_MEAN) || (mode & ~(0xFF | EB_HINT_STREAM_ROWS)) != 0)
-        return fail(EB_ERR_INVALID, "eb_forward: unknown mode or hint bits");
-    if (nnz < 0 || B < 0) return fail(EB_ERR_INVALID, "eb_forward: negative nnz or B");
-    if (shard_lo < 0 || shard_hi < shard_lo) return fail(EB_ERR_INVALID, "eb_forward: bad shard range");
-    if (T > 0 && !rows) return fail(EB_ERR_INVALID, "eb_forward: NULL rows");
-    if (T == 0 || B == 0) return EB_OK;
-    if (!offsets || !out) return fail(EB_ERR_INVALID, "eb_forward: NULL offsets or out");
-    if (nnz > 0 && !indices) return fail(EB_ERR_INVALID, "eb_forward: NULL indices with nnz > 0");
-    const int64_t kMax = std::numeric_limits<int64_t>::max();
-    if (B > kMax / T || B * T > kMax / D) return fail(EB_ERR_INVALID, "eb_forward: B*T*D overflows");
+    const int64_t ldo = (T > 0 && D > 0) ? (int64_t)T * D : 0; // overflow is caught below
+    return forward_impl("eb_forward", h, T, rows, D, dtype, EB_IDX_I64, indices, nnz, offsets, B, mode,
+                        shard_lo, shard_hi, out, ldo, nullptr, hits, T, stream);
+}
 
-    std::vector<uint64_t> nlocal(T);
-    for (int32_t t = 0; t < T; ++t) {
-        if (rows[t] < 0) return fail(EB_ERR_INVALID, "eb_forward: negative rows[t]");
-        const int64_t hi = std::min(shard_hi, rows[t]);
-        const int64_t n = hi > shard_lo ? hi - shard_lo : 0;
-        if (n > h->stored_rows[t])
-            return fail(EB_ERR_INVALID, "eb_forward: stored rows of table " + std::to_string(t) +
-                                            " do not cover [shard_lo, min(shard_hi, rows[t]))");
-        if ((uint64_t)n > kMaxLocalRows)
-            return fail(EB_ERR_UNSUPPORTED, "eb_forward: more than 4294967294 gatherable rows in a table");
-        nlocal[t] = (uint64_t)n;
-    }
-
-    const int64_t rb = (int64_t)D * elem_bytes(dtype);
-    const bool team_path = rb % 16 == 0 && rb <= 8192 && h->aligned16 && ((uintptr_t)out) % 16 == 0;
-    KernelFn fn = nullptr;
-    int bags_per_block = kWavesPerBlock;
-    bool xcd_remap = false;
-    if (team_path) {
-        // Non-temporal loads lose for rows narrower than 128 bytes.
-        const bool stream = (mode & EB_HINT_STREAM_ROWS) && rb >= 128;
-        const Shape normal = team_shape((int)rb, false);
-        const int64_t bags = (int64_t)T * B;
-        const int64_t waves = bags / (kWave / (normal.R * normal.P));
-        const bool few = waves < kWaveSlots && bags <= kFewBagsMax &&
-                         nnz > 2 * (int64_t)rows_in_flight_per_bag(normal, stream) * bags;
-        const Shape sh = team_shape((int)rb, few);
-        switch (dtype) {
-        case EB_F32: fn = pick_team_kernel<EB_F32>(sh.R, sh.C, stream, few); break;
-        case EB_F16: fn = pick_team_kernel<EB_F16>(sh.R, sh.C, stream, few); break;
-        default: fn = pick_team_kernel<EB_BF16>(sh.R, sh.C, stream, few); break;
-        }
-        bags_per_block = (kWave / (sh.R * sh.P)) * kWavesPerBlock;
-        // No reuse: each XCD takes a contiguous run of bags.  Otherwise
-        // hardware order, so all XCDs work on the same table at once and its
-        // hot rows share the last-level cache.
-        xcd_remap = (mode & EB_HINT_STREAM_ROWS) != 0;
-    } else {
-        fn = pick_plain_kernel(dtype);
-    }
-    if (!fn) return fail(EB_ERR_UNSUPPORTED, "eb_forward: no kernel for this row shape");
-
-    // Launch in pieces of at most 64 tables and a bounded grid.
-    const int64_t kMaxBlocks = (int64_t)1 << 22;
-    GatherArgs a;
-    std::memset(&a, 0, sizeof a);
-    a.indices = indices;
-    a.nnz = nnz;
-    a.B = B;
-    a.shard_lo = shard_lo;
-    a.ldo = (int64_t)T * D;
-    a.ldh = T;
-    a.D = D;
-    a.row_bytes = team_path ? (int32_t)rb : 0;
-    a.chunks = team_path ? (int32_t)(rb / 16) : 0;
-    a.mean = pool == EB_MEAN;
-    a.xcd_runs = xcd_remap ? 1 : 0;
-    hipStream_t st = (hipStream_t)stream;
-
-    const int64_t blocks_all_bags = (B + bags_per_block - 1) / bags_per_block;
-    for (int32_t t0 = 0; t0 < T; t0 += kMaxTablesPerLaunch) {
-        const int32_t nt = std::min<int32_t>(kMaxTablesPerLaunch, T - t0);
-        for (int32_t j = 0; j < nt; ++j) {
-            a.base[j] = h->ptrs[t0 + j];
-            a.nlocal[j] = nlocal[t0 + j];
-        }
-        a.offsets = offsets + (int64_t)t0 * B;
-        a.out = out + (int64_t)t0 * D;
-        a.hits = hits ? hits + t0 : nullptr;
-        // Bag ranges per launch keep nt * blocks_per_table within the grid bound.
-        const int64_t bpt_max = std::max<int64_t>(1, kMaxBlocks / nt);
-        for (int64_t blk0 = 0; blk0 < blocks_all_bags; blk0 += bpt_max) {
-            const int64_t bpt = std::min(bpt_max, blocks_all_bags - blk0);
-            a.bag_begin = blk0 * bags_per_block;
-            a.blocks_per_table = (int32_t)bpt;
-            a.nblocks = (int32_t)(bpt * nt);
-            const int64_t grid = xcd_remap ? (a.nblocks + kXcds - 1) / kXcds * kXcds : a.nblocks;
-            void *args[] = {&a};
-            hipError_t err = hipLaunchKernel((const void *)fn, dim3((unsigned)grid), dim3(kBlock), args, 0, st);
-            if (err != hipSuccess)
-                return fail(EB_ERR_HIP, std::string("eb_forward: kernel launch failed: ") + hipGetErrorString(err));
-        }
-    }
-    return EB_OK;
+int eb_forward_ex(const eb_tables *h, int32_t T, const int64_t *rows, int32_t D, int32_t dtype,
+                  int32_t index_type, const void *indices, int64_t nnz, const void *offsets, int64_t B,
+                  int32_t mode, int64_t shard_lo, int64_t shard_hi, float *out, int64_t ldo,
+                  const int64_t *out_cols, int32_t *hits, int64_t ldh, void *stream)
+{
+    return forward_impl("eb_forward_ex", h, T, rows, D, dtype, index_type, indices, nnz, offsets, B, mode,
+                        shard_lo, shard_hi, out, ldo, out_cols, hits, ldh, stream);
 }
 
 } // extern "C"

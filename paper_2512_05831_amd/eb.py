@@ -18,6 +18,7 @@ from . import build as _build
 EB_F32, EB_F16, EB_BF16 = 0, 1, 2
 EB_SUM, EB_MEAN = 0, 1
 EB_HINT_STREAM_ROWS = 0x100
+EB_IDX_I64, EB_IDX_I32 = 0, 1
 EB_OK, EB_ERR_INVALID, EB_ERR_UNSUPPORTED, EB_ERR_HIP, EB_ERR_NOMEM = 0, -1, -2, -3, -4
 INT64_MAX = (1 << 63) - 1
 
@@ -45,6 +46,9 @@ def library() -> ctypes.CDLL:
         lib.eb_create_tables.restype = ctypes.c_int
         lib.eb_forward.argtypes = [p, i32, p, i32, i32, p, i64, p, i64, i32, i64, i64, p, p, p]
         lib.eb_forward.restype = ctypes.c_int
+        lib.eb_forward_ex.argtypes = [p, i32, p, i32, i32, i32, p, i64, p, i64, i32, i64, i64, p,
+                                      i64, p, p, i64, p]
+        lib.eb_forward_ex.restype = ctypes.c_int
         lib.eb_destroy.argtypes = [p]
         lib.eb_destroy.restype = None
         lib.eb_last_error.argtypes = []
@@ -92,6 +96,18 @@ def eb_forward(handle, T: int, rows, D: int, dtype: int, indices_ptr: int, nnz: 
     _check(library().eb_forward(handle, T, _i64_array(rows), D, dtype, indices_ptr, nnz,
                                 offsets_ptr, B, mode, shard_lo, shard_hi, out_ptr,
                                 hits_ptr or None, stream_ptr or None))
+
+
+def eb_forward_ex(handle, T: int, rows, D: int, dtype: int, index_type: int, indices_ptr: int,
+                  nnz: int, offsets_ptr: int, B: int, mode: int, shard_lo: int, shard_hi: int,
+                  out_ptr: int, ldo: int, out_cols, hits_ptr: int | None, ldh: int,
+                  stream_ptr: int | None) -> None:
+    """eb_forward with an index width and an output layout (``out_cols``: a
+    list of T columns, or None for t*D).  Raises EbError."""
+    cols = None if out_cols is None else _i64_array(out_cols)
+    _check(library().eb_forward_ex(handle, T, _i64_array(rows), D, dtype, index_type, indices_ptr,
+                                   nnz, offsets_ptr, B, mode, shard_lo, shard_hi, out_ptr, ldo,
+                                   cols, hits_ptr or None, ldh, stream_ptr or None))
 
 
 def eb_destroy(handle) -> None:
@@ -169,6 +185,18 @@ def sum_partials(partials, B: int, T: int, D: int, mean_offsets=None, nnz: int =
     return out
 
 
+def _index_type(indices, offsets) -> int:
+    """EB_IDX_I64 / EB_IDX_I32 from two contiguous tensors of one integer type."""
+    import torch
+
+    codes = {torch.int64: EB_IDX_I64, torch.int32: EB_IDX_I32}
+    if indices.dtype not in codes or offsets.dtype != indices.dtype:
+        raise ValueError("indices and offsets must both be int64 or both int32")
+    if not (indices.is_contiguous() and offsets.is_contiguous()):
+        raise ValueError("indices / offsets must be contiguous")
+    return codes[indices.dtype]
+
+
 _TORCH_DTYPE_CODES = {"torch.float32": EB_F32, "torch.float16": EB_F16, "torch.bfloat16": EB_BF16}
 
 
@@ -224,6 +252,42 @@ class EmbeddingBagTables:
                    out.data_ptr(), hits.data_ptr() if want_hits else None, stream.cuda_stream)
         return (out, hits) if want_hits else out
 
+    def forward_ex(self, indices, offsets, B: int, mode: int = EB_SUM, out=None, out_cols=None,
+                   hits=None, stream=None):
+        """eb_forward_ex.  indices / offsets: contiguous device int64 or int32
+        (the same for both).  ``out``: fp32 [B, W] with unit column stride (a
+        view such as a column slice is fine; ldo = out.stride(0)); table t goes
+        to columns [out_cols[t], out_cols[t] + D) of it (default t*D).
+        ``hits``: int32 [B, >= T] with unit column stride, or None."""
+        import torch
+
+        dev = self.tables[0].device
+        itype = _index_type(indices, offsets)
+        if out is None:
+            out = torch.empty((B, self.T * self.D), dtype=torch.float32, device=dev)
+        if out.dtype != torch.float32 or out.dim() != 2 or out.shape[0] != B or \
+                (B > 1 and out.stride(1) != 1):
+            raise ValueError("out must be fp32 [B, W] with unit column stride")
+        if hits is not None and (hits.dtype != torch.int32 or hits.dim() != 2 or
+                                 hits.shape[0] != B or (B > 1 and hits.stride(1) != 1)):
+            raise ValueError("hits must be int32 [B, >= T] with unit column stride")
+        if offsets.numel() != self.T * B + 1:
+            raise ValueError("offsets must have T*B+1 entries")
+        cols = [t * self.D for t in range(self.T)] if out_cols is None else list(out_cols)
+        if len(cols) != self.T or any(c < 0 or c + self.D > out.shape[1] for c in cols):
+            raise ValueError("out_cols must give T columns with c + D <= out.shape[1]")
+        if hits is not None and hits.shape[1] < self.T:
+            raise ValueError("hits must be int32 [B, >= T]")
+        if stream is None:
+            stream = torch.cuda.current_stream(dev)
+        ldo = out.stride(0) if B > 1 else out.shape[1]
+        ldh = (hits.stride(0) if B > 1 else hits.shape[1]) if hits is not None else 0
+        eb_forward_ex(self.handle, self.T, self.rows, self.D, self.dtype, itype, indices.data_ptr(),
+                      indices.numel(), offsets.data_ptr(), B, mode, self.shard_lo, self.shard_hi,
+                      out.data_ptr(), ldo, cols,
+                      hits.data_ptr() if hits is not None else None, ldh, stream.cuda_stream)
+        return (out, hits) if hits is not None else out
+
     def prepare(self, indices, offsets, B: int, mode: int, out, hits=None, stream=None):
         """Marshal the arguments of one eb_forward call once; the returned
         function enqueues that call (on ``stream``) each time it is invoked."""
@@ -234,14 +298,23 @@ class EmbeddingBagTables:
         if offsets.numel() != self.T * B + 1 or out.numel() < B * self.T * self.D:
             raise ValueError("offsets / out do not match T, B, D")
         lib = library()
-        args = (self.handle, self.T, _i64_array(self.rows), self.D, self.dtype,
-                indices.data_ptr(), indices.numel(), offsets.data_ptr(), B, mode, self.shard_lo,
-                self.shard_hi, out.data_ptr(), hits.data_ptr() if hits is not None else None,
-                stream.cuda_stream)
+        itype = _index_type(indices, offsets)
+        hits_ptr = hits.data_ptr() if hits is not None else None
+        if itype == EB_IDX_I64:
+            fn = lib.eb_forward
+            args = (self.handle, self.T, _i64_array(self.rows), self.D, self.dtype,
+                    indices.data_ptr(), indices.numel(), offsets.data_ptr(), B, mode, self.shard_lo,
+                    self.shard_hi, out.data_ptr(), hits_ptr, stream.cuda_stream)
+        else:
+            fn = lib.eb_forward_ex
+            args = (self.handle, self.T, _i64_array(self.rows), self.D, self.dtype, itype,
+                    indices.data_ptr(), indices.numel(), offsets.data_ptr(), B, mode, self.shard_lo,
+                    self.shard_hi, out.data_ptr(), self.T * self.D, None, hits_ptr, self.T,
+                    stream.cuda_stream)
         keep = (indices, offsets, out, hits)
 
         def call():
-            _check(lib.eb_forward(*args))
+            _check(fn(*args))
             return keep
 
         return call

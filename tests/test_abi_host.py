@@ -25,7 +25,8 @@ def declared_functions():
 
 def test_header_declares_the_boundary():
     assert declared_functions() == ["eb_bucketize", "eb_bucketize_workspace", "eb_create_tables",
-                                    "eb_destroy", "eb_forward", "eb_last_error", "eb_sum_partials"]
+                                    "eb_destroy", "eb_forward", "eb_forward_ex", "eb_last_error",
+                                    "eb_sum_partials"]
 
 
 def test_library_exports_every_declared_symbol():
@@ -130,6 +131,53 @@ def test_error_message_is_per_failure():
         assert "D" in eb.eb_last_error()
         code_of(lambda: forward(h, mode=9))
         assert "mode" in eb.eb_last_error()
+    finally:
+        eb.eb_destroy(h)
+
+
+def forward_ex(h, **kw):
+    args = dict(T=2, rows=[100, 100], D=16, dtype=eb.EB_F32, index_type=eb.EB_IDX_I32,
+                indices_ptr=FAKE, nnz=10, offsets_ptr=FAKE, B=4, mode=eb.EB_SUM, shard_lo=0,
+                shard_hi=I64MAX, out_ptr=FAKE, ldo=40, out_cols=[0, 20], hits_ptr=None, ldh=0,
+                stream_ptr=None)
+    args.update(kw)
+    return eb.eb_forward_ex(h, **args)
+
+
+@pytest.mark.parametrize("kw", [
+    dict(index_type=2), dict(index_type=-1),
+    dict(ldo=0), dict(ldo=-40),
+    dict(out_cols=[0, 25]),            # table 1 ends past ldo
+    dict(out_cols=[-4, 20]),
+    dict(out_cols=[0, 12]),            # tables overlap
+    dict(out_cols=[20, 8]),            # overlap, listed out of order
+    dict(ldo=31, out_cols=[0, 16]),    # 16 + 16 > 31
+    dict(hits_ptr=FAKE, ldh=1),        # ldh < T
+    dict(B=1 << 60, ldo=1 << 10),      # B * ldo overflows
+    dict(hits_ptr=FAKE, ldh=1 << 61, B=8),
+    dict(D=8), dict(mode=3), dict(shard_lo=5, shard_hi=4), dict(offsets_ptr=None),
+])
+def test_forward_ex_rejects(kw):
+    h = handle()
+    try:
+        assert code_of(lambda: forward_ex(h, **kw)) == eb.EB_ERR_INVALID
+        assert eb.eb_last_error().startswith("eb_forward_ex: ")
+    finally:
+        eb.eb_destroy(h)
+
+
+def test_forward_ex_noops_and_default_columns():
+    h = handle()
+    try:
+        forward_ex(h, B=0)
+        forward_ex(h, T=0, rows=[], out_cols=[])
+        forward_ex(h, B=0, index_type=eb.EB_IDX_I64, out_cols=None, ldo=32)
+        # default columns t*D need ldo >= T*D: rejected before any launch
+        assert code_of(lambda: forward_ex(h, out_cols=None, ldo=31)) == eb.EB_ERR_INVALID
+        # adjacent (touching) column ranges are not an overlap: only the
+        # launch itself could fail here, so stop at validation with B*ldo overflow
+        assert code_of(lambda: forward_ex(h, out_cols=[16, 0], ldo=1 << 62, B=8)) == eb.EB_ERR_INVALID
+        assert "ldo" in eb.eb_last_error()
     finally:
         eb.eb_destroy(h)
 
