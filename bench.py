@@ -88,24 +88,87 @@ def pick_workload(args):
     return w
 
 
+def host_cpu() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(w, host_tables, batches, off, budget_s: float):
+    """The oracle over whole batches for about budget_s seconds, with the
+    calling thread pinned to one core of those this process may use."""
     import oracle
 
-    lookups = 0
-    passes = 0
-    t0 = time.perf_counter()
-    while True:
-        idx = batches[passes % len(batches)]
-        oracle.forward(host_tables, [w.rows] * w.T, w.D, w.dtype, idx, off, w.B, w.modes[0],
-                       w.shard_lo, w.shard_hi)
-        lookups += idx.size
-        passes += 1
-        if time.perf_counter() - t0 >= budget_s:
-            break
-    dt = time.perf_counter() - t0
+    allowed = os.sched_getaffinity(0)
+    core = min(allowed)
+    os.sched_setaffinity(0, {core})
+    try:
+        lookups = 0
+        passes = 0
+        t0 = time.perf_counter()
+        while True:
+            idx = batches[passes % len(batches)]
+            oracle.forward(host_tables, [w.rows] * w.T, w.D, w.dtype, idx, off, w.B, w.modes[0],
+                           w.shard_lo, w.shard_hi)
+            lookups += idx.size
+            passes += 1
+            if time.perf_counter() - t0 >= budget_s:
+                break
+        dt = time.perf_counter() - t0
+    finally:
+        os.sched_setaffinity(0, allowed)
     return {"value": lookups / dt, "unit": "lookups/s", "cores": 1, "kind": "oracle",
             "sample": f"{passes} full batch(es) of this workload ({lookups} lookups), "
-                      f"single-threaded fp64 C loop, {dt:.1f} s"}
+                      f"single-threaded fp64 C loop pinned to core {core}, {dt:.1f} s",
+            "host": f"{host_cpu()}, {len(allowed)} hardware threads available"}
+
+
+def per_launch_us(torch, stream, fn_list, K, flush=None):
+    """Median / p10 / p90 of single launches, each bracketed by its own HIP
+    event pair on the launch stream; ``flush`` (if given) runs on the same
+    stream before every launch, outside the events."""
+    times = []
+    with torch.cuda.stream(stream):
+        for i in range(K):
+            if flush is not None:
+                flush(i)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            fn_list[i % len(fn_list)]()
+            e1.record(stream)
+            times.append((e0, e1))
+        torch.cuda.synchronize()
+    us = sorted(a.elapsed_time(b) * 1e3 for a, b in times)
+    pick = lambda q: us[min(len(us) - 1, int(q * len(us)))]
+    return {"median_us": pick(0.5), "p10_us": pick(0.1), "p90_us": pick(0.9), "launches": K}
+
+
+def torch_embedding_bag_step(torch, w, d_idx, d_off_all, dev_tables, mode):
+    """PyTorch's own GPU embedding_bag over the same batch (one call per table),
+    for context; its outputs are discarded."""
+    import torch.nn.functional as F
+
+    B = w.B
+    per_table = []
+    for t in range(w.T):
+        s0 = d_off_all[t * B]
+        per_table.append((t, d_off_all[t * B:(t + 1) * B] - s0, s0, d_off_all[(t + 1) * B]))
+    bounds = [(int(s), int(e)) for _, _, s, e in per_table]
+    offs = [o.contiguous() for _, o, _, _ in per_table]
+    tmode = "sum" if mode == wl.SUM else "mean"
+
+    def make(idx):
+        parts = [idx[s:e] for s, e in bounds]
+
+        def step():
+            for t in range(w.T):
+                F.embedding_bag(parts[t], dev_tables[t], offs[t], mode=tmode)
+        return step
+    return [make(i) for i in d_idx]
 
 
 def copy_calibration(torch, dev, nbytes: int, steps: int):
@@ -279,6 +342,10 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--rows-policy", default="auto", choices=["auto", "cached", "stream"])
+    ap.add_argument("--cold", action="store_true",
+                    help="also time single launches after writing a 512 MB buffer (caches flushed)")
+    ap.add_argument("--torch-baseline", action="store_true",
+                    help="also time torch.nn.functional.embedding_bag on the same batches (context)")
     ap.add_argument("--index-type", default="i64", choices=["i64", "i32"],
                     help="integer type of the ids and offsets handed to the library")
     ap.add_argument("--graph", action="store_true",
@@ -388,6 +455,40 @@ def main():
     log(f"bench: mean launch {launch_ms * 1e3:.1f} us over {K} back-to-back launches, "
         f"wall step {ms_per_step * 1e3:.1f} us, {achieved:.0f} GB/s algorithmic")
 
+    extra = {}
+    if args.cold:
+        scratch = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+        n = max(20, min(K, 200))
+        extra["single_launch_warm"] = per_launch_us(torch, stream, step_fns, n)
+        extra["single_launch_cold"] = per_launch_us(torch, stream, step_fns, n,
+                                                    flush=lambda i: scratch.fill_(i & 0xFF))
+        extra["single_launch_cold"]["flush"] = "512 MB written on the launch stream before each launch"
+        del scratch
+        log(f"bench: single launch warm {extra['single_launch_warm']['median_us']:.1f} us, "
+            f"cold {extra['single_launch_cold']['median_us']:.1f} us (medians)")
+    if args.torch_baseline:
+        if w.sharded:
+            log("bench: torch baseline skipped (a row shard has no torch equivalent)")
+        else:
+            tsteps = torch_embedding_bag_step(torch, w, d_idx, d_off, dev_tables, mode)
+            tk = max(10, K // 4)
+            with torch.cuda.stream(stream):
+                for i in range(3):
+                    tsteps[i % len(tsteps)]()
+                torch.cuda.synchronize()
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+                for i in range(tk):
+                    tsteps[i % len(tsteps)]()
+                e1.record(stream)
+                torch.cuda.synchronize()
+            tus = e0.elapsed_time(e1) * 1e3 / tk
+            extra["torch_embedding_bag"] = {
+                "us_per_step": tus, "lookups_per_s": (steps_lookups / K) / (tus / 1e6),
+                "calls_per_step": w.T, "steps": tk,
+                "note": "torch.nn.functional.embedding_bag, one call per table, same device tables and ids"}
+            log(f"bench: torch embedding_bag {tus:.1f} us per step")
+
     cpu = None
     if not args.no_cpu_baseline:
         log("bench: timing the CPU oracle")
@@ -427,6 +528,7 @@ def main():
                      "traffic": traffic},
         "cpu_baseline": cpu,
     }
+    line.update(extra)
     print(json.dumps(line), flush=True)
     et.close()
 
