@@ -17,12 +17,13 @@
 // Both are HBM-bound integer / streaming work; nothing here is a contraction.
 //
 // eb_bucketize runs three kernels on the caller's stream:
-//   1. count   : a wave takes 64 consecutive bags; each id's owner by binary
-//                search over the table's block bounds (staged in LDS); for
-//                ordinary CSR offsets the wave streams its whole id range in
-//                64-id chunks into a [bag][destination] histogram in LDS,
-//                else it walks the bags one at a time; counts land in
-//                out_offsets[g][p + 1] (coalesced per destination).
+//   1. count   : a wave takes 16 consecutive bags; each id's owner by
+//                comparison with the table's block bounds (up to 8 blocks) or
+//                by binary search over them (staged in LDS); for ordinary CSR
+//                offsets the wave streams its whole id range in 64-id chunks
+//                into a [bag][destination] histogram in LDS, else it walks the
+//                bags one at a time; counts land in out_offsets[g][p + 1]
+//                (coalesced per destination).
 //   2. scan    : inclusive scan of every destination's row of counts
 //                (reduce-then-scan over 2048-entry tiles: tile sums in the
 //                workspace, one workgroup scans them and writes segments).
@@ -31,7 +32,9 @@
 //                the bag with the same owner (ballots per distinct owner in
 //                each 64-id chunk), so the order is stable.  For ordinary CSR
 //                offsets one running slot per destination and wave suffices,
-//                since position order is then (bag, position) order.
+//                since position order is then (bag, position) order.  Every
+//                store is checked against nnz, so no bounds, offsets or ids
+//                can make it write outside out_indices.
 
 #include <hip/hip_runtime.h>
 
@@ -77,12 +80,51 @@ __device__ __forceinline__ int owner_of(const int64_t *bnd, int G, int64_t i)
     return lo;
 }
 
-// A wave takes 64 consecutive bags of one table; a block 4 waves.
-constexpr int kBagsPerWave = 64;
+// A table's bounds for at most 8 blocks, read once from LDS: the
+// outer pair and the inner bounds, unused inner bounds set past every id.
+constexpr int kFewShards = 8;
+
+struct FewBounds {
+    int64_t lo, hi;
+    int64_t inner[kFewShards - 1];
+};
+
+__device__ __forceinline__ FewBounds few_bounds(const int64_t *bnd, int G)
+{
+    FewBounds b;
+    b.lo = bnd[0];
+    b.hi = bnd[G];
+#pragma unroll
+    for (int j = 1; j < kFewShards; ++j) b.inner[j - 1] = j < G ? bnd[j] : INT64_MAX;
+    return b;
+}
+
+// owner_of for G <= 8 by comparisons: -1 outside [lo, hi), else the number of
+// inner bounds at or below i, which for non-decreasing bounds is the block
+// holding i.  Always -1 or in [0, G).
+__device__ __forceinline__ int few_owner(const FewBounds &b, int64_t i)
+{
+    if (i < b.lo || i >= b.hi) return -1;
+    int g = 0;
+#pragma unroll
+    for (int j = 0; j < kFewShards - 1; ++j) g += i >= b.inner[j] ? 1 : 0;
+    return g;
+}
+
+// Number of set bits of m in the lanes below this one.
+__device__ __forceinline__ int rank_below(uint64_t m)
+{
+    return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+}
+
+// A wave takes kBagsPerWave consecutive bags of one table; a block 4 waves.
+// Few bags per wave keep many waves (and their id loads) in flight.
+constexpr int kBagsPerWave = 16;
 constexpr int kBagsPerBlock = kBagsPerWave * kWavesPerBlock;
+static_assert(kBagsPerWave <= kWave && (kBagsPerWave & (kBagsPerWave - 1)) == 0, "bags per wave");
 constexpr int kFastShards = 32; // count's per-(bag, destination) histogram fits LDS up to here
 constexpr int kChunks = 4;      // 64-id chunks loaded ahead
-constexpr int kBallotShards = 8; // scatter ranks by one ballot per destination up to here
+constexpr int kBallotShards = kFewShards; // compare-based owners, one ballot per destination
 
 struct BucketArgs {
     const int64_t *bounds;   // [T][G+1]
@@ -99,7 +141,7 @@ struct BucketArgs {
 };
 
 // Dynamic LDS: the table's G+1 bounds, then one area per wave.
-__host__ __device__ inline size_t count_wave_bytes(int G) { return 64 * 8 + (size_t)4 * G * (G <= kFastShards ? kBagsPerWave : 1); }
+__host__ __device__ inline size_t count_wave_bytes(int G) { return kBagsPerWave * 8 + (size_t)4 * G * (G <= kFastShards ? kBagsPerWave : 1); }
 __host__ __device__ inline size_t count_lds_bytes(int G) { return (size_t)(G + 1) * 8 + kWavesPerBlock * count_wave_bytes(G); }
 __host__ __device__ inline size_t scatter_lds_bytes(int G) { return (size_t)(G + 1) * 8 + (size_t)kWavesPerBlock * G * 8; }
 
@@ -153,8 +195,8 @@ __global__ __launch_bounds__(kBlock) void eb_bucket_count(const BucketArgs a)
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = threadIdx.x / kWave;
     char *area = (char *)(lds + G + 1) + wave * count_wave_bytes(G);
-    int64_t *starts = (int64_t *)area; // 64 bag starts
-    int *hist = (int *)(area + 64 * 8);
+    int64_t *starts = (int64_t *)area; // the wave's bag starts
+    int *hist = (int *)(area + kBagsPerWave * 8);
     for (int g = threadIdx.x; g <= G; g += kBlock) bnd[g] = a.bounds[(int64_t)t * (G + 1) + g];
     __syncthreads();
 
@@ -169,7 +211,8 @@ __global__ __launch_bounds__(kBlock) void eb_bucket_count(const BucketArgs a)
     const bool contiguous = wave_bags(a, p0, nb, lane, s, e, S, E);
 
     if (contiguous && G <= kFastShards) {
-        starts[lane] = lane < nb ? s : INT64_MAX;
+        const FewBounds fb = few_bounds(bnd, G <= kFewShards ? G : 0);
+        if (lane < kBagsPerWave) starts[lane] = lane < nb ? s : INT64_MAX;
         for (int x = lane; x < kBagsPerWave * G; x += kWave) hist[x] = 0;
         wave_sync_lds();
         for (int64_t k0 = S; k0 < E; k0 += kChunks * kWave) {
@@ -185,9 +228,9 @@ __global__ __launch_bounds__(kBlock) void eb_bucket_count(const BucketArgs a)
                 if (k < E) {
                     int l = 0; // last bag starting at or before k
 #pragma unroll
-                    for (int step = 32; step > 0; step >>= 1)
+                    for (int step = kBagsPerWave / 2; step > 0; step >>= 1)
                         if (starts[l + step] <= k) l += step;
-                    const int g = owner_of(bnd, G, id[u]);
+                    const int g = G <= kFewShards ? few_owner(fb, id[u]) : owner_of(bnd, G, id[u]);
                     if (g >= 0) atomicAdd(&hist[l * G + g], 1);
                 }
             }
@@ -329,7 +372,8 @@ __device__ __forceinline__ void scatter_chunk(const BucketArgs &a, int64_t *next
         const int og = __shfl(g, leader);
         const uint64_t same = __ballot(g == og);
         const int64_t base = next[og];
-        if (g == og) a.out_indices[base + __popcll(same & below)] = id;
+        const int64_t pos = base + __popcll(same & below);
+        if (g == og && (uint64_t)pos < (uint64_t)a.nnz) a.out_indices[pos] = id;
         __builtin_amdgcn_wave_barrier();
         if (lane == leader) next[og] = base + __popcll(same);
         wave_sync_lds();
@@ -359,10 +403,13 @@ __global__ __launch_bounds__(kBlock) void eb_bucket_scatter(const BucketArgs a)
     if (contiguous && G <= kBallotShards) {
         // Contiguous bags, few destinations: one ballot per destination and
         // chunk gives every id its rank among the chunk's ids for the same
-        // destination; a single store then places the whole chunk.  Lane g
-        // keeps destination g's output slot in a register.
-        int64_t slot = lane < G ? a.segments[lane] + a.out_offsets[(int64_t)lane * row + p0] : 0;
-        const uint64_t below = (1ull << lane) - 1;
+        // destination; a single store then places the whole chunk.  The
+        // running output slot of each destination is wave-uniform.
+        const FewBounds fb = few_bounds(bnd, G);
+        int64_t slot[kBallotShards];
+#pragma unroll
+        for (int d = 0; d < kBallotShards; ++d)
+            slot[d] = d < G ? a.segments[d] + a.out_offsets[(int64_t)d * row + p0] : 0;
         for (int64_t k0 = S; k0 < E; k0 += kChunks * kWave) {
             int64_t id[kChunks];
 #pragma unroll
@@ -373,22 +420,17 @@ __global__ __launch_bounds__(kBlock) void eb_bucket_scatter(const BucketArgs a)
 #pragma unroll
             for (int u = 0; u < kChunks; ++u) {
                 const int64_t k = k0 + u * kWave + lane;
-                const int g = k < E ? owner_of(bnd, G, id[u]) : -1;
-                uint64_t mine = 0;
-                int added = 0;
+                const int g = k < E ? few_owner(fb, id[u]) : -1;
+                int64_t pos = -1;
 #pragma unroll
                 for (int d = 0; d < kBallotShards; ++d) {
                     if (d < G) {
                         const uint64_t m = __ballot(g == d);
-                        mine = g == d ? m : mine;
-                        added = lane == d ? __popcll(m) : added;
+                        pos = g == d ? slot[d] + rank_below(m) : pos;
+                        slot[d] += __popcll(m);
                     }
                 }
-                const int src = g >= 0 ? g : 0;
-                const int64_t base = ((int64_t)__shfl((int)(slot >> 32), src) << 32) |
-                                     (uint32_t)__shfl((int)(slot & 0xFFFFFFFF), src);
-                if (g >= 0) a.out_indices[base + __popcll(mine & below)] = id[u];
-                slot += added;
+                if (g >= 0 && (uint64_t)pos < (uint64_t)a.nnz) a.out_indices[pos] = id[u];
             }
         }
         return;
@@ -415,7 +457,8 @@ __global__ __launch_bounds__(kBlock) void eb_bucket_scatter(const BucketArgs a)
                     const int og = __builtin_amdgcn_readlane(g, __builtin_ctzll(pending));
                     const uint64_t same = __ballot(g == og);
                     const int64_t base = readlane64(slot, og);
-                    if (g == og) a.out_indices[base + __popcll(same & below)] = id[u];
+                    const int64_t pos = base + __popcll(same & below);
+                    if (g == og && (uint64_t)pos < (uint64_t)a.nnz) a.out_indices[pos] = id[u];
                     if (lane == og) slot += __popcll(same);
                     pending &= ~same;
                 }
