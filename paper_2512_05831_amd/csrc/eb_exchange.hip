@@ -104,11 +104,10 @@ __device__ __forceinline__ FewBounds few_bounds(const int64_t *bnd, int G)
 // holding i.  Always -1 or in [0, G).
 __device__ __forceinline__ int few_owner(const FewBounds &b, int64_t i)
 {
-    if (i < b.lo || i >= b.hi) return -1;
     int g = 0;
 #pragma unroll
     for (int j = 0; j < kFewShards - 1; ++j) g += i >= b.inner[j] ? 1 : 0;
-    return g;
+    return (i >= b.lo && i < b.hi) ? g : -1;
 }
 
 // Number of set bits of m in the lanes below this one.
@@ -417,21 +416,33 @@ __global__ __launch_bounds__(kBlock) void eb_bucket_scatter(const BucketArgs a)
                 const int64_t k = k0 + u * kWave + lane;
                 id[u] = k < E ? __builtin_nontemporal_load(a.indices + k) : 0;
             }
+            // Rank all chunks first, store afterwards: loads and stores
+            // share one completion counter, so a store between two chunks
+            // would make the next chunk wait for it.
+            int64_t pos[kChunks];
 #pragma unroll
             for (int u = 0; u < kChunks; ++u) {
                 const int64_t k = k0 + u * kWave + lane;
                 const int g = k < E ? few_owner(fb, id[u]) : -1;
-                int64_t pos = -1;
+                // Straight-line over all 8 destinations (those >= G match no
+                // lane): the rank is computed for every lane, then selected.
+                int64_t base = 0;
+                int rank = 0;
 #pragma unroll
                 for (int d = 0; d < kBallotShards; ++d) {
-                    if (d < G) {
-                        const uint64_t m = __ballot(g == d);
-                        pos = g == d ? slot[d] + rank_below(m) : pos;
-                        slot[d] += __popcll(m);
-                    }
+                    const bool mine = g == d;
+                    const uint64_t m = __ballot(mine);
+                    const int r = rank_below(m);
+                    base = mine ? slot[d] : base;
+                    rank = mine ? r : rank;
+                    slot[d] += __popcll(m);
                 }
-                if (g >= 0 && (uint64_t)pos < (uint64_t)a.nnz) a.out_indices[pos] = id[u];
+                pos[u] = g >= 0 ? base + rank : -1;
             }
+            __builtin_amdgcn_sched_barrier(0); // keep the stores after all ranking
+#pragma unroll
+            for (int u = 0; u < kChunks; ++u)
+                if ((uint64_t)pos[u] < (uint64_t)a.nnz) a.out_indices[pos[u]] = id[u];
         }
         return;
     }
