@@ -1,0 +1,74 @@
+"""The benchmark's measurement contract, on the host: algorithmic bytes per
+launch, traffic taken from committed counter summaries only while the kernel
+source matches them, and the one-GPU restriction."""
+import os
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+
+import bench  # noqa: E402
+from paper_2512_05831_amd import workloads as wl  # noqa: E402
+
+
+def test_algorithmic_bytes_of_the_headline_workload():
+    # 655,360 lookups x (512-B row + 8-B id) + 16,384 bags x (8-B offset + 512-B output) + 8
+    w = wl.config(2)
+    n = w.T * w.B * w.L
+    assert bench.algorithmic_bytes(w, n, n, False) == 349_306_888
+    # int32 ids and offsets: 4 B less per lookup and per offset
+    assert bench.algorithmic_bytes(w, n, n, False, 4) == 349_306_888 - 4 * (n + w.T * w.B + 1)
+
+
+def test_algorithmic_bytes_count_only_local_rows_and_hits():
+    w = wl.config(5)
+    nnz, local = 1000, 600
+    base = bench.algorithmic_bytes(w, local, nnz, False)
+    assert base == local * w.D * 2 + nnz * 8 + (w.T * w.B + 1) * 8 + w.B * w.T * w.D * 4
+    assert bench.algorithmic_bytes(w, local, nnz, True) == base + w.B * w.T * 4
+
+
+def write_profile(path, sha, fetch_kib, write_kib, ff=2.0, fw=1.0):
+    path.write_text(f"""# a comment: with a colon
+kernel: eb_gather_team
+kernel_source_sha256: {sha}
+fetch_kib_per_dispatch: {fetch_kib}
+write_kib_per_dispatch: {write_kib}
+copy_fetch_factor: {ff}
+copy_write_factor: {fw}
+""")
+
+
+def test_traffic_only_while_the_source_matches(tmp_path, monkeypatch):
+    monkeypatch.setattr(bench, "PROFILES", str(tmp_path))
+    name = "some-workload"
+    assert bench.measured_traffic(name) is None  # no summary
+    prof = tmp_path / f"eb_gather_team__{name}__counters.txt"
+    write_profile(prof, bench.kernel_source_hash(), 100.0, 10.0)
+    assert bench.measured_traffic(name) == pytest.approx(100 * 1024 * 2.0 + 10 * 1024 * 1.0)
+    write_profile(prof, "0" * 16, 100.0, 10.0)
+    assert bench.measured_traffic(name) is None  # kernel changed since the counters were taken
+    prof.write_text(f"kernel_source_sha256: {bench.kernel_source_hash()}\nfetch_kib_per_dispatch: x\n")
+    assert bench.measured_traffic(name) is None  # malformed
+
+
+def test_committed_profiles_match_the_kernel_source():
+    """Every committed counter summary names the current kernel source, so the
+    benchmark reports traffic for those workloads."""
+    profiles = os.path.join(ROOT, "profiles")
+    names = [f for f in os.listdir(profiles) if f.startswith("eb_gather_team__") and f.endswith("__counters.txt")]
+    assert names
+    for f in names:
+        workload = f[len("eb_gather_team__"):-len("__counters.txt")]
+        assert bench.measured_traffic(workload) is not None, f
+
+
+def test_more_than_one_gpu_is_refused():
+    res = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                         capture_output=True, text=True, timeout=120)
+    assert res.returncode == 2
+    assert "one GPU" in res.stderr
+    assert res.stdout == ""
