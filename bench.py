@@ -18,6 +18,11 @@ Prints one JSON line: lookups/s over the timed steps (wall clock between two
 device synchronisations), the kernel's HBM roofline (algorithmic bytes per
 launch / mean launch duration, from HIP events on the launch stream around the
 K back-to-back launches, against 8 TB/s) and the CPU oracle's rate on the host.
+After the timed region it also measures, for context: ``attainable`` (random
+whole-row reads over the same footprint with the library's probe, uniform-id
+workloads only) and ``torch_embedding_bag`` (PyTorch's own GPU embedding_bag
+on the same tables and ids); ``--cold`` adds single-launch timings with and
+without the caches flushed.
 """
 from __future__ import annotations
 
@@ -145,6 +150,63 @@ def per_launch_us(torch, stream, fn_list, K, flush=None):
     us = sorted(a.elapsed_time(b) * 1e3 for a, b in times)
     pick = lambda q: us[min(len(us) - 1, int(q * len(us)))]
     return {"median_us": pick(0.5), "p10_us": pick(0.1), "p90_us": pick(0.9), "launches": K}
+
+
+def attainable_ceiling(torch, dev, w, lookups: int, stream):
+    """Random whole-row reads over the workload's footprint (same row size,
+    same number of rows in all tables together, ids uniform, pre-resolved as
+    int32) with the probe in the library: the most a gather of these rows can
+    sustain.  Best over rows in flight 2/4/8 and cached / non-temporal loads;
+    GB/s counts the rows and the 4-byte ids read."""
+    import ctypes
+
+    from paper_2512_05831_amd import eb
+
+    rb = w.D * w.elem_bytes
+    if rb not in (32, 64, 128, 256, 512, 1024):
+        return None
+    rows = w.T * w.stored_rows
+    if rows > np.iinfo(np.int32).max:
+        return None
+    lib = eb.library()
+    f = lib.eb_probe_random_rows
+    f.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p, ctypes.c_int64,
+                  ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p]
+    f.restype = ctypes.c_int
+    table = torch.empty(rows * rb, dtype=torch.uint8, device=dev)
+    sink = torch.zeros(1, dtype=torch.float32, device=dev)
+    gen = torch.Generator(device=dev).manual_seed(w.seed + 99)
+    ids = [torch.randint(0, rows, (lookups,), generator=gen, device=dev, dtype=torch.int32)
+           for _ in range(4)]
+    best = None
+    K = 50
+    for U in (2, 4, 8):
+        for nt in (0, 1):
+            grid = 8192
+
+            def launch(i):
+                rc = f(table.data_ptr(), rows, rb, ids[i % 4].data_ptr(), lookups, U, nt, grid,
+                       sink.data_ptr(), stream.cuda_stream)
+                if rc != 0:
+                    raise RuntimeError(f"eb_probe_random_rows returned {rc}")
+            with torch.cuda.stream(stream):
+                for i in range(5):
+                    launch(i)
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+                for i in range(K):
+                    launch(i)
+                e1.record(stream)
+                torch.cuda.synchronize()
+            us = e0.elapsed_time(e1) * 1e3 / K
+            gbps = lookups * (rb + 4) / us / 1e3
+            if best is None or gbps > best["GBps"]:
+                best = {"GBps": gbps, "us_per_launch": us, "rows_in_flight": U, "nontemporal": bool(nt)}
+    del table, ids
+    torch.cuda.empty_cache()
+    best.update({"kind": "random whole-row reads, pre-resolved int32 ids, no pooling",
+                 "row_bytes": rb, "rows": rows, "footprint_GB": rows * rb / 1e9, "lookups": lookups})
+    return best
 
 
 def torch_embedding_bag_step(torch, w, d_idx, d_off_all, dev_tables, mode):
@@ -344,8 +406,11 @@ def main():
     ap.add_argument("--rows-policy", default="auto", choices=["auto", "cached", "stream"])
     ap.add_argument("--cold", action="store_true",
                     help="also time single launches after writing a 512 MB buffer (caches flushed)")
-    ap.add_argument("--torch-baseline", action="store_true",
-                    help="also time torch.nn.functional.embedding_bag on the same batches (context)")
+    ap.add_argument("--no-ceiling", dest="ceiling", action="store_false",
+                    help="skip measuring random whole-row reads over the same footprint (the "
+                         "attainable bandwidth of a gather, uniform-id workloads)")
+    ap.add_argument("--no-torch-baseline", dest="torch_baseline", action="store_false",
+                    help="skip timing torch.nn.functional.embedding_bag on the same batches (context)")
     ap.add_argument("--index-type", default="i64", choices=["i64", "i32"],
                     help="integer type of the ids and offsets handed to the library")
     ap.add_argument("--graph", action="store_true",
@@ -466,6 +531,16 @@ def main():
         del scratch
         log(f"bench: single launch warm {extra['single_launch_warm']['median_us']:.1f} us, "
             f"cold {extra['single_launch_cold']['median_us']:.1f} us (medians)")
+    if args.ceiling:
+        if w.dist != "uniform":
+            log("bench: ceiling skipped (skewed ids are served partly from caches)")
+        else:
+            ceil = attainable_ceiling(torch, dev, w, steps_lookups // K, stream)
+            if ceil is not None:
+                ceil["frac"] = achieved / ceil["GBps"]
+                extra["attainable"] = ceil
+                log(f"bench: attainable random-row rate {ceil['GBps']:.0f} GB/s; "
+                    f"this kernel {achieved:.0f} GB/s = {ceil['frac'] * 100:.1f}% of it")
     if args.torch_baseline:
         if w.sharded:
             log("bench: torch baseline skipped (a row shard has no torch equivalent)")

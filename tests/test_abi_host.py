@@ -12,15 +12,24 @@ import pytest
 
 from paper_2512_05831_amd import eb
 
-HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "eb.h")
+INCLUDE = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include")
+HEADER = os.path.join(INCLUDE, "eb.h")
 FAKE = 0x7F0000000000  # 16-byte aligned, never dereferenced by these tests
 I64MAX = (1 << 63) - 1
 
 
-def declared_functions():
-    text = open(HEADER).read()
+def declared_functions(header=HEADER):
+    text = open(header).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
     return sorted(set(re.findall(r"\b(eb_\w+)\s*\(", text)))
+
+
+def all_declared_functions():
+    names = set()
+    for f in os.listdir(INCLUDE):
+        if f.endswith(".h"):
+            names.update(declared_functions(os.path.join(INCLUDE, f)))
+    return sorted(names)
 
 
 def test_header_declares_the_boundary():
@@ -31,8 +40,28 @@ def test_header_declares_the_boundary():
 
 def test_library_exports_every_declared_symbol():
     lib = eb.library()
-    for name in declared_functions():
+    names = all_declared_functions()
+    assert "eb_probe_random_rows" in names
+    for name in names:
         assert hasattr(lib, name), name
+
+
+def test_ceiling_probe_rejects_bad_arguments():
+    lib = eb.library()
+    f = lib.eb_probe_random_rows
+    f.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p, ctypes.c_int64,
+                  ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p]
+    ok = dict(table=FAKE, rows=10, row_bytes=512, ids=FAKE, n=5, u=4, nt=1, grid=8, sink=FAKE)
+
+    def call(**kw):
+        a = dict(ok, **kw)
+        return f(a["table"], a["rows"], a["row_bytes"], a["ids"], a["n"], a["u"], a["nt"], a["grid"],
+                 a["sink"], None)
+    for kw in (dict(table=None), dict(ids=None), dict(sink=None), dict(rows=0), dict(n=0),
+               dict(u=3), dict(grid=0)):
+        assert call(**kw) == -1, kw
+    for rb in (16, 48, 2048):
+        assert call(row_bytes=rb) == -2
 
 
 def handle(T=2, D=16, dtype=eb.EB_F32, rows=(100, 100)):
