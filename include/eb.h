@@ -61,9 +61,14 @@ enum { EB_SUM = 0, EB_MEAN = 1 };
  * library that the ids have little reuse (for example drawn uniformly from
  * tables much larger than the 256 MB last-level cache).  It then reads rows of
  * 128 bytes or more with non-temporal loads, which bypass L2 and the
- * last-level cache, and gives each XCD a contiguous run of bags.  Faster for
- * such ids, slower for skewed ones (hot rows then miss the caches); it
- * changes no result. */
+ * last-level cache, gives each XCD a contiguous run of bags, and in large
+ * batches pools rows wider than 128 and at most 512 bytes with one lane group
+ * per bag.  Faster for such ids, slower
+ * for skewed ones (hot rows then miss the caches).  It changes no hit count;
+ * by splitting a bag's rows differently over lanes it may change the order of
+ * the fp32 additions and so the last bits of a sum (every result stays within
+ * the same accuracy bound, exact sums stay exact).  Repeated calls with the
+ * same mode give identical bits. */
 enum { EB_HINT_STREAM_ROWS = 0x100 };
 
 /* Integer type of eb_forward_ex's indices and offsets (both the same).

@@ -15,11 +15,13 @@
 //     two covering min(64, rb/16), each loading C = ceil(rb/(16R)) 16-byte
 //     chunks (global_load_dwordx4); surplus lanes of a ragged row idle.
 //   * P such lane groups form the team that pools one bag: group g takes the
-//     bag's rows g, g+P, g+2P, ...; a wave holds 64/(R*P) teams.  Partial
+//     bag's rows g, g+P, g+2P, ...; a wave holds 64/(R*P) teams (P = 64/R
+//     for rows of 16 lanes or more, halved for streamed rows of large
+//     batches).  Partial
 //     sums of the P groups are combined at the end with cross-lane moves
 //     (DPP, ds_swizzle, v_permlane32_swap).
 //   * A team stages a window of its bag's indices in LDS: the window is read
-//     with coalesced int64 loads, filtered against the shard, and rewritten as
+//     with coalesced index loads, filtered against the shard, and rewritten as
 //     32-bit local row numbers (or an invalid marker).  The gather loop then
 //     reads them from LDS and keeps U rows per group in flight (unrolled;
 //     U = 2 for streamed rows of 128 B or more, else 6).
@@ -433,17 +435,24 @@ int rows_in_flight_per_bag(const Shape &s, bool stream)
     return s.P * u;
 }
 
-Shape team_shape(int rb, bool few)
+// Lane groups per bag; the kernels' template arguments follow the same rule.
+constexpr int groups_per_bag(int R, bool few, bool single)
+{
+    // Wide rows or small batches: one bag per wave.  Otherwise narrow rows
+    // get 16-lane teams (4 bags per wave), so the group reduction stays
+    // inside a DPP row.  "single": rows of 16 or 32 lanes with one lane group
+    // per bag (two bags per wave), used for streamed rows of large batches.
+    return few ? kWave / R : (single && R >= 16 && R < kWave) ? kWave / R / 2 : R >= 16 ? kWave / R : 16 / R;
+}
+
+Shape team_shape(int rb, bool few, bool single)
 {
     Shape s;
     const int chunks = rb / 16;
     s.R = 1;
     while (s.R < chunks && s.R < kWave) s.R *= 2;
     s.C = (chunks + s.R - 1) / s.R;
-    // Wide rows or small batches: one bag per wave.  Otherwise narrow rows
-    // get 16-lane teams (4 bags per wave), so the group reduction stays
-    // inside a DPP row.
-    s.P = (few || s.R >= 16) ? kWave / s.R : 16 / s.R;
+    s.P = groups_per_bag(s.R, few, single);
     return s;
 }
 
@@ -456,53 +465,57 @@ using KernelFn = void (*)(GatherArgs);
 // bags than fill the GPU) is bound by each bag's chain of dependent loads
 // instead: every bag then gets a whole wave and 6 rows in flight per lane.
 template <typename IT, int DT, int R, int C, bool kFew>
-KernelFn team_kernel(bool stream)
+KernelFn team_kernel(bool stream, bool single)
 {
-    constexpr int P = (kFew || R >= 16) ? kWave / R : 16 / R;
+    constexpr int P = groups_per_bag(R, kFew, false);
+    constexpr int P_SINGLE = groups_per_bag(R, kFew, true);
     constexpr int U_CACHED = C >= 6 ? 1 : 6 / C;
     constexpr int U_STREAM = (!kFew && R * C >= 8) ? (C >= 2 ? 1 : 2) : U_CACHED;
-    return stream ? eb_gather_team<IT, DT, R, P, C, U_STREAM, true>
-                  : eb_gather_team<IT, DT, R, P, C, U_CACHED, false>;
+    if (!stream) return eb_gather_team<IT, DT, R, P, C, U_CACHED, false>;
+    if constexpr (P_SINGLE != P) {
+        if (single) return eb_gather_team<IT, DT, R, P_SINGLE, C, U_STREAM, true>;
+    }
+    return eb_gather_team<IT, DT, R, P, C, U_STREAM, true>;
 }
 
 template <typename IT, int DT, int R, int C>
-KernelFn team_kernel(bool stream, bool few)
+KernelFn team_kernel(bool stream, bool few, bool single)
 {
-    return few ? team_kernel<IT, DT, R, C, true>(stream) : team_kernel<IT, DT, R, C, false>(stream);
+    return few ? team_kernel<IT, DT, R, C, true>(stream, false) : team_kernel<IT, DT, R, C, false>(stream, single);
 }
 
 template <typename IT, int DT>
-KernelFn pick_team_kernel(int R, int C, bool stream, bool few)
+KernelFn pick_team_kernel(int R, int C, bool stream, bool few, bool single)
 {
     switch (R) {
-    case 1: return team_kernel<IT, DT, 1, 1>(stream, few);
-    case 2: return team_kernel<IT, DT, 2, 1>(stream, few);
-    case 4: return team_kernel<IT, DT, 4, 1>(stream, few);
-    case 8: return team_kernel<IT, DT, 8, 1>(stream, few);
-    case 16: return team_kernel<IT, DT, 16, 1>(stream, few);
-    case 32: return team_kernel<IT, DT, 32, 1>(stream, few);
+    case 1: return team_kernel<IT, DT, 1, 1>(stream, few, single);
+    case 2: return team_kernel<IT, DT, 2, 1>(stream, few, single);
+    case 4: return team_kernel<IT, DT, 4, 1>(stream, few, single);
+    case 8: return team_kernel<IT, DT, 8, 1>(stream, few, single);
+    case 16: return team_kernel<IT, DT, 16, 1>(stream, few, single);
+    case 32: return team_kernel<IT, DT, 32, 1>(stream, few, single);
     default:
         switch (C) {
-        case 1: return team_kernel<IT, DT, 64, 1>(stream, few);
-        case 2: return team_kernel<IT, DT, 64, 2>(stream, few);
-        case 3: return team_kernel<IT, DT, 64, 3>(stream, few);
-        case 4: return team_kernel<IT, DT, 64, 4>(stream, few);
-        case 5: return team_kernel<IT, DT, 64, 5>(stream, few);
-        case 6: return team_kernel<IT, DT, 64, 6>(stream, few);
-        case 7: return team_kernel<IT, DT, 64, 7>(stream, few);
-        case 8: return team_kernel<IT, DT, 64, 8>(stream, few);
+        case 1: return team_kernel<IT, DT, 64, 1>(stream, few, single);
+        case 2: return team_kernel<IT, DT, 64, 2>(stream, few, single);
+        case 3: return team_kernel<IT, DT, 64, 3>(stream, few, single);
+        case 4: return team_kernel<IT, DT, 64, 4>(stream, few, single);
+        case 5: return team_kernel<IT, DT, 64, 5>(stream, few, single);
+        case 6: return team_kernel<IT, DT, 64, 6>(stream, few, single);
+        case 7: return team_kernel<IT, DT, 64, 7>(stream, few, single);
+        case 8: return team_kernel<IT, DT, 64, 8>(stream, few, single);
         }
     }
     return nullptr;
 }
 
 template <typename IT>
-KernelFn pick_team_kernel(int dtype, int R, int C, bool stream, bool few)
+KernelFn pick_team_kernel(int dtype, int R, int C, bool stream, bool few, bool single)
 {
     switch (dtype) {
-    case EB_F32: return pick_team_kernel<IT, EB_F32>(R, C, stream, few);
-    case EB_F16: return pick_team_kernel<IT, EB_F16>(R, C, stream, few);
-    default: return pick_team_kernel<IT, EB_BF16>(R, C, stream, few);
+    case EB_F32: return pick_team_kernel<IT, EB_F32>(R, C, stream, few, single);
+    case EB_F16: return pick_team_kernel<IT, EB_F16>(R, C, stream, few, single);
+    default: return pick_team_kernel<IT, EB_BF16>(R, C, stream, few, single);
     }
 }
 
@@ -605,14 +618,21 @@ int forward_impl(const char *who, const eb_tables *h, int32_t T, const int64_t *
     if (team_path) {
         // Non-temporal loads lose for rows narrower than 128 bytes.
         const bool stream = (mode & EB_HINT_STREAM_ROWS) && rb >= 128;
-        const Shape normal = team_shape((int)rb, false);
+        const Shape normal = team_shape((int)rb, false, false);
         const int64_t bags = (int64_t)T * B;
         const int64_t waves = bags / (kWave / (normal.R * normal.P));
         const bool few = waves < kWaveSlots && bags <= kFewBagsMax &&
                          nnz > 2 * (int64_t)rows_in_flight_per_bag(normal, stream) * bags;
-        const Shape sh = team_shape((int)rb, few);
-        fn = i32 ? pick_team_kernel<int32_t>(dtype, sh.R, sh.C, stream, few)
-                 : pick_team_kernel<int64_t>(dtype, sh.R, sh.C, stream, few);
+        // Streamed rows of 16 or 32 lanes: one lane group per bag (two bags
+        // per wave) when that still gives half the GPU's wave slots or more.
+        // Over the paper's shapes and workloads 2 and 4 that is 2-6% faster;
+        // smaller batches lose more from halving their waves.
+        const Shape halved = team_shape((int)rb, false, true);
+        const bool single = stream && !few && halved.P != normal.P &&
+                            bags / (kWave / (halved.R * halved.P)) >= kWaveSlots / 2;
+        const Shape sh = few ? team_shape((int)rb, true, false) : single ? halved : normal;
+        fn = i32 ? pick_team_kernel<int32_t>(dtype, sh.R, sh.C, stream, few, single)
+                 : pick_team_kernel<int64_t>(dtype, sh.R, sh.C, stream, few, single);
         bags_per_block = (kWave / (sh.R * sh.P)) * kWavesPerBlock;
         // No reuse: each XCD takes a contiguous run of bags.  Otherwise
         // hardware order, so all XCDs work on the same table at once and its

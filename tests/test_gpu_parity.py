@@ -93,15 +93,26 @@ def test_dyadic_mean_within_one_ulp(dtype):
 
 @pytest.mark.parametrize("dtype", DT)
 @pytest.mark.parametrize("D", [8, 16, 32, 64, 100, 128, 256, 512, 1024, 2048])
-def test_stream_hint_changes_no_result(dtype, D):
-    tables, rows, idx, off = case(D=D, dtype=dtype, seed=300 + D, lo=100, hi=2900, dist="zipf")
-    for mode in (wl.SUM, wl.MEAN):
-        plain, h1 = run(tables, rows, D, dtype, idx, off, 37, mode, 100, 2900)
-        hinted, h2 = run(tables, rows, D, dtype, idx, off, 37, mode | eb.EB_HINT_STREAM_ROWS, 100, 2900)
-        assert np.array_equal(plain.view(np.uint32), hinted.view(np.uint32))
-        assert np.array_equal(h1, h2)
-        ref, ref_hits, mag = oracle.forward(tables, rows, D, dtype, idx, off, 37, mode, 100, 2900)
-        assert_parity(hinted, ref, mag, max_bag_len(off, idx.size), dtype, h2, ref_hits)
+# 37 bags per table: the small-batch mapping; 1500: the normal one; 3000: two
+# bags per wave for streamed rows of 16 or 32 lanes
+@pytest.mark.parametrize("B", [37, 1500, 3000])
+def test_stream_hint_keeps_results(dtype, D, B):
+    """The hint changes cache policy and lane mapping: hit counts are equal,
+    both results meet the bound, and exact (dyadic) sums are bit-identical."""
+    rows_n = 2000 if D >= 1024 else 3000
+    for values in ("normal", "dyadic"):
+        tables, rows, idx, off = case(D=D, dtype=dtype, seed=300 + D, lo=100, hi=2900, dist="zipf",
+                                      B=B, rows=rows_n, values=values,
+                                      lengths=("var", 0, 70 if B < 100 else 12))
+        for mode in (wl.SUM, wl.MEAN):
+            plain, h1 = run(tables, rows, D, dtype, idx, off, B, mode, 100, 2900)
+            hinted, h2 = run(tables, rows, D, dtype, idx, off, B, mode | eb.EB_HINT_STREAM_ROWS, 100, 2900)
+            assert np.array_equal(h1, h2)
+            ref, ref_hits, mag = oracle.forward(tables, rows, D, dtype, idx, off, B, mode, 100, 2900)
+            for got, h in ((plain, h1), (hinted, h2)):
+                assert_parity(got, ref, mag, max_bag_len(off, idx.size), dtype, h, ref_hits)
+            if values == "dyadic" and mode == wl.SUM:
+                assert np.array_equal(plain.view(np.uint32), hinted.view(np.uint32))
 
 
 # ----------------------------------------------------------------------------- bag lengths

@@ -125,8 +125,9 @@ def test_int32_empty_and_workload_batch(device):
     idx = w.indices(off)
     gen = torch.Generator(device=device).manual_seed(5)
     dts = [torch.randn((w.rows, w.D), generator=gen, device=device) for _ in range(w.T)]
-    got, hits = run_ex(dts, [w.rows] * w.T, idx, off, w.B, wl.SUM | eb.EB_HINT_STREAM_ROWS, device)
-    want, want_hits = run_i64(dts, [w.rows] * w.T, idx, off, w.B, wl.SUM, device)
+    mode = wl.SUM | eb.EB_HINT_STREAM_ROWS  # the same mode (and so the same lane mapping) on both sides
+    got, hits = run_ex(dts, [w.rows] * w.T, idx, off, w.B, mode, device)
+    want, want_hits = run_i64(dts, [w.rows] * w.T, idx, off, w.B, mode, device)
     assert same_bits(got.cpu().numpy(), want) and np.array_equal(hits.cpu().numpy(), want_hits)
     # no ids at all: every bag pools to +0
     z_off = np.zeros(w.T * 4 + 1, dtype=np.int64)
