@@ -294,8 +294,8 @@ def exchange_bench(torch, dev, eb, K, W):
 
     def bucket():
         eb.eb_bucketize(w.T, w.B, G, d_b.data_ptr(), d_i.data_ptr(), idx.size, d_o.data_ptr(),
-                        out_off.data_ptr(), out_idx.data_ptr(), seg.data_ptr(), ws.data_ptr(), nws,
-                        stream.cuda_stream)
+                        out_off.data_ptr(), out_idx.data_ptr(), idx.size, seg.data_ptr(),
+                        ws.data_ptr(), nws, stream.cuda_stream)
     us = _time_launches(torch, stream, bucket, K, W)
     kept = int(seg[-1].item())
     by = idx.size * 8 + (TB + 1) * 8 + bounds.size * 8 + kept * 8 + G * (TB + 1) * 8 + (G + 1) * 8

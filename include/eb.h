@@ -230,29 +230,38 @@ int eb_bucketize_workspace(int32_t T, int64_t B, int32_t G, size_t *bytes);
  *                [bounds[t][0], bounds[t][G]) go to no GPU and are dropped.
  *   indices, nnz, offsets
  *                the mini-batch in the layout eb_forward takes (offsets
- *                [T*B+1] clamped into [0, nnz]).
+ *                [T*B+1] clamped into [0, nnz]; every bag sends the ids of
+ *                its own clamped range, so bags whose ranges overlap, which
+ *                only malformed offsets produce, send such ids once each).
  *   out_offsets  device int64 [G][T*B+1]: destination g's CSR offsets for
  *                the same T*B bags, out_offsets[g][0] = 0.
- *   out_indices  device int64 [nnz]: destination g's ids at
+ *   out_indices  device int64 [out_capacity]: destination g's ids at
  *                [segments[g], segments[g+1]), in (table, bag, position)
  *                order.  They stay global ids: the receiving GPU pools them
- *                with eb_forward and its own shard range.
- *   segments     device int64 [G+1]; segments[G] = ids kept.
+ *                with eb_forward and its own shard range.  Positions at or
+ *                past out_capacity are not written.
+ *   out_capacity entries of out_indices, >= 0.  nnz always suffices for
+ *                ordinary offsets (non-decreasing within [0, nnz]).
+ *   segments     device int64 [G+1]; segments[G] = ids sent, the full
+ *                count even where it exceeds out_capacity (then only the
+ *                first out_capacity ids were stored; out_offsets and
+ *                segments are complete either way).
  *   workspace    device scratch of at least eb_bucketize_workspace() bytes,
  *                owned by the caller; its contents are not kept.
  *   stream       a hipStream_t (NULL = the null stream); asynchronous.
  *
  * No allocation, no host synchronisation; calls that overlap on the same
- * workspace race.  Errors: EB_ERR_INVALID for NULL buffers (indices and
- * out_indices may be NULL when nnz == 0), negative sizes, or a workspace
- * that is too small; EB_ERR_UNSUPPORTED for G > 1024 or a batch too large
+ * workspace race.  Errors: EB_ERR_INVALID for NULL buffers (indices may be
+ * NULL when nnz == 0, out_indices when out_capacity == 0), negative sizes, or
+ * a workspace that is too small; EB_ERR_UNSUPPORTED for G > 1024 or a batch too large
  * for one launch; EB_ERR_HIP when a launch fails.  With non-decreasing
  * bounds the result equals the definition above; other bounds give an
  * unspecified split but every access stays in bounds.
  */
 int eb_bucketize(int32_t T, int64_t B, int32_t G, const int64_t *bounds, const int64_t *indices,
                  int64_t nnz, const int64_t *offsets, int64_t *out_offsets, int64_t *out_indices,
-                 int64_t *segments, void *workspace, size_t workspace_bytes, void *stream);
+                 int64_t out_capacity, int64_t *segments, void *workspace, size_t workspace_bytes,
+                 void *stream);
 
 /*
  * eb_sum_partials -- add the partial results every GPU computed for this

@@ -53,7 +53,7 @@ def load_library(path: str) -> ctypes.CDLL:
     lib.oracle_eb_bags.restype = ctypes.c_int
     lib.oracle_decode.argtypes = [i32, p, i64, p]
     lib.oracle_decode.restype = ctypes.c_int
-    lib.oracle_bucketize.argtypes = [i32, i64, i32, p, p, i64, p, p, p, p]
+    lib.oracle_bucketize.argtypes = [i32, i64, i32, p, p, i64, p, p, p, i64, p]
     lib.oracle_bucketize.restype = ctypes.c_int
     lib.oracle_sum_partials.argtypes = [i32, p, i64, i32, i32, p, i64, p]
     lib.oracle_sum_partials.restype = ctypes.c_int
@@ -162,11 +162,12 @@ def decode(dtype, bits) -> np.ndarray:
     return out
 
 
-def bucketize(bounds, indices, offsets, T: int, B: int):
+def bucketize(bounds, indices, offsets, T: int, B: int, capacity=None):
     """Destination lists of the row-wise exchange.  ``bounds``: int64 [T, G+1].
 
-    Returns (out_offsets int64 [G, T*B+1], out_indices int64 [total],
-    segments int64 [G+1])."""
+    Returns (out_offsets int64 [G, T*B+1], out_indices int64 [min(total,
+    capacity)], segments int64 [G+1]).  ``capacity`` (default: room for
+    every id) bounds the ids written; segments[G] is always the full total."""
     bounds = np.ascontiguousarray(bounds, dtype=np.int64)
     if bounds.ndim != 2 or bounds.shape[0] != T:
         raise ValueError("bounds must be [T, G+1]")
@@ -175,15 +176,21 @@ def bucketize(bounds, indices, offsets, T: int, B: int):
     offsets = np.ascontiguousarray(offsets, dtype=np.int64)
     if offsets.size != T * B + 1:
         raise ValueError("offsets must have T*B+1 entries")
+    if capacity is None:
+        # every bag's clamped length: room for all ids, overlapping bags included
+        nnz = indices.size
+        s = np.clip(offsets[:-1], 0, nnz)
+        e = np.maximum(np.minimum(offsets[1:], nnz), s)
+        capacity = int(np.sum(e - s))
     out_off = np.zeros((G, T * B + 1), dtype=np.int64)
-    out_idx = np.zeros(max(1, indices.size), dtype=np.int64)
+    out_idx = np.zeros(max(1, capacity), dtype=np.int64)
     seg = np.zeros(G + 1, dtype=np.int64)
     rc = _load().oracle_bucketize(T, B, G, bounds.ctypes.data, indices.ctypes.data, indices.size,
                                   offsets.ctypes.data, out_off.ctypes.data, out_idx.ctypes.data,
-                                  seg.ctypes.data)
+                                  capacity, seg.ctypes.data)
     if rc != 0:
         raise ValueError("oracle_bucketize rejected its arguments")
-    return out_off, out_idx[:seg[-1]].copy(), seg
+    return out_off, out_idx[:min(int(seg[-1]), capacity)].copy(), seg
 
 
 def sum_partials(partials, B: int, T: int, D: int, mean_offsets=None, nnz: int = 0):

@@ -200,15 +200,19 @@ int oracle_decode(int32_t dtype, const void *bits, int64_t n, double *out)
  * For each destination g in turn, the ids of every bag (t, b) that fall in
  * g's block are appended in (table, bag, position) order; ids outside
  * [bounds[t][0], bounds[t][G]) go nowhere.  Bags follow the clamped-offset
- * rule of pool_bag.
+ * rule of pool_bag; bags whose ranges overlap (malformed offsets) each send
+ * their ids, so the total can exceed nnz.
  *   out_offsets [G][T*B+1]: CSR offsets of destination g's ids, from 0.
- *   out_indices [total]:    the ids, destination g's at [segments[g], segments[g+1]).
- *   segments    [G+1]. */
+ *   out_indices [out_capacity]: the ids, destination g's at
+ *                           [segments[g], segments[g+1]); positions at or past
+ *                           out_capacity are not written.
+ *   segments    [G+1]:      segments[G] is the full total, written or not. */
 int oracle_bucketize(int32_t T, int64_t B, int32_t G, const int64_t *bounds,
                      const int64_t *indices, int64_t nnz, const int64_t *offsets,
-                     int64_t *out_offsets, int64_t *out_indices, int64_t *segments)
+                     int64_t *out_offsets, int64_t *out_indices, int64_t out_capacity,
+                     int64_t *segments)
 {
-    if (T < 0 || B < 0 || G < 1 || nnz < 0) return -1;
+    if (T < 0 || B < 0 || G < 1 || nnz < 0 || out_capacity < 0) return -1;
     int64_t TB = (int64_t)T * B;
     int64_t pos = 0;
     for (int32_t g = 0; g < G; ++g) {
@@ -226,7 +230,10 @@ int oracle_bucketize(int32_t T, int64_t B, int32_t G, const int64_t *bounds,
                 if (e < s) e = s;
                 for (int64_t k = s; k < e; ++k) {
                     int64_t i = indices[k];
-                    if (i >= lo && i < hi) out_indices[pos++] = i;
+                    if (i >= lo && i < hi) {
+                        if (pos < out_capacity) out_indices[pos] = i;
+                        ++pos;
+                    }
                 }
             }
         }

@@ -33,8 +33,9 @@
 //                each 64-id chunk), so the order is stable.  For ordinary CSR
 //                offsets one running slot per destination and wave suffices,
 //                since position order is then (bag, position) order.  Every
-//                store is checked against nnz, so no bounds, offsets or ids
-//                can make it write outside out_indices.
+//                store is checked against the capacity of out_indices (an
+//                argument), so no bounds, offsets or ids can make it write
+//                outside it; bags that overlap send an id once per bag.
 
 #include <hip/hip_runtime.h>
 
@@ -132,6 +133,7 @@ struct BucketArgs {
     int64_t *out_offsets;    // [G][T*B+1]
     int64_t *out_indices;
     const int64_t *segments; // [G+1] (scatter pass)
+    int64_t out_cap;         // entries of out_indices; positions at or past it are not written
     int64_t nnz;
     int64_t B;
     int64_t TB;
@@ -372,7 +374,7 @@ __device__ __forceinline__ void scatter_chunk(const BucketArgs &a, int64_t *next
         const uint64_t same = __ballot(g == og);
         const int64_t base = next[og];
         const int64_t pos = base + __popcll(same & below);
-        if (g == og && (uint64_t)pos < (uint64_t)a.nnz) a.out_indices[pos] = id;
+        if (g == og && (uint64_t)pos < (uint64_t)a.out_cap) a.out_indices[pos] = id;
         __builtin_amdgcn_wave_barrier();
         if (lane == leader) next[og] = base + __popcll(same);
         wave_sync_lds();
@@ -442,7 +444,7 @@ __global__ __launch_bounds__(kBlock) void eb_bucket_scatter(const BucketArgs a)
             __builtin_amdgcn_sched_barrier(0); // keep the stores after all ranking
 #pragma unroll
             for (int u = 0; u < kChunks; ++u)
-                if ((uint64_t)pos[u] < (uint64_t)a.nnz) a.out_indices[pos[u]] = id[u];
+                if ((uint64_t)pos[u] < (uint64_t)a.out_cap) a.out_indices[pos[u]] = id[u];
         }
         return;
     }
@@ -469,7 +471,7 @@ __global__ __launch_bounds__(kBlock) void eb_bucket_scatter(const BucketArgs a)
                     const uint64_t same = __ballot(g == og);
                     const int64_t base = readlane64(slot, og);
                     const int64_t pos = base + __popcll(same & below);
-                    if (g == og && (uint64_t)pos < (uint64_t)a.nnz) a.out_indices[pos] = id[u];
+                    if (g == og && (uint64_t)pos < (uint64_t)a.out_cap) a.out_indices[pos] = id[u];
                     if (lane == og) slot += __popcll(same);
                     pending &= ~same;
                 }
@@ -587,17 +589,19 @@ int eb_bucketize_workspace(int32_t T, int64_t B, int32_t G, size_t *bytes)
 
 int eb_bucketize(int32_t T, int64_t B, int32_t G, const int64_t *bounds, const int64_t *indices,
                  int64_t nnz, const int64_t *offsets, int64_t *out_offsets, int64_t *out_indices,
-                 int64_t *segments, void *workspace, size_t workspace_bytes, void *stream)
+                 int64_t out_capacity, int64_t *segments, void *workspace, size_t workspace_bytes,
+                 void *stream)
 {
     size_t need = 0;
     const int rc = eb_bucketize_workspace(T, B, G, &need);
     if (rc != EB_OK) return rc;
-    if (nnz < 0) return fail(EB_ERR_INVALID, "eb_bucketize: negative nnz");
+    if (nnz < 0 || out_capacity < 0) return fail(EB_ERR_INVALID, "eb_bucketize: negative nnz or out_capacity");
     if (!segments || !out_offsets) return fail(EB_ERR_INVALID, "eb_bucketize: NULL segments or out_offsets");
     const int64_t TB = (int64_t)T * B;
     if (TB > 0 && (!bounds || !offsets)) return fail(EB_ERR_INVALID, "eb_bucketize: NULL bounds or offsets");
-    if (TB > 0 && nnz > 0 && (!indices || !out_indices))
-        return fail(EB_ERR_INVALID, "eb_bucketize: NULL indices or out_indices with nnz > 0");
+    if (TB > 0 && nnz > 0 && !indices) return fail(EB_ERR_INVALID, "eb_bucketize: NULL indices with nnz > 0");
+    if (out_capacity > 0 && !out_indices)
+        return fail(EB_ERR_INVALID, "eb_bucketize: NULL out_indices with out_capacity > 0");
     if (workspace_bytes < need || (need > 0 && !workspace))
         return fail(EB_ERR_INVALID, "eb_bucketize: workspace smaller than eb_bucketize_workspace reports");
     hipStream_t st = (hipStream_t)stream;
@@ -609,6 +613,7 @@ int eb_bucketize(int32_t T, int64_t B, int32_t G, const int64_t *bounds, const i
     ba.offsets = offsets;
     ba.out_offsets = out_offsets;
     ba.out_indices = out_indices;
+    ba.out_cap = out_capacity;
     ba.segments = segments;
     ba.nnz = nnz;
     ba.B = B;

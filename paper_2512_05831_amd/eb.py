@@ -55,7 +55,7 @@ def library() -> ctypes.CDLL:
         lib.eb_last_error.restype = ctypes.c_char_p
         lib.eb_bucketize_workspace.argtypes = [i32, i64, i32, ctypes.POINTER(ctypes.c_size_t)]
         lib.eb_bucketize_workspace.restype = ctypes.c_int
-        lib.eb_bucketize.argtypes = [i32, i64, i32, p, p, i64, p, p, p, p, p, ctypes.c_size_t, p]
+        lib.eb_bucketize.argtypes = [i32, i64, i32, p, p, i64, p, p, p, i64, p, p, ctypes.c_size_t, p]
         lib.eb_bucketize.restype = ctypes.c_int
         lib.eb_sum_partials.argtypes = [i32, p, i64, i32, i32, p, i64, p, p]
         lib.eb_sum_partials.restype = ctypes.c_int
@@ -122,11 +122,12 @@ def eb_bucketize_workspace(T: int, B: int, G: int) -> int:
 
 def eb_bucketize(T: int, B: int, G: int, bounds_ptr: int, indices_ptr: int | None, nnz: int,
                  offsets_ptr: int, out_offsets_ptr: int, out_indices_ptr: int | None,
-                 segments_ptr: int, workspace_ptr: int | None, workspace_bytes: int,
-                 stream_ptr: int | None) -> None:
+                 out_capacity: int, segments_ptr: int, workspace_ptr: int | None,
+                 workspace_bytes: int, stream_ptr: int | None) -> None:
     _check(library().eb_bucketize(T, B, G, bounds_ptr, indices_ptr or None, nnz, offsets_ptr,
-                                  out_offsets_ptr, out_indices_ptr or None, segments_ptr,
-                                  workspace_ptr or None, workspace_bytes, stream_ptr or None))
+                                  out_offsets_ptr, out_indices_ptr or None, out_capacity,
+                                  segments_ptr, workspace_ptr or None, workspace_bytes,
+                                  stream_ptr or None))
 
 
 def eb_sum_partials(G: int, partials_ptr: int, B: int, T: int, D: int,
@@ -136,10 +137,12 @@ def eb_sum_partials(G: int, partials_ptr: int, B: int, T: int, D: int,
                                      out_ptr, stream_ptr or None))
 
 
-def bucketize(bounds, indices, offsets, T: int, B: int, stream=None):
+def bucketize(bounds, indices, offsets, T: int, B: int, stream=None, capacity=None):
     """Torch convenience for eb_bucketize.  ``bounds``: int64 device [T, G+1].
-    Returns (out_offsets [G, T*B+1], out_indices [nnz], segments [G+1]) on the
-    device; the ids kept are out_indices[:segments[G]]."""
+    Returns (out_offsets [G, T*B+1], out_indices [capacity], segments [G+1],
+    workspace) on the device; ``capacity`` defaults to nnz (enough for
+    ordinary offsets).  The ids sent are out_indices[:segments[G]], of which
+    the first ``capacity`` are stored."""
     import torch
 
     dev = indices.device
@@ -150,14 +153,15 @@ def bucketize(bounds, indices, offsets, T: int, B: int, stream=None):
     if bounds.shape[0] != T or offsets.numel() != T * B + 1:
         raise ValueError("bounds must be [T, G+1] and offsets [T*B+1]")
     out_off = torch.empty((G, T * B + 1), dtype=torch.int64, device=dev)
-    out_idx = torch.empty(max(1, indices.numel()), dtype=torch.int64, device=dev)
+    cap = indices.numel() if capacity is None else int(capacity)
+    out_idx = torch.empty(max(1, cap), dtype=torch.int64, device=dev)
     seg = torch.empty(G + 1, dtype=torch.int64, device=dev)
     nbytes = eb_bucketize_workspace(T, B, G)
     ws = torch.empty(max(1, nbytes), dtype=torch.uint8, device=dev)
     if stream is None:
         stream = torch.cuda.current_stream(dev)
     eb_bucketize(T, B, G, bounds.data_ptr(), indices.data_ptr() if indices.numel() else None,
-                 indices.numel(), offsets.data_ptr(), out_off.data_ptr(), out_idx.data_ptr(),
+                 indices.numel(), offsets.data_ptr(), out_off.data_ptr(), out_idx.data_ptr(), cap,
                  seg.data_ptr(), ws.data_ptr(), nbytes, stream.cuda_stream)
     return out_off, out_idx, seg, ws
 

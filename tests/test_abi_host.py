@@ -222,8 +222,8 @@ def test_bucketize_workspace_sizes():
 
 def bucketize(**kw):
     args = dict(T=2, B=4, G=2, bounds_ptr=FAKE, indices_ptr=FAKE, nnz=10, offsets_ptr=FAKE,
-                out_offsets_ptr=FAKE, out_indices_ptr=FAKE, segments_ptr=FAKE, workspace_ptr=FAKE,
-                workspace_bytes=1 << 20, stream_ptr=None)
+                out_offsets_ptr=FAKE, out_indices_ptr=FAKE, out_capacity=10, segments_ptr=FAKE,
+                workspace_ptr=FAKE, workspace_bytes=1 << 20, stream_ptr=None)
     args.update(kw)
     return eb.eb_bucketize(**args)
 
@@ -232,7 +232,7 @@ def bucketize(**kw):
     dict(G=0), dict(T=-1), dict(B=-1), dict(nnz=-1), dict(segments_ptr=None),
     dict(out_offsets_ptr=None), dict(bounds_ptr=None), dict(offsets_ptr=None),
     dict(indices_ptr=None), dict(out_indices_ptr=None), dict(workspace_bytes=8),
-    dict(workspace_ptr=None),
+    dict(workspace_ptr=None), dict(out_capacity=-1),
 ])
 def test_bucketize_rejects(kw):
     assert code_of(lambda: bucketize(**kw)) == eb.EB_ERR_INVALID

@@ -22,14 +22,17 @@ def even_bounds(rows, G):
     return np.array([[g * r // G for g in range(G + 1)] for r in rows], dtype=np.int64)
 
 
-def run_bucketize(bounds, idx, off, T, B, device):
+def run_bucketize(bounds, idx, off, T, B, device, capacity=None):
+    """eb_bucketize on the device; out_indices has ``capacity`` entries
+    (default nnz).  Returns the stored ids: min(segments[G], capacity)."""
     d_b = torch.from_numpy(np.ascontiguousarray(bounds, dtype=np.int64)).to(device)
     d_i = torch.from_numpy(np.ascontiguousarray(idx, dtype=np.int64)).to(device)
     d_o = torch.from_numpy(np.ascontiguousarray(off, dtype=np.int64)).to(device)
-    out_off, out_idx, seg, ws = eb.bucketize(d_b, d_i, d_o, T, B)
+    cap = len(idx) if capacity is None else capacity
+    out_off, out_idx, seg, ws = eb.bucketize(d_b, d_i, d_o, T, B, capacity=cap)
     torch.cuda.synchronize()
     seg_h = seg.cpu().numpy()
-    return out_off.cpu().numpy(), out_idx.cpu().numpy()[:seg_h[-1]], seg_h
+    return out_off.cpu().numpy(), out_idx.cpu().numpy()[:min(int(seg_h[-1]), cap)], seg_h
 
 
 def bucket_case(seed, G, T=None, B=None, maxL=40, uneven=False, oob=True):
@@ -48,9 +51,10 @@ def bucket_case(seed, G, T=None, B=None, maxL=40, uneven=False, oob=True):
     return T, B, idx, off, bounds
 
 
-def check_bucketize(T, B, idx, off, bounds, device):
-    got = run_bucketize(bounds, idx, off, T, B, device)
-    want = oracle.bucketize(bounds, idx, off, T, B)
+def check_bucketize(T, B, idx, off, bounds, device, capacity=None):
+    cap = len(idx) if capacity is None else capacity
+    got = run_bucketize(bounds, idx, off, T, B, device, capacity=cap)
+    want = oracle.bucketize(bounds, idx, off, T, B, capacity=cap)
     for name, a, b in zip(("out_offsets", "out_indices", "segments"), got, want):
         assert np.array_equal(a, b), name
 
@@ -91,6 +95,25 @@ def test_bucketize_edge_cases(device):
     off = np.array([0, 3, 2, -4, 99], dtype=np.int64)
     bounds = np.array([[0, 0, 4, 4, 10]], dtype=np.int64)
     check_bucketize(1, 4, idx, off, bounds, device)
+
+
+@pytest.mark.parametrize("G", [3, 8, 40, 300])
+def test_bucketize_unordered_offsets(G, device):
+    """Offsets that go back and forth (bags overlap, some end before they
+    start): the kernels' bag-at-a-time paths, against the oracle."""
+    g = np.random.default_rng(G)
+    T, B = 3, 200
+    rows = [5000, 300, 70000]
+    nnz = 3000
+    off = g.integers(-20, nnz + 20, T * B + 1).astype(np.int64)
+    off[::7] = np.sort(off[::7])  # some stretches in order, most not
+    idx = g.integers(-5, 70005, nnz).astype(np.int64)
+    bounds = np.array([np.sort(g.integers(0, r + 1, G + 1)) for r in rows], dtype=np.int64)
+    total = int(oracle.bucketize(bounds, idx, off, T, B)[2][-1])
+    assert total > nnz  # overlapping bags send more ids than the batch holds
+    check_bucketize(T, B, idx, off, bounds, device, capacity=nnz)      # stores a prefix
+    check_bucketize(T, B, idx, off, bounds, device, capacity=total)    # room for all
+    check_bucketize(T, B, idx, off, bounds, device, capacity=total + 5)
 
 
 def test_bucketize_dlrm_batch(device):

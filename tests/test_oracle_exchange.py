@@ -104,6 +104,37 @@ def test_bucketize_matches_stable_sort(G, seed):
         assert np.array_equal(a, b)
 
 
+def overlapping_case(seed, G):
+    """Offsets that go back and forth: bags overlap, so an id position can be
+    sent by several bags and the total can exceed nnz."""
+    g = np.random.default_rng(seed)
+    T, B, nnz = 2, 30, 200
+    rows = [500, 90]
+    off = g.integers(-10, nnz + 10, T * B + 1).astype(np.int64)
+    idx = g.integers(-3, 503, nnz).astype(np.int64)
+    bounds = np.array([np.sort(g.integers(0, r + 1, G + 1)) for r in rows], dtype=np.int64)
+    return T, B, idx, off, bounds
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_bucketize_overlapping_bags_match_stable_sort(seed):
+    T, B, idx, off, bounds = overlapping_case(seed, 5)
+    got = oracle.bucketize(bounds, idx, off, T, B)
+    want = numpy_bucketize(bounds, idx, off, T, B)
+    assert want[2][-1] > idx.size  # the case really overflows nnz
+    for a, b in zip(got, want):
+        assert np.array_equal(a, b)
+
+
+@pytest.mark.parametrize("cap", [0, 1, 57, 200])
+def test_bucketize_capacity_keeps_a_prefix_and_the_full_counts(cap):
+    T, B, idx, off, bounds = overlapping_case(7, 3)
+    full_off, full_idx, full_seg = oracle.bucketize(bounds, idx, off, T, B)
+    off_c, idx_c, seg_c = oracle.bucketize(bounds, idx, off, T, B, capacity=cap)
+    assert np.array_equal(off_c, full_off) and np.array_equal(seg_c, full_seg)
+    assert np.array_equal(idx_c, full_idx[:cap])
+
+
 @pytest.mark.parametrize("seed", range(6))
 def test_bucketize_invariants(seed):
     G = 4

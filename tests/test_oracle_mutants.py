@@ -37,8 +37,10 @@ MUTANTS = {
     "bucketize_drop_last_index": ("for (int64_t k = s; k < e; ++k) {\n                    int64_t i = indices[k];\n                    if (i >= lo",
                                   "for (int64_t k = s; k + 1 < e; ++k) {\n                    int64_t i = indices[k];\n                    if (i >= lo"),
     "hits_once_per_bag": ("++hits;", "hits = 1;"),
-    "bucketize_hi_inclusive": ("if (i >= lo && i < hi) out_indices[pos++] = i;",
-                               "if (i >= lo && i <= hi) out_indices[pos++] = i;"),
+    "bucketize_hi_inclusive": ("if (i >= lo && i < hi) {\n                        if (pos < out_capacity)",
+                               "if (i >= lo && i <= hi) {\n                        if (pos < out_capacity)"),
+    "bucketize_capacity_stops_count": ("if (pos < out_capacity) out_indices[pos] = i;\n                        ++pos;",
+                                       "if (pos < out_capacity) out_indices[pos++] = i;"),
     "bucketize_absolute_offsets": ("out_offsets[(int64_t)g * (TB + 1) + p] = pos - segments[g];",
                                    "out_offsets[(int64_t)g * (TB + 1) + p] = pos;"),
     "partials_drop_last_source": ("for (int32_t s = 0; s < G; ++s) acc +=",
@@ -73,6 +75,8 @@ def pin_checks():
         checks.append((f"x_sort_{seed}", lambda s=seed: xpins.test_bucketize_matches_stable_sort(3, s)))
     for mode in (oracle.SUM, oracle.MEAN):
         checks.append((f"x_pipeline_{mode}", lambda m=mode: xpins.test_row_wise_pipeline_equals_unsharded(3, m)))
+    checks.append(("x_overlap", lambda: xpins.test_bucketize_overlapping_bags_match_stable_sort(0)))
+    checks.append(("x_capacity", lambda: xpins.test_bucketize_capacity_keeps_a_prefix_and_the_full_counts(57)))
     checks.append(("x_partials", xpins.test_sum_partials_against_numpy))
     checks.append(("x_partials_mean", xpins.test_sum_partials_mean_divides_by_bag_length))
     return checks
