@@ -45,10 +45,10 @@ def load_library(path: str) -> ctypes.CDLL:
     """Open an oracle build (the default one, or a test's own variant)."""
     lib = ctypes.CDLL(path)
     p, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
-    lib.oracle_eb_forward.argtypes = [i32, p, p, p, i32, i32, p, i64, p, i64, i32, i64, i64,
+    lib.oracle_eb_forward.argtypes = [i32, p, p, p, i32, i32, p, i64, p, p, i64, i32, i64, i64,
                                       p, p, p]
     lib.oracle_eb_forward.restype = ctypes.c_int
-    lib.oracle_eb_bags.argtypes = [i32, p, p, p, i32, i32, p, i64, p, i64, i32, i64, i64,
+    lib.oracle_eb_bags.argtypes = [i32, p, p, p, i32, i32, p, i64, p, p, i64, i32, i64, i64,
                                    i64, p, p, p, p]
     lib.oracle_eb_bags.restype = ctypes.c_int
     lib.oracle_decode.argtypes = [i32, p, i64, p]
@@ -108,22 +108,33 @@ def _prep(tables, rows, D, dtype, indices, offsets):
     return T, tabs, ptrs, stored, rows, indices, offsets
 
 
+def _weights(weights, nnz):
+    if weights is None:
+        return None, None
+    weights = np.ascontiguousarray(weights, dtype=np.float32)
+    if weights.size != nnz:
+        raise ValueError("weights must have one entry per index position")
+    return weights, weights.ctypes.data
+
+
 def forward(tables, rows, D, dtype, indices, offsets, B, mode=SUM, shard_lo=0,
-            shard_hi=np.iinfo(np.int64).max):
+            shard_hi=np.iinfo(np.int64).max, weights=None):
     """Pool every bag.  ``tables``: list of [stored_rows, D] arrays (float32, or
     uint16 bit patterns for fp16/bf16).  ``offsets``: int64 [T*B+1].
+    ``weights``: float32 [nnz] per-sample weights (sum pooling only) or None.
 
     Returns (out float64 [B, T*D], hits int32 [B, T], absmag float64 [B, T*D]).
     """
     T, tabs, ptrs, stored, rows, indices, offsets = _prep(tables, rows, D, dtype, indices, offsets)
     if offsets.size != T * B + 1:
         raise ValueError("offsets must have T*B+1 entries")
+    wts, wptr = _weights(weights, indices.size)
     out = np.zeros((B, T * D), dtype=np.float64)
     hits = np.zeros((B, T), dtype=np.int32)
     mag = np.zeros((B, T * D), dtype=np.float64)
     rc = _load().oracle_eb_forward(T, ptrs, stored.ctypes.data, rows.ctypes.data, D, dtype,
-                                   indices.ctypes.data, indices.size, offsets.ctypes.data, B,
-                                   mode, shard_lo, shard_hi, out.ctypes.data, hits.ctypes.data,
+                                   indices.ctypes.data, indices.size, offsets.ctypes.data, wptr,
+                                   B, mode, shard_lo, shard_hi, out.ctypes.data, hits.ctypes.data,
                                    mag.ctypes.data)
     if rc != 0:
         raise ValueError("oracle_eb_forward rejected its arguments")
@@ -131,7 +142,7 @@ def forward(tables, rows, D, dtype, indices, offsets, B, mode=SUM, shard_lo=0,
 
 
 def bags(tables, rows, D, dtype, indices, offsets, B, sel, mode=SUM, shard_lo=0,
-         shard_hi=np.iinfo(np.int64).max):
+         shard_hi=np.iinfo(np.int64).max, weights=None):
     """Pool only the bags ``sel`` (flat ids t*B+b).
 
     Returns (out float64 [n, D], hits int32 [n], absmag float64 [n, D]).
@@ -139,14 +150,15 @@ def bags(tables, rows, D, dtype, indices, offsets, B, sel, mode=SUM, shard_lo=0,
     T, tabs, ptrs, stored, rows, indices, offsets = _prep(tables, rows, D, dtype, indices, offsets)
     if offsets.size != T * B + 1:
         raise ValueError("offsets must have T*B+1 entries")
+    wts, wptr = _weights(weights, indices.size)
     sel = np.ascontiguousarray(sel, dtype=np.int64)
     n = sel.size
     out = np.zeros((n, D), dtype=np.float64)
     hits = np.zeros(n, dtype=np.int32)
     mag = np.zeros((n, D), dtype=np.float64)
     rc = _load().oracle_eb_bags(T, ptrs, stored.ctypes.data, rows.ctypes.data, D, dtype,
-                                indices.ctypes.data, indices.size, offsets.ctypes.data, B, mode,
-                                shard_lo, shard_hi, n, sel.ctypes.data, out.ctypes.data,
+                                indices.ctypes.data, indices.size, offsets.ctypes.data, wptr, B,
+                                mode, shard_lo, shard_hi, n, sel.ctypes.data, out.ctypes.data,
                                 hits.ctypes.data, mag.ctypes.data)
     if rc != 0:
         raise ValueError("oracle_eb_bags rejected its arguments")

@@ -22,6 +22,10 @@
  *   - Mean pooling is not in the paper; it is taken as the bag sum divided by
  *     the bag's full length (all its indices, gathered here or not), and an
  *     empty bag pools to zero.
+ *   - Per-sample weights are not in the paper either: with weights, sum
+ *     pooling adds weights[k] times the row of index position k (a weighted
+ *     sum, the usual extension of sum pooling); they are defined for sum
+ *     pooling only.
  *
  * The method reaches this result exactly up to rounding order, so the oracle
  * is the plain definition: a single-threaded loop, accumulating in double.
@@ -75,22 +79,25 @@ static double stored_value(const void *table, int32_t dtype, int64_t D, int64_t 
 }
 
 static int check_args(int32_t T, int32_t D, int32_t dtype, int64_t nnz, int64_t B, int32_t mode,
-                      int64_t shard_lo, int64_t shard_hi)
+                      int64_t shard_lo, int64_t shard_hi, const float *weights)
 {
     if (T < 0 || D <= 0 || nnz < 0 || B < 0) return -1;
     if (dtype != ORACLE_F32 && dtype != ORACLE_F16 && dtype != ORACLE_BF16) return -1;
     if (mode != ORACLE_SUM && mode != ORACLE_MEAN) return -1;
+    if (weights && mode != ORACLE_SUM) return -1;
     if (shard_lo < 0 || shard_hi < shard_lo) return -1;
     return 0;
 }
 
 /* Pool one bag (t, b) into acc[D] (and the magnitude sum[|w|] into mag[D] when
- * mag is not NULL).  Returns the hit count, or -1 if a local row falls
- * outside the stored rows the caller declared. */
+ * mag is not NULL), w being each pooled term: the stored value, times the
+ * position's weight when weights is not NULL (the product of two values of at
+ * most 24 significant bits is exact in double).  Returns the hit count, or -1
+ * if a local row falls outside the stored rows the caller declared. */
 static int64_t pool_bag(int32_t t, int64_t b, const void *const *tables, const int64_t *stored_rows,
                         const int64_t *rows, int32_t D, int32_t dtype, const int64_t *indices,
-                        int64_t nnz, const int64_t *offsets, int64_t B, int32_t mode,
-                        int64_t shard_lo, int64_t shard_hi, double *acc, double *mag)
+                        int64_t nnz, const int64_t *offsets, const float *weights, int64_t B,
+                        int32_t mode, int64_t shard_lo, int64_t shard_hi, double *acc, double *mag)
 {
     int64_t p = (int64_t)t * B + b;
     int64_t s = offsets[p], e = offsets[p + 1];
@@ -115,8 +122,9 @@ static int64_t pool_bag(int32_t t, int64_t b, const void *const *tables, const i
         int64_t r = i - shard_lo;
         if (r >= stored_rows[t]) return -1;
         ++hits;
+        double scale = weights ? (double)weights[k] : 1.0;
         for (int32_t c = 0; c < D; ++c) {
-            double w = stored_value(tables[t], dtype, D, r, c);
+            double w = scale * stored_value(tables[t], dtype, D, r, c);
             acc[c] += w;
             if (mag) mag[c] += fabs(w);
         }
@@ -131,24 +139,25 @@ static int64_t pool_bag(int32_t t, int64_t b, const void *const *tables, const i
 }
 
 /* Full forward.  out: [B, T*D] doubles, table t in columns [t*D, (t+1)*D).
+ * weights: [nnz] floats or NULL (sum pooling only).
  * hits: [B, T] or NULL.  absmag: [B, T*D] or NULL, receives the sum of the
  * absolute values that were pooled (divided by L for mean), the scale the
  * floating-point error of any summation order is measured against.
  * Returns 0, or -1 on invalid arguments. */
 int oracle_eb_forward(int32_t T, const void *const *tables, const int64_t *stored_rows,
                       const int64_t *rows, int32_t D, int32_t dtype, const int64_t *indices,
-                      int64_t nnz, const int64_t *offsets, int64_t B, int32_t mode,
-                      int64_t shard_lo, int64_t shard_hi, double *out, int32_t *hits,
-                      double *absmag)
+                      int64_t nnz, const int64_t *offsets, const float *weights, int64_t B,
+                      int32_t mode, int64_t shard_lo, int64_t shard_hi, double *out,
+                      int32_t *hits, double *absmag)
 {
-    if (check_args(T, D, dtype, nnz, B, mode, shard_lo, shard_hi)) return -1;
+    if (check_args(T, D, dtype, nnz, B, mode, shard_lo, shard_hi, weights)) return -1;
     int64_t width = (int64_t)T * D;
     for (int32_t t = 0; t < T; ++t) {
         for (int64_t b = 0; b < B; ++b) {
             double *acc = out + b * width + (int64_t)t * D;
             double *mag = absmag ? absmag + b * width + (int64_t)t * D : 0;
             int64_t h = pool_bag(t, b, tables, stored_rows, rows, D, dtype, indices, nnz, offsets,
-                                 B, mode, shard_lo, shard_hi, acc, mag);
+                                 weights, B, mode, shard_lo, shard_hi, acc, mag);
             if (h < 0) return -1;
             if (hits) hits[b * T + t] = (int32_t)h;
         }
@@ -160,17 +169,18 @@ int oracle_eb_forward(int32_t T, const void *const *tables, const int64_t *store
  * out / absmag: [nsel, D]; hits: [nsel] or NULL. */
 int oracle_eb_bags(int32_t T, const void *const *tables, const int64_t *stored_rows,
                    const int64_t *rows, int32_t D, int32_t dtype, const int64_t *indices,
-                   int64_t nnz, const int64_t *offsets, int64_t B, int32_t mode, int64_t shard_lo,
-                   int64_t shard_hi, int64_t nsel, const int64_t *sel, double *out, int32_t *hits,
-                   double *absmag)
+                   int64_t nnz, const int64_t *offsets, const float *weights, int64_t B,
+                   int32_t mode, int64_t shard_lo, int64_t shard_hi, int64_t nsel,
+                   const int64_t *sel, double *out, int32_t *hits, double *absmag)
 {
-    if (check_args(T, D, dtype, nnz, B, mode, shard_lo, shard_hi) || nsel < 0) return -1;
+    if (check_args(T, D, dtype, nnz, B, mode, shard_lo, shard_hi, weights) || nsel < 0) return -1;
     for (int64_t j = 0; j < nsel; ++j) {
         if (sel[j] < 0 || sel[j] >= (int64_t)T * B) return -1;
         int32_t t = (int32_t)(sel[j] / B);
         int64_t b = sel[j] % B;
-        int64_t h = pool_bag(t, b, tables, stored_rows, rows, D, dtype, indices, nnz, offsets, B,
-                             mode, shard_lo, shard_hi, out + j * D, absmag ? absmag + j * D : 0);
+        int64_t h = pool_bag(t, b, tables, stored_rows, rows, D, dtype, indices, nnz, offsets,
+                             weights, B, mode, shard_lo, shard_hi, out + j * D,
+                             absmag ? absmag + j * D : 0);
         if (h < 0) return -1;
         if (hits) hits[j] = (int32_t)h;
     }

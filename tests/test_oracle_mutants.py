@@ -16,6 +16,7 @@ import pytest
 import oracle
 import test_oracle_exchange as xpins
 import test_oracle_pins as pins
+import test_oracle_weights as wpins
 
 SRC = os.path.join(os.path.dirname(oracle.__file__), "eb_oracle.c")
 
@@ -34,6 +35,9 @@ MUTANTS = {
     "magnitude_without_abs": ("mag[c] += fabs(w);", "mag[c] += w;"),
     "bag_end_from_start": ("e = offsets[p + 1];\n    /* Offsets are clamped",
                            "e = offsets[p] + (offsets[p + 1] > offsets[p]);\n    /* Offsets are clamped"),
+    "weight_ignored": ("double scale = weights ? (double)weights[k] : 1.0;", "double scale = 1.0;"),
+    "weight_of_bag_start": ("double scale = weights ? (double)weights[k] : 1.0;",
+                            "double scale = weights ? (double)weights[s] : 1.0;"),
     "bucketize_drop_last_index": ("for (int64_t k = s; k < e; ++k) {\n                    int64_t i = indices[k];\n                    if (i >= lo",
                                   "for (int64_t k = s; k + 1 < e; ++k) {\n                    int64_t i = indices[k];\n                    if (i >= lo"),
     "hits_once_per_bag": ("++hits;", "hits = 1;"),
@@ -69,6 +73,10 @@ def pin_checks():
     checks.append(("empty", pins.test_empty_bags_pool_to_zero))
     checks.append(("malformed", pins.test_malformed_offsets))
     checks.append(("scipy", lambda: pins.test_scipy_csr_spmm(0)))
+    for seed in range(2):
+        checks.append((f"w_brute_{seed}", lambda s=seed: wpins.test_weighted_brute_force(oracle.F32, s)))
+    checks.append(("w_torch", lambda: wpins.test_torch_per_sample_weights(0)))
+    checks.append(("w_dup", wpins.test_integer_weights_are_duplicated_ids))
     checks.append(("x_example30", xpins.test_worked_example_two_gpus_thirty_rows))
     checks.append(("x_example20", xpins.test_worked_example_two_gpus_twenty_rows))
     for seed in range(3):
