@@ -42,7 +42,8 @@ from paper_2512_05831_amd import workloads as wl  # noqa: E402
 
 METRIC = "pooled lookups/sec + effective HBM GB/s (% of MI355X peak) per config"
 HBM_PEAK_GBPS = 8000.0
-KERNEL_SRC = os.path.join(ROOT, "paper_2512_05831_amd", "csrc", "eb.hip")
+# the gather kernel's source: its host side and the kernels themselves
+KERNEL_SRCS = [os.path.join(ROOT, "paper_2512_05831_amd", "csrc", f) for f in ("eb.hip", "eb_gather.h")]
 PROFILES = os.path.join(ROOT, "profiles")
 
 
@@ -51,14 +52,19 @@ def log(msg):
 
 
 def kernel_source_hash() -> str:
-    return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()[:16]
+    h = hashlib.sha256()
+    for path in KERNEL_SRCS:
+        h.update(open(path, "rb").read())
+    return h.hexdigest()[:16]
 
 
-def algorithmic_bytes(w, local_ids: int, nnz: int, with_hits: bool, index_bytes: int = 8) -> int:
-    """Every gathered row once, every id and offset (index_bytes each), the
-    fp32 output (and the int32 hit counts when written)."""
+def algorithmic_bytes(w, local_ids: int, nnz: int, with_hits: bool, index_bytes: int = 8,
+                      weighted: bool = False) -> int:
+    """Every gathered row once, every id and offset (index_bytes each), every
+    per-sample weight (4 bytes, when weighted), the fp32 output (and the int32
+    hit counts when written)."""
     b = (local_ids * w.D * w.elem_bytes + (nnz + w.T * w.B + 1) * index_bytes +
-         w.B * w.T * w.D * 4)
+         w.B * w.T * w.D * 4 + (nnz * 4 if weighted else 0))
     if with_hits:
         b += w.B * w.T * 4
     return int(b)
@@ -103,7 +109,7 @@ def host_cpu() -> str:
     return "unknown"
 
 
-def cpu_baseline(w, host_tables, batches, off, budget_s: float):
+def cpu_baseline(w, host_tables, batches, off, budget_s: float, weights=None):
     """The oracle over whole batches for about budget_s seconds, with the
     calling thread pinned to one core of those this process may use."""
     import oracle
@@ -117,8 +123,9 @@ def cpu_baseline(w, host_tables, batches, off, budget_s: float):
         t0 = time.perf_counter()
         while True:
             idx = batches[passes % len(batches)]
+            wts = None if weights is None else weights[passes % len(batches)]
             oracle.forward(host_tables, [w.rows] * w.T, w.D, w.dtype, idx, off, w.B, w.modes[0],
-                           w.shard_lo, w.shard_hi)
+                           w.shard_lo, w.shard_hi, weights=wts)
             lookups += idx.size
             passes += 1
             if time.perf_counter() - t0 >= budget_s:
@@ -411,6 +418,8 @@ def main():
                          "attainable bandwidth of a gather, uniform-id workloads)")
     ap.add_argument("--no-torch-baseline", dest="torch_baseline", action="store_false",
                     help="skip timing torch.nn.functional.embedding_bag on the same batches (context)")
+    ap.add_argument("--weights", action="store_true",
+                    help="pool a weighted sum with random per-sample weights (sum workloads)")
     ap.add_argument("--index-type", default="i64", choices=["i64", "i32"],
                     help="integer type of the ids and offsets handed to the library")
     ap.add_argument("--graph", action="store_true",
@@ -473,7 +482,14 @@ def main():
     d_idx = [torch.from_numpy(b).to(dev).to(idt) for b in batches]
     out = torch.empty((w.B, w.T * w.D), dtype=torch.float32, device=dev)
     hits = torch.empty((w.B, w.T), dtype=torch.int32, device=dev) if w.want_hits else None
-    calls = [et.prepare(i, d_off, w.B, call_mode, out, hits, stream) for i in d_idx]
+    d_wts = [None] * len(d_idx)
+    if args.weights:
+        if mode != wl.SUM:
+            raise SystemExit("per-sample weights need a sum-pooling workload")
+        gen = torch.Generator(device=dev).manual_seed(w.seed + 5)
+        d_wts = [torch.randn(i.numel(), generator=gen, device=dev) for i in d_idx]
+    calls = [et.prepare(i, d_off, w.B, call_mode, out, hits, stream, weights=wt)
+             for i, wt in zip(d_idx, d_wts)]
     local = [int(np.count_nonzero((b >= w.shard_lo) & (b < w.local_hi))) for b in batches]
     nnz = [int(b.size) for b in batches]
     torch.cuda.synchronize()
@@ -512,11 +528,11 @@ def main():
 
     steps_lookups = sum(nnz[i % len(nnz)] for i in range(K))
     steps_bytes = sum(algorithmic_bytes(w, local[i % len(local)], nnz[i % len(nnz)], hits is not None,
-                                        index_bytes) for i in range(K))
+                                        index_bytes, args.weights) for i in range(K))
     value = steps_lookups / (wall_ms / 1e3)
     achieved = steps_bytes / (region_ms / 1e3) / 1e9
     bytes_per_launch = steps_bytes / K
-    traffic = measured_traffic(w.name + ("-i32" if i32 else ""))
+    traffic = measured_traffic(w.name + ("-i32" if i32 else "") + ("-weighted" if args.weights else ""))
     log(f"bench: mean launch {launch_ms * 1e3:.1f} us over {K} back-to-back launches, "
         f"wall step {ms_per_step * 1e3:.1f} us, {achieved:.0f} GB/s algorithmic")
 
@@ -567,7 +583,8 @@ def main():
     cpu = None
     if not args.no_cpu_baseline:
         log("bench: timing the CPU oracle")
-        cpu = cpu_baseline(w, host_tables, batches, off, args.cpu_seconds)
+        host_wts = None if not args.weights else [x.cpu().numpy() for x in d_wts]
+        cpu = cpu_baseline(w, host_tables, batches, off, args.cpu_seconds, host_wts)
 
     line = {
         "metric": METRIC,
@@ -592,6 +609,7 @@ def main():
                    "mode": "sum" if mode == wl.SUM else "mean",
                    "rows_cache_policy": "stream" if stream_rows else "cached",
                    "index_type": "int32" if i32 else "int64",
+                   "per_sample_weights": bool(args.weights),
                    "index_batches_cycled": len(batches),
                    "launch": "hip graph replay" if args.graph else "eb_forward per step"},
         "bags_per_s": w.T * w.B / (ms_per_step / 1e3),

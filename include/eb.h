@@ -172,6 +172,11 @@ int eb_forward(const eb_tables *tables, int32_t T, const int64_t *rows, int32_t 
  *   tables ... B     as eb_forward, except:
  *   index_type       EB_IDX_I64: indices and offsets are device int64;
  *                    EB_IDX_I32: both are device int32.
+ *   weights          device fp32 [nnz] per-sample weights, or NULL.  With
+ *                    weights (EB_SUM only) position k of a bag adds
+ *                    weights[k] times its row: a weighted sum, the usual
+ *                    extension of sum pooling (not in the paper).  Hit
+ *                    counts still count gathered rows.
  *   mode, shard_lo, shard_hi
  *                    as eb_forward.
  *   out              device fp32 [B, ldo]: bag b of table t goes to
@@ -186,19 +191,20 @@ int eb_forward(const eb_tables *tables, int32_t T, const int64_t *rows, int32_t 
  *   ldh              hits row stride, >= T when hits is not NULL.
  *   stream           as eb_forward.
  *
- * eb_forward(...) is eb_forward_ex with EB_IDX_I64, ldo = T*D,
- * out_cols = NULL and ldh = T.  Rows take the 16-byte vector path only when
+ * eb_forward(...) is eb_forward_ex with EB_IDX_I64, weights = NULL,
+ * ldo = T*D, out_cols = NULL and ldh = T.  Rows take the 16-byte vector path only when
  * out, ldo and every out_cols[t] keep each output row 16-byte aligned; other
  * layouts are correct but slower.
  *
  * Errors: those of eb_forward, and EB_ERR_INVALID for an unknown index_type,
- * ldo < 1, a table's columns outside [0, ldo), overlapping tables, ldh < T
+ * weights with EB_MEAN, ldo < 1, a table's columns outside [0, ldo), overlapping tables, ldh < T
  * with hits, or B*ldo / B*ldh overflowing int64.
  */
 int eb_forward_ex(const eb_tables *tables, int32_t T, const int64_t *rows, int32_t D, int32_t dtype,
-                  int32_t index_type, const void *indices, int64_t nnz, const void *offsets, int64_t B,
-                  int32_t mode, int64_t shard_lo, int64_t shard_hi, float *out, int64_t ldo,
-                  const int64_t *out_cols, int32_t *hits, int64_t ldh, void *stream);
+                  int32_t index_type, const void *indices, int64_t nnz, const void *offsets,
+                  const float *weights, int64_t B, int32_t mode, int64_t shard_lo, int64_t shard_hi,
+                  float *out, int64_t ldo, const int64_t *out_cols, int32_t *hits, int64_t ldh,
+                  void *stream);
 
 /*
  * The row-wise exchange around the gather, one GPU's part (Sec. 4.2; the

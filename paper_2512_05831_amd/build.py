@@ -1,8 +1,9 @@
 """Build step: compile the HIP library for gfx950, in tree.
 
 ``python -m paper_2512_05831_amd.build`` (or ``build_library()``) runs hipcc on
-``csrc/eb.hip``, ``csrc/eb_exchange.hip`` and ``csrc/eb_ceiling.hip`` (the
-bandwidth probe the benchmark uses) and writes ``libeb.so`` next to this file.
+``csrc/eb.hip`` (with ``csrc/eb_gather.h``), ``csrc/eb_gather_weighted.hip``,
+``csrc/eb_exchange.hip`` and ``csrc/eb_ceiling.hip`` (the bandwidth probe the
+benchmark uses) and writes ``libeb.so`` next to this file.
 """
 from __future__ import annotations
 
@@ -12,7 +13,8 @@ import subprocess
 import sys
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-SRCS = [os.path.join(HERE, "csrc", f) for f in ("eb.hip", "eb_exchange.hip", "eb_ceiling.hip")]
+SRCS = [os.path.join(HERE, "csrc", f)
+        for f in ("eb.hip", "eb_gather_weighted.hip", "eb_exchange.hip", "eb_ceiling.hip")]
 LIB = os.path.join(HERE, "libeb.so")
 ARCH = "gfx950"
 

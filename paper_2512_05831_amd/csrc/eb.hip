@@ -50,363 +50,11 @@
 #include "../../include/eb.h"
 #include "eb_internal.h"
 
+#include "eb_gather.h"
+
 namespace {
 
-typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-
-constexpr int kWave = 64;
-constexpr int kWavesPerBlock = 4;
-constexpr int kBlock = kWave * kWavesPerBlock;
-constexpr int kXcds = 8;
-constexpr int kMaxTablesPerLaunch = 64;
-constexpr int kStagePerWave = 256;                // LDS index window, entries per wave
-constexpr uint32_t kInvalidRow = 0xFFFFFFFFu;     // staged marker: index not gathered here
-constexpr uint64_t kMaxLocalRows = 0xFFFFFFFEull; // local rows must fit below the marker
-
-// Per-launch arguments.  The table arrays are read with a block-uniform
-// index, so they stay in the kernel-argument segment (scalar loads).
-struct GatherArgs {
-    const char *base[kMaxTablesPerLaunch]; // stored table (local row 0 = global row shard_lo)
-    uint64_t nlocal[kMaxTablesPerLaunch];  // gatherable local rows of each table
-    int64_t col[kMaxTablesPerLaunch];      // output column of each table's first element
-    const void *indices;    // int64 or int32 (the kernel's index type)
-    const void *offsets;    // bag (t, b) of this launch at offsets[t*B + b]
-    float *out;             // element (b, t, c) at out[b*ldo + col[t] + c]
-    int32_t *hits;          // hits[b*ldh + t], or null
-    int64_t nnz;
-    int64_t B;
-    int64_t bag_begin;      // first bag (within each table) of this launch
-    int64_t shard_lo;
-    int64_t ldo;
-    int64_t ldh;
-    int32_t D;
-    int32_t row_bytes;      // D * element bytes
-    int32_t chunks;         // row_bytes / 16 (team kernel)
-    int32_t blocks_per_table;
-    int32_t nblocks;        // logical blocks; the grid is padded to a multiple of 8
-    int32_t mean;
-    int32_t xcd_runs;       // give each XCD a contiguous run of logical blocks
-};
-
-// ---------------------------------------------------------------------------- device helpers
-
-// Block id -> logical block such that XCD x (which receives hardware blocks
-// x, x+8, x+16, ...) works on logical blocks [x*per, (x+1)*per).
-__device__ __forceinline__ int xcd_contiguous_block(int bid, int padded)
-{
-    const int per = padded / kXcds;
-    return (bid % kXcds) * per + bid / kXcds;
-}
-
-// v + (v of lane ^ m), for the lane-group sizes the teams use.
-template <int M>
-__device__ __forceinline__ float add_xor(float v)
-{
-    static_assert(M == 1 || M == 2 || M == 4 || M == 8 || M == 16 || M == 32, "lane mask");
-    if constexpr (M == 1) {   // DPP quad_perm [1,0,3,2]
-        return v + __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xB1, 0xF, 0xF, false));
-    } else if constexpr (M == 2) { // DPP quad_perm [2,3,0,1]
-        return v + __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x4E, 0xF, 0xF, false));
-    } else if constexpr (M == 8) { // DPP row_ror:8 == xor 8 inside a 16-lane row
-        return v + __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x128, 0xF, 0xF, false));
-    } else if constexpr (M == 32) { // swap the two 32-lane halves
-        auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
-        return __uint_as_float(r[0]) + __uint_as_float(r[1]);
-    } else { // ds_swizzle bit mode: and 0x1f, xor M (within 32 lanes)
-        return v + __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(v), (M << 10) | 0x1F));
-    }
-}
-
-// Sum over the P lane groups of a team (groups are R lanes apart).
-template <int R, int P, int N>
-__device__ __forceinline__ void team_reduce(float (&acc)[N])
-{
-    if constexpr (P > 1) {
-#pragma unroll
-        for (int j = 0; j < N; ++j) acc[j] = add_xor<R>(acc[j]);
-        if constexpr (P > 2) team_reduce<R * 2, P / 2, N>(acc);
-    }
-}
-
-template <int R, int P>
-__device__ __forceinline__ int team_reduce_count(int v)
-{
-    if constexpr (P > 1) {
-        v += __builtin_amdgcn_ds_bpermute(((int)__lane_id() ^ R) << 2, v);
-        if constexpr (P > 2) v = team_reduce_count<R * 2, P / 2>(v);
-    }
-    return v;
-}
-
-// Elements per 16-byte chunk and their widening to fp32.
-template <int DT> struct Elem;
-template <> struct Elem<EB_F32> {
-    static constexpr int kPerChunk = 4;
-    __device__ static __forceinline__ void add(float *acc, uint4 v)
-    {
-        acc[0] += __uint_as_float(v.x);
-        acc[1] += __uint_as_float(v.y);
-        acc[2] += __uint_as_float(v.z);
-        acc[3] += __uint_as_float(v.w);
-    }
-    __device__ static __forceinline__ float load1(const char *p) { return *(const float *)p; }
-};
-template <> struct Elem<EB_F16> {
-    static constexpr int kPerChunk = 8;
-    __device__ static __forceinline__ float lo(uint32_t w) { return (float)__builtin_bit_cast(_Float16, (uint16_t)(w & 0xFFFFu)); }
-    __device__ static __forceinline__ float hi(uint32_t w) { return (float)__builtin_bit_cast(_Float16, (uint16_t)(w >> 16)); }
-    __device__ static __forceinline__ void add(float *acc, uint4 v)
-    {
-        acc[0] += lo(v.x); acc[1] += hi(v.x);
-        acc[2] += lo(v.y); acc[3] += hi(v.y);
-        acc[4] += lo(v.z); acc[5] += hi(v.z);
-        acc[6] += lo(v.w); acc[7] += hi(v.w);
-    }
-    __device__ static __forceinline__ float load1(const char *p) { return (float)*(const _Float16 *)p; }
-};
-template <> struct Elem<EB_BF16> {
-    static constexpr int kPerChunk = 8;
-    __device__ static __forceinline__ float lo(uint32_t w) { return __uint_as_float(w << 16); }
-    __device__ static __forceinline__ float hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
-    __device__ static __forceinline__ void add(float *acc, uint4 v)
-    {
-        acc[0] += lo(v.x); acc[1] += hi(v.x);
-        acc[2] += lo(v.y); acc[3] += hi(v.y);
-        acc[4] += lo(v.z); acc[5] += hi(v.z);
-        acc[6] += lo(v.w); acc[7] += hi(v.w);
-    }
-    __device__ static __forceinline__ float load1(const char *p) { return __uint_as_float((uint32_t)(*(const uint16_t *)p) << 16); }
-};
-
-// Row chunk load: default cache policy, or non-temporal (streamed past L2
-// and the last-level cache) when the caller hints that ids have no reuse.
-template <bool kStream>
-__device__ __forceinline__ uint4 load_chunk(const char *p)
-{
-    if constexpr (kStream) {
-        const u32x4 v = __builtin_nontemporal_load((const u32x4 *)p);
-        return make_uint4(v[0], v[1], v[2], v[3]);
-    } else {
-        return *(const uint4 *)p;
-    }
-}
-
-// Results, ids and offsets are touched once: non-temporal accesses.
-__device__ __forceinline__ void store_nt(float *p, float a, float b, float c, float d)
-{
-    const f32x4 v = {a, b, c, d};
-    __builtin_nontemporal_store(v, (f32x4 *)p);
-}
-
-__device__ __forceinline__ void clamp_bag(int64_t &s, int64_t &e, int64_t nnz)
-{
-    s = s < 0 ? 0 : (s > nnz ? nnz : s);
-    e = e > nnz ? nnz : e;
-    e = e < s ? s : e;
-}
-
-// ---------------------------------------------------------------------------- team gather kernel
-
-template <typename IT, int DT, int R, int P, int C, int U, bool kStream>
-__global__ __launch_bounds__(kBlock) void eb_gather_team(const GatherArgs a)
-{
-    constexpr int kTeam = R * P;
-    constexpr int kTeamsPerWave = kWave / kTeam;
-    constexpr int kStage = kStagePerWave / kTeamsPerWave; // window entries per team
-    constexpr int kEpc = Elem<DT>::kPerChunk;
-    static_assert(kTeam <= kWave && kWave % kTeam == 0, "team shape");
-    static_assert(kStage % kTeam == 0, "window shape");
-
-    __shared__ uint32_t stage[kWavesPerBlock * kStagePerWave];
-
-    const int lb = a.xcd_runs ? xcd_contiguous_block(blockIdx.x, gridDim.x) : (int)blockIdx.x;
-    if (lb >= a.nblocks) return;
-
-    const int lane = threadIdx.x & (kWave - 1);
-    const int wave = threadIdx.x / kWave;
-    const int team = lane / kTeam;
-    const int tl = lane % kTeam;
-    const int g = tl / R;  // lane group within the team
-    const int rl = tl % R; // lane within the row
-
-    const int t = lb / a.blocks_per_table;
-    const int64_t b = a.bag_begin +
-                      (int64_t)(lb - t * a.blocks_per_table) * (kTeamsPerWave * kWavesPerBlock) +
-                      wave * kTeamsPerWave + team;
-    const bool bag_ok = b < a.B;
-
-    int64_t s = 0, e = 0;
-    if (bag_ok) {
-        const IT *o = (const IT *)a.offsets + (int64_t)t * a.B + b;
-        s = __builtin_nontemporal_load(o);
-        e = __builtin_nontemporal_load(o + 1);
-        clamp_bag(s, e, a.nnz);
-    }
-
-    // Chunk c of a row goes to lane rl of a group when c*R + rl < chunks.
-    // Surplus lanes (rows whose chunk count is not R*C) re-read the last
-    // chunk, which the wave's other lanes fetch anyway, and never store.
-    int coff[C];
-#pragma unroll
-    for (int c = 0; c < C; ++c) coff[c] = 16 * min(c * R + rl, a.chunks - 1);
-    const char *base = a.base[t];
-    const size_t row_bytes = (size_t)a.row_bytes;
-    const uint64_t nlocal = a.nlocal[t];
-    const uint64_t shard_lo = (uint64_t)a.shard_lo;
-    uint32_t *my_stage = stage + wave * kStagePerWave + team * kStage;
-
-    float acc[C * kEpc];
-#pragma unroll
-    for (int j = 0; j < C * kEpc; ++j) acc[j] = 0.f;
-    int count = 0;
-
-    for (int64_t w0 = s; w0 < e; w0 += kStage) {
-        const int n = (int)((e - w0) < kStage ? (e - w0) : kStage);
-        // Stage: coalesced index loads, all issued before the first is
-        // used (positions past the window re-read its last entry), then
-        // rewritten as 32-bit local rows or the marker.
-        constexpr int kQ = kStage / kTeam;
-        const IT *src = (const IT *)a.indices + w0;
-        int64_t iv[kQ];
-#pragma unroll
-        for (int q = 0; q < kQ; ++q) {
-            const int k = q * kTeam + tl;
-            iv[q] = __builtin_nontemporal_load(src + (k < n ? k : n - 1));
-        }
-#pragma unroll
-        for (int q = 0; q < kQ; ++q) {
-            const int k = q * kTeam + tl;
-            const uint64_t r = (uint64_t)iv[q] - shard_lo;
-            if (k < n) my_stage[k] = r < nlocal ? (uint32_t)r : kInvalidRow;
-        }
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-        __builtin_amdgcn_wave_barrier();
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-
-        // Gather: group g pools window rows g, g+P, ...; U rows in flight.
-        int k = g;
-        for (; k + (U - 1) * P < n; k += U * P) {
-            uint32_t rr[U];
-#pragma unroll
-            for (int u = 0; u < U; ++u) rr[u] = my_stage[k + u * P];
-            uint4 v[U][C];
-#pragma unroll
-            for (int u = 0; u < U; ++u) {
-#pragma unroll
-                for (int c = 0; c < C; ++c) v[u][c] = make_uint4(0, 0, 0, 0);
-                if (rr[u] != kInvalidRow) {
-                    const char *p = base + (size_t)rr[u] * row_bytes;
-#pragma unroll
-                    for (int c = 0; c < C; ++c) v[u][c] = load_chunk<kStream>(p + coff[c]);
-                }
-            }
-#pragma unroll
-            for (int u = 0; u < U; ++u) {
-                count += rr[u] != kInvalidRow;
-#pragma unroll
-                for (int c = 0; c < C; ++c) Elem<DT>::add(acc + c * kEpc, v[u][c]);
-            }
-        }
-        for (; k < n; k += P) {
-            const uint32_t r = my_stage[k];
-            if (r != kInvalidRow) {
-                const char *p = base + (size_t)r * row_bytes;
-                uint4 v[C];
-#pragma unroll
-                for (int c = 0; c < C; ++c) v[c] = load_chunk<kStream>(p + coff[c]);
-                ++count;
-#pragma unroll
-                for (int c = 0; c < C; ++c) Elem<DT>::add(acc + c * kEpc, v[c]);
-            }
-        }
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-        __builtin_amdgcn_wave_barrier();
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    }
-
-    team_reduce<R, P>(acc);
-    count = team_reduce_count<R, P>(count);
-
-    if (bag_ok && g == 0) {
-        if (a.mean) {
-            const int64_t L = e - s;
-            const float fl = (float)L;
-#pragma unroll
-            for (int j = 0; j < C * kEpc; ++j) acc[j] = L > 0 ? acc[j] / fl : 0.f;
-        }
-        float *o = a.out + b * a.ldo + a.col[t];
-#pragma unroll
-        for (int c = 0; c < C; ++c) {
-            if (c * R + rl >= a.chunks) break;
-            float *dst = o + (size_t)(c * R + rl) * kEpc;
-#pragma unroll
-            for (int h = 0; h < kEpc / 4; ++h)
-                store_nt(dst + 4 * h, acc[c * kEpc + 4 * h], acc[c * kEpc + 4 * h + 1],
-                         acc[c * kEpc + 4 * h + 2], acc[c * kEpc + 4 * h + 3]);
-        }
-        if (a.hits && rl == 0) a.hits[b * a.ldh + t] = count;
-    }
-}
-
-// ---------------------------------------------------------------------------- plain kernel
-
-// One wave per bag, lanes striding over the columns; any D, any alignment.
-template <typename IT, int DT>
-__global__ __launch_bounds__(kBlock) void eb_gather_plain(const GatherArgs a)
-{
-    constexpr int kEs = DT == EB_F32 ? 4 : 2;
-    constexpr int kCols = 4; // columns per lane per pass
-    const int lb = blockIdx.x;
-    if (lb >= a.nblocks) return;
-    const int lane = threadIdx.x & (kWave - 1);
-    const int wave = threadIdx.x / kWave;
-    const int t = lb / a.blocks_per_table;
-    const int64_t b = a.bag_begin + (int64_t)(lb - t * a.blocks_per_table) * kWavesPerBlock + wave;
-    if (b >= a.B) return;
-
-    int64_t s, e;
-    {
-        const IT *o = (const IT *)a.offsets + (int64_t)t * a.B + b;
-        s = o[0];
-        e = o[1];
-        clamp_bag(s, e, a.nnz);
-    }
-    const char *base = a.base[t];
-    const uint64_t nlocal = a.nlocal[t];
-    const uint64_t shard_lo = (uint64_t)a.shard_lo;
-    const int D = a.D;
-    const size_t pitch = (size_t)D * kEs;
-    float *o = a.out + b * a.ldo + a.col[t];
-    int count = 0;
-
-    for (int c0 = 0; c0 < D; c0 += kWave * kCols) {
-        float acc[kCols];
-#pragma unroll
-        for (int j = 0; j < kCols; ++j) acc[j] = 0.f;
-        for (int64_t k = s; k < e; ++k) {
-            const uint64_t r = (uint64_t)(int64_t)((const IT *)a.indices)[k] - shard_lo;
-            if (r >= nlocal) continue;
-            if (c0 == 0) ++count;
-            const char *p = base + r * pitch;
-#pragma unroll
-            for (int j = 0; j < kCols; ++j) {
-                const int c = c0 + j * kWave + lane;
-                if (c < D) acc[j] += Elem<DT>::load1(p + (size_t)c * kEs);
-            }
-        }
-#pragma unroll
-        for (int j = 0; j < kCols; ++j) {
-            const int c = c0 + j * kWave + lane;
-            if (c < D) {
-                float v = acc[j];
-                if (a.mean) v = (e > s) ? v / (float)(e - s) : 0.f;
-                o[c] = v;
-            }
-        }
-    }
-    if (a.hits && lane == 0) a.hits[b * a.ldh + t] = count;
-}
+using namespace eb_gather;
 
 // ---------------------------------------------------------------------------- host side
 
@@ -435,15 +83,6 @@ int rows_in_flight_per_bag(const Shape &s, bool stream)
     return s.P * u;
 }
 
-// Lane groups per bag; the kernels' template arguments follow the same rule.
-constexpr int groups_per_bag(int R, bool few, bool single)
-{
-    // Wide rows or small batches: one bag per wave.  Otherwise narrow rows
-    // get 16-lane teams (4 bags per wave), so the group reduction stays
-    // inside a DPP row.  "single": rows of 16 or 32 lanes with one lane group
-    // per bag (two bags per wave), used for streamed rows of large batches.
-    return few ? kWave / R : (single && R >= 16 && R < kWave) ? kWave / R / 2 : R >= 16 ? kWave / R : 16 / R;
-}
 
 Shape team_shape(int rb, bool few, bool single)
 {
@@ -455,81 +94,6 @@ Shape team_shape(int rb, bool few, bool single)
     s.P = groups_per_bag(s.R, few, single);
     return s;
 }
-
-using KernelFn = void (*)(GatherArgs);
-
-// Rows in flight per lane: streamed (non-temporal) rows of 128 B and more all
-// go to HBM, where two per lane saturate the random-read rate and more only
-// queue; narrower rows need more requests per byte in flight, and cached rows
-// profit from deeper overlap while hits return early.  A small batch (fewer
-// bags than fill the GPU) is bound by each bag's chain of dependent loads
-// instead: every bag then gets a whole wave and 6 rows in flight per lane.
-template <typename IT, int DT, int R, int C, bool kFew>
-KernelFn team_kernel(bool stream, bool single)
-{
-    constexpr int P = groups_per_bag(R, kFew, false);
-    constexpr int P_SINGLE = groups_per_bag(R, kFew, true);
-    constexpr int U_CACHED = C >= 6 ? 1 : 6 / C;
-    constexpr int U_STREAM = (!kFew && R * C >= 8) ? (C >= 2 ? 1 : 2) : U_CACHED;
-    if (!stream) return eb_gather_team<IT, DT, R, P, C, U_CACHED, false>;
-    if constexpr (P_SINGLE != P) {
-        if (single) return eb_gather_team<IT, DT, R, P_SINGLE, C, U_STREAM, true>;
-    }
-    return eb_gather_team<IT, DT, R, P, C, U_STREAM, true>;
-}
-
-template <typename IT, int DT, int R, int C>
-KernelFn team_kernel(bool stream, bool few, bool single)
-{
-    return few ? team_kernel<IT, DT, R, C, true>(stream, false) : team_kernel<IT, DT, R, C, false>(stream, single);
-}
-
-template <typename IT, int DT>
-KernelFn pick_team_kernel(int R, int C, bool stream, bool few, bool single)
-{
-    switch (R) {
-    case 1: return team_kernel<IT, DT, 1, 1>(stream, few, single);
-    case 2: return team_kernel<IT, DT, 2, 1>(stream, few, single);
-    case 4: return team_kernel<IT, DT, 4, 1>(stream, few, single);
-    case 8: return team_kernel<IT, DT, 8, 1>(stream, few, single);
-    case 16: return team_kernel<IT, DT, 16, 1>(stream, few, single);
-    case 32: return team_kernel<IT, DT, 32, 1>(stream, few, single);
-    default:
-        switch (C) {
-        case 1: return team_kernel<IT, DT, 64, 1>(stream, few, single);
-        case 2: return team_kernel<IT, DT, 64, 2>(stream, few, single);
-        case 3: return team_kernel<IT, DT, 64, 3>(stream, few, single);
-        case 4: return team_kernel<IT, DT, 64, 4>(stream, few, single);
-        case 5: return team_kernel<IT, DT, 64, 5>(stream, few, single);
-        case 6: return team_kernel<IT, DT, 64, 6>(stream, few, single);
-        case 7: return team_kernel<IT, DT, 64, 7>(stream, few, single);
-        case 8: return team_kernel<IT, DT, 64, 8>(stream, few, single);
-        }
-    }
-    return nullptr;
-}
-
-template <typename IT>
-KernelFn pick_team_kernel(int dtype, int R, int C, bool stream, bool few, bool single)
-{
-    switch (dtype) {
-    case EB_F32: return pick_team_kernel<IT, EB_F32>(R, C, stream, few, single);
-    case EB_F16: return pick_team_kernel<IT, EB_F16>(R, C, stream, few, single);
-    default: return pick_team_kernel<IT, EB_BF16>(R, C, stream, few, single);
-    }
-}
-
-template <typename IT>
-KernelFn pick_plain_kernel(int dtype)
-{
-    switch (dtype) {
-    case EB_F32: return eb_gather_plain<IT, EB_F32>;
-    case EB_F16: return eb_gather_plain<IT, EB_F16>;
-    default: return eb_gather_plain<IT, EB_BF16>;
-    }
-}
-
-int elem_bytes(int dtype) { return dtype == EB_F32 ? 4 : 2; }
 
 } // namespace
 
@@ -553,7 +117,7 @@ namespace {
 // Both forward entry points.  out_cols == nullptr means table t at column t*D.
 int forward_impl(const char *who, const eb_tables *h, int32_t T, const int64_t *rows, int32_t D,
                  int32_t dtype, int32_t index_type, const void *indices, int64_t nnz, const void *offsets,
-                 int64_t B, int32_t mode, int64_t shard_lo, int64_t shard_hi, float *out, int64_t ldo,
+                 const float *weights, int64_t B, int32_t mode, int64_t shard_lo, int64_t shard_hi, float *out, int64_t ldo,
                  const int64_t *out_cols, int32_t *hits, int64_t ldh, void *stream)
 {
     const std::string fn_name(who);
@@ -572,6 +136,7 @@ int forward_impl(const char *who, const eb_tables *h, int32_t T, const int64_t *
     if (T == 0 || B == 0) return EB_OK;
     if (!offsets || !out) return invalid("NULL offsets or out");
     if (nnz > 0 && !indices) return invalid("NULL indices with nnz > 0");
+    if (weights && pool != EB_SUM) return invalid("per-sample weights need sum pooling");
     const int64_t kMax = std::numeric_limits<int64_t>::max();
     if (B > kMax / T || B * T > kMax / D) return invalid("B*T*D overflows");
 
@@ -631,15 +196,16 @@ int forward_impl(const char *who, const eb_tables *h, int32_t T, const int64_t *
         const bool single = stream && !few && halved.P != normal.P &&
                             bags / (kWave / (halved.R * halved.P)) >= kWaveSlots / 2;
         const Shape sh = few ? team_shape((int)rb, true, false) : single ? halved : normal;
-        fn = i32 ? pick_team_kernel<int32_t>(dtype, sh.R, sh.C, stream, few, single)
-                 : pick_team_kernel<int64_t>(dtype, sh.R, sh.C, stream, few, single);
+        fn = weights ? pick_weighted_kernel(i32, dtype, true, sh.R, sh.C, stream, few, single)
+                     : pick_kernel<false>(i32, dtype, true, sh.R, sh.C, stream, few, single);
         bags_per_block = (kWave / (sh.R * sh.P)) * kWavesPerBlock;
         // No reuse: each XCD takes a contiguous run of bags.  Otherwise
         // hardware order, so all XCDs work on the same table at once and its
         // hot rows share the last-level cache.
         xcd_remap = (mode & EB_HINT_STREAM_ROWS) != 0;
     } else {
-        fn = i32 ? pick_plain_kernel<int32_t>(dtype) : pick_plain_kernel<int64_t>(dtype);
+        fn = weights ? pick_weighted_kernel(i32, dtype, false, 0, 0, false, false, false)
+                     : pick_kernel<false>(i32, dtype, false, 0, 0, false, false, false);
     }
     if (!fn) return fail(EB_ERR_UNSUPPORTED, fn_name + ": no kernel for this row shape");
 
@@ -649,6 +215,7 @@ int forward_impl(const char *who, const eb_tables *h, int32_t T, const int64_t *
     GatherArgs a;
     std::memset(&a, 0, sizeof a);
     a.indices = indices;
+    a.weights = weights;
     a.nnz = nnz;
     a.B = B;
     a.shard_lo = shard_lo;
@@ -736,17 +303,18 @@ int eb_forward(const eb_tables *h, int32_t T, const int64_t *rows, int32_t D, in
                int64_t shard_lo, int64_t shard_hi, float *out, int32_t *hits, void *stream)
 {
     const int64_t ldo = (T > 0 && D > 0) ? (int64_t)T * D : 0; // overflow is caught below
-    return forward_impl("eb_forward", h, T, rows, D, dtype, EB_IDX_I64, indices, nnz, offsets, B, mode,
-                        shard_lo, shard_hi, out, ldo, nullptr, hits, T, stream);
+    return forward_impl("eb_forward", h, T, rows, D, dtype, EB_IDX_I64, indices, nnz, offsets, nullptr, B,
+                        mode, shard_lo, shard_hi, out, ldo, nullptr, hits, T, stream);
 }
 
 int eb_forward_ex(const eb_tables *h, int32_t T, const int64_t *rows, int32_t D, int32_t dtype,
-                  int32_t index_type, const void *indices, int64_t nnz, const void *offsets, int64_t B,
-                  int32_t mode, int64_t shard_lo, int64_t shard_hi, float *out, int64_t ldo,
-                  const int64_t *out_cols, int32_t *hits, int64_t ldh, void *stream)
+                  int32_t index_type, const void *indices, int64_t nnz, const void *offsets,
+                  const float *weights, int64_t B, int32_t mode, int64_t shard_lo, int64_t shard_hi,
+                  float *out, int64_t ldo, const int64_t *out_cols, int32_t *hits, int64_t ldh,
+                  void *stream)
 {
-    return forward_impl("eb_forward_ex", h, T, rows, D, dtype, index_type, indices, nnz, offsets, B, mode,
-                        shard_lo, shard_hi, out, ldo, out_cols, hits, ldh, stream);
+    return forward_impl("eb_forward_ex", h, T, rows, D, dtype, index_type, indices, nnz, offsets, weights,
+                        B, mode, shard_lo, shard_hi, out, ldo, out_cols, hits, ldh, stream);
 }
 
 } // extern "C"

@@ -46,8 +46,8 @@ def library() -> ctypes.CDLL:
         lib.eb_create_tables.restype = ctypes.c_int
         lib.eb_forward.argtypes = [p, i32, p, i32, i32, p, i64, p, i64, i32, i64, i64, p, p, p]
         lib.eb_forward.restype = ctypes.c_int
-        lib.eb_forward_ex.argtypes = [p, i32, p, i32, i32, i32, p, i64, p, i64, i32, i64, i64, p,
-                                      i64, p, p, i64, p]
+        lib.eb_forward_ex.argtypes = [p, i32, p, i32, i32, i32, p, i64, p, p, i64, i32, i64, i64,
+                                      p, i64, p, p, i64, p]
         lib.eb_forward_ex.restype = ctypes.c_int
         lib.eb_destroy.argtypes = [p]
         lib.eb_destroy.restype = None
@@ -99,15 +99,17 @@ def eb_forward(handle, T: int, rows, D: int, dtype: int, indices_ptr: int, nnz: 
 
 
 def eb_forward_ex(handle, T: int, rows, D: int, dtype: int, index_type: int, indices_ptr: int,
-                  nnz: int, offsets_ptr: int, B: int, mode: int, shard_lo: int, shard_hi: int,
-                  out_ptr: int, ldo: int, out_cols, hits_ptr: int | None, ldh: int,
-                  stream_ptr: int | None) -> None:
-    """eb_forward with an index width and an output layout (``out_cols``: a
-    list of T columns, or None for t*D).  Raises EbError."""
+                  nnz: int, offsets_ptr: int, weights_ptr: int | None, B: int, mode: int,
+                  shard_lo: int, shard_hi: int, out_ptr: int, ldo: int, out_cols,
+                  hits_ptr: int | None, ldh: int, stream_ptr: int | None) -> None:
+    """eb_forward with an index width, optional per-sample weights and an
+    output layout (``out_cols``: a list of T columns, or None for t*D).
+    Raises EbError."""
     cols = None if out_cols is None else _i64_array(out_cols)
     _check(library().eb_forward_ex(handle, T, _i64_array(rows), D, dtype, index_type, indices_ptr,
-                                   nnz, offsets_ptr, B, mode, shard_lo, shard_hi, out_ptr, ldo,
-                                   cols, hits_ptr or None, ldh, stream_ptr or None))
+                                   nnz, offsets_ptr, weights_ptr or None, B, mode, shard_lo,
+                                   shard_hi, out_ptr, ldo, cols, hits_ptr or None, ldh,
+                                   stream_ptr or None))
 
 
 def eb_destroy(handle) -> None:
@@ -257,12 +259,14 @@ class EmbeddingBagTables:
         return (out, hits) if want_hits else out
 
     def forward_ex(self, indices, offsets, B: int, mode: int = EB_SUM, out=None, out_cols=None,
-                   hits=None, stream=None):
+                   hits=None, stream=None, weights=None):
         """eb_forward_ex.  indices / offsets: contiguous device int64 or int32
         (the same for both).  ``out``: fp32 [B, W] with unit column stride (a
         view such as a column slice is fine; ldo = out.stride(0)); table t goes
         to columns [out_cols[t], out_cols[t] + D) of it (default t*D).
-        ``hits``: int32 [B, >= T] with unit column stride, or None."""
+        ``hits``: int32 [B, >= T] with unit column stride, or None.
+        ``weights``: contiguous device fp32 [nnz] per-sample weights (sum
+        pooling), or None."""
         import torch
 
         dev = self.tables[0].device
@@ -282,19 +286,25 @@ class EmbeddingBagTables:
             raise ValueError("out_cols must give T columns with c + D <= out.shape[1]")
         if hits is not None and hits.shape[1] < self.T:
             raise ValueError("hits must be int32 [B, >= T]")
+        if weights is not None and (weights.dtype != torch.float32 or not weights.is_contiguous() or
+                                    weights.numel() != indices.numel()):
+            raise ValueError("weights must be contiguous fp32 with one entry per index")
         if stream is None:
             stream = torch.cuda.current_stream(dev)
         ldo = out.stride(0) if B > 1 else out.shape[1]
         ldh = (hits.stride(0) if B > 1 else hits.shape[1]) if hits is not None else 0
         eb_forward_ex(self.handle, self.T, self.rows, self.D, self.dtype, itype, indices.data_ptr(),
-                      indices.numel(), offsets.data_ptr(), B, mode, self.shard_lo, self.shard_hi,
+                      indices.numel(), offsets.data_ptr(),
+                      weights.data_ptr() if weights is not None and weights.numel() else None,
+                      B, mode, self.shard_lo, self.shard_hi,
                       out.data_ptr(), ldo, cols,
                       hits.data_ptr() if hits is not None else None, ldh, stream.cuda_stream)
         return (out, hits) if hits is not None else out
 
-    def prepare(self, indices, offsets, B: int, mode: int, out, hits=None, stream=None):
-        """Marshal the arguments of one eb_forward call once; the returned
-        function enqueues that call (on ``stream``) each time it is invoked."""
+    def prepare(self, indices, offsets, B: int, mode: int, out, hits=None, stream=None, weights=None):
+        """Marshal the arguments of one eb_forward call (eb_forward_ex for
+        int32 ids or weights) once; the returned function enqueues that call
+        (on ``stream``) each time it is invoked."""
         import torch
 
         if stream is None:
@@ -304,7 +314,7 @@ class EmbeddingBagTables:
         lib = library()
         itype = _index_type(indices, offsets)
         hits_ptr = hits.data_ptr() if hits is not None else None
-        if itype == EB_IDX_I64:
+        if itype == EB_IDX_I64 and weights is None:
             fn = lib.eb_forward
             args = (self.handle, self.T, _i64_array(self.rows), self.D, self.dtype,
                     indices.data_ptr(), indices.numel(), offsets.data_ptr(), B, mode, self.shard_lo,
@@ -312,10 +322,11 @@ class EmbeddingBagTables:
         else:
             fn = lib.eb_forward_ex
             args = (self.handle, self.T, _i64_array(self.rows), self.D, self.dtype, itype,
-                    indices.data_ptr(), indices.numel(), offsets.data_ptr(), B, mode, self.shard_lo,
+                    indices.data_ptr(), indices.numel(), offsets.data_ptr(),
+                    weights.data_ptr() if weights is not None else None, B, mode, self.shard_lo,
                     self.shard_hi, out.data_ptr(), self.T * self.D, None, hits_ptr, self.T,
                     stream.cuda_stream)
-        keep = (indices, offsets, out, hits)
+        keep = (indices, offsets, out, hits, weights)
 
         def call():
             _check(fn(*args))

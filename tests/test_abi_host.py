@@ -166,7 +166,8 @@ def test_error_message_is_per_failure():
 
 def forward_ex(h, **kw):
     args = dict(T=2, rows=[100, 100], D=16, dtype=eb.EB_F32, index_type=eb.EB_IDX_I32,
-                indices_ptr=FAKE, nnz=10, offsets_ptr=FAKE, B=4, mode=eb.EB_SUM, shard_lo=0,
+                indices_ptr=FAKE, nnz=10, offsets_ptr=FAKE, weights_ptr=None, B=4, mode=eb.EB_SUM,
+                shard_lo=0,
                 shard_hi=I64MAX, out_ptr=FAKE, ldo=40, out_cols=[0, 20], hits_ptr=None, ldh=0,
                 stream_ptr=None)
     args.update(kw)
@@ -185,6 +186,8 @@ def forward_ex(h, **kw):
     dict(B=1 << 60, ldo=1 << 10),      # B * ldo overflows
     dict(hits_ptr=FAKE, ldh=1 << 61, B=8),
     dict(D=8), dict(mode=3), dict(shard_lo=5, shard_hi=4), dict(offsets_ptr=None),
+    dict(weights_ptr=FAKE, mode=eb.EB_MEAN),            # weights are for sum pooling
+    dict(weights_ptr=FAKE, mode=eb.EB_MEAN | eb.EB_HINT_STREAM_ROWS),
 ])
 def test_forward_ex_rejects(kw):
     h = handle()

@@ -1,6 +1,6 @@
-"""GPU parity of eb_forward_ex: int32 ids and offsets, and output layouts for
-column-wise and table-wise shards (Sec. 4.1's other two schemes) and for
-strided outputs.
+"""GPU parity of eb_forward_ex: int32 ids and offsets, per-sample weights, and
+output layouts for column-wise and table-wise shards (Sec. 4.1's other two
+schemes) and for strided outputs.
 
 int32 inputs are the same integers as int64 ones, so the int32 path must give
 the int64 path's output bit for bit (the kernels differ only in the width of
@@ -38,7 +38,7 @@ def dev(a, np_dtype, device):
 
 
 def run_ex(dev_tables, rows, idx, off, B, mode, device, index_dtype=np.int32, lo=0,
-           hi=wl.INT64_MAX, out=None, out_cols=None, hits=True):
+           hi=wl.INT64_MAX, out=None, out_cols=None, hits=True, weights=None):
     """One eb_forward_ex; returns (out tensor, hits tensor or None)."""
     et = eb.EmbeddingBagTables(dev_tables, rows=rows, shard_lo=lo, shard_hi=hi)
     T, D = et.T, et.D
@@ -46,7 +46,8 @@ def run_ex(dev_tables, rows, idx, off, B, mode, device, index_dtype=np.int32, lo
         out = torch.full((B, T * D), float("nan"), dtype=torch.float32, device=device)
     h = torch.full((B, T), -7, dtype=torch.int32, device=device) if hits else None
     d_idx, d_off = dev(idx, index_dtype, device), dev(off, index_dtype, device)
-    et.forward_ex(d_idx, d_off, B, mode=mode, out=out, out_cols=out_cols, hits=h)
+    d_w = None if weights is None else dev(weights, np.float32, device)
+    et.forward_ex(d_idx, d_off, B, mode=mode, out=out, out_cols=out_cols, hits=h, weights=d_w)
     torch.cuda.synchronize()
     et.close()
     return out, h
@@ -232,3 +233,74 @@ def test_more_tables_than_one_launch_reversed_columns(device):
     got = out.cpu().numpy().reshape(B, T, D)[:, ::-1, :].reshape(B, T * D)
     assert same_bits(np.ascontiguousarray(got), want)
     assert np.array_equal(hits.cpu().numpy(), want_hits)
+
+
+# ----------------------------------------------------------------------------- per-sample weights
+
+
+def weighted_case(D, dtype, seed, B=37, maxL=70, lo=0, hi=wl.INT64_MAX, values="normal", T=3):
+    tables, rows, idx, off = make_case(T=T, D=D, dtype=dtype, B=B, maxL=maxL, lo=lo, hi=hi,
+                                       seed=seed, values=values)
+    w = np.random.default_rng(seed + 1).standard_normal(idx.size).astype(np.float32)
+    return tables, rows, idx, off, w
+
+
+@pytest.mark.parametrize("dtype", DT)
+@pytest.mark.parametrize("D", [1, 4, 7, 12, 16, 64, 100, 128, 256, 1024])
+@pytest.mark.parametrize("itype", [np.int64, np.int32])
+def test_weighted_sum_matches_oracle(dtype, D, itype, device):
+    lo, hi = (500, 2600) if D % 2 else (0, wl.INT64_MAX)
+    tables, rows, idx, off, w = weighted_case(D, dtype, D + 7 * dtype, lo=lo, hi=hi)
+    dts = [to_device_table(t, dtype, device) for t in tables]
+    got, hits = run_ex(dts, rows, idx, off, 37, wl.SUM, device, index_dtype=itype, lo=lo, hi=hi,
+                       weights=w)
+    ref, ref_hits, mag = oracle.forward(tables, rows, D, dtype, idx, off, 37, wl.SUM, lo, hi, weights=w)
+    assert_parity(got.cpu().numpy(), ref, mag, max_bag_len(off, idx.size), dtype,
+                  hits.cpu().numpy(), ref_hits)
+
+
+@pytest.mark.parametrize("hint", [0, eb.EB_HINT_STREAM_ROWS])
+@pytest.mark.parametrize("B", [8, 1500, 3000])  # small-batch, normal and two-bags-per-wave mappings
+def test_weighted_mappings(hint, B, device):
+    maxL = 1200 if B == 8 else 24
+    tables, rows, idx, off, w = weighted_case(128, wl.F32, 40 + B, B=B, maxL=maxL, T=2)
+    dts = [to_device_table(t, wl.F32, device) for t in tables]
+    got, hits = run_ex(dts, rows, idx, off, B, wl.SUM | hint, device, weights=w)
+    ref, ref_hits, mag = oracle.forward(tables, rows, 128, wl.F32, idx, off, B, wl.SUM, weights=w)
+    assert_parity(got.cpu().numpy(), ref, mag, max_bag_len(off, idx.size), wl.F32,
+                  hits.cpu().numpy(), ref_hits)
+
+
+def test_weighted_dyadic_exact_and_unit_weights(device):
+    """Dyadic rows and weights make every product and sum exact; unit weights
+    give the unweighted kernel's output bit for bit."""
+    for dtype, D in ((wl.F32, 64), (wl.F16, 256), (wl.BF16, 24)):
+        tables, rows, idx, off, _ = weighted_case(D, dtype, 3, values="dyadic", maxL=40)
+        w = (np.random.default_rng(5).integers(-8, 9, idx.size) / 4.0).astype(np.float32)
+        dts = [to_device_table(t, dtype, device) for t in tables]
+        got, _ = run_ex(dts, rows, idx, off, 37, wl.SUM, device, weights=w)
+        ref, _, _ = oracle.forward(tables, rows, D, dtype, idx, off, 37, wl.SUM, weights=w)
+        assert np.array_equal(got.cpu().numpy().astype(np.float64), ref)
+        ones, _ = run_ex(dts, rows, idx, off, 37, wl.SUM, device, weights=np.ones(idx.size, np.float32))
+        plain, _ = run_ex(dts, rows, idx, off, 37, wl.SUM, device)
+        assert same_bits(ones.cpu().numpy(), plain.cpu().numpy())
+
+
+def test_weights_of_skipped_ids_do_not_matter(device):
+    """Ids outside the table or the shard contribute nothing, whatever their
+    weight (even inf or NaN)."""
+    D, rows, B = 32, 1000, 6
+    g = np.random.default_rng(4)
+    idx = g.integers(0, rows, 40).astype(np.int64)
+    idx[[0, 5, 9]] = [-1, rows, rows + 50]
+    w = g.standard_normal(40).astype(np.float32)
+    w[[0, 5, 9]] = [np.inf, np.nan, -np.inf]
+    off = np.array([0, 3, 10, 10, 25, 38, 40], dtype=np.int64)
+    tables = [wl.table(9, 0, D, wl.F16, 0, rows)]
+    dts = [to_device_table(tables[0], wl.F16, device)]
+    got, hits = run_ex(dts, [rows], idx, off, B, wl.SUM, device, weights=w)
+    w_ok = w.copy()
+    w_ok[[0, 5, 9]] = 0
+    ref, ref_hits, mag = oracle.forward(tables, [rows], D, wl.F16, idx, off, B, wl.SUM, weights=w_ok)
+    assert np.all(np.isfinite(got.cpu().numpy()))
+    assert_parity(got.cpu().numpy(), ref, mag, 40, wl.F16, hits.cpu().numpy(), ref_hits)
