@@ -216,3 +216,62 @@ def test_row_wise_pipeline_on_one_gpu(G, mode, device):
         assert np.all(np.abs(got.cpu().numpy() - ref32) <= np.spacing(np.abs(ref32)))
     for et, *_ in keep:
         et.close()
+
+
+def test_exchange_in_a_hip_graph(device):
+    """bucketize and sum_partials allocate nothing, set no memory with memset
+    and never synchronise, so they record into a HIP graph; every replay must
+    reproduce the oracle for whatever ids and partials the buffers hold then."""
+    g = np.random.default_rng(77)
+    T, B, G, D = 3, 700, 8, 32
+    rows = [20_000, 9_000, 700]
+    L = g.integers(0, 30, T * B)
+    off = wl.offsets_from_lengths(L)
+    nnz = int(off[-1])
+    bounds = even_bounds(rows, G)
+
+    def new_ids():
+        return np.concatenate([g.integers(-3, rows[t] + 3, int(off[(t + 1) * B] - off[t * B]))
+                               for t in range(T)]).astype(np.int64)
+
+    d_b = torch.from_numpy(bounds).to(device)
+    d_i = torch.from_numpy(new_ids()).to(device)
+    d_o = torch.from_numpy(off).to(device)
+    parts = torch.zeros((G, B, T * D), dtype=torch.float32, device=device)
+    out = torch.zeros((B, T * D), dtype=torch.float32, device=device)
+    side = torch.cuda.Stream(device)
+    side.wait_stream(torch.cuda.current_stream(device))
+    with torch.cuda.stream(side):
+        # buffers and workspace come from an eager call, the graph reuses them
+        out_off, out_idx, seg, ws = eb.bucketize(d_b, d_i, d_o, T, B, stream=side)
+        eb.sum_partials(parts, B, T, D, d_o, nnz, out=out, stream=side)
+    torch.cuda.synchronize()
+    nws = ws.numel()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=side):
+        eb.eb_bucketize(T, B, G, d_b.data_ptr(), d_i.data_ptr(), nnz, d_o.data_ptr(),
+                        out_off.data_ptr(), out_idx.data_ptr(), nnz, seg.data_ptr(), ws.data_ptr(),
+                        nws, side.cuda_stream)
+        eb.eb_sum_partials(G, parts.data_ptr(), B, T, D, d_o.data_ptr(), nnz, out.data_ptr(),
+                           side.cuda_stream)
+    for replay in range(4):
+        idx = new_ids()
+        p = g.standard_normal((G, B, T * D)).astype(np.float32)
+        d_i.copy_(torch.from_numpy(idx))
+        parts.copy_(torch.from_numpy(p))
+        out_idx.fill_(-9)
+        out.fill_(float("nan"))
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        want = oracle.bucketize(bounds, idx, off, T, B, capacity=nnz)
+        seg_h = seg.cpu().numpy()
+        got = (out_off.cpu().numpy(), out_idx.cpu().numpy()[:seg_h[-1]], seg_h)
+        for name, a, b in zip(("out_offsets", "out_indices", "segments"), got, want):
+            assert np.array_equal(a, b), (replay, name)
+        ref = oracle.sum_partials(p, B, T, D, off, nnz)
+        mag = oracle.sum_partials(np.abs(p), B, T, D, off, nnz)
+        o = out.cpu().numpy()
+        zero = mag == 0
+        assert np.all(o[zero] == 0)
+        assert np.max(np.abs(o[~zero] - ref[~zero]) / mag[~zero]) <= partial_tolerance(G)
