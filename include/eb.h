@@ -26,7 +26,8 @@
  *   - Return value: EB_OK (0) or a negative EB_ERR_* code; eb_last_error()
  *     then returns a message for the calling thread.  No entry point throws.
  *   - Lengths arrive as offsets, their exclusive prefix sum (CSR form).  For
- *     T tables and B bags per table, offsets has T*B+1 int64 entries and bag
+ *     T tables and B bags per table, offsets has T*B+1 entries (int64, or
+ *     int32 through eb_forward_ex) and bag
  *     (t, b) owns the index positions [offsets[t*B+b], offsets[t*B+b+1]),
  *     so the indices of table 0 come first, then those of table 1, ...
  *   - Offsets are clamped into [0, nnz]; a bag whose end precedes its start is
@@ -63,12 +64,12 @@ enum { EB_SUM = 0, EB_MEAN = 1 };
  * 128 bytes or more with non-temporal loads, which bypass L2 and the
  * last-level cache, gives each XCD a contiguous run of bags, and in large
  * batches pools rows wider than 128 and at most 512 bytes with one lane group
- * per bag.  Faster for such ids, slower
- * for skewed ones (hot rows then miss the caches).  It changes no hit count;
- * by splitting a bag's rows differently over lanes it may change the order of
- * the fp32 additions and so the last bits of a sum (every result stays within
- * the same accuracy bound, exact sums stay exact).  Repeated calls with the
- * same mode give identical bits. */
+ * per bag.  Faster for such ids, slower for skewed ones (hot rows then miss
+ * the caches).  It changes no hit count; by splitting a bag's rows
+ * differently over lanes it may change the order of the fp32 additions and so
+ * the last bits of a sum (every result stays within the same accuracy bound,
+ * exact sums stay exact).  Repeated calls with the same mode give identical
+ * bits. */
 enum { EB_HINT_STREAM_ROWS = 0x100 };
 
 /* Integer type of eb_forward_ex's indices and offsets (both the same).
@@ -159,8 +160,9 @@ int eb_forward(const eb_tables *tables, int32_t T, const int64_t *rows, int32_t 
                void *stream);
 
 /*
- * eb_forward_ex -- eb_forward with a choice of index width and of where each
- * table's result lands in the output.  The pooling is exactly eb_forward's.
+ * eb_forward_ex -- eb_forward with a choice of index width, optional
+ * per-sample weights, and a choice of where each table's result lands in the
+ * output.  Without weights the pooling is exactly eb_forward's.
  *
  * The output layout serves the other two sharding schemes of Sec. 4.1 as well
  * as row-wise shards: under column-wise parallelism a GPU stores columns
@@ -192,13 +194,13 @@ int eb_forward(const eb_tables *tables, int32_t T, const int64_t *rows, int32_t 
  *   stream           as eb_forward.
  *
  * eb_forward(...) is eb_forward_ex with EB_IDX_I64, weights = NULL,
- * ldo = T*D, out_cols = NULL and ldh = T.  Rows take the 16-byte vector path only when
- * out, ldo and every out_cols[t] keep each output row 16-byte aligned; other
- * layouts are correct but slower.
+ * ldo = T*D, out_cols = NULL and ldh = T.  Rows take the 16-byte vector path
+ * only when out, ldo and every out_cols[t] keep each output row 16-byte
+ * aligned; other layouts are correct but slower.
  *
  * Errors: those of eb_forward, and EB_ERR_INVALID for an unknown index_type,
- * weights with EB_MEAN, ldo < 1, a table's columns outside [0, ldo), overlapping tables, ldh < T
- * with hits, or B*ldo / B*ldh overflowing int64.
+ * weights with EB_MEAN, ldo < 1, a table's columns outside [0, ldo),
+ * overlapping tables, ldh < T with hits, or B*ldo / B*ldh overflowing int64.
  */
 int eb_forward_ex(const eb_tables *tables, int32_t T, const int64_t *rows, int32_t D, int32_t dtype,
                   int32_t index_type, const void *indices, int64_t nnz, const void *offsets,
