@@ -26,7 +26,8 @@
 //                (coalesced per destination).
 //   2. scan    : inclusive scan of every destination's row of counts
 //                (reduce-then-scan over 2048-entry tiles: tile sums in the
-//                workspace, one workgroup scans them and writes segments).
+//                workspace, one workgroup scans all rows' tile sums as one
+//                sequence, which also gives the segments).
 //   3. scatter : same waves; ids are written to segments[g] +
 //                out_offsets[g][p] + rank, the rank counting earlier ids of
 //                the bag with the same owner (ballots per distinct owner in
@@ -142,7 +143,7 @@ struct BucketArgs {
 };
 
 // Dynamic LDS: the table's G+1 bounds, then one area per wave.
-__host__ __device__ inline size_t count_wave_bytes(int G) { return kBagsPerWave * 8 + (size_t)4 * G * (G <= kFastShards ? kBagsPerWave : 1); }
+__host__ __device__ inline size_t count_wave_bytes(int G) { return (size_t)4 * G * (G <= kFastShards ? kBagsPerWave : 1); }
 __host__ __device__ inline size_t count_lds_bytes(int G) { return (size_t)(G + 1) * 8 + kWavesPerBlock * count_wave_bytes(G); }
 __host__ __device__ inline size_t scatter_lds_bytes(int G) { return (size_t)(G + 1) * 8 + (size_t)kWavesPerBlock * G * 8; }
 
@@ -195,9 +196,7 @@ __global__ __launch_bounds__(kBlock) void eb_bucket_count(const BucketArgs a)
     const int t = blockIdx.x / a.blocks_per_table;
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = threadIdx.x / kWave;
-    char *area = (char *)(lds + G + 1) + wave * count_wave_bytes(G);
-    int64_t *starts = (int64_t *)area; // the wave's bag starts
-    int *hist = (int *)(area + kBagsPerWave * 8);
+    int *hist = (int *)((char *)(lds + G + 1) + wave * count_wave_bytes(G));
     for (int g = threadIdx.x; g <= G; g += kBlock) bnd[g] = a.bounds[(int64_t)t * (G + 1) + g];
     __syncthreads();
 
@@ -213,7 +212,7 @@ __global__ __launch_bounds__(kBlock) void eb_bucket_count(const BucketArgs a)
 
     if (contiguous && G <= kFastShards) {
         const FewBounds fb = few_bounds(bnd, G <= kFewShards ? G : 0);
-        if (lane < kBagsPerWave) starts[lane] = lane < nb ? s : INT64_MAX;
+        const uint64_t bags = __ballot(lane < nb);
         for (int x = lane; x < kBagsPerWave * G; x += kWave) hist[x] = 0;
         wave_sync_lds();
         for (int64_t k0 = S; k0 < E; k0 += kChunks * kWave) {
@@ -225,12 +224,21 @@ __global__ __launch_bounds__(kBlock) void eb_bucket_count(const BucketArgs a)
             }
 #pragma unroll
             for (int u = 0; u < kChunks; ++u) {
-                const int64_t k = k0 + u * kWave + lane;
+                // The bag of position k is the last one starting at or
+                // before k: the bags starting by the chunk's first position,
+                // plus one for each bag starting inside the chunk at or
+                // below this lane (bag starts ascend for these offsets).
+                const int64_t kb = k0 + u * kWave;
+                const uint64_t started = bags & __ballot(s <= kb);
+                uint64_t inside = bags & ~started & __ballot(s < kb + kWave);
+                int l = __popcll(started) - 1;
+                while (inside) {
+                    const int o = __builtin_amdgcn_readlane((int)(uint32_t)s, __builtin_ctzll(inside)) - (int)(uint32_t)kb;
+                    l += lane >= o ? 1 : 0;
+                    inside &= inside - 1;
+                }
+                const int64_t k = kb + lane;
                 if (k < E) {
-                    int l = 0; // last bag starting at or before k
-#pragma unroll
-                    for (int step = kBagsPerWave / 2; step > 0; step >>= 1)
-                        if (starts[l + step] <= k) l += step;
                     const int g = G <= kFewShards ? few_owner(fb, id[u]) : owner_of(bnd, G, id[u]);
                     if (g >= 0) atomicAdd(&hist[l * G + g], 1);
                 }
@@ -298,67 +306,152 @@ struct ScanArgs {
     int32_t ntiles;
 };
 
-// Pass 2a: sum of every tile (entries 1 + k*kScanTile ... of row g).
+constexpr int kScanPer = kScanTile / kBlock; // counts per thread in a tile
+constexpr int kPrefixRegs = 16;              // tile sums per thread held in registers
+static_assert(kScanTile % kBlock == 0, "scan tile");
+
+// Pass 2a: sum of every tile (entries 1 + k*kScanTile ... of row g); all of a
+// thread's loads are issued before the first is used.
 __global__ __launch_bounds__(kBlock) void eb_scan_tile_sums(const ScanArgs a)
 {
     const int g = blockIdx.y;
     const int k = blockIdx.x;
     const int64_t *row = a.rows + (int64_t)g * (a.TB + 1) + 1;
     const int64_t lo = (int64_t)k * kScanTile;
-    const int64_t hi = std::min<int64_t>(lo + kScanTile, a.TB);
-    int64_t v = 0;
-    for (int64_t i = lo + threadIdx.x; i < hi; i += kBlock) v += row[i];
+    const int n = (int)std::min<int64_t>(kScanTile, a.TB - lo);
+    int64_t v[kScanPer];
+#pragma unroll
+    for (int j = 0; j < kScanPer; ++j) {
+        const int i = j * kBlock + threadIdx.x;
+        v[j] = i < n ? row[lo + i] : 0;
+    }
+    int64_t sum = 0;
+#pragma unroll
+    for (int j = 0; j < kScanPer; ++j) sum += v[j];
     int64_t total;
-    block_inclusive_scan(v, &total);
+    block_inclusive_scan(sum, &total);
     if (threadIdx.x == 0) a.tile_sums[(int64_t)g * a.ntiles + k] = total;
 }
 
-// Pass 2b: exclusive scan of the tile sums of every row (in place), and the
-// destination segments (exclusive scan of the row totals).  One workgroup.
+// Pass 2b: the tile sums of all rows, row after row, as one sequence: its
+// exclusive scan at a row's first tile is that destination's segment start,
+// and the scan minus it is the tile's prefix within its row (written back in
+// place).  One workgroup; every thread takes a contiguous run of tiles.
 __global__ __launch_bounds__(kBlock) void eb_scan_tile_prefix(const ScanArgs a)
 {
-    __shared__ int64_t row_total;
-    if (a.TB == 0) // no bags: every destination's offsets are the single 0
-        for (int g = threadIdx.x; g < a.G; g += kBlock) a.rows[g] = 0;
-    int64_t seg = 0;
-    for (int g = 0; g < a.G; ++g) {
-        int64_t carry = 0;
-        int64_t *ts = a.tile_sums + (int64_t)g * a.ntiles;
-        for (int k0 = 0; k0 < a.ntiles; k0 += kBlock) {
-            const int k = k0 + threadIdx.x;
-            const int64_t v = k < a.ntiles ? ts[k] : 0;
-            int64_t total;
-            const int64_t inc = block_inclusive_scan(v, &total);
-            if (k < a.ntiles) ts[k] = carry + inc - v;
-            carry += total;
+    __shared__ int64_t seg[kMaxShards];
+    if (a.ntiles == 0) { // no bags: every destination is empty, its offsets the single 0
+        for (int g = threadIdx.x; g < a.G; g += kBlock) {
+            a.rows[g] = 0;
+            a.segments[g] = 0;
         }
-        if (threadIdx.x == 0) {
-            a.segments[g] = seg;
-            row_total = carry;
-        }
-        __syncthreads();
-        seg += row_total;
-        __syncthreads();
+        if (threadIdx.x == 0) a.segments[a.G] = 0;
+        return;
     }
-    if (threadIdx.x == 0) a.segments[a.G] = seg;
+    int64_t *ts = a.tile_sums;
+    const int64_t n = (int64_t)a.G * a.ntiles;
+    const int64_t per = (n + kBlock - 1) / kBlock;
+    const int64_t lo = std::min<int64_t>(n, threadIdx.x * per);
+    const int64_t hi = std::min<int64_t>(n, lo + per);
+    if (per <= kPrefixRegs) {
+        // Few tiles (the usual case): the thread's run stays in registers,
+        // its loads all in flight at once, and the row is tracked by
+        // counting rather than dividing.
+        int64_t v[kPrefixRegs];
+        const int cnt = (int)(hi - lo);
+#pragma unroll
+        for (int j = 0; j < kPrefixRegs; ++j) v[j] = j < cnt ? ts[lo + j] : 0;
+        int64_t sum = 0;
+#pragma unroll
+        for (int j = 0; j < kPrefixRegs; ++j) sum += v[j];
+        int64_t total;
+        const int64_t before = block_inclusive_scan(sum, &total) - sum;
+        const int r0 = (int)(lo / a.ntiles);
+        const int c0 = (int)(lo - (int64_t)r0 * a.ntiles);
+        int64_t run = before;
+        int r = r0, c = c0;
+#pragma unroll
+        for (int j = 0; j < kPrefixRegs; ++j) {
+            if (j < cnt) {
+                if (c == 0) seg[r] = run;
+                run += v[j];
+                if (++c == a.ntiles) { c = 0; ++r; }
+            }
+        }
+        __syncthreads();
+        run = before;
+        r = r0;
+        c = c0;
+#pragma unroll
+        for (int j = 0; j < kPrefixRegs; ++j) {
+            if (j < cnt) {
+                ts[lo + j] = run - seg[r];
+                run += v[j];
+                if (++c == a.ntiles) { c = 0; ++r; }
+            }
+        }
+        for (int g = threadIdx.x; g < a.G; g += kBlock) a.segments[g] = seg[g];
+        if (threadIdx.x == 0) a.segments[a.G] = total;
+        return;
+    }
+    int64_t sum = 0;
+    for (int64_t i = lo; i < hi; ++i) sum += ts[i];
+    int64_t total;
+    const int64_t before = block_inclusive_scan(sum, &total) - sum;
+    int64_t run = before;
+    for (int64_t i = lo; i < hi; ++i) {
+        if (i % a.ntiles == 0) seg[i / a.ntiles] = run;
+        run += ts[i];
+    }
+    __syncthreads();
+    run = before;
+    for (int64_t i = lo; i < hi; ++i) {
+        const int64_t v = ts[i];
+        ts[i] = run - seg[i / a.ntiles];
+        run += v;
+    }
+    for (int g = threadIdx.x; g < a.G; g += kBlock) a.segments[g] = seg[g];
+    if (threadIdx.x == 0) a.segments[a.G] = total;
 }
 
-// Pass 2c: scan every tile and add its prefix, in place.
+// Pass 2c: scan every tile and add its prefix, in place.  The tile passes
+// through LDS so that each thread scans kScanPer consecutive counts of its
+// own and a single block-wide scan joins the threads.
+__device__ __forceinline__ int scan_slot(int e) { return e + e / kScanPer; } // conflict-free row reads
+
 __global__ __launch_bounds__(kBlock) void eb_scan_tiles(const ScanArgs a)
 {
+    __shared__ int64_t sm[kScanTile + kScanTile / kScanPer];
     const int g = blockIdx.y;
     const int k = blockIdx.x;
     int64_t *row = a.rows + (int64_t)g * (a.TB + 1) + 1;
     const int64_t lo = (int64_t)k * kScanTile;
-    const int64_t hi = std::min<int64_t>(lo + kScanTile, a.TB);
-    int64_t carry = a.tile_sums[(int64_t)g * a.ntiles + k];
-    for (int64_t i0 = lo; i0 < hi; i0 += kBlock) {
-        const int64_t i = i0 + threadIdx.x;
-        const int64_t v = i < hi ? row[i] : 0;
-        int64_t total;
-        const int64_t inc = block_inclusive_scan(v, &total);
-        if (i < hi) row[i] = carry + inc;
-        carry += total;
+    const int n = (int)std::min<int64_t>(kScanTile, a.TB - lo);
+    const int64_t carry = a.tile_sums[(int64_t)g * a.ntiles + k];
+    int64_t v[kScanPer];
+#pragma unroll
+    for (int j = 0; j < kScanPer; ++j) {
+        const int i = j * kBlock + threadIdx.x;
+        v[j] = i < n ? row[lo + i] : 0;
+    }
+#pragma unroll
+    for (int j = 0; j < kScanPer; ++j) sm[scan_slot(j * kBlock + threadIdx.x)] = v[j];
+    __syncthreads();
+    int64_t run = 0;
+#pragma unroll
+    for (int j = 0; j < kScanPer; ++j) {
+        run += sm[scan_slot(threadIdx.x * kScanPer + j)];
+        v[j] = run;
+    }
+    int64_t total;
+    const int64_t base = carry + block_inclusive_scan(run, &total) - run;
+#pragma unroll
+    for (int j = 0; j < kScanPer; ++j) sm[scan_slot(threadIdx.x * kScanPer + j)] = base + v[j];
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < kScanPer; ++j) {
+        const int i = j * kBlock + threadIdx.x;
+        if (i < n) row[lo + i] = sm[scan_slot(i)];
     }
 }
 
