@@ -500,10 +500,10 @@ __global__ __launch_bounds__(kBlock) void eb_bucket_scatter(const BucketArgs a)
         // destination; a single store then places the whole chunk.  The
         // running output slot of each destination is wave-uniform.
         const FewBounds fb = few_bounds(bnd, G);
-        int64_t slot[kBallotShards];
-#pragma unroll
-        for (int d = 0; d < kBallotShards; ++d)
-            slot[d] = d < G ? a.segments[d] + a.out_offsets[(int64_t)d * row + p0] : 0;
+        // Lane d < G keeps destination d's next output slot.
+        int64_t slot = lane < G ? a.segments[lane] + a.out_offsets[(int64_t)lane * row + p0] : 0;
+        const uint32_t l0 = (uint32_t)(lane & 1) - 1u, l1 = (uint32_t)((lane >> 1) & 1) - 1u,
+                       l2 = (uint32_t)((lane >> 2) & 1) - 1u;
         for (int64_t k0 = S; k0 < E; k0 += kChunks * kWave) {
             int64_t id[kChunks];
 #pragma unroll
@@ -519,20 +519,30 @@ __global__ __launch_bounds__(kBlock) void eb_bucket_scatter(const BucketArgs a)
             for (int u = 0; u < kChunks; ++u) {
                 const int64_t k = k0 + u * kWave + lane;
                 const int g = k < E ? few_owner(fb, id[u]) : -1;
-                // Straight-line over all 8 destinations (those >= G match no
-                // lane): the rank is computed for every lane, then selected.
-                int64_t base = 0;
-                int rank = 0;
-#pragma unroll
-                for (int d = 0; d < kBallotShards; ++d) {
-                    const bool mine = g == d;
-                    const uint64_t m = __ballot(mine);
-                    const int r = rank_below(m);
-                    base = mine ? slot[d] : base;
-                    rank = mine ? r : rank;
-                    slot[d] += __popcll(m);
-                }
+                // The owner's three bits as ballots: the lanes sharing this
+                // lane's owner are the valid ones agreeing with it on every
+                // bit (b ^ ~x keeps the lanes whose bit equals x's).
+                const uint64_t valid = __ballot(g >= 0);
+                const uint64_t b0 = __ballot(g & 1), b1 = __ballot(g & 2), b2 = __ballot(g & 4);
+                const uint32_t n0 = (uint32_t)(g & 1) - 1u, n1 = (uint32_t)((g >> 1) & 1) - 1u,
+                               n2 = (uint32_t)((g >> 2) & 1) - 1u;
+                const uint32_t same_lo = (uint32_t)valid & ((uint32_t)b0 ^ n0) & ((uint32_t)b1 ^ n1) &
+                                         ((uint32_t)b2 ^ n2);
+                const uint32_t same_hi = (uint32_t)(valid >> 32) & ((uint32_t)(b0 >> 32) ^ n0) &
+                                         ((uint32_t)(b1 >> 32) ^ n1) & ((uint32_t)(b2 >> 32) ^ n2);
+                const int rank = (int)__builtin_amdgcn_mbcnt_hi(same_hi, __builtin_amdgcn_mbcnt_lo(same_lo, 0u));
+                // This lane's slot from lane g (any lane for g < 0: unused).
+                const int src = g & (kWave - 1);
+                const int base_lo = __shfl((int)(uint32_t)slot, src);
+                const int base_hi = __shfl((int)(slot >> 32), src);
+                const int64_t base = ((int64_t)base_hi << 32) | (uint32_t)base_lo;
                 pos[u] = g >= 0 ? base + rank : -1;
+                // Lane d advances destination d's slot by the chunk's ids
+                // for d: the same agreement, with d's bits in place of g's.
+                const uint32_t own_lo = (uint32_t)valid & ((uint32_t)b0 ^ l0) & ((uint32_t)b1 ^ l1) & ((uint32_t)b2 ^ l2);
+                const uint32_t own_hi = (uint32_t)(valid >> 32) & ((uint32_t)(b0 >> 32) ^ l0) &
+                                        ((uint32_t)(b1 >> 32) ^ l1) & ((uint32_t)(b2 >> 32) ^ l2);
+                slot += __popc(own_lo) + __popc(own_hi);
             }
             __builtin_amdgcn_sched_barrier(0); // keep the stores after all ranking
 #pragma unroll
