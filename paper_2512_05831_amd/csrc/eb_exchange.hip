@@ -30,8 +30,9 @@
 //                sequence, which also gives the segments).
 //   3. scatter : same waves; ids are written to segments[g] +
 //                out_offsets[g][p] + rank, the rank counting earlier ids of
-//                the bag with the same owner (ballots per distinct owner in
-//                each 64-id chunk), so the order is stable.  For ordinary CSR
+//                the bag with the same owner (per 64-id chunk: three ballots
+//                of the owner's bits for up to 8 destinations, else a ballot
+//                per distinct owner), so the order is stable.  For ordinary CSR
 //                offsets one running slot per destination and wave suffices,
 //                since position order is then (bag, position) order.  Every
 //                store is checked against the capacity of out_indices (an
@@ -124,7 +125,8 @@ constexpr int kBagsPerWave = 16;
 constexpr int kBagsPerBlock = kBagsPerWave * kWavesPerBlock;
 static_assert(kBagsPerWave <= kWave && (kBagsPerWave & (kBagsPerWave - 1)) == 0, "bags per wave");
 constexpr int kFastShards = 32; // count's per-(bag, destination) histogram fits LDS up to here
-constexpr int kChunks = 4;      // 64-id chunks loaded ahead
+constexpr int kCountChunks = 4;   // 64-id chunks loaded ahead by count
+constexpr int kScatterChunks = 8; // and by scatter (measured best for each)
 constexpr int kBallotShards = kFewShards; // compare-based owners, one ballot per destination
 
 struct BucketArgs {
@@ -215,15 +217,15 @@ __global__ __launch_bounds__(kBlock) void eb_bucket_count(const BucketArgs a)
         const uint64_t bags = __ballot(lane < nb);
         for (int x = lane; x < kBagsPerWave * G; x += kWave) hist[x] = 0;
         wave_sync_lds();
-        for (int64_t k0 = S; k0 < E; k0 += kChunks * kWave) {
-            int64_t id[kChunks];
+        for (int64_t k0 = S; k0 < E; k0 += kCountChunks * kWave) {
+            int64_t id[kCountChunks];
 #pragma unroll
-            for (int u = 0; u < kChunks; ++u) {
+            for (int u = 0; u < kCountChunks; ++u) {
                 const int64_t k = k0 + u * kWave + lane;
                 id[u] = k < E ? __builtin_nontemporal_load(a.indices + k) : 0;
             }
 #pragma unroll
-            for (int u = 0; u < kChunks; ++u) {
+            for (int u = 0; u < kCountChunks; ++u) {
                 // The bag of position k is the last one starting at or
                 // before k: the bags starting by the chunk's first position,
                 // plus one for each bag starting inside the chunk at or
@@ -504,19 +506,19 @@ __global__ __launch_bounds__(kBlock) void eb_bucket_scatter(const BucketArgs a)
         int64_t slot = lane < G ? a.segments[lane] + a.out_offsets[(int64_t)lane * row + p0] : 0;
         const uint32_t l0 = (uint32_t)(lane & 1) - 1u, l1 = (uint32_t)((lane >> 1) & 1) - 1u,
                        l2 = (uint32_t)((lane >> 2) & 1) - 1u;
-        for (int64_t k0 = S; k0 < E; k0 += kChunks * kWave) {
-            int64_t id[kChunks];
+        for (int64_t k0 = S; k0 < E; k0 += kScatterChunks * kWave) {
+            int64_t id[kScatterChunks];
 #pragma unroll
-            for (int u = 0; u < kChunks; ++u) {
+            for (int u = 0; u < kScatterChunks; ++u) {
                 const int64_t k = k0 + u * kWave + lane;
                 id[u] = k < E ? __builtin_nontemporal_load(a.indices + k) : 0;
             }
             // Rank all chunks first, store afterwards: loads and stores
             // share one completion counter, so a store between two chunks
             // would make the next chunk wait for it.
-            int64_t pos[kChunks];
+            int64_t pos[kScatterChunks];
 #pragma unroll
-            for (int u = 0; u < kChunks; ++u) {
+            for (int u = 0; u < kScatterChunks; ++u) {
                 const int64_t k = k0 + u * kWave + lane;
                 const int g = k < E ? few_owner(fb, id[u]) : -1;
                 // The owner's three bits as ballots: the lanes sharing this
@@ -546,7 +548,7 @@ __global__ __launch_bounds__(kBlock) void eb_bucket_scatter(const BucketArgs a)
             }
             __builtin_amdgcn_sched_barrier(0); // keep the stores after all ranking
 #pragma unroll
-            for (int u = 0; u < kChunks; ++u)
+            for (int u = 0; u < kScatterChunks; ++u)
                 if ((uint64_t)pos[u] < (uint64_t)a.out_cap) a.out_indices[pos[u]] = id[u];
         }
         return;
@@ -557,15 +559,15 @@ __global__ __launch_bounds__(kBlock) void eb_bucket_scatter(const BucketArgs a)
         // lane g keeps destination g's in a register.
         int64_t slot = lane < G ? a.segments[lane] + a.out_offsets[(int64_t)lane * row + p0] : 0;
         const uint64_t below = (1ull << lane) - 1;
-        for (int64_t k0 = S; k0 < E; k0 += kChunks * kWave) {
-            int64_t id[kChunks];
+        for (int64_t k0 = S; k0 < E; k0 += kScatterChunks * kWave) {
+            int64_t id[kScatterChunks];
 #pragma unroll
-            for (int u = 0; u < kChunks; ++u) {
+            for (int u = 0; u < kScatterChunks; ++u) {
                 const int64_t k = k0 + u * kWave + lane;
                 id[u] = k < E ? __builtin_nontemporal_load(a.indices + k) : 0;
             }
 #pragma unroll
-            for (int u = 0; u < kChunks; ++u) {
+            for (int u = 0; u < kScatterChunks; ++u) {
                 const int64_t k = k0 + u * kWave + lane;
                 const int g = k < E ? owner_of(bnd, G, id[u]) : -1;
                 uint64_t pending = __ballot(g >= 0);
@@ -585,15 +587,15 @@ __global__ __launch_bounds__(kBlock) void eb_bucket_scatter(const BucketArgs a)
     if (contiguous) {
         for (int g = lane; g < G; g += kWave) next[g] = a.segments[g] + a.out_offsets[(int64_t)g * row + p0];
         wave_sync_lds();
-        for (int64_t k0 = S; k0 < E; k0 += kChunks * kWave) {
-            int64_t id[kChunks];
+        for (int64_t k0 = S; k0 < E; k0 += kScatterChunks * kWave) {
+            int64_t id[kScatterChunks];
 #pragma unroll
-            for (int u = 0; u < kChunks; ++u) {
+            for (int u = 0; u < kScatterChunks; ++u) {
                 const int64_t k = k0 + u * kWave + lane;
                 id[u] = k < E ? __builtin_nontemporal_load(a.indices + k) : 0;
             }
 #pragma unroll
-            for (int u = 0; u < kChunks; ++u) {
+            for (int u = 0; u < kScatterChunks; ++u) {
                 const int64_t k = k0 + u * kWave + lane;
                 scatter_chunk(a, next, lane, k < E ? owner_of(bnd, G, id[u]) : -1, id[u]);
             }
