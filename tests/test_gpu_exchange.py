@@ -72,6 +72,15 @@ def test_bucketize_batch_tails(B, device):
     check_bucketize(T, B, idx, off, bounds, device)
 
 
+@pytest.mark.parametrize("G,T,B", [(8, 5, 5001), (3, 1, 40960), (300, 2, 14000), (1024, 2, 6000)])
+def test_bucketize_many_scan_tiles(G, T, B, device):
+    # Many 2048-bag scan tiles with a ragged last one; with 300 and 1024
+    # destinations the tile sums exceed 16 per thread of the one-workgroup
+    # prefix pass (destinations x tiles > 4096).
+    T, B, idx, off, bounds = bucket_case(G * 7 + B, G, T=T, B=B, maxL=4)
+    check_bucketize(T, B, idx, off, bounds, device)
+
+
 def test_bucketize_long_bags_and_skew(device):
     g = np.random.default_rng(9)
     T, B, G = 2, 50, 8
