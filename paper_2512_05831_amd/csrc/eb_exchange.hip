@@ -497,12 +497,12 @@ __global__ __launch_bounds__(kBlock) void eb_bucket_scatter(const BucketArgs a)
     int64_t s, e, S, E;
     const bool contiguous = wave_bags(a, p0, nb, lane, s, e, S, E);
     if (contiguous && G <= kBallotShards) {
-        // Contiguous bags, few destinations: one ballot per destination and
-        // chunk gives every id its rank among the chunk's ids for the same
-        // destination; a single store then places the whole chunk.  The
-        // running output slot of each destination is wave-uniform.
+        // Contiguous bags, few destinations: ballots of the owner's bits give
+        // every id of a chunk its rank among the chunk's ids for the same
+        // destination; a single store then places the whole chunk.
         const FewBounds fb = few_bounds(bnd, G);
-        // Lane d < G keeps destination d's next output slot.
+        // Lane d < G keeps destination d's next output slot; l0..l2 are the
+        // complements of this lane's low three bits as all-ones / zero masks.
         int64_t slot = lane < G ? a.segments[lane] + a.out_offsets[(int64_t)lane * row + p0] : 0;
         const uint32_t l0 = (uint32_t)(lane & 1) - 1u, l1 = (uint32_t)((lane >> 1) & 1) - 1u,
                        l2 = (uint32_t)((lane >> 2) & 1) - 1u;
