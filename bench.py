@@ -23,6 +23,10 @@ whole-row reads over the same footprint with the library's probe, uniform-id
 workloads only) and ``torch_embedding_bag`` (PyTorch's own GPU embedding_bag
 on the same tables and ids); ``--cold`` adds single-launch timings with and
 without the caches flushed.
+
+Other modes print their own JSON lines instead: ``--exchange`` (the row-wise
+exchange's local kernels), ``--rw-pipeline G`` (one GPU's compute in a
+row-wise step over G GPUs) and ``--sweep paper`` (the paper's gather shapes).
 """
 from __future__ import annotations
 
@@ -331,6 +335,143 @@ def exchange_bench(torch, dev, eb, K, W):
                       "frac_of_8TBps": round(by / us / 1e3 / HBM_PEAK_GBPS, 4)}), flush=True)
 
 
+def rw_receive(torch, dev, eb, idx, off, T: int, B: int, bounds, G: int):
+    """The row-wise exchange of one batch as GPU 0 of G sees it.  Mini-batch s
+    is bags [s*B/G, (s+1)*B/G) of every table.  Every mini-batch is bucketized
+    here by ``bounds`` (int64 [T, G+1]); what GPU 0 receives is block 0 of
+    each, laid out table-major over all B bags (source s's bags at
+    s*B/G ...), ready for one eb_forward on row block 0.
+
+    Returns (ids and offsets of mini-batch 0, received ids, received offsets,
+    ids mini-batch 0 sends to other GPUs, ids GPU 0 receives from others)."""
+    Bs = B // G
+    d_b = torch.from_numpy(np.ascontiguousarray(bounds, dtype=np.int64)).to(dev)
+
+    def minibatch(s):
+        ids, lens = [], []
+        for t in range(T):
+            p0 = t * B + s * Bs
+            ids.append(idx[off[p0]:off[p0 + Bs]])
+            lens.append(np.diff(off[p0:p0 + Bs + 1]))
+        return np.concatenate(ids), wl.offsets_from_lengths(np.concatenate(lens))
+
+    recv_ids, recv_len = [[None] * G for _ in range(T)], np.zeros(T * B, dtype=np.int64)
+    sent = 0
+    for s in range(G):
+        ids_s, off_s = minibatch(s)
+        d_i, d_o = torch.from_numpy(ids_s).to(dev), torch.from_numpy(off_s).to(dev)
+        out_off, out_idx, seg, _ = eb.bucketize(d_b, d_i, d_o, T, Bs)
+        torch.cuda.synchronize()
+        seg_h = seg.cpu().numpy()
+        o0 = out_off[0].cpu().numpy()
+        ids0 = out_idx[int(seg_h[0]):int(seg_h[1])].cpu().numpy()
+        for t in range(T):
+            o = o0[t * Bs:(t + 1) * Bs + 1]
+            recv_ids[t][s] = ids0[o[0]:o[-1]]
+            recv_len[t * B + s * Bs:t * B + (s + 1) * Bs] = np.diff(o)
+        if s == 0:
+            sent = int(seg_h[G] - (seg_h[1] - seg_h[0]))
+            mb_ids, mb_off = ids_s, off_s
+    r_ids = np.concatenate([recv_ids[t][s] for t in range(T) for s in range(G)]).astype(np.int64)
+    r_off = wl.offsets_from_lengths(recv_len)
+    received = int(r_ids.size - sum(recv_ids[t][0].size for t in range(T)))
+    return mb_ids, mb_off, r_ids, r_off, sent, received
+
+
+def rw_pipeline_bench(torch, dev, eb, w, G, K, W, rows_policy="auto"):
+    """One GPU's compute in one step of the row-wise path (Sec. 4.2-4.3) with
+    workload w's batch split over G GPUs: this GPU holds rows [0, rows/G) of
+    every table and bags [0, B/G) of every table's batch (its mini-batch).
+
+      A  eb_bucketize of its mini-batch into G row blocks: the send buffers of
+         the id all-to-all;
+      B  eb_forward over the ids it receives from all G mini-batches, on its
+         row block, for all B bags: the partial sums;
+      C  eb_sum_partials of the G partial blocks it receives for its own bags.
+
+    The collectives between the stages need other GPUs and are not run; the
+    line gives the bytes each would move for this GPU.  The ids this GPU would
+    receive come from bucketizing every mini-batch here, before timing; the
+    received partial blocks are random (their values do not change the time)."""
+    T, B, D = w.T, w.B, w.D
+    if w.sharded or B % G:
+        raise SystemExit("--rw-pipeline needs an unsharded workload whose batch splits evenly")
+    Bs = B // G
+    blk = w.rows // G
+    K = min(K, 100)
+    stream = torch.cuda.Stream(dev)
+    off = w.offsets()
+    idx = w.indices(off)
+    bounds = np.array([[g * w.rows // G for g in range(G + 1)]] * T, dtype=np.int64)
+    d_b = torch.from_numpy(bounds).to(dev)
+
+    mb_ids, mb_off, r_ids, r_off, sent, received = rw_receive(torch, dev, eb, idx, off, T, B, bounds, G)
+
+    # A: bucketize this GPU's mini-batch
+    d_mi, d_mo = torch.from_numpy(mb_ids).to(dev), torch.from_numpy(mb_off).to(dev)
+    TBs = T * Bs
+    a_off = torch.empty((G, TBs + 1), dtype=torch.int64, device=dev)
+    a_idx = torch.empty(max(1, mb_ids.size), dtype=torch.int64, device=dev)
+    a_seg = torch.empty(G + 1, dtype=torch.int64, device=dev)
+    nws = eb.eb_bucketize_workspace(T, Bs, G)
+    ws = torch.empty(max(1, nws), dtype=torch.uint8, device=dev)
+
+    def stage_a():
+        eb.eb_bucketize(T, Bs, G, d_b.data_ptr(), d_mi.data_ptr(), mb_ids.size, d_mo.data_ptr(),
+                        a_off.data_ptr(), a_idx.data_ptr(), mb_ids.size, a_seg.data_ptr(),
+                        ws.data_ptr(), nws, stream.cuda_stream)
+
+    # B: gather the received ids on row block 0
+    wb = w.with_(shard_lo=0, shard_hi=blk)
+    tdt = {wl.F32: torch.float32, wl.F16: torch.float16, wl.BF16: torch.bfloat16}[w.dtype]
+    tables = []
+    for t in range(T):
+        h = wb.table(t)
+        tables.append(torch.from_numpy(h.view(np.int16) if h.dtype == np.uint16 else h).to(dev).view(tdt))
+    et = eb.EmbeddingBagTables(tables, rows=[w.rows] * T, shard_lo=0, shard_hi=blk)
+    d_ri, d_ro = torch.from_numpy(r_ids).to(dev), torch.from_numpy(r_off).to(dev)
+    partial = torch.empty((B, T * D), dtype=torch.float32, device=dev)
+    stream_rows = rows_policy == "stream" or (rows_policy == "auto" and w.dist == "uniform")
+    mode = w.modes[0] | (eb.EB_HINT_STREAM_ROWS if stream_rows else 0)
+    stage_b = et.prepare(d_ri, d_ro, B, mode, partial, None, stream)
+
+    # C: add the G partial blocks of this GPU's bags
+    gen = torch.Generator(device=dev).manual_seed(w.seed + 11)
+    recv_parts = torch.randn((G, Bs, T * D), generator=gen, device=dev)
+    summed = torch.empty((Bs, T * D), dtype=torch.float32, device=dev)
+
+    def stage_c():
+        eb.eb_sum_partials(G, recv_parts.data_ptr(), Bs, T, D, None, 0, summed.data_ptr(),
+                           stream.cuda_stream)
+
+    def step():
+        stage_a()
+        stage_b()
+        stage_c()
+
+    us = {"bucketize": _time_launches(torch, stream, stage_a, K, W),
+          "gather": _time_launches(torch, stream, stage_b, K, W),
+          "sum_partials": _time_launches(torch, stream, stage_c, K, W)}
+    step_us = _time_launches(torch, stream, step, K, W)
+    gathered = int(r_ids.size)
+    by = {"bucketize": mb_ids.size * 16 + (TBs + 1) * 8 + bounds.size * 8 + G * (TBs + 1) * 8 + (G + 1) * 8,
+          "gather": gathered * (D * w.elem_bytes + 8) + (T * B + 1) * 8 + B * T * D * 4,
+          "sum_partials": (G + 1) * Bs * T * D * 4}
+    print(json.dumps({
+        "kernel": "rw_pipeline", "workload": f"{w.name}-row-block-0-of-{G}",
+        "gpus_emulated": G, "bags_per_gpu": Bs, "ids_in_minibatch": int(mb_ids.size),
+        "ids_gathered": gathered,
+        "stages_us": {k: round(v, 1) for k, v in us.items()},
+        "stages_algorithmic_GBps": {k: round(by[k] / us[k] / 1e3, 1) for k in us},
+        "step_us": round(step_us, 1), "sum_of_stages_us": round(sum(us.values()), 1),
+        "collectives_not_run_bytes": {
+            "ids_sent": sent * 8, "ids_received": received * 8,
+            "offsets_sent": (G - 1) * (TBs + 1) * 8,
+            "partials_sent": (G - 1) * Bs * T * D * 4, "partials_received": (G - 1) * Bs * T * D * 4},
+        "rows_cache_policy": "stream" if mode & eb.EB_HINT_STREAM_ROWS else "cached"}), flush=True)
+    et.close()
+
+
 def paper_sweep(torch, dev, eb, index_type="i64"):
     """The gather shapes the paper varies (Sec. 4.3 / 4.4: 2..64 tables, batch
     128 / 1024 / 4096, pooling 4 / 8 / 16, 128-byte rows; Sec. 5.1: one table
@@ -426,6 +567,9 @@ def main():
                     help="replay the steps from a captured HIP graph (launch-bound workloads)")
     ap.add_argument("--exchange", action="store_true",
                     help="time the row-wise exchange kernels instead (bucketize, sum_partials)")
+    ap.add_argument("--rw-pipeline", type=int, default=0, metavar="G",
+                    help="time one GPU's compute in a row-wise step of the chosen workload split "
+                         "over G GPUs instead (bucketize, gather of the received ids, sum of partials)")
     ap.add_argument("--sweep", choices=["paper"], default=None,
                     help="time the paper's single-GPU gather shapes instead (one JSON line each)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
@@ -450,6 +594,10 @@ def main():
         return
     if args.exchange:
         exchange_bench(torch, dev, eb, args.steps, args.warmup)
+        return
+    if args.rw_pipeline:
+        rw_pipeline_bench(torch, dev, eb, pick_workload(args), args.rw_pipeline, args.steps, args.warmup,
+                          args.rows_policy)
         return
     w = pick_workload(args)
     mode = w.modes[0]

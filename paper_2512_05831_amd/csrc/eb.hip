@@ -16,10 +16,11 @@
 //     chunks (global_load_dwordx4); surplus lanes of a ragged row idle.
 //   * P such lane groups form the team that pools one bag: group g takes the
 //     bag's rows g, g+P, g+2P, ...; a wave holds 64/(R*P) teams (P = 64/R
-//     for rows of 16 lanes or more, halved for streamed rows of large
-//     batches).  Partial
-//     sums of the P groups are combined at the end with cross-lane moves
-//     (DPP, ds_swizzle, v_permlane32_swap).
+//     for rows of 16 lanes or more).  Large batches of streamed rows, or of
+//     short cached bags, take teams of one lane group instead (two or four
+//     bags per wave; 256-B and 1-KB rows as 16 lanes of 1 or 4 chunks).
+//     Partial sums of the P groups are combined at the end with cross-lane
+//     moves (DPP, ds_swizzle, v_permlane32_swap).
 //   * A team stages a window of its bag's indices in LDS: the window is read
 //     with coalesced index loads, filtered against the shard, and rewritten as
 //     32-bit local row numbers (or an invalid marker).  The gather loop then
@@ -84,13 +85,20 @@ int rows_in_flight_per_bag(const Shape &s, bool stream)
 }
 
 
-Shape team_shape(int rb, bool few, bool single)
+// single: one lane group per bag for large batches; 256-B and 1-KB rows
+// then go to 16-lane teams (1 or 4 chunks per lane), and 512-B rows too when
+// narrow512 is set (else 32-lane teams).
+Shape team_shape(int rb, bool few, bool single, bool narrow512 = false)
 {
     Shape s;
     const int chunks = rb / 16;
     s.R = 1;
     while (s.R < chunks && s.R < kWave) s.R *= 2;
     s.C = (chunks + s.R - 1) / s.R;
+    if (single && (rb == 256 || rb == 1024 || (rb == 512 && narrow512))) {
+        s.R = 16;
+        s.C = rb / 256;
+    }
     s.P = groups_per_bag(s.R, few, single);
     return s;
 }
@@ -188,14 +196,19 @@ int forward_impl(const char *who, const eb_tables *h, int32_t T, const int64_t *
         const int64_t waves = bags / (kWave / (normal.R * normal.P));
         const bool few = waves < kWaveSlots && bags <= kFewBagsMax &&
                          nnz > 2 * (int64_t)rows_in_flight_per_bag(normal, stream) * bags;
-        // Streamed rows of 16 or 32 lanes: one lane group per bag (two bags
-        // per wave) when that still gives half the GPU's wave slots or more.
-        // Over the paper's shapes and workloads 2 and 4 that is 2-6% faster;
-        // smaller batches lose more from halving their waves.
-        const Shape halved = team_shape((int)rb, false, true);
-        const bool single = stream && !few && halved.P != normal.P &&
-                            bags / (kWave / (halved.R * halved.P)) >= kWaveSlots / 2;
-        const Shape sh = few ? team_shape((int)rb, true, false) : single ? halved : normal;
+        // Teams narrower than a wave, one lane group per bag, when they still
+        // give half the GPU's wave slots or more: for streamed rows, and for
+        // cached rows when the mean bag is shorter than the rows the normal
+        // mapping keeps in flight per bag (most of a wave would idle: the
+        // bags a row block receives in a row-wise exchange).  512-B rows take
+        // 32-lane teams when streamed (16-lane teams were 2-5% slower on the
+        // paper's multi-table shapes) and 16-lane teams for short cached bags.
+        const bool short_bags = nnz < (int64_t)rows_in_flight_per_bag(normal, false) * bags;
+        const Shape narrow = team_shape((int)rb, false, true, !stream && short_bags);
+        const int narrow_team = narrow.R * narrow.P;
+        const bool single = (stream || short_bags) && !few && narrow_team < normal.R * normal.P &&
+                            bags / (kWave / narrow_team) >= kWaveSlots / 2;
+        const Shape sh = few ? team_shape((int)rb, true, false) : single ? narrow : normal;
         fn = weights ? pick_weighted_kernel(i32, dtype, true, sh.R, sh.C, stream, few, single)
                      : pick_kernel<false>(i32, dtype, true, sh.R, sh.C, stream, few, single);
         bags_per_block = (kWave / (sh.R * sh.P)) * kWavesPerBlock;

@@ -418,9 +418,11 @@ constexpr int groups_per_bag(int R, bool few, bool single)
 {
     // Wide rows or small batches: one bag per wave.  Otherwise narrow rows
     // get 16-lane teams (4 bags per wave), so the group reduction stays
-    // inside a DPP row.  "single": rows of 16 or 32 lanes with one lane group
-    // per bag (two bags per wave), used for streamed rows of large batches.
-    return few ? kWave / R : (single && R >= 16 && R < kWave) ? kWave / R / 2 : R >= 16 ? kWave / R : 16 / R;
+    // inside a DPP row.  "single": teams narrower than a wave for large
+    // batches, one lane group per bag: rows of 32 lanes two bags per wave,
+    // rows read by 16 lanes (256-B rows, and 512-B / 1-KB rows as 2 / 4
+    // chunks per lane) four.
+    return few ? kWave / R : (single && R >= 16 && R < kWave) ? 1 : R >= 16 ? kWave / R : 16 / R;
 }
 
 using KernelFn = void (*)(GatherArgs);
@@ -438,7 +440,12 @@ KernelFn team_kernel(bool stream, bool single)
     constexpr int P_SINGLE = groups_per_bag(R, kFew, true);
     constexpr int U_CACHED = C >= 6 ? 1 : 6 / C;
     constexpr int U_STREAM = (!kFew && R * C >= 8) ? (C >= 2 ? 1 : 2) : U_CACHED;
-    if (!stream) return eb_gather_team<IT, DT, R, P, C, U_CACHED, false, kW>;
+    if (!stream) {
+        if constexpr (P_SINGLE != P) {
+            if (single) return eb_gather_team<IT, DT, R, P_SINGLE, C, U_CACHED, false, kW>;
+        }
+        return eb_gather_team<IT, DT, R, P, C, U_CACHED, false, kW>;
+    }
     if constexpr (P_SINGLE != P) {
         if (single) return eb_gather_team<IT, DT, R, P_SINGLE, C, U_STREAM, true, kW>;
     }
@@ -460,7 +467,10 @@ KernelFn pick_team_kernel(int R, int C, bool stream, bool few, bool single)
     case 2: return team_kernel<IT, DT, 2, 1, kW>(stream, few, single);
     case 4: return team_kernel<IT, DT, 4, 1, kW>(stream, few, single);
     case 8: return team_kernel<IT, DT, 8, 1, kW>(stream, few, single);
-    case 16: return team_kernel<IT, DT, 16, 1, kW>(stream, few, single);
+    case 16: // 256-B rows; 512-B and 1-KB rows in 16-lane teams
+        return C == 4 ? team_kernel<IT, DT, 16, 4, kW>(stream, few, single)
+               : C == 2 ? team_kernel<IT, DT, 16, 2, kW>(stream, few, single)
+                        : team_kernel<IT, DT, 16, 1, kW>(stream, few, single);
     case 32: return team_kernel<IT, DT, 32, 1, kW>(stream, few, single);
     default:
         switch (C) {

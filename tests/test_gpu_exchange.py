@@ -12,7 +12,7 @@ import pytest
 import torch
 
 import oracle
-from gpu_util import U32, gamma, to_device_table
+from gpu_util import U32, gamma, run, to_device_table
 from paper_2512_05831_amd import eb, workloads as wl
 
 pytestmark = pytest.mark.gpu
@@ -225,6 +225,33 @@ def test_row_wise_pipeline_on_one_gpu(G, mode, device):
         assert np.all(np.abs(got.cpu().numpy() - ref32) <= np.spacing(np.abs(ref32)))
     for et, *_ in keep:
         et.close()
+
+
+@pytest.mark.parametrize("G", [2, 4, 8])
+def test_rw_receive_gathers_the_row_block(G, device):
+    """What GPU 0 of G receives in the row-wise exchange (the benchmark's
+    rw_receive: every mini-batch bucketized, block 0 of each laid out over
+    all bags), gathered on row block 0, equals the oracle pooling the whole
+    batch restricted to that block; exact on dyadic tables."""
+    import bench
+
+    g = np.random.default_rng(50 + G)
+    T, B, D, rows = 3, 400, 32, 5000
+    off = wl.offsets_from_lengths(g.integers(0, 30, T * B))
+    idx = g.integers(-5, rows + 5, int(off[-1])).astype(np.int64)  # ids outside every block go nowhere
+    bounds = even_bounds([rows] * T, G)
+    mb_ids, mb_off, r_ids, r_off, sent, received = bench.rw_receive(torch, device, eb, idx, off, T, B, bounds, G)
+    blk = int(bounds[0][1])
+    tables = [wl.table(9, t, D, wl.F32, 0, blk, values="dyadic") for t in range(T)]
+    got, hits = run(tables, [rows] * T, D, wl.F32, r_ids, r_off, B, wl.SUM, 0, blk, device=device)
+    ref, ref_hits, _ = oracle.forward(tables, [rows] * T, D, wl.F32, idx, off, B, wl.SUM, 0, blk)
+    assert np.array_equal(got.astype(np.float64), ref)
+    assert np.array_equal(hits, ref_hits)
+    # every received id lies in block 0; mini-batch 0 keeps its block-0 ids and sends the rest
+    assert r_ids.size == 0 or (r_ids.min() >= 0 and r_ids.max() < blk)
+    in_range = int(np.count_nonzero((mb_ids >= 0) & (mb_ids < rows)))
+    kept = int(np.count_nonzero((mb_ids >= 0) & (mb_ids < blk)))
+    assert sent == in_range - kept and received == r_ids.size - kept
 
 
 def test_exchange_in_a_hip_graph(device):

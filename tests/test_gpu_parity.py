@@ -94,7 +94,7 @@ def test_dyadic_mean_within_one_ulp(dtype):
 @pytest.mark.parametrize("dtype", DT)
 @pytest.mark.parametrize("D", [8, 16, 32, 64, 100, 128, 256, 512, 1024, 2048])
 # 37 bags per table: the small-batch mapping; 1500: the normal one; 3000: two
-# bags per wave for streamed rows of 16 or 32 lanes
+# bags per wave for streamed rows of 32 lanes
 @pytest.mark.parametrize("B", [37, 1500, 3000])
 def test_stream_hint_keeps_results(dtype, D, B):
     """The hint changes cache policy and lane mapping: hit counts are equal,
@@ -113,6 +113,31 @@ def test_stream_hint_keeps_results(dtype, D, B):
                 assert_parity(got, ref, mag, max_bag_len(off, idx.size), dtype, h, ref_hits)
             if values == "dyadic" and mode == wl.SUM:
                 assert np.array_equal(plain.view(np.uint32), hinted.view(np.uint32))
+
+
+@pytest.mark.parametrize("D,dtype", [(64, wl.F32), (128, wl.F16), (128, wl.F32), (256, wl.BF16), (256, wl.F32),
+                                     (512, wl.F16), (100, wl.F32)])
+@pytest.mark.parametrize("hint", [0, eb.EB_HINT_STREAM_ROWS])
+@pytest.mark.parametrize("B", [4500, 1000])
+def test_narrow_teams(D, dtype, hint, B):
+    """Large batches of streamed rows, or of cached bags shorter than the rows
+    a wave keeps in flight per bag, take teams narrower than a wave: 256-B
+    and 1-KB rows 16 lanes of 1 or 4 chunks (four bags per wave), 512-B rows
+    32 lanes streamed and 16 lanes of 2 chunks cached, 400-B rows 32 lanes.
+    4 x 4500 bags switch them on; 4 x 1000 stay on the normal mapping.
+    Out-of-range ids, a shard, sum and mean; dyadic tables exactly."""
+    maxL = 30 if hint else 10
+    for values in ("normal", "dyadic"):
+        tables, rows, idx, off = case(T=4, D=D, dtype=dtype, B=B, lengths=("var", 0, maxL), lo=100, hi=2900,
+                                      seed=700 + D + dtype + B + hint, values=values, oob=True)
+        for mode in (wl.SUM, wl.MEAN):
+            got, hits = run(tables, rows, D, dtype, idx, off, B, mode | hint, 100, 2900)
+            ref, ref_hits, mag = oracle.forward(tables, rows, D, dtype, idx, off, B, mode, 100, 2900)
+            assert np.array_equal(hits, ref_hits)
+            if values == "dyadic" and mode == wl.SUM:
+                assert np.array_equal(got.astype(np.float64), ref), "dyadic sums must be bit-exact"
+            else:
+                assert_parity(got, ref, mag, max_bag_len(off, idx.size), dtype)
 
 
 # ----------------------------------------------------------------------------- bag lengths

@@ -260,15 +260,20 @@ def test_weighted_sum_matches_oracle(dtype, D, itype, device):
 
 
 @pytest.mark.parametrize("hint", [0, eb.EB_HINT_STREAM_ROWS])
-@pytest.mark.parametrize("B", [8, 1500, 3000])  # small-batch, normal and two-bags-per-wave mappings
+# small-batch, normal and two-bags-per-wave mappings; 4 x 4500 short bags:
+# narrow teams cached too (512-B rows as 16 lanes of 2 chunks, 1-KB rows as
+# 16 lanes of 4), with int32 ids
+@pytest.mark.parametrize("B", [8, 1500, 3000, 4500])
 def test_weighted_mappings(hint, B, device):
-    maxL = 1200 if B == 8 else 24
-    tables, rows, idx, off, w = weighted_case(128, wl.F32, 40 + B, B=B, maxL=maxL, T=2)
-    dts = [to_device_table(t, wl.F32, device) for t in tables]
-    got, hits = run_ex(dts, rows, idx, off, B, wl.SUM | hint, device, weights=w)
-    ref, ref_hits, mag = oracle.forward(tables, rows, 128, wl.F32, idx, off, B, wl.SUM, weights=w)
-    assert_parity(got.cpu().numpy(), ref, mag, max_bag_len(off, idx.size), wl.F32,
-                  hits.cpu().numpy(), ref_hits)
+    maxL = 1200 if B == 8 else 10 if B == 4500 else 24
+    T, itype = (4, np.int32) if B == 4500 else (2, np.int64)
+    for D in ((128, 256) if B == 4500 else (128,)):
+        tables, rows, idx, off, w = weighted_case(D, wl.F32, 40 + B + D, B=B, maxL=maxL, T=T)
+        dts = [to_device_table(t, wl.F32, device) for t in tables]
+        got, hits = run_ex(dts, rows, idx, off, B, wl.SUM | hint, device, index_dtype=itype, weights=w)
+        ref, ref_hits, mag = oracle.forward(tables, rows, D, wl.F32, idx, off, B, wl.SUM, weights=w)
+        assert_parity(got.cpu().numpy(), ref, mag, max_bag_len(off, idx.size), wl.F32,
+                      hits.cpu().numpy(), ref_hits)
 
 
 def test_weighted_dyadic_exact_and_unit_weights(device):
