@@ -63,8 +63,7 @@ enum { EB_SUM = 0, EB_MEAN = 1 };
  * tables much larger than the 256 MB last-level cache).  It then reads rows of
  * 128 bytes or more with non-temporal loads, which bypass L2 and the
  * last-level cache, gives each XCD a contiguous run of bags, and in large
- * batches pools rows wider than 128 bytes and at most 1 KB with one lane
- * group per bag.  Faster for such ids, slower for skewed ones (hot rows then
+ * batches pools rows of 128 bytes to 1 KB with one lane group per bag.  Faster for such ids, slower for skewed ones (hot rows then
  * miss the caches).  Without the hint, large batches of short bags (a mean
  * length below the rows the library keeps in flight per bag, as in the bags
  * one row block receives in a row-wise exchange) are pooled the same way.  It changes no hit count; by splitting a bag's rows

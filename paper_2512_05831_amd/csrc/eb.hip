@@ -16,9 +16,10 @@
 //     chunks (global_load_dwordx4); surplus lanes of a ragged row idle.
 //   * P such lane groups form the team that pools one bag: group g takes the
 //     bag's rows g, g+P, g+2P, ...; a wave holds 64/(R*P) teams (P = 64/R
-//     for rows of 16 lanes or more).  Large batches of streamed rows, or of
-//     short cached bags, take teams of one lane group instead (two or four
-//     bags per wave; 256-B and 1-KB rows as 16 lanes of 1 or 4 chunks).
+//     for rows of 16 lanes or more, 16/R below).  Large batches of streamed
+//     rows, or of short cached bags, take teams of one lane group instead
+//     (two, four or eight bags per wave; 256-B and 1-KB rows as 16 lanes of
+//     1 or 4 chunks).
 //     Partial sums of the P groups are combined at the end with cross-lane
 //     moves (DPP, ds_swizzle, v_permlane32_swap).
 //   * A team stages a window of its bag's indices in LDS: the window is read

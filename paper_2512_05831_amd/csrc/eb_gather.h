@@ -421,8 +421,8 @@ constexpr int groups_per_bag(int R, bool few, bool single)
     // inside a DPP row.  "single": teams narrower than a wave for large
     // batches, one lane group per bag: rows of 32 lanes two bags per wave,
     // rows read by 16 lanes (256-B rows, and 512-B / 1-KB rows as 2 / 4
-    // chunks per lane) four.
-    return few ? kWave / R : (single && R >= 16 && R < kWave) ? 1 : R >= 16 ? kWave / R : 16 / R;
+    // chunks per lane) four, rows of 8 lanes (up to 128 B) eight.
+    return few ? kWave / R : (single && R >= 8 && R < kWave) ? 1 : R >= 16 ? kWave / R : 16 / R;
 }
 
 using KernelFn = void (*)(GatherArgs);

@@ -140,6 +140,27 @@ def test_narrow_teams(D, dtype, hint, B):
                 assert_parity(got, ref, mag, max_bag_len(off, idx.size), dtype)
 
 
+@pytest.mark.parametrize("D,dtype", [(32, wl.F32), (64, wl.F16), (48, wl.BF16)])
+@pytest.mark.parametrize("hint", [0, eb.EB_HINT_STREAM_ROWS])
+def test_eight_lane_teams(D, dtype, hint):
+    """Rows of 8 lanes (128-B rows, and 96-B rows of 6 chunks) in batches of
+    4 x 8500 bags: 8-lane teams, eight bags per wave, when streamed (128-B
+    rows) or when the bags are short (cached).  Sum and mean, a shard,
+    out-of-range ids; dyadic tables exactly."""
+    maxL = 12 if hint else 6
+    for values in ("normal", "dyadic"):
+        tables, rows, idx, off = case(T=4, D=D, dtype=dtype, B=8500, lengths=("var", 0, maxL), lo=100,
+                                      hi=2900, seed=900 + D + dtype + hint, values=values, oob=True)
+        for mode in (wl.SUM, wl.MEAN):
+            got, hits = run(tables, rows, D, dtype, idx, off, 8500, mode | hint, 100, 2900)
+            ref, ref_hits, mag = oracle.forward(tables, rows, D, dtype, idx, off, 8500, mode, 100, 2900)
+            assert np.array_equal(hits, ref_hits)
+            if values == "dyadic" and mode == wl.SUM:
+                assert np.array_equal(got.astype(np.float64), ref), "dyadic sums must be bit-exact"
+            else:
+                assert_parity(got, ref, mag, max_bag_len(off, idx.size), dtype)
+
+
 # ----------------------------------------------------------------------------- bag lengths
 
 
