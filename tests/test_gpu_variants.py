@@ -223,6 +223,32 @@ def test_strided_output_keeps_other_columns(pad, device):
     assert_parity(got[written], placed[written], mplaced[written], max_bag_len(off, idx.size), wl.F32)
 
 
+@pytest.mark.parametrize("D,hint", [(256, eb.EB_HINT_STREAM_ROWS), (128, 0), (32, eb.EB_HINT_STREAM_ROWS)])
+def test_narrow_teams_strided_output(D, hint, device):
+    """Large batches in narrow teams (1-KB rows as 16 lanes of 4 chunks,
+    512-B short cached bags as 16 lanes of 2, 128-B rows as 8 lanes) writing
+    a column window of a wider buffer with int32 ids: only the tables'
+    columns change."""
+    T, B = 4, 8500
+    tables, rows, idx, off = make_case(T=T, D=D, dtype=wl.F32, B=B, seed=71 + D, maxL=8)
+    dts = [to_device_table(w, wl.F32, device) for w in tables]
+    W = T * D + 12
+    big = torch.full((B, W), float("nan"), dtype=torch.float32, device=device)
+    cols = [3 * D + 12, D, 0, 2 * D + 8]  # tables out of order, gaps between them
+    run_ex(dts, rows, idx, off, B, wl.SUM | hint, device, index_dtype=np.int32, out=big, out_cols=cols,
+           hits=False)
+    got = big.cpu().numpy()
+    ref, _, mag = oracle.forward(tables, rows, D, wl.F32, idx, off, B, wl.SUM)
+    placed = np.full((B, W), np.nan)
+    mplaced = np.full((B, W), np.nan)
+    for t, c in enumerate(cols):
+        placed[:, c:c + D] = ref[:, t * D:(t + 1) * D]
+        mplaced[:, c:c + D] = mag[:, t * D:(t + 1) * D]
+    written = ~np.isnan(placed)
+    assert np.all(np.isnan(got[~written])), "columns outside the tables were touched"
+    assert_parity(got[written], placed[written], mplaced[written], max_bag_len(off, idx.size), wl.F32)
+
+
 def test_more_tables_than_one_launch_reversed_columns(device):
     T, D, B = 70, 8, 9
     tables, rows, idx, off = make_case(T=T, D=D, dtype=wl.BF16, B=B, rows=400, seed=61, maxL=20)
