@@ -315,7 +315,8 @@ def exchange_bench(torch, dev, eb, K, W):
                       "us_per_call": round(us, 1), "ids_per_s": idx.size / us * 1e6,
                       "algorithmic_bytes": by, "algorithmic_GBps": round(by / us / 1e3, 1),
                       "frac_of_8TBps": round(by / us / 1e3 / HBM_PEAK_GBPS, 4),
-                      "kernels_per_call": 5}), flush=True)
+                      # count, tile sums, (tile prefix when over 16384 tile sums,) tile scan, scatter
+                      "kernels_per_call": 4 if G * -(-TB // 2048) <= 16384 else 5}), flush=True)
     del d_i, out_idx
     B, T, D = 65536 // G, 1, 256
     # six receive buffers cycled (400 MB), so the last-level cache cannot hold the input

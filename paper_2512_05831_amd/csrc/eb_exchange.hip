@@ -26,8 +26,10 @@
 //                (coalesced per destination).
 //   2. scan    : inclusive scan of every destination's row of counts
 //                (reduce-then-scan over 2048-entry tiles: tile sums in the
-//                workspace, one workgroup scans all rows' tile sums as one
-//                sequence, which also gives the segments).
+//                workspace; each tile then adds up its row's earlier tiles,
+//                and the rows' first tiles the segments; with more than
+//                16384 tile sums one workgroup first scans them as one
+//                sequence instead).
 //   3. scatter : same waves; ids are written to segments[g] +
 //                out_offsets[g][p] + rank, the rank counting earlier ids of
 //                the bag with the same owner (per 64-id chunk: three ballots
@@ -306,7 +308,12 @@ struct ScanArgs {
     int64_t TB;
     int32_t G;
     int32_t ntiles;
+    int32_t fused;      // pass 2c takes the tile prefixes and segments from the raw tile sums
 };
+
+// Pass 2c adds up the earlier tile sums itself (no pass 2b) while every
+// workgroup reads at most this many of them.
+constexpr int64_t kFusedScanMax = 16384;
 
 constexpr int kScanPer = kScanTile / kBlock; // counts per thread in a tile
 constexpr int kPrefixRegs = 16;              // tile sums per thread held in registers
@@ -418,7 +425,11 @@ __global__ __launch_bounds__(kBlock) void eb_scan_tile_prefix(const ScanArgs a)
 
 // Pass 2c: scan every tile and add its prefix, in place.  The tile passes
 // through LDS so that each thread scans kScanPer consecutive counts of its
-// own and a single block-wide scan joins the threads.
+// own and a single block-wide scan joins the threads.  Fused (few tiles in
+// all): the tile's prefix is the sum of its row's earlier tiles, and each
+// row's first tile also writes the row's segment start (the sum of all
+// earlier rows' tiles; the last row also the total), which saves pass 2b's
+// launch.
 __device__ __forceinline__ int scan_slot(int e) { return e + e / kScanPer; } // conflict-free row reads
 
 __global__ __launch_bounds__(kBlock) void eb_scan_tiles(const ScanArgs a)
@@ -429,12 +440,36 @@ __global__ __launch_bounds__(kBlock) void eb_scan_tiles(const ScanArgs a)
     int64_t *row = a.rows + (int64_t)g * (a.TB + 1) + 1;
     const int64_t lo = (int64_t)k * kScanTile;
     const int n = (int)std::min<int64_t>(kScanTile, a.TB - lo);
-    const int64_t carry = a.tile_sums[(int64_t)g * a.ntiles + k];
     int64_t v[kScanPer];
 #pragma unroll
     for (int j = 0; j < kScanPer; ++j) {
         const int i = j * kBlock + threadIdx.x;
         v[j] = i < n ? row[lo + i] : 0;
+    }
+    const int64_t row0 = (int64_t)g * a.ntiles;
+    int64_t carry;
+    if (a.fused) {
+        int64_t c = 0;
+        for (int j = threadIdx.x; j < k; j += kBlock) c += a.tile_sums[row0 + j];
+        block_inclusive_scan(c, &carry);
+        if (k == 0) {
+            const int64_t upto = g == a.G - 1 ? (int64_t)a.G * a.ntiles : row0;
+            int64_t before = 0, all = 0;
+            for (int64_t j = threadIdx.x; j < upto; j += kBlock) {
+                const int64_t x = a.tile_sums[j];
+                if (j < row0) before += x;
+                all += x;
+            }
+            int64_t seg, total;
+            block_inclusive_scan(before, &seg);
+            block_inclusive_scan(all, &total);
+            if (threadIdx.x == 0) {
+                a.segments[g] = seg;
+                if (g == a.G - 1) a.segments[a.G] = total;
+            }
+        }
+    } else {
+        carry = a.tile_sums[row0 + k];
     }
 #pragma unroll
     for (int j = 0; j < kScanPer; ++j) sm[scan_slot(j * kBlock + threadIdx.x)] = v[j];
@@ -736,6 +771,7 @@ int eb_bucketize(int32_t T, int64_t B, int32_t G, const int64_t *bounds, const i
     sa.TB = TB;
     sa.G = G;
     sa.ntiles = (int32_t)scan_tiles(TB);
+    sa.fused = (int64_t)G * sa.ntiles <= kFusedScanMax ? 1 : 0;
 
     if (TB > 0) {
         void *args[] = {&ba};
@@ -744,7 +780,7 @@ int eb_bucketize(int32_t T, int64_t B, int32_t G, const int64_t *bounds, const i
         if (err != hipSuccess) return fail(EB_ERR_HIP, std::string("eb_bucketize: ") + hipGetErrorString(err));
         void *sargs[] = {&sa};
         err = hipLaunchKernel((const void *)eb_scan_tile_sums, dim3(sa.ntiles, G), dim3(kBlock), sargs, 0, st);
-        if (err == hipSuccess)
+        if (err == hipSuccess && !sa.fused)
             err = hipLaunchKernel((const void *)eb_scan_tile_prefix, dim3(1), dim3(kBlock), sargs, 0, st);
         if (err == hipSuccess)
             err = hipLaunchKernel((const void *)eb_scan_tiles, dim3(sa.ntiles, G), dim3(kBlock), sargs, 0, st);
