@@ -305,19 +305,59 @@ __global__ __launch_bounds__(kBlock) void eb_gather_team(const GatherArgs a)
                 }
             }
         }
-        for (; k < n; k += P) {
-            const uint32_t r = my_stage[k];
-            if (r != kInvalidRow) {
-                const char *p = base + (size_t)r * row_bytes;
-                uint4 v[C];
+        // The window's last rows (fewer than U for this group) in one
+        // predicated pass, rows past the end reading as the invalid marker:
+        // a bag's tail costs one round trip instead of one per row, and the
+        // rows are added in the same order.  With U = 1 there is no tail; the
+        // row-at-a-time loop kept there never runs, but without it the
+        // compiler allocates the main loop's registers so that it waits for
+        // loads still in flight (2.5% slower for 1-KB rows).
+        if constexpr (U == 1) {
+            for (; k < n; k += P) {
+                const uint32_t r = my_stage[k];
+                if (r != kInvalidRow) {
+                    const char *p = base + (size_t)r * row_bytes;
+                    uint4 v[C];
 #pragma unroll
-                for (int c = 0; c < C; ++c) v[c] = load_chunk<kStream>(p + coff[c]);
-                ++count;
-                const float w = kW ? my_wstage[k] : 1.f;
+                    for (int c = 0; c < C; ++c) v[c] = load_chunk<kStream>(p + coff[c]);
+                    ++count;
+                    const float w = kW ? my_wstage[k] : 1.f;
 #pragma unroll
-                for (int c = 0; c < C; ++c) {
-                    if constexpr (kW) Elem<DT>::fma(acc + c * kEpc, v[c], w);
-                    else Elem<DT>::add(acc + c * kEpc, v[c]);
+                    for (int c = 0; c < C; ++c) {
+                        if constexpr (kW) Elem<DT>::fma(acc + c * kEpc, v[c], w);
+                        else Elem<DT>::add(acc + c * kEpc, v[c]);
+                    }
+                }
+            }
+        } else {
+            if (k < n) {
+                uint32_t rr[U - 1];
+                float ww[U - 1];
+#pragma unroll
+                for (int u = 0; u < U - 1; ++u) {
+                    const bool in = k + u * P < n;
+                    rr[u] = in ? my_stage[k + u * P] : kInvalidRow;
+                    if constexpr (kW) ww[u] = in ? my_wstage[k + u * P] : 0.f;
+                }
+                uint4 v[U - 1][C];
+#pragma unroll
+                for (int u = 0; u < U - 1; ++u) {
+#pragma unroll
+                    for (int c = 0; c < C; ++c) v[u][c] = make_uint4(0, 0, 0, 0);
+                    if (rr[u] != kInvalidRow) {
+                        const char *p = base + (size_t)rr[u] * row_bytes;
+#pragma unroll
+                        for (int c = 0; c < C; ++c) v[u][c] = load_chunk<kStream>(p + coff[c]);
+                    }
+                }
+#pragma unroll
+                for (int u = 0; u < U - 1; ++u) {
+                    count += rr[u] != kInvalidRow;
+#pragma unroll
+                    for (int c = 0; c < C; ++c) {
+                        if constexpr (kW) Elem<DT>::fma(acc + c * kEpc, v[u][c], ww[u]);
+                        else Elem<DT>::add(acc + c * kEpc, v[u][c]);
+                    }
                 }
             }
         }
