@@ -26,7 +26,8 @@
 //     with coalesced index loads, filtered against the shard, and rewritten as
 //     32-bit local row numbers (or an invalid marker).  The gather loop then
 //     reads them from LDS and keeps U rows per group in flight (unrolled;
-//     U = 2 for streamed rows of 128 B or more, else 6).
+//     U = 2 for streamed rows of 128 B or more, else 6; 8 in small batches),
+//     a bag's last rows in one predicated pass.
 //   * Accumulation is fp32; fp16 / bf16 rows are widened exactly.
 //   * Workgroups are 4 waves, bags in table-major order.  The hardware deals
 //     workgroups to the 8 XCDs round-robin, so by default all XCDs work on
@@ -71,7 +72,7 @@ struct Shape {
 
 // Small batches.  A launch whose normal mapping has fewer waves than the GPU
 // holds (256 CUs x 32) leaves it partly idle, and each bag's chain of
-// dependent loads sets the time.  One wave per bag with 6 rows in flight per
+// dependent loads sets the time.  One wave per bag with 8 rows in flight per
 // lane then wins when bags are long (more than twice the rows the normal
 // mapping keeps in flight per bag) and few enough (measured over the paper's
 // single-GPU shapes: up to 1.5x faster, never slower).

@@ -472,13 +472,13 @@ using KernelFn = void (*)(GatherArgs);
 // queue; narrower rows need more requests per byte in flight, and cached rows
 // profit from deeper overlap while hits return early.  A small batch (fewer
 // bags than fill the GPU) is bound by each bag's chain of dependent loads
-// instead: every bag then gets a whole wave and 6 rows in flight per lane.
+// instead: every bag then gets a whole wave and 8 rows in flight per lane.
 template <typename IT, int DT, int R, int C, bool kFew, bool kW>
 KernelFn team_kernel(bool stream, bool single)
 {
     constexpr int P = groups_per_bag(R, kFew, false);
     constexpr int P_SINGLE = groups_per_bag(R, kFew, true);
-    constexpr int U_CACHED = C >= 6 ? 1 : 6 / C;
+    constexpr int U_CACHED = kFew ? (C >= 8 ? 1 : 8 / C) : (C >= 6 ? 1 : 6 / C);
     constexpr int U_STREAM = (!kFew && R * C >= 8) ? (C >= 2 ? 1 : 2) : U_CACHED;
     if (!stream) {
         if constexpr (P_SINGLE != P) {
