@@ -14,12 +14,15 @@
 //   eb_sum_partials  adds the G partial blocks received for this GPU's bags
 //                    (optionally dividing by the bag lengths for mean).
 //
-// Both are HBM-bound integer / streaming work; nothing here is a contraction.
+// Both are integer / streaming work priced against HBM (nothing here is a
+// contraction); eb_sum_partials is bound by it, eb_bucketize by its waves'
+// chains of dependent loads and by instruction issue.
 //
 // eb_bucketize runs three kernels on the caller's stream:
 //   1. count   : a wave takes 16 consecutive bags; each id's owner by
-//                comparison with the table's block bounds (up to 8 blocks) or
-//                by binary search over them (staged in LDS); for ordinary CSR
+//                comparisons with the table's block bounds (up to 8 blocks:
+//                a search tree evaluated as wave-wide lane masks) or by
+//                binary search over them (staged in LDS); for ordinary CSR
 //                offsets the wave streams its whole id range in 64-id chunks
 //                into a [bag][destination] histogram in LDS, else it walks the
 //                bags one at a time; counts land in out_offsets[g][p + 1]
@@ -104,15 +107,49 @@ __device__ __forceinline__ FewBounds few_bounds(const int64_t *bnd, int G)
     return b;
 }
 
-// owner_of for G <= 8 by comparisons: -1 outside [lo, hi), else the number of
-// inner bounds at or below i, which for non-decreasing bounds is the block
-// holding i.  Always -1 or in [0, G).
-__device__ __forceinline__ int few_owner(const FewBounds &b, int64_t i)
+// owner_of for G <= 8 by comparisons, as the three bits of the owner: a
+// search tree over the 7 inner bounds, m_j = [i >= inner bound j]:
+//   bit 2 = m_3,  bit 1 = bit 2 ? m_5 : m_1,
+//   bit 0 = bit 2 ? (bit 1 ? m_6 : m_4) : (bit 1 ? m_2 : m_0).
+// For non-decreasing bounds this is the number of inner bounds at or below
+// i, the block holding i.  The wave computes it as lane masks: one compare
+// per bound, the selections on the scalar unit, and each lane reads its own
+// bits back from the masks.  For any bounds a valid id's owner stays below
+// G: a leaf at or above G lies past a right turn at an unused inner bound
+// (INT64_MAX), which no id below hi reaches.
+struct FewMasks {
+    uint64_t valid;      // lanes of `in` with lo <= i < hi
+    uint64_t b0, b1, b2; // lanes whose owner has bit 0, 1, 2 set
+};
+
+__device__ __forceinline__ FewMasks few_owner_masks(const FewBounds &b, int64_t i, uint64_t in)
 {
-    int g = 0;
-#pragma unroll
-    for (int j = 0; j < kFewShards - 1; ++j) g += i >= b.inner[j] ? 1 : 0;
-    return (i >= b.lo && i < b.hi) ? g : -1;
+    const uint64_t m0 = __ballot(i >= b.inner[0]), m1 = __ballot(i >= b.inner[1]), m2 = __ballot(i >= b.inner[2]),
+                   m3 = __ballot(i >= b.inner[3]), m4 = __ballot(i >= b.inner[4]), m5 = __ballot(i >= b.inner[5]),
+                   m6 = __ballot(i >= b.inner[6]);
+    FewMasks o;
+    o.valid = in & __ballot(i >= b.lo) & __ballot(i < b.hi);
+    o.b2 = m3;
+    o.b1 = (m3 & m5) | (~m3 & m1);
+    const uint64_t upper = (o.b1 & m6) | (~o.b1 & m4), lower = (o.b1 & m2) | (~o.b1 & m0);
+    o.b0 = (m3 & upper) | (~m3 & lower);
+    return o;
+}
+
+// This lane's bit of a wave mask.
+__device__ __forceinline__ bool lane_bit(uint64_t m) { return __builtin_amdgcn_inverse_ballot_w64(m); }
+
+// The lanes below n, for any n (a wave-uniform value, so scalar work).
+__device__ __forceinline__ uint64_t lanes_below(int n)
+{
+    return n >= kWave ? ~0ull : n <= 0 ? 0ull : (1ull << n) - 1;
+}
+
+// This lane's owner from the masks, times the given scale (a power of two).
+template <int kScale>
+__device__ __forceinline__ int few_bits(const FewMasks &o)
+{
+    return (lane_bit(o.b0) ? kScale : 0) | (lane_bit(o.b1) ? 2 * kScale : 0) | (lane_bit(o.b2) ? 4 * kScale : 0);
 }
 
 // Number of set bits of m in the lanes below this one.
@@ -147,7 +184,10 @@ struct BucketArgs {
 };
 
 // Dynamic LDS: the table's G+1 bounds, then one area per wave.
-__host__ __device__ inline size_t count_wave_bytes(int G) { return (size_t)4 * G * (G <= kFastShards ? kBagsPerWave : 1); }
+// count's histogram row per bag: 8 entries for up to 8 destinations (an
+// index by shift), else G.
+__host__ __device__ inline int count_stride(int G) { return G <= kFewShards ? kFewShards : G; }
+__host__ __device__ inline size_t count_wave_bytes(int G) { return (size_t)4 * (G <= kFastShards ? count_stride(G) * kBagsPerWave : G); }
 __host__ __device__ inline size_t count_lds_bytes(int G) { return (size_t)(G + 1) * 8 + kWavesPerBlock * count_wave_bytes(G); }
 __host__ __device__ inline size_t scatter_lds_bytes(int G) { return (size_t)(G + 1) * 8 + (size_t)kWavesPerBlock * G * 8; }
 
@@ -192,6 +232,64 @@ __device__ __forceinline__ void wave_sync_lds()
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+// count's loop over the wave's ids [S, E) for contiguous bags (bag l of the
+// wave starts at lane l's s; bags = lanes holding a bag): adds each id with
+// an owner to hist[bag * count_stride(G) + owner].
+// One pass of count's loop: the ids at k0 + u * 64 + lane, the first R of
+// them (all kCountChunks * 64 when kFull, the usual case, which then needs
+// no tail masks).
+template <bool kFew, bool kFull>
+__device__ __forceinline__ void count_pass(const BucketArgs &a, const int64_t *bnd, const FewBounds &fb, int *hist,
+                                           int lane, int64_t s, uint64_t bags, int64_t k0, int R)
+{
+    const int64_t *src = a.indices + k0 + lane;
+    int64_t id[kCountChunks];
+#pragma unroll
+    for (int u = 0; u < kCountChunks; ++u)
+        id[u] = (kFull || lane_bit(lanes_below(R - u * kWave))) ? __builtin_nontemporal_load(src + u * kWave) : 0;
+#pragma unroll
+    for (int u = 0; u < kCountChunks; ++u) {
+        // The bag of position k is the last one starting at or
+        // before k: the bags starting by the chunk's first position,
+        // plus one for each bag starting inside the chunk at or
+        // below this lane (bag starts ascend for these offsets).
+        const int64_t kb = k0 + u * kWave;
+        const uint64_t started = bags & __ballot(s <= kb);
+        uint64_t inside = bags & ~started & __ballot(s < kb + kWave);
+        int l = __popcll(started) - 1;
+        while (inside) {
+            const int o = __builtin_amdgcn_readlane((int)(uint32_t)s, __builtin_ctzll(inside)) - (int)(uint32_t)kb;
+            l += lane >= o ? 1 : 0;
+            inside &= inside - 1;
+        }
+        const uint64_t in = kFull ? ~0ull : lanes_below(R - u * kWave);
+        if constexpr (kFew) {
+            const FewMasks o = few_owner_masks(fb, id[u], in);
+            if (lane_bit(o.valid)) atomicAdd(&hist[l * kFewShards + few_bits<1>(o)], 1);
+        } else if (lane_bit(in)) {
+            const int g = owner_of(bnd, a.G, id[u]);
+            if (g >= 0) atomicAdd(&hist[l * a.G + g], 1);
+        }
+    }
+}
+
+// count's loop over the wave's ids [S, E) for contiguous bags (bag l of the
+// wave starts at lane l's s; bags = lanes holding a bag): adds each id with
+// an owner to hist[bag * count_stride(G) + owner].
+template <bool kFew>
+__device__ __forceinline__ void count_chunks(const BucketArgs &a, const int64_t *bnd, const FewBounds &fb, int *hist,
+                                             int lane, int64_t s, uint64_t bags, int64_t S, int64_t E)
+{
+    constexpr int kPass = kCountChunks * kWave;
+    for (int64_t k0 = S; k0 < E; k0 += kPass) {
+        const int R = __builtin_amdgcn_readfirstlane((int)min<int64_t>(E - k0, (int64_t)kPass));
+        if (R == kPass)
+            count_pass<kFew, true>(a, bnd, fb, hist, lane, s, bags, k0, R);
+        else
+            count_pass<kFew, false>(a, bnd, fb, hist, lane, s, bags, k0, R);
+    }
+}
+
 __global__ __launch_bounds__(kBlock) void eb_bucket_count(const BucketArgs a)
 {
     extern __shared__ int64_t lds[];
@@ -215,42 +313,17 @@ __global__ __launch_bounds__(kBlock) void eb_bucket_count(const BucketArgs a)
     const bool contiguous = wave_bags(a, p0, nb, lane, s, e, S, E);
 
     if (contiguous && G <= kFastShards) {
-        const FewBounds fb = few_bounds(bnd, G <= kFewShards ? G : 0);
         const uint64_t bags = __ballot(lane < nb);
-        for (int x = lane; x < kBagsPerWave * G; x += kWave) hist[x] = 0;
+        for (int x = lane; x < kBagsPerWave * count_stride(G); x += kWave) hist[x] = 0;
         wave_sync_lds();
-        for (int64_t k0 = S; k0 < E; k0 += kCountChunks * kWave) {
-            int64_t id[kCountChunks];
-#pragma unroll
-            for (int u = 0; u < kCountChunks; ++u) {
-                const int64_t k = k0 + u * kWave + lane;
-                id[u] = k < E ? __builtin_nontemporal_load(a.indices + k) : 0;
-            }
-#pragma unroll
-            for (int u = 0; u < kCountChunks; ++u) {
-                // The bag of position k is the last one starting at or
-                // before k: the bags starting by the chunk's first position,
-                // plus one for each bag starting inside the chunk at or
-                // below this lane (bag starts ascend for these offsets).
-                const int64_t kb = k0 + u * kWave;
-                const uint64_t started = bags & __ballot(s <= kb);
-                uint64_t inside = bags & ~started & __ballot(s < kb + kWave);
-                int l = __popcll(started) - 1;
-                while (inside) {
-                    const int o = __builtin_amdgcn_readlane((int)(uint32_t)s, __builtin_ctzll(inside)) - (int)(uint32_t)kb;
-                    l += lane >= o ? 1 : 0;
-                    inside &= inside - 1;
-                }
-                const int64_t k = kb + lane;
-                if (k < E) {
-                    const int g = G <= kFewShards ? few_owner(fb, id[u]) : owner_of(bnd, G, id[u]);
-                    if (g >= 0) atomicAdd(&hist[l * G + g], 1);
-                }
-            }
-        }
+        if (G <= kFewShards)
+            count_chunks<true>(a, bnd, few_bounds(bnd, G), hist, lane, s, bags, S, E);
+        else
+            count_chunks<false>(a, bnd, FewBounds{}, hist, lane, s, bags, S, E);
         wave_sync_lds();
+        const int stride = count_stride(G);
         for (int g = 0; g < G; ++g)
-            if (lane < nb) a.out_offsets[(int64_t)g * row + p0 + lane + 1] = hist[lane * G + g];
+            if (lane < nb) a.out_offsets[(int64_t)g * row + p0 + lane + 1] = hist[lane * stride + g];
         return;
     }
     // Any offsets, any G: one bag at a time.
@@ -512,6 +585,59 @@ __device__ __forceinline__ void scatter_chunk(const BucketArgs &a, int64_t *next
     }
 }
 
+// One pass of the scatter for contiguous bags and at most 8 destinations:
+// the ids at k0 + u * 64 + lane, the first R of them (all kScatterChunks * 64
+// when kFull, the usual case, which then needs no tail masks).  Ballots of
+// the owner's bits give every id of a chunk its rank among the chunk's ids
+// for the same destination; a single store then places the whole chunk.
+// Lane d < G holds destination d's next output slot in `slot`; l0..l2 are the
+// complements of the lane's low three bits as all-ones / zero masks.
+template <bool kFull>
+__device__ __forceinline__ void scatter_few_pass(const BucketArgs &a, const FewBounds &fb, int lane, uint32_t l0,
+                                                 uint32_t l1, uint32_t l2, int64_t &slot, int64_t k0, int R)
+{
+    const int64_t *src = a.indices + k0 + lane;
+    int64_t id[kScatterChunks];
+#pragma unroll
+    for (int u = 0; u < kScatterChunks; ++u)
+        id[u] = (kFull || lane_bit(lanes_below(R - u * kWave))) ? __builtin_nontemporal_load(src + u * kWave) : 0;
+    // Rank all chunks first, store afterwards: loads and stores share one
+    // completion counter, so a store between two chunks would make the next
+    // chunk wait for it.
+    int64_t pos[kScatterChunks];
+#pragma unroll
+    for (int u = 0; u < kScatterChunks; ++u) {
+        const FewMasks o = few_owner_masks(fb, id[u], kFull ? ~0ull : lanes_below(R - u * kWave));
+        // The lanes sharing this lane's owner are the valid ones agreeing
+        // with it on every bit (b ^ ~x keeps the lanes whose bit equals x's).
+        const uint64_t valid = o.valid, b0 = o.b0, b1 = o.b1, b2 = o.b2;
+        const bool ok = lane_bit(valid);
+        const uint32_t n0 = lane_bit(~b0) ? ~0u : 0u, n1 = lane_bit(~b1) ? ~0u : 0u, n2 = lane_bit(~b2) ? ~0u : 0u;
+        const uint32_t same_lo = (uint32_t)valid & ((uint32_t)b0 ^ n0) & ((uint32_t)b1 ^ n1) & ((uint32_t)b2 ^ n2);
+        const uint32_t same_hi = (uint32_t)(valid >> 32) & ((uint32_t)(b0 >> 32) ^ n0) &
+                                 ((uint32_t)(b1 >> 32) ^ n1) & ((uint32_t)(b2 >> 32) ^ n2);
+        const int rank = (int)__builtin_amdgcn_mbcnt_hi(same_hi, __builtin_amdgcn_mbcnt_lo(same_lo, 0u));
+        // This lane's slot from the lane numbered by its owner's bits (a
+        // lane below 8 where not valid: unused); the permute takes the
+        // source lane as a byte offset.
+        const int from = few_bits<4>(o);
+        const int base_lo = __builtin_amdgcn_ds_bpermute(from, (int)(uint32_t)slot);
+        const int base_hi = __builtin_amdgcn_ds_bpermute(from, (int)(slot >> 32));
+        const int64_t base = ((int64_t)base_hi << 32) | (uint32_t)base_lo;
+        pos[u] = ok ? base + rank : -1;
+        // Lane d advances destination d's slot by the chunk's ids for d: the
+        // same agreement, with d's bits in place of the owner's.
+        const uint32_t own_lo = (uint32_t)valid & ((uint32_t)b0 ^ l0) & ((uint32_t)b1 ^ l1) & ((uint32_t)b2 ^ l2);
+        const uint32_t own_hi = (uint32_t)(valid >> 32) & ((uint32_t)(b0 >> 32) ^ l0) & ((uint32_t)(b1 >> 32) ^ l1) &
+                                ((uint32_t)(b2 >> 32) ^ l2);
+        slot += __popc(own_lo) + __popc(own_hi);
+    }
+    __builtin_amdgcn_sched_barrier(0); // keep the stores after all ranking
+#pragma unroll
+    for (int u = 0; u < kScatterChunks; ++u)
+        if ((uint64_t)pos[u] < (uint64_t)a.out_cap) a.out_indices[pos[u]] = id[u];
+}
+
 __global__ __launch_bounds__(kBlock) void eb_bucket_scatter(const BucketArgs a)
 {
     extern __shared__ int64_t lds[];
@@ -532,59 +658,19 @@ __global__ __launch_bounds__(kBlock) void eb_bucket_scatter(const BucketArgs a)
     int64_t s, e, S, E;
     const bool contiguous = wave_bags(a, p0, nb, lane, s, e, S, E);
     if (contiguous && G <= kBallotShards) {
-        // Contiguous bags, few destinations: ballots of the owner's bits give
-        // every id of a chunk its rank among the chunk's ids for the same
-        // destination; a single store then places the whole chunk.
+        // Contiguous bags, few destinations: ranks from ballots of the
+        // owners' bits (scatter_few_pass).
         const FewBounds fb = few_bounds(bnd, G);
-        // Lane d < G keeps destination d's next output slot; l0..l2 are the
-        // complements of this lane's low three bits as all-ones / zero masks.
         int64_t slot = lane < G ? a.segments[lane] + a.out_offsets[(int64_t)lane * row + p0] : 0;
         const uint32_t l0 = (uint32_t)(lane & 1) - 1u, l1 = (uint32_t)((lane >> 1) & 1) - 1u,
                        l2 = (uint32_t)((lane >> 2) & 1) - 1u;
-        for (int64_t k0 = S; k0 < E; k0 += kScatterChunks * kWave) {
-            int64_t id[kScatterChunks];
-#pragma unroll
-            for (int u = 0; u < kScatterChunks; ++u) {
-                const int64_t k = k0 + u * kWave + lane;
-                id[u] = k < E ? __builtin_nontemporal_load(a.indices + k) : 0;
-            }
-            // Rank all chunks first, store afterwards: loads and stores
-            // share one completion counter, so a store between two chunks
-            // would make the next chunk wait for it.
-            int64_t pos[kScatterChunks];
-#pragma unroll
-            for (int u = 0; u < kScatterChunks; ++u) {
-                const int64_t k = k0 + u * kWave + lane;
-                const int g = k < E ? few_owner(fb, id[u]) : -1;
-                // The owner's three bits as ballots: the lanes sharing this
-                // lane's owner are the valid ones agreeing with it on every
-                // bit (b ^ ~x keeps the lanes whose bit equals x's).
-                const uint64_t valid = __ballot(g >= 0);
-                const uint64_t b0 = __ballot(g & 1), b1 = __ballot(g & 2), b2 = __ballot(g & 4);
-                const uint32_t n0 = (uint32_t)(g & 1) - 1u, n1 = (uint32_t)((g >> 1) & 1) - 1u,
-                               n2 = (uint32_t)((g >> 2) & 1) - 1u;
-                const uint32_t same_lo = (uint32_t)valid & ((uint32_t)b0 ^ n0) & ((uint32_t)b1 ^ n1) &
-                                         ((uint32_t)b2 ^ n2);
-                const uint32_t same_hi = (uint32_t)(valid >> 32) & ((uint32_t)(b0 >> 32) ^ n0) &
-                                         ((uint32_t)(b1 >> 32) ^ n1) & ((uint32_t)(b2 >> 32) ^ n2);
-                const int rank = (int)__builtin_amdgcn_mbcnt_hi(same_hi, __builtin_amdgcn_mbcnt_lo(same_lo, 0u));
-                // This lane's slot from lane g (any lane for g < 0: unused).
-                const int src = g & (kWave - 1);
-                const int base_lo = __shfl((int)(uint32_t)slot, src);
-                const int base_hi = __shfl((int)(slot >> 32), src);
-                const int64_t base = ((int64_t)base_hi << 32) | (uint32_t)base_lo;
-                pos[u] = g >= 0 ? base + rank : -1;
-                // Lane d advances destination d's slot by the chunk's ids
-                // for d: the same agreement, with d's bits in place of g's.
-                const uint32_t own_lo = (uint32_t)valid & ((uint32_t)b0 ^ l0) & ((uint32_t)b1 ^ l1) & ((uint32_t)b2 ^ l2);
-                const uint32_t own_hi = (uint32_t)(valid >> 32) & ((uint32_t)(b0 >> 32) ^ l0) &
-                                        ((uint32_t)(b1 >> 32) ^ l1) & ((uint32_t)(b2 >> 32) ^ l2);
-                slot += __popc(own_lo) + __popc(own_hi);
-            }
-            __builtin_amdgcn_sched_barrier(0); // keep the stores after all ranking
-#pragma unroll
-            for (int u = 0; u < kScatterChunks; ++u)
-                if ((uint64_t)pos[u] < (uint64_t)a.out_cap) a.out_indices[pos[u]] = id[u];
+        constexpr int kPass = kScatterChunks * kWave;
+        for (int64_t k0 = S; k0 < E; k0 += kPass) {
+            const int R = __builtin_amdgcn_readfirstlane((int)min<int64_t>(E - k0, (int64_t)kPass));
+            if (R == kPass)
+                scatter_few_pass<true>(a, fb, lane, l0, l1, l2, slot, k0, R);
+            else
+                scatter_few_pass<false>(a, fb, lane, l0, l1, l2, slot, k0, R);
         }
         return;
     }
