@@ -205,19 +205,26 @@ __device__ __forceinline__ int64_t readlane64(int64_t v, int l)
     return ((int64_t)hi << 32) | (uint32_t)lo;
 }
 
-// The wave's bags: lane l < nb gets bag p0+l's clamped range [s, e).  Returns
-// whether those ranges tile [S, E) in bag order (ordinary CSR offsets), the
-// case where position order within the wave is (bag, position) order.
-__device__ __forceinline__ bool wave_bags(const BucketArgs &a, int64_t p0, int nb, int lane,
-                                          int64_t &s, int64_t &e, int64_t &S, int64_t &E)
+// The wave's bags, in two steps so that other loads can be issued between
+// them: wave_bag_loads gives lane l < nb bag p0+l's raw offsets [s, e);
+// wave_bags clamps them and returns whether the ranges tile [S, E) in bag
+// order (ordinary CSR offsets), the case where position order within the
+// wave is (bag, position) order.
+__device__ __forceinline__ void wave_bag_loads(const BucketArgs &a, int64_t p0, int nb, int lane, int64_t &s,
+                                               int64_t &e)
 {
     s = 0;
     e = 0;
     if (lane < nb) {
         s = a.offsets[p0 + lane];
         e = a.offsets[p0 + lane + 1];
-        clamp_bag(s, e, a.nnz);
     }
+}
+
+__device__ __forceinline__ bool wave_bags(const BucketArgs &a, int nb, int lane, int64_t &s, int64_t &e, int64_t &S,
+                                          int64_t &E)
+{
+    if (lane < nb) clamp_bag(s, e, a.nnz);
     const int64_t s_next = shfl_down64(s, 1);
     const bool gap = lane + 1 < nb && e != s_next;
     S = readlane64(s, 0);
@@ -299,18 +306,21 @@ __global__ __launch_bounds__(kBlock) void eb_bucket_count(const BucketArgs a)
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = threadIdx.x / kWave;
     int *hist = (int *)((char *)(lds + G + 1) + wave * count_wave_bytes(G));
-    for (int g = threadIdx.x; g <= G; g += kBlock) bnd[g] = a.bounds[(int64_t)t * (G + 1) + g];
-    __syncthreads();
-
     const int64_t b0 = (int64_t)(blockIdx.x - t * a.blocks_per_table) * kBagsPerBlock + wave * kBagsPerWave;
-    if (b0 >= a.B) return; // no block-wide barrier follows
-    const int nb = (int)min<int64_t>(kBagsPerWave, a.B - b0);
+    const bool live = b0 < a.B; // the wave has bags
+    const int nb = live ? (int)min<int64_t>(kBagsPerWave, a.B - b0) : 0;
     const int64_t p0 = (int64_t)t * a.B + b0;
     const int64_t row = a.TB + 1;
+    // The wave's bag ranges do not depend on the bounds: read them first, so
+    // that both loads are in flight together.
+    int64_t s = 0, e = 0, S, E;
+    if (live) wave_bag_loads(a, p0, nb, lane, s, e);
+    for (int g = threadIdx.x; g <= G; g += kBlock) bnd[g] = a.bounds[(int64_t)t * (G + 1) + g];
+    __syncthreads();
+    if (!live) return; // no block-wide barrier follows
+    const bool contiguous = wave_bags(a, nb, lane, s, e, S, E);
     if (p0 == 0)
         for (int g = lane; g < G; g += kWave) a.out_offsets[(int64_t)g * row] = 0;
-    int64_t s, e, S, E;
-    const bool contiguous = wave_bags(a, p0, nb, lane, s, e, S, E);
 
     if (contiguous && G <= kFastShards) {
         const uint64_t bags = __ballot(lane < nb);
@@ -647,21 +657,29 @@ __global__ __launch_bounds__(kBlock) void eb_bucket_scatter(const BucketArgs a)
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = threadIdx.x / kWave;
     int64_t *next = lds + G + 1 + wave * G; // next free slot per destination
-    for (int g = threadIdx.x; g <= G; g += kBlock) bnd[g] = a.bounds[(int64_t)t * (G + 1) + g];
-    __syncthreads();
-
     const int64_t b0 = (int64_t)(blockIdx.x - t * a.blocks_per_table) * kBagsPerBlock + wave * kBagsPerWave;
-    if (b0 >= a.B) return; // no block-wide barrier follows
-    const int nb = (int)min<int64_t>(kBagsPerWave, a.B - b0);
+    const bool live = b0 < a.B; // the wave has bags
+    const int nb = live ? (int)min<int64_t>(kBagsPerWave, a.B - b0) : 0;
     const int64_t p0 = (int64_t)t * a.B + b0;
     const int64_t row = a.TB + 1;
-    int64_t s, e, S, E;
-    const bool contiguous = wave_bags(a, p0, nb, lane, s, e, S, E);
+    // Neither the wave's bag ranges nor its first output slots (lane d <
+    // G <= 64: destination d's, for contiguous bags) depend on the bounds:
+    // read them first, so that these loads are in flight together.
+    int64_t s = 0, e = 0, S, E;
+    int64_t first_slot = 0;
+    if (live) {
+        wave_bag_loads(a, p0, nb, lane, s, e);
+        if (G <= kWave && lane < G) first_slot = a.segments[lane] + a.out_offsets[(int64_t)lane * row + p0];
+    }
+    for (int g = threadIdx.x; g <= G; g += kBlock) bnd[g] = a.bounds[(int64_t)t * (G + 1) + g];
+    __syncthreads();
+    if (!live) return; // no block-wide barrier follows
+    const bool contiguous = wave_bags(a, nb, lane, s, e, S, E);
     if (contiguous && G <= kBallotShards) {
         // Contiguous bags, few destinations: ranks from ballots of the
         // owners' bits (scatter_few_pass).
         const FewBounds fb = few_bounds(bnd, G);
-        int64_t slot = lane < G ? a.segments[lane] + a.out_offsets[(int64_t)lane * row + p0] : 0;
+        int64_t slot = first_slot;
         const uint32_t l0 = (uint32_t)(lane & 1) - 1u, l1 = (uint32_t)((lane >> 1) & 1) - 1u,
                        l2 = (uint32_t)((lane >> 2) & 1) - 1u;
         constexpr int kPass = kScatterChunks * kWave;
@@ -678,7 +696,7 @@ __global__ __launch_bounds__(kBlock) void eb_bucket_scatter(const BucketArgs a)
         // Contiguous bags: within a destination, (bag, position) order is
         // position order, so one running slot per destination suffices;
         // lane g keeps destination g's in a register.
-        int64_t slot = lane < G ? a.segments[lane] + a.out_offsets[(int64_t)lane * row + p0] : 0;
+        int64_t slot = first_slot;
         const uint64_t below = (1ull << lane) - 1;
         for (int64_t k0 = S; k0 < E; k0 += kScatterChunks * kWave) {
             int64_t id[kScatterChunks];
