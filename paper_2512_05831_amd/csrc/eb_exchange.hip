@@ -175,6 +175,8 @@ struct BucketArgs {
     int64_t *out_offsets;    // [G][T*B+1]
     int64_t *out_indices;
     const int64_t *segments; // [G+1] (scatter pass)
+    const int64_t *starts;   // [G][nq]: out_offsets[g][16 q] (scatter pass; workspace)
+    int64_t nq;
     int64_t out_cap;         // entries of out_indices; positions at or past it are not written
     int64_t nnz;
     int64_t B;
@@ -239,9 +241,6 @@ __device__ __forceinline__ void wave_sync_lds()
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-// count's loop over the wave's ids [S, E) for contiguous bags (bag l of the
-// wave starts at lane l's s; bags = lanes holding a bag): adds each id with
-// an owner to hist[bag * count_stride(G) + owner].
 // One pass of count's loop: the ids at k0 + u * 64 + lane, the first R of
 // them (all kCountChunks * 64 when kFull, the usual case, which then needs
 // no tail masks).
@@ -388,6 +387,8 @@ struct ScanArgs {
     int64_t *rows;      // out_offsets: G rows of TB+1 entries; entries 1..TB are scanned
     int64_t *tile_sums; // [G][ntiles]
     int64_t *segments;  // [G+1]
+    int64_t *starts;    // [G][nq]: every 16th entry of each row, starts[g][q] = rows[g][16 q]
+    int64_t nq;         // TB / 16 + 1
     int64_t TB;
     int32_t G;
     int32_t ntiles;
@@ -397,6 +398,12 @@ struct ScanArgs {
 // Pass 2c adds up the earlier tile sums itself (no pass 2b) while every
 // workgroup reads at most this many of them.
 constexpr int64_t kFusedScanMax = 16384;
+
+// The scan also keeps every kStartStride-th entry of each row in a compact
+// array, where the scatter's waves (kBagsPerWave bags each) find their first
+// output slots: 16 waves share a line there instead of one each in the rows.
+constexpr int kStartStride = 16;
+static_assert(kScanTile % kStartStride == 0 && kBlock % kStartStride == 0, "scan tiles start at multiples of the stride");
 
 constexpr int kScanPer = kScanTile / kBlock; // counts per thread in a tile
 constexpr int kPrefixRegs = 16;              // tile sums per thread held in registers
@@ -568,11 +575,21 @@ __global__ __launch_bounds__(kBlock) void eb_scan_tiles(const ScanArgs a)
 #pragma unroll
     for (int j = 0; j < kScanPer; ++j) sm[scan_slot(threadIdx.x * kScanPer + j)] = base + v[j];
     __syncthreads();
+    // Thread x writes entries lo + j * 256 + x + 1 of the row; where that is
+    // a multiple of 16 (x % 16 == 15: tiles and j * 256 are), also starts[]
+    // at its index / 16.
+    const bool keeps = threadIdx.x % kStartStride == kStartStride - 1;
+    int64_t *start = a.starts + (int64_t)g * a.nq + lo / kStartStride + (threadIdx.x + 1) / kStartStride;
 #pragma unroll
     for (int j = 0; j < kScanPer; ++j) {
         const int i = j * kBlock + threadIdx.x;
-        if (i < n) row[lo + i] = sm[scan_slot(i)];
+        if (i < n) {
+            const int64_t x = sm[scan_slot(i)];
+            row[lo + i] = x;
+            if (keeps) start[j * (kBlock / kStartStride)] = x;
+        }
     }
+    if (k == 0 && threadIdx.x == 0) a.starts[(int64_t)g * a.nq] = 0;
 }
 
 // Scatter one chunk of up to 64 ids (lanes with g < 0 hold none): every
@@ -669,7 +686,9 @@ __global__ __launch_bounds__(kBlock) void eb_bucket_scatter(const BucketArgs a)
     int64_t first_slot = 0;
     if (live) {
         wave_bag_loads(a, p0, nb, lane, s, e);
-        if (G <= kWave && lane < G) first_slot = a.segments[lane] + a.out_offsets[(int64_t)lane * row + p0];
+        if (G <= kWave && lane < G)
+            first_slot = a.segments[lane] + (p0 % kStartStride == 0 ? a.starts[(int64_t)lane * a.nq + p0 / kStartStride]
+                                                                   : a.out_offsets[(int64_t)lane * row + p0]);
     }
     for (int g = threadIdx.x; g <= G; g += kBlock) bnd[g] = a.bounds[(int64_t)t * (G + 1) + g];
     __syncthreads();
@@ -814,6 +833,7 @@ __global__ __launch_bounds__(kBlock) void eb_sum_partials_scalar(const PartialAr
 }
 
 int64_t scan_tiles(int64_t TB) { return std::max<int64_t>(1, (TB + kScanTile - 1) / kScanTile); }
+int64_t start_entries(int64_t TB) { return TB / kStartStride + 1; }
 
 } // namespace
 
@@ -827,7 +847,8 @@ int eb_bucketize_workspace(int32_t T, int64_t B, int32_t G, size_t *bytes)
     if (G > kMaxShards) return fail(EB_ERR_UNSUPPORTED, "eb_bucketize_workspace: more than 1024 shards");
     if (T > 0 && B > std::numeric_limits<int64_t>::max() / T / G / 8)
         return fail(EB_ERR_INVALID, "eb_bucketize_workspace: sizes overflow");
-    *bytes = (size_t)G * (size_t)scan_tiles((int64_t)T * B) * sizeof(int64_t);
+    // tile sums, then every 16th entry of each destination's offsets
+    *bytes = (size_t)G * (size_t)(scan_tiles((int64_t)T * B) + start_entries((int64_t)T * B)) * sizeof(int64_t);
     return EB_OK;
 }
 
@@ -871,6 +892,10 @@ int eb_bucketize(int32_t T, int64_t B, int32_t G, const int64_t *bounds, const i
     ScanArgs sa;
     sa.rows = out_offsets;
     sa.tile_sums = (int64_t *)workspace;
+    sa.nq = start_entries(TB);
+    sa.starts = sa.tile_sums + (int64_t)G * scan_tiles(TB);
+    ba.starts = sa.starts;
+    ba.nq = sa.nq;
     sa.segments = segments;
     sa.TB = TB;
     sa.G = G;

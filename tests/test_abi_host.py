@@ -215,8 +215,10 @@ def test_forward_ex_noops_and_default_columns():
 
 
 def test_bucketize_workspace_sizes():
-    assert eb.eb_bucketize_workspace(26, 16384, 8) == 8 * ((26 * 16384 + 2047) // 2048) * 8
-    assert eb.eb_bucketize_workspace(0, 0, 1) == 8
+    # per destination: one sum per 2048-bag scan tile, then every 16th offset
+    assert eb.eb_bucketize_workspace(26, 16384, 8) == 8 * ((26 * 16384 + 2047) // 2048 + 26 * 16384 // 16 + 1) * 8
+    assert eb.eb_bucketize_workspace(3, 7, 2) == 2 * (1 + 21 // 16 + 1) * 8
+    assert eb.eb_bucketize_workspace(0, 0, 1) == 16
     assert code_of(lambda: eb.eb_bucketize_workspace(1, 1, 0)) == eb.EB_ERR_INVALID
     assert code_of(lambda: eb.eb_bucketize_workspace(-1, 1, 2)) == eb.EB_ERR_INVALID
     assert code_of(lambda: eb.eb_bucketize_workspace(1, 1, 1025)) == eb.EB_ERR_UNSUPPORTED
