@@ -152,12 +152,6 @@ __device__ __forceinline__ int few_bits(const FewMasks &o)
     return (lane_bit(o.b0) ? kScale : 0) | (lane_bit(o.b1) ? 2 * kScale : 0) | (lane_bit(o.b2) ? 4 * kScale : 0);
 }
 
-// Number of set bits of m in the lanes below this one.
-__device__ __forceinline__ int rank_below(uint64_t m)
-{
-    return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
-}
-
 // A wave takes kBagsPerWave consecutive bags of one table; a block 4 waves.
 // Few bags per wave keep many waves (and their id loads) in flight.
 constexpr int kBagsPerWave = 16;
