@@ -179,6 +179,19 @@ struct BucketArgs {
     int32_t blocks_per_table;
 };
 
+// Workgroups are dealt to the 8 XCDs in turn (workgroup b to XCD b % 8).
+// count and scatter take their bags by logical workgroup xcd_run_block(b, n),
+// which gives each XCD one contiguous run of the n logical workgroups (runs
+// differ by at most one), so that neighbouring bags' output lines meet in
+// one L2.
+constexpr int kXcds = 8;
+
+__device__ __forceinline__ int xcd_run_block(int b, int n)
+{
+    const int x = b % kXcds, per = n / kXcds, rem = n % kXcds;
+    return x * per + min(x, rem) + b / kXcds;
+}
+
 // Dynamic LDS: the table's G+1 bounds, then one area per wave.
 // count's histogram row per bag: 8 entries for up to 8 destinations (an
 // index by shift), else G.
@@ -295,11 +308,12 @@ __global__ __launch_bounds__(kBlock) void eb_bucket_count(const BucketArgs a)
     extern __shared__ int64_t lds[];
     const int G = a.G;
     int64_t *bnd = lds;
-    const int t = blockIdx.x / a.blocks_per_table;
+    const int lb = xcd_run_block(blockIdx.x, gridDim.x);
+    const int t = lb / a.blocks_per_table;
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = threadIdx.x / kWave;
     int *hist = (int *)((char *)(lds + G + 1) + wave * count_wave_bytes(G));
-    const int64_t b0 = (int64_t)(blockIdx.x - t * a.blocks_per_table) * kBagsPerBlock + wave * kBagsPerWave;
+    const int64_t b0 = (int64_t)(lb - t * a.blocks_per_table) * kBagsPerBlock + wave * kBagsPerWave;
     const bool live = b0 < a.B; // the wave has bags
     const int nb = live ? (int)min<int64_t>(kBagsPerWave, a.B - b0) : 0;
     const int64_t p0 = (int64_t)t * a.B + b0;
@@ -664,11 +678,12 @@ __global__ __launch_bounds__(kBlock) void eb_bucket_scatter(const BucketArgs a)
     extern __shared__ int64_t lds[];
     const int G = a.G;
     int64_t *bnd = lds;
-    const int t = blockIdx.x / a.blocks_per_table;
+    const int lb = xcd_run_block(blockIdx.x, gridDim.x);
+    const int t = lb / a.blocks_per_table;
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = threadIdx.x / kWave;
     int64_t *next = lds + G + 1 + wave * G; // next free slot per destination
-    const int64_t b0 = (int64_t)(blockIdx.x - t * a.blocks_per_table) * kBagsPerBlock + wave * kBagsPerWave;
+    const int64_t b0 = (int64_t)(lb - t * a.blocks_per_table) * kBagsPerBlock + wave * kBagsPerWave;
     const bool live = b0 < a.B; // the wave has bags
     const int nb = live ? (int)min<int64_t>(kBagsPerWave, a.B - b0) : 0;
     const int64_t p0 = (int64_t)t * a.B + b0;
