@@ -19,7 +19,8 @@
 // chains of dependent loads and by instruction issue.
 //
 // eb_bucketize runs three kernels on the caller's stream:
-//   1. count   : a wave takes 16 consecutive bags; each id's owner by
+//   1. count   : a wave takes 16 consecutive bags (each XCD one contiguous
+//                run of workgroups); each id's owner by
 //                comparisons with the table's block bounds (up to 8 blocks:
 //                a search tree evaluated as wave-wide lane masks) or by
 //                binary search over them (staged in LDS); for ordinary CSR
@@ -32,9 +33,11 @@
 //                workspace; each tile then adds up its row's earlier tiles,
 //                and the rows' first tiles the segments; with more than
 //                16384 tile sums one workgroup first scans them as one
-//                sequence instead).
+//                sequence instead); every 16th scanned entry of each row
+//                is also copied to the workspace for the scatter.
 //   3. scatter : same waves; ids are written to segments[g] +
-//                out_offsets[g][p] + rank, the rank counting earlier ids of
+//                out_offsets[g][p] + rank (a wave's first out_offsets from
+//                the workspace copy), the rank counting earlier ids of
 //                the bag with the same owner (per 64-id chunk: three ballots
 //                of the owner's bits for up to 8 destinations, else a ballot
 //                per distinct owner), so the order is stable.  For ordinary CSR
