@@ -108,6 +108,70 @@ def test_bucketize_edge_cases(device):
     check_bucketize(1, 4, idx, off, bounds, device)
 
 
+@pytest.mark.parametrize("G", [3, 8, 17])
+def test_bucketize_extreme_ids(G, device):
+    """Bounds reaching both ends of int64 and ids at, just below and just
+    above every bound (including INT64_MIN and INT64_MAX): the owner's
+    compares, the padding of unused bounds (up to 8 destinations) and the
+    binary search (more), against the oracle."""
+    lo64, hi64 = np.iinfo(np.int64).min, np.iinfo(np.int64).max
+    g = np.random.default_rng(G)
+    T, B = 3, 40
+    rows = []
+    for t in range(T):
+        first = lo64 if t == 0 else -2**40
+        last = hi64 if t != 2 else 2**40
+        inner = np.sort(g.integers(max(first, -2**62), min(last, 2**62), G - 1))
+        rows.append([first, *inner.tolist(), last])
+    bounds = np.array(rows, dtype=np.int64)
+    assert np.all(bounds[:, 1:] >= bounds[:, :-1])  # non-decreasing (a difference could overflow)
+    L = g.integers(0, 30, T * B)
+    off = wl.offsets_from_lengths(L)
+    ids = []
+    for t in range(T):
+        near = {v + d for v in bounds[t].tolist() for d in (-1, 0, 1)} | {lo64, lo64 + 1, -1, 0, 1, hi64 - 1, hi64}
+        near = np.array(sorted(v for v in near if lo64 <= v <= hi64), dtype=np.int64)
+        ids.append(g.choice(near, int(off[(t + 1) * B] - off[t * B])))
+    idx = np.concatenate(ids).astype(np.int64)
+    check_bucketize(T, B, idx, off, bounds, device)
+
+
+def check_split(bounds, idx, off, T, B, got):
+    """What eb_bucketize still promises for bounds that are not sorted (an
+    unspecified split): every destination's share of a bag is a subsequence
+    of that bag's ids, and the offsets and segments describe exactly what was
+    stored."""
+    out_off, out_idx, seg = got
+    G = bounds.shape[1] - 1
+    assert seg[0] == 0 and np.all(np.diff(seg) >= 0)
+    assert np.all(out_off[:, 0] == 0) and np.all(np.diff(out_off, axis=1) >= 0)
+    assert np.array_equal(out_off[:, -1], np.diff(seg)) and len(out_idx) == seg[-1]
+    for t in range(T):
+        for b in range(B):
+            p = t * B + b
+            mine = idx[off[p]:off[p + 1]].tolist()
+            for d in range(G):
+                part = out_idx[seg[d] + out_off[d][p]:seg[d] + out_off[d][p + 1]].tolist()
+                it = iter(mine)
+                assert all(any(v == w for w in it) for v in part), (t, b, d)
+
+
+@pytest.mark.parametrize("G", [2, 5, 8, 17])
+def test_bucketize_arbitrary_bounds(G, device):
+    """Bounds that are not sorted: the promises of check_split hold (the
+    oracle's own split meets them too)."""
+    g = np.random.default_rng(100 + G)
+    T, B = 3, 300
+    L = g.integers(0, 25, T * B)
+    off = wl.offsets_from_lengths(L)
+    idx = g.integers(-20, 3000, int(off[-1])).astype(np.int64)
+    bounds = g.integers(-10, 3000, (T, G + 1)).astype(np.int64)
+    cap = G * len(idx)  # the oracle's split may send an id to several destinations
+    want = oracle.bucketize(bounds, idx, off, T, B, capacity=cap)
+    check_split(bounds, idx, off, T, B, (want[0], want[1][:int(want[2][-1])], want[2]))
+    check_split(bounds, idx, off, T, B, run_bucketize(bounds, idx, off, T, B, device))
+
+
 @pytest.mark.parametrize("G", [3, 8, 40, 300])
 def test_bucketize_unordered_offsets(G, device):
     """Offsets that go back and forth (bags overlap, some end before they
