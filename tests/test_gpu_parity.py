@@ -214,11 +214,13 @@ def test_shard_partials_add_up_on_gpu():
 def test_out_of_range_and_negative_ids():
     D = 64
     tables, rows, _, _ = case(T=1, D=D, rows=100)
-    idx = np.array([-1, 0, 99, 100, -(1 << 62), (1 << 62), 5, 1 << 40, -5, 50], dtype=np.int64)
-    off = np.array([0, 3, 6, 10], dtype=np.int64)
+    i64 = np.iinfo(np.int64)
+    idx = np.array([-1, 0, 99, 100, -(1 << 62), (1 << 62), 5, 1 << 40, -5, 50,
+                    i64.min, i64.max, i64.max - 1, 7], dtype=np.int64)
+    off = np.array([0, 3, 6, 10, 14], dtype=np.int64)
     for lo, hi in ((0, wl.INT64_MAX), (5, 60)):
         t = [tables[0][lo:min(hi, 100)]]
-        check(t, rows, D, wl.F32, idx, off, 3, wl.SUM, lo, hi)
+        check(t, rows, D, wl.F32, idx, off, 4, wl.SUM, lo, hi)
 
 
 def test_malformed_offsets():
