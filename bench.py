@@ -96,10 +96,13 @@ def measured_traffic(workload_name: str):
 
 
 def pick_workload(args):
-    if args.workload == 4:
+    wid = 2 if args.workload is None else args.workload
+    if wid == 4:
         w = wl.config(4, D=args.dim, dtype={"f16": wl.F16, "bf16": wl.BF16}[args.dtype])
+    elif wid == 5:
+        w = wl.config(5, permuted=args.permuted)
     else:
-        w = wl.config(args.workload)
+        w = wl.config(wid)
     return w
 
 
@@ -541,12 +544,128 @@ def paper_sweep(torch, dev, eb, index_type="i64"):
         et.close()
 
 
+# Workloads timed besides the headline (workload 2), each on its own:
+# (workload id, arguments of workloads.config, pooling modes).
+def other_workloads():
+    runs = [(1, {}, (wl.SUM,)), (3, {}, (wl.SUM, wl.MEAN))]
+    for dtype in (wl.F16, wl.BF16):
+        for D in wl.CONFIG4_DIMS:
+            runs.append((4, dict(D=D, dtype=dtype), (wl.SUM,)))
+    runs += [(5, {}, (wl.SUM,)), (5, dict(permuted=True), (wl.SUM,))]
+    return runs
+
+
+def timing_tables(torch, dev, w, seed):
+    """Tables for timing only: N(0, 0.01) drawn on the device (the values
+    do not change the time; generating 16-27 GB on the host would)."""
+    tdt = {wl.F32: torch.float32, wl.F16: torch.float16, wl.BF16: torch.bfloat16}[w.dtype]
+    gen = torch.Generator(device=dev).manual_seed(seed)
+    tabs = []
+    for _ in range(w.T):
+        x = torch.empty((w.stored_rows, w.D), dtype=tdt, device=dev)
+        x.normal_(0.0, 0.01, generator=gen)
+        tabs.append(x)
+    return tabs
+
+
+def index_batches(w, n, cache):
+    """The headline's batch scheme: the workload's ids, then n - 1 batches
+    drawn with other seeds; shared by workloads that differ only in D/dtype."""
+    key = (w.seed, w.T, w.B, w.rows, w.lengths_kind, w.L, w.dist, w.alpha, w.permuted)
+    if key not in cache:
+        cache.clear()
+        off = w.offsets()
+        cache[key] = (off, [w.with_(seed=w.seed + 7919 * j).indices(off) if j else w.indices(off)
+                            for j in range(n)])
+    return cache[key]
+
+
+def time_workload(torch, dev, eb, cid, w, modes, K, W, nbatches, cache, stream):
+    """Entries (one per pooling mode) for one workload: mean launch time over
+    K back-to-back launches (HIP events on the launch stream) and the rates
+    and roofline fraction that follow; for skewed ids also single launches
+    warm and after a 512 MB flush (the caches' share)."""
+    off, batches = index_batches(w, nbatches, cache)
+    tables = timing_tables(torch, dev, w, w.seed + 31)
+    et = eb.EmbeddingBagTables(tables, rows=[w.rows] * w.T, shard_lo=w.shard_lo, shard_hi=w.shard_hi)
+    d_off = torch.from_numpy(off).to(dev)
+    d_idx = [torch.from_numpy(b).to(dev) for b in batches]
+    out = torch.empty((w.B, w.T * w.D), dtype=torch.float32, device=dev)
+    hits = torch.empty((w.B, w.T), dtype=torch.int32, device=dev) if w.want_hits else None
+    local = [int(np.count_nonzero((b >= w.shard_lo) & (b < w.local_hi))) for b in batches]
+    nnz = [int(b.size) for b in batches]
+    uniform = w.dist == "uniform"
+    entries = []
+    for mode in modes:
+        call_mode = mode | (eb.EB_HINT_STREAM_ROWS if uniform else 0)
+        calls = [et.prepare(i, d_off, w.B, call_mode, out, hits, stream) for i in d_idx]
+        turn = [0]
+
+        def step():
+            calls[turn[0] % len(calls)]()
+            turn[0] += 1
+        us = _time_launches(torch, stream, step, K, W)
+        n_avg = sum(nnz) / len(nnz)
+        by = sum(algorithmic_bytes(w, local[j], nnz[j], hits is not None) for j in range(len(nnz))) / len(nnz)
+        name = w.name + ("-mean" if mode == wl.MEAN else "")
+        e = {"config": cid, "workload": name, "mode": "sum" if mode == wl.SUM else "mean",
+             "storage": wl.DTYPE_NAMES[w.dtype], "rows_cache_policy": "stream" if uniform else "cached",
+             "kernel_us": round(us, 2), "lookups_per_s": n_avg / us * 1e6,
+             "bags_per_s": w.T * w.B / us * 1e6,
+             "algorithmic_bytes_per_launch": int(by), "algorithmic_GBps": round(by / us / 1e3, 1),
+             "frac_of_8TBps": round(by / us / 1e3 / HBM_PEAK_GBPS, 4)}
+        if w.sharded:
+            e["local_fraction"] = round(sum(local) / sum(nnz), 4)
+        if not uniform:
+            e["note"] = ("skewed ids: algorithmic bytes count every lookup's row, part of which "
+                         "L2 and the last-level cache serve, so the fraction is not an HBM fraction")
+            warm = per_launch_us(torch, stream, calls, 20)
+            flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+            cold = per_launch_us(torch, stream, calls, 20, flush=lambda i: flush.fill_(i & 0xFF))
+            del flush
+            e["single_launch_us"] = {"warm_median": round(warm["median_us"], 1),
+                                     "cold_median_512MB_flushed": round(cold["median_us"], 1)}
+        tr = measured_traffic(name)
+        e["traffic_GBps"] = None if tr is None else round(tr / us / 1e3, 1)
+        entries.append(e)
+        log(f"bench: {name}: {us:.1f} us, {by / us / 1e3:.0f} GB/s algorithmic "
+            f"({by / us / 1e3 / HBM_PEAK_GBPS * 100:.1f}% of 8 TB/s)")
+    et.close()
+    del tables, d_idx, d_off, out, hits
+    torch.cuda.empty_cache()
+    return entries
+
+
+def all_workloads(torch, dev, eb, headline, K, W, nbatches):
+    """One entry per workload and pooling mode: the headline's numbers for
+    workload 2, then every other workload timed the same way.  A workload
+    that fails records its error in its own entry."""
+    stream = torch.cuda.Stream(dev)
+    entries = [dict(headline, config=2, source="headline run")]
+    cache = {}
+    for cid, kw, modes in other_workloads():
+        w = wl.config(cid, **kw)
+        try:
+            entries.extend(time_workload(torch, dev, eb, cid, w, modes, K, W, nbatches, cache, stream))
+        except Exception as exc:  # noqa: BLE001 -- recorded, the line is still printed
+            entries.append({"config": cid, "workload": w.name, "error": f"{type(exc).__name__}: {exc}"})
+            log(f"bench: {w.name} failed: {exc}")
+            torch.cuda.empty_cache()
+    return entries
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=400)
     ap.add_argument("--warmup", type=int, default=40)
-    ap.add_argument("--workload", type=int, default=2, choices=[1, 2, 3, 4, 5])
+    ap.add_argument("--workload", type=int, default=None, choices=[1, 2, 3, 4, 5],
+                    help="time this workload only (default: workload 2 as the headline, then "
+                         "every workload under \"workloads\")")
+    ap.add_argument("--permuted", action="store_true",
+                    help="workload 5 with its Zipf ranks permuted over the id space")
+    ap.add_argument("--headline-only", action="store_true",
+                    help="skip timing the other workloads after the headline")
     ap.add_argument("--dim", type=int, default=128)
     ap.add_argument("--dtype", default="f16", choices=["f16", "bf16"])
     ap.add_argument("--batches", type=int, default=8, help="distinct index batches cycled")
@@ -723,6 +842,7 @@ def main():
                 e1.record(stream)
                 torch.cuda.synchronize()
             tus = e0.elapsed_time(e1) * 1e3 / tk
+            del tsteps
             extra["torch_embedding_bag"] = {
                 "us_per_step": tus, "lookups_per_s": (steps_lookups / K) / (tus / 1e6),
                 "calls_per_step": w.T, "steps": tk,
@@ -771,8 +891,20 @@ def main():
         "cpu_baseline": cpu,
     }
     line.update(extra)
-    print(json.dumps(line), flush=True)
     et.close()
+    if args.workload is None and not args.headline_only:
+        del dev_tables, d_idx, d_off, out, hits, calls, step_fns, d_wts
+        torch.cuda.empty_cache()
+        head = {"workload": w.name, "mode": "sum" if mode == wl.SUM else "mean",
+                "storage": wl.DTYPE_NAMES[w.dtype],
+                "rows_cache_policy": "stream" if stream_rows else "cached",
+                "kernel_us": round(launch_ms * 1e3, 2), "lookups_per_s": steps_lookups / K / launch_ms * 1e3,
+                "bags_per_s": w.T * w.B / launch_ms * 1e3,
+                "algorithmic_bytes_per_launch": int(bytes_per_launch),
+                "algorithmic_GBps": round(achieved, 1), "frac_of_8TBps": round(achieved / HBM_PEAK_GBPS, 4),
+                "traffic_GBps": None if traffic is None else round(traffic / launch_ms / 1e6, 1)}
+        line["workloads"] = all_workloads(torch, dev, eb, head, K, W, args.batches)
+    print(json.dumps(line), flush=True)
 
 
 if __name__ == "__main__":

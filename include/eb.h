@@ -25,6 +25,9 @@
  * Conventions used by every entry point
  *   - Return value: EB_OK (0) or a negative EB_ERR_* code; eb_last_error()
  *     then returns a message for the calling thread.  No entry point throws.
+ *   - Only eb_create_tables allocates (the handle's host memory).  The other
+ *     entry points allocate no host or device memory, on success or error
+ *     paths; messages are kept in a fixed per-thread buffer.
  *   - Lengths arrive as offsets, their exclusive prefix sum (CSR form).  For
  *     T tables and B bags per table, offsets has T*B+1 entries (int64, or
  *     int32 through eb_forward_ex) and bag

@@ -43,11 +43,11 @@
 #include <stdint.h>
 
 #include <algorithm>
+#include <cstdarg>
+#include <cstdio>
 #include <cstring>
 #include <limits>
 #include <new>
-#include <string>
-#include <utility>
 #include <vector>
 
 #include "../../include/eb.h"
@@ -61,7 +61,8 @@ using namespace eb_gather;
 
 // ---------------------------------------------------------------------------- host side
 
-thread_local std::string g_last_error;
+// Error messages live in a fixed per-thread buffer.
+thread_local char g_last_error[512];
 
 using eb_detail::fail;
 
@@ -107,10 +108,20 @@ Shape team_shape(int rb, bool few, bool single, bool narrow512 = false)
 
 } // namespace
 
-int eb_detail::fail(int code, const std::string &msg)
+int eb_detail::fail(int code, const char *fmt, ...)
 {
-    g_last_error = msg;
+    va_list ap;
+    va_start(ap, fmt);
+    std::vsnprintf(g_last_error, sizeof g_last_error, fmt, ap);
+    va_end(ap);
     return code;
+}
+
+const char *eb_detail::last_error() { return g_last_error; }
+
+int eb_detail::unexpected_exception(const char *who)
+{
+    return fail(EB_ERR_NOMEM, "%s: unexpected exception (out of host memory?)", who);
 }
 
 struct eb_tables {
@@ -124,67 +135,90 @@ struct eb_tables {
 
 namespace {
 
-// Both forward entry points.  out_cols == nullptr means table t at column t*D.
+// Output column of table t's first element.
+inline int64_t out_col(const int64_t *out_cols, int32_t t, int32_t D)
+{
+    return out_cols ? out_cols[t] : (int64_t)t * D;
+}
+
+// Whether two of the T column ranges [cols[t], cols[t] + D) overlap (all
+// have width D, so two overlap iff their starts differ by less than D).
+// Sorts a copy on the stack for up to kSortMax tables, else compares pairs.
+bool columns_overlap(const int64_t *cols, int32_t T, int32_t D)
+{
+    constexpr int32_t kSortMax = 1024;
+    if (T <= kSortMax) {
+        int64_t c[kSortMax];
+        std::memcpy(c, cols, sizeof(int64_t) * (size_t)T);
+        std::sort(c, c + T);
+        for (int32_t t = 1; t < T; ++t)
+            if (c[t] - c[t - 1] < D) return true;
+        return false;
+    }
+    for (int32_t i = 0; i < T; ++i)
+        for (int32_t j = i + 1; j < T; ++j)
+            if ((cols[i] > cols[j] ? cols[i] - cols[j] : cols[j] - cols[i]) < D) return true;
+    return false;
+}
+
+// Gatherable local rows of a table: min(shard_hi, rows) - shard_lo, or 0.
+inline int64_t local_rows(int64_t rows, int64_t shard_lo, int64_t shard_hi)
+{
+    const int64_t hi = std::min(shard_hi, rows);
+    return hi > shard_lo ? hi - shard_lo : 0;
+}
+
+// Both forward entry points.  out_cols == nullptr means table t at column
+// t*D.  Every argument is checked before the first launch, so a rejected call
+// enqueues nothing.  Allocates nothing.
 int forward_impl(const char *who, const eb_tables *h, int32_t T, const int64_t *rows, int32_t D,
                  int32_t dtype, int32_t index_type, const void *indices, int64_t nnz, const void *offsets,
                  const float *weights, int64_t B, int32_t mode, int64_t shard_lo, int64_t shard_hi, float *out, int64_t ldo,
                  const int64_t *out_cols, int32_t *hits, int64_t ldh, void *stream)
 {
-    const std::string fn_name(who);
-    auto invalid = [&](const std::string &msg) { return fail(EB_ERR_INVALID, fn_name + ": " + msg); };
-    if (!h) return invalid("NULL handle");
-    if (T < 0 || T > h->T) return invalid("T out of range for the handle");
-    if (D != h->D) return invalid("D differs from the handle's");
-    if (dtype != h->dtype) return invalid("dtype differs from the handle's");
-    if (index_type != EB_IDX_I64 && index_type != EB_IDX_I32) return invalid("unknown index_type");
+    if (!h) return fail(EB_ERR_INVALID, "%s: NULL handle", who);
+    if (T < 0 || T > h->T) return fail(EB_ERR_INVALID, "%s: T out of range for the handle", who);
+    if (D != h->D) return fail(EB_ERR_INVALID, "%s: D differs from the handle's", who);
+    if (dtype != h->dtype) return fail(EB_ERR_INVALID, "%s: dtype differs from the handle's", who);
+    if (index_type != EB_IDX_I64 && index_type != EB_IDX_I32) return fail(EB_ERR_INVALID, "%s: unknown index_type", who);
     const int32_t pool = mode & 0xFF;
     if ((pool != EB_SUM && pool != EB_MEAN) || (mode & ~(0xFF | EB_HINT_STREAM_ROWS)) != 0)
-        return invalid("unknown mode or hint bits");
-    if (nnz < 0 || B < 0) return invalid("negative nnz or B");
-    if (shard_lo < 0 || shard_hi < shard_lo) return invalid("bad shard range");
-    if (T > 0 && !rows) return invalid("NULL rows");
+        return fail(EB_ERR_INVALID, "%s: unknown mode or hint bits", who);
+    if (nnz < 0 || B < 0) return fail(EB_ERR_INVALID, "%s: negative nnz or B", who);
+    if (shard_lo < 0 || shard_hi < shard_lo) return fail(EB_ERR_INVALID, "%s: bad shard range", who);
+    if (T > 0 && !rows) return fail(EB_ERR_INVALID, "%s: NULL rows", who);
     if (T == 0 || B == 0) return EB_OK;
-    if (!offsets || !out) return invalid("NULL offsets or out");
-    if (nnz > 0 && !indices) return invalid("NULL indices with nnz > 0");
-    if (weights && pool != EB_SUM) return invalid("per-sample weights need sum pooling");
+    if (!offsets || !out) return fail(EB_ERR_INVALID, "%s: NULL offsets or out", who);
+    if (nnz > 0 && !indices) return fail(EB_ERR_INVALID, "%s: NULL indices with nnz > 0", who);
+    if (weights && pool != EB_SUM) return fail(EB_ERR_INVALID, "%s: per-sample weights need sum pooling", who);
     const int64_t kMax = std::numeric_limits<int64_t>::max();
-    if (B > kMax / T || B * T > kMax / D) return invalid("B*T*D overflows");
+    if (B > kMax / T || B * T > kMax / D) return fail(EB_ERR_INVALID, "%s: B*T*D overflows", who);
 
     // Output layout: every table's D columns inside [0, ldo), no two tables
     // sharing a column, B rows of ldo floats addressable.
-    std::vector<int64_t> cols(T);
-    for (int32_t t = 0; t < T; ++t) cols[t] = out_cols ? out_cols[t] : (int64_t)t * D;
-    if (ldo < 1 || B > kMax / ldo) return invalid("bad ldo (must be >= 1 with B*ldo in int64)");
-    {
-        std::vector<std::pair<int64_t, int64_t>> spans(T);
-        for (int32_t t = 0; t < T; ++t) {
-            if (cols[t] < 0 || cols[t] > ldo - D)
-                return invalid("output columns of table " + std::to_string(t) + " leave [0, ldo)");
-            spans[t] = {cols[t], cols[t] + D};
-        }
-        std::sort(spans.begin(), spans.end());
-        for (int32_t t = 1; t < T; ++t)
-            if (spans[t].first < spans[t - 1].second) return invalid("two tables share output columns");
-    }
-    if (hits && (ldh < T || B > kMax / ldh)) return invalid("bad ldh (must be >= T with B*ldh in int64)");
-
-    std::vector<uint64_t> nlocal(T);
+    if (ldo < 1 || B > kMax / ldo) return fail(EB_ERR_INVALID, "%s: bad ldo (must be >= 1 with B*ldo in int64)", who);
     for (int32_t t = 0; t < T; ++t) {
-        if (rows[t] < 0) return invalid("negative rows[t]");
-        const int64_t hi = std::min(shard_hi, rows[t]);
-        const int64_t n = hi > shard_lo ? hi - shard_lo : 0;
+        const int64_t c = out_col(out_cols, t, D);
+        if (c < 0 || c > ldo - D)
+            return fail(EB_ERR_INVALID, "%s: output columns of table %d leave [0, ldo)", who, (int)t);
+    }
+    if (out_cols && columns_overlap(out_cols, T, D)) return fail(EB_ERR_INVALID, "%s: two tables share output columns", who);
+    if (hits && (ldh < T || B > kMax / ldh)) return fail(EB_ERR_INVALID, "%s: bad ldh (must be >= T with B*ldh in int64)", who);
+
+    for (int32_t t = 0; t < T; ++t) {
+        if (rows[t] < 0) return fail(EB_ERR_INVALID, "%s: negative rows[t]", who);
+        const int64_t n = local_rows(rows[t], shard_lo, shard_hi);
         if (n > h->stored_rows[t])
-            return invalid("stored rows of table " + std::to_string(t) +
-                           " do not cover [shard_lo, min(shard_hi, rows[t]))");
+            return fail(EB_ERR_INVALID, "%s: stored rows of table %d do not cover [shard_lo, min(shard_hi, rows[t]))",
+                        who, (int)t);
         if ((uint64_t)n > kMaxLocalRows)
-            return fail(EB_ERR_UNSUPPORTED, fn_name + ": more than 4294967294 gatherable rows in a table");
-        nlocal[t] = (uint64_t)n;
+            return fail(EB_ERR_UNSUPPORTED, "%s: more than 4294967294 gatherable rows in a table", who);
     }
 
     const int64_t rb = (int64_t)D * elem_bytes(dtype);
     // 16-byte stores need every (bag, table) output row start 16-byte aligned.
     bool out_aligned = ((uintptr_t)out) % 16 == 0 && ldo % 4 == 0;
-    for (int32_t t = 0; t < T; ++t) out_aligned = out_aligned && cols[t] % 4 == 0;
+    for (int32_t t = 0; t < T; ++t) out_aligned = out_aligned && out_col(out_cols, t, D) % 4 == 0;
     const bool team_path = rb % 16 == 0 && rb <= 8192 && h->aligned16 && out_aligned;
     const bool i32 = index_type == EB_IDX_I32;
     KernelFn fn = nullptr;
@@ -222,7 +256,7 @@ int forward_impl(const char *who, const eb_tables *h, int32_t T, const int64_t *
         fn = weights ? pick_weighted_kernel(i32, dtype, false, 0, 0, false, false, false)
                      : pick_kernel<false>(i32, dtype, false, 0, 0, false, false, false);
     }
-    if (!fn) return fail(EB_ERR_UNSUPPORTED, fn_name + ": no kernel for this row shape");
+    if (!fn) return fail(EB_ERR_UNSUPPORTED, "%s: no kernel for this row shape", who);
 
     // Launch in pieces of at most 64 tables and a bounded grid.
     const int64_t kMaxBlocks = (int64_t)1 << 22;
@@ -249,8 +283,8 @@ int forward_impl(const char *who, const eb_tables *h, int32_t T, const int64_t *
         const int32_t nt = std::min<int32_t>(kMaxTablesPerLaunch, T - t0);
         for (int32_t j = 0; j < nt; ++j) {
             a.base[j] = h->ptrs[t0 + j];
-            a.nlocal[j] = nlocal[t0 + j];
-            a.col[j] = cols[t0 + j];
+            a.nlocal[j] = (uint64_t)local_rows(rows[t0 + j], shard_lo, shard_hi);
+            a.col[j] = out_col(out_cols, t0 + j, D);
         }
         a.offsets = (const char *)offsets + (size_t)t0 * B * ies;
         a.hits = hits ? hits + t0 : nullptr;
@@ -264,8 +298,7 @@ int forward_impl(const char *who, const eb_tables *h, int32_t T, const int64_t *
             const int64_t grid = xcd_remap ? (a.nblocks + kXcds - 1) / kXcds * kXcds : a.nblocks;
             void *args[] = {&a};
             hipError_t err = hipLaunchKernel((const void *)fn, dim3((unsigned)grid), dim3(kBlock), args, 0, st);
-            if (err != hipSuccess)
-                return fail(EB_ERR_HIP, fn_name + ": kernel launch failed: " + hipGetErrorString(err));
+            if (err != hipSuccess) return fail(EB_ERR_HIP, "%s: kernel launch failed: %s", who, hipGetErrorString(err));
         }
     }
     return EB_OK;
@@ -278,48 +311,56 @@ extern "C" {
 int eb_create_tables(int32_t T, const void *const *table_ptrs, const int64_t *stored_rows, int32_t D,
                      int32_t dtype, eb_tables **out_handle)
 {
-    if (!out_handle) return fail(EB_ERR_INVALID, "eb_create_tables: out_handle is NULL");
-    *out_handle = nullptr;
-    if (T < 1) return fail(EB_ERR_INVALID, "eb_create_tables: T must be >= 1");
-    if (!table_ptrs || !stored_rows) return fail(EB_ERR_INVALID, "eb_create_tables: NULL table_ptrs or stored_rows");
-    if (D < 1) return fail(EB_ERR_INVALID, "eb_create_tables: D must be >= 1");
-    if (dtype != EB_F32 && dtype != EB_F16 && dtype != EB_BF16)
-        return fail(EB_ERR_INVALID, "eb_create_tables: unknown dtype");
-    for (int32_t t = 0; t < T; ++t) {
-        if (stored_rows[t] < 0) return fail(EB_ERR_INVALID, "eb_create_tables: negative stored_rows");
-        if (!table_ptrs[t] && stored_rows[t] > 0)
-            return fail(EB_ERR_INVALID, "eb_create_tables: NULL table pointer with stored rows");
-    }
-    eb_tables *h = new (std::nothrow) eb_tables;
-    if (!h) return fail(EB_ERR_NOMEM, "eb_create_tables: out of host memory");
     try {
-        h->T = T;
-        h->D = D;
-        h->dtype = dtype;
-        h->ptrs.assign((const char *const *)table_ptrs, (const char *const *)table_ptrs + T);
-        h->stored_rows.assign(stored_rows, stored_rows + T);
+        if (!out_handle) return fail(EB_ERR_INVALID, "eb_create_tables: out_handle is NULL");
+        *out_handle = nullptr;
+        if (T < 1) return fail(EB_ERR_INVALID, "eb_create_tables: T must be >= 1");
+        if (!table_ptrs || !stored_rows) return fail(EB_ERR_INVALID, "eb_create_tables: NULL table_ptrs or stored_rows");
+        if (D < 1) return fail(EB_ERR_INVALID, "eb_create_tables: D must be >= 1");
+        if (dtype != EB_F32 && dtype != EB_F16 && dtype != EB_BF16)
+            return fail(EB_ERR_INVALID, "eb_create_tables: unknown dtype");
+        for (int32_t t = 0; t < T; ++t) {
+            if (stored_rows[t] < 0) return fail(EB_ERR_INVALID, "eb_create_tables: negative stored_rows");
+            if (!table_ptrs[t] && stored_rows[t] > 0)
+                return fail(EB_ERR_INVALID, "eb_create_tables: NULL table pointer with stored rows");
+        }
+        eb_tables *h = new (std::nothrow) eb_tables;
+        if (!h) return fail(EB_ERR_NOMEM, "eb_create_tables: out of host memory");
+        try {
+            h->T = T;
+            h->D = D;
+            h->dtype = dtype;
+            h->ptrs.assign((const char *const *)table_ptrs, (const char *const *)table_ptrs + T);
+            h->stored_rows.assign(stored_rows, stored_rows + T);
+        } catch (...) {
+            delete h;
+            return fail(EB_ERR_NOMEM, "eb_create_tables: out of host memory");
+        }
+        h->aligned16 = true;
+        for (int32_t t = 0; t < T; ++t)
+            if (((uintptr_t)h->ptrs[t]) % 16 != 0) h->aligned16 = false;
+        *out_handle = h;
+        return EB_OK;
     } catch (...) {
-        delete h;
-        return fail(EB_ERR_NOMEM, "eb_create_tables: out of host memory");
+        return eb_detail::unexpected_exception("eb_create_tables");
     }
-    h->aligned16 = true;
-    for (int32_t t = 0; t < T; ++t)
-        if (((uintptr_t)h->ptrs[t]) % 16 != 0) h->aligned16 = false;
-    *out_handle = h;
-    return EB_OK;
 }
 
 void eb_destroy(eb_tables *tables) { delete tables; }
 
-const char *eb_last_error(void) { return g_last_error.c_str(); }
+const char *eb_last_error(void) { return eb_detail::last_error(); }
 
 int eb_forward(const eb_tables *h, int32_t T, const int64_t *rows, int32_t D, int32_t dtype,
                const int64_t *indices, int64_t nnz, const int64_t *offsets, int64_t B, int32_t mode,
                int64_t shard_lo, int64_t shard_hi, float *out, int32_t *hits, void *stream)
 {
-    const int64_t ldo = (T > 0 && D > 0) ? (int64_t)T * D : 0; // overflow is caught below
-    return forward_impl("eb_forward", h, T, rows, D, dtype, EB_IDX_I64, indices, nnz, offsets, nullptr, B,
-                        mode, shard_lo, shard_hi, out, ldo, nullptr, hits, T, stream);
+    try {
+        const int64_t ldo = (T > 0 && D > 0) ? (int64_t)T * D : 0; // overflow is caught below
+        return forward_impl("eb_forward", h, T, rows, D, dtype, EB_IDX_I64, indices, nnz, offsets, nullptr, B,
+                            mode, shard_lo, shard_hi, out, ldo, nullptr, hits, T, stream);
+    } catch (...) {
+        return eb_detail::unexpected_exception("eb_forward");
+    }
 }
 
 int eb_forward_ex(const eb_tables *h, int32_t T, const int64_t *rows, int32_t D, int32_t dtype,
@@ -328,8 +369,12 @@ int eb_forward_ex(const eb_tables *h, int32_t T, const int64_t *rows, int32_t D,
                   float *out, int64_t ldo, const int64_t *out_cols, int32_t *hits, int64_t ldh,
                   void *stream)
 {
-    return forward_impl("eb_forward_ex", h, T, rows, D, dtype, index_type, indices, nnz, offsets, weights,
-                        B, mode, shard_lo, shard_hi, out, ldo, out_cols, hits, ldh, stream);
+    try {
+        return forward_impl("eb_forward_ex", h, T, rows, D, dtype, index_type, indices, nnz, offsets, weights,
+                            B, mode, shard_lo, shard_hi, out, ldo, out_cols, hits, ldh, stream);
+    } catch (...) {
+        return eb_detail::unexpected_exception("eb_forward_ex");
+    }
 }
 
 } // extern "C"

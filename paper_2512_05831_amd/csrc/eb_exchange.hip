@@ -54,7 +54,6 @@
 #include <algorithm>
 #include <cstring>
 #include <limits>
-#include <string>
 
 #include "../../include/eb.h"
 #include "eb_internal.h"
@@ -849,9 +848,9 @@ int64_t start_entries(int64_t TB) { return TB / kStartStride + 1; }
 
 } // namespace
 
-extern "C" {
+namespace {
 
-int eb_bucketize_workspace(int32_t T, int64_t B, int32_t G, size_t *bytes)
+int bucketize_workspace_impl(int32_t T, int64_t B, int32_t G, size_t *bytes)
 {
     if (!bytes) return fail(EB_ERR_INVALID, "eb_bucketize_workspace: NULL bytes");
     *bytes = 0;
@@ -864,13 +863,13 @@ int eb_bucketize_workspace(int32_t T, int64_t B, int32_t G, size_t *bytes)
     return EB_OK;
 }
 
-int eb_bucketize(int32_t T, int64_t B, int32_t G, const int64_t *bounds, const int64_t *indices,
-                 int64_t nnz, const int64_t *offsets, int64_t *out_offsets, int64_t *out_indices,
-                 int64_t out_capacity, int64_t *segments, void *workspace, size_t workspace_bytes,
-                 void *stream)
+int bucketize_impl(int32_t T, int64_t B, int32_t G, const int64_t *bounds, const int64_t *indices,
+                   int64_t nnz, const int64_t *offsets, int64_t *out_offsets, int64_t *out_indices,
+                   int64_t out_capacity, int64_t *segments, void *workspace, size_t workspace_bytes,
+                   void *stream)
 {
     size_t need = 0;
-    const int rc = eb_bucketize_workspace(T, B, G, &need);
+    const int rc = bucketize_workspace_impl(T, B, G, &need);
     if (rc != EB_OK) return rc;
     if (nnz < 0 || out_capacity < 0) return fail(EB_ERR_INVALID, "eb_bucketize: negative nnz or out_capacity");
     if (!segments || !out_offsets) return fail(EB_ERR_INVALID, "eb_bucketize: NULL segments or out_offsets");
@@ -918,7 +917,7 @@ int eb_bucketize(int32_t T, int64_t B, int32_t G, const int64_t *bounds, const i
         void *args[] = {&ba};
         hipError_t err = hipLaunchKernel((const void *)eb_bucket_count, dim3((unsigned)(T * bpt)),
                                          dim3(kBlock), args, count_lds_bytes(G), st);
-        if (err != hipSuccess) return fail(EB_ERR_HIP, std::string("eb_bucketize: ") + hipGetErrorString(err));
+        if (err != hipSuccess) return fail(EB_ERR_HIP, "eb_bucketize: %s", hipGetErrorString(err));
         void *sargs[] = {&sa};
         err = hipLaunchKernel((const void *)eb_scan_tile_sums, dim3(sa.ntiles, G), dim3(kBlock), sargs, 0, st);
         if (err == hipSuccess && !sa.fused)
@@ -928,19 +927,19 @@ int eb_bucketize(int32_t T, int64_t B, int32_t G, const int64_t *bounds, const i
         if (err == hipSuccess)
             err = hipLaunchKernel((const void *)eb_bucket_scatter, dim3((unsigned)(T * bpt)), dim3(kBlock), args,
                                   scatter_lds_bytes(G), st);
-        if (err != hipSuccess) return fail(EB_ERR_HIP, std::string("eb_bucketize: ") + hipGetErrorString(err));
+        if (err != hipSuccess) return fail(EB_ERR_HIP, "eb_bucketize: %s", hipGetErrorString(err));
     } else {
         // No bags: every destination is empty.
         sa.ntiles = 0;
         void *sargs[] = {&sa};
         hipError_t err = hipLaunchKernel((const void *)eb_scan_tile_prefix, dim3(1), dim3(kBlock), sargs, 0, st);
-        if (err != hipSuccess) return fail(EB_ERR_HIP, std::string("eb_bucketize: ") + hipGetErrorString(err));
+        if (err != hipSuccess) return fail(EB_ERR_HIP, "eb_bucketize: %s", hipGetErrorString(err));
     }
     return EB_OK;
 }
 
-int eb_sum_partials(int32_t G, const float *partials, int64_t B, int32_t T, int32_t D,
-                    const int64_t *mean_offsets, int64_t nnz, float *out, void *stream)
+int sum_partials_impl(int32_t G, const float *partials, int64_t B, int32_t T, int32_t D,
+                      const int64_t *mean_offsets, int64_t nnz, float *out, void *stream)
 {
     if (G < 1 || B < 0 || T < 0 || D < 1 || nnz < 0)
         return fail(EB_ERR_INVALID, "eb_sum_partials: bad G, B, T, D or nnz");
@@ -965,8 +964,44 @@ int eb_sum_partials(int32_t G, const float *partials, int64_t B, int32_t T, int3
     void *args[] = {&a};
     hipError_t err = hipLaunchKernel(vec ? (const void *)eb_sum_partials_vec4 : (const void *)eb_sum_partials_scalar,
                                      dim3((unsigned)grid), dim3(kBlock), args, 0, (hipStream_t)stream);
-    if (err != hipSuccess) return fail(EB_ERR_HIP, std::string("eb_sum_partials: ") + hipGetErrorString(err));
+    if (err != hipSuccess) return fail(EB_ERR_HIP, "eb_sum_partials: %s", hipGetErrorString(err));
     return EB_OK;
+}
+
+} // namespace
+
+extern "C" {
+
+int eb_bucketize_workspace(int32_t T, int64_t B, int32_t G, size_t *bytes)
+{
+    try {
+        return bucketize_workspace_impl(T, B, G, bytes);
+    } catch (...) {
+        return eb_detail::unexpected_exception("eb_bucketize_workspace");
+    }
+}
+
+int eb_bucketize(int32_t T, int64_t B, int32_t G, const int64_t *bounds, const int64_t *indices,
+                 int64_t nnz, const int64_t *offsets, int64_t *out_offsets, int64_t *out_indices,
+                 int64_t out_capacity, int64_t *segments, void *workspace, size_t workspace_bytes,
+                 void *stream)
+{
+    try {
+        return bucketize_impl(T, B, G, bounds, indices, nnz, offsets, out_offsets, out_indices, out_capacity,
+                              segments, workspace, workspace_bytes, stream);
+    } catch (...) {
+        return eb_detail::unexpected_exception("eb_bucketize");
+    }
+}
+
+int eb_sum_partials(int32_t G, const float *partials, int64_t B, int32_t T, int32_t D,
+                    const int64_t *mean_offsets, int64_t nnz, float *out, void *stream)
+{
+    try {
+        return sum_partials_impl(G, partials, B, T, D, mean_offsets, nnz, out, stream);
+    } catch (...) {
+        return eb_detail::unexpected_exception("eb_sum_partials");
+    }
 }
 
 } // extern "C"

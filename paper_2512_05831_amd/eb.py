@@ -273,11 +273,12 @@ class EmbeddingBagTables:
         itype = _index_type(indices, offsets)
         if out is None:
             out = torch.empty((B, self.T * self.D), dtype=torch.float32, device=dev)
+        # The library writes rows of unit column stride, whatever B is.
         if out.dtype != torch.float32 or out.dim() != 2 or out.shape[0] != B or \
-                (B > 1 and out.stride(1) != 1):
+                (out.shape[1] > 1 and out.stride(1) != 1):
             raise ValueError("out must be fp32 [B, W] with unit column stride")
         if hits is not None and (hits.dtype != torch.int32 or hits.dim() != 2 or
-                                 hits.shape[0] != B or (B > 1 and hits.stride(1) != 1)):
+                                 hits.shape[0] != B or (hits.shape[1] > 1 and hits.stride(1) != 1)):
             raise ValueError("hits must be int32 [B, >= T] with unit column stride")
         if offsets.numel() != self.T * B + 1:
             raise ValueError("offsets must have T*B+1 entries")

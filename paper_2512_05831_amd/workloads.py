@@ -16,7 +16,9 @@ shapes below are the five single-GPU workloads this library is measured on:
   4. 16 tables 1,000,000 rows, D in {16,...,512}, fp16 / bf16, B=4096, fixed
      length 64, uniform ids;
   5. a 400,000,000-row id space of which this GPU stores rows [0, 5e7) x 256
-     fp16, B=65536, fixed length 80, Zipf(0.9) ranks used as ids directly.
+     fp16, B=65536, fixed length 80, Zipf(0.9) ranks used as ids directly
+     (about 78% of lookups local) or, as a variant, mapped through a seeded
+     permutation of the id space (about 12% local).
 
 Recipe (deterministic; any part can be regenerated alone):
   * every stream is numpy PCG64 seeded by SeedSequence([seed, purpose, t, ...])
@@ -28,7 +30,9 @@ Recipe (deterministic; any part can be regenerated alone):
   * "dyadic" tables hold k * 2^-12 (k integer, |k| <= 2048; bf16: k * 2^-8,
     |k| <= 127), so every partial sum of a few hundred of them is exact in fp32;
   * bounded Zipf ranks use Hoermann and Derflinger's rejection-inversion
-    sampler (ACM TOMACS 6(3), 1996).
+    sampler (ACM TOMACS 6(3), 1996);
+  * a permutation of a table's ids is a seeded shuffle, or for the 400M-id
+    space a keyed Feistel network with cycle walking, applied pointwise.
 """
 from __future__ import annotations
 
@@ -96,8 +100,10 @@ def _table_key(seed: int, t: int) -> np.uint64:
     return np.random.SeedSequence([int(seed), PURPOSE_VALUES, int(t)]).generate_state(1, np.uint64)[0]
 
 
-def _rows_values(key: np.uint64, rows: np.ndarray, D: int, dtype: int, values: str) -> np.ndarray:
-    """Stored values of the given global rows: [len(rows), D]."""
+def _rows_values(key: np.uint64, rows: np.ndarray, D: int, dtype: int, values: str,
+                 master: bool = False) -> np.ndarray:
+    """Stored values of the given global rows: [len(rows), D]; with ``master``
+    the fp32 values before rounding to the storage type."""
     z = rows.astype(np.uint64)[:, None] * np.uint64(D) + np.arange(1, D + 1, dtype=np.uint64)
     with np.errstate(over="ignore"):
         z *= _GOLDEN
@@ -129,16 +135,19 @@ def _rows_values(key: np.uint64, rows: np.ndarray, D: int, dtype: int, values: s
             x = k.astype(np.float32) * np.float32(2.0 ** -12)
     else:
         raise ValueError(f"unknown value recipe {values!r}")
-    return to_storage(x, dtype)
+    return x if master else to_storage(x, dtype)
 
 
-def table_rows(seed: int, t: int, D: int, dtype: int, rows, values: str = "normal") -> np.ndarray:
-    """Stored values of an arbitrary list of global rows of table t."""
+def table_rows(seed: int, t: int, D: int, dtype: int, rows, values: str = "normal",
+               master: bool = False) -> np.ndarray:
+    """Stored values of an arbitrary list of global rows of table t (with
+    ``master``: the fp32 values they were rounded from)."""
     rows = np.asarray(rows, dtype=np.int64).reshape(-1)
-    out = np.empty((rows.size, D), dtype=storage_np_dtype(dtype))
+    out = np.empty((rows.size, D), dtype=np.float32 if master else storage_np_dtype(dtype))
     key = _table_key(seed, t)
     for lo in range(0, rows.size, _CHUNK_ROWS):
-        out[lo:lo + _CHUNK_ROWS] = _rows_values(key, rows[lo:lo + _CHUNK_ROWS], D, dtype, values)
+        out[lo:lo + _CHUNK_ROWS] = _rows_values(key, rows[lo:lo + _CHUNK_ROWS], D, dtype, values,
+                                                master)
     return out
 
 
@@ -256,13 +265,72 @@ def permutation(seed: int, t: int, N: int) -> np.ndarray:
     return rng(seed, PURPOSE_PERM, t).permutation(N).astype(np.int64)
 
 
+def _mix64(z: np.ndarray) -> np.ndarray:
+    """SplitMix64's output function, in place on a uint64 array."""
+    with np.errstate(over="ignore"):
+        for shift, mult in ((30, _MIX1), (27, _MIX2)):
+            z ^= z >> np.uint64(shift)
+            z *= mult
+        z ^= z >> np.uint64(31)
+    return z
+
+
+def feistel_permute(seed: int, t: int, N: int, x) -> np.ndarray:
+    """Image of x (values in [0, N)) under a seeded permutation of [0, N),
+    computed pointwise, for id spaces too large to shuffle whole.
+
+    A four-round Feistel network on 2h-bit words (2^(2h) >= N; the round
+    function is SplitMix64's output function of the right half plus a round
+    key, masked to h bits) permutes [0, 2^(2h)); cycle walking (re-applying it
+    until the value falls below N) restricts that to a permutation of [0, N)
+    (Black & Rogaway, "Ciphers with Arbitrary Finite Domains", CT-RSA 2002).
+    Fewer than 4 rounds of walking are expected, since 2^(2h) < 4N."""
+    x = np.asarray(x, dtype=np.int64)
+    if N < 1 or np.any(x < 0) or np.any(x >= N):
+        raise ValueError("feistel_permute needs 0 <= x < N")
+    h = max(1, ((int(N) - 1).bit_length() + 1) // 2)
+    mask = np.uint64((1 << h) - 1)
+    keys = np.random.SeedSequence([int(seed), PURPOSE_PERM, int(t)]).generate_state(4, np.uint64)
+    sh = np.uint64(h)
+
+    def encrypt(v):
+        left, right = v >> sh, v & mask
+        for k in keys:
+            with np.errstate(over="ignore"):
+                f = _mix64((right + k) * _GOLDEN) & mask
+            left, right = right, left ^ f
+        return (left << sh) | right
+
+    def walk(v):
+        y = encrypt(v)
+        out = y >= np.uint64(N)
+        while np.any(out):
+            y[out] = encrypt(y[out])
+            out = y >= np.uint64(N)
+        return y
+
+    x = x.astype(np.uint64).reshape(-1)
+    chunk = 1 << 18
+    if x.size <= chunk:
+        return walk(x).astype(np.int64)
+    with ThreadPoolExecutor(_threads()) as ex:
+        parts = list(ex.map(walk, [x[i:i + chunk] for i in range(0, x.size, chunk)]))
+    return np.concatenate(parts).astype(np.int64)
+
+
 def indices_for_table(seed: int, t: int, n: int, id_space: int, dist: str, alpha: float = 0.0,
-                      permuted: bool = False) -> np.ndarray:
+                      permuted: bool = False, perm: str = "shuffle") -> np.ndarray:
+    """n ids of table t.  Zipf ranks become ids through a seeded permutation
+    of the id space when ``permuted``: a whole shuffle ("shuffle") or the
+    pointwise Feistel permutation ("feistel", for id spaces too large to
+    shuffle), else rank r is id r - 1."""
     g = rng(seed, PURPOSE_INDICES, t)
     if dist == "uniform":
         return g.integers(0, id_space, n, dtype=np.int64)
     if dist == "zipf":
         ranks = zipf_ranks(g, n, id_space, alpha)
+        if permuted and perm == "feistel":
+            return feistel_permute(seed, t, id_space, ranks - 1)
         if permuted:
             return permutation(seed, t, id_space)[ranks - 1]
         return ranks - 1
@@ -289,6 +357,7 @@ class Workload:
     dist: str = "uniform"          # "uniform" or "zipf"
     alpha: float = 0.0
     permuted: bool = False
+    perm: str = "shuffle"          # permutation of Zipf ranks: "shuffle" or "feistel"
     shard_lo: int = 0
     shard_hi: int = INT64_MAX
     modes: tuple = (SUM,)
@@ -325,11 +394,17 @@ class Workload:
     def indices(self, offsets: np.ndarray | None = None) -> np.ndarray:
         if offsets is None:
             offsets = self.offsets()
-        parts = []
-        for t in range(self.T):
+        def one(t):
             n = int(offsets[(t + 1) * self.B] - offsets[t * self.B])
-            parts.append(indices_for_table(self.seed, t, n, self.rows, self.dist, self.alpha,
-                                           self.permuted))
+            return indices_for_table(self.seed, t, n, self.rows, self.dist, self.alpha,
+                                     self.permuted, self.perm)
+
+        # every table has its own stream, so threads change no value
+        if self.T > 1:
+            with ThreadPoolExecutor(_threads()) as ex:
+                parts = list(ex.map(one, range(self.T)))
+        else:
+            parts = [one(t) for t in range(self.T)]
         return np.concatenate(parts) if parts else np.zeros(0, dtype=np.int64)
 
     def table(self, t: int, out: np.ndarray | None = None) -> np.ndarray:
@@ -339,12 +414,21 @@ class Workload:
     def tables(self) -> list:
         return [self.table(t) for t in range(self.T)]
 
+    def master_rows(self, t: int, rows) -> np.ndarray:
+        """fp32 values of the given global rows of table t before rounding to
+        the storage type."""
+        return table_rows(self.seed, t, self.D, self.dtype, rows, self.values, master=True)
+
     def with_(self, **kw) -> "Workload":
         return dataclasses.replace(self, **kw)
 
 
-def config(cid: int, D: int | None = None, dtype: int | None = None) -> Workload:
-    """The five measured workloads (see the module docstring), seed 1000 + id."""
+def config(cid: int, D: int | None = None, dtype: int | None = None,
+           permuted: bool = False) -> Workload:
+    """The five measured workloads (see the module docstring), seed 1000 + id.
+    ``permuted`` (workload 5 only) maps the Zipf ranks through a seeded
+    permutation of the 400M-id space, so the hot ids spread over all row
+    blocks and about 1/8 of the lookups fall in this GPU's."""
     seed = 1000 + cid
     if cid == 1:
         return Workload("single-table-100k-d64-f32-b256-l20", T=1, rows=100_000, D=64, dtype=F32,
@@ -362,9 +446,10 @@ def config(cid: int, D: int | None = None, dtype: int | None = None) -> Workload
         return Workload(f"16x1M-d{D}-{DTYPE_NAMES[dtype]}-b4096-l64-uniform", T=16,
                         rows=1_000_000, D=D, dtype=dtype, B=4096, L=64, seed=seed)
     if cid == 5:
-        return Workload("shard0of8-400M-d256-f16-b65536-l80-zipf0.9", T=1, rows=400_000_000,
-                        D=256, dtype=F16, B=65536, L=80, dist="zipf", alpha=0.9, permuted=False,
-                        shard_lo=0, shard_hi=50_000_000, want_hits=True, seed=seed)
+        return Workload("shard0of8-400M-d256-f16-b65536-l80-zipf0.9" + ("-permuted" if permuted else ""),
+                        T=1, rows=400_000_000, D=256, dtype=F16, B=65536, L=80, dist="zipf",
+                        alpha=0.9, permuted=permuted, perm="feistel", shard_lo=0,
+                        shard_hi=50_000_000, want_hits=True, seed=seed)
     raise ValueError(f"no workload {cid}")
 
 

@@ -265,3 +265,34 @@ def test_sum_partials_rejects(kw):
 def test_sum_partials_empty_is_noop():
     sum_partials(B=0, partials_ptr=None, out_ptr=None)
     sum_partials(T=0, partials_ptr=None, out_ptr=None)
+
+
+@pytest.mark.parametrize("T", [5, 1500])  # the sorted check (T <= 1024) and the pairwise one
+def test_forward_ex_column_overlap_any_table_count(T):
+    D = 4
+    h = handle(T=T, D=D, rows=[100] * T)
+    try:
+        cols = [D * (T - 1 - t) for t in range(T)]   # disjoint, listed backwards
+        bad = list(cols)
+        bad[0] = bad[-1] + D - 1                    # the first table now overlaps the last by one
+        kw = dict(T=T, rows=[100] * T, D=D, ldo=T * D)
+        assert code_of(lambda: forward_ex(h, out_cols=bad, **kw)) == eb.EB_ERR_INVALID
+        assert "share output columns" in eb.eb_last_error()
+        # disjoint columns pass the overlap check and stop at the next one
+        assert code_of(lambda: forward_ex(h, out_cols=cols, **dict(kw, rows=[-1] * T))) == \
+            eb.EB_ERR_INVALID
+        assert "negative rows" in eb.eb_last_error()
+    finally:
+        eb.eb_destroy(h)
+
+
+def test_error_messages_name_the_table_and_stay_bounded():
+    h = handle(T=3, rows=(100, 100, 10))
+    try:
+        # stored rows of table 2 (10) do not cover its 100 gatherable rows
+        assert code_of(lambda: forward(h, T=3, rows=[100, 100, 100])) == eb.EB_ERR_INVALID
+        msg = eb.eb_last_error()
+        assert "table 2" in msg and msg.startswith("eb_forward: ")
+        assert len(msg) < 512
+    finally:
+        eb.eb_destroy(h)

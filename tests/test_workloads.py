@@ -139,3 +139,52 @@ def test_literal_zipf_shard_hit_fraction():
     idx = w.indices()
     frac = np.mean(idx < w.shard_hi)
     assert 0.76 < frac < 0.81
+
+
+@pytest.mark.parametrize("N", [1, 2, 3, 5, 64, 1000, 4097, 65536, 100003])
+def test_feistel_permute_is_a_permutation(N):
+    p = wl.feistel_permute(1005, 0, N, np.arange(N))
+    assert np.array_equal(np.sort(p), np.arange(N))
+    # pointwise: any subset maps as the whole does, and the map is seeded
+    sub = np.arange(N)[::7]
+    assert np.array_equal(wl.feistel_permute(1005, 0, N, sub), p[sub])
+    if N > 64:
+        assert not np.array_equal(wl.feistel_permute(1006, 0, N, np.arange(N)), p)
+        assert not np.array_equal(p, np.arange(N))
+
+
+def test_feistel_permute_rejects_out_of_range():
+    with pytest.raises(ValueError):
+        wl.feistel_permute(1, 0, 10, [10])
+    with pytest.raises(ValueError):
+        wl.feistel_permute(1, 0, 10, [-1])
+
+
+def test_permuted_shard_workload_spreads_hot_ids():
+    """The permuted reading of the 400M-id shard workload: the same Zipf
+    ranks as the literal one, mapped one-to-one, so about 1/8 of the lookups
+    stay in rows [0, 5e7) (the literal reading keeps about 78%)."""
+    lit = wl.config(5)
+    per = wl.config(5, permuted=True)
+    assert per.name == lit.name + "-permuted"
+    off = lit.offsets()
+    a = lit.with_(B=4096).indices(lit.with_(B=4096).offsets())
+    b = per.with_(B=4096).indices(per.with_(B=4096).offsets())
+    # rank r of the literal reading is id r - 1; the permuted one maps it
+    assert np.array_equal(b, wl.feistel_permute(per.seed, 0, per.rows, a))
+    frac = np.mean(b < per.shard_hi)
+    assert 0.10 < frac < 0.15, frac
+    assert 0.74 < np.mean(a < lit.shard_hi) < 0.82
+    assert off.size == lit.T * lit.B + 1
+
+
+@pytest.mark.parametrize("dtype", [wl.F32, wl.F16, wl.BF16])
+def test_master_values_round_to_the_stored_ones(dtype):
+    rows = np.array([0, 5, 99_999, 123_456_789])
+    m = wl.table_rows(1004, 3, 64, dtype, rows, master=True)
+    s = wl.table_rows(1004, 3, 64, dtype, rows)
+    assert m.dtype == np.float32 and m.shape == (4, 64)
+    assert np.array_equal(wl.to_storage(m, dtype), s)
+    w = wl.config(4, D=64, dtype=dtype if dtype != wl.F32 else wl.F16)
+    assert np.array_equal(wl.to_storage(w.master_rows(2, rows), w.dtype),
+                          wl.table_rows(w.seed, 2, 64, w.dtype, rows))
