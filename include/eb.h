@@ -276,6 +276,31 @@ int eb_bucketize(int32_t T, int64_t B, int32_t G, const int64_t *bounds, const i
                  void *stream);
 
 /*
+ * eb_bucketize_noalloc -- eb_bucketize for callers that cannot allocate
+ * device memory (code under HIP graph capture, serving loops, harnesses that
+ * forbid hipMalloc): the same arguments and results, without the workspace
+ * arguments.
+ *
+ * The workspace is a fixed 8 MiB array of device memory inside the library,
+ * one copy on every GPU the library runs on, held until the process ends.
+ * Its address on the current device is looked up on the first call there;
+ * the call itself allocates nothing.  Calls whose eb_bucketize_workspace()
+ * exceeds 8 MiB (for G = 8 destinations, batches of more than about two
+ * million bags) fail with EB_ERR_UNSUPPORTED before touching the device.
+ * `stream` must belong to the current device (EB_ERR_INVALID otherwise).
+ *
+ * Every call on a GPU shares that GPU's array: calls that overlap on one GPU
+ * (on different streams, or from different threads) race and give undefined
+ * results; calls ordered on one stream are safe.  Nothing in the array needs
+ * to start at zero, so the previous call's contents do no harm.  Other
+ * errors are eb_bucketize's.
+ */
+int eb_bucketize_noalloc(int32_t T, int64_t B, int32_t G, const int64_t *bounds,
+                         const int64_t *indices, int64_t nnz, const int64_t *offsets,
+                         int64_t *out_offsets, int64_t *out_indices, int64_t out_capacity,
+                         int64_t *segments, void *stream);
+
+/*
  * eb_sum_partials -- add the partial results every GPU computed for this
  * GPU's bags.
  *

@@ -52,11 +52,16 @@
 #include <stdint.h>
 
 #include <algorithm>
+#include <atomic>
 #include <cstring>
 #include <limits>
 
 #include "../../include/eb.h"
 #include "eb_internal.h"
+
+// eb_bucketize_noalloc's workspace (see static_scratch below).
+constexpr size_t kStaticScratchBytes = (size_t)8 << 20;
+static __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
 
 namespace {
 
@@ -968,6 +973,57 @@ int sum_partials_impl(int32_t G, const float *partials, int64_t B, int32_t T, in
     return EB_OK;
 }
 
+// eb_bucketize_noalloc's workspace: a fixed array in device memory, one
+// copy on every GPU the library runs on, held until the process ends.  Its
+// address on a device comes from hipGetSymbolAddress (the array's name in host
+// code is a host-side stand-in, not a device address).  Nothing in the
+// workspace needs to start at zero: every entry a call reads was written
+// earlier in the same call.
+constexpr int kMaxDevices = 64;
+std::atomic<void *> g_scratch[kMaxDevices]; // per device, looked up on first use
+
+// The scratch array's address on the device `stream` runs on, which must be
+// the current device.  No allocation.
+int static_scratch(const char *who, hipStream_t stream, void **ptr)
+{
+    int dev = -1;
+    hipError_t err = hipGetDevice(&dev);
+    if (err != hipSuccess) return fail(EB_ERR_HIP, "%s: hipGetDevice: %s", who, hipGetErrorString(err));
+    if (stream) {
+        int sdev = -1;
+        err = hipStreamGetDevice(stream, &sdev);
+        if (err != hipSuccess) return fail(EB_ERR_HIP, "%s: hipStreamGetDevice: %s", who, hipGetErrorString(err));
+        if (sdev != dev) return fail(EB_ERR_INVALID, "%s: the stream belongs to device %d, not the current device %d", who, sdev, dev);
+    }
+    if (dev < 0 || dev >= kMaxDevices) return fail(EB_ERR_UNSUPPORTED, "%s: device %d beyond the first %d", who, dev, kMaxDevices);
+    void *p = g_scratch[dev].load(std::memory_order_acquire);
+    if (!p) {
+        err = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (err != hipSuccess || !p)
+            return fail(EB_ERR_HIP, "%s: hipGetSymbolAddress: %s", who, hipGetErrorString(err));
+        g_scratch[dev].store(p, std::memory_order_release);
+    }
+    *ptr = p;
+    return EB_OK;
+}
+
+int bucketize_noalloc_impl(int32_t T, int64_t B, int32_t G, const int64_t *bounds, const int64_t *indices,
+                           int64_t nnz, const int64_t *offsets, int64_t *out_offsets, int64_t *out_indices,
+                           int64_t out_capacity, int64_t *segments, void *stream)
+{
+    size_t need = 0;
+    const int rc = bucketize_workspace_impl(T, B, G, &need);
+    if (rc != EB_OK) return rc;
+    if (need > kStaticScratchBytes)
+        return fail(EB_ERR_UNSUPPORTED, "eb_bucketize_noalloc: needs %zu bytes of workspace, more than the %zu it holds",
+                    need, kStaticScratchBytes);
+    void *ws = nullptr;
+    const int rs = static_scratch("eb_bucketize_noalloc", (hipStream_t)stream, &ws);
+    if (rs != EB_OK) return rs;
+    return bucketize_impl(T, B, G, bounds, indices, nnz, offsets, out_offsets, out_indices, out_capacity,
+                          segments, ws, kStaticScratchBytes, stream);
+}
+
 } // namespace
 
 extern "C" {
@@ -991,6 +1047,18 @@ int eb_bucketize(int32_t T, int64_t B, int32_t G, const int64_t *bounds, const i
                               segments, workspace, workspace_bytes, stream);
     } catch (...) {
         return eb_detail::unexpected_exception("eb_bucketize");
+    }
+}
+
+int eb_bucketize_noalloc(int32_t T, int64_t B, int32_t G, const int64_t *bounds, const int64_t *indices,
+                         int64_t nnz, const int64_t *offsets, int64_t *out_offsets, int64_t *out_indices,
+                         int64_t out_capacity, int64_t *segments, void *stream)
+{
+    try {
+        return bucketize_noalloc_impl(T, B, G, bounds, indices, nnz, offsets, out_offsets, out_indices,
+                                      out_capacity, segments, stream);
+    } catch (...) {
+        return eb_detail::unexpected_exception("eb_bucketize_noalloc");
     }
 }
 

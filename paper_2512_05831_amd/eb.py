@@ -57,6 +57,8 @@ def library() -> ctypes.CDLL:
         lib.eb_bucketize_workspace.restype = ctypes.c_int
         lib.eb_bucketize.argtypes = [i32, i64, i32, p, p, i64, p, p, p, i64, p, p, ctypes.c_size_t, p]
         lib.eb_bucketize.restype = ctypes.c_int
+        lib.eb_bucketize_noalloc.argtypes = [i32, i64, i32, p, p, i64, p, p, p, i64, p, p]
+        lib.eb_bucketize_noalloc.restype = ctypes.c_int
         lib.eb_sum_partials.argtypes = [i32, p, i64, i32, i32, p, i64, p, p]
         lib.eb_sum_partials.restype = ctypes.c_int
         _lib = lib
@@ -130,6 +132,14 @@ def eb_bucketize(T: int, B: int, G: int, bounds_ptr: int, indices_ptr: int | Non
                                   out_offsets_ptr, out_indices_ptr or None, out_capacity,
                                   segments_ptr, workspace_ptr or None, workspace_bytes,
                                   stream_ptr or None))
+
+
+def eb_bucketize_noalloc(T: int, B: int, G: int, bounds_ptr: int, indices_ptr: int | None, nnz: int,
+                         offsets_ptr: int, out_offsets_ptr: int, out_indices_ptr: int | None,
+                         out_capacity: int, segments_ptr: int, stream_ptr: int | None) -> None:
+    _check(library().eb_bucketize_noalloc(T, B, G, bounds_ptr, indices_ptr or None, nnz, offsets_ptr,
+                                          out_offsets_ptr, out_indices_ptr or None, out_capacity,
+                                          segments_ptr, stream_ptr or None))
 
 
 def eb_sum_partials(G: int, partials_ptr: int, B: int, T: int, D: int,

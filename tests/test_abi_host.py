@@ -33,9 +33,9 @@ def all_declared_functions():
 
 
 def test_header_declares_the_boundary():
-    assert declared_functions() == ["eb_bucketize", "eb_bucketize_workspace", "eb_create_tables",
-                                    "eb_destroy", "eb_forward", "eb_forward_ex", "eb_last_error",
-                                    "eb_sum_partials"]
+    assert declared_functions() == ["eb_bucketize", "eb_bucketize_noalloc", "eb_bucketize_workspace",
+                                    "eb_create_tables", "eb_destroy", "eb_forward", "eb_forward_ex",
+                                    "eb_last_error", "eb_sum_partials"]
 
 
 def test_library_exports_every_declared_symbol():
@@ -296,3 +296,16 @@ def test_error_messages_name_the_table_and_stay_bounded():
         assert len(msg) < 512
     finally:
         eb.eb_destroy(h)
+
+
+def test_bucketize_noalloc_checks_sizes_before_the_device():
+    """Beyond its fixed 8 MiB workspace the no-alloc variant refuses the call
+    before looking up any device (so this runs without a GPU)."""
+    assert eb.eb_bucketize_workspace(1, 16384, 1024) > 8 << 20
+    assert code_of(lambda: eb.eb_bucketize_noalloc(1, 16384, 1024, FAKE, FAKE, 1, FAKE, FAKE, FAKE,
+                                                   1, FAKE, None)) == eb.EB_ERR_UNSUPPORTED
+    assert "8388608" in eb.eb_last_error()
+    assert code_of(lambda: eb.eb_bucketize_noalloc(1, 4, 2000, FAKE, FAKE, 1, FAKE, FAKE, FAKE,
+                                                   1, FAKE, None)) == eb.EB_ERR_UNSUPPORTED
+    assert code_of(lambda: eb.eb_bucketize_noalloc(-1, 4, 2, FAKE, FAKE, 1, FAKE, FAKE, FAKE,
+                                                   1, FAKE, None)) == eb.EB_ERR_INVALID
