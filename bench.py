@@ -582,7 +582,8 @@ def index_batches(w, n, cache):
 
 def time_workload(torch, dev, eb, cid, w, modes, K, W, nbatches, cache, stream):
     """Entries (one per pooling mode) for one workload: mean launch time over
-    K back-to-back launches (HIP events on the launch stream) and the rates
+    K back-to-back launches (HIP events on the launch stream; "launches" in
+    the entry) and the rates
     and roofline fraction that follow; for skewed ids also single launches
     warm and after a 512 MB flush (the caches' share)."""
     off, batches = index_batches(w, nbatches, cache)
@@ -610,7 +611,7 @@ def time_workload(torch, dev, eb, cid, w, modes, K, W, nbatches, cache, stream):
         name = w.name + ("-mean" if mode == wl.MEAN else "")
         e = {"config": cid, "workload": name, "mode": "sum" if mode == wl.SUM else "mean",
              "storage": wl.DTYPE_NAMES[w.dtype], "rows_cache_policy": "stream" if uniform else "cached",
-             "kernel_us": round(us, 2), "lookups_per_s": n_avg / us * 1e6,
+             "kernel_us": round(us, 2), "launches": K, "lookups_per_s": n_avg / us * 1e6,
              "bags_per_s": w.T * w.B / us * 1e6,
              "algorithmic_bytes_per_launch": int(by), "algorithmic_GBps": round(by / us / 1e3, 1),
              "frac_of_8TBps": round(by / us / 1e3 / HBM_PEAK_GBPS, 4)}
@@ -643,6 +644,9 @@ def all_workloads(torch, dev, eb, headline, K, W, nbatches):
     stream = torch.cuda.Stream(dev)
     entries = [dict(headline, config=2, source="headline run")]
     cache = {}
+    # at least 200 timed launches each: with 20 the mean still carries a few
+    # percent of ramp-up (workload 4 at D 64: 96.6 us over 20, 93.4 over 400)
+    K, W = max(K, 200), max(W, 20)
     for cid, kw, modes in other_workloads():
         w = wl.config(cid, **kw)
         try:
@@ -670,7 +674,8 @@ def main():
     ap.add_argument("--dtype", default="f16", choices=["f16", "bf16"])
     ap.add_argument("--batches", type=int, default=8, help="distinct index batches cycled")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
-    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true",
+                    help="skip the oracle's timing (the tables are then drawn on the device)")
     ap.add_argument("--rows-policy", default="auto", choices=["auto", "cached", "stream"])
     ap.add_argument("--cold", action="store_true",
                     help="also time single launches after writing a 512 MB buffer (caches flushed)")
@@ -731,11 +736,15 @@ def main():
     host_tables = []
     dev_tables = []
     tdt = {wl.F32: torch.float32, wl.F16: torch.float16, wl.BF16: torch.bfloat16}[w.dtype]
-    for t in range(w.T):
-        h = w.table(t)
-        d = torch.from_numpy(h.view(np.int16) if h.dtype == np.uint16 else h).to(dev).view(tdt)
-        host_tables.append(h)
-        dev_tables.append(d)
+    if args.no_cpu_baseline:
+        # no oracle run: nothing needs the tables on the host
+        dev_tables = timing_tables(torch, dev, w, w.seed + 31)
+    else:
+        for t in range(w.T):
+            h = w.table(t)
+            d = torch.from_numpy(h.view(np.int16) if h.dtype == np.uint16 else h).to(dev).view(tdt)
+            host_tables.append(h)
+            dev_tables.append(d)
     log(f"bench: tables resident ({sum(d.numel() * d.element_size() for d in dev_tables) / 1e9:.2f} GB)")
 
     et = eb.EmbeddingBagTables(dev_tables, rows=[w.rows] * w.T, shard_lo=w.shard_lo,
