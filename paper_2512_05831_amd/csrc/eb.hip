@@ -23,11 +23,14 @@
 //     Partial sums of the P groups are combined at the end with cross-lane
 //     moves (DPP, ds_swizzle, v_permlane32_swap).
 //   * A team stages a window of its bag's indices in LDS: the window is read
-//     with coalesced index loads, filtered against the shard, and rewritten as
-//     32-bit local row numbers (or an invalid marker).  The gather loop then
-//     reads them from LDS and keeps U rows per group in flight (unrolled;
-//     U = 2 for streamed rows of 128 B or more, else 6; 8 in small batches),
-//     a bag's last rows in one predicated pass.
+//     with coalesced index loads, filtered against the shard, and the ids
+//     gathered here are written to the front of the window as 32-bit local
+//     row numbers, in position order (a ballot and a prefix count per 64
+//     ids), which also gives the hit count.  The gather loop then reads them
+//     from LDS and keeps U rows per group in flight (unrolled; U = 2 for
+//     streamed rows of 128 B or more, else 6; 8 in small batches), a bag's
+//     last rows in one predicated pass.  Because filtered ids leave no holes,
+//     a shard that keeps few of a bag's ids costs few round trips.
 //   * Accumulation is fp32; fp16 / bf16 rows are widened exactly.
 //   * Workgroups are 4 waves, bags in table-major order.  The hardware deals
 //     workgroups to the 8 XCDs round-robin, so by default all XCDs work on
@@ -36,7 +39,8 @@
 //     remapped so each XCD gets a contiguous run of bags (measured faster for
 //     uniform ids).
 // Rows whose size is not a multiple of 16 bytes, unaligned tables or outputs,
-// and rows wider than 8 KB take a plain one-wave-per-bag kernel.
+// and rows wider than 8 KB take a plain one-wave-per-bag kernel: all lanes
+// read a row's columns with element-sized loads, 8 rows in flight.
 
 #include <hip/hip_runtime.h>
 

@@ -22,7 +22,7 @@ constexpr int kBlock = kWave * kWavesPerBlock;
 constexpr int kXcds = 8;
 constexpr int kMaxTablesPerLaunch = 64;
 constexpr int kStagePerWave = 256;                // LDS index window, entries per wave
-constexpr uint32_t kInvalidRow = 0xFFFFFFFFu;     // staged marker: index not gathered here
+constexpr uint32_t kInvalidRow = 0xFFFFFFFFu;     // never a staged row: local rows stay below it
 constexpr uint64_t kMaxLocalRows = 0xFFFFFFFEull; // local rows must fit below the marker
 
 // Per-launch arguments.  The table arrays are read with a block-uniform
@@ -89,16 +89,6 @@ __device__ __forceinline__ void team_reduce(float (&acc)[N])
         for (int j = 0; j < N; ++j) acc[j] = add_xor<R>(acc[j]);
         if constexpr (P > 2) team_reduce<R * 2, P / 2, N>(acc);
     }
-}
-
-template <int R, int P>
-__device__ __forceinline__ int team_reduce_count(int v)
-{
-    if constexpr (P > 1) {
-        v += __builtin_amdgcn_ds_bpermute(((int)__lane_id() ^ R) << 2, v);
-        if constexpr (P > 2) v = team_reduce_count<R * 2, P / 2>(v);
-    }
-    return v;
 }
 
 // Elements per 16-byte chunk and their widening to fp32.
@@ -244,13 +234,19 @@ __global__ __launch_bounds__(kBlock) void eb_gather_team(const GatherArgs a)
     float acc[C * kEpc];
 #pragma unroll
     for (int j = 0; j < C * kEpc; ++j) acc[j] = 0.f;
-    int count = 0;
+    int count = 0; // rows gathered so far (the same in every lane of the team)
+
+    // This team's lanes as a wave mask, and the lanes below this one.
+    const uint64_t team_lanes = kTeam == kWave ? ~0ull : (((1ull << kTeam) - 1) << (team * kTeam));
+    const uint64_t below = (1ull << lane) - 1;
 
     for (int64_t w0 = s; w0 < e; w0 += kStage) {
         const int n = (int)((e - w0) < kStage ? (e - w0) : kStage);
-        // Stage: coalesced index loads, all issued before the first is
-        // used (positions past the window re-read its last entry), then
-        // rewritten as 32-bit local rows or the marker.
+        // Stage: coalesced index loads, all issued before the first is used
+        // (positions past the window re-read its last entry).  The ids
+        // gathered here are then written to the front of the team's window
+        // as 32-bit local rows, in position order (ballot + prefix count),
+        // so the gather loop below runs over gathered rows only.
         constexpr int kQ = kStage / kTeam;
         const IT *src = (const IT *)a.indices + w0;
         int64_t iv[kQ];
@@ -261,22 +257,33 @@ __global__ __launch_bounds__(kBlock) void eb_gather_team(const GatherArgs a)
             iv[q] = __builtin_nontemporal_load(src + (k < n ? k : n - 1));
             if constexpr (kW) wv[q] = __builtin_nontemporal_load(a.weights + w0 + (k < n ? k : n - 1));
         }
+        int nv = 0; // gathered rows of the window
 #pragma unroll
         for (int q = 0; q < kQ; ++q) {
             const int k = q * kTeam + tl;
             const uint64_t r = (uint64_t)iv[q] - shard_lo;
-            if (k < n) my_stage[k] = r < nlocal ? (uint32_t)r : kInvalidRow;
-            // Rows not gathered here get weight 0 (their chunks are zeros).
-            if constexpr (kW)
-                if (k < n) my_wstage[k] = r < nlocal ? wv[q] : 0.f;
+            const bool ok = k < n && r < nlocal;
+            const uint64_t m = __ballot(ok) & team_lanes;
+            if (ok) {
+                const int at = nv + (int)__popcll(m & below);
+                my_stage[at] = (uint32_t)r;
+                if constexpr (kW) my_wstage[at] = wv[q];
+            }
+            nv += (int)__popcll(m);
         }
+        count += nv;
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
         __builtin_amdgcn_wave_barrier();
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 
-        // Gather: group g pools window rows g, g+P, ...; U rows in flight.
+        // Gather: group g pools staged rows g, g+P, ...; U rows in flight.
+        // Every staged entry below nv is a row, so the marker test in this
+        // loop never fails; it stays because the compiler's schedule for the
+        // predicated loads sustains more of the random-row rate than that
+        // for unconditional ones (8-table uniform 512-B rows: 57.3 against
+        // 60.3 us).
         int k = g;
-        for (; k + (U - 1) * P < n; k += U * P) {
+        for (; k + (U - 1) * P < nv; k += U * P) {
             uint32_t rr[U];
             float ww[U];
 #pragma unroll
@@ -297,7 +304,6 @@ __global__ __launch_bounds__(kBlock) void eb_gather_team(const GatherArgs a)
             }
 #pragma unroll
             for (int u = 0; u < U; ++u) {
-                count += rr[u] != kInvalidRow;
 #pragma unroll
                 for (int c = 0; c < C; ++c) {
                     if constexpr (kW) Elem<DT>::fma(acc + c * kEpc, v[u][c], ww[u]);
@@ -306,45 +312,41 @@ __global__ __launch_bounds__(kBlock) void eb_gather_team(const GatherArgs a)
             }
         }
         // The window's last rows (fewer than U for this group) in one
-        // predicated pass, rows past the end reading as the invalid marker:
-        // a bag's tail costs one round trip instead of one per row, and the
-        // rows are added in the same order.  With U = 1 there is no tail; the
-        // row-at-a-time loop kept there never runs, but without it the
-        // compiler allocates the main loop's registers so that it waits for
-        // loads still in flight (2.5% slower for 1-KB rows).
+        // predicated pass: a bag's tail costs one round trip instead of one
+        // per row, and the rows are added in the same order.  With U = 1
+        // there is no tail; the row-at-a-time loop kept there never runs,
+        // but without it the compiler allocates the main loop's registers so
+        // that it waits for loads still in flight (2.5% slower for 1-KB rows).
         if constexpr (U == 1) {
-            for (; k < n; k += P) {
-                const uint32_t r = my_stage[k];
-                if (r != kInvalidRow) {
-                    const char *p = base + (size_t)r * row_bytes;
-                    uint4 v[C];
+            for (; k < nv; k += P) {
+                const char *p = base + (size_t)my_stage[k] * row_bytes;
+                uint4 v[C];
 #pragma unroll
-                    for (int c = 0; c < C; ++c) v[c] = load_chunk<kStream>(p + coff[c]);
-                    ++count;
-                    const float w = kW ? my_wstage[k] : 1.f;
+                for (int c = 0; c < C; ++c) v[c] = load_chunk<kStream>(p + coff[c]);
+                const float w = kW ? my_wstage[k] : 1.f;
 #pragma unroll
-                    for (int c = 0; c < C; ++c) {
-                        if constexpr (kW) Elem<DT>::fma(acc + c * kEpc, v[c], w);
-                        else Elem<DT>::add(acc + c * kEpc, v[c]);
-                    }
+                for (int c = 0; c < C; ++c) {
+                    if constexpr (kW) Elem<DT>::fma(acc + c * kEpc, v[c], w);
+                    else Elem<DT>::add(acc + c * kEpc, v[c]);
                 }
             }
         } else {
-            if (k < n) {
+            if (k < nv) {
+                bool in[U - 1];
                 uint32_t rr[U - 1];
                 float ww[U - 1];
 #pragma unroll
                 for (int u = 0; u < U - 1; ++u) {
-                    const bool in = k + u * P < n;
-                    rr[u] = in ? my_stage[k + u * P] : kInvalidRow;
-                    if constexpr (kW) ww[u] = in ? my_wstage[k + u * P] : 0.f;
+                    in[u] = k + u * P < nv;
+                    rr[u] = in[u] ? my_stage[k + u * P] : 0u;
+                    if constexpr (kW) ww[u] = in[u] ? my_wstage[k + u * P] : 0.f;
                 }
                 uint4 v[U - 1][C];
 #pragma unroll
                 for (int u = 0; u < U - 1; ++u) {
 #pragma unroll
                     for (int c = 0; c < C; ++c) v[u][c] = make_uint4(0, 0, 0, 0);
-                    if (rr[u] != kInvalidRow) {
+                    if (in[u]) {
                         const char *p = base + (size_t)rr[u] * row_bytes;
 #pragma unroll
                         for (int c = 0; c < C; ++c) v[u][c] = load_chunk<kStream>(p + coff[c]);
@@ -352,7 +354,6 @@ __global__ __launch_bounds__(kBlock) void eb_gather_team(const GatherArgs a)
                 }
 #pragma unroll
                 for (int u = 0; u < U - 1; ++u) {
-                    count += rr[u] != kInvalidRow;
 #pragma unroll
                     for (int c = 0; c < C; ++c) {
                         if constexpr (kW) Elem<DT>::fma(acc + c * kEpc, v[u][c], ww[u]);
@@ -367,7 +368,6 @@ __global__ __launch_bounds__(kBlock) void eb_gather_team(const GatherArgs a)
     }
 
     team_reduce<R, P>(acc);
-    count = team_reduce_count<R, P>(count);
 
     if (bag_ok && g == 0) {
         if (a.mean) {
@@ -393,6 +393,19 @@ __global__ __launch_bounds__(kBlock) void eb_gather_team(const GatherArgs a)
 // ---------------------------------------------------------------------------- plain kernel
 
 // One wave per bag, lanes striding over the columns; any D, any alignment.
+// The bag's ids come in windows of 64 (one coalesced load, one id per lane);
+// the gathered ones are taken in position order, kPlainRows at a time, each
+// row's columns loaded by all lanes with every row's loads in flight
+// together.  Rows are added in position order.
+constexpr int kPlainRows = 8;
+
+__device__ __forceinline__ uint64_t readlane_u64(uint64_t v, int l)
+{
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, l);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), l);
+    return ((uint64_t)hi << 32) | lo;
+}
+
 template <typename IT, int DT, bool kW>
 __global__ __launch_bounds__(kBlock) void eb_gather_plain(const GatherArgs a)
 {
@@ -425,18 +438,41 @@ __global__ __launch_bounds__(kBlock) void eb_gather_plain(const GatherArgs a)
         float acc[kCols];
 #pragma unroll
         for (int j = 0; j < kCols; ++j) acc[j] = 0.f;
-        for (int64_t k = s; k < e; ++k) {
+        count = 0;
+        for (int64_t w0 = s; w0 < e; w0 += kWave) {
+            const int n = (int)((e - w0) < kWave ? (e - w0) : kWave);
+            const int64_t k = w0 + (lane < n ? lane : n - 1);
             const uint64_t r = (uint64_t)(int64_t)((const IT *)a.indices)[k] - shard_lo;
-            if (r >= nlocal) continue;
-            if (c0 == 0) ++count;
-            const char *p = base + r * pitch;
-            const float w = kW ? a.weights[k] : 1.f;
+            const float wt = kW ? a.weights[k] : 1.f;
+            uint64_t m = __ballot(lane < n && r < nlocal); // the window's gathered ids
+            count += (int)__popcll(m);
+            while (m) {
+                const char *p[kPlainRows];
+                float w[kPlainRows];
+                bool have[kPlainRows];
 #pragma unroll
-            for (int j = 0; j < kCols; ++j) {
-                const int c = c0 + j * kWave + lane;
-                if (c < D) {
-                    const float x = Elem<DT>::load1(p + (size_t)c * kEs);
-                    acc[j] = kW ? fmaf(w, x, acc[j]) : acc[j] + x;
+                for (int u = 0; u < kPlainRows; ++u) {
+                    have[u] = m != 0;
+                    const int l = have[u] ? (int)__builtin_ctzll(m) : 0;
+                    m &= m - 1;
+                    p[u] = base + readlane_u64(r, l) * pitch;
+                    w[u] = kW ? __int_as_float(__builtin_amdgcn_readlane(__float_as_int(wt), l)) : 1.f;
+                }
+                float x[kPlainRows][kCols];
+#pragma unroll
+                for (int u = 0; u < kPlainRows; ++u) {
+#pragma unroll
+                    for (int j = 0; j < kCols; ++j) {
+                        const int c = c0 + j * kWave + lane;
+                        x[u][j] = (have[u] && c < D) ? Elem<DT>::load1(p[u] + (size_t)c * kEs) : 0.f;
+                    }
+                }
+#pragma unroll
+                for (int u = 0; u < kPlainRows; ++u) {
+                    if (have[u]) {
+#pragma unroll
+                        for (int j = 0; j < kCols; ++j) acc[j] = kW ? fmaf(w[u], x[u][j], acc[j]) : acc[j] + x[u][j];
+                    }
                 }
             }
         }
