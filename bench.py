@@ -46,8 +46,9 @@ from paper_2512_05831_amd import workloads as wl  # noqa: E402
 
 METRIC = "pooled lookups/sec + effective HBM GB/s (% of MI355X peak) per config"
 HBM_PEAK_GBPS = 8000.0
-# the gather kernel's source: its host side and the kernels themselves
-KERNEL_SRCS = [os.path.join(ROOT, "paper_2512_05831_amd", "csrc", f) for f in ("eb.hip", "eb_gather.h")]
+# the gather kernels and the host code that shapes their launches (the C ABI's
+# argument checks in eb.hip do not change what runs)
+KERNEL_SRCS = [os.path.join(ROOT, "paper_2512_05831_amd", "csrc", "eb_gather.h")]
 PROFILES = os.path.join(ROOT, "profiles")
 
 

@@ -70,46 +70,6 @@ thread_local char g_last_error[512];
 
 using eb_detail::fail;
 
-// Team shape for a row of rb bytes (rb % 16 == 0, rb <= 8192).
-struct Shape {
-    int R, P, C;
-};
-
-// Small batches.  A launch whose normal mapping has fewer waves than the GPU
-// holds (256 CUs x 32) leaves it partly idle, and each bag's chain of
-// dependent loads sets the time.  One wave per bag with 8 rows in flight per
-// lane then wins when bags are long (more than twice the rows the normal
-// mapping keeps in flight per bag) and few enough (measured over the paper's
-// single-GPU shapes: up to 1.5x faster, never slower).
-constexpr int64_t kWaveSlots = 256 * 32;
-constexpr int64_t kFewBagsMax = 2048;
-
-int rows_in_flight_per_bag(const Shape &s, bool stream)
-{
-    const int u_cached = s.C >= 6 ? 1 : 6 / s.C;
-    const int u = (stream && s.R * s.C >= 8) ? (s.C >= 2 ? 1 : 2) : u_cached;
-    return s.P * u;
-}
-
-
-// single: one lane group per bag for large batches; 256-B and 1-KB rows
-// then go to 16-lane teams (1 or 4 chunks per lane), and 512-B rows too when
-// narrow512 is set (else 32-lane teams).
-Shape team_shape(int rb, bool few, bool single, bool narrow512 = false)
-{
-    Shape s;
-    const int chunks = rb / 16;
-    s.R = 1;
-    while (s.R < chunks && s.R < kWave) s.R *= 2;
-    s.C = (chunks + s.R - 1) / s.R;
-    if (single && (rb == 256 || rb == 1024 || (rb == 512 && narrow512))) {
-        s.R = 16;
-        s.C = rb / 256;
-    }
-    s.P = groups_per_bag(s.R, few, single);
-    return s;
-}
-
 } // namespace
 
 int eb_detail::fail(int code, const char *fmt, ...)
@@ -219,52 +179,13 @@ int forward_impl(const char *who, const eb_tables *h, int32_t T, const int64_t *
             return fail(EB_ERR_UNSUPPORTED, "%s: more than 4294967294 gatherable rows in a table", who);
     }
 
-    const int64_t rb = (int64_t)D * elem_bytes(dtype);
     // 16-byte stores need every (bag, table) output row start 16-byte aligned.
     bool out_aligned = ((uintptr_t)out) % 16 == 0 && ldo % 4 == 0;
     for (int32_t t = 0; t < T; ++t) out_aligned = out_aligned && out_col(out_cols, t, D) % 4 == 0;
-    const bool team_path = rb % 16 == 0 && rb <= 8192 && h->aligned16 && out_aligned;
-    const bool i32 = index_type == EB_IDX_I32;
-    KernelFn fn = nullptr;
-    int bags_per_block = kWavesPerBlock;
-    bool xcd_remap = false;
-    if (team_path) {
-        // Non-temporal loads lose for rows narrower than 128 bytes.
-        const bool stream = (mode & EB_HINT_STREAM_ROWS) && rb >= 128;
-        const Shape normal = team_shape((int)rb, false, false);
-        const int64_t bags = (int64_t)T * B;
-        const int64_t waves = bags / (kWave / (normal.R * normal.P));
-        const bool few = waves < kWaveSlots && bags <= kFewBagsMax &&
-                         nnz > 2 * (int64_t)rows_in_flight_per_bag(normal, stream) * bags;
-        // Teams narrower than a wave, one lane group per bag, when they still
-        // give half the GPU's wave slots or more: for streamed rows, and for
-        // cached rows when the mean bag is shorter than the rows the normal
-        // mapping keeps in flight per bag (most of a wave would idle: the
-        // bags a row block receives in a row-wise exchange).  512-B rows take
-        // 32-lane teams when streamed (16-lane teams were 2-5% slower on the
-        // paper's multi-table shapes) and 16-lane teams for short cached bags.
-        const bool short_bags = nnz < (int64_t)rows_in_flight_per_bag(normal, false) * bags;
-        const Shape narrow = team_shape((int)rb, false, true, !stream && short_bags);
-        const int narrow_team = narrow.R * narrow.P;
-        const bool single = (stream || short_bags) && !few && narrow_team < normal.R * normal.P &&
-                            bags / (kWave / narrow_team) >= kWaveSlots / 2;
-        const Shape sh = few ? team_shape((int)rb, true, false) : single ? narrow : normal;
-        fn = weights ? pick_weighted_kernel(i32, dtype, true, sh.R, sh.C, stream, few, single)
-                     : pick_kernel<false>(i32, dtype, true, sh.R, sh.C, stream, few, single);
-        bags_per_block = (kWave / (sh.R * sh.P)) * kWavesPerBlock;
-        // No reuse: each XCD takes a contiguous run of bags.  Otherwise
-        // hardware order, so all XCDs work on the same table at once and its
-        // hot rows share the last-level cache.
-        xcd_remap = (mode & EB_HINT_STREAM_ROWS) != 0;
-    } else {
-        fn = weights ? pick_weighted_kernel(i32, dtype, false, 0, 0, false, false, false)
-                     : pick_kernel<false>(i32, dtype, false, 0, 0, false, false, false);
-    }
-    if (!fn) return fail(EB_ERR_UNSUPPORTED, "%s: no kernel for this row shape", who);
+    const GatherPlan plan = plan_gather(D, dtype, h->aligned16 && out_aligned, index_type == EB_IDX_I32,
+                                        weights != nullptr, T, B, nnz, mode);
+    if (!plan.fn) return fail(EB_ERR_UNSUPPORTED, "%s: no kernel for this row shape", who);
 
-    // Launch in pieces of at most 64 tables and a bounded grid.
-    const int64_t kMaxBlocks = (int64_t)1 << 22;
-    const size_t ies = i32 ? 4 : 8;
     GatherArgs a;
     std::memset(&a, 0, sizeof a);
     a.indices = indices;
@@ -276,13 +197,13 @@ int forward_impl(const char *who, const eb_tables *h, int32_t T, const int64_t *
     a.ldo = ldo;
     a.ldh = ldh;
     a.D = D;
-    a.row_bytes = team_path ? (int32_t)rb : 0;
-    a.chunks = team_path ? (int32_t)(rb / 16) : 0;
+    a.row_bytes = plan.team ? D * elem_bytes(dtype) : 0;
+    a.chunks = plan.team ? D * elem_bytes(dtype) / 16 : 0;
     a.mean = pool == EB_MEAN;
-    a.xcd_runs = xcd_remap ? 1 : 0;
-    hipStream_t st = (hipStream_t)stream;
+    a.xcd_runs = plan.xcd_runs ? 1 : 0;
 
-    const int64_t blocks_all_bags = (B + bags_per_block - 1) / bags_per_block;
+    // Launch in pieces of at most 64 tables.
+    const size_t ies = index_type == EB_IDX_I32 ? 4 : 8;
     for (int32_t t0 = 0; t0 < T; t0 += kMaxTablesPerLaunch) {
         const int32_t nt = std::min<int32_t>(kMaxTablesPerLaunch, T - t0);
         for (int32_t j = 0; j < nt; ++j) {
@@ -292,18 +213,8 @@ int forward_impl(const char *who, const eb_tables *h, int32_t T, const int64_t *
         }
         a.offsets = (const char *)offsets + (size_t)t0 * B * ies;
         a.hits = hits ? hits + t0 : nullptr;
-        // Bag ranges per launch keep nt * blocks_per_table within the grid bound.
-        const int64_t bpt_max = std::max<int64_t>(1, kMaxBlocks / nt);
-        for (int64_t blk0 = 0; blk0 < blocks_all_bags; blk0 += bpt_max) {
-            const int64_t bpt = std::min(bpt_max, blocks_all_bags - blk0);
-            a.bag_begin = blk0 * bags_per_block;
-            a.blocks_per_table = (int32_t)bpt;
-            a.nblocks = (int32_t)(bpt * nt);
-            const int64_t grid = xcd_remap ? (a.nblocks + kXcds - 1) / kXcds * kXcds : a.nblocks;
-            void *args[] = {&a};
-            hipError_t err = hipLaunchKernel((const void *)fn, dim3((unsigned)grid), dim3(kBlock), args, 0, st);
-            if (err != hipSuccess) return fail(EB_ERR_HIP, "%s: kernel launch failed: %s", who, hipGetErrorString(err));
-        }
+        const hipError_t err = launch_gather(plan, a, nt, (hipStream_t)stream);
+        if (err != hipSuccess) return fail(EB_ERR_HIP, "%s: kernel launch failed: %s", who, hipGetErrorString(err));
     }
     return EB_OK;
 }

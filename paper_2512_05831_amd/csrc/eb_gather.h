@@ -601,4 +601,118 @@ KernelFn pick_weighted_kernel(bool i32, int dtype, bool team, int R, int C, bool
 
 inline int elem_bytes(int dtype) { return dtype == EB_F32 ? 4 : 2; }
 
+// ---------------------------------------------------------------------------- launch shape (host)
+
+// Team shape for a row of rb bytes (rb % 16 == 0, rb <= 8192).
+struct Shape {
+    int R, P, C;
+};
+
+// Small batches.  A launch whose normal mapping has fewer waves than the GPU
+// holds (256 CUs x 32) leaves it partly idle, and each bag's chain of
+// dependent loads sets the time.  One wave per bag with 8 rows in flight per
+// lane then wins when bags are long (more than twice the rows the normal
+// mapping keeps in flight per bag) and few enough (measured over the paper's
+// single-GPU shapes: up to 1.5x faster, never slower).
+constexpr int64_t kWaveSlots = 256 * 32;
+constexpr int64_t kFewBagsMax = 2048;
+
+inline int rows_in_flight_per_bag(const Shape &s, bool stream)
+{
+    const int u_cached = s.C >= 6 ? 1 : 6 / s.C;
+    const int u = (stream && s.R * s.C >= 8) ? (s.C >= 2 ? 1 : 2) : u_cached;
+    return s.P * u;
+}
+
+// single: one lane group per bag for large batches; 256-B and 1-KB rows
+// then go to 16-lane teams (1 or 4 chunks per lane), and 512-B rows too when
+// narrow512 is set (else 32-lane teams).
+inline Shape team_shape(int rb, bool few, bool single, bool narrow512 = false)
+{
+    Shape s;
+    const int chunks = rb / 16;
+    s.R = 1;
+    while (s.R < chunks && s.R < kWave) s.R *= 2;
+    s.C = (chunks + s.R - 1) / s.R;
+    if (single && (rb == 256 || rb == 1024 || (rb == 512 && narrow512))) {
+        s.R = 16;
+        s.C = rb / 256;
+    }
+    s.P = groups_per_bag(s.R, few, single);
+    return s;
+}
+
+// The kernel of a call and how its bags map to workgroups.
+struct GatherPlan {
+    KernelFn fn;
+    bool team;           // team kernel (else plain)
+    int bags_per_block;
+    bool xcd_runs;       // each XCD takes a contiguous run of workgroups
+};
+
+// aligned: tables and every output row start are 16-byte aligned.
+inline GatherPlan plan_gather(int32_t D, int32_t dtype, bool aligned, bool i32, bool weighted, int64_t T,
+                              int64_t B, int64_t nnz, int32_t mode)
+{
+    GatherPlan plan{nullptr, false, kWavesPerBlock, false};
+    const int64_t rb = (int64_t)D * elem_bytes(dtype);
+    plan.team = rb % 16 == 0 && rb <= 8192 && aligned;
+    if (!plan.team) {
+        plan.fn = weighted ? pick_weighted_kernel(i32, dtype, false, 0, 0, false, false, false)
+                           : pick_kernel<false>(i32, dtype, false, 0, 0, false, false, false);
+        return plan;
+    }
+    // Non-temporal loads lose for rows narrower than 128 bytes.
+    const bool hint = (mode & EB_HINT_STREAM_ROWS) != 0;
+    const bool stream = hint && rb >= 128;
+    const Shape normal = team_shape((int)rb, false, false);
+    const int64_t bags = T * B;
+    const int64_t waves = bags / (kWave / (normal.R * normal.P));
+    const bool few = waves < kWaveSlots && bags <= kFewBagsMax &&
+                     nnz > 2 * (int64_t)rows_in_flight_per_bag(normal, stream) * bags;
+    // Teams narrower than a wave, one lane group per bag, when they still
+    // give half the GPU's wave slots or more: for streamed rows, and for
+    // cached rows when the mean bag is shorter than the rows the normal
+    // mapping keeps in flight per bag (most of a wave would idle: the bags a
+    // row block receives in a row-wise exchange).  512-B rows take 32-lane
+    // teams when streamed (16-lane teams were 2-5% slower on the paper's
+    // multi-table shapes) and 16-lane teams for short cached bags.
+    const bool short_bags = nnz < (int64_t)rows_in_flight_per_bag(normal, false) * bags;
+    const Shape narrow = team_shape((int)rb, false, true, !stream && short_bags);
+    const int narrow_team = narrow.R * narrow.P;
+    const bool single = (stream || short_bags) && !few && narrow_team < normal.R * normal.P &&
+                        bags / (kWave / narrow_team) >= kWaveSlots / 2;
+    const Shape sh = few ? team_shape((int)rb, true, false) : single ? narrow : normal;
+    plan.fn = weighted ? pick_weighted_kernel(i32, dtype, true, sh.R, sh.C, stream, few, single)
+                       : pick_kernel<false>(i32, dtype, true, sh.R, sh.C, stream, few, single);
+    plan.bags_per_block = (kWave / (sh.R * sh.P)) * kWavesPerBlock;
+    // No reuse: each XCD takes a contiguous run of bags (measured faster for
+    // uniform ids, also for rows under 128 B).  Otherwise hardware order, so
+    // all XCDs work on the same table at once and its hot rows share the
+    // last-level cache.
+    plan.xcd_runs = hint;
+    return plan;
+}
+
+// Launch one piece of at most 64 tables (a.base / nlocal / col / offsets /
+// hits already set for it), in as many launches as the grid bound needs:
+// each launch covers a range of every table's bags.
+inline hipError_t launch_gather(const GatherPlan &plan, GatherArgs &a, int32_t nt, hipStream_t stream)
+{
+    const int64_t kMaxBlocks = (int64_t)1 << 22;
+    const int64_t blocks_all_bags = (a.B + plan.bags_per_block - 1) / plan.bags_per_block;
+    const int64_t bpt_max = kMaxBlocks / nt > 1 ? kMaxBlocks / nt : 1;
+    for (int64_t blk0 = 0; blk0 < blocks_all_bags; blk0 += bpt_max) {
+        const int64_t bpt = bpt_max < blocks_all_bags - blk0 ? bpt_max : blocks_all_bags - blk0;
+        a.bag_begin = blk0 * plan.bags_per_block;
+        a.blocks_per_table = (int32_t)bpt;
+        a.nblocks = (int32_t)(bpt * nt);
+        const int64_t grid = plan.xcd_runs ? (a.nblocks + kXcds - 1) / kXcds * kXcds : a.nblocks;
+        void *args[] = {&a};
+        const hipError_t err = hipLaunchKernel((const void *)plan.fn, dim3((unsigned)grid), dim3(kBlock), args, 0, stream);
+        if (err != hipSuccess) return err;
+    }
+    return hipSuccess;
+}
+
 } // namespace eb_gather
