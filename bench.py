@@ -99,7 +99,7 @@ def measured_traffic(workload_name: str):
 def pick_workload(args):
     wid = 2 if args.workload is None else args.workload
     if wid == 4:
-        w = wl.config(4, D=args.dim, dtype={"f16": wl.F16, "bf16": wl.BF16}[args.dtype])
+        w = wl.config(4, D=args.dim, dtype={"f16": wl.F16, "bf16": wl.BF16, "f32": wl.F32}[args.dtype])
     elif wid == 5:
         w = wl.config(5, permuted=args.permuted)
     else:
@@ -672,7 +672,9 @@ def main():
     ap.add_argument("--headline-only", action="store_true",
                     help="skip timing the other workloads after the headline")
     ap.add_argument("--dim", type=int, default=128)
-    ap.add_argument("--dtype", default="f16", choices=["f16", "bf16"])
+    ap.add_argument("--dtype", default="f16", choices=["f16", "bf16", "f32"],
+                    help="workload 4's storage type (f32 and D not a multiple of 8 reach other "
+                         "row shapes, e.g. the plain kernel)")
     ap.add_argument("--batches", type=int, default=8, help="distinct index batches cycled")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true",
