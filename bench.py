@@ -569,97 +569,69 @@ def timing_tables(torch, dev, w, seed):
     return tabs
 
 
-def index_batches(w, n, cache):
-    """The headline's batch scheme: the workload's ids, then n - 1 batches
-    drawn with other seeds; shared by workloads that differ only in D/dtype."""
-    key = (w.seed, w.T, w.B, w.rows, w.lengths_kind, w.L, w.dist, w.alpha, w.permuted)
-    if key not in cache:
-        cache.clear()
-        off = w.offsets()
-        cache[key] = (off, [w.with_(seed=w.seed + 7919 * j).indices(off) if j else w.indices(off)
-                            for j in range(n)])
-    return cache[key]
+def workload_args(cid, kw):
+    """Command-line arguments that select workload cid with wl.config(cid, **kw)."""
+    args = ["--workload", str(cid)]
+    if "D" in kw:
+        args += ["--dim", str(kw["D"]), "--dtype", {wl.F16: "f16", wl.BF16: "bf16", wl.F32: "f32"}[kw["dtype"]]]
+    if kw.get("permuted"):
+        args.append("--permuted")
+    return args
 
 
-def time_workload(torch, dev, eb, cid, w, modes, K, W, nbatches, cache, stream):
-    """Entries (one per pooling mode) for one workload: mean launch time over
-    K back-to-back launches (HIP events on the launch stream; "launches" in
-    the entry) and the rates
-    and roofline fraction that follow; for skewed ids also single launches
-    warm and after a 512 MB flush (the caches' share)."""
-    off, batches = index_batches(w, nbatches, cache)
-    tables = timing_tables(torch, dev, w, w.seed + 31)
-    et = eb.EmbeddingBagTables(tables, rows=[w.rows] * w.T, shard_lo=w.shard_lo, shard_hi=w.shard_hi)
-    d_off = torch.from_numpy(off).to(dev)
-    d_idx = [torch.from_numpy(b).to(dev) for b in batches]
-    out = torch.empty((w.B, w.T * w.D), dtype=torch.float32, device=dev)
-    hits = torch.empty((w.B, w.T), dtype=torch.int32, device=dev) if w.want_hits else None
-    local = [int(np.count_nonzero((b >= w.shard_lo) & (b < w.local_hi))) for b in batches]
-    nnz = [int(b.size) for b in batches]
-    uniform = w.dist == "uniform"
-    entries = []
-    for mode in modes:
-        call_mode = mode | (eb.EB_HINT_STREAM_ROWS if uniform else 0)
-        calls = [et.prepare(i, d_off, w.B, call_mode, out, hits, stream) for i in d_idx]
-        turn = [0]
-
-        def step():
-            calls[turn[0] % len(calls)]()
-            turn[0] += 1
-        us = _time_launches(torch, stream, step, K, W)
-        n_avg = sum(nnz) / len(nnz)
-        by = sum(algorithmic_bytes(w, local[j], nnz[j], hits is not None) for j in range(len(nnz))) / len(nnz)
-        name = w.name + ("-mean" if mode == wl.MEAN else "")
-        e = {"config": cid, "workload": name, "mode": "sum" if mode == wl.SUM else "mean",
-             "storage": wl.DTYPE_NAMES[w.dtype], "rows_cache_policy": "stream" if uniform else "cached",
-             "kernel_us": round(us, 2), "launches": K, "lookups_per_s": n_avg / us * 1e6,
-             "bags_per_s": w.T * w.B / us * 1e6,
-             "algorithmic_bytes_per_launch": int(by), "algorithmic_GBps": round(by / us / 1e3, 1),
-             "frac_of_8TBps": round(by / us / 1e3 / HBM_PEAK_GBPS, 4)}
-        if w.sharded:
-            e["local_fraction"] = round(sum(local) / sum(nnz), 4)
-        if not uniform:
-            e["note"] = ("skewed ids: algorithmic bytes count every lookup's row, part of which "
-                         "L2 and the last-level cache serve, so the fraction is not an HBM fraction")
-            warm = per_launch_us(torch, stream, calls, 20)
-            flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
-            cold = per_launch_us(torch, stream, calls, 20, flush=lambda i: flush.fill_(i & 0xFF))
-            del flush
-            e["single_launch_us"] = {"warm_median": round(warm["median_us"], 1),
-                                     "cold_median_512MB_flushed": round(cold["median_us"], 1)}
-        tr = measured_traffic(name)
-        e["traffic_GBps"] = None if tr is None else round(tr / us / 1e3, 1)
-        entries.append(e)
-        log(f"bench: {name}: {us:.1f} us, {by / us / 1e3:.0f} GB/s algorithmic "
-            f"({by / us / 1e3 / HBM_PEAK_GBPS * 100:.1f}% of 8 TB/s)")
-    et.close()
-    del tables, d_idx, d_off, out, hits
-    torch.cuda.empty_cache()
-    return entries
-
-
-def all_workloads(torch, dev, eb, headline, K, W, nbatches):
+def all_workloads(headline, K, W, nbatches):
     """One entry per workload and pooling mode: the headline's numbers for
-    workload 2, then every other workload timed the same way.  A workload
-    that fails records its error in its own entry."""
-    stream = torch.cuda.Stream(dev)
+    workload 2, then every other workload timed by this script in a process
+    of its own (a child run with --workload ...), so that each is measured as
+    a standalone run is: large tables allocated after other workloads' were
+    freed gather 2-4% slower.  At least 200 timed launches each (20 still
+    carry a few percent of ramp-up: workload 4 at D 64 96.6 us over 20, 93.4
+    over 400).  A workload that fails records its error in its own entry."""
+    import subprocess
+
     entries = [dict(headline, config=2, source="headline run")]
-    cache = {}
-    # at least 200 timed launches each: with 20 the mean still carries a few
-    # percent of ramp-up (workload 4 at D 64: 96.6 us over 20, 93.4 over 400)
     K, W = max(K, 200), max(W, 20)
     for cid, kw, modes in other_workloads():
         w = wl.config(cid, **kw)
-        try:
-            entries.extend(time_workload(torch, dev, eb, cid, w, modes, K, W, nbatches, cache, stream))
-        except Exception as exc:  # noqa: BLE001 -- recorded, the line is still printed
-            entries.append({"config": cid, "workload": w.name, "error": f"{type(exc).__name__}: {exc}"})
-            log(f"bench: {w.name} failed: {exc}")
-            torch.cuda.empty_cache()
+        for mode in modes:
+            name = w.name + ("-mean" if mode == wl.MEAN else "")
+            cmd = [sys.executable, os.path.abspath(__file__), *workload_args(cid, kw),
+                   "--mode", "sum" if mode == wl.SUM else "mean", "--steps", str(K), "--warmup", str(W),
+                   "--batches", str(nbatches), "--no-cpu-baseline", "--no-ceiling", "--no-torch-baseline",
+                   "--headline-only"]
+            if w.dist != "uniform":
+                cmd.append("--cold")
+            try:
+                res = subprocess.run(cmd, stdout=subprocess.PIPE, text=True, timeout=600)
+                if res.returncode != 0:
+                    raise RuntimeError(f"child run exited with {res.returncode}")
+                r = json.loads(res.stdout.strip().splitlines()[-1])
+                us = r["kernel_us_mean"]
+                by = r["roofline"]["algorithmic_bytes_per_launch"]
+                tr = r["roofline"]["traffic"]
+                e = {"config": cid, "workload": name, "mode": r["config"]["mode"], "storage": r["dtype"],
+                     "rows_cache_policy": r["config"]["rows_cache_policy"], "kernel_us": round(us, 2),
+                     "launches": K, "lookups_per_s": r["lookups_per_launch"] / us * 1e6,
+                     "bags_per_s": w.T * w.B / us * 1e6, "algorithmic_bytes_per_launch": int(by),
+                     "algorithmic_GBps": round(by / us / 1e3, 1), "frac_of_8TBps": round(by / us / 1e3 / HBM_PEAK_GBPS, 4),
+                     "traffic_GBps": None if tr is None else round(tr / us / 1e3, 1), "process": "own"}
+                if "local_fraction" in r:
+                    e["local_fraction"] = r["local_fraction"]
+                if w.dist != "uniform":
+                    e["note"] = ("skewed ids: algorithmic bytes count every lookup's row, part of which "
+                                 "L2 and the last-level cache serve, so the fraction is not an HBM fraction")
+                    e["single_launch_us"] = {"warm_median": round(r["single_launch_warm"]["median_us"], 1),
+                                             "cold_median_512MB_flushed": round(r["single_launch_cold"]["median_us"], 1)}
+                entries.append(e)
+                log(f"bench: {name}: {us:.1f} us, {by / us / 1e3:.0f} GB/s algorithmic "
+                    f"({by / us / 1e3 / HBM_PEAK_GBPS * 100:.1f}% of 8 TB/s)")
+            except Exception as exc:  # noqa: BLE001 -- recorded, the line is still printed
+                entries.append({"config": cid, "workload": name, "error": f"{type(exc).__name__}: {exc}"})
+                log(f"bench: {name} failed: {exc}")
     return entries
 
 
-def main():
+def parser() -> argparse.ArgumentParser:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=400)
@@ -671,6 +643,8 @@ def main():
                     help="workload 5 with its Zipf ranks permuted over the id space")
     ap.add_argument("--headline-only", action="store_true",
                     help="skip timing the other workloads after the headline")
+    ap.add_argument("--mode", choices=["sum", "mean"], default=None,
+                    help="pooling of the timed workload (default: its first mode)")
     ap.add_argument("--dim", type=int, default=128)
     ap.add_argument("--dtype", default="f16", choices=["f16", "bf16", "f32"],
                     help="workload 4's storage type (f32 and D not a multiple of 8 reach other "
@@ -702,7 +676,11 @@ def main():
                     help="time the paper's single-GPU gather shapes instead (one JSON line each)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run a plain streaming copy of BYTES (for scaling HBM counters)")
-    args = ap.parse_args()
+    return ap
+
+
+def main():
+    args = parser().parse_args()
 
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
@@ -728,7 +706,7 @@ def main():
                           args.rows_policy)
         return
     w = pick_workload(args)
-    mode = w.modes[0]
+    mode = {"sum": wl.SUM, "mean": wl.MEAN}[args.mode] if args.mode else w.modes[0]
     stream_rows = (args.rows_policy == "stream" or
                    (args.rows_policy == "auto" and w.dist == "uniform"))
     call_mode = mode | (eb.EB_HINT_STREAM_ROWS if stream_rows else 0)
@@ -812,7 +790,8 @@ def main():
     value = steps_lookups / (wall_ms / 1e3)
     achieved = steps_bytes / (region_ms / 1e3) / 1e9
     bytes_per_launch = steps_bytes / K
-    traffic = measured_traffic(w.name + ("-i32" if i32 else "") + ("-weighted" if args.weights else ""))
+    traffic = measured_traffic(w.name + ("-mean" if mode == wl.MEAN else "") + ("-i32" if i32 else "") +
+                               ("-weighted" if args.weights else ""))
     log(f"bench: mean launch {launch_ms * 1e3:.1f} us over {K} back-to-back launches, "
         f"wall step {ms_per_step * 1e3:.1f} us, {achieved:.0f} GB/s algorithmic")
 
@@ -894,6 +873,7 @@ def main():
                    "index_batches_cycled": len(batches),
                    "launch": "hip graph replay" if args.graph else "eb_forward per step"},
         "bags_per_s": w.T * w.B / (ms_per_step / 1e3),
+        "lookups_per_launch": steps_lookups / K,
         "kernel_us_mean": launch_ms * 1e3,
         "effective_GBps": achieved,
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
@@ -902,6 +882,8 @@ def main():
                      "traffic": traffic},
         "cpu_baseline": cpu,
     }
+    if w.sharded:
+        line["local_fraction"] = round(sum(local) / sum(nnz), 4)
     line.update(extra)
     et.close()
     if args.workload is None and not args.headline_only:
@@ -915,7 +897,7 @@ def main():
                 "algorithmic_bytes_per_launch": int(bytes_per_launch),
                 "algorithmic_GBps": round(achieved, 1), "frac_of_8TBps": round(achieved / HBM_PEAK_GBPS, 4),
                 "traffic_GBps": None if traffic is None else round(traffic / launch_ms / 1e6, 1)}
-        line["workloads"] = all_workloads(torch, dev, eb, head, K, W, args.batches)
+        line["workloads"] = all_workloads(head, K, W, args.batches)
     print(json.dumps(line), flush=True)
 
 

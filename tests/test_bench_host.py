@@ -72,3 +72,16 @@ def test_more_than_one_gpu_is_refused():
     assert res.returncode == 2
     assert "one GPU" in res.stderr
     assert res.stdout == ""
+
+
+def test_child_runs_select_every_other_workload():
+    """The default run times each workload in a child run of this script;
+    the arguments it passes must select exactly that workload."""
+    seen = set()
+    for cid, kw, modes in bench.other_workloads():
+        args = bench.parser().parse_args(bench.workload_args(cid, kw) + ["--mode", "mean"])
+        assert bench.pick_workload(args).name == wl.config(cid, **kw).name
+        seen.update(wl.config(cid, **kw).name + ("-mean" if m == wl.MEAN else "") for m in modes)
+    # workloads 1, 3 (sum, mean), 4 (6 D x 2 dtypes), 5 (literal, permuted); 2 is the headline
+    assert len(seen) == 1 + 2 + 12 + 2
+    assert wl.config(5, permuted=True).name in seen and wl.config(3).name + "-mean" in seen
