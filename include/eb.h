@@ -198,9 +198,13 @@ int eb_forward(const eb_tables *tables, int32_t T, const int64_t *rows, int32_t 
  *   stream           as eb_forward.
  *
  * eb_forward(...) is eb_forward_ex with EB_IDX_I64, weights = NULL,
- * ldo = T*D, out_cols = NULL and ldh = T.  Rows take the 16-byte vector path
- * only when out, ldo and every out_cols[t] keep each output row 16-byte
- * aligned; other layouts are correct but slower.
+ * ldo = T*D, out_cols = NULL and ldh = T.  Rows are read in 16-, 8- or
+ * 4-byte pieces per lane: the widest that divides the row, that every table
+ * pointer is aligned to, and whose results (4 floats per 16 bytes of fp32,
+ * 8 of fp16 / bf16; at most 16 bytes) the output rows' alignment (out, ldo
+ * and every out_cols[t]) allows to store as one access.  Rows that allow none
+ * of them, and rows of more than 64 pieces of 8 or 4 bytes, take a plain
+ * element-by-element path: correct, but slower.
  *
  * Errors: those of eb_forward, and EB_ERR_INVALID for an unknown index_type,
  * weights with EB_MEAN, ldo < 1, a table's columns outside [0, ldo),

@@ -2,6 +2,7 @@
 
 ``python -m paper_2512_05831_amd.build`` (or ``build_library()``) runs hipcc on
 ``csrc/eb.hip`` (with ``csrc/eb_gather.h``), ``csrc/eb_gather_weighted.hip``,
+``csrc/eb_gather_narrow.hip``, ``csrc/eb_gather_narrow_weighted.hip``,
 ``csrc/eb_exchange.hip`` and ``csrc/eb_ceiling.hip`` (the bandwidth probe the
 benchmark uses) and writes ``libeb.so`` next to this file.
 """
@@ -14,7 +15,8 @@ import sys
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 SRCS = [os.path.join(HERE, "csrc", f)
-        for f in ("eb.hip", "eb_gather_weighted.hip", "eb_exchange.hip", "eb_ceiling.hip")]
+        for f in ("eb.hip", "eb_gather_weighted.hip", "eb_gather_narrow.hip",
+                  "eb_gather_narrow_weighted.hip", "eb_exchange.hip", "eb_ceiling.hip")]
 LIB = os.path.join(HERE, "libeb.so")
 ARCH = "gfx950"
 

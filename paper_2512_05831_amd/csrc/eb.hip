@@ -92,12 +92,20 @@ struct eb_tables {
     int32_t T;
     int32_t D;
     int32_t dtype;
-    bool aligned16;
+    int align;           // largest power of two up to 16 dividing every table pointer
     std::vector<const char *> ptrs;
     std::vector<int64_t> stored_rows;
 };
 
 namespace {
+
+// The largest power of two up to 16 that divides x (16 for x == 0).
+inline int pow2_align(uintptr_t x)
+{
+    int a = 1;
+    while (a < 16 && x % (uintptr_t)(2 * a) == 0) a *= 2;
+    return a;
+}
 
 // Output column of table t's first element.
 inline int64_t out_col(const int64_t *out_cols, int32_t t, int32_t D)
@@ -179,11 +187,12 @@ int forward_impl(const char *who, const eb_tables *h, int32_t T, const int64_t *
             return fail(EB_ERR_UNSUPPORTED, "%s: more than 4294967294 gatherable rows in a table", who);
     }
 
-    // 16-byte stores need every (bag, table) output row start 16-byte aligned.
-    bool out_aligned = ((uintptr_t)out) % 16 == 0 && ldo % 4 == 0;
-    for (int32_t t = 0; t < T; ++t) out_aligned = out_aligned && out_col(out_cols, t, D) % 4 == 0;
-    const GatherPlan plan = plan_gather(D, dtype, h->aligned16 && out_aligned, index_type == EB_IDX_I32,
-                                        weights != nullptr, T, B, nnz, mode);
+    // Vector stores need every (bag, table) output row start aligned to them.
+    int out_align = std::min(pow2_align((uintptr_t)out), pow2_align((uintptr_t)ldo * 4));
+    for (int32_t t = 0; t < T; ++t)
+        out_align = std::min(out_align, pow2_align((uintptr_t)out_col(out_cols, t, D) * 4));
+    const GatherPlan plan = plan_gather(D, dtype, h->align, out_align, index_type == EB_IDX_I32, weights != nullptr,
+                                        T, B, nnz, mode);
     if (!plan.fn) return fail(EB_ERR_UNSUPPORTED, "%s: no kernel for this row shape", who);
 
     GatherArgs a;
@@ -198,7 +207,7 @@ int forward_impl(const char *who, const eb_tables *h, int32_t T, const int64_t *
     a.ldh = ldh;
     a.D = D;
     a.row_bytes = plan.team ? D * elem_bytes(dtype) : 0;
-    a.chunks = plan.team ? D * elem_bytes(dtype) / 16 : 0;
+    a.chunks = plan.team ? D * elem_bytes(dtype) / plan.chunk_bytes : 0;
     a.mean = pool == EB_MEAN;
     a.xcd_runs = plan.xcd_runs ? 1 : 0;
 
@@ -251,9 +260,11 @@ int eb_create_tables(int32_t T, const void *const *table_ptrs, const int64_t *st
             delete h;
             return fail(EB_ERR_NOMEM, "eb_create_tables: out of host memory");
         }
-        h->aligned16 = true;
-        for (int32_t t = 0; t < T; ++t)
-            if (((uintptr_t)h->ptrs[t]) % 16 != 0) h->aligned16 = false;
+        h->align = 16;
+        for (int32_t t = 0; t < T; ++t) {
+            if (stored_rows[t] == 0) continue; // never read
+            h->align = std::min(h->align, pow2_align((uintptr_t)h->ptrs[t]));
+        }
         *out_handle = h;
         return EB_OK;
     } catch (...) {

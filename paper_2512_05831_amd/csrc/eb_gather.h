@@ -109,6 +109,18 @@ template <> struct Elem<EB_F32> {
         acc[2] = fmaf(w, __uint_as_float(v.z), acc[2]);
         acc[3] = fmaf(w, __uint_as_float(v.w), acc[3]);
     }
+    __device__ static __forceinline__ void add(float *acc, uint2 v)
+    {
+        acc[0] += __uint_as_float(v.x);
+        acc[1] += __uint_as_float(v.y);
+    }
+    __device__ static __forceinline__ void fma(float *acc, uint2 v, float w)
+    {
+        acc[0] = fmaf(w, __uint_as_float(v.x), acc[0]);
+        acc[1] = fmaf(w, __uint_as_float(v.y), acc[1]);
+    }
+    __device__ static __forceinline__ void add(float *acc, uint32_t v) { acc[0] += __uint_as_float(v); }
+    __device__ static __forceinline__ void fma(float *acc, uint32_t v, float w) { acc[0] = fmaf(w, __uint_as_float(v), acc[0]); }
     __device__ static __forceinline__ float load1(const char *p) { return *(const float *)p; }
 };
 template <> struct Elem<EB_F16> {
@@ -128,6 +140,21 @@ template <> struct Elem<EB_F16> {
         acc[2] = fmaf(w, lo(v.y), acc[2]); acc[3] = fmaf(w, hi(v.y), acc[3]);
         acc[4] = fmaf(w, lo(v.z), acc[4]); acc[5] = fmaf(w, hi(v.z), acc[5]);
         acc[6] = fmaf(w, lo(v.w), acc[6]); acc[7] = fmaf(w, hi(v.w), acc[7]);
+    }
+    __device__ static __forceinline__ void add(float *acc, uint2 v)
+    {
+        acc[0] += lo(v.x); acc[1] += hi(v.x);
+        acc[2] += lo(v.y); acc[3] += hi(v.y);
+    }
+    __device__ static __forceinline__ void fma(float *acc, uint2 v, float w)
+    {
+        acc[0] = fmaf(w, lo(v.x), acc[0]); acc[1] = fmaf(w, hi(v.x), acc[1]);
+        acc[2] = fmaf(w, lo(v.y), acc[2]); acc[3] = fmaf(w, hi(v.y), acc[3]);
+    }
+    __device__ static __forceinline__ void add(float *acc, uint32_t v) { acc[0] += lo(v); acc[1] += hi(v); }
+    __device__ static __forceinline__ void fma(float *acc, uint32_t v, float w)
+    {
+        acc[0] = fmaf(w, lo(v), acc[0]); acc[1] = fmaf(w, hi(v), acc[1]);
     }
     __device__ static __forceinline__ float load1(const char *p) { return (float)*(const _Float16 *)p; }
 };
@@ -149,6 +176,21 @@ template <> struct Elem<EB_BF16> {
         acc[4] = fmaf(w, lo(v.z), acc[4]); acc[5] = fmaf(w, hi(v.z), acc[5]);
         acc[6] = fmaf(w, lo(v.w), acc[6]); acc[7] = fmaf(w, hi(v.w), acc[7]);
     }
+    __device__ static __forceinline__ void add(float *acc, uint2 v)
+    {
+        acc[0] += lo(v.x); acc[1] += hi(v.x);
+        acc[2] += lo(v.y); acc[3] += hi(v.y);
+    }
+    __device__ static __forceinline__ void fma(float *acc, uint2 v, float w)
+    {
+        acc[0] = fmaf(w, lo(v.x), acc[0]); acc[1] = fmaf(w, hi(v.x), acc[1]);
+        acc[2] = fmaf(w, lo(v.y), acc[2]); acc[3] = fmaf(w, hi(v.y), acc[3]);
+    }
+    __device__ static __forceinline__ void add(float *acc, uint32_t v) { acc[0] += lo(v); acc[1] += hi(v); }
+    __device__ static __forceinline__ void fma(float *acc, uint32_t v, float w)
+    {
+        acc[0] = fmaf(w, lo(v), acc[0]); acc[1] = fmaf(w, hi(v), acc[1]);
+    }
     __device__ static __forceinline__ float load1(const char *p) { return __uint_as_float((uint32_t)(*(const uint16_t *)p) << 16); }
 };
 
@@ -165,12 +207,57 @@ __device__ __forceinline__ uint4 load_chunk(const char *p)
     }
 }
 
-// Results, ids and offsets are touched once: non-temporal accesses.
+// The part of a row one lane loads: 16 bytes (global_load_dwordx4) for rows
+// that are a multiple of 16 bytes, else 8 or 4 bytes.  Loads are cached, or
+// non-temporal when the caller hints that ids have no reuse.
+template <int CB> struct Chunk;
+template <> struct Chunk<16> {
+    using T = uint4;
+    __device__ static __forceinline__ T zero() { return make_uint4(0, 0, 0, 0); }
+    template <bool kStream> __device__ static __forceinline__ T load(const char *p) { return load_chunk<kStream>(p); }
+};
+template <> struct Chunk<8> {
+    using T = uint2;
+    __device__ static __forceinline__ T zero() { return make_uint2(0, 0); }
+    template <bool kStream> __device__ static __forceinline__ T load(const char *p)
+    {
+        typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+        if constexpr (kStream) {
+            const u32x2 v = __builtin_nontemporal_load((const u32x2 *)p);
+            return make_uint2(v[0], v[1]);
+        } else {
+            return *(const uint2 *)p;
+        }
+    }
+};
+template <> struct Chunk<4> {
+    using T = uint32_t;
+    __device__ static __forceinline__ T zero() { return 0u; }
+    template <bool kStream> __device__ static __forceinline__ T load(const char *p)
+    {
+        if constexpr (kStream) return __builtin_nontemporal_load((const uint32_t *)p);
+        else return *(const uint32_t *)p;
+    }
+};
+
+// Results, ids and offsets are touched once: non-temporal accesses.  Four
+// fp32 results of a chunk, stored as one access.
 __device__ __forceinline__ void store_nt(float *p, float a, float b, float c, float d)
 {
     const f32x4 v = {a, b, c, d};
     __builtin_nontemporal_store(v, (f32x4 *)p);
 }
+
+// The kE fp32 results of one chunk, stored as one 16-, 8- or 4-byte access
+// per group of up to four.
+// The one or two fp32 results of a narrow chunk, stored as one access.
+__device__ __forceinline__ void store_nt(float *p, float a, float b)
+{
+    typedef float f32x2 __attribute__((ext_vector_type(2)));
+    const f32x2 v = {a, b};
+    __builtin_nontemporal_store(v, (f32x2 *)p);
+}
+__device__ __forceinline__ void store_nt(float *p, float a) { __builtin_nontemporal_store(a, p); }
 
 __device__ __forceinline__ void clamp_bag(int64_t &s, int64_t &e, int64_t nnz)
 {
@@ -181,13 +268,14 @@ __device__ __forceinline__ void clamp_bag(int64_t &s, int64_t &e, int64_t nnz)
 
 // ---------------------------------------------------------------------------- team gather kernel
 
-template <typename IT, int DT, int R, int P, int C, int U, bool kStream, bool kW>
+template <typename IT, int DT, int R, int P, int C, int U, bool kStream, bool kW, int CB>
 __global__ __launch_bounds__(kBlock) void eb_gather_team(const GatherArgs a)
 {
     constexpr int kTeam = R * P;
     constexpr int kTeamsPerWave = kWave / kTeam;
     constexpr int kStage = kStagePerWave / kTeamsPerWave; // window entries per team
-    constexpr int kEpc = Elem<DT>::kPerChunk;
+    constexpr int kEpc = CB / (DT == EB_F32 ? 4 : 2);    // elements per chunk
+    using V = typename Chunk<CB>::T;
     static_assert(kTeam <= kWave && kWave % kTeam == 0, "team shape");
     static_assert(kStage % kTeam == 0, "window shape");
 
@@ -223,7 +311,7 @@ __global__ __launch_bounds__(kBlock) void eb_gather_team(const GatherArgs a)
     // chunk, which the wave's other lanes fetch anyway, and never store.
     int coff[C];
 #pragma unroll
-    for (int c = 0; c < C; ++c) coff[c] = 16 * min(c * R + rl, a.chunks - 1);
+    for (int c = 0; c < C; ++c) coff[c] = CB * min(c * R + rl, a.chunks - 1);
     const char *base = a.base[t];
     const size_t row_bytes = (size_t)a.row_bytes;
     const uint64_t nlocal = a.nlocal[t];
@@ -291,15 +379,15 @@ __global__ __launch_bounds__(kBlock) void eb_gather_team(const GatherArgs a)
                 rr[u] = my_stage[k + u * P];
                 if constexpr (kW) ww[u] = my_wstage[k + u * P];
             }
-            uint4 v[U][C];
+            V v[U][C];
 #pragma unroll
             for (int u = 0; u < U; ++u) {
 #pragma unroll
-                for (int c = 0; c < C; ++c) v[u][c] = make_uint4(0, 0, 0, 0);
+                for (int c = 0; c < C; ++c) v[u][c] = Chunk<CB>::zero();
                 if (rr[u] != kInvalidRow) {
                     const char *p = base + (size_t)rr[u] * row_bytes;
 #pragma unroll
-                    for (int c = 0; c < C; ++c) v[u][c] = load_chunk<kStream>(p + coff[c]);
+                    for (int c = 0; c < C; ++c) v[u][c] = Chunk<CB>::template load<kStream>(p + coff[c]);
                 }
             }
 #pragma unroll
@@ -320,9 +408,9 @@ __global__ __launch_bounds__(kBlock) void eb_gather_team(const GatherArgs a)
         if constexpr (U == 1) {
             for (; k < nv; k += P) {
                 const char *p = base + (size_t)my_stage[k] * row_bytes;
-                uint4 v[C];
+                V v[C];
 #pragma unroll
-                for (int c = 0; c < C; ++c) v[c] = load_chunk<kStream>(p + coff[c]);
+                for (int c = 0; c < C; ++c) v[c] = Chunk<CB>::template load<kStream>(p + coff[c]);
                 const float w = kW ? my_wstage[k] : 1.f;
 #pragma unroll
                 for (int c = 0; c < C; ++c) {
@@ -341,15 +429,15 @@ __global__ __launch_bounds__(kBlock) void eb_gather_team(const GatherArgs a)
                     rr[u] = in[u] ? my_stage[k + u * P] : 0u;
                     if constexpr (kW) ww[u] = in[u] ? my_wstage[k + u * P] : 0.f;
                 }
-                uint4 v[U - 1][C];
+                V v[U - 1][C];
 #pragma unroll
                 for (int u = 0; u < U - 1; ++u) {
 #pragma unroll
-                    for (int c = 0; c < C; ++c) v[u][c] = make_uint4(0, 0, 0, 0);
+                    for (int c = 0; c < C; ++c) v[u][c] = Chunk<CB>::zero();
                     if (in[u]) {
                         const char *p = base + (size_t)rr[u] * row_bytes;
 #pragma unroll
-                        for (int c = 0; c < C; ++c) v[u][c] = load_chunk<kStream>(p + coff[c]);
+                        for (int c = 0; c < C; ++c) v[u][c] = Chunk<CB>::template load<kStream>(p + coff[c]);
                     }
                 }
 #pragma unroll
@@ -381,10 +469,16 @@ __global__ __launch_bounds__(kBlock) void eb_gather_team(const GatherArgs a)
         for (int c = 0; c < C; ++c) {
             if (c * R + rl >= a.chunks) break;
             float *dst = o + (size_t)(c * R + rl) * kEpc;
+            if constexpr (kEpc == 1) {
+                store_nt(dst, acc[c]);
+            } else if constexpr (kEpc == 2) {
+                store_nt(dst, acc[2 * c], acc[2 * c + 1]);
+            } else {
 #pragma unroll
-            for (int h = 0; h < kEpc / 4; ++h)
-                store_nt(dst + 4 * h, acc[c * kEpc + 4 * h], acc[c * kEpc + 4 * h + 1],
-                         acc[c * kEpc + 4 * h + 2], acc[c * kEpc + 4 * h + 3]);
+                for (int h = 0; h < kEpc / 4; ++h)
+                    store_nt(dst + 4 * h, acc[c * kEpc + 4 * h], acc[c * kEpc + 4 * h + 1],
+                             acc[c * kEpc + 4 * h + 2], acc[c * kEpc + 4 * h + 3]);
+            }
         }
         if (a.hits && rl == 0) a.hits[b * a.ldh + t] = count;
     }
@@ -509,67 +603,83 @@ using KernelFn = void (*)(GatherArgs);
 // profit from deeper overlap while hits return early.  A small batch (fewer
 // bags than fill the GPU) is bound by each bag's chain of dependent loads
 // instead: every bag then gets a whole wave and 8 rows in flight per lane.
-template <typename IT, int DT, int R, int C, bool kFew, bool kW>
+template <typename IT, int DT, int R, int C, bool kFew, bool kW, int CB>
 KernelFn team_kernel(bool stream, bool single)
 {
     constexpr int P = groups_per_bag(R, kFew, false);
     constexpr int P_SINGLE = groups_per_bag(R, kFew, true);
     constexpr int U_CACHED = kFew ? (C >= 8 ? 1 : 8 / C) : (C >= 6 ? 1 : 6 / C);
-    constexpr int U_STREAM = (!kFew && R * C >= 8) ? (C >= 2 ? 1 : 2) : U_CACHED;
+    constexpr int U_STREAM = (!kFew && R * C * CB >= 128) ? (C >= 2 ? 1 : 2) : U_CACHED;
     if (!stream) {
         if constexpr (P_SINGLE != P) {
-            if (single) return eb_gather_team<IT, DT, R, P_SINGLE, C, U_CACHED, false, kW>;
+            if (single) return eb_gather_team<IT, DT, R, P_SINGLE, C, U_CACHED, false, kW, CB>;
         }
-        return eb_gather_team<IT, DT, R, P, C, U_CACHED, false, kW>;
+        return eb_gather_team<IT, DT, R, P, C, U_CACHED, false, kW, CB>;
     }
     if constexpr (P_SINGLE != P) {
-        if (single) return eb_gather_team<IT, DT, R, P_SINGLE, C, U_STREAM, true, kW>;
+        if (single) return eb_gather_team<IT, DT, R, P_SINGLE, C, U_STREAM, true, kW, CB>;
     }
-    return eb_gather_team<IT, DT, R, P, C, U_STREAM, true, kW>;
+    return eb_gather_team<IT, DT, R, P, C, U_STREAM, true, kW, CB>;
 }
 
-template <typename IT, int DT, int R, int C, bool kW>
+template <typename IT, int DT, int R, int C, bool kW, int CB>
 KernelFn team_kernel(bool stream, bool few, bool single)
 {
-    return few ? team_kernel<IT, DT, R, C, true, kW>(stream, false)
-               : team_kernel<IT, DT, R, C, false, kW>(stream, single);
+    return few ? team_kernel<IT, DT, R, C, true, kW, CB>(stream, false)
+               : team_kernel<IT, DT, R, C, false, kW, CB>(stream, single);
 }
 
-template <typename IT, int DT, bool kW>
+// 16-byte chunks: the row shapes of the library's mappings.  8- and 4-byte
+// chunks: one chunk per lane (C = 1), rows of up to 64 chunks.
+template <typename IT, int DT, bool kW, int CB>
 KernelFn pick_team_kernel(int R, int C, bool stream, bool few, bool single)
 {
-    switch (R) {
-    case 1: return team_kernel<IT, DT, 1, 1, kW>(stream, few, single);
-    case 2: return team_kernel<IT, DT, 2, 1, kW>(stream, few, single);
-    case 4: return team_kernel<IT, DT, 4, 1, kW>(stream, few, single);
-    case 8: return team_kernel<IT, DT, 8, 1, kW>(stream, few, single);
-    case 16: // 256-B rows; 512-B and 1-KB rows in 16-lane teams
-        return C == 4 ? team_kernel<IT, DT, 16, 4, kW>(stream, few, single)
-               : C == 2 ? team_kernel<IT, DT, 16, 2, kW>(stream, few, single)
-                        : team_kernel<IT, DT, 16, 1, kW>(stream, few, single);
-    case 32: return team_kernel<IT, DT, 32, 1, kW>(stream, few, single);
-    default:
-        switch (C) {
-        case 1: return team_kernel<IT, DT, 64, 1, kW>(stream, few, single);
-        case 2: return team_kernel<IT, DT, 64, 2, kW>(stream, few, single);
-        case 3: return team_kernel<IT, DT, 64, 3, kW>(stream, few, single);
-        case 4: return team_kernel<IT, DT, 64, 4, kW>(stream, few, single);
-        case 5: return team_kernel<IT, DT, 64, 5, kW>(stream, few, single);
-        case 6: return team_kernel<IT, DT, 64, 6, kW>(stream, few, single);
-        case 7: return team_kernel<IT, DT, 64, 7, kW>(stream, few, single);
-        case 8: return team_kernel<IT, DT, 64, 8, kW>(stream, few, single);
+    if constexpr (CB != 16) {
+        if (C != 1) return nullptr;
+        switch (R) {
+        case 1: return team_kernel<IT, DT, 1, 1, kW, CB>(stream, few, single);
+        case 2: return team_kernel<IT, DT, 2, 1, kW, CB>(stream, few, single);
+        case 4: return team_kernel<IT, DT, 4, 1, kW, CB>(stream, few, single);
+        case 8: return team_kernel<IT, DT, 8, 1, kW, CB>(stream, few, single);
+        case 16: return team_kernel<IT, DT, 16, 1, kW, CB>(stream, few, single);
+        case 32: return team_kernel<IT, DT, 32, 1, kW, CB>(stream, few, single);
+        case 64: return team_kernel<IT, DT, 64, 1, kW, CB>(stream, few, single);
         }
+        return nullptr;
+    } else {
+        switch (R) {
+        case 1: return team_kernel<IT, DT, 1, 1, kW, 16>(stream, few, single);
+        case 2: return team_kernel<IT, DT, 2, 1, kW, 16>(stream, few, single);
+        case 4: return team_kernel<IT, DT, 4, 1, kW, 16>(stream, few, single);
+        case 8: return team_kernel<IT, DT, 8, 1, kW, 16>(stream, few, single);
+        case 16: // 256-B rows; 512-B and 1-KB rows in 16-lane teams
+            return C == 4 ? team_kernel<IT, DT, 16, 4, kW, 16>(stream, few, single)
+                   : C == 2 ? team_kernel<IT, DT, 16, 2, kW, 16>(stream, few, single)
+                            : team_kernel<IT, DT, 16, 1, kW, 16>(stream, few, single);
+        case 32: return team_kernel<IT, DT, 32, 1, kW, 16>(stream, few, single);
+        default:
+            switch (C) {
+            case 1: return team_kernel<IT, DT, 64, 1, kW, 16>(stream, few, single);
+            case 2: return team_kernel<IT, DT, 64, 2, kW, 16>(stream, few, single);
+            case 3: return team_kernel<IT, DT, 64, 3, kW, 16>(stream, few, single);
+            case 4: return team_kernel<IT, DT, 64, 4, kW, 16>(stream, few, single);
+            case 5: return team_kernel<IT, DT, 64, 5, kW, 16>(stream, few, single);
+            case 6: return team_kernel<IT, DT, 64, 6, kW, 16>(stream, few, single);
+            case 7: return team_kernel<IT, DT, 64, 7, kW, 16>(stream, few, single);
+            case 8: return team_kernel<IT, DT, 64, 8, kW, 16>(stream, few, single);
+            }
+        }
+        return nullptr;
     }
-    return nullptr;
 }
 
-template <typename IT, bool kW>
+template <typename IT, bool kW, int CB>
 KernelFn pick_team_kernel(int dtype, int R, int C, bool stream, bool few, bool single)
 {
     switch (dtype) {
-    case EB_F32: return pick_team_kernel<IT, EB_F32, kW>(R, C, stream, few, single);
-    case EB_F16: return pick_team_kernel<IT, EB_F16, kW>(R, C, stream, few, single);
-    default: return pick_team_kernel<IT, EB_BF16, kW>(R, C, stream, few, single);
+    case EB_F32: return pick_team_kernel<IT, EB_F32, kW, CB>(R, C, stream, few, single);
+    case EB_F16: return pick_team_kernel<IT, EB_F16, kW, CB>(R, C, stream, few, single);
+    default: return pick_team_kernel<IT, EB_BF16, kW, CB>(R, C, stream, few, single);
     }
 }
 
@@ -583,27 +693,34 @@ KernelFn pick_plain_kernel(int dtype)
     }
 }
 
-// The kernel of one launch: team (R lanes per row, C chunks per lane) or
-// plain, by index type, element type and mapping.
+// The kernel of one launch with 16-byte chunks (team: R lanes per row, C
+// chunks per lane) or the plain kernel, by index type, element type and
+// mapping.
 template <bool kW>
 KernelFn pick_kernel(bool i32, int dtype, bool team, int R, int C, bool stream, bool few, bool single)
 {
     if (team)
-        return i32 ? pick_team_kernel<int32_t, kW>(dtype, R, C, stream, few, single)
-                   : pick_team_kernel<int64_t, kW>(dtype, R, C, stream, few, single);
+        return i32 ? pick_team_kernel<int32_t, kW, 16>(dtype, R, C, stream, few, single)
+                   : pick_team_kernel<int64_t, kW, 16>(dtype, R, C, stream, few, single);
     return i32 ? pick_plain_kernel<int32_t, kW>(dtype) : pick_plain_kernel<int64_t, kW>(dtype);
 }
 
 // pick_kernel<true>, instantiated in its own translation unit
-// (eb_gather_weighted.hip) so the two halves build in parallel.
+// (eb_gather_weighted.hip) so the parts build in parallel.
 KernelFn pick_weighted_kernel(bool i32, int dtype, bool team, int R, int C, bool stream, bool few,
                               bool single);
+
+// Team kernels with 8- or 4-byte chunks (cb), weighted or not, instantiated
+// in eb_gather_narrow.hip and eb_gather_narrow_weighted.hip.
+KernelFn pick_narrow_kernel(bool weighted, bool i32, int dtype, int cb, int R, bool stream, bool few,
+                            bool single);
+KernelFn pick_narrow_weighted_kernel(bool i32, int dtype, int cb, int R, bool stream, bool few, bool single);
 
 inline int elem_bytes(int dtype) { return dtype == EB_F32 ? 4 : 2; }
 
 // ---------------------------------------------------------------------------- launch shape (host)
 
-// Team shape for a row of rb bytes (rb % 16 == 0, rb <= 8192).
+// Team shape for a row of rb bytes in chunks of cb bytes (rb % cb == 0).
 struct Shape {
     int R, P, C;
 };
@@ -627,14 +744,14 @@ inline int rows_in_flight_per_bag(const Shape &s, bool stream)
 // single: one lane group per bag for large batches; 256-B and 1-KB rows
 // then go to 16-lane teams (1 or 4 chunks per lane), and 512-B rows too when
 // narrow512 is set (else 32-lane teams).
-inline Shape team_shape(int rb, bool few, bool single, bool narrow512 = false)
+inline Shape team_shape(int rb, int cb, bool few, bool single, bool narrow512 = false)
 {
     Shape s;
-    const int chunks = rb / 16;
+    const int chunks = rb / cb;
     s.R = 1;
     while (s.R < chunks && s.R < kWave) s.R *= 2;
     s.C = (chunks + s.R - 1) / s.R;
-    if (single && (rb == 256 || rb == 1024 || (rb == 512 && narrow512))) {
+    if (cb == 16 && single && (rb == 256 || rb == 1024 || (rb == 512 && narrow512))) {
         s.R = 16;
         s.C = rb / 256;
     }
@@ -648,15 +765,35 @@ struct GatherPlan {
     bool team;           // team kernel (else plain)
     int bags_per_block;
     bool xcd_runs;       // each XCD takes a contiguous run of workgroups
+    int chunk_bytes;     // team kernel: bytes of a row one lane loads at a time
 };
 
-// aligned: tables and every output row start are 16-byte aligned.
-inline GatherPlan plan_gather(int32_t D, int32_t dtype, bool aligned, bool i32, bool weighted, int64_t T,
-                              int64_t B, int64_t nnz, int32_t mode)
+// Chunk size of the team kernel for rows of rb bytes, or 0 for the plain
+// kernel: the widest of 16, 8 and 4 bytes that divides the row, that the
+// tables' alignment allows, whose results (chunk / element size floats) the
+// output rows' alignment allows to store as one access, and whose rows fit
+// (16-byte chunks up to 8 KB, narrower ones one chunk per lane).
+// table_align / out_align: the largest power of two up to 16 dividing every
+// table pointer / every output row start in bytes.
+inline int chunk_bytes(int64_t rb, int dtype, int table_align, int out_align)
 {
-    GatherPlan plan{nullptr, false, kWavesPerBlock, false};
+    const int es = elem_bytes(dtype);
+    for (int cb = 16; cb >= 4; cb /= 2) {
+        const int out_need = cb / es * 4 < 16 ? cb / es * 4 : 16;
+        const int64_t max_rb = cb == 16 ? 8192 : (int64_t)kWave * cb;
+        if (rb % cb == 0 && rb <= max_rb && table_align >= cb && out_align >= out_need) return cb;
+    }
+    return 0;
+}
+
+inline GatherPlan plan_gather(int32_t D, int32_t dtype, int table_align, int out_align, bool i32, bool weighted,
+                              int64_t T, int64_t B, int64_t nnz, int32_t mode)
+{
+    GatherPlan plan{nullptr, false, kWavesPerBlock, false, 0};
     const int64_t rb = (int64_t)D * elem_bytes(dtype);
-    plan.team = rb % 16 == 0 && rb <= 8192 && aligned;
+    const int cb = chunk_bytes(rb, dtype, table_align, out_align);
+    plan.team = cb > 0;
+    plan.chunk_bytes = cb;
     if (!plan.team) {
         plan.fn = weighted ? pick_weighted_kernel(i32, dtype, false, 0, 0, false, false, false)
                            : pick_kernel<false>(i32, dtype, false, 0, 0, false, false, false);
@@ -665,7 +802,7 @@ inline GatherPlan plan_gather(int32_t D, int32_t dtype, bool aligned, bool i32, 
     // Non-temporal loads lose for rows narrower than 128 bytes.
     const bool hint = (mode & EB_HINT_STREAM_ROWS) != 0;
     const bool stream = hint && rb >= 128;
-    const Shape normal = team_shape((int)rb, false, false);
+    const Shape normal = team_shape((int)rb, cb, false, false);
     const int64_t bags = T * B;
     const int64_t waves = bags / (kWave / (normal.R * normal.P));
     const bool few = waves < kWaveSlots && bags <= kFewBagsMax &&
@@ -678,13 +815,16 @@ inline GatherPlan plan_gather(int32_t D, int32_t dtype, bool aligned, bool i32, 
     // teams when streamed (16-lane teams were 2-5% slower on the paper's
     // multi-table shapes) and 16-lane teams for short cached bags.
     const bool short_bags = nnz < (int64_t)rows_in_flight_per_bag(normal, false) * bags;
-    const Shape narrow = team_shape((int)rb, false, true, !stream && short_bags);
+    const Shape narrow = team_shape((int)rb, cb, false, true, !stream && short_bags);
     const int narrow_team = narrow.R * narrow.P;
     const bool single = (stream || short_bags) && !few && narrow_team < normal.R * normal.P &&
                         bags / (kWave / narrow_team) >= kWaveSlots / 2;
-    const Shape sh = few ? team_shape((int)rb, true, false) : single ? narrow : normal;
-    plan.fn = weighted ? pick_weighted_kernel(i32, dtype, true, sh.R, sh.C, stream, few, single)
-                       : pick_kernel<false>(i32, dtype, true, sh.R, sh.C, stream, few, single);
+    const Shape sh = few ? team_shape((int)rb, cb, true, false) : single ? narrow : normal;
+    if (cb == 16)
+        plan.fn = weighted ? pick_weighted_kernel(i32, dtype, true, sh.R, sh.C, stream, few, single)
+                           : pick_kernel<false>(i32, dtype, true, sh.R, sh.C, stream, few, single);
+    else
+        plan.fn = pick_narrow_kernel(weighted, i32, dtype, cb, sh.R, stream, few, single);
     plan.bags_per_block = (kWave / (sh.R * sh.P)) * kWavesPerBlock;
     // No reuse: each XCD takes a contiguous run of bags (measured faster for
     // uniform ids, also for rows under 128 B).  Otherwise hardware order, so
