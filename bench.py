@@ -579,18 +579,22 @@ def workload_args(cid, kw):
     return args
 
 
-def all_workloads(headline, K, W, nbatches):
+def all_workloads(headline, K, W, nbatches, budget_s=420.0):
     """One entry per workload and pooling mode: the headline's numbers for
     workload 2, then every other workload timed by this script in a process
     of its own (a child run with --workload ...), so that each is measured as
     a standalone run is: large tables allocated after other workloads' were
     freed gather 2-4% slower.  At least 200 timed launches each (20 still
     carry a few percent of ramp-up: workload 4 at D 64 96.6 us over 20, 93.4
-    over 400).  A workload that fails records its error in its own entry."""
+    over 400).  A workload that fails records its error in its own entry.
+    The child runs share budget_s seconds (about 40 s is normal): a child
+    past its share is stopped and the rest are recorded as skipped, so the
+    line is always printed."""
     import subprocess
 
     entries = [dict(headline, config=2, source="headline run")]
     K, W = max(K, 200), max(W, 20)
+    deadline = time.monotonic() + budget_s
     for cid, kw, modes in other_workloads():
         w = wl.config(cid, **kw)
         for mode in modes:
@@ -601,8 +605,12 @@ def all_workloads(headline, K, W, nbatches):
                    "--headline-only"]
             if w.dist != "uniform":
                 cmd.append("--cold")
+            left = deadline - time.monotonic()
+            if left < 10:
+                entries.append({"config": cid, "workload": name, "error": "skipped: the child runs' time budget is spent"})
+                continue
             try:
-                res = subprocess.run(cmd, stdout=subprocess.PIPE, text=True, timeout=600)
+                res = subprocess.run(cmd, stdout=subprocess.PIPE, text=True, timeout=left)
                 if res.returncode != 0:
                     raise RuntimeError(f"child run exited with {res.returncode}")
                 r = json.loads(res.stdout.strip().splitlines()[-1])
@@ -614,12 +622,16 @@ def all_workloads(headline, K, W, nbatches):
                      "launches": K, "lookups_per_s": r["lookups_per_launch"] / us * 1e6,
                      "bags_per_s": w.T * w.B / us * 1e6, "algorithmic_bytes_per_launch": int(by),
                      "algorithmic_GBps": round(by / us / 1e3, 1), "frac_of_8TBps": round(by / us / 1e3 / HBM_PEAK_GBPS, 4),
-                     "traffic_GBps": None if tr is None else round(tr / us / 1e3, 1), "process": "own"}
+                     "traffic_GBps": None if tr is None else round(tr / us / 1e3, 1),
+                     "traffic_frac_of_8TBps": None if tr is None else round(tr / us / 1e3 / HBM_PEAK_GBPS, 4),
+                     "process": "own"}
                 if "local_fraction" in r:
                     e["local_fraction"] = r["local_fraction"]
                 if w.dist != "uniform":
                     e["note"] = ("skewed ids: algorithmic bytes count every lookup's row, part of which "
-                                 "L2 and the last-level cache serve, so the fraction is not an HBM fraction")
+                                 "L2 and the last-level cache serve, so frac_of_8TBps is not an HBM fraction; "
+                                 "traffic_frac_of_8TBps is the L2-fabric traffic's (last-level-cache hits "
+                                 "included)")
                     e["single_launch_us"] = {"warm_median": round(r["single_launch_warm"]["median_us"], 1),
                                              "cold_median_512MB_flushed": round(r["single_launch_cold"]["median_us"], 1)}
                 entries.append(e)
@@ -896,7 +908,8 @@ def main():
                 "bags_per_s": w.T * w.B / launch_ms * 1e3,
                 "algorithmic_bytes_per_launch": int(bytes_per_launch),
                 "algorithmic_GBps": round(achieved, 1), "frac_of_8TBps": round(achieved / HBM_PEAK_GBPS, 4),
-                "traffic_GBps": None if traffic is None else round(traffic / launch_ms / 1e6, 1)}
+                "traffic_GBps": None if traffic is None else round(traffic / launch_ms / 1e6, 1),
+                "traffic_frac_of_8TBps": None if traffic is None else round(traffic / launch_ms / 1e6 / HBM_PEAK_GBPS, 4)}
         line["workloads"] = all_workloads(head, K, W, args.batches)
     print(json.dumps(line), flush=True)
 
