@@ -627,13 +627,15 @@ def all_workloads(headline, K, W, nbatches, budget_s=420.0):
                      "process": "own"}
                 if "local_fraction" in r:
                     e["local_fraction"] = r["local_fraction"]
+                sw = r["single_launch_warm"]
+                e["single_launch_us"] = {"median": round(sw["median_us"], 1), "p10": round(sw["p10_us"], 1),
+                                         "p90": round(sw["p90_us"], 1), "launches": sw["launches"]}
                 if w.dist != "uniform":
                     e["note"] = ("skewed ids: algorithmic bytes count every lookup's row, part of which "
                                  "L2 and the last-level cache serve, so frac_of_8TBps is not an HBM fraction; "
                                  "traffic_frac_of_8TBps is the L2-fabric traffic's (last-level-cache hits "
                                  "included)")
-                    e["single_launch_us"] = {"warm_median": round(r["single_launch_warm"]["median_us"], 1),
-                                             "cold_median_512MB_flushed": round(r["single_launch_cold"]["median_us"], 1)}
+                    e["single_launch_us"]["cold_median_512MB_flushed"] = round(r["single_launch_cold"]["median_us"], 1)
                 entries.append(e)
                 log(f"bench: {name}: {us:.1f} us, {by / us / 1e3:.0f} GB/s algorithmic "
                     f"({by / us / 1e3 / HBM_PEAK_GBPS * 100:.1f}% of 8 TB/s)")
@@ -808,10 +810,12 @@ def main():
         f"wall step {ms_per_step * 1e3:.1f} us, {achieved:.0f} GB/s algorithmic")
 
     extra = {}
+    # The distribution of single launches (each between its own pair of HIP
+    # events; about 2 us above the back-to-back mean for the events' cost).
+    n = max(20, min(K, 200)) if args.cold else 100
+    extra["single_launch_warm"] = per_launch_us(torch, stream, step_fns, n)
     if args.cold:
         scratch = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
-        n = max(20, min(K, 200))
-        extra["single_launch_warm"] = per_launch_us(torch, stream, step_fns, n)
         extra["single_launch_cold"] = per_launch_us(torch, stream, step_fns, n,
                                                     flush=lambda i: scratch.fill_(i & 0xFF))
         extra["single_launch_cold"]["flush"] = "512 MB written on the launch stream before each launch"
@@ -909,7 +913,8 @@ def main():
                 "algorithmic_bytes_per_launch": int(bytes_per_launch),
                 "algorithmic_GBps": round(achieved, 1), "frac_of_8TBps": round(achieved / HBM_PEAK_GBPS, 4),
                 "traffic_GBps": None if traffic is None else round(traffic / launch_ms / 1e6, 1),
-                "traffic_frac_of_8TBps": None if traffic is None else round(traffic / launch_ms / 1e6 / HBM_PEAK_GBPS, 4)}
+                "traffic_frac_of_8TBps": None if traffic is None else round(traffic / launch_ms / 1e6 / HBM_PEAK_GBPS, 4),
+                "single_launch_us": {k: round(extra["single_launch_warm"][k + "_us"], 1) for k in ("median", "p10", "p90")}}
         line["workloads"] = all_workloads(head, K, W, args.batches)
     print(json.dumps(line), flush=True)
 
