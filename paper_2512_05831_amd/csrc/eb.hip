@@ -11,9 +11,11 @@
 // read, so it is bound by HBM bandwidth and never by ALU or matrix cores.
 //
 // Kernel shape ("team" gather):
-//   * A row of rb = D*es bytes is read by R lanes, R the smallest power of
-//     two covering min(64, rb/16), each loading C = ceil(rb/(16R)) 16-byte
-//     chunks (global_load_dwordx4); surplus lanes of a ragged row idle.
+//   * A row of rb = D*es bytes is read in chunks of CB = 16 bytes
+//     (global_load_dwordx4), or 8 or 4 bytes when 16 does not divide the row
+//     or the tables' or output's alignment does not allow it: R lanes, R the
+//     smallest power of two covering min(64, rb/CB), each load C =
+//     ceil(rb/(CB*R)) chunks; surplus lanes of a ragged row idle.
 //   * P such lane groups form the team that pools one bag: group g takes the
 //     bag's rows g, g+P, g+2P, ...; a wave holds 64/(R*P) teams (P = 64/R
 //     for rows of 16 lanes or more, 16/R below).  Large batches of streamed
@@ -38,9 +40,10 @@
 //     cache (best for skewed ids).  Under the no-reuse hint block ids are
 //     remapped so each XCD gets a contiguous run of bags (measured faster for
 //     uniform ids).
-// Rows whose size is not a multiple of 16 bytes, unaligned tables or outputs,
-// and rows wider than 8 KB take a plain one-wave-per-bag kernel: all lanes
-// read a row's columns with element-sized loads, 8 rows in flight.
+// Rows that no chunk width fits (sizes not a multiple of 4 bytes, tables or
+// outputs aligned to less than 4 bytes, narrow chunks beyond 64 per row, rows
+// wider than 8 KB) take a plain one-wave-per-bag kernel: all lanes read a
+// row's columns with element-sized loads, 8 rows in flight.
 
 #include <hip/hip_runtime.h>
 
