@@ -219,8 +219,8 @@ def attainable_ceiling(torch, dev, w, lookups: int, stream):
                 best = {"GBps": gbps, "us_per_launch": us, "rows_in_flight": U, "nontemporal": bool(nt)}
     del table, ids
     torch.cuda.empty_cache()
-    best.update({"kind": "random whole-row reads, pre-resolved int32 ids, no pooling",
-                 "row_bytes": rb, "rows": rows, "footprint_GB": rows * rb / 1e9, "lookups": lookups})
+    best.update({"kind": "random whole-row reads, int32 ids, no pooling",
+                 "row_bytes": rb, "rows": rows, "footprint_GB": round(rows * rb / 1e9, 3), "lookups": lookups})
     return best
 
 
@@ -631,10 +631,6 @@ def all_workloads(headline, K, W, nbatches, budget_s=420.0):
                 e["single_launch_us"] = {"median": round(sw["median_us"], 1), "p10": round(sw["p10_us"], 1),
                                          "p90": round(sw["p90_us"], 1), "launches": sw["launches"]}
                 if w.dist != "uniform":
-                    e["note"] = ("skewed ids: algorithmic bytes count every lookup's row, part of which "
-                                 "L2 and the last-level cache serve, so frac_of_8TBps is not an HBM fraction; "
-                                 "traffic_frac_of_8TBps is the L2-fabric traffic's (last-level-cache hits "
-                                 "included)")
                     e["single_launch_us"]["cold_median_512MB_flushed"] = round(r["single_launch_cold"]["median_us"], 1)
                 entries.append(e)
                 log(f"bench: {name}: {us:.1f} us, {by / us / 1e3:.0f} GB/s algorithmic "
@@ -691,6 +687,39 @@ def parser() -> argparse.ArgumentParser:
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run a plain streaming copy of BYTES (for scaling HBM counters)")
     return ap
+
+
+WORKLOAD_COLUMNS = ["workload", "kernel_us", "lookups_per_s", "bags_per_s", "algorithmic_GBps", "frac_of_8TBps",
+                    "traffic_GBps", "traffic_frac_of_8TBps", "single_launch_us_median_p10_p90",
+                    "cold_single_launch_us_median", "local_fraction"]
+
+
+def _sig(x, n=4):
+    return None if x is None else float(f"{x:.{n}g}")
+
+
+def workloads_table(entries):
+    """The per-workload entries as one table (column names once)."""
+    rows, errors = [], {}
+    for e in entries:
+        if "error" in e:
+            errors[e["workload"]] = e["error"]
+            continue
+        sl = e.get("single_launch_us", {})
+        rows.append([e["workload"], e["kernel_us"], _sig(e["lookups_per_s"]), _sig(e["bags_per_s"]),
+                     e["algorithmic_GBps"], e["frac_of_8TBps"], e.get("traffic_GBps"), e.get("traffic_frac_of_8TBps"),
+                     [sl.get("median"), sl.get("p10"), sl.get("p90")] if sl else None,
+                     sl.get("cold_median_512MB_flushed"), e.get("local_fraction")])
+    table = {"columns": WORKLOAD_COLUMNS, "rows": rows,
+             "note": ("workload 2 from the headline run; every other workload timed in a process of its own: "
+                      "kernel_us is the mean of >= 200 back-to-back launches (HIP events on the launch stream), "
+                      "single launches each between their own events; uniform ids use the streaming hint. "
+                      "For skewed ids (zipf) algorithmic bytes count rows that L2 and the last-level cache "
+                      "serve, so read traffic_frac_of_8TBps (L2-fabric traffic from committed counters) "
+                      "against the peak; cold = after 512 MB written on the launch stream")}
+    if errors:
+        table["errors"] = errors
+    return table
 
 
 def main():
@@ -853,7 +882,7 @@ def main():
             extra["torch_embedding_bag"] = {
                 "us_per_step": tus, "lookups_per_s": (steps_lookups / K) / (tus / 1e6),
                 "calls_per_step": w.T, "steps": tk,
-                "note": "torch.nn.functional.embedding_bag, one call per table, same device tables and ids"}
+                "note": "torch embedding_bag, one call per table, same tables and ids"}
             log(f"bench: torch embedding_bag {tus:.1f} us per step")
 
     cpu = None
@@ -915,7 +944,7 @@ def main():
                 "traffic_GBps": None if traffic is None else round(traffic / launch_ms / 1e6, 1),
                 "traffic_frac_of_8TBps": None if traffic is None else round(traffic / launch_ms / 1e6 / HBM_PEAK_GBPS, 4),
                 "single_launch_us": {k: round(extra["single_launch_warm"][k + "_us"], 1) for k in ("median", "p10", "p90")}}
-        line["workloads"] = all_workloads(head, K, W, args.batches)
+        line["workloads"] = workloads_table(all_workloads(head, K, W, args.batches))
     print(json.dumps(line), flush=True)
 
 

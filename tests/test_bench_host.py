@@ -85,3 +85,21 @@ def test_child_runs_select_every_other_workload():
     # workloads 1, 3 (sum, mean), 4 (6 D x 2 dtypes), 5 (literal, permuted); 2 is the headline
     assert len(seen) == 1 + 2 + 12 + 2
     assert wl.config(5, permuted=True).name in seen and wl.config(3).name + "-mean" in seen
+
+
+def test_workloads_table_keeps_every_entry():
+    ok = {"workload": "w-a", "kernel_us": 10.0, "lookups_per_s": 123456789.0, "bags_per_s": 4.5e6,
+          "algorithmic_GBps": 100.0, "frac_of_8TBps": 0.0125, "traffic_GBps": None,
+          "traffic_frac_of_8TBps": None, "single_launch_us": {"median": 12.0, "p10": 11.0, "p90": 13.0}}
+    skew = dict(ok, workload="w-b", local_fraction=0.12,
+                single_launch_us={"median": 12.0, "p10": 11.0, "p90": 13.0, "cold_median_512MB_flushed": 20.0})
+    bad = {"workload": "w-c", "error": "RuntimeError: child run exited with 1"}
+    t = bench.workloads_table([ok, skew, bad])
+    cols = t["columns"]
+    assert [r[cols.index("workload")] for r in t["rows"]] == ["w-a", "w-b"]
+    assert t["errors"] == {"w-c": bad["error"]}
+    row = dict(zip(cols, t["rows"][1]))
+    assert row["lookups_per_s"] == 123500000.0 and row["local_fraction"] == 0.12
+    assert row["single_launch_us_median_p10_p90"] == [12.0, 11.0, 13.0]
+    assert row["cold_single_launch_us_median"] == 20.0
+    assert dict(zip(cols, t["rows"][0]))["cold_single_launch_us_median"] is None
