@@ -698,6 +698,25 @@ def _sig(x, n=4):
     return None if x is None else float(f"{x:.{n}g}")
 
 
+def exchange_entries(budget_s=120.0):
+    """The row-wise exchange's local kernels (bucketize, sum of partials), timed
+    by a child run of --exchange; one compact entry each, or an error."""
+    import subprocess
+
+    cmd = [sys.executable, os.path.abspath(__file__), "--exchange", "--steps", "100", "--warmup", "10"]
+    try:
+        res = subprocess.run(cmd, stdout=subprocess.PIPE, text=True, timeout=budget_s)
+        if res.returncode != 0:
+            raise RuntimeError(f"child run exited with {res.returncode}")
+        out = {}
+        for ln in res.stdout.strip().splitlines():
+            r = json.loads(ln)
+            out[r["kernel"]] = {k: r[k] for k in ("workload", "us_per_call", "algorithmic_GBps", "frac_of_8TBps")}
+        return out
+    except Exception as exc:  # noqa: BLE001 -- recorded, the line is still printed
+        return {"error": f"{type(exc).__name__}: {exc}"}
+
+
 def workloads_table(entries):
     """The per-workload entries as one table (column names once)."""
     rows, errors = [], {}
@@ -945,6 +964,7 @@ def main():
                 "traffic_frac_of_8TBps": None if traffic is None else round(traffic / launch_ms / 1e6 / HBM_PEAK_GBPS, 4),
                 "single_launch_us": {k: round(extra["single_launch_warm"][k + "_us"], 1) for k in ("median", "p10", "p90")}}
         line["workloads"] = workloads_table(all_workloads(head, K, W, args.batches))
+        line["exchange"] = exchange_entries()
     print(json.dumps(line), flush=True)
 
 
