@@ -60,3 +60,45 @@ def test_no_alloc_rejects_batches_beyond_its_workspace(device):
         eb.eb_bucketize_noalloc(1, 16384, 1024, 1, 1, 1, 1, 1, 1, 1, 1, None)
     assert e.value.code == eb.EB_ERR_UNSUPPORTED
     assert "eb_bucketize_noalloc" in eb.eb_last_error()
+
+
+def test_no_alloc_in_a_hip_graph(device):
+    """The callers the entry point is for capture it: recorded once into a
+    HIP graph, every replay (with eager work and new ids between replays)
+    must equal an eager eb_bucketize of the ids the buffers hold then."""
+    T, B, G = 4, 900, 8
+    idx, off, bounds = batch(11, T, B, G)
+    nnz = idx.size
+    d_b, d_i, d_o = (torch.from_numpy(x).to(device) for x in (bounds, idx, off))
+    out_off = torch.empty((G, T * B + 1), dtype=torch.int64, device=device)
+    out_idx = torch.empty((nnz,), dtype=torch.int64, device=device)
+    seg = torch.empty((G + 1,), dtype=torch.int64, device=device)
+    side = torch.cuda.Stream(device)
+    side.wait_stream(torch.cuda.current_stream(device))
+
+    def call():
+        eb.eb_bucketize_noalloc(T, B, G, d_b.data_ptr(), d_i.data_ptr(), nnz, d_o.data_ptr(),
+                                out_off.data_ptr(), out_idx.data_ptr(), nnz, seg.data_ptr(),
+                                side.cuda_stream)
+    with torch.cuda.stream(side):
+        call()  # the first call on a device looks up the array's address, outside the capture
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=side):
+        call()
+    g = np.random.default_rng(12)
+    for replay in range(4):
+        new = g.integers(-3, 1_000_003, nnz, dtype=np.int64)
+        d_i.copy_(torch.from_numpy(new))
+        out_idx.fill_(-9)
+        out_off.fill_(-9)
+        seg.fill_(-9)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        ref_off, ref_idx, ref_seg, _ = eb.bucketize(d_b, d_i, d_o, T, B)
+        torch.cuda.synchronize()
+        n = int(ref_seg[-1])
+        assert torch.equal(seg, ref_seg), replay
+        assert torch.equal(out_off, ref_off), replay
+        assert torch.equal(out_idx[:n], ref_idx[:n]), replay
