@@ -19,8 +19,9 @@
 // chains of dependent loads and by instruction issue.
 //
 // eb_bucketize runs three kernels on the caller's stream:
-//   1. count   : a wave takes 16 consecutive bags (each XCD one contiguous
-//                run of workgroups); each id's owner by
+//   1. count   : a wave takes 16, 32 or 64 consecutive bags (the most that
+//                leave at least 4608 waves; each XCD one contiguous run of
+//                workgroups); each id's owner by
 //                comparisons with the table's block bounds (up to 8 blocks:
 //                a search tree evaluated as wave-wide lane masks) or by
 //                binary search over them (staged in LDS); for ordinary CSR
@@ -35,7 +36,7 @@
 //                16384 tile sums one workgroup first scans them as one
 //                sequence instead); every 16th scanned entry of each row
 //                is also copied to the workspace for the scatter.
-//   3. scatter : same waves; ids are written to segments[g] +
+//   3. scatter : waves of 16 bags; ids are written to segments[g] +
 //                out_offsets[g][p] + rank (a wave's first out_offsets from
 //                the workspace copy), the rank counting earlier ids of
 //                the bag with the same owner (per 64-id chunk: three ballots
@@ -159,11 +160,15 @@ __device__ __forceinline__ int few_bits(const FewMasks &o)
     return (lane_bit(o.b0) ? kScale : 0) | (lane_bit(o.b1) ? 2 * kScale : 0) | (lane_bit(o.b2) ? 4 * kScale : 0);
 }
 
-// A wave takes kBagsPerWave consecutive bags of one table; a block 4 waves.
-// Few bags per wave keep many waves (and their id loads) in flight.
+// A scatter wave takes kBagsPerWave consecutive bags of one table; a block 4
+// waves.  Few bags per wave keep many waves (and their id loads) in flight.
+// A count wave takes 16, 32 or 64 bags: the most that still leave at least
+// kCountWavesMin waves, since count's waves are short and each starts with a
+// dependent load of its offsets, which longer waves pay less often.
 constexpr int kBagsPerWave = 16;
 constexpr int kBagsPerBlock = kBagsPerWave * kWavesPerBlock;
 static_assert(kBagsPerWave <= kWave && (kBagsPerWave & (kBagsPerWave - 1)) == 0, "bags per wave");
+constexpr int64_t kCountWavesMin = 4608; // 18 per compute unit
 constexpr int kFastShards = 32; // count's per-(bag, destination) histogram fits LDS up to here
 constexpr int kCountChunks = 4;   // 64-id chunks loaded ahead by count
 constexpr int kScatterChunks = 8; // and by scatter (measured best for each)
@@ -183,7 +188,8 @@ struct BucketArgs {
     int64_t B;
     int64_t TB;
     int32_t G;
-    int32_t blocks_per_table;
+    int32_t blocks_per_table;       // scatter's workgroups per table
+    int32_t count_blocks_per_table; // count's
 };
 
 // Workgroups are dealt to the 8 XCDs in turn (workgroup b to XCD b % 8).
@@ -203,8 +209,8 @@ __device__ __forceinline__ int xcd_run_block(int b, int n)
 // count's histogram row per bag: 8 entries for up to 8 destinations (an
 // index by shift), else G.
 __host__ __device__ inline int count_stride(int G) { return G <= kFewShards ? kFewShards : G; }
-__host__ __device__ inline size_t count_wave_bytes(int G) { return (size_t)4 * (G <= kFastShards ? count_stride(G) * kBagsPerWave : G); }
-__host__ __device__ inline size_t count_lds_bytes(int G) { return (size_t)(G + 1) * 8 + kWavesPerBlock * count_wave_bytes(G); }
+__host__ __device__ inline size_t count_wave_bytes(int G, int bags) { return (size_t)4 * (G <= kFastShards ? count_stride(G) * bags : G); }
+__host__ __device__ inline size_t count_lds_bytes(int G, int bags) { return (size_t)(G + 1) * 8 + kWavesPerBlock * count_wave_bytes(G, bags); }
 __host__ __device__ inline size_t scatter_lds_bytes(int G) { return (size_t)(G + 1) * 8 + (size_t)kWavesPerBlock * G * 8; }
 
 __device__ __forceinline__ int64_t shfl_down64(int64_t v, int d)
@@ -310,19 +316,21 @@ __device__ __forceinline__ void count_chunks(const BucketArgs &a, const int64_t 
     }
 }
 
+template <int kBags>
 __global__ __launch_bounds__(kBlock) void eb_bucket_count(const BucketArgs a)
 {
+    static_assert(kBags <= kWave && (kBags & (kBags - 1)) == 0, "bags per count wave");
     extern __shared__ int64_t lds[];
     const int G = a.G;
     int64_t *bnd = lds;
     const int lb = xcd_run_block(blockIdx.x, gridDim.x);
-    const int t = lb / a.blocks_per_table;
+    const int t = lb / a.count_blocks_per_table;
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = threadIdx.x / kWave;
-    int *hist = (int *)((char *)(lds + G + 1) + wave * count_wave_bytes(G));
-    const int64_t b0 = (int64_t)(lb - t * a.blocks_per_table) * kBagsPerBlock + wave * kBagsPerWave;
+    int *hist = (int *)((char *)(lds + G + 1) + wave * count_wave_bytes(G, kBags));
+    const int64_t b0 = (int64_t)(lb - t * a.count_blocks_per_table) * (kBags * kWavesPerBlock) + wave * kBags;
     const bool live = b0 < a.B; // the wave has bags
-    const int nb = live ? (int)min<int64_t>(kBagsPerWave, a.B - b0) : 0;
+    const int nb = live ? (int)min<int64_t>(kBags, a.B - b0) : 0;
     const int64_t p0 = (int64_t)t * a.B + b0;
     const int64_t row = a.TB + 1;
     // The wave's bag ranges do not depend on the bounds: read them first, so
@@ -338,7 +346,7 @@ __global__ __launch_bounds__(kBlock) void eb_bucket_count(const BucketArgs a)
 
     if (contiguous && G <= kFastShards) {
         const uint64_t bags = __ballot(lane < nb);
-        for (int x = lane; x < kBagsPerWave * count_stride(G); x += kWave) hist[x] = 0;
+        for (int x = lane; x < kBags * count_stride(G); x += kWave) hist[x] = 0;
         wave_sync_lds();
         if (G <= kFewShards)
             count_chunks<true>(a, bnd, few_bounds(bnd, G), hist, lane, s, bags, S, E);
@@ -849,6 +857,14 @@ __global__ __launch_bounds__(kBlock) void eb_sum_partials_scalar(const PartialAr
 }
 
 int64_t scan_tiles(int64_t TB) { return std::max<int64_t>(1, (TB + kScanTile - 1) / kScanTile); }
+
+// Bags per count wave for T*B bags in all (see kCountWavesMin).
+int count_bags(int64_t TB)
+{
+    for (int bags = 64; bags > 16; bags /= 2)
+        if (TB / bags >= kCountWavesMin) return bags;
+    return 16;
+}
 int64_t start_entries(int64_t TB) { return TB / kStartStride + 1; }
 
 } // namespace
@@ -904,6 +920,9 @@ int bucketize_impl(int32_t T, int64_t B, int32_t G, const int64_t *bounds, const
     if (TB > 0 && (int64_t)T * bpt > std::numeric_limits<int32_t>::max())
         return fail(EB_ERR_UNSUPPORTED, "eb_bucketize: batch too large for one launch");
     ba.blocks_per_table = (int32_t)bpt;
+    const int cbags = count_bags(TB);
+    const int64_t cbpt = (B + cbags * kWavesPerBlock - 1) / (cbags * kWavesPerBlock);
+    ba.count_blocks_per_table = (int32_t)cbpt;
 
     ScanArgs sa;
     sa.rows = out_offsets;
@@ -920,8 +939,10 @@ int bucketize_impl(int32_t T, int64_t B, int32_t G, const int64_t *bounds, const
 
     if (TB > 0) {
         void *args[] = {&ba};
-        hipError_t err = hipLaunchKernel((const void *)eb_bucket_count, dim3((unsigned)(T * bpt)),
-                                         dim3(kBlock), args, count_lds_bytes(G), st);
+        const void *count = cbags == 64 ? (const void *)eb_bucket_count<64>
+                            : cbags == 32 ? (const void *)eb_bucket_count<32> : (const void *)eb_bucket_count<16>;
+        hipError_t err = hipLaunchKernel(count, dim3((unsigned)(T * cbpt)), dim3(kBlock), args,
+                                         count_lds_bytes(G, cbags), st);
         if (err != hipSuccess) return fail(EB_ERR_HIP, "eb_bucketize: %s", hipGetErrorString(err));
         void *sargs[] = {&sa};
         err = hipLaunchKernel((const void *)eb_scan_tile_sums, dim3(sa.ntiles, G), dim3(kBlock), sargs, 0, st);

@@ -191,6 +191,36 @@ def test_bucketize_unordered_offsets(G, device):
     check_bucketize(T, B, idx, off, bounds, device, capacity=total + 5)
 
 
+@pytest.mark.parametrize("G,T,B", [(8, 3, 100_001), (8, 2, 75_000), (20, 3, 100_001), (100, 3, 100_001),
+                                   (3, 1, 147_456), (8, 1, 294_911)])
+def test_bucketize_long_count_waves(G, T, B, device):
+    """Batches large enough for count waves of 32 bags (from 147,456 bags)
+    or 64 (from 294,912), with ragged last waves and workgroups: the
+    ballot-owner path (G <= 8), the searched-owner path (G <= 32) and the
+    bag-at-a-time path (larger G), against the oracle."""
+    T, B, idx, off, bounds = bucket_case(G * 13 + B, G, T=T, B=B, maxL=4)
+    check_bucketize(T, B, idx, off, bounds, device)
+
+
+@pytest.mark.parametrize("G", [8, 40])
+def test_bucketize_long_count_waves_unordered(G, device):
+    """Mostly ordinary offsets with some out of order, in a batch of
+    300,003 bags (64-bag count waves): waves whose bags do not tile their id
+    range take the bag-at-a-time path, the others the fast one."""
+    g = np.random.default_rng(G + 5)
+    T, B = 3, 100_001
+    L = g.integers(0, 5, T * B)
+    off = wl.offsets_from_lengths(L)
+    nnz = int(off[-1])
+    p = g.choice(np.arange(1, T * B), 2000, replace=False)
+    off[p] = np.clip(off[p] + g.integers(-12, 13, p.size), -3, nnz + 3)
+    rows = [5000, 300, 70000]
+    idx = g.integers(-5, 70_005, nnz).astype(np.int64)
+    bounds = np.array([np.sort(g.integers(0, r + 1, G + 1)) for r in rows], dtype=np.int64)
+    total = int(oracle.bucketize(bounds, idx, off, T, B)[2][-1])
+    check_bucketize(T, B, idx, off, bounds, device, capacity=max(total, 1))
+
+
 def test_bucketize_dlrm_batch(device):
     # the 26-table, 16384-bag, Zipf(1.05) batch, split over 8 GPUs by rows
     w = wl.config(3)
