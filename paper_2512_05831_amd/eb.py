@@ -149,6 +149,15 @@ def eb_sum_partials(G: int, partials_ptr: int, B: int, T: int, D: int,
                                      out_ptr, stream_ptr or None))
 
 
+def _same_device(dev, *tensors) -> None:
+    """Every tensor given (None skipped) must live on the GPU ``dev``: the
+    library takes their addresses as device pointers, so a host tensor would
+    send a kernel to host memory."""
+    for x in tensors:
+        if x is not None and (not x.is_cuda or x.device != dev):
+            raise ValueError(f"tensor on {x.device}, expected {dev}")
+
+
 def bucketize(bounds, indices, offsets, T: int, B: int, stream=None, capacity=None):
     """Torch convenience for eb_bucketize.  ``bounds``: int64 device [T, G+1].
     Returns (out_offsets [G, T*B+1], out_indices [capacity], segments [G+1],
@@ -158,6 +167,9 @@ def bucketize(bounds, indices, offsets, T: int, B: int, stream=None, capacity=No
     import torch
 
     dev = indices.device
+    if not indices.is_cuda:
+        raise ValueError("indices must be a device tensor")
+    _same_device(dev, bounds, offsets)
     G = int(bounds.shape[1]) - 1
     for x in (bounds, indices, offsets):
         if x.dtype != torch.int64 or not x.is_contiguous():
@@ -185,14 +197,19 @@ def sum_partials(partials, B: int, T: int, D: int, mean_offsets=None, nnz: int =
 
     if partials.dtype != torch.float32 or not partials.is_contiguous():
         raise ValueError("partials must be contiguous fp32")
+    if not partials.is_cuda:
+        raise ValueError("partials must be a device tensor")
+    _same_device(partials.device, out, mean_offsets)
     G = int(partials.shape[0])
     if partials.numel() != G * B * T * D:
         raise ValueError("partials must be [G, B, T*D]")
     if out is None:
         out = torch.empty((B, T * D), dtype=torch.float32, device=partials.device)
-    if mean_offsets is not None and (mean_offsets.dtype != torch.int64 or
+    elif out.dtype != torch.float32 or not out.is_contiguous() or out.numel() != B * T * D:
+        raise ValueError("out must be contiguous fp32 [B, T*D]")
+    if mean_offsets is not None and (mean_offsets.dtype != torch.int64 or not mean_offsets.is_contiguous() or
                                      mean_offsets.numel() != T * B + 1):
-        raise ValueError("mean_offsets must be int64 [T*B+1]")
+        raise ValueError("mean_offsets must be contiguous int64 [T*B+1]")
     if stream is None:
         stream = torch.cuda.current_stream(partials.device)
     eb_sum_partials(G, partials.data_ptr(), B, T, D,
@@ -231,6 +248,8 @@ class EmbeddingBagTables:
         for w in self.tables:
             if w.dim() != 2 or w.shape[1] != self.D or w.dtype != t0.dtype or not w.is_cuda:
                 raise ValueError("tables must be 2-D device tensors of one dtype and width")
+            if w.device != t0.device:
+                raise ValueError("tables must all be on one device")
             if not w.is_contiguous():
                 raise ValueError("tables must be contiguous")
         self.T = len(self.tables)
@@ -261,8 +280,9 @@ class EmbeddingBagTables:
             raise ValueError("offsets must have T*B+1 entries")
         if out.dtype != torch.float32 or not out.is_contiguous() or out.numel() < B * self.T * self.D:
             raise ValueError("out must be contiguous fp32 [B, T*D]")
-        if want_hits and (hits.dtype != torch.int32 or hits.numel() < B * self.T):
-            raise ValueError("hits must be int32 [B, T]")
+        if want_hits and (hits.dtype != torch.int32 or not hits.is_contiguous() or hits.numel() < B * self.T):
+            raise ValueError("hits must be contiguous int32 [B, T]")
+        _same_device(dev, indices, offsets, out, hits if want_hits else None)
         eb_forward(self.handle, self.T, self.rows, self.D, self.dtype, indices.data_ptr(),
                    indices.numel(), offsets.data_ptr(), B, mode, self.shard_lo, self.shard_hi,
                    out.data_ptr(), hits.data_ptr() if want_hits else None, stream.cuda_stream)
@@ -300,6 +320,7 @@ class EmbeddingBagTables:
         if weights is not None and (weights.dtype != torch.float32 or not weights.is_contiguous() or
                                     weights.numel() != indices.numel()):
             raise ValueError("weights must be contiguous fp32 with one entry per index")
+        _same_device(dev, indices, offsets, out, hits, weights)
         if stream is None:
             stream = torch.cuda.current_stream(dev)
         ldo = out.stride(0) if B > 1 else out.shape[1]
@@ -322,6 +343,15 @@ class EmbeddingBagTables:
             stream = torch.cuda.current_stream(self.tables[0].device)
         if offsets.numel() != self.T * B + 1 or out.numel() < B * self.T * self.D:
             raise ValueError("offsets / out do not match T, B, D")
+        if out.dtype != torch.float32 or not out.is_contiguous():
+            raise ValueError("out must be contiguous fp32 [B, T*D]")
+        if hits is not None and (hits.dtype != torch.int32 or not hits.is_contiguous() or
+                                 hits.numel() < B * self.T):
+            raise ValueError("hits must be contiguous int32 [B, T]")
+        if weights is not None and (weights.dtype != torch.float32 or not weights.is_contiguous() or
+                                    weights.numel() != indices.numel()):
+            raise ValueError("weights must be contiguous fp32 with one entry per index")
+        _same_device(self.tables[0].device, indices, offsets, out, hits, weights)
         lib = library()
         itype = _index_type(indices, offsets)
         hits_ptr = hits.data_ptr() if hits is not None else None

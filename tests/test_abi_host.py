@@ -309,3 +309,18 @@ def test_bucketize_noalloc_checks_sizes_before_the_device():
                                                    1, FAKE, None)) == eb.EB_ERR_UNSUPPORTED
     assert code_of(lambda: eb.eb_bucketize_noalloc(-1, 4, 2, FAKE, FAKE, 1, FAKE, FAKE, FAKE,
                                                    1, FAKE, None)) == eb.EB_ERR_INVALID
+
+
+def test_torch_helpers_refuse_host_tensors():
+    """The torch helpers pass tensor addresses to the library as device
+    pointers: host tensors, mismatched outputs and bad layouts are refused
+    before any library call."""
+    torch = pytest.importorskip("torch")
+    b = torch.zeros((2, 4), dtype=torch.int64)
+    i = torch.zeros(5, dtype=torch.int64)
+    o = torch.zeros(2 * 3 + 1, dtype=torch.int64)
+    with pytest.raises(ValueError, match="device"):
+        eb.bucketize(b, i, o, 2, 3)
+    p = torch.zeros((2, 3, 8), dtype=torch.float32)
+    with pytest.raises(ValueError, match="device"):
+        eb.sum_partials(p, 3, 1, 8)

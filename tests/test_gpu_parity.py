@@ -352,6 +352,46 @@ def test_async_on_caller_stream(device):
     et.close()
 
 
+def test_binding_refuses_host_and_misshapen_tensors(device):
+    """The torch helpers refuse host tensors (whose addresses a kernel would
+    take for device memory), tensors on another device than the tables, and
+    outputs of the wrong type or layout, before launching anything; the same
+    call with proper tensors then runs as usual."""
+    g = np.random.default_rng(3)
+    T, B, D, rows = 2, 9, 16, 100
+    tabs = [torch.from_numpy(g.standard_normal((rows, D)).astype(np.float32)).to(device) for _ in range(T)]
+    L = g.integers(0, 5, T * B)
+    off = wl.offsets_from_lengths(L)
+    idx = g.integers(0, rows, int(off[-1])).astype(np.int64)
+    d_i, d_o = torch.from_numpy(idx).to(device), torch.from_numpy(off).to(device)
+    tables = eb.EmbeddingBagTables(tabs)
+    with pytest.raises(ValueError, match="expected"):
+        tables.forward(d_i.cpu(), d_o, B)
+    with pytest.raises(ValueError, match="expected"):
+        tables.forward(d_i, d_o, B, out=torch.empty((B, T * D), dtype=torch.float32))
+    with pytest.raises(ValueError, match="hits"):
+        tables.forward(d_i, d_o, B, hits=torch.empty((T, B), dtype=torch.int32, device=device).t())
+    with pytest.raises(ValueError, match="expected"):
+        tables.forward_ex(d_i, d_o.cpu(), B)
+    with pytest.raises(ValueError, match="expected"):
+        tables.forward_ex(d_i, d_o, B, weights=torch.ones(idx.size, dtype=torch.float32))
+    with pytest.raises(ValueError, match="out"):
+        tables.prepare(d_i, d_o, B, eb.EB_SUM, torch.empty((T * D, B), dtype=torch.float32, device=device).t())
+    with pytest.raises(ValueError, match="out"):
+        tables.prepare(d_i, d_o, B, eb.EB_SUM, torch.empty((B, T * D), dtype=torch.float16, device=device))
+    with pytest.raises(ValueError, match="expected"):
+        eb.bucketize(torch.zeros((T, 3), dtype=torch.int64), d_i, d_o, T, B)
+    parts = torch.zeros((2, B, T * D), dtype=torch.float32, device=device)
+    with pytest.raises(ValueError, match="out"):
+        eb.sum_partials(parts, B, T, D, out=torch.empty((B, T * D), dtype=torch.float16, device=device))
+    with pytest.raises(ValueError, match="expected"):
+        eb.sum_partials(parts, B, T, D, mean_offsets=d_o.cpu(), nnz=idx.size)
+    got = tables.forward(d_i, d_o, B).cpu().numpy()
+    torch.cuda.synchronize()
+    ref, _, mag = oracle.forward([t.cpu().numpy() for t in tabs], [rows] * T, D, wl.F32, idx, off, B, wl.SUM)
+    assert max_rel_error(got, ref, mag) <= sum_tolerance(4)
+
+
 def test_hip_graph_capture_and_replay(device):
     """eb_forward allocates nothing and never synchronises, so it records into
     a HIP graph; each replay pools the ids the input buffers hold then."""
