@@ -42,6 +42,10 @@
  *     count with multiplicity.
  *   - Device buffers are borrowed: the caller owns and frees them, and must
  *     keep table memory alive while a handle that names it is in use.
+ *   - One call's device buffers (tables included) and its stream belong to
+ *     one GPU: the kernels run on the stream's device (the current device
+ *     for the NULL stream) and address the buffers there.  Host pointers in
+ *     their place are not detected and fault the device.
  */
 #ifndef EB_H
 #define EB_H
