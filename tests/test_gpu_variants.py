@@ -128,8 +128,22 @@ def test_int32_empty_and_workload_batch(device):
     dts = [torch.randn((w.rows, w.D), generator=gen, device=device) for _ in range(w.T)]
     mode = wl.SUM | eb.EB_HINT_STREAM_ROWS  # the same mode (and so the same lane mapping) on both sides
     got, hits = run_ex(dts, [w.rows] * w.T, idx, off, w.B, mode, device)
+    got, hits = got.cpu().numpy(), hits.cpu().numpy()
     want, want_hits = run_i64(dts, [w.rows] * w.T, idx, off, w.B, mode, device)
-    assert same_bits(got.cpu().numpy(), want) and np.array_equal(hits.cpu().numpy(), want_hits)
+    assert same_bits(got, want) and np.array_equal(hits, want_hits)
+    # and directly against the oracle on 64 sampled bags per table, pooled
+    # from host copies of just the rows those bags read
+    g = np.random.default_rng(6)
+    for t in range(w.T):
+        bags = np.sort(g.choice(w.B, 64, replace=False))
+        spans = [(int(off[t * w.B + b]), int(off[t * w.B + b + 1])) for b in bags]
+        ids = np.concatenate([idx[s:e] for s, e in spans])
+        need = np.unique(ids)
+        host = dts[t][torch.from_numpy(need).to(device)].cpu().numpy()
+        sub_off = wl.offsets_from_lengths(np.array([e - s for s, e in spans]))
+        ref, ref_hits, mag = oracle.forward([host], [need.size], w.D, wl.F32, np.searchsorted(need, ids),
+                                            sub_off, bags.size, wl.SUM)
+        assert_parity(got[bags, t * w.D:(t + 1) * w.D], ref, mag, w.L, wl.F32, hits[bags, t:t + 1], ref_hits)
     # no ids at all: every bag pools to +0
     z_off = np.zeros(w.T * 4 + 1, dtype=np.int64)
     got, hits = run_ex(dts, [w.rows] * w.T, np.zeros(0, np.int64), z_off, 4, wl.MEAN, device)
