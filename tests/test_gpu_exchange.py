@@ -221,6 +221,52 @@ def test_bucketize_long_count_waves_unordered(G, device):
     check_bucketize(T, B, idx, off, bounds, device, capacity=max(total, 1))
 
 
+def draw_bucket_case(seed):
+    """One seeded random bucketize case over every axis at once: destinations
+    (across the ballot, searched and per-owner paths), tables, batch (up to
+    count's 64-bag waves), lengths, ids (out of range too), bounds (even,
+    uneven, with empty blocks, or unsorted), ordinary or disordered offsets
+    and the capacity of out_indices."""
+    g = np.random.default_rng(seed)
+    G = int(g.choice([1, 2, 3, 5, 8, 9, 16, 31, 32, 33, 64, 65, 200, 1024]))
+    T = int(g.integers(1, 7))
+    B = int(g.choice([1, 15, 16, 17, 300, 2048, 2049, 9000, 30000, 60000]))
+    while G * T * B > 20_000_000:  # out_offsets stays under 160 MB
+        B = max(1, B // 4)
+    maxL = int(g.choice([0, 3, 40, 300])) if T * B <= 2000 else int(g.choice([0, 3, 12]))
+    L = g.integers(0, maxL + 1, T * B)
+    off = wl.offsets_from_lengths(L)
+    nnz = int(off[-1])
+    kind = g.choice(["even", "uneven", "empty", "unsorted"], p=[0.35, 0.3, 0.2, 0.15])
+    # disordered offsets only with sorted bounds: with unsorted ones the split
+    # is unspecified, and check_split needs every id sent stored
+    if kind != "unsorted" and g.random() < 0.2 and T * B > 1:
+        p = g.choice(np.arange(1, T * B), min(T * B - 1, 1 + T * B // 50), replace=False)
+        off[p] = np.clip(off[p] + g.integers(-9, 10, p.size), -3, nnz + 3)
+    rows = [int(g.integers(1, 100_000)) for _ in range(T)]
+    if kind == "even":
+        bounds = even_bounds(rows, G)
+    elif kind == "uneven":
+        bounds = np.array([np.sort(g.integers(-5, r + 5, G + 1)) for r in rows], dtype=np.int64)
+    elif kind == "empty":
+        bounds = np.array([np.sort(g.choice([0, r // 3, r // 2, r], G + 1)) for r in rows], dtype=np.int64)
+    else:
+        bounds = g.integers(0, max(rows) + 1, (T, G + 1)).astype(np.int64)
+    idx = g.integers(-7, max(rows) + 7, nnz).astype(np.int64)
+    return T, B, G, idx, off, bounds, kind == "unsorted", g
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_bucketize_random_config(seed, device):
+    T, B, G, idx, off, bounds, unsorted, g = draw_bucket_case(5000 + seed)
+    if unsorted:
+        check_split(bounds, idx, off, T, B, run_bucketize(bounds, idx, off, T, B, device))
+        return
+    total = int(oracle.bucketize(bounds, idx, off, T, B, capacity=0)[2][-1])
+    cap = int(g.choice([len(idx), total, total // 2, total + 5]))
+    check_bucketize(T, B, idx, off, bounds, device, capacity=cap)
+
+
 def test_bucketize_dlrm_batch(device):
     # the 26-table, 16384-bag, Zipf(1.05) batch, split over 8 GPUs by rows
     w = wl.config(3)
