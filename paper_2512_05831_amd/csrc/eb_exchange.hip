@@ -19,15 +19,16 @@
 // chains of dependent loads and by instruction issue.
 //
 // eb_bucketize runs three kernels on the caller's stream:
-//   1. count   : a wave takes 16, 32 or 64 consecutive bags (the most that
-//                leave at least 4608 waves; each XCD one contiguous run of
-//                workgroups); each id's owner by
+//   1. count   : a wave takes 16, 32 or 64 consecutive bags (for up to 8
+//                destinations the most that leave at least 4608 waves, else
+//                16; each XCD one contiguous run of workgroups); each id's
+//                owner by
 //                comparisons with the table's block bounds (up to 8 blocks:
 //                a search tree evaluated as wave-wide lane masks) or by
 //                binary search over them (staged in LDS); for ordinary CSR
-//                offsets the wave streams its whole id range in 64-id chunks
-//                into a [bag][destination] histogram in LDS, else it walks the
-//                bags one at a time; counts land in out_offsets[g][p + 1]
+//                offsets and up to 64 destinations the wave streams its whole
+//                id range in 64-id chunks into a [bag][destination] histogram
+//                in LDS, else it walks the bags one at a time; counts land in out_offsets[g][p + 1]
 //                (coalesced per destination).
 //   2. scan    : inclusive scan of every destination's row of counts
 //                (reduce-then-scan over 2048-entry tiles: tile sums in the
@@ -39,9 +40,10 @@
 //   3. scatter : waves of 16 bags; ids are written to segments[g] +
 //                out_offsets[g][p] + rank (a wave's first out_offsets from
 //                the workspace copy), the rank counting earlier ids of
-//                the bag with the same owner (per 64-id chunk: three ballots
-//                of the owner's bits for up to 8 destinations, else a ballot
-//                per distinct owner), so the order is stable.  For ordinary CSR
+//                the bag with the same owner (per 64-id chunk: ballots of
+//                the owner's bits, three for up to 8 destinations and 4 to 6
+//                for up to 64, else a ballot per distinct owner), so the
+//                order is stable.  For ordinary CSR
 //                offsets one running slot per destination and wave suffices,
 //                since position order is then (bag, position) order.  Every
 //                store is checked against the capacity of out_indices (an
@@ -162,14 +164,15 @@ __device__ __forceinline__ int few_bits(const FewMasks &o)
 
 // A scatter wave takes kBagsPerWave consecutive bags of one table; a block 4
 // waves.  Few bags per wave keep many waves (and their id loads) in flight.
-// A count wave takes 16, 32 or 64 bags: the most that still leave at least
-// kCountWavesMin waves, since count's waves are short and each starts with a
-// dependent load of its offsets, which longer waves pay less often.
+// A count wave takes 16, 32 or 64 bags (up to 8 destinations; 16 beyond):
+// the most that still leave at least kCountWavesMin waves, since count's
+// waves are short and each starts with a dependent load of its offsets,
+// which longer waves pay less often.
 constexpr int kBagsPerWave = 16;
 constexpr int kBagsPerBlock = kBagsPerWave * kWavesPerBlock;
 static_assert(kBagsPerWave <= kWave && (kBagsPerWave & (kBagsPerWave - 1)) == 0, "bags per wave");
 constexpr int64_t kCountWavesMin = 4608; // 18 per compute unit
-constexpr int kFastShards = 32; // count's per-(bag, destination) histogram fits LDS up to here
+constexpr int kFastShards = 64; // count's per-(bag, destination) histogram fits LDS up to here
 constexpr int kCountChunks = 4;   // 64-id chunks loaded ahead by count
 constexpr int kScatterChunks = 8; // and by scatter (measured best for each)
 constexpr int kBallotShards = kFewShards; // compare-based owners, one ballot per destination
@@ -688,6 +691,69 @@ __device__ __forceinline__ void scatter_few_pass(const BucketArgs &a, const FewB
         if ((uint64_t)pos[u] < (uint64_t)a.out_cap) a.out_indices[pos[u]] = id[u];
 }
 
+// One pass of the scatter for contiguous bags and 9 to 64 destinations: as
+// scatter_few_pass, with each id's owner found by binary search over the
+// bounds in LDS and ranked through kBits ballots of the owner's bits (lane d
+// < G holds destination d's slot; lbit[i] is the complement of the lane's
+// bit i as an all-ones / zero mask).
+template <bool kFull, int kBits>
+__device__ __forceinline__ void scatter_mid_pass(const BucketArgs &a, const int64_t *bnd, int lane,
+                                                 const uint32_t (&lbit)[kBits], int64_t &slot, int64_t k0, int R)
+{
+    const int64_t *src = a.indices + k0 + lane;
+    int64_t id[kScatterChunks];
+#pragma unroll
+    for (int u = 0; u < kScatterChunks; ++u)
+        id[u] = (kFull || lane_bit(lanes_below(R - u * kWave))) ? __builtin_nontemporal_load(src + u * kWave) : 0;
+    int64_t pos[kScatterChunks];
+#pragma unroll
+    for (int u = 0; u < kScatterChunks; ++u) {
+        const bool in = kFull || lane_bit(lanes_below(R - u * kWave));
+        const int g = in ? owner_of(bnd, a.G, id[u]) : -1;
+        const bool ok = g >= 0;
+        const uint64_t valid = __ballot(ok);
+        uint32_t same_lo = (uint32_t)valid, same_hi = (uint32_t)(valid >> 32);
+        uint32_t own_lo = same_lo, own_hi = same_hi;
+#pragma unroll
+        for (int i = 0; i < kBits; ++i) {
+            const uint64_t b = __ballot(ok && ((g >> i) & 1));
+            const uint32_t n = ((g >> i) & 1) ? 0u : ~0u; // complement of this lane's owner bit
+            same_lo &= (uint32_t)b ^ n;
+            same_hi &= (uint32_t)(b >> 32) ^ n;
+            own_lo &= (uint32_t)b ^ lbit[i];
+            own_hi &= (uint32_t)(b >> 32) ^ lbit[i];
+        }
+        const int rank = (int)__builtin_amdgcn_mbcnt_hi(same_hi, __builtin_amdgcn_mbcnt_lo(same_lo, 0u));
+        const int from = ok ? g * 4 : 0;
+        const int base_lo = __builtin_amdgcn_ds_bpermute(from, (int)(uint32_t)slot);
+        const int base_hi = __builtin_amdgcn_ds_bpermute(from, (int)(slot >> 32));
+        const int64_t base = ((int64_t)base_hi << 32) | (uint32_t)base_lo;
+        pos[u] = ok ? base + rank : -1;
+        slot += __popc(own_lo) + __popc(own_hi);
+    }
+    __builtin_amdgcn_sched_barrier(0); // keep the stores after all ranking
+#pragma unroll
+    for (int u = 0; u < kScatterChunks; ++u)
+        if ((uint64_t)pos[u] < (uint64_t)a.out_cap) a.out_indices[pos[u]] = id[u];
+}
+
+template <int kBits>
+__device__ __forceinline__ void scatter_mid(const BucketArgs &a, const int64_t *bnd, int lane, int64_t slot, int64_t S,
+                                            int64_t E)
+{
+    uint32_t lbit[kBits];
+#pragma unroll
+    for (int i = 0; i < kBits; ++i) lbit[i] = (uint32_t)((lane >> i) & 1) - 1u;
+    constexpr int kPass = kScatterChunks * kWave;
+    for (int64_t k0 = S; k0 < E; k0 += kPass) {
+        const int R = __builtin_amdgcn_readfirstlane((int)min<int64_t>(E - k0, (int64_t)kPass));
+        if (R == kPass)
+            scatter_mid_pass<true, kBits>(a, bnd, lane, lbit, slot, k0, R);
+        else
+            scatter_mid_pass<false, kBits>(a, bnd, lane, lbit, slot, k0, R);
+    }
+}
+
 __global__ __launch_bounds__(kBlock) void eb_bucket_scatter(const BucketArgs a)
 {
     extern __shared__ int64_t lds[];
@@ -736,34 +802,16 @@ __global__ __launch_bounds__(kBlock) void eb_bucket_scatter(const BucketArgs a)
         return;
     }
     if (contiguous && G <= kWave) {
-        // Contiguous bags: within a destination, (bag, position) order is
-        // position order, so one running slot per destination suffices;
-        // lane g keeps destination g's in a register.
-        int64_t slot = first_slot;
-        const uint64_t below = (1ull << lane) - 1;
-        for (int64_t k0 = S; k0 < E; k0 += kScatterChunks * kWave) {
-            int64_t id[kScatterChunks];
-#pragma unroll
-            for (int u = 0; u < kScatterChunks; ++u) {
-                const int64_t k = k0 + u * kWave + lane;
-                id[u] = k < E ? __builtin_nontemporal_load(a.indices + k) : 0;
-            }
-#pragma unroll
-            for (int u = 0; u < kScatterChunks; ++u) {
-                const int64_t k = k0 + u * kWave + lane;
-                const int g = k < E ? owner_of(bnd, G, id[u]) : -1;
-                uint64_t pending = __ballot(g >= 0);
-                while (pending) {
-                    const int og = __builtin_amdgcn_readlane(g, __builtin_ctzll(pending));
-                    const uint64_t same = __ballot(g == og);
-                    const int64_t base = readlane64(slot, og);
-                    const int64_t pos = base + __popcll(same & below);
-                    if (g == og && (uint64_t)pos < (uint64_t)a.out_cap) a.out_indices[pos] = id[u];
-                    if (lane == og) slot += __popcll(same);
-                    pending &= ~same;
-                }
-            }
-        }
+        // Contiguous bags, 9 to 64 destinations: within a destination, (bag,
+        // position) order is position order, so one running slot per
+        // destination (lane g keeps destination g's) suffices, and ballots of
+        // the owners' 4, 5 or 6 bits rank a whole chunk at once.
+        if (G <= 16)
+            scatter_mid<4>(a, bnd, lane, first_slot, S, E);
+        else if (G <= 32)
+            scatter_mid<5>(a, bnd, lane, first_slot, S, E);
+        else
+            scatter_mid<6>(a, bnd, lane, first_slot, S, E);
         return;
     }
     if (contiguous) {
@@ -858,9 +906,13 @@ __global__ __launch_bounds__(kBlock) void eb_sum_partials_scalar(const PartialAr
 
 int64_t scan_tiles(int64_t TB) { return std::max<int64_t>(1, (TB + kScanTile - 1) / kScanTile); }
 
-// Bags per count wave for T*B bags in all (see kCountWavesMin).
-int count_bags(int64_t TB)
+// Bags per count wave for T*B bags in all and G destinations (see
+// kCountWavesMin).  Only the owner-mask path (G <= 8, 8 histogram entries per
+// bag) gains from longer waves; with more destinations each bag's histogram
+// row, or the bag-at-a-time loop, makes them slower.
+int count_bags(int64_t TB, int G)
 {
+    if (G > kFewShards) return 16;
     for (int bags = 64; bags > 16; bags /= 2)
         if (TB / bags >= kCountWavesMin) return bags;
     return 16;
@@ -920,7 +972,7 @@ int bucketize_impl(int32_t T, int64_t B, int32_t G, const int64_t *bounds, const
     if (TB > 0 && (int64_t)T * bpt > std::numeric_limits<int32_t>::max())
         return fail(EB_ERR_UNSUPPORTED, "eb_bucketize: batch too large for one launch");
     ba.blocks_per_table = (int32_t)bpt;
-    const int cbags = count_bags(TB);
+    const int cbags = count_bags(TB, G);
     const int64_t cbpt = (B + cbags * kWavesPerBlock - 1) / (cbags * kWavesPerBlock);
     ba.count_blocks_per_table = (int32_t)cbpt;
 

@@ -195,9 +195,9 @@ def test_bucketize_unordered_offsets(G, device):
                                    (3, 1, 147_456), (8, 1, 294_911)])
 def test_bucketize_long_count_waves(G, T, B, device):
     """Batches large enough for count waves of 32 bags (from 147,456 bags)
-    or 64 (from 294,912), with ragged last waves and workgroups: the
-    ballot-owner path (G <= 8), the searched-owner path (G <= 32) and the
-    bag-at-a-time path (larger G), against the oracle."""
+    or 64 (from 294,912) at up to 8 destinations, with ragged last waves and
+    workgroups, and the same sizes through the searched-owner path (G <= 32)
+    and the bag-at-a-time path (larger G), against the oracle."""
     T, B, idx, off, bounds = bucket_case(G * 13 + B, G, T=T, B=B, maxL=4)
     check_bucketize(T, B, idx, off, bounds, device)
 
