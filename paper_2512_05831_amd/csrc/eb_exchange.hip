@@ -34,7 +34,7 @@
 //                (reduce-then-scan over 2048-entry tiles: tile sums in the
 //                workspace; each tile then adds up its row's earlier tiles,
 //                and the rows' first tiles the segments; with more than
-//                16384 tile sums one workgroup first scans them as one
+//                131072 tile sums one workgroup first scans them as one
 //                sequence instead); every 16th scanned entry of each row
 //                is also copied to the workspace for the scatter.
 //   3. scatter : waves of 16 bags; ids are written to segments[g] +
@@ -172,7 +172,7 @@ constexpr int kBagsPerWave = 16;
 constexpr int kBagsPerBlock = kBagsPerWave * kWavesPerBlock;
 static_assert(kBagsPerWave <= kWave && (kBagsPerWave & (kBagsPerWave - 1)) == 0, "bags per wave");
 constexpr int64_t kCountWavesMin = 4608; // 18 per compute unit
-constexpr int kFastShards = 64; // count's per-(bag, destination) histogram fits LDS up to here
+constexpr int kCountHistBytes = 8192; // count's per-wave [bag][destination] histogram, at most
 constexpr int kCountChunks = 4;   // 64-id chunks loaded ahead by count
 constexpr int kScatterChunks = 8; // and by scatter (measured best for each)
 constexpr int kBallotShards = kFewShards; // compare-based owners, one ballot per destination
@@ -212,7 +212,7 @@ __device__ __forceinline__ int xcd_run_block(int b, int n)
 // count's histogram row per bag: 8 entries for up to 8 destinations (an
 // index by shift), else G.
 __host__ __device__ inline int count_stride(int G) { return G <= kFewShards ? kFewShards : G; }
-__host__ __device__ inline size_t count_wave_bytes(int G, int bags) { return (size_t)4 * (G <= kFastShards ? count_stride(G) * bags : G); }
+__host__ __device__ inline size_t count_wave_bytes(int G, int bags) { return (size_t)4 * count_stride(G) * bags; }
 __host__ __device__ inline size_t count_lds_bytes(int G, int bags) { return (size_t)(G + 1) * 8 + kWavesPerBlock * count_wave_bytes(G, bags); }
 __host__ __device__ inline size_t scatter_lds_bytes(int G) { return (size_t)(G + 1) * 8 + (size_t)kWavesPerBlock * G * 8; }
 
@@ -347,7 +347,7 @@ __global__ __launch_bounds__(kBlock) void eb_bucket_count(const BucketArgs a)
     if (p0 == 0)
         for (int g = lane; g < G; g += kWave) a.out_offsets[(int64_t)g * row] = 0;
 
-    if (contiguous && G <= kFastShards) {
+    if (contiguous) {
         const uint64_t bags = __ballot(lane < nb);
         for (int x = lane; x < kBags * count_stride(G); x += kWave) hist[x] = 0;
         wave_sync_lds();
@@ -356,9 +356,13 @@ __global__ __launch_bounds__(kBlock) void eb_bucket_count(const BucketArgs a)
         else
             count_chunks<false>(a, bnd, FewBounds{}, hist, lane, s, bags, S, E);
         wave_sync_lds();
+        // Entry x of the histogram's transpose: bag x % kBags, destination
+        // x / kBags; a store covers 64 / kBags rows, kBags bags of each.
         const int stride = count_stride(G);
-        for (int g = 0; g < G; ++g)
-            if (lane < nb) a.out_offsets[(int64_t)g * row + p0 + lane + 1] = hist[lane * stride + g];
+        for (int x = lane; x < kBags * G; x += kWave) {
+            const int j = x & (kBags - 1), g = x / kBags;
+            if (j < nb) a.out_offsets[(int64_t)g * row + p0 + j + 1] = hist[j * stride + g];
+        }
         return;
     }
     // Any offsets, any G: one bag at a time.
@@ -422,8 +426,10 @@ struct ScanArgs {
 };
 
 // Pass 2c adds up the earlier tile sums itself (no pass 2b) while every
-// workgroup reads at most this many of them.
-constexpr int64_t kFusedScanMax = 16384;
+// workgroup reads at most this many of them: a row's first tile reads all
+// earlier rows' sums (at most 1 MB, from L2), still far quicker than one
+// workgroup scanning them all in sequence.
+constexpr int64_t kFusedScanMax = 131072;
 
 // The scan also keeps every kStartStride-th entry of each row in a compact
 // array, where the scatter's waves (kBagsPerWave bags each) find their first
@@ -432,7 +438,6 @@ constexpr int kStartStride = 16;
 static_assert(kScanTile % kStartStride == 0 && kBlock % kStartStride == 0, "scan tiles start at multiples of the stride");
 
 constexpr int kScanPer = kScanTile / kBlock; // counts per thread in a tile
-constexpr int kPrefixRegs = 16;              // tile sums per thread held in registers
 static_assert(kScanTile % kBlock == 0, "scan tile");
 
 // Pass 2a: sum of every tile (entries 1 + k*kScanTile ... of row g); all of a
@@ -461,7 +466,9 @@ __global__ __launch_bounds__(kBlock) void eb_scan_tile_sums(const ScanArgs a)
 // Pass 2b: the tile sums of all rows, row after row, as one sequence: its
 // exclusive scan at a row's first tile is that destination's segment start,
 // and the scan minus it is the tile's prefix within its row (written back in
-// place).  One workgroup; every thread takes a contiguous run of tiles.
+// place).  One workgroup; every thread takes a contiguous run of tiles.  Run
+// only beyond kFusedScanMax tile sums, or to fill the outputs of a batch
+// without bags.
 __global__ __launch_bounds__(kBlock) void eb_scan_tile_prefix(const ScanArgs a)
 {
     __shared__ int64_t seg[kMaxShards];
@@ -478,47 +485,6 @@ __global__ __launch_bounds__(kBlock) void eb_scan_tile_prefix(const ScanArgs a)
     const int64_t per = (n + kBlock - 1) / kBlock;
     const int64_t lo = std::min<int64_t>(n, threadIdx.x * per);
     const int64_t hi = std::min<int64_t>(n, lo + per);
-    if (per <= kPrefixRegs) {
-        // Few tiles (the usual case): the thread's run stays in registers,
-        // its loads all in flight at once, and the row is tracked by
-        // counting rather than dividing.
-        int64_t v[kPrefixRegs];
-        const int cnt = (int)(hi - lo);
-#pragma unroll
-        for (int j = 0; j < kPrefixRegs; ++j) v[j] = j < cnt ? ts[lo + j] : 0;
-        int64_t sum = 0;
-#pragma unroll
-        for (int j = 0; j < kPrefixRegs; ++j) sum += v[j];
-        int64_t total;
-        const int64_t before = block_inclusive_scan(sum, &total) - sum;
-        const int r0 = (int)(lo / a.ntiles);
-        const int c0 = (int)(lo - (int64_t)r0 * a.ntiles);
-        int64_t run = before;
-        int r = r0, c = c0;
-#pragma unroll
-        for (int j = 0; j < kPrefixRegs; ++j) {
-            if (j < cnt) {
-                if (c == 0) seg[r] = run;
-                run += v[j];
-                if (++c == a.ntiles) { c = 0; ++r; }
-            }
-        }
-        __syncthreads();
-        run = before;
-        r = r0;
-        c = c0;
-#pragma unroll
-        for (int j = 0; j < kPrefixRegs; ++j) {
-            if (j < cnt) {
-                ts[lo + j] = run - seg[r];
-                run += v[j];
-                if (++c == a.ntiles) { c = 0; ++r; }
-            }
-        }
-        for (int g = threadIdx.x; g < a.G; g += kBlock) a.segments[g] = seg[g];
-        if (threadIdx.x == 0) a.segments[a.G] = total;
-        return;
-    }
     int64_t sum = 0;
     for (int64_t i = lo; i < hi; ++i) sum += ts[i];
     int64_t total;
@@ -737,6 +703,46 @@ __device__ __forceinline__ void scatter_mid_pass(const BucketArgs &a, const int6
         if ((uint64_t)pos[u] < (uint64_t)a.out_cap) a.out_indices[pos[u]] = id[u];
 }
 
+// One pass of the scatter for contiguous bags and more than 64 destinations:
+// owners by binary search, ranks from ballots of the owner's nbits bits, and
+// each destination's running slot in the wave's LDS array next[] (read by
+// every lane of the owner, advanced by the first of them).
+template <bool kFull>
+__device__ __forceinline__ void scatter_many_pass(const BucketArgs &a, const int64_t *bnd, int64_t *next, int nbits,
+                                                  int lane, int64_t k0, int R)
+{
+    const int64_t *src = a.indices + k0 + lane;
+    int64_t id[kScatterChunks];
+#pragma unroll
+    for (int u = 0; u < kScatterChunks; ++u)
+        id[u] = (kFull || lane_bit(lanes_below(R - u * kWave))) ? __builtin_nontemporal_load(src + u * kWave) : 0;
+    int64_t pos[kScatterChunks];
+#pragma unroll
+    for (int u = 0; u < kScatterChunks; ++u) {
+        const bool in = kFull || lane_bit(lanes_below(R - u * kWave));
+        const int g = in ? owner_of(bnd, a.G, id[u]) : -1;
+        const bool ok = g >= 0;
+        const uint64_t valid = __ballot(ok);
+        uint32_t same_lo = (uint32_t)valid, same_hi = (uint32_t)(valid >> 32);
+        for (int i = 0; i < nbits; ++i) {
+            const uint64_t b = __ballot(ok && ((g >> i) & 1));
+            const uint32_t n = ((g >> i) & 1) ? 0u : ~0u;
+            same_lo &= (uint32_t)b ^ n;
+            same_hi &= (uint32_t)(b >> 32) ^ n;
+        }
+        const int rank = (int)__builtin_amdgcn_mbcnt_hi(same_hi, __builtin_amdgcn_mbcnt_lo(same_lo, 0u));
+        const int64_t base = ok ? next[g] : 0;
+        wave_sync_lds(); // every lane has its base before any slot advances
+        if (ok && rank == 0) next[g] = base + __popc(same_lo) + __popc(same_hi);
+        wave_sync_lds();
+        pos[u] = ok ? base + rank : -1;
+    }
+    __builtin_amdgcn_sched_barrier(0); // keep the stores after all ranking
+#pragma unroll
+    for (int u = 0; u < kScatterChunks; ++u)
+        if ((uint64_t)pos[u] < (uint64_t)a.out_cap) a.out_indices[pos[u]] = id[u];
+}
+
 template <int kBits>
 __device__ __forceinline__ void scatter_mid(const BucketArgs &a, const int64_t *bnd, int lane, int64_t slot, int64_t S,
                                             int64_t E)
@@ -815,20 +821,20 @@ __global__ __launch_bounds__(kBlock) void eb_bucket_scatter(const BucketArgs a)
         return;
     }
     if (contiguous) {
-        for (int g = lane; g < G; g += kWave) next[g] = a.segments[g] + a.out_offsets[(int64_t)g * row + p0];
+        // More than 64 destinations: slots in LDS, ranks from ballots of the
+        // owners' bits.
+        for (int g = lane; g < G; g += kWave)
+            next[g] = a.segments[g] + (p0 % kStartStride == 0 ? a.starts[(int64_t)g * a.nq + p0 / kStartStride]
+                                                              : a.out_offsets[(int64_t)g * row + p0]);
         wave_sync_lds();
-        for (int64_t k0 = S; k0 < E; k0 += kScatterChunks * kWave) {
-            int64_t id[kScatterChunks];
-#pragma unroll
-            for (int u = 0; u < kScatterChunks; ++u) {
-                const int64_t k = k0 + u * kWave + lane;
-                id[u] = k < E ? __builtin_nontemporal_load(a.indices + k) : 0;
-            }
-#pragma unroll
-            for (int u = 0; u < kScatterChunks; ++u) {
-                const int64_t k = k0 + u * kWave + lane;
-                scatter_chunk(a, next, lane, k < E ? owner_of(bnd, G, id[u]) : -1, id[u]);
-            }
+        const int nbits = 32 - __builtin_clz((unsigned)(G - 1));
+        constexpr int kPass = kScatterChunks * kWave;
+        for (int64_t k0 = S; k0 < E; k0 += kPass) {
+            const int R = __builtin_amdgcn_readfirstlane((int)min<int64_t>(E - k0, (int64_t)kPass));
+            if (R == kPass)
+                scatter_many_pass<true>(a, bnd, next, nbits, lane, k0, R);
+            else
+                scatter_many_pass<false>(a, bnd, next, nbits, lane, k0, R);
         }
         return;
     }
@@ -908,11 +914,15 @@ int64_t scan_tiles(int64_t TB) { return std::max<int64_t>(1, (TB + kScanTile - 1
 
 // Bags per count wave for T*B bags in all and G destinations (see
 // kCountWavesMin).  Only the owner-mask path (G <= 8, 8 histogram entries per
-// bag) gains from longer waves; with more destinations each bag's histogram
-// row, or the bag-at-a-time loop, makes them slower.
+// bag) gains from longer waves; beyond 8 destinations a wave takes 16 bags,
+// fewer when their [bag][destination] histogram would pass kCountHistBytes.
 int count_bags(int64_t TB, int G)
 {
-    if (G > kFewShards) return 16;
+    if (G > kFewShards) {
+        int bags = 16;
+        while (bags > 2 && count_wave_bytes(G, bags) > (size_t)kCountHistBytes) bags /= 2;
+        return bags;
+    }
     for (int bags = 64; bags > 16; bags /= 2)
         if (TB / bags >= kCountWavesMin) return bags;
     return 16;
@@ -991,8 +1001,12 @@ int bucketize_impl(int32_t T, int64_t B, int32_t G, const int64_t *bounds, const
 
     if (TB > 0) {
         void *args[] = {&ba};
-        const void *count = cbags == 64 ? (const void *)eb_bucket_count<64>
-                            : cbags == 32 ? (const void *)eb_bucket_count<32> : (const void *)eb_bucket_count<16>;
+        const void *count = cbags == 64   ? (const void *)eb_bucket_count<64>
+                            : cbags == 32 ? (const void *)eb_bucket_count<32>
+                            : cbags == 16 ? (const void *)eb_bucket_count<16>
+                            : cbags == 8  ? (const void *)eb_bucket_count<8>
+                            : cbags == 4  ? (const void *)eb_bucket_count<4>
+                                          : (const void *)eb_bucket_count<2>;
         hipError_t err = hipLaunchKernel(count, dim3((unsigned)(T * cbpt)), dim3(kBlock), args,
                                          count_lds_bytes(G, cbags), st);
         if (err != hipSuccess) return fail(EB_ERR_HIP, "eb_bucketize: %s", hipGetErrorString(err));
