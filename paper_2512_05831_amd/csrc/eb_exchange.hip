@@ -172,7 +172,7 @@ constexpr int kBagsPerWave = 16;
 constexpr int kBagsPerBlock = kBagsPerWave * kWavesPerBlock;
 static_assert(kBagsPerWave <= kWave && (kBagsPerWave & (kBagsPerWave - 1)) == 0, "bags per wave");
 constexpr int64_t kCountWavesMin = 4608; // 18 per compute unit
-constexpr int kCountHistBytes = 8192; // count's per-wave [bag][destination] histogram, at most
+constexpr int kCountHistBytes = 32768; // count's per-wave [bag][destination] histogram, at most
 constexpr int kCountChunks = 4;   // 64-id chunks loaded ahead by count
 constexpr int kScatterChunks = 8; // and by scatter (measured best for each)
 constexpr int kBallotShards = kFewShards; // compare-based owners, one ballot per destination
@@ -914,15 +914,18 @@ int64_t scan_tiles(int64_t TB) { return std::max<int64_t>(1, (TB + kScanTile - 1
 
 // Bags per count wave for T*B bags in all and G destinations (see
 // kCountWavesMin).  Only the owner-mask path (G <= 8, 8 histogram entries per
-// bag) gains from longer waves; beyond 8 destinations a wave takes 16 bags,
-// fewer when their [bag][destination] histogram would pass kCountHistBytes.
+// bag) gains from longer waves; 9 to 64 destinations take 16 bags, more take
+// 8, fewer when their [bag][destination] histogram would pass
+// kCountHistBytes (measured: 8 bags beat 16 at 200 destinations, and at 1024
+// beat 2 or 4 even though the histograms then limit a compute unit to 4 waves).
 int count_bags(int64_t TB, int G)
 {
-    if (G > kFewShards) {
-        int bags = 16;
+    if (G > kWave) {
+        int bags = 8;
         while (bags > 2 && count_wave_bytes(G, bags) > (size_t)kCountHistBytes) bags /= 2;
         return bags;
     }
+    if (G > kFewShards) return 16;
     for (int bags = 64; bags > 16; bags /= 2)
         if (TB / bags >= kCountWavesMin) return bags;
     return 16;
