@@ -283,10 +283,11 @@ def _time_launches(torch, stream, fn, K, W):
     return ev0.elapsed_time(ev1) * 1e3 / K
 
 
-def exchange_bench(torch, dev, eb, K, W):
+def exchange_bench(torch, dev, eb, K, W, G=8):
     """The row-wise exchange's local kernels at the sizes of the skewed
     workloads split over 8 GPUs by rows.  bucketize: the 26-table,
-    16384-bag Zipf(1.05) batch (21.1 M ids) into 8 row blocks per table.
+    16384-bag Zipf(1.05) batch (21.1 M ids) into G row blocks per table
+    (``--destinations``, default 8).
     sum_partials: the 400M-id shard workload's bags, 65536 / 8 = 8192 per GPU,
     D = 256, 8 partial blocks.  One JSON line each: mean launch time (HIP
     events around K launches) and algorithmic bytes against 8 TB/s."""
@@ -295,7 +296,6 @@ def exchange_bench(torch, dev, eb, K, W):
     w = wl.config(3)
     off = w.offsets()
     idx = w.indices(off)
-    G = 8
     bounds = np.array([[g * w.rows // G for g in range(G + 1)]] * w.T, dtype=np.int64)
     d_b = torch.from_numpy(bounds).to(dev)
     d_i = torch.from_numpy(idx).to(dev)
@@ -319,22 +319,23 @@ def exchange_bench(torch, dev, eb, K, W):
                       "us_per_call": round(us, 1), "ids_per_s": idx.size / us * 1e6,
                       "algorithmic_bytes": by, "algorithmic_GBps": round(by / us / 1e3, 1),
                       "frac_of_8TBps": round(by / us / 1e3 / HBM_PEAK_GBPS, 4),
-                      # count, tile sums, (tile prefix when over 16384 tile sums,) tile scan, scatter
-                      "kernels_per_call": 4 if G * -(-TB // 2048) <= 16384 else 5}), flush=True)
+                      # count, tile sums, (tile prefix when over 131072 tile sums,) tile scan, scatter
+                      "kernels_per_call": 4 if G * -(-TB // 2048) <= 131072 else 5}), flush=True)
     del d_i, out_idx
-    B, T, D = 65536 // G, 1, 256
+    Gp = 8  # the partial blocks of 8 GPUs, whatever --destinations says
+    B, T, D = 65536 // Gp, 1, 256
     # six receive buffers cycled (400 MB), so the last-level cache cannot hold the input
-    parts = [torch.randn((G, B, T * D), dtype=torch.float32, device=dev) for _ in range(6)]
+    parts = [torch.randn((Gp, B, T * D), dtype=torch.float32, device=dev) for _ in range(6)]
     out = torch.empty((B, T * D), dtype=torch.float32, device=dev)
     turn = [0]
 
     def reduce():
         p = parts[turn[0] % len(parts)]
         turn[0] += 1
-        eb.eb_sum_partials(G, p.data_ptr(), B, T, D, None, 0, out.data_ptr(), stream.cuda_stream)
+        eb.eb_sum_partials(Gp, p.data_ptr(), B, T, D, None, 0, out.data_ptr(), stream.cuda_stream)
     us = _time_launches(torch, stream, reduce, K * 4, W)
-    by = G * B * T * D * 4 + B * T * D * 4
-    print(json.dumps({"kernel": "eb_sum_partials", "workload": f"{G}x{B}x{T * D}-f32",
+    by = Gp * B * T * D * 4 + B * T * D * 4
+    print(json.dumps({"kernel": "eb_sum_partials", "workload": f"{Gp}x{B}x{T * D}-f32",
                       "us_per_call": round(us, 1), "algorithmic_bytes": by,
                       "algorithmic_GBps": round(by / us / 1e3, 1),
                       "frac_of_8TBps": round(by / us / 1e3 / HBM_PEAK_GBPS, 4)}), flush=True)
@@ -679,6 +680,8 @@ def parser() -> argparse.ArgumentParser:
                     help="replay the steps from a captured HIP graph (launch-bound workloads)")
     ap.add_argument("--exchange", action="store_true",
                     help="time the row-wise exchange kernels instead (bucketize, sum_partials)")
+    ap.add_argument("--destinations", type=int, default=8, metavar="G",
+                    help="with --exchange: bucketize into G row blocks per table (1..1024)")
     ap.add_argument("--rw-pipeline", type=int, default=0, metavar="G",
                     help="time one GPU's compute in a row-wise step of the chosen workload split "
                          "over G GPUs instead (bucketize, gather of the received ids, sum of partials)")
@@ -761,7 +764,7 @@ def main():
         paper_sweep(torch, dev, eb, args.index_type)
         return
     if args.exchange:
-        exchange_bench(torch, dev, eb, args.steps, args.warmup)
+        exchange_bench(torch, dev, eb, args.steps, args.warmup, args.destinations)
         return
     if args.rw_pipeline:
         rw_pipeline_bench(torch, dev, eb, pick_workload(args), args.rw_pipeline, args.steps, args.warmup,
