@@ -23,7 +23,7 @@
 //                destinations the most that leave at least 4608 waves, else
 //                16; each XCD one contiguous run of workgroups); each id's
 //                owner by
-//                comparisons with the table's block bounds (up to 8 blocks:
+//                comparisons with the table's block bounds (up to 16 blocks:
 //                a search tree evaluated as wave-wide lane masks) or by
 //                binary search over them (staged in LDS); for ordinary CSR
 //                offsets and up to 64 destinations the wave streams its whole
@@ -162,6 +162,67 @@ __device__ __forceinline__ int few_bits(const FewMasks &o)
     return (lane_bit(o.b0) ? kScale : 0) | (lane_bit(o.b1) ? 2 * kScale : 0) | (lane_bit(o.b2) ? 4 * kScale : 0);
 }
 
+// The same search tree one level deeper, for 9 to 16 blocks: 15 inner bounds
+// (unused ones past every id) and the owner's four bits.  Level l of the tree
+// decides bit 3 - l; its 2^l candidate bound masks are those at (2p + 1) *
+// 2^(3 - l) - 1 for the 2^l values p of the bits above, and the bits already
+// decided select among them, the lowest of them first.
+constexpr int kTreeShards = 16;
+constexpr int kTreeBits = 4;
+
+struct TreeBounds {
+    int64_t lo, hi;
+    int64_t inner[kTreeShards - 1];
+};
+
+__device__ __forceinline__ TreeBounds tree_bounds(const int64_t *bnd, int G)
+{
+    TreeBounds b;
+    b.lo = bnd[0];
+    b.hi = bnd[G];
+#pragma unroll
+    for (int j = 1; j < kTreeShards; ++j) b.inner[j - 1] = j < G ? bnd[j] : INT64_MAX;
+    return b;
+}
+
+struct TreeMasks {
+    uint64_t valid;        // lanes of `in` with lo <= i < hi
+    uint64_t b[kTreeBits]; // lanes whose owner has bit k set
+};
+
+__device__ __forceinline__ TreeMasks tree_owner_masks(const TreeBounds &t, int64_t i, uint64_t in)
+{
+    uint64_t m[kTreeShards - 1];
+#pragma unroll
+    for (int j = 0; j < kTreeShards - 1; ++j) m[j] = __ballot(i >= t.inner[j]);
+    TreeMasks o;
+    o.valid = in & __ballot(i >= t.lo) & __ballot(i < t.hi);
+#pragma unroll
+    for (int l = 0; l < kTreeBits; ++l) {
+        const int bit = kTreeBits - 1 - l;
+        uint64_t c[kTreeShards / 2];
+#pragma unroll
+        for (int p = 0; p < (1 << l); ++p) c[p] = m[((2 * p + 1) << bit) - 1];
+#pragma unroll
+        for (int q = 0; q < l; ++q) {
+            const uint64_t sel = o.b[bit + 1 + q];
+#pragma unroll
+            for (int p = 0; p < (1 << (l - q - 1)); ++p) c[p] = (sel & c[2 * p + 1]) | (~sel & c[2 * p]);
+        }
+        o.b[bit] = c[0];
+    }
+    return o;
+}
+
+template <int kScale>
+__device__ __forceinline__ int tree_bits(const TreeMasks &o)
+{
+    int v = 0;
+#pragma unroll
+    for (int k = 0; k < kTreeBits; ++k) v |= lane_bit(o.b[k]) ? kScale << k : 0;
+    return v;
+}
+
 // A scatter wave takes kBagsPerWave consecutive bags of one table; a block 4
 // waves.  Few bags per wave keep many waves (and their id loads) in flight.
 // A count wave takes 16, 32 or 64 bags (up to 8 destinations; 16 beyond):
@@ -211,7 +272,7 @@ __device__ __forceinline__ int xcd_run_block(int b, int n)
 // Dynamic LDS: the table's G+1 bounds, then one area per wave.
 // count's histogram row per bag: 8 entries for up to 8 destinations (an
 // index by shift), else G.
-__host__ __device__ inline int count_stride(int G) { return G <= kFewShards ? kFewShards : G; }
+__host__ __device__ inline int count_stride(int G) { return G <= kFewShards ? kFewShards : G <= kTreeShards ? kTreeShards : G; }
 __host__ __device__ inline size_t count_wave_bytes(int G, int bags) { return (size_t)4 * count_stride(G) * bags; }
 __host__ __device__ inline size_t count_lds_bytes(int G, int bags) { return (size_t)(G + 1) * 8 + kWavesPerBlock * count_wave_bytes(G, bags); }
 __host__ __device__ inline size_t scatter_lds_bytes(int G) { return (size_t)(G + 1) * 8 + (size_t)kWavesPerBlock * G * 8; }
@@ -267,9 +328,12 @@ __device__ __forceinline__ void wave_sync_lds()
 // One pass of count's loop: the ids at k0 + u * 64 + lane, the first R of
 // them (all kCountChunks * 64 when kFull, the usual case, which then needs
 // no tail masks).
-template <bool kFew, bool kFull>
-__device__ __forceinline__ void count_pass(const BucketArgs &a, const int64_t *bnd, const FewBounds &fb, int *hist,
-                                           int lane, int64_t s, uint64_t bags, int64_t k0, int R)
+// kOwners: 8 (owners by the 3-bit tree), 16 (the 4-bit tree), or 0 (by
+// binary search over the bounds in LDS).
+template <int kOwners, bool kFull>
+__device__ __forceinline__ void count_pass(const BucketArgs &a, const int64_t *bnd, const FewBounds &fb,
+                                           const TreeBounds &tb, int *hist, int lane, int64_t s, uint64_t bags,
+                                           int64_t k0, int R)
 {
     const int64_t *src = a.indices + k0 + lane;
     int64_t id[kCountChunks];
@@ -292,12 +356,15 @@ __device__ __forceinline__ void count_pass(const BucketArgs &a, const int64_t *b
             inside &= inside - 1;
         }
         const uint64_t in = kFull ? ~0ull : lanes_below(R - u * kWave);
-        if constexpr (kFew) {
+        if constexpr (kOwners == kFewShards) {
             const FewMasks o = few_owner_masks(fb, id[u], in);
             if (lane_bit(o.valid)) atomicAdd(&hist[l * kFewShards + few_bits<1>(o)], 1);
+        } else if constexpr (kOwners == kTreeShards) {
+            const TreeMasks o = tree_owner_masks(tb, id[u], in);
+            if (lane_bit(o.valid)) atomicAdd(&hist[l * kTreeShards + tree_bits<1>(o)], 1);
         } else if (lane_bit(in)) {
             const int g = owner_of(bnd, a.G, id[u]);
-            if (g >= 0) atomicAdd(&hist[l * a.G + g], 1);
+            if (g >= 0) atomicAdd(&hist[l * count_stride(a.G) + g], 1);
         }
     }
 }
@@ -305,21 +372,25 @@ __device__ __forceinline__ void count_pass(const BucketArgs &a, const int64_t *b
 // count's loop over the wave's ids [S, E) for contiguous bags (bag l of the
 // wave starts at lane l's s; bags = lanes holding a bag): adds each id with
 // an owner to hist[bag * count_stride(G) + owner].
-template <bool kFew>
-__device__ __forceinline__ void count_chunks(const BucketArgs &a, const int64_t *bnd, const FewBounds &fb, int *hist,
-                                             int lane, int64_t s, uint64_t bags, int64_t S, int64_t E)
+template <int kOwners>
+__device__ __forceinline__ void count_chunks(const BucketArgs &a, const int64_t *bnd, const FewBounds &fb,
+                                             const TreeBounds &tb, int *hist, int lane, int64_t s, uint64_t bags,
+                                             int64_t S, int64_t E)
 {
     constexpr int kPass = kCountChunks * kWave;
     for (int64_t k0 = S; k0 < E; k0 += kPass) {
         const int R = __builtin_amdgcn_readfirstlane((int)min<int64_t>(E - k0, (int64_t)kPass));
         if (R == kPass)
-            count_pass<kFew, true>(a, bnd, fb, hist, lane, s, bags, k0, R);
+            count_pass<kOwners, true>(a, bnd, fb, tb, hist, lane, s, bags, k0, R);
         else
-            count_pass<kFew, false>(a, bnd, fb, hist, lane, s, bags, k0, R);
+            count_pass<kOwners, false>(a, bnd, fb, tb, hist, lane, s, bags, k0, R);
     }
 }
 
-template <int kBags>
+// kOwners: how the instantiation finds owners (8: 3-bit compare tree, 16:
+// 4-bit tree, 0: binary search); one instantiation per method and wave size,
+// so that each keeps only its own path's registers.
+template <int kBags, int kOwners>
 __global__ __launch_bounds__(kBlock) void eb_bucket_count(const BucketArgs a)
 {
     static_assert(kBags <= kWave && (kBags & (kBags - 1)) == 0, "bags per count wave");
@@ -351,10 +422,12 @@ __global__ __launch_bounds__(kBlock) void eb_bucket_count(const BucketArgs a)
         const uint64_t bags = __ballot(lane < nb);
         for (int x = lane; x < kBags * count_stride(G); x += kWave) hist[x] = 0;
         wave_sync_lds();
-        if (G <= kFewShards)
-            count_chunks<true>(a, bnd, few_bounds(bnd, G), hist, lane, s, bags, S, E);
+        if constexpr (kOwners == kFewShards)
+            count_chunks<kFewShards>(a, bnd, few_bounds(bnd, G), TreeBounds{}, hist, lane, s, bags, S, E);
+        else if constexpr (kOwners == kTreeShards)
+            count_chunks<kTreeShards>(a, bnd, FewBounds{}, tree_bounds(bnd, G), hist, lane, s, bags, S, E);
         else
-            count_chunks<false>(a, bnd, FewBounds{}, hist, lane, s, bags, S, E);
+            count_chunks<0>(a, bnd, FewBounds{}, TreeBounds{}, hist, lane, s, bags, S, E);
         wave_sync_lds();
         // Entry x of the histogram's transpose: bag x % kBags, destination
         // x / kBags; a store covers 64 / kBags rows, kBags bags of each.
@@ -657,7 +730,46 @@ __device__ __forceinline__ void scatter_few_pass(const BucketArgs &a, const FewB
         if ((uint64_t)pos[u] < (uint64_t)a.out_cap) a.out_indices[pos[u]] = id[u];
 }
 
-// One pass of the scatter for contiguous bags and 9 to 64 destinations: as
+// scatter_few_pass for 9 to 16 destinations: owners from the 4-bit tree.
+template <bool kFull>
+__device__ __forceinline__ void scatter_tree_pass(const BucketArgs &a, const TreeBounds &tb, int lane,
+                                                  const uint32_t (&lbit)[kTreeBits], int64_t &slot, int64_t k0, int R)
+{
+    const int64_t *src = a.indices + k0 + lane;
+    int64_t id[kScatterChunks];
+#pragma unroll
+    for (int u = 0; u < kScatterChunks; ++u)
+        id[u] = (kFull || lane_bit(lanes_below(R - u * kWave))) ? __builtin_nontemporal_load(src + u * kWave) : 0;
+    int64_t pos[kScatterChunks];
+#pragma unroll
+    for (int u = 0; u < kScatterChunks; ++u) {
+        const TreeMasks o = tree_owner_masks(tb, id[u], kFull ? ~0ull : lanes_below(R - u * kWave));
+        const bool ok = lane_bit(o.valid);
+        uint32_t same_lo = (uint32_t)o.valid, same_hi = (uint32_t)(o.valid >> 32);
+        uint32_t own_lo = same_lo, own_hi = same_hi;
+#pragma unroll
+        for (int k = 0; k < kTreeBits; ++k) {
+            const uint32_t n = lane_bit(~o.b[k]) ? ~0u : 0u;
+            same_lo &= (uint32_t)o.b[k] ^ n;
+            same_hi &= (uint32_t)(o.b[k] >> 32) ^ n;
+            own_lo &= (uint32_t)o.b[k] ^ lbit[k];
+            own_hi &= (uint32_t)(o.b[k] >> 32) ^ lbit[k];
+        }
+        const int rank = (int)__builtin_amdgcn_mbcnt_hi(same_hi, __builtin_amdgcn_mbcnt_lo(same_lo, 0u));
+        const int from = tree_bits<4>(o);
+        const int base_lo = __builtin_amdgcn_ds_bpermute(from, (int)(uint32_t)slot);
+        const int base_hi = __builtin_amdgcn_ds_bpermute(from, (int)(slot >> 32));
+        const int64_t base = ((int64_t)base_hi << 32) | (uint32_t)base_lo;
+        pos[u] = ok ? base + rank : -1;
+        slot += __popc(own_lo) + __popc(own_hi);
+    }
+    __builtin_amdgcn_sched_barrier(0); // keep the stores after all ranking
+#pragma unroll
+    for (int u = 0; u < kScatterChunks; ++u)
+        if ((uint64_t)pos[u] < (uint64_t)a.out_cap) a.out_indices[pos[u]] = id[u];
+}
+
+// One pass of the scatter for contiguous bags and 17 to 64 destinations: as
 // scatter_few_pass, with each id's owner found by binary search over the
 // bounds in LDS and ranked through kBits ballots of the owner's bits (lane d
 // < G holds destination d's slot; lbit[i] is the complement of the lane's
@@ -760,6 +872,13 @@ __device__ __forceinline__ void scatter_mid(const BucketArgs &a, const int64_t *
     }
 }
 
+// kOwners: the most destinations the instantiation ranks in one chunk's
+// ballots (8: 3-bit compare tree; 16: 4-bit tree; 32 / 64: binary search and
+// 5 / 6 bit ballots; kMaxShards: binary search, slots in LDS).  One
+// instantiation per method keeps each one's registers, and so its occupancy,
+// to what its own path needs; the bag-at-a-time path for out-of-order
+// offsets is in all of them.
+template <int kOwners>
 __global__ __launch_bounds__(kBlock) void eb_bucket_scatter(const BucketArgs a)
 {
     extern __shared__ int64_t lds[];
@@ -790,7 +909,7 @@ __global__ __launch_bounds__(kBlock) void eb_bucket_scatter(const BucketArgs a)
     __syncthreads();
     if (!live) return; // no block-wide barrier follows
     const bool contiguous = wave_bags(a, nb, lane, s, e, S, E);
-    if (contiguous && G <= kBallotShards) {
+    if (kOwners == kBallotShards && contiguous) {
         // Contiguous bags, few destinations: ranks from ballots of the
         // owners' bits (scatter_few_pass).
         const FewBounds fb = few_bounds(bnd, G);
@@ -807,20 +926,34 @@ __global__ __launch_bounds__(kBlock) void eb_bucket_scatter(const BucketArgs a)
         }
         return;
     }
-    if (contiguous && G <= kWave) {
+    if (kOwners > kBallotShards && kOwners <= kWave && contiguous) {
         // Contiguous bags, 9 to 64 destinations: within a destination, (bag,
         // position) order is position order, so one running slot per
         // destination (lane g keeps destination g's) suffices, and ballots of
-        // the owners' 4, 5 or 6 bits rank a whole chunk at once.
-        if (G <= 16)
-            scatter_mid<4>(a, bnd, lane, first_slot, S, E);
-        else if (G <= 32)
+        // the owners' 4, 5 or 6 bits rank a whole chunk at once (owners by
+        // the 4-bit tree up to 16 destinations, else by binary search).
+        if constexpr (kOwners == kTreeShards) {
+            const TreeBounds tb = tree_bounds(bnd, G);
+            uint32_t lbit[kTreeBits];
+#pragma unroll
+            for (int k = 0; k < kTreeBits; ++k) lbit[k] = (uint32_t)((lane >> k) & 1) - 1u;
+            int64_t slot = first_slot;
+            constexpr int kPass = kScatterChunks * kWave;
+            for (int64_t k0 = S; k0 < E; k0 += kPass) {
+                const int R = __builtin_amdgcn_readfirstlane((int)min<int64_t>(E - k0, (int64_t)kPass));
+                if (R == kPass)
+                    scatter_tree_pass<true>(a, tb, lane, lbit, slot, k0, R);
+                else
+                    scatter_tree_pass<false>(a, tb, lane, lbit, slot, k0, R);
+            }
+        } else if constexpr (kOwners == 32) {
             scatter_mid<5>(a, bnd, lane, first_slot, S, E);
-        else
+        } else if constexpr (kOwners == kWave) {
             scatter_mid<6>(a, bnd, lane, first_slot, S, E);
+        }
         return;
     }
-    if (contiguous) {
+    if (kOwners == kMaxShards && contiguous) {
         // More than 64 destinations: slots in LDS, ranks from ballots of the
         // owners' bits.
         for (int g = lane; g < G; g += kWave)
@@ -932,6 +1065,30 @@ int count_bags(int64_t TB, int G)
 }
 int64_t start_entries(int64_t TB) { return TB / kStartStride + 1; }
 
+// The count and scatter instantiations for G destinations (count_bags bags
+// per count wave).
+const void *count_kernel(int G, int bags)
+{
+    if (G <= kFewShards)
+        return bags == 64 ? (const void *)eb_bucket_count<64, kFewShards>
+               : bags == 32 ? (const void *)eb_bucket_count<32, kFewShards>
+                            : (const void *)eb_bucket_count<16, kFewShards>;
+    if (G <= kTreeShards) return (const void *)eb_bucket_count<16, kTreeShards>;
+    return bags == 16  ? (const void *)eb_bucket_count<16, 0>
+           : bags == 8 ? (const void *)eb_bucket_count<8, 0>
+           : bags == 4 ? (const void *)eb_bucket_count<4, 0>
+                       : (const void *)eb_bucket_count<2, 0>;
+}
+
+const void *scatter_kernel(int G)
+{
+    return G <= kBallotShards  ? (const void *)eb_bucket_scatter<kBallotShards>
+           : G <= kTreeShards ? (const void *)eb_bucket_scatter<kTreeShards>
+           : G <= 32          ? (const void *)eb_bucket_scatter<32>
+           : G <= kWave       ? (const void *)eb_bucket_scatter<kWave>
+                              : (const void *)eb_bucket_scatter<kMaxShards>;
+}
+
 } // namespace
 
 namespace {
@@ -1004,12 +1161,7 @@ int bucketize_impl(int32_t T, int64_t B, int32_t G, const int64_t *bounds, const
 
     if (TB > 0) {
         void *args[] = {&ba};
-        const void *count = cbags == 64   ? (const void *)eb_bucket_count<64>
-                            : cbags == 32 ? (const void *)eb_bucket_count<32>
-                            : cbags == 16 ? (const void *)eb_bucket_count<16>
-                            : cbags == 8  ? (const void *)eb_bucket_count<8>
-                            : cbags == 4  ? (const void *)eb_bucket_count<4>
-                                          : (const void *)eb_bucket_count<2>;
+        const void *count = count_kernel(G, cbags);
         hipError_t err = hipLaunchKernel(count, dim3((unsigned)(T * cbpt)), dim3(kBlock), args,
                                          count_lds_bytes(G, cbags), st);
         if (err != hipSuccess) return fail(EB_ERR_HIP, "eb_bucketize: %s", hipGetErrorString(err));
@@ -1020,7 +1172,7 @@ int bucketize_impl(int32_t T, int64_t B, int32_t G, const int64_t *bounds, const
         if (err == hipSuccess)
             err = hipLaunchKernel((const void *)eb_scan_tiles, dim3(sa.ntiles, G), dim3(kBlock), sargs, 0, st);
         if (err == hipSuccess)
-            err = hipLaunchKernel((const void *)eb_bucket_scatter, dim3((unsigned)(T * bpt)), dim3(kBlock), args,
+            err = hipLaunchKernel(scatter_kernel(G), dim3((unsigned)(T * bpt)), dim3(kBlock), args,
                                   scatter_lds_bytes(G), st);
         if (err != hipSuccess) return fail(EB_ERR_HIP, "eb_bucketize: %s", hipGetErrorString(err));
     } else {
