@@ -107,12 +107,13 @@ def test_bucketize_edge_cases(device):
     check_bucketize(1, 4, idx, off, bounds, device)
 
 
-@pytest.mark.parametrize("G", [3, 8, 17])
+@pytest.mark.parametrize("G", [3, 8, 12, 16, 17, 64, 65])
 def test_bucketize_extreme_ids(G, device):
     """Bounds reaching both ends of int64 and ids at, just below and just
     above every bound (including INT64_MIN and INT64_MAX): the owner's
-    compares, the padding of unused bounds (up to 8 destinations) and the
-    binary search (more), against the oracle."""
+    compare trees and their padding of unused bounds (up to 8 and up to 16
+    destinations), the binary search with lane slots (up to 64) and with
+    slots in LDS (more), against the oracle."""
     lo64, hi64 = np.iinfo(np.int64).min, np.iinfo(np.int64).max
     g = np.random.default_rng(G)
     T, B = 3, 40
@@ -155,7 +156,7 @@ def check_split(bounds, idx, off, T, B, got):
                 assert all(any(v == w for w in it) for v in part), (t, b, d)
 
 
-@pytest.mark.parametrize("G", [2, 5, 8, 17])
+@pytest.mark.parametrize("G", [2, 5, 8, 9, 16, 17, 40, 100])
 def test_bucketize_arbitrary_bounds(G, device):
     """Bounds that are not sorted: the promises of check_split hold (the
     oracle's own split meets them too)."""
