@@ -223,6 +223,36 @@ __device__ __forceinline__ int tree_bits(const TreeMasks &o)
     return v;
 }
 
+// owner_of beyond 16 blocks, for the lanes of `in`: the first three steps of
+// the binary search at once, as the 3-bit compare tree over the first bounds
+// of the eighths [k G / 8, (k + 1) G / 8) of the blocks (every id's eighth is
+// the number of those bounds at or below it), then binary search within the
+// eighth from the bounds in LDS.  For non-decreasing bounds bnd[lo] <= i <
+// bnd[hi] holds for the eighth found, so the search ends at owner_of's block;
+// for any bounds the result stays in [0, G).
+__device__ __forceinline__ FewBounds eighth_bounds(const int64_t *bnd, int G)
+{
+    FewBounds b;
+    b.lo = bnd[0];
+    b.hi = bnd[G];
+#pragma unroll
+    for (int k = 1; k < kFewShards; ++k) b.inner[k - 1] = bnd[(k * G) >> 3];
+    return b;
+}
+
+__device__ __forceinline__ int owner_by_eighths(const int64_t *bnd, int G, const FewBounds &eb, int64_t i, uint64_t in)
+{
+    const FewMasks o = few_owner_masks(eb, i, in);
+    if (!lane_bit(o.valid)) return -1;
+    const int r = few_bits<1>(o);
+    int lo = (r * G) >> 3, hi = ((r + 1) * G) >> 3;
+    while (hi - lo > 1) {
+        const int mid = (lo + hi) >> 1;
+        if (bnd[mid] <= i) lo = mid; else hi = mid;
+    }
+    return lo;
+}
+
 // A scatter wave takes kBagsPerWave consecutive bags of one table; a block 4
 // waves.  Few bags per wave keep many waves (and their id loads) in flight.
 // A count wave takes 16, 32 or 64 bags (up to 8 destinations; 16 beyond):
@@ -362,8 +392,8 @@ __device__ __forceinline__ void count_pass(const BucketArgs &a, const int64_t *b
         } else if constexpr (kOwners == kTreeShards) {
             const TreeMasks o = tree_owner_masks(tb, id[u], in);
             if (lane_bit(o.valid)) atomicAdd(&hist[l * kTreeShards + tree_bits<1>(o)], 1);
-        } else if (lane_bit(in)) {
-            const int g = owner_of(bnd, a.G, id[u]);
+        } else {
+            const int g = owner_by_eighths(bnd, a.G, fb, id[u], in);
             if (g >= 0) atomicAdd(&hist[l * count_stride(a.G) + g], 1);
         }
     }
@@ -427,7 +457,7 @@ __global__ __launch_bounds__(kBlock) void eb_bucket_count(const BucketArgs a)
         else if constexpr (kOwners == kTreeShards)
             count_chunks<kTreeShards>(a, bnd, FewBounds{}, tree_bounds(bnd, G), hist, lane, s, bags, S, E);
         else
-            count_chunks<0>(a, bnd, FewBounds{}, TreeBounds{}, hist, lane, s, bags, S, E);
+            count_chunks<0>(a, bnd, eighth_bounds(bnd, G), TreeBounds{}, hist, lane, s, bags, S, E);
         wave_sync_lds();
         // Entry x of the histogram's transpose: bag x % kBags, destination
         // x / kBags; a store covers 64 / kBags rows, kBags bags of each.
@@ -775,7 +805,7 @@ __device__ __forceinline__ void scatter_tree_pass(const BucketArgs &a, const Tre
 // < G holds destination d's slot; lbit[i] is the complement of the lane's
 // bit i as an all-ones / zero mask).
 template <bool kFull, int kBits>
-__device__ __forceinline__ void scatter_mid_pass(const BucketArgs &a, const int64_t *bnd, int lane,
+__device__ __forceinline__ void scatter_mid_pass(const BucketArgs &a, const int64_t *bnd, const FewBounds &eb, int lane,
                                                  const uint32_t (&lbit)[kBits], int64_t &slot, int64_t k0, int R)
 {
     const int64_t *src = a.indices + k0 + lane;
@@ -786,8 +816,7 @@ __device__ __forceinline__ void scatter_mid_pass(const BucketArgs &a, const int6
     int64_t pos[kScatterChunks];
 #pragma unroll
     for (int u = 0; u < kScatterChunks; ++u) {
-        const bool in = kFull || lane_bit(lanes_below(R - u * kWave));
-        const int g = in ? owner_of(bnd, a.G, id[u]) : -1;
+        const int g = owner_by_eighths(bnd, a.G, eb, id[u], kFull ? ~0ull : lanes_below(R - u * kWave));
         const bool ok = g >= 0;
         const uint64_t valid = __ballot(ok);
         uint32_t same_lo = (uint32_t)valid, same_hi = (uint32_t)(valid >> 32);
@@ -820,8 +849,8 @@ __device__ __forceinline__ void scatter_mid_pass(const BucketArgs &a, const int6
 // each destination's running slot in the wave's LDS array next[] (read by
 // every lane of the owner, advanced by the first of them).
 template <bool kFull>
-__device__ __forceinline__ void scatter_many_pass(const BucketArgs &a, const int64_t *bnd, int64_t *next, int nbits,
-                                                  int lane, int64_t k0, int R)
+__device__ __forceinline__ void scatter_many_pass(const BucketArgs &a, const int64_t *bnd, const FewBounds &eb,
+                                                  int64_t *next, int nbits, int lane, int64_t k0, int R)
 {
     const int64_t *src = a.indices + k0 + lane;
     int64_t id[kScatterChunks];
@@ -831,8 +860,7 @@ __device__ __forceinline__ void scatter_many_pass(const BucketArgs &a, const int
     int64_t pos[kScatterChunks];
 #pragma unroll
     for (int u = 0; u < kScatterChunks; ++u) {
-        const bool in = kFull || lane_bit(lanes_below(R - u * kWave));
-        const int g = in ? owner_of(bnd, a.G, id[u]) : -1;
+        const int g = owner_by_eighths(bnd, a.G, eb, id[u], kFull ? ~0ull : lanes_below(R - u * kWave));
         const bool ok = g >= 0;
         const uint64_t valid = __ballot(ok);
         uint32_t same_lo = (uint32_t)valid, same_hi = (uint32_t)(valid >> 32);
@@ -862,13 +890,14 @@ __device__ __forceinline__ void scatter_mid(const BucketArgs &a, const int64_t *
     uint32_t lbit[kBits];
 #pragma unroll
     for (int i = 0; i < kBits; ++i) lbit[i] = (uint32_t)((lane >> i) & 1) - 1u;
+    const FewBounds eb = eighth_bounds(bnd, a.G);
     constexpr int kPass = kScatterChunks * kWave;
     for (int64_t k0 = S; k0 < E; k0 += kPass) {
         const int R = __builtin_amdgcn_readfirstlane((int)min<int64_t>(E - k0, (int64_t)kPass));
         if (R == kPass)
-            scatter_mid_pass<true, kBits>(a, bnd, lane, lbit, slot, k0, R);
+            scatter_mid_pass<true, kBits>(a, bnd, eb, lane, lbit, slot, k0, R);
         else
-            scatter_mid_pass<false, kBits>(a, bnd, lane, lbit, slot, k0, R);
+            scatter_mid_pass<false, kBits>(a, bnd, eb, lane, lbit, slot, k0, R);
     }
 }
 
@@ -961,13 +990,14 @@ __global__ __launch_bounds__(kBlock) void eb_bucket_scatter(const BucketArgs a)
                                                               : a.out_offsets[(int64_t)g * row + p0]);
         wave_sync_lds();
         const int nbits = 32 - __builtin_clz((unsigned)(G - 1));
+        const FewBounds eb = eighth_bounds(bnd, G);
         constexpr int kPass = kScatterChunks * kWave;
         for (int64_t k0 = S; k0 < E; k0 += kPass) {
             const int R = __builtin_amdgcn_readfirstlane((int)min<int64_t>(E - k0, (int64_t)kPass));
             if (R == kPass)
-                scatter_many_pass<true>(a, bnd, next, nbits, lane, k0, R);
+                scatter_many_pass<true>(a, bnd, eb, next, nbits, lane, k0, R);
             else
-                scatter_many_pass<false>(a, bnd, next, nbits, lane, k0, R);
+                scatter_many_pass<false>(a, bnd, eb, next, nbits, lane, k0, R);
         }
         return;
     }
