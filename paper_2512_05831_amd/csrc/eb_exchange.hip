@@ -255,10 +255,11 @@ __device__ __forceinline__ int owner_by_eighths(const int64_t *bnd, int G, const
 
 // A scatter wave takes kBagsPerWave consecutive bags of one table; a block 4
 // waves.  Few bags per wave keep many waves (and their id loads) in flight.
-// A count wave takes 16, 32 or 64 bags (up to 8 destinations; 16 beyond):
-// the most that still leave at least kCountWavesMin waves, since count's
-// waves are short and each starts with a dependent load of its offsets,
-// which longer waves pay less often.
+// A count wave takes 16, 32 or 64 bags up to 8 destinations (the most that
+// still leave at least kCountWavesMin waves, since count's waves are short
+// and each starts with a dependent load of its offsets, which longer waves
+// pay less often), 16 up to 64 destinations and 8 or fewer beyond
+// (count_bags).
 constexpr int kBagsPerWave = 16;
 constexpr int kBagsPerBlock = kBagsPerWave * kWavesPerBlock;
 static_assert(kBagsPerWave <= kWave && (kBagsPerWave & (kBagsPerWave - 1)) == 0, "bags per wave");
@@ -266,7 +267,6 @@ constexpr int64_t kCountWavesMin = 4608; // 18 per compute unit
 constexpr int kCountHistBytes = 32768; // count's per-wave [bag][destination] histogram, at most
 constexpr int kCountChunks = 4;   // 64-id chunks loaded ahead by count
 constexpr int kScatterChunks = 8; // and by scatter (measured best for each)
-constexpr int kBallotShards = kFewShards; // compare-based owners, one ballot per destination
 
 struct BucketArgs {
     const int64_t *bounds;   // [T][G+1]
@@ -300,8 +300,8 @@ __device__ __forceinline__ int xcd_run_block(int b, int n)
 }
 
 // Dynamic LDS: the table's G+1 bounds, then one area per wave.
-// count's histogram row per bag: 8 entries for up to 8 destinations (an
-// index by shift), else G.
+// count's histogram row per bag: 8 entries for up to 8 destinations and 16
+// for up to 16 (an index by shift), else G.
 __host__ __device__ inline int count_stride(int G) { return G <= kFewShards ? kFewShards : G <= kTreeShards ? kTreeShards : G; }
 __host__ __device__ inline size_t count_wave_bytes(int G, int bags) { return (size_t)4 * count_stride(G) * bags; }
 __host__ __device__ inline size_t count_lds_bytes(int G, int bags) { return (size_t)(G + 1) * 8 + kWavesPerBlock * count_wave_bytes(G, bags); }
@@ -938,7 +938,7 @@ __global__ __launch_bounds__(kBlock) void eb_bucket_scatter(const BucketArgs a)
     __syncthreads();
     if (!live) return; // no block-wide barrier follows
     const bool contiguous = wave_bags(a, nb, lane, s, e, S, E);
-    if (kOwners == kBallotShards && contiguous) {
+    if (kOwners == kFewShards && contiguous) {
         // Contiguous bags, few destinations: ranks from ballots of the
         // owners' bits (scatter_few_pass).
         const FewBounds fb = few_bounds(bnd, G);
@@ -955,7 +955,7 @@ __global__ __launch_bounds__(kBlock) void eb_bucket_scatter(const BucketArgs a)
         }
         return;
     }
-    if (kOwners > kBallotShards && kOwners <= kWave && contiguous) {
+    if (kOwners > kFewShards && kOwners <= kWave && contiguous) {
         // Contiguous bags, 9 to 64 destinations: within a destination, (bag,
         // position) order is position order, so one running slot per
         // destination (lane g keeps destination g's) suffices, and ballots of
@@ -1112,7 +1112,7 @@ const void *count_kernel(int G, int bags)
 
 const void *scatter_kernel(int G)
 {
-    return G <= kBallotShards  ? (const void *)eb_bucket_scatter<kBallotShards>
+    return G <= kFewShards  ? (const void *)eb_bucket_scatter<kFewShards>
            : G <= kTreeShards ? (const void *)eb_bucket_scatter<kTreeShards>
            : G <= 32          ? (const void *)eb_bucket_scatter<32>
            : G <= kWave       ? (const void *)eb_bucket_scatter<kWave>
