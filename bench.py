@@ -283,11 +283,11 @@ def _time_launches(torch, stream, fn, K, W):
     return ev0.elapsed_time(ev1) * 1e3 / K
 
 
-def exchange_bench(torch, dev, eb, K, W, G=8):
+def exchange_bench(torch, dev, eb, K, W, Gs=(8,)):
     """The row-wise exchange's local kernels at the sizes of the skewed
-    workloads split over 8 GPUs by rows.  bucketize: the 26-table,
-    16384-bag Zipf(1.05) batch (21.1 M ids) into G row blocks per table
-    (``--destinations``, default 8).
+    workloads split over GPUs by rows.  bucketize: the 26-table, 16384-bag
+    Zipf(1.05) batch (21.1 M ids) into G row blocks per table, for each G of
+    ``Gs`` (``--destinations``, default 8).
     sum_partials: the 400M-id shard workload's bags, 65536 / 8 = 8192 per GPU,
     D = 256, 8 partial blocks.  One JSON line each: mean launch time (HIP
     events around K launches) and algorithmic bytes against 8 TB/s."""
@@ -296,31 +296,33 @@ def exchange_bench(torch, dev, eb, K, W, G=8):
     w = wl.config(3)
     off = w.offsets()
     idx = w.indices(off)
-    bounds = np.array([[g * w.rows // G for g in range(G + 1)]] * w.T, dtype=np.int64)
-    d_b = torch.from_numpy(bounds).to(dev)
     d_i = torch.from_numpy(idx).to(dev)
     d_o = torch.from_numpy(off).to(dev)
     TB = w.T * w.B
-    out_off = torch.empty((G, TB + 1), dtype=torch.int64, device=dev)
     out_idx = torch.empty(idx.size, dtype=torch.int64, device=dev)
-    seg = torch.empty(G + 1, dtype=torch.int64, device=dev)
-    nws = eb.eb_bucketize_workspace(w.T, w.B, G)
-    ws = torch.empty(nws, dtype=torch.uint8, device=dev)
+    for G in Gs:
+        bounds = np.array([[g * w.rows // G for g in range(G + 1)]] * w.T, dtype=np.int64)
+        d_b = torch.from_numpy(bounds).to(dev)
+        out_off = torch.empty((G, TB + 1), dtype=torch.int64, device=dev)
+        seg = torch.empty(G + 1, dtype=torch.int64, device=dev)
+        nws = eb.eb_bucketize_workspace(w.T, w.B, G)
+        ws = torch.empty(nws, dtype=torch.uint8, device=dev)
 
-    def bucket():
-        eb.eb_bucketize(w.T, w.B, G, d_b.data_ptr(), d_i.data_ptr(), idx.size, d_o.data_ptr(),
-                        out_off.data_ptr(), out_idx.data_ptr(), idx.size, seg.data_ptr(),
-                        ws.data_ptr(), nws, stream.cuda_stream)
-    us = _time_launches(torch, stream, bucket, K, W)
-    kept = int(seg[-1].item())
-    by = idx.size * 8 + (TB + 1) * 8 + bounds.size * 8 + kept * 8 + G * (TB + 1) * 8 + (G + 1) * 8
-    print(json.dumps({"kernel": "eb_bucketize", "workload": w.name + f"-to-{G}-row-blocks",
-                      "ids": int(idx.size), "bags": TB, "destinations": G,
-                      "us_per_call": round(us, 1), "ids_per_s": idx.size / us * 1e6,
-                      "algorithmic_bytes": by, "algorithmic_GBps": round(by / us / 1e3, 1),
-                      "frac_of_8TBps": round(by / us / 1e3 / HBM_PEAK_GBPS, 4),
-                      # count, tile sums, (tile prefix when over 131072 tile sums,) tile scan, scatter
-                      "kernels_per_call": 4 if G * -(-TB // 2048) <= 131072 else 5}), flush=True)
+        def bucket():
+            eb.eb_bucketize(w.T, w.B, G, d_b.data_ptr(), d_i.data_ptr(), idx.size, d_o.data_ptr(),
+                            out_off.data_ptr(), out_idx.data_ptr(), idx.size, seg.data_ptr(),
+                            ws.data_ptr(), nws, stream.cuda_stream)
+        us = _time_launches(torch, stream, bucket, K, W)
+        kept = int(seg[-1].item())
+        by = idx.size * 8 + (TB + 1) * 8 + bounds.size * 8 + kept * 8 + G * (TB + 1) * 8 + (G + 1) * 8
+        print(json.dumps({"kernel": "eb_bucketize", "workload": w.name + f"-to-{G}-row-blocks",
+                          "ids": int(idx.size), "bags": TB, "destinations": G,
+                          "us_per_call": round(us, 1), "ids_per_s": idx.size / us * 1e6,
+                          "algorithmic_bytes": by, "algorithmic_GBps": round(by / us / 1e3, 1),
+                          "frac_of_8TBps": round(by / us / 1e3 / HBM_PEAK_GBPS, 4),
+                          # count, tile sums, (tile prefix when over 131072 tile sums,) tile scan, scatter
+                          "kernels_per_call": 4 if G * -(-TB // 2048) <= 131072 else 5}), flush=True)
+        del out_off, ws
     del d_i, out_idx
     Gp = 8  # the partial blocks of 8 GPUs, whatever --destinations says
     B, T, D = 65536 // Gp, 1, 256
@@ -680,8 +682,8 @@ def parser() -> argparse.ArgumentParser:
                     help="replay the steps from a captured HIP graph (launch-bound workloads)")
     ap.add_argument("--exchange", action="store_true",
                     help="time the row-wise exchange kernels instead (bucketize, sum_partials)")
-    ap.add_argument("--destinations", type=int, default=8, metavar="G",
-                    help="with --exchange: bucketize into G row blocks per table (1..1024)")
+    ap.add_argument("--destinations", default="8", metavar="G[,G...]",
+                    help="with --exchange: bucketize into G row blocks per table (1..1024), for each G given")
     ap.add_argument("--rw-pipeline", type=int, default=0, metavar="G",
                     help="time one GPU's compute in a row-wise step of the chosen workload split "
                          "over G GPUs instead (bucketize, gather of the received ids, sum of partials)")
@@ -701,23 +703,47 @@ def _sig(x, n=4):
     return None if x is None else float(f"{x:.{n}g}")
 
 
+def destination_counts(text):
+    """--destinations: one count or a comma-separated list, each in 1..1024."""
+    Gs = [int(x) for x in str(text).split(",") if x.strip()]
+    if not Gs or any(not 1 <= G <= 1024 for G in Gs):
+        raise SystemExit("--destinations takes counts between 1 and 1024")
+    return Gs
+
+
+EXCHANGE_DESTINATIONS = (8, 16, 64)
+
+
 def exchange_entries(budget_s=120.0):
-    """The row-wise exchange's local kernels (bucketize, sum of partials), timed
-    by a child run of --exchange; one compact entry each, or an error."""
+    """The row-wise exchange's local kernels (bucketize into 8, 16 and 64 row
+    blocks, sum of partials), timed by a child run of --exchange; one compact
+    entry for 8 blocks and for the sum, the other block counts beside them, or
+    an error."""
     import subprocess
 
-    cmd = [sys.executable, os.path.abspath(__file__), "--exchange", "--steps", "100", "--warmup", "10"]
+    cmd = [sys.executable, os.path.abspath(__file__), "--exchange", "--steps", "100", "--warmup", "10",
+           "--destinations", ",".join(str(G) for G in EXCHANGE_DESTINATIONS)]
     try:
         res = subprocess.run(cmd, stdout=subprocess.PIPE, text=True, timeout=budget_s)
         if res.returncode != 0:
             raise RuntimeError(f"child run exited with {res.returncode}")
-        out = {}
-        for ln in res.stdout.strip().splitlines():
-            r = json.loads(ln)
-            out[r["kernel"]] = {k: r[k] for k in ("workload", "us_per_call", "algorithmic_GBps", "frac_of_8TBps")}
-        return out
+        return exchange_summary(res.stdout)
     except Exception as exc:  # noqa: BLE001 -- recorded, the line is still printed
         return {"error": f"{type(exc).__name__}: {exc}"}
+
+
+def exchange_summary(stdout):
+    """The child's JSON lines as the bench line's `exchange` entry."""
+    out = {}
+    for ln in stdout.strip().splitlines():
+        r = json.loads(ln)
+        entry = {k: r[k] for k in ("workload", "us_per_call", "algorithmic_GBps", "frac_of_8TBps")}
+        if r["kernel"] == "eb_bucketize" and r["destinations"] != 8:
+            out.setdefault("eb_bucketize_other_destinations", {})[str(r["destinations"])] = {
+                k: r[k] for k in ("us_per_call", "algorithmic_GBps")}
+        else:
+            out[r["kernel"]] = entry
+    return out
 
 
 def workloads_table(entries):
@@ -764,7 +790,7 @@ def main():
         paper_sweep(torch, dev, eb, args.index_type)
         return
     if args.exchange:
-        exchange_bench(torch, dev, eb, args.steps, args.warmup, args.destinations)
+        exchange_bench(torch, dev, eb, args.steps, args.warmup, destination_counts(args.destinations))
         return
     if args.rw_pipeline:
         rw_pipeline_bench(torch, dev, eb, pick_workload(args), args.rw_pipeline, args.steps, args.warmup,

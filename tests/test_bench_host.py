@@ -103,3 +103,23 @@ def test_workloads_table_keeps_every_entry():
     assert row["single_launch_us_median_p10_p90"] == [12.0, 11.0, 13.0]
     assert row["cold_single_launch_us_median"] == 20.0
     assert dict(zip(cols, t["rows"][0]))["cold_single_launch_us_median"] is None
+
+
+def test_exchange_summary_keeps_every_destination_count():
+    """The default line's `exchange` entry: bucketize into 8 row blocks and the
+    sum of partials as full entries, the other block counts beside them."""
+    import json
+    lines = [{"kernel": "eb_bucketize", "workload": "w-to-8-row-blocks", "destinations": 8, "us_per_call": 132.0,
+              "algorithmic_GBps": 2788.0, "frac_of_8TBps": 0.35, "ids": 5},
+             {"kernel": "eb_bucketize", "workload": "w-to-64-row-blocks", "destinations": 64, "us_per_call": 339.0,
+              "algorithmic_GBps": 1649.0, "frac_of_8TBps": 0.21, "ids": 5},
+             {"kernel": "eb_sum_partials", "workload": "8x8192x256-f32", "us_per_call": 12.3,
+              "algorithmic_GBps": 6113.0, "frac_of_8TBps": 0.76}]
+    out = bench.exchange_summary("\n".join(json.dumps(x) for x in lines))
+    assert out["eb_bucketize"]["workload"] == "w-to-8-row-blocks" and "ids" not in out["eb_bucketize"]
+    assert out["eb_bucketize_other_destinations"] == {"64": {"us_per_call": 339.0, "algorithmic_GBps": 1649.0}}
+    assert out["eb_sum_partials"]["us_per_call"] == 12.3
+    assert bench.destination_counts("8,16, 64") == [8, 16, 64]
+    for bad in ("0", "1025", ""):
+        with pytest.raises(SystemExit):
+            bench.destination_counts(bad)
