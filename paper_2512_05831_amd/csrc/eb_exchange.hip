@@ -19,10 +19,10 @@
 // chains of dependent loads and by instruction issue.
 //
 // eb_bucketize runs three kernels on the caller's stream:
-//   1. count   : a wave takes 16, 32 or 64 consecutive bags (for up to 8
-//                destinations the most that leave at least 4608 waves, else
-//                16; each XCD one contiguous run of workgroups); each id's
-//                owner by
+//   1. count   : a wave takes 2 to 64 consecutive bags (for up to 16
+//                destinations the most of 16, 32, 64 that leave at least
+//                4608 waves, else 16, and 8 or fewer beyond 64; each XCD one
+//                contiguous run of workgroups); each id's owner by
 //                comparisons with the table's block bounds (up to 16 blocks:
 //                a search tree evaluated as wave-wide lane masks) or by
 //                binary search over them (staged in LDS); for ordinary CSR
@@ -255,7 +255,7 @@ __device__ __forceinline__ int owner_by_eighths(const int64_t *bnd, int G, const
 
 // A scatter wave takes kBagsPerWave consecutive bags of one table; a block 4
 // waves.  Few bags per wave keep many waves (and their id loads) in flight.
-// A count wave takes 16, 32 or 64 bags up to 8 destinations (the most that
+// A count wave takes 16, 32 or 64 bags up to 16 destinations (the most that
 // still leave at least kCountWavesMin waves, since count's waves are short
 // and each starts with a dependent load of its offsets, which longer waves
 // pay less often), 16 up to 64 destinations and 8 or fewer beyond
@@ -1076,9 +1076,9 @@ __global__ __launch_bounds__(kBlock) void eb_sum_partials_scalar(const PartialAr
 int64_t scan_tiles(int64_t TB) { return std::max<int64_t>(1, (TB + kScanTile - 1) / kScanTile); }
 
 // Bags per count wave for T*B bags in all and G destinations (see
-// kCountWavesMin).  Only the owner-mask path (G <= 8, 8 histogram entries per
-// bag) gains from longer waves; 9 to 64 destinations take 16 bags, more take
-// 8, fewer when their [bag][destination] histogram would pass
+// kCountWavesMin).  Only the compare-tree paths (G <= 16, 8 or 16 histogram
+// entries per bag) gain from longer waves; 17 to 64 destinations take 16
+// bags, more take 8, fewer when their [bag][destination] histogram would pass
 // kCountHistBytes (measured: 8 bags beat 16 at 200 destinations, and at 1024
 // beat 2 or 4 even though the histograms then limit a compute unit to 4 waves).
 int count_bags(int64_t TB, int G)
@@ -1088,7 +1088,7 @@ int count_bags(int64_t TB, int G)
         while (bags > 2 && count_wave_bytes(G, bags) > (size_t)kCountHistBytes) bags /= 2;
         return bags;
     }
-    if (G > kFewShards) return 16;
+    if (G > kTreeShards) return 16;
     for (int bags = 64; bags > 16; bags /= 2)
         if (TB / bags >= kCountWavesMin) return bags;
     return 16;
@@ -1103,7 +1103,10 @@ const void *count_kernel(int G, int bags)
         return bags == 64 ? (const void *)eb_bucket_count<64, kFewShards>
                : bags == 32 ? (const void *)eb_bucket_count<32, kFewShards>
                             : (const void *)eb_bucket_count<16, kFewShards>;
-    if (G <= kTreeShards) return (const void *)eb_bucket_count<16, kTreeShards>;
+    if (G <= kTreeShards)
+        return bags == 64 ? (const void *)eb_bucket_count<64, kTreeShards>
+               : bags == 32 ? (const void *)eb_bucket_count<32, kTreeShards>
+                            : (const void *)eb_bucket_count<16, kTreeShards>;
     return bags == 16  ? (const void *)eb_bucket_count<16, 0>
            : bags == 8 ? (const void *)eb_bucket_count<8, 0>
            : bags == 4 ? (const void *)eb_bucket_count<4, 0>

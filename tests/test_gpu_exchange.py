@@ -191,13 +191,14 @@ def test_bucketize_unordered_offsets(G, device):
     check_bucketize(T, B, idx, off, bounds, device, capacity=total + 5)
 
 
-@pytest.mark.parametrize("G,T,B", [(8, 3, 100_001), (8, 2, 75_000), (20, 3, 100_001), (100, 3, 100_001),
-                                   (3, 1, 147_456), (8, 1, 294_911)])
+@pytest.mark.parametrize("G,T,B", [(8, 3, 100_001), (8, 2, 75_000), (12, 3, 100_001), (16, 2, 75_000),
+                                   (20, 3, 100_001), (100, 3, 100_001), (3, 1, 147_456), (8, 1, 294_911)])
 def test_bucketize_long_count_waves(G, T, B, device):
     """Batches large enough for count waves of 32 bags (from 147,456 bags)
-    or 64 (from 294,912) at up to 8 destinations, with ragged last waves and
-    workgroups, and the same sizes through the searched-owner path (G <= 32)
-    and the bag-at-a-time path (larger G), against the oracle."""
+    or 64 (from 294,912) at up to 16 destinations (both compare trees), with
+    ragged last waves and workgroups, and the same sizes through the searched
+    owners with lane slots (up to 64) and with slots in LDS (more), against
+    the oracle."""
     T, B, idx, off, bounds = bucket_case(G * 13 + B, G, T=T, B=B, maxL=4)
     check_bucketize(T, B, idx, off, bounds, device)
 
