@@ -283,11 +283,13 @@ def _time_launches(torch, stream, fn, K, W):
     return ev0.elapsed_time(ev1) * 1e3 / K
 
 
-def exchange_bench(torch, dev, eb, K, W, Gs=(8,)):
+def exchange_bench(torch, dev, eb, K, W, Gs=(8,), i32=False):
     """The row-wise exchange's local kernels at the sizes of the skewed
     workloads split over GPUs by rows.  bucketize: the 26-table, 16384-bag
     Zipf(1.05) batch (21.1 M ids) into G row blocks per table, for each G of
-    ``Gs`` (``--destinations``, default 8).
+    ``Gs`` (``--destinations``, default 8), with int64 ids and offsets or, with
+    ``--index-type i32``, int32 ones (eb_bucketize_ex; 4 bytes less per id read
+    and per id written, 4 per offset).
     sum_partials: the 400M-id shard workload's bags, 65536 / 8 = 8192 per GPU,
     D = 256, 8 partial blocks.  One JSON line each: mean launch time (HIP
     events around K launches) and algorithmic bytes against 8 TB/s."""
@@ -296,10 +298,12 @@ def exchange_bench(torch, dev, eb, K, W, Gs=(8,)):
     w = wl.config(3)
     off = w.offsets()
     idx = w.indices(off)
-    d_i = torch.from_numpy(idx).to(dev)
-    d_o = torch.from_numpy(off).to(dev)
+    ity = np.int32 if i32 else np.int64
+    d_i = torch.from_numpy(idx.astype(ity)).to(dev)
+    d_o = torch.from_numpy(off.astype(ity)).to(dev)
+    es = 4 if i32 else 8  # bytes per id and per offset
     TB = w.T * w.B
-    out_idx = torch.empty(idx.size, dtype=torch.int64, device=dev)
+    out_idx = torch.empty(idx.size, dtype=d_i.dtype, device=dev)
     for G in Gs:
         bounds = np.array([[g * w.rows // G for g in range(G + 1)]] * w.T, dtype=np.int64)
         d_b = torch.from_numpy(bounds).to(dev)
@@ -309,14 +313,14 @@ def exchange_bench(torch, dev, eb, K, W, Gs=(8,)):
         ws = torch.empty(nws, dtype=torch.uint8, device=dev)
 
         def bucket():
-            eb.eb_bucketize(w.T, w.B, G, d_b.data_ptr(), d_i.data_ptr(), idx.size, d_o.data_ptr(),
-                            out_off.data_ptr(), out_idx.data_ptr(), idx.size, seg.data_ptr(),
-                            ws.data_ptr(), nws, stream.cuda_stream)
+            eb.eb_bucketize_ex(w.T, w.B, G, d_b.data_ptr(), eb.EB_IDX_I32 if i32 else eb.EB_IDX_I64,
+                               d_i.data_ptr(), idx.size, d_o.data_ptr(), out_off.data_ptr(), out_idx.data_ptr(),
+                               idx.size, seg.data_ptr(), ws.data_ptr(), nws, stream.cuda_stream)
         us = _time_launches(torch, stream, bucket, K, W)
         kept = int(seg[-1].item())
-        by = idx.size * 8 + (TB + 1) * 8 + bounds.size * 8 + kept * 8 + G * (TB + 1) * 8 + (G + 1) * 8
-        print(json.dumps({"kernel": "eb_bucketize", "workload": w.name + f"-to-{G}-row-blocks",
-                          "ids": int(idx.size), "bags": TB, "destinations": G,
+        by = idx.size * es + (TB + 1) * es + bounds.size * 8 + kept * es + G * (TB + 1) * 8 + (G + 1) * 8
+        print(json.dumps({"kernel": "eb_bucketize", "workload": w.name + f"-to-{G}-row-blocks" + ("-i32" if i32 else ""),
+                          "ids": int(idx.size), "bags": TB, "destinations": G, "index_type": "i32" if i32 else "i64",
                           "us_per_call": round(us, 1), "ids_per_s": idx.size / us * 1e6,
                           "algorithmic_bytes": by, "algorithmic_GBps": round(by / us / 1e3, 1),
                           "frac_of_8TBps": round(by / us / 1e3 / HBM_PEAK_GBPS, 4),
@@ -790,7 +794,8 @@ def main():
         paper_sweep(torch, dev, eb, args.index_type)
         return
     if args.exchange:
-        exchange_bench(torch, dev, eb, args.steps, args.warmup, destination_counts(args.destinations))
+        exchange_bench(torch, dev, eb, args.steps, args.warmup, destination_counts(args.destinations),
+                       args.index_type == "i32")
         return
     if args.rw_pipeline:
         rw_pipeline_bench(torch, dev, eb, pick_workload(args), args.rw_pipeline, args.steps, args.warmup,

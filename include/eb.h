@@ -80,9 +80,10 @@ enum { EB_SUM = 0, EB_MEAN = 1 };
  * bits. */
 enum { EB_HINT_STREAM_ROWS = 0x100 };
 
-/* Integer type of eb_forward_ex's indices and offsets (both the same).
- * int32 ids save 4 bytes of HBM traffic per lookup; values are widened to
- * int64 by sign extension, so every rule above applies unchanged. */
+/* Integer type of eb_forward_ex's indices and offsets (both the same), and of
+ * eb_bucketize_ex's indices, offsets and out_indices.  int32 ids save 4 bytes
+ * of HBM traffic per lookup; values are widened to int64 by sign extension,
+ * so every rule above applies unchanged. */
 enum { EB_IDX_I64 = 0, EB_IDX_I32 = 1 };
 
 /* Return codes. */
@@ -282,6 +283,25 @@ int eb_bucketize(int32_t T, int64_t B, int32_t G, const int64_t *bounds, const i
                  int64_t nnz, const int64_t *offsets, int64_t *out_offsets, int64_t *out_indices,
                  int64_t out_capacity, int64_t *segments, void *workspace, size_t workspace_bytes,
                  void *stream);
+
+/*
+ * eb_bucketize_ex -- eb_bucketize with a choice of index width (Sec. 4.2's
+ * ids and lengths, in either integer width).
+ *
+ *   index_type   EB_IDX_I64: indices, offsets and out_indices are int64, as
+ *                in eb_bucketize; EB_IDX_I32: all three are int32 (ids and
+ *                offsets widen by sign extension, so every statement of
+ *                eb_bucketize holds for the widened values, and the ids
+ *                stored keep their value).  bounds, out_offsets, segments and
+ *                the workspace (eb_bucketize_workspace) are unchanged.
+ *
+ * Every other argument and error as for eb_bucketize; EB_ERR_INVALID for an
+ * unknown index_type.
+ */
+int eb_bucketize_ex(int32_t T, int64_t B, int32_t G, const int64_t *bounds, int32_t index_type,
+                    const void *indices, int64_t nnz, const void *offsets, int64_t *out_offsets,
+                    void *out_indices, int64_t out_capacity, int64_t *segments, void *workspace,
+                    size_t workspace_bytes, void *stream);
 
 /*
  * eb_bucketize_noalloc -- eb_bucketize for callers that cannot allocate

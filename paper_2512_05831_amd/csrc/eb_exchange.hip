@@ -18,7 +18,8 @@
 // contraction); eb_sum_partials is bound by it, eb_bucketize by its waves'
 // chains of dependent loads and by instruction issue.
 //
-// eb_bucketize runs three kernels on the caller's stream:
+// eb_bucketize runs three kernels on the caller's stream (eb_bucketize_ex the
+// same with int32 ids, offsets and scattered ids, each widened on load):
 //   1. count   : a wave takes 2 to 64 consecutive bags (for up to 16
 //                destinations the most of 16, 32, 64 that leave at least
 //                4608 waves, else 16, and 8 or fewer beyond 64; each XCD one
@@ -270,10 +271,10 @@ constexpr int kScatterChunks = 8; // and by scatter (measured best for each)
 
 struct BucketArgs {
     const int64_t *bounds;   // [T][G+1]
-    const int64_t *indices;
-    const int64_t *offsets;  // [T*B+1]
+    const void *indices;     // IT [nnz]
+    const void *offsets;     // IT [T*B+1]
     int64_t *out_offsets;    // [G][T*B+1]
-    int64_t *out_indices;
+    void *out_indices;       // IT [out_cap]
     const int64_t *segments; // [G+1] (scatter pass)
     const int64_t *starts;   // [G][nq]: out_offsets[g][16 q] (scatter pass; workspace)
     int64_t nq;
@@ -285,6 +286,17 @@ struct BucketArgs {
     int32_t blocks_per_table;       // scatter's workgroups per table
     int32_t count_blocks_per_table; // count's
 };
+
+// The batch's index type IT (int64_t or int32_t) types the ids, the offsets
+// and the scattered ids; every value is widened to int64 as it is loaded.
+template <typename IT>
+__device__ __forceinline__ const IT *ids_of(const BucketArgs &a) { return (const IT *)a.indices; }
+
+template <typename IT>
+__device__ __forceinline__ int64_t offset_at(const BucketArgs &a, int64_t p) { return (int64_t)((const IT *)a.offsets)[p]; }
+
+template <typename IT>
+__device__ __forceinline__ void put_id(const BucketArgs &a, int64_t pos, int64_t id) { ((IT *)a.out_indices)[pos] = (IT)id; }
 
 // Workgroups are dealt to the 8 XCDs in turn (workgroup b to XCD b % 8).
 // count and scatter take their bags by logical workgroup xcd_run_block(b, n),
@@ -326,14 +338,15 @@ __device__ __forceinline__ int64_t readlane64(int64_t v, int l)
 // wave_bags clamps them and returns whether the ranges tile [S, E) in bag
 // order (ordinary CSR offsets), the case where position order within the
 // wave is (bag, position) order.
+template <typename IT>
 __device__ __forceinline__ void wave_bag_loads(const BucketArgs &a, int64_t p0, int nb, int lane, int64_t &s,
                                                int64_t &e)
 {
     s = 0;
     e = 0;
     if (lane < nb) {
-        s = a.offsets[p0 + lane];
-        e = a.offsets[p0 + lane + 1];
+        s = offset_at<IT>(a, p0 + lane);
+        e = offset_at<IT>(a, p0 + lane + 1);
     }
 }
 
@@ -360,16 +373,16 @@ __device__ __forceinline__ void wave_sync_lds()
 // no tail masks).
 // kOwners: 8 (owners by the 3-bit tree), 16 (the 4-bit tree), or 0 (by
 // binary search over the bounds in LDS).
-template <int kOwners, bool kFull>
+template <typename IT, int kOwners, bool kFull>
 __device__ __forceinline__ void count_pass(const BucketArgs &a, const int64_t *bnd, const FewBounds &fb,
                                            const TreeBounds &tb, int *hist, int lane, int64_t s, uint64_t bags,
                                            int64_t k0, int R)
 {
-    const int64_t *src = a.indices + k0 + lane;
+    const IT *src = ids_of<IT>(a) + k0 + lane;
     int64_t id[kCountChunks];
 #pragma unroll
     for (int u = 0; u < kCountChunks; ++u)
-        id[u] = (kFull || lane_bit(lanes_below(R - u * kWave))) ? __builtin_nontemporal_load(src + u * kWave) : 0;
+        id[u] = (kFull || lane_bit(lanes_below(R - u * kWave))) ? (int64_t)__builtin_nontemporal_load(src + u * kWave) : 0;
 #pragma unroll
     for (int u = 0; u < kCountChunks; ++u) {
         // The bag of position k is the last one starting at or
@@ -402,7 +415,7 @@ __device__ __forceinline__ void count_pass(const BucketArgs &a, const int64_t *b
 // count's loop over the wave's ids [S, E) for contiguous bags (bag l of the
 // wave starts at lane l's s; bags = lanes holding a bag): adds each id with
 // an owner to hist[bag * count_stride(G) + owner].
-template <int kOwners>
+template <typename IT, int kOwners>
 __device__ __forceinline__ void count_chunks(const BucketArgs &a, const int64_t *bnd, const FewBounds &fb,
                                              const TreeBounds &tb, int *hist, int lane, int64_t s, uint64_t bags,
                                              int64_t S, int64_t E)
@@ -411,16 +424,16 @@ __device__ __forceinline__ void count_chunks(const BucketArgs &a, const int64_t 
     for (int64_t k0 = S; k0 < E; k0 += kPass) {
         const int R = __builtin_amdgcn_readfirstlane((int)min<int64_t>(E - k0, (int64_t)kPass));
         if (R == kPass)
-            count_pass<kOwners, true>(a, bnd, fb, tb, hist, lane, s, bags, k0, R);
+            count_pass<IT, kOwners, true>(a, bnd, fb, tb, hist, lane, s, bags, k0, R);
         else
-            count_pass<kOwners, false>(a, bnd, fb, tb, hist, lane, s, bags, k0, R);
+            count_pass<IT, kOwners, false>(a, bnd, fb, tb, hist, lane, s, bags, k0, R);
     }
 }
 
 // kOwners: how the instantiation finds owners (8: 3-bit compare tree, 16:
 // 4-bit tree, 0: binary search); one instantiation per method and wave size,
 // so that each keeps only its own path's registers.
-template <int kBags, int kOwners>
+template <typename IT, int kBags, int kOwners>
 __global__ __launch_bounds__(kBlock) void eb_bucket_count(const BucketArgs a)
 {
     static_assert(kBags <= kWave && (kBags & (kBags - 1)) == 0, "bags per count wave");
@@ -440,7 +453,7 @@ __global__ __launch_bounds__(kBlock) void eb_bucket_count(const BucketArgs a)
     // The wave's bag ranges do not depend on the bounds: read them first, so
     // that both loads are in flight together.
     int64_t s = 0, e = 0, S, E;
-    if (live) wave_bag_loads(a, p0, nb, lane, s, e);
+    if (live) wave_bag_loads<IT>(a, p0, nb, lane, s, e);
     for (int g = threadIdx.x; g <= G; g += kBlock) bnd[g] = a.bounds[(int64_t)t * (G + 1) + g];
     __syncthreads();
     if (!live) return; // no block-wide barrier follows
@@ -453,11 +466,11 @@ __global__ __launch_bounds__(kBlock) void eb_bucket_count(const BucketArgs a)
         for (int x = lane; x < kBags * count_stride(G); x += kWave) hist[x] = 0;
         wave_sync_lds();
         if constexpr (kOwners == kFewShards)
-            count_chunks<kFewShards>(a, bnd, few_bounds(bnd, G), TreeBounds{}, hist, lane, s, bags, S, E);
+            count_chunks<IT, kFewShards>(a, bnd, few_bounds(bnd, G), TreeBounds{}, hist, lane, s, bags, S, E);
         else if constexpr (kOwners == kTreeShards)
-            count_chunks<kTreeShards>(a, bnd, FewBounds{}, tree_bounds(bnd, G), hist, lane, s, bags, S, E);
+            count_chunks<IT, kTreeShards>(a, bnd, FewBounds{}, tree_bounds(bnd, G), hist, lane, s, bags, S, E);
         else
-            count_chunks<0>(a, bnd, eighth_bounds(bnd, G), TreeBounds{}, hist, lane, s, bags, S, E);
+            count_chunks<IT, 0>(a, bnd, eighth_bounds(bnd, G), TreeBounds{}, hist, lane, s, bags, S, E);
         wave_sync_lds();
         // Entry x of the histogram's transpose: bag x % kBags, destination
         // x / kBags; a store covers 64 / kBags rows, kBags bags of each.
@@ -474,7 +487,7 @@ __global__ __launch_bounds__(kBlock) void eb_bucket_count(const BucketArgs a)
         for (int g = lane; g < G; g += kWave) hist[g] = 0;
         wave_sync_lds();
         for (int64_t k = sj + lane; k < ej; k += kWave) {
-            const int g = owner_of(bnd, G, __builtin_nontemporal_load(a.indices + k));
+            const int g = owner_of(bnd, G, (int64_t)__builtin_nontemporal_load(ids_of<IT>(a) + k));
             if (g >= 0) atomicAdd(&hist[g], 1);
         }
         wave_sync_lds();
@@ -689,6 +702,7 @@ __global__ __launch_bounds__(kBlock) void eb_scan_tiles(const ScanArgs a)
 
 // Scatter one chunk of up to 64 ids (lanes with g < 0 hold none): every
 // distinct destination in turn, lowest lane first, so the order is stable.
+template <typename IT>
 __device__ __forceinline__ void scatter_chunk(const BucketArgs &a, int64_t *next, int lane, int g, int64_t id)
 {
     const uint64_t below = (1ull << lane) - 1;
@@ -699,7 +713,7 @@ __device__ __forceinline__ void scatter_chunk(const BucketArgs &a, int64_t *next
         const uint64_t same = __ballot(g == og);
         const int64_t base = next[og];
         const int64_t pos = base + __popcll(same & below);
-        if (g == og && (uint64_t)pos < (uint64_t)a.out_cap) a.out_indices[pos] = id;
+        if (g == og && (uint64_t)pos < (uint64_t)a.out_cap) put_id<IT>(a, pos, id);
         __builtin_amdgcn_wave_barrier();
         if (lane == leader) next[og] = base + __popcll(same);
         wave_sync_lds();
@@ -714,15 +728,15 @@ __device__ __forceinline__ void scatter_chunk(const BucketArgs &a, int64_t *next
 // for the same destination; a single store then places the whole chunk.
 // Lane d < G holds destination d's next output slot in `slot`; l0..l2 are the
 // complements of the lane's low three bits as all-ones / zero masks.
-template <bool kFull>
+template <typename IT, bool kFull>
 __device__ __forceinline__ void scatter_few_pass(const BucketArgs &a, const FewBounds &fb, int lane, uint32_t l0,
                                                  uint32_t l1, uint32_t l2, int64_t &slot, int64_t k0, int R)
 {
-    const int64_t *src = a.indices + k0 + lane;
+    const IT *src = ids_of<IT>(a) + k0 + lane;
     int64_t id[kScatterChunks];
 #pragma unroll
     for (int u = 0; u < kScatterChunks; ++u)
-        id[u] = (kFull || lane_bit(lanes_below(R - u * kWave))) ? __builtin_nontemporal_load(src + u * kWave) : 0;
+        id[u] = (kFull || lane_bit(lanes_below(R - u * kWave))) ? (int64_t)__builtin_nontemporal_load(src + u * kWave) : 0;
     // Rank all chunks first, store afterwards: loads and stores share one
     // completion counter, so a store between two chunks would make the next
     // chunk wait for it.
@@ -757,19 +771,19 @@ __device__ __forceinline__ void scatter_few_pass(const BucketArgs &a, const FewB
     __builtin_amdgcn_sched_barrier(0); // keep the stores after all ranking
 #pragma unroll
     for (int u = 0; u < kScatterChunks; ++u)
-        if ((uint64_t)pos[u] < (uint64_t)a.out_cap) a.out_indices[pos[u]] = id[u];
+        if ((uint64_t)pos[u] < (uint64_t)a.out_cap) put_id<IT>(a, pos[u], id[u]);
 }
 
 // scatter_few_pass for 9 to 16 destinations: owners from the 4-bit tree.
-template <bool kFull>
+template <typename IT, bool kFull>
 __device__ __forceinline__ void scatter_tree_pass(const BucketArgs &a, const TreeBounds &tb, int lane,
                                                   const uint32_t (&lbit)[kTreeBits], int64_t &slot, int64_t k0, int R)
 {
-    const int64_t *src = a.indices + k0 + lane;
+    const IT *src = ids_of<IT>(a) + k0 + lane;
     int64_t id[kScatterChunks];
 #pragma unroll
     for (int u = 0; u < kScatterChunks; ++u)
-        id[u] = (kFull || lane_bit(lanes_below(R - u * kWave))) ? __builtin_nontemporal_load(src + u * kWave) : 0;
+        id[u] = (kFull || lane_bit(lanes_below(R - u * kWave))) ? (int64_t)__builtin_nontemporal_load(src + u * kWave) : 0;
     int64_t pos[kScatterChunks];
 #pragma unroll
     for (int u = 0; u < kScatterChunks; ++u) {
@@ -796,7 +810,7 @@ __device__ __forceinline__ void scatter_tree_pass(const BucketArgs &a, const Tre
     __builtin_amdgcn_sched_barrier(0); // keep the stores after all ranking
 #pragma unroll
     for (int u = 0; u < kScatterChunks; ++u)
-        if ((uint64_t)pos[u] < (uint64_t)a.out_cap) a.out_indices[pos[u]] = id[u];
+        if ((uint64_t)pos[u] < (uint64_t)a.out_cap) put_id<IT>(a, pos[u], id[u]);
 }
 
 // One pass of the scatter for contiguous bags and 17 to 64 destinations: as
@@ -804,15 +818,15 @@ __device__ __forceinline__ void scatter_tree_pass(const BucketArgs &a, const Tre
 // bounds in LDS and ranked through kBits ballots of the owner's bits (lane d
 // < G holds destination d's slot; lbit[i] is the complement of the lane's
 // bit i as an all-ones / zero mask).
-template <bool kFull, int kBits>
+template <typename IT, bool kFull, int kBits>
 __device__ __forceinline__ void scatter_mid_pass(const BucketArgs &a, const int64_t *bnd, const FewBounds &eb, int lane,
                                                  const uint32_t (&lbit)[kBits], int64_t &slot, int64_t k0, int R)
 {
-    const int64_t *src = a.indices + k0 + lane;
+    const IT *src = ids_of<IT>(a) + k0 + lane;
     int64_t id[kScatterChunks];
 #pragma unroll
     for (int u = 0; u < kScatterChunks; ++u)
-        id[u] = (kFull || lane_bit(lanes_below(R - u * kWave))) ? __builtin_nontemporal_load(src + u * kWave) : 0;
+        id[u] = (kFull || lane_bit(lanes_below(R - u * kWave))) ? (int64_t)__builtin_nontemporal_load(src + u * kWave) : 0;
     int64_t pos[kScatterChunks];
 #pragma unroll
     for (int u = 0; u < kScatterChunks; ++u) {
@@ -841,22 +855,22 @@ __device__ __forceinline__ void scatter_mid_pass(const BucketArgs &a, const int6
     __builtin_amdgcn_sched_barrier(0); // keep the stores after all ranking
 #pragma unroll
     for (int u = 0; u < kScatterChunks; ++u)
-        if ((uint64_t)pos[u] < (uint64_t)a.out_cap) a.out_indices[pos[u]] = id[u];
+        if ((uint64_t)pos[u] < (uint64_t)a.out_cap) put_id<IT>(a, pos[u], id[u]);
 }
 
 // One pass of the scatter for contiguous bags and more than 64 destinations:
 // owners by binary search, ranks from ballots of the owner's nbits bits, and
 // each destination's running slot in the wave's LDS array next[] (read by
 // every lane of the owner, advanced by the first of them).
-template <bool kFull>
+template <typename IT, bool kFull>
 __device__ __forceinline__ void scatter_many_pass(const BucketArgs &a, const int64_t *bnd, const FewBounds &eb,
                                                   int64_t *next, int nbits, int lane, int64_t k0, int R)
 {
-    const int64_t *src = a.indices + k0 + lane;
+    const IT *src = ids_of<IT>(a) + k0 + lane;
     int64_t id[kScatterChunks];
 #pragma unroll
     for (int u = 0; u < kScatterChunks; ++u)
-        id[u] = (kFull || lane_bit(lanes_below(R - u * kWave))) ? __builtin_nontemporal_load(src + u * kWave) : 0;
+        id[u] = (kFull || lane_bit(lanes_below(R - u * kWave))) ? (int64_t)__builtin_nontemporal_load(src + u * kWave) : 0;
     int64_t pos[kScatterChunks];
 #pragma unroll
     for (int u = 0; u < kScatterChunks; ++u) {
@@ -880,10 +894,10 @@ __device__ __forceinline__ void scatter_many_pass(const BucketArgs &a, const int
     __builtin_amdgcn_sched_barrier(0); // keep the stores after all ranking
 #pragma unroll
     for (int u = 0; u < kScatterChunks; ++u)
-        if ((uint64_t)pos[u] < (uint64_t)a.out_cap) a.out_indices[pos[u]] = id[u];
+        if ((uint64_t)pos[u] < (uint64_t)a.out_cap) put_id<IT>(a, pos[u], id[u]);
 }
 
-template <int kBits>
+template <typename IT, int kBits>
 __device__ __forceinline__ void scatter_mid(const BucketArgs &a, const int64_t *bnd, int lane, int64_t slot, int64_t S,
                                             int64_t E)
 {
@@ -895,9 +909,9 @@ __device__ __forceinline__ void scatter_mid(const BucketArgs &a, const int64_t *
     for (int64_t k0 = S; k0 < E; k0 += kPass) {
         const int R = __builtin_amdgcn_readfirstlane((int)min<int64_t>(E - k0, (int64_t)kPass));
         if (R == kPass)
-            scatter_mid_pass<true, kBits>(a, bnd, eb, lane, lbit, slot, k0, R);
+            scatter_mid_pass<IT, true, kBits>(a, bnd, eb, lane, lbit, slot, k0, R);
         else
-            scatter_mid_pass<false, kBits>(a, bnd, eb, lane, lbit, slot, k0, R);
+            scatter_mid_pass<IT, false, kBits>(a, bnd, eb, lane, lbit, slot, k0, R);
     }
 }
 
@@ -907,7 +921,7 @@ __device__ __forceinline__ void scatter_mid(const BucketArgs &a, const int64_t *
 // instantiation per method keeps each one's registers, and so its occupancy,
 // to what its own path needs; the bag-at-a-time path for out-of-order
 // offsets is in all of them.
-template <int kOwners>
+template <typename IT, int kOwners>
 __global__ __launch_bounds__(kBlock) void eb_bucket_scatter(const BucketArgs a)
 {
     extern __shared__ int64_t lds[];
@@ -929,7 +943,7 @@ __global__ __launch_bounds__(kBlock) void eb_bucket_scatter(const BucketArgs a)
     int64_t s = 0, e = 0, S, E;
     int64_t first_slot = 0;
     if (live) {
-        wave_bag_loads(a, p0, nb, lane, s, e);
+        wave_bag_loads<IT>(a, p0, nb, lane, s, e);
         if (G <= kWave && lane < G)
             first_slot = a.segments[lane] + (p0 % kStartStride == 0 ? a.starts[(int64_t)lane * a.nq + p0 / kStartStride]
                                                                    : a.out_offsets[(int64_t)lane * row + p0]);
@@ -949,9 +963,9 @@ __global__ __launch_bounds__(kBlock) void eb_bucket_scatter(const BucketArgs a)
         for (int64_t k0 = S; k0 < E; k0 += kPass) {
             const int R = __builtin_amdgcn_readfirstlane((int)min<int64_t>(E - k0, (int64_t)kPass));
             if (R == kPass)
-                scatter_few_pass<true>(a, fb, lane, l0, l1, l2, slot, k0, R);
+                scatter_few_pass<IT, true>(a, fb, lane, l0, l1, l2, slot, k0, R);
             else
-                scatter_few_pass<false>(a, fb, lane, l0, l1, l2, slot, k0, R);
+                scatter_few_pass<IT, false>(a, fb, lane, l0, l1, l2, slot, k0, R);
         }
         return;
     }
@@ -971,14 +985,14 @@ __global__ __launch_bounds__(kBlock) void eb_bucket_scatter(const BucketArgs a)
             for (int64_t k0 = S; k0 < E; k0 += kPass) {
                 const int R = __builtin_amdgcn_readfirstlane((int)min<int64_t>(E - k0, (int64_t)kPass));
                 if (R == kPass)
-                    scatter_tree_pass<true>(a, tb, lane, lbit, slot, k0, R);
+                    scatter_tree_pass<IT, true>(a, tb, lane, lbit, slot, k0, R);
                 else
-                    scatter_tree_pass<false>(a, tb, lane, lbit, slot, k0, R);
+                    scatter_tree_pass<IT, false>(a, tb, lane, lbit, slot, k0, R);
             }
         } else if constexpr (kOwners == 32) {
-            scatter_mid<5>(a, bnd, lane, first_slot, S, E);
+            scatter_mid<IT, 5>(a, bnd, lane, first_slot, S, E);
         } else if constexpr (kOwners == kWave) {
-            scatter_mid<6>(a, bnd, lane, first_slot, S, E);
+            scatter_mid<IT, 6>(a, bnd, lane, first_slot, S, E);
         }
         return;
     }
@@ -995,9 +1009,9 @@ __global__ __launch_bounds__(kBlock) void eb_bucket_scatter(const BucketArgs a)
         for (int64_t k0 = S; k0 < E; k0 += kPass) {
             const int R = __builtin_amdgcn_readfirstlane((int)min<int64_t>(E - k0, (int64_t)kPass));
             if (R == kPass)
-                scatter_many_pass<true>(a, bnd, eb, next, nbits, lane, k0, R);
+                scatter_many_pass<IT, true>(a, bnd, eb, next, nbits, lane, k0, R);
             else
-                scatter_many_pass<false>(a, bnd, eb, next, nbits, lane, k0, R);
+                scatter_many_pass<IT, false>(a, bnd, eb, next, nbits, lane, k0, R);
         }
         return;
     }
@@ -1012,10 +1026,10 @@ __global__ __launch_bounds__(kBlock) void eb_bucket_scatter(const BucketArgs a)
             int64_t id = 0;
             int g = -1;
             if (k < ej) {
-                id = __builtin_nontemporal_load(a.indices + k);
+                id = (int64_t)__builtin_nontemporal_load(ids_of<IT>(a) + k);
                 g = owner_of(bnd, G, id);
             }
-            scatter_chunk(a, next, lane, g, id);
+            scatter_chunk<IT>(a, next, lane, g, id);
         }
     }
 }
@@ -1097,29 +1111,31 @@ int64_t start_entries(int64_t TB) { return TB / kStartStride + 1; }
 
 // The count and scatter instantiations for G destinations (count_bags bags
 // per count wave).
+template <typename IT>
 const void *count_kernel(int G, int bags)
 {
     if (G <= kFewShards)
-        return bags == 64 ? (const void *)eb_bucket_count<64, kFewShards>
-               : bags == 32 ? (const void *)eb_bucket_count<32, kFewShards>
-                            : (const void *)eb_bucket_count<16, kFewShards>;
+        return bags == 64 ? (const void *)eb_bucket_count<IT, 64, kFewShards>
+               : bags == 32 ? (const void *)eb_bucket_count<IT, 32, kFewShards>
+                            : (const void *)eb_bucket_count<IT, 16, kFewShards>;
     if (G <= kTreeShards)
-        return bags == 64 ? (const void *)eb_bucket_count<64, kTreeShards>
-               : bags == 32 ? (const void *)eb_bucket_count<32, kTreeShards>
-                            : (const void *)eb_bucket_count<16, kTreeShards>;
-    return bags == 16  ? (const void *)eb_bucket_count<16, 0>
-           : bags == 8 ? (const void *)eb_bucket_count<8, 0>
-           : bags == 4 ? (const void *)eb_bucket_count<4, 0>
-                       : (const void *)eb_bucket_count<2, 0>;
+        return bags == 64 ? (const void *)eb_bucket_count<IT, 64, kTreeShards>
+               : bags == 32 ? (const void *)eb_bucket_count<IT, 32, kTreeShards>
+                            : (const void *)eb_bucket_count<IT, 16, kTreeShards>;
+    return bags == 16  ? (const void *)eb_bucket_count<IT, 16, 0>
+           : bags == 8 ? (const void *)eb_bucket_count<IT, 8, 0>
+           : bags == 4 ? (const void *)eb_bucket_count<IT, 4, 0>
+                       : (const void *)eb_bucket_count<IT, 2, 0>;
 }
 
+template <typename IT>
 const void *scatter_kernel(int G)
 {
-    return G <= kFewShards  ? (const void *)eb_bucket_scatter<kFewShards>
-           : G <= kTreeShards ? (const void *)eb_bucket_scatter<kTreeShards>
-           : G <= 32          ? (const void *)eb_bucket_scatter<32>
-           : G <= kWave       ? (const void *)eb_bucket_scatter<kWave>
-                              : (const void *)eb_bucket_scatter<kMaxShards>;
+    return G <= kFewShards  ? (const void *)eb_bucket_scatter<IT, kFewShards>
+           : G <= kTreeShards ? (const void *)eb_bucket_scatter<IT, kTreeShards>
+           : G <= 32          ? (const void *)eb_bucket_scatter<IT, 32>
+           : G <= kWave       ? (const void *)eb_bucket_scatter<IT, kWave>
+                              : (const void *)eb_bucket_scatter<IT, kMaxShards>;
 }
 
 } // namespace
@@ -1139,11 +1155,14 @@ int bucketize_workspace_impl(int32_t T, int64_t B, int32_t G, size_t *bytes)
     return EB_OK;
 }
 
-int bucketize_impl(int32_t T, int64_t B, int32_t G, const int64_t *bounds, const int64_t *indices,
-                   int64_t nnz, const int64_t *offsets, int64_t *out_offsets, int64_t *out_indices,
+int bucketize_impl(int32_t T, int64_t B, int32_t G, const int64_t *bounds, int32_t index_type,
+                   const void *indices, int64_t nnz, const void *offsets, int64_t *out_offsets, void *out_indices,
                    int64_t out_capacity, int64_t *segments, void *workspace, size_t workspace_bytes,
                    void *stream)
 {
+    if (index_type != EB_IDX_I64 && index_type != EB_IDX_I32)
+        return fail(EB_ERR_INVALID, "eb_bucketize: unknown index_type");
+    const bool i32 = index_type == EB_IDX_I32;
     size_t need = 0;
     const int rc = bucketize_workspace_impl(T, B, G, &need);
     if (rc != EB_OK) return rc;
@@ -1194,7 +1213,7 @@ int bucketize_impl(int32_t T, int64_t B, int32_t G, const int64_t *bounds, const
 
     if (TB > 0) {
         void *args[] = {&ba};
-        const void *count = count_kernel(G, cbags);
+        const void *count = i32 ? count_kernel<int32_t>(G, cbags) : count_kernel<int64_t>(G, cbags);
         hipError_t err = hipLaunchKernel(count, dim3((unsigned)(T * cbpt)), dim3(kBlock), args,
                                          count_lds_bytes(G, cbags), st);
         if (err != hipSuccess) return fail(EB_ERR_HIP, "eb_bucketize: %s", hipGetErrorString(err));
@@ -1205,7 +1224,8 @@ int bucketize_impl(int32_t T, int64_t B, int32_t G, const int64_t *bounds, const
         if (err == hipSuccess)
             err = hipLaunchKernel((const void *)eb_scan_tiles, dim3(sa.ntiles, G), dim3(kBlock), sargs, 0, st);
         if (err == hipSuccess)
-            err = hipLaunchKernel(scatter_kernel(G), dim3((unsigned)(T * bpt)), dim3(kBlock), args,
+            err = hipLaunchKernel(i32 ? scatter_kernel<int32_t>(G) : scatter_kernel<int64_t>(G),
+                                  dim3((unsigned)(T * bpt)), dim3(kBlock), args,
                                   scatter_lds_bytes(G), st);
         if (err != hipSuccess) return fail(EB_ERR_HIP, "eb_bucketize: %s", hipGetErrorString(err));
     } else {
@@ -1295,8 +1315,8 @@ int bucketize_noalloc_impl(int32_t T, int64_t B, int32_t G, const int64_t *bound
     void *ws = nullptr;
     const int rs = static_scratch("eb_bucketize_noalloc", (hipStream_t)stream, &ws);
     if (rs != EB_OK) return rs;
-    return bucketize_impl(T, B, G, bounds, indices, nnz, offsets, out_offsets, out_indices, out_capacity,
-                          segments, ws, kStaticScratchBytes, stream);
+    return bucketize_impl(T, B, G, bounds, EB_IDX_I64, indices, nnz, offsets, out_offsets, out_indices,
+                          out_capacity, segments, ws, kStaticScratchBytes, stream);
 }
 
 } // namespace
@@ -1318,10 +1338,23 @@ int eb_bucketize(int32_t T, int64_t B, int32_t G, const int64_t *bounds, const i
                  void *stream)
 {
     try {
-        return bucketize_impl(T, B, G, bounds, indices, nnz, offsets, out_offsets, out_indices, out_capacity,
-                              segments, workspace, workspace_bytes, stream);
+        return bucketize_impl(T, B, G, bounds, EB_IDX_I64, indices, nnz, offsets, out_offsets, out_indices,
+                              out_capacity, segments, workspace, workspace_bytes, stream);
     } catch (...) {
         return eb_detail::unexpected_exception("eb_bucketize");
+    }
+}
+
+int eb_bucketize_ex(int32_t T, int64_t B, int32_t G, const int64_t *bounds, int32_t index_type,
+                    const void *indices, int64_t nnz, const void *offsets, int64_t *out_offsets,
+                    void *out_indices, int64_t out_capacity, int64_t *segments, void *workspace,
+                    size_t workspace_bytes, void *stream)
+{
+    try {
+        return bucketize_impl(T, B, G, bounds, index_type, indices, nnz, offsets, out_offsets, out_indices,
+                              out_capacity, segments, workspace, workspace_bytes, stream);
+    } catch (...) {
+        return eb_detail::unexpected_exception("eb_bucketize_ex");
     }
 }
 

@@ -57,6 +57,8 @@ def library() -> ctypes.CDLL:
         lib.eb_bucketize_workspace.restype = ctypes.c_int
         lib.eb_bucketize.argtypes = [i32, i64, i32, p, p, i64, p, p, p, i64, p, p, ctypes.c_size_t, p]
         lib.eb_bucketize.restype = ctypes.c_int
+        lib.eb_bucketize_ex.argtypes = [i32, i64, i32, p, i32, p, i64, p, p, p, i64, p, p, ctypes.c_size_t, p]
+        lib.eb_bucketize_ex.restype = ctypes.c_int
         lib.eb_bucketize_noalloc.argtypes = [i32, i64, i32, p, p, i64, p, p, p, i64, p, p]
         lib.eb_bucketize_noalloc.restype = ctypes.c_int
         lib.eb_sum_partials.argtypes = [i32, p, i64, i32, i32, p, i64, p, p]
@@ -134,6 +136,15 @@ def eb_bucketize(T: int, B: int, G: int, bounds_ptr: int, indices_ptr: int | Non
                                   stream_ptr or None))
 
 
+def eb_bucketize_ex(T: int, B: int, G: int, bounds_ptr: int, index_type: int, indices_ptr: int | None,
+                    nnz: int, offsets_ptr: int, out_offsets_ptr: int, out_indices_ptr: int | None,
+                    out_capacity: int, segments_ptr: int, workspace_ptr: int | None, workspace_bytes: int,
+                    stream_ptr: int | None) -> None:
+    _check(library().eb_bucketize_ex(T, B, G, bounds_ptr, index_type, indices_ptr or None, nnz, offsets_ptr,
+                                     out_offsets_ptr, out_indices_ptr or None, out_capacity, segments_ptr,
+                                     workspace_ptr or None, workspace_bytes, stream_ptr or None))
+
+
 def eb_bucketize_noalloc(T: int, B: int, G: int, bounds_ptr: int, indices_ptr: int | None, nnz: int,
                          offsets_ptr: int, out_offsets_ptr: int, out_indices_ptr: int | None,
                          out_capacity: int, segments_ptr: int, stream_ptr: int | None) -> None:
@@ -159,11 +170,13 @@ def _same_device(dev, *tensors) -> None:
 
 
 def bucketize(bounds, indices, offsets, T: int, B: int, stream=None, capacity=None):
-    """Torch convenience for eb_bucketize.  ``bounds``: int64 device [T, G+1].
-    Returns (out_offsets [G, T*B+1], out_indices [capacity], segments [G+1],
-    workspace) on the device; ``capacity`` defaults to nnz (enough for
-    ordinary offsets).  The ids sent are out_indices[:segments[G]], of which
-    the first ``capacity`` are stored."""
+    """Torch convenience for eb_bucketize / eb_bucketize_ex.  ``bounds``:
+    int64 device [T, G+1]; ``indices`` and ``offsets`` both int64 or both
+    int32 (eb_bucketize_ex).  Returns (out_offsets [G, T*B+1] int64,
+    out_indices [capacity] of the indices' type, segments [G+1], workspace) on
+    the device; ``capacity`` defaults to nnz (enough for ordinary offsets).
+    The ids sent are out_indices[:segments[G]], of which the first
+    ``capacity`` are stored."""
     import torch
 
     dev = indices.device
@@ -171,22 +184,22 @@ def bucketize(bounds, indices, offsets, T: int, B: int, stream=None, capacity=No
         raise ValueError("indices must be a device tensor")
     _same_device(dev, bounds, offsets)
     G = int(bounds.shape[1]) - 1
-    for x in (bounds, indices, offsets):
-        if x.dtype != torch.int64 or not x.is_contiguous():
-            raise ValueError("bounds / indices / offsets must be contiguous int64")
+    if bounds.dtype != torch.int64 or not bounds.is_contiguous():
+        raise ValueError("bounds must be contiguous int64")
+    itype = _index_type(indices, offsets)
     if bounds.shape[0] != T or offsets.numel() != T * B + 1:
         raise ValueError("bounds must be [T, G+1] and offsets [T*B+1]")
     out_off = torch.empty((G, T * B + 1), dtype=torch.int64, device=dev)
     cap = indices.numel() if capacity is None else int(capacity)
-    out_idx = torch.empty(max(1, cap), dtype=torch.int64, device=dev)
+    out_idx = torch.empty(max(1, cap), dtype=indices.dtype, device=dev)
     seg = torch.empty(G + 1, dtype=torch.int64, device=dev)
     nbytes = eb_bucketize_workspace(T, B, G)
     ws = torch.empty(max(1, nbytes), dtype=torch.uint8, device=dev)
     if stream is None:
         stream = torch.cuda.current_stream(dev)
-    eb_bucketize(T, B, G, bounds.data_ptr(), indices.data_ptr() if indices.numel() else None,
-                 indices.numel(), offsets.data_ptr(), out_off.data_ptr(), out_idx.data_ptr(), cap,
-                 seg.data_ptr(), ws.data_ptr(), nbytes, stream.cuda_stream)
+    eb_bucketize_ex(T, B, G, bounds.data_ptr(), itype, indices.data_ptr() if indices.numel() else None,
+                    indices.numel(), offsets.data_ptr(), out_off.data_ptr(), out_idx.data_ptr(), cap,
+                    seg.data_ptr(), ws.data_ptr(), nbytes, stream.cuda_stream)
     return out_off, out_idx, seg, ws
 
 

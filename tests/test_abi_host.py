@@ -33,7 +33,7 @@ def all_declared_functions():
 
 
 def test_header_declares_the_boundary():
-    assert declared_functions() == ["eb_bucketize", "eb_bucketize_noalloc", "eb_bucketize_workspace",
+    assert declared_functions() == ["eb_bucketize", "eb_bucketize_ex", "eb_bucketize_noalloc", "eb_bucketize_workspace",
                                     "eb_create_tables", "eb_destroy", "eb_forward", "eb_forward_ex",
                                     "eb_last_error", "eb_sum_partials"]
 
@@ -246,6 +246,25 @@ def test_bucketize_rejects(kw):
 
 def test_bucketize_too_many_shards():
     assert code_of(lambda: bucketize(G=2000)) == eb.EB_ERR_UNSUPPORTED
+
+
+def bucketize_ex(**kw):
+    args = dict(T=2, B=4, G=2, bounds_ptr=FAKE, index_type=eb.EB_IDX_I32, indices_ptr=FAKE, nnz=10,
+                offsets_ptr=FAKE, out_offsets_ptr=FAKE, out_indices_ptr=FAKE, out_capacity=10,
+                segments_ptr=FAKE, workspace_ptr=FAKE, workspace_bytes=1 << 20, stream_ptr=None)
+    args.update(kw)
+    return eb.eb_bucketize_ex(**args)
+
+
+@pytest.mark.parametrize("kw", [
+    dict(index_type=2), dict(index_type=-1), dict(G=0), dict(nnz=-1), dict(indices_ptr=None),
+    dict(offsets_ptr=None), dict(out_indices_ptr=None), dict(workspace_bytes=8),
+])
+def test_bucketize_ex_rejects(kw):
+    """eb_bucketize_ex checks its index type and then every argument as
+    eb_bucketize does, before touching the device."""
+    assert code_of(lambda: bucketize_ex(**kw)) == eb.EB_ERR_INVALID
+    assert "eb_bucketize" in eb.eb_last_error()
 
 
 def sum_partials(**kw):

@@ -22,17 +22,22 @@ def even_bounds(rows, G):
     return np.array([[g * r // G for g in range(G + 1)] for r in rows], dtype=np.int64)
 
 
-def run_bucketize(bounds, idx, off, T, B, device, capacity=None):
-    """eb_bucketize on the device; out_indices has ``capacity`` entries
-    (default nnz).  Returns the stored ids: min(segments[G], capacity)."""
+def run_bucketize(bounds, idx, off, T, B, device, capacity=None, index_dtype=np.int64):
+    """eb_bucketize (eb_bucketize_ex for int32 ids and offsets) on the
+    device; out_indices has ``capacity`` entries (default nnz).  Returns the
+    stored ids, widened to int64: min(segments[G], capacity) of them."""
     d_b = torch.from_numpy(np.ascontiguousarray(bounds, dtype=np.int64)).to(device)
-    d_i = torch.from_numpy(np.ascontiguousarray(idx, dtype=np.int64)).to(device)
-    d_o = torch.from_numpy(np.ascontiguousarray(off, dtype=np.int64)).to(device)
+    if index_dtype == np.int32:
+        assert np.all(np.asarray(idx) == np.asarray(idx).astype(np.int32))
+        assert np.all(np.asarray(off) == np.asarray(off).astype(np.int32))
+    d_i = torch.from_numpy(np.ascontiguousarray(idx, dtype=index_dtype)).to(device)
+    d_o = torch.from_numpy(np.ascontiguousarray(off, dtype=index_dtype)).to(device)
     cap = len(idx) if capacity is None else capacity
     out_off, out_idx, seg, ws = eb.bucketize(d_b, d_i, d_o, T, B, capacity=cap)
     torch.cuda.synchronize()
     seg_h = seg.cpu().numpy()
-    return out_off.cpu().numpy(), out_idx.cpu().numpy()[:min(int(seg_h[-1]), cap)], seg_h
+    assert out_idx.dtype == d_i.dtype
+    return out_off.cpu().numpy(), out_idx.cpu().numpy()[:min(int(seg_h[-1]), cap)].astype(np.int64), seg_h
 
 
 def bucket_case(seed, G, T=None, B=None, maxL=40, uneven=False, oob=True):
@@ -51,9 +56,9 @@ def bucket_case(seed, G, T=None, B=None, maxL=40, uneven=False, oob=True):
     return T, B, idx, off, bounds
 
 
-def check_bucketize(T, B, idx, off, bounds, device, capacity=None):
+def check_bucketize(T, B, idx, off, bounds, device, capacity=None, index_dtype=np.int64):
     cap = len(idx) if capacity is None else capacity
-    got = run_bucketize(bounds, idx, off, T, B, device, capacity=cap)
+    got = run_bucketize(bounds, idx, off, T, B, device, capacity=cap, index_dtype=index_dtype)
     want = oracle.bucketize(bounds, idx, off, T, B, capacity=cap)
     for name, a, b in zip(("out_offsets", "out_indices", "segments"), got, want):
         assert np.array_equal(a, b), name
@@ -260,12 +265,52 @@ def draw_bucket_case(seed):
 @pytest.mark.parametrize("seed", range(40))
 def test_bucketize_random_config(seed, device):
     T, B, G, idx, off, bounds, unsorted, g = draw_bucket_case(5000 + seed)
+    itype = np.int32 if g.random() < 0.4 else np.int64
     if unsorted:
-        check_split(bounds, idx, off, T, B, run_bucketize(bounds, idx, off, T, B, device))
+        check_split(bounds, idx, off, T, B, run_bucketize(bounds, idx, off, T, B, device, index_dtype=itype))
         return
     total = int(oracle.bucketize(bounds, idx, off, T, B, capacity=0)[2][-1])
     cap = int(g.choice([len(idx), total, total // 2, total + 5]))
-    check_bucketize(T, B, idx, off, bounds, device, capacity=cap)
+    check_bucketize(T, B, idx, off, bounds, device, capacity=cap, index_dtype=itype)
+
+
+@pytest.mark.parametrize("G", [1, 3, 8, 12, 16, 40, 100, 1024])
+def test_bucketize_int32_ids(G, device):
+    """eb_bucketize_ex with int32 ids, offsets and out_indices over every
+    owner method: the oracle's result on the widened values, and bit for bit
+    the int64 call's."""
+    T, B, idx, off, bounds = bucket_case(G * 5 + 3, G, T=3, B=700, maxL=40)
+    check_bucketize(T, B, idx, off, bounds, device, index_dtype=np.int32)
+    a = run_bucketize(bounds, idx, off, T, B, device, index_dtype=np.int32)
+    b = run_bucketize(bounds, idx, off, T, B, device)
+    assert all(np.array_equal(x, y) for x, y in zip(a, b))
+
+
+@pytest.mark.parametrize("G", [3, 8, 16, 65])
+def test_bucketize_int32_limits_and_malformed_offsets(G, device):
+    """int32 ids at and next to both ends of int32 against int64 bounds that
+    reach past them, and int32 offsets that are negative, past nnz or go
+    back (clamped as for int64), at capacities that truncate and that hold
+    everything."""
+    g = np.random.default_rng(G + 77)
+    lo32, hi32 = np.iinfo(np.int32).min, np.iinfo(np.int32).max
+    T, B, nnz = 2, 300, 4000
+    near = np.array([lo32, lo32 + 1, -1, 0, 1, hi32 - 1, hi32], dtype=np.int64)
+    idx = np.where(g.random(nnz) < 0.2, g.choice(near, nnz), g.integers(-50, 5000, nnz)).astype(np.int64)
+    off = np.sort(g.integers(0, nnz + 1, T * B + 1)).astype(np.int64)
+    off[g.choice(T * B + 1, 40, replace=False)] = g.integers(-30, nnz + 30, 40)
+    bounds = np.array([[-2**40, *np.sort(g.integers(-100, 5000, G - 1)).tolist(), 2**40],
+                       [lo32, *np.sort(g.integers(0, 4000, G - 1)).tolist(), hi32]], dtype=np.int64)
+    total = int(oracle.bucketize(bounds, idx, off, T, B, capacity=0)[2][-1])
+    for cap in (nnz // 3, total):
+        check_bucketize(T, B, idx, off, bounds, device, capacity=cap, index_dtype=np.int32)
+
+
+@pytest.mark.parametrize("G,T,B", [(8, 3, 100_001), (16, 2, 75_000), (64, 3, 100_001)])
+def test_bucketize_int32_long_count_waves(G, T, B, device):
+    """int32 ids through count waves of 32 and 64 bags and the other sizes."""
+    T, B, idx, off, bounds = bucket_case(G * 11 + B, G, T=T, B=B, maxL=4)
+    check_bucketize(T, B, idx, off, bounds, device, index_dtype=np.int32)
 
 
 def test_bucketize_dlrm_batch(device):
