@@ -283,6 +283,14 @@ def _time_launches(torch, stream, fn, K, W):
     return ev0.elapsed_time(ev1) * 1e3 / K
 
 
+def scan_tile_count(T, B):
+    """Tiles of eb_bucketize's scan per destination: 2048 bags of one table,
+    or 2048 // B whole tables when B < 2048."""
+    if B >= 2048:
+        return T * -(-B // 2048)
+    return -(-T // (2048 // B))
+
+
 def exchange_bench(torch, dev, eb, K, W, Gs=(8,), i32=False):
     """The row-wise exchange's local kernels at the sizes of the skewed
     workloads split over GPUs by rows.  bucketize: the 26-table, 16384-bag
@@ -325,7 +333,7 @@ def exchange_bench(torch, dev, eb, K, W, Gs=(8,), i32=False):
                           "algorithmic_bytes": by, "algorithmic_GBps": round(by / us / 1e3, 1),
                           "frac_of_8TBps": round(by / us / 1e3 / HBM_PEAK_GBPS, 4),
                           # count, tile sums, (tile prefix when over 131072 tile sums,) tile scan, scatter
-                          "kernels_per_call": 4 if G * -(-TB // 2048) <= 131072 else 5}), flush=True)
+                          "kernels_per_call": 4 if G * scan_tile_count(w.T, w.B) <= 131072 else 5}), flush=True)
         del out_off, ws
     del d_i, out_idx
     Gp = 8  # the partial blocks of 8 GPUs, whatever --destinations says

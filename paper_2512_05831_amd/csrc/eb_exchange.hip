@@ -20,19 +20,21 @@
 //
 // eb_bucketize runs three kernels on the caller's stream (eb_bucketize_ex the
 // same with int32 ids, offsets and scattered ids, each widened on load):
-//   1. count   : a wave takes 2 to 64 consecutive bags (for up to 16
+//   1. count   : a wave takes 8 to 64 consecutive bags (for up to 16
 //                destinations the most of 16, 32, 64 that leave at least
-//                4608 waves, else 16, and 8 or fewer beyond 64; each XCD one
+//                4608 waves, else 16, and 8 beyond 64; each XCD one
 //                contiguous run of workgroups); each id's owner by
 //                comparisons with the table's block bounds (up to 16 blocks:
 //                a search tree evaluated as wave-wide lane masks) or by
 //                binary search over them (staged in LDS); for ordinary CSR
-//                offsets and up to 64 destinations the wave streams its whole
-//                id range in 64-id chunks into a [bag][destination] histogram
-//                in LDS, else it walks the bags one at a time; counts land in out_offsets[g][p + 1]
-//                (coalesced per destination).
+//                offsets the wave streams its whole id range in 64-id chunks
+//                into a [bag][destination] histogram in LDS, else it walks
+//                the bags one at a time; counts land
+//                in out_offsets[g][p + 1] (coalesced per destination), the
+//                wave's total per destination in the workspace.
 //   2. scan    : inclusive scan of every destination's row of counts
-//                (reduce-then-scan over 2048-entry tiles: tile sums in the
+//                (reduce-then-scan over tiles of up to 2048 entries made of
+//                whole count waves: tile sums from the wave totals into the
 //                workspace; each tile then adds up its row's earlier tiles,
 //                and the rows' first tiles the segments; with more than
 //                131072 tile sums one workgroup first scans them as one
@@ -259,13 +261,11 @@ __device__ __forceinline__ int owner_by_eighths(const int64_t *bnd, int G, const
 // A count wave takes 16, 32 or 64 bags up to 16 destinations (the most that
 // still leave at least kCountWavesMin waves, since count's waves are short
 // and each starts with a dependent load of its offsets, which longer waves
-// pay less often), 16 up to 64 destinations and 8 or fewer beyond
-// (count_bags).
+// pay less often), 16 up to 64 destinations and 8 beyond (count_bags).
 constexpr int kBagsPerWave = 16;
 constexpr int kBagsPerBlock = kBagsPerWave * kWavesPerBlock;
 static_assert(kBagsPerWave <= kWave && (kBagsPerWave & (kBagsPerWave - 1)) == 0, "bags per wave");
 constexpr int64_t kCountWavesMin = 4608; // 18 per compute unit
-constexpr int kCountHistBytes = 32768; // count's per-wave [bag][destination] histogram, at most
 constexpr int kCountChunks = 4;   // 64-id chunks loaded ahead by count
 constexpr int kScatterChunks = 8; // and by scatter (measured best for each)
 
@@ -278,6 +278,8 @@ struct BucketArgs {
     const int64_t *segments; // [G+1] (scatter pass)
     const int64_t *starts;   // [G][nq]: out_offsets[g][16 q] (scatter pass; workspace)
     int64_t nq;
+    int64_t *wave_totals;    // [nparts][G]: each count wave's ids per destination (workspace)
+    int64_t nparts;          // T * count_waves_per_table
     int64_t out_cap;         // entries of out_indices; positions at or past it are not written
     int64_t nnz;
     int64_t B;
@@ -285,6 +287,7 @@ struct BucketArgs {
     int32_t G;
     int32_t blocks_per_table;       // scatter's workgroups per table
     int32_t count_blocks_per_table; // count's
+    int32_t count_waves_per_table;  // count's waves that hold bags, per table
 };
 
 // The batch's index type IT (int64_t or int32_t) types the ids, the offsets
@@ -314,8 +317,10 @@ __device__ __forceinline__ int xcd_run_block(int b, int n)
 // Dynamic LDS: the table's G+1 bounds, then one area per wave.
 // count's histogram row per bag: 8 entries for up to 8 destinations and 16
 // for up to 16 (an index by shift), else G.
-__host__ __device__ inline int count_stride(int G) { return G <= kFewShards ? kFewShards : G <= kTreeShards ? kTreeShards : G; }
-__host__ __device__ inline size_t count_wave_bytes(int G, int bags) { return (size_t)4 * count_stride(G) * bags; }
+__host__ __device__ constexpr int count_stride(int G) { return G <= kFewShards ? kFewShards : G <= kTreeShards ? kTreeShards : G; }
+__host__ __device__ constexpr size_t count_wave_bytes(int G, int bags) { return (size_t)4 * count_stride(G) * bags; }
+// 8-bag waves keep the histogram of the most destinations within 32 KB.
+static_assert(count_wave_bytes(kMaxShards, 8) <= 32768, "count histogram");
 __host__ __device__ inline size_t count_lds_bytes(int G, int bags) { return (size_t)(G + 1) * 8 + kWavesPerBlock * count_wave_bytes(G, bags); }
 __host__ __device__ inline size_t scatter_lds_bytes(int G) { return (size_t)(G + 1) * 8 + (size_t)kWavesPerBlock * G * 8; }
 
@@ -323,6 +328,13 @@ __device__ __forceinline__ int64_t shfl_down64(int64_t v, int d)
 {
     const int lo = __shfl_down((int)(v & 0xFFFFFFFF), d);
     const int hi = __shfl_down((int)(v >> 32), d);
+    return ((int64_t)hi << 32) | (uint32_t)lo;
+}
+
+__device__ __forceinline__ int64_t shfl_xor64(int64_t v, int m)
+{
+    const int lo = __shfl_xor((int)(v & 0xFFFFFFFF), m);
+    const int hi = __shfl_xor((int)(v >> 32), m);
     return ((int64_t)hi << 32) | (uint32_t)lo;
 }
 
@@ -436,7 +448,7 @@ __device__ __forceinline__ void count_chunks(const BucketArgs &a, const int64_t 
 template <typename IT, int kBags, int kOwners>
 __global__ __launch_bounds__(kBlock) void eb_bucket_count(const BucketArgs a)
 {
-    static_assert(kBags <= kWave && (kBags & (kBags - 1)) == 0, "bags per count wave");
+    static_assert(kBags >= 8 && kBags <= kWave && (kBags & (kBags - 1)) == 0, "bags per count wave");
     extern __shared__ int64_t lds[];
     const int G = a.G;
     int64_t *bnd = lds;
@@ -460,6 +472,9 @@ __global__ __launch_bounds__(kBlock) void eb_bucket_count(const BucketArgs a)
     const bool contiguous = wave_bags(a, nb, lane, s, e, S, E);
     if (p0 == 0)
         for (int g = lane; g < G; g += kWave) a.out_offsets[(int64_t)g * row] = 0;
+    // The wave's totals per destination (one contiguous run), for the scan's
+    // tile sums.
+    int64_t *totals = a.wave_totals + ((int64_t)t * a.count_waves_per_table + b0 / kBags) * G;
 
     if (contiguous) {
         const uint64_t bags = __ballot(lane < nb);
@@ -479,9 +494,36 @@ __global__ __launch_bounds__(kBlock) void eb_bucket_count(const BucketArgs a)
             const int j = x & (kBags - 1), g = x / kBags;
             if (j < nb) a.out_offsets[(int64_t)g * row + p0 + j + 1] = hist[j * stride + g];
         }
+        // The wave's totals: up to 64 destinations, lane q * Gp + g (Gp =
+        // G rounded up to a power of two) adds up destination g over every
+        // (64 / Gp)-th bag from bag q on, then the lanes of each destination
+        // combine; beyond 64 (8 bags), lane g + 64 r adds up destination g +
+        // 64 r over all bags.
+        if (kOwners != 0 || G <= kWave) { // the compare trees take at most 16
+            const int Gp = 1 << (32 - __builtin_clz((unsigned)(2 * G - 1)) - 1);
+            const int P = kWave / Gp, g = lane & (Gp - 1), q = lane / Gp;
+            int64_t sum = 0;
+            if (g < G) {
+#pragma unroll 4
+                for (int j = q; j < nb; j += P) sum += hist[j * stride + g];
+            }
+            for (int o = Gp; o < kWave; o <<= 1) sum += shfl_xor64(sum, o);
+            if (q == 0 && g < G) totals[g] = sum;
+        } else if constexpr (kOwners == 0) {
+            for (int g = lane; g < G; g += kWave) {
+                int64_t sum = 0;
+#pragma unroll
+                for (int j = 0; j < kBags; ++j) sum += j < nb ? hist[j * stride + g] : 0;
+                totals[g] = sum;
+            }
+        }
         return;
     }
-    // Any offsets, any G: one bag at a time.
+    // Any offsets, any G: one bag at a time, with the running totals in the
+    // wave's LDS area after the bag's G counts (it holds 4 * count_stride(G)
+    // * kBags >= 12 G bytes, since kBags >= 8 beyond 16 destinations).
+    int64_t *run = (int64_t *)(hist + ((G + 1) & ~1));
+    for (int g = lane; g < G; g += kWave) run[g] = 0;
     for (int j = 0; j < nb; ++j) {
         const int64_t sj = readlane64(s, j), ej = readlane64(e, j);
         for (int g = lane; g < G; g += kWave) hist[g] = 0;
@@ -491,9 +533,13 @@ __global__ __launch_bounds__(kBlock) void eb_bucket_count(const BucketArgs a)
             if (g >= 0) atomicAdd(&hist[g], 1);
         }
         wave_sync_lds();
-        for (int g = lane; g < G; g += kWave) a.out_offsets[(int64_t)g * row + p0 + j + 1] = hist[g];
+        for (int g = lane; g < G; g += kWave) {
+            a.out_offsets[(int64_t)g * row + p0 + j + 1] = hist[g];
+            run[g] += hist[g];
+        }
         wave_sync_lds();
     }
+    for (int g = lane; g < G; g += kWave) totals[g] = run[g];
 }
 
 // Wave-level inclusive scan of one int64 per lane (Hillis-Steele over 64 lanes).
@@ -534,12 +580,51 @@ struct ScanArgs {
     int64_t *tile_sums; // [G][ntiles]
     int64_t *segments;  // [G+1]
     int64_t *starts;    // [G][nq]: every 16th entry of each row, starts[g][q] = rows[g][16 q]
+    const int64_t *wave_totals; // [nparts][G]: count's totals per wave (T * waves_per_table)
+    int64_t nparts;
     int64_t nq;         // TB / 16 + 1
     int64_t TB;
+    int64_t B;
+    int32_t T;
     int32_t G;
     int32_t ntiles;
+    int32_t tiles_per_group;  // tiles per group of tables_per_tile tables
+    int32_t tables_per_tile;  // 1 when B >= kScanTile
+    int32_t waves_per_table;  // count's waves holding bags, per table
+    int32_t bags_per_wave;    // count's (a power of two dividing kScanTile)
     int32_t fused;      // pass 2c takes the tile prefixes and segments from the raw tile sums
 };
+
+// The scan's tiles are made of whole count waves, so that their sums are sums
+// of count's wave totals: with B >= kScanTile bags per table, tile k holds
+// bags [k' kScanTile, (k' + 1) kScanTile) of one table (k' = k mod tiles per
+// table, the last one ragged); with fewer, it holds kScanTile / B whole
+// tables (the last tile fewer).  Either way a tile is a run of consecutive
+// positions (rows entries lo + 1 ... lo + n) and its waves a run of
+// consecutive wave totals (plo ... plo + pn - 1), at most kScanTile of each.
+struct ScanTile {
+    int64_t lo, plo;
+    int n, pn;
+};
+
+__device__ __forceinline__ ScanTile scan_tile(const ScanArgs &a, int k)
+{
+    const int grp = k / a.tiles_per_group, kk = k - grp * a.tiles_per_group;
+    const int64_t t0 = (int64_t)grp * a.tables_per_tile;
+    const int64_t t1 = min<int64_t>(a.T, t0 + a.tables_per_tile);
+    const int per = kScanTile / a.bags_per_wave; // waves per full tile of one table
+    ScanTile r;
+    r.lo = t0 * a.B + (int64_t)kk * kScanTile;
+    r.plo = t0 * a.waves_per_table + (int64_t)kk * per;
+    if (a.tables_per_tile == 1) {
+        r.n = (int)min<int64_t>(kScanTile, a.B - (int64_t)kk * kScanTile);
+        r.pn = (int)min<int64_t>(per, a.waves_per_table - (int64_t)kk * per);
+    } else {
+        r.n = (int)((t1 - t0) * a.B);
+        r.pn = (int)((t1 - t0) * a.waves_per_table);
+    }
+    return r;
+}
 
 // Pass 2c adds up the earlier tile sums itself (no pass 2b) while every
 // workgroup reads at most this many of them: a row's first tile reads all
@@ -551,32 +636,54 @@ constexpr int64_t kFusedScanMax = 131072;
 // array, where the scatter's waves (kBagsPerWave bags each) find their first
 // output slots: 16 waves share a line there instead of one each in the rows.
 constexpr int kStartStride = 16;
-static_assert(kScanTile % kStartStride == 0 && kBlock % kStartStride == 0, "scan tiles start at multiples of the stride");
 
 constexpr int kScanPer = kScanTile / kBlock; // counts per thread in a tile
 static_assert(kScanTile % kBlock == 0, "scan tile");
 
-// Pass 2a: sum of every tile (entries 1 + k*kScanTile ... of row g); all of a
-// thread's loads are issued before the first is used.
+// Pass 2a: tile k's sums for destinations d0 ... d0 + Gy - 1 (d0 =
+// blockIdx.y * 256, Gy <= 256), from the totals of the tile's count waves.
+// Thread x adds up destination d0 + x % Gy over every R-th wave from wave
+// x / Gy on (R = 256 / Gy waves side by side, so that each step reads R
+// waves' totals as one run when Gy = G); then thread d < Gy adds up the R
+// partial sums of its destination.
+constexpr int kSumAhead = 8; // loads issued before the first is added
+
 __global__ __launch_bounds__(kBlock) void eb_scan_tile_sums(const ScanArgs a)
 {
-    const int g = blockIdx.y;
+    __shared__ int64_t part[kBlock];
     const int k = blockIdx.x;
-    const int64_t *row = a.rows + (int64_t)g * (a.TB + 1) + 1;
-    const int64_t lo = (int64_t)k * kScanTile;
-    const int n = (int)std::min<int64_t>(kScanTile, a.TB - lo);
-    int64_t v[kScanPer];
-#pragma unroll
-    for (int j = 0; j < kScanPer; ++j) {
-        const int i = j * kBlock + threadIdx.x;
-        v[j] = i < n ? row[lo + i] : 0;
-    }
+    const int d0 = blockIdx.y * kBlock;
+    const int Gy = min(kBlock, a.G - d0);
+    const int R = kBlock / Gy;
+    const int r = threadIdx.x / Gy, d = threadIdx.x - r * Gy;
+    const ScanTile tl = scan_tile(a, k);
     int64_t sum = 0;
+    if (r < R) {
+        const int64_t *src = a.wave_totals + tl.plo * a.G + d0 + d;
+        for (int i0 = r; i0 < tl.pn; i0 += R * kSumAhead) {
+            int64_t v[kSumAhead];
 #pragma unroll
-    for (int j = 0; j < kScanPer; ++j) sum += v[j];
-    int64_t total;
-    block_inclusive_scan(sum, &total);
-    if (threadIdx.x == 0) a.tile_sums[(int64_t)g * a.ntiles + k] = total;
+            for (int j = 0; j < kSumAhead; ++j) {
+                const int i = i0 + j * R;
+                v[j] = i < tl.pn ? src[(int64_t)i * a.G] : 0;
+            }
+#pragma unroll
+            for (int j = 0; j < kSumAhead; ++j) sum += v[j];
+        }
+    }
+    part[threadIdx.x] = sum;
+    __syncthreads();
+    if (threadIdx.x < Gy) {
+        int64_t total = 0;
+        for (int q0 = 0; q0 < R; q0 += kSumAhead) {
+            int64_t v[kSumAhead];
+#pragma unroll
+            for (int j = 0; j < kSumAhead; ++j) v[j] = q0 + j < R ? part[(q0 + j) * Gy + threadIdx.x] : 0;
+#pragma unroll
+            for (int j = 0; j < kSumAhead; ++j) total += v[j];
+        }
+        a.tile_sums[(int64_t)(d0 + threadIdx.x) * a.ntiles + k] = total;
+    }
 }
 
 // Pass 2b: the tile sums of all rows, row after row, as one sequence: its
@@ -636,8 +743,9 @@ __global__ __launch_bounds__(kBlock) void eb_scan_tiles(const ScanArgs a)
     const int g = blockIdx.y;
     const int k = blockIdx.x;
     int64_t *row = a.rows + (int64_t)g * (a.TB + 1) + 1;
-    const int64_t lo = (int64_t)k * kScanTile;
-    const int n = (int)std::min<int64_t>(kScanTile, a.TB - lo);
+    const ScanTile tl = scan_tile(a, k);
+    const int64_t lo = tl.lo;
+    const int n = tl.n;
     int64_t v[kScanPer];
 #pragma unroll
     for (int j = 0; j < kScanPer; ++j) {
@@ -683,18 +791,17 @@ __global__ __launch_bounds__(kBlock) void eb_scan_tiles(const ScanArgs a)
 #pragma unroll
     for (int j = 0; j < kScanPer; ++j) sm[scan_slot(threadIdx.x * kScanPer + j)] = base + v[j];
     __syncthreads();
-    // Thread x writes entries lo + j * 256 + x + 1 of the row; where that is
-    // a multiple of 16 (x % 16 == 15: tiles and j * 256 are), also starts[]
-    // at its index / 16.
-    const bool keeps = threadIdx.x % kStartStride == kStartStride - 1;
-    int64_t *start = a.starts + (int64_t)g * a.nq + lo / kStartStride + (threadIdx.x + 1) / kStartStride;
+    // Thread x writes entries lo + j * 256 + x + 1 of the row, and where that
+    // is a multiple of 16 also starts[] at its index / 16.
+    int64_t *start = a.starts + (int64_t)g * a.nq;
 #pragma unroll
     for (int j = 0; j < kScanPer; ++j) {
         const int i = j * kBlock + threadIdx.x;
         if (i < n) {
             const int64_t x = sm[scan_slot(i)];
             row[lo + i] = x;
-            if (keeps) start[j * (kBlock / kStartStride)] = x;
+            const uint64_t entry = (uint64_t)(lo + i + 1);
+            if (entry % kStartStride == 0) start[entry / kStartStride] = x;
         }
     }
     if (k == 0 && threadIdx.x == 0) a.starts[(int64_t)g * a.nq] = 0;
@@ -1087,27 +1194,53 @@ __global__ __launch_bounds__(kBlock) void eb_sum_partials_scalar(const PartialAr
     }
 }
 
-int64_t scan_tiles(int64_t TB) { return std::max<int64_t>(1, (TB + kScanTile - 1) / kScanTile); }
 
 // Bags per count wave for T*B bags in all and G destinations (see
 // kCountWavesMin).  Only the compare-tree paths (G <= 16, 8 or 16 histogram
 // entries per bag) gain from longer waves; 17 to 64 destinations take 16
-// bags, more take 8, fewer when their [bag][destination] histogram would pass
-// kCountHistBytes (measured: 8 bags beat 16 at 200 destinations, and at 1024
-// beat 2 or 4 even though the histograms then limit a compute unit to 4 waves).
+// bags, more take 8 (measured: 8 bags beat 16 at 200 destinations, and at
+// 1024 beat 2 or 4 even though the histograms then limit a compute unit to 4
+// waves).  Always a power of two from 8 to 64, so that it divides the scan's
+// 2048-bag tiles.
 int count_bags(int64_t TB, int G)
 {
-    if (G > kWave) {
-        int bags = 8;
-        while (bags > 2 && count_wave_bytes(G, bags) > (size_t)kCountHistBytes) bags /= 2;
-        return bags;
-    }
+    if (G > kWave) return 8;
     if (G > kTreeShards) return 16;
     for (int bags = 64; bags > 16; bags /= 2)
         if (TB / bags >= kCountWavesMin) return bags;
     return 16;
 }
 int64_t start_entries(int64_t TB) { return TB / kStartStride + 1; }
+
+// The shape of one call's scan (see scan_tile) and the workspace it takes.
+struct ScanShape {
+    int64_t ntiles;          // at least 1, also without bags
+    int64_t tiles_per_group;
+    int64_t tables_per_tile;
+    int64_t waves_per_table; // count's waves holding bags, per table
+    int64_t nparts;          // T * waves_per_table
+    int bags_per_wave;
+};
+
+ScanShape scan_shape(int32_t T, int64_t B, int32_t G)
+{
+    ScanShape s;
+    s.bags_per_wave = count_bags((int64_t)T * B, G);
+    s.waves_per_table = (B + s.bags_per_wave - 1) / s.bags_per_wave;
+    s.nparts = (int64_t)T * s.waves_per_table;
+    s.tiles_per_group = B >= kScanTile ? (B + kScanTile - 1) / kScanTile : 1;
+    s.tables_per_tile = B >= kScanTile ? 1 : kScanTile / std::max<int64_t>(B, 1);
+    s.ntiles = T > 0 && B > 0 ? (T + s.tables_per_tile - 1) / s.tables_per_tile * s.tiles_per_group : 1;
+    return s;
+}
+
+// Workspace entries (int64): tile sums, every 16th entry of each
+// destination's offsets, count's wave totals.
+int64_t workspace_entries(int32_t T, int64_t B, int32_t G)
+{
+    const ScanShape s = scan_shape(T, B, G);
+    return (int64_t)G * (s.ntiles + start_entries((int64_t)T * B) + s.nparts);
+}
 
 // The count and scatter instantiations for G destinations (count_bags bags
 // per count wave).
@@ -1122,10 +1255,7 @@ const void *count_kernel(int G, int bags)
         return bags == 64 ? (const void *)eb_bucket_count<IT, 64, kTreeShards>
                : bags == 32 ? (const void *)eb_bucket_count<IT, 32, kTreeShards>
                             : (const void *)eb_bucket_count<IT, 16, kTreeShards>;
-    return bags == 16  ? (const void *)eb_bucket_count<IT, 16, 0>
-           : bags == 8 ? (const void *)eb_bucket_count<IT, 8, 0>
-           : bags == 4 ? (const void *)eb_bucket_count<IT, 4, 0>
-                       : (const void *)eb_bucket_count<IT, 2, 0>;
+    return bags == 16 ? (const void *)eb_bucket_count<IT, 16, 0> : (const void *)eb_bucket_count<IT, 8, 0>;
 }
 
 template <typename IT>
@@ -1150,8 +1280,7 @@ int bucketize_workspace_impl(int32_t T, int64_t B, int32_t G, size_t *bytes)
     if (G > kMaxShards) return fail(EB_ERR_UNSUPPORTED, "eb_bucketize_workspace: more than 1024 shards");
     if (T > 0 && B > std::numeric_limits<int64_t>::max() / T / G / 8)
         return fail(EB_ERR_INVALID, "eb_bucketize_workspace: sizes overflow");
-    // tile sums, then every 16th entry of each destination's offsets
-    *bytes = (size_t)G * (size_t)(scan_tiles((int64_t)T * B) + start_entries((int64_t)T * B)) * sizeof(int64_t);
+    *bytes = (size_t)workspace_entries(T, B, G) * sizeof(int64_t);
     return EB_OK;
 }
 
@@ -1194,21 +1323,34 @@ int bucketize_impl(int32_t T, int64_t B, int32_t G, const int64_t *bounds, int32
     if (TB > 0 && (int64_t)T * bpt > std::numeric_limits<int32_t>::max())
         return fail(EB_ERR_UNSUPPORTED, "eb_bucketize: batch too large for one launch");
     ba.blocks_per_table = (int32_t)bpt;
-    const int cbags = count_bags(TB, G);
+    const ScanShape shape = scan_shape(T, B, G);
+    const int cbags = shape.bags_per_wave;
     const int64_t cbpt = (B + cbags * kWavesPerBlock - 1) / (cbags * kWavesPerBlock);
     ba.count_blocks_per_table = (int32_t)cbpt;
+    ba.count_waves_per_table = (int32_t)shape.waves_per_table;
 
+    // Workspace: tile sums [G][ntiles], starts [G][nq], wave totals [nparts][G].
     ScanArgs sa;
     sa.rows = out_offsets;
     sa.tile_sums = (int64_t *)workspace;
     sa.nq = start_entries(TB);
-    sa.starts = sa.tile_sums + (int64_t)G * scan_tiles(TB);
+    sa.starts = sa.tile_sums + (int64_t)G * shape.ntiles;
+    sa.nparts = shape.nparts;
+    sa.wave_totals = sa.starts + (int64_t)G * sa.nq;
     ba.starts = sa.starts;
     ba.nq = sa.nq;
+    ba.wave_totals = sa.starts + (int64_t)G * sa.nq;
+    ba.nparts = shape.nparts;
     sa.segments = segments;
     sa.TB = TB;
+    sa.B = B;
+    sa.T = T;
     sa.G = G;
-    sa.ntiles = (int32_t)scan_tiles(TB);
+    sa.ntiles = (int32_t)shape.ntiles;
+    sa.tiles_per_group = (int32_t)shape.tiles_per_group;
+    sa.tables_per_tile = (int32_t)shape.tables_per_tile;
+    sa.waves_per_table = (int32_t)shape.waves_per_table;
+    sa.bags_per_wave = cbags;
     sa.fused = (int64_t)G * sa.ntiles <= kFusedScanMax ? 1 : 0;
 
     if (TB > 0) {
@@ -1218,7 +1360,8 @@ int bucketize_impl(int32_t T, int64_t B, int32_t G, const int64_t *bounds, int32
                                          count_lds_bytes(G, cbags), st);
         if (err != hipSuccess) return fail(EB_ERR_HIP, "eb_bucketize: %s", hipGetErrorString(err));
         void *sargs[] = {&sa};
-        err = hipLaunchKernel((const void *)eb_scan_tile_sums, dim3(sa.ntiles, G), dim3(kBlock), sargs, 0, st);
+        err = hipLaunchKernel((const void *)eb_scan_tile_sums, dim3(sa.ntiles, (G + kBlock - 1) / kBlock),
+                              dim3(kBlock), sargs, 0, st);
         if (err == hipSuccess && !sa.fused)
             err = hipLaunchKernel((const void *)eb_scan_tile_prefix, dim3(1), dim3(kBlock), sargs, 0, st);
         if (err == hipSuccess)
