@@ -291,6 +291,13 @@ def scan_tile_count(T, B):
     return -(-T // (2048 // B))
 
 
+def fused_scan(G, ntiles):
+    """Whether eb_bucketize's tile scan adds up the earlier tile sums itself
+    (G * ntiles * (ntiles + G) / 2 tile-sum reads up to 2^20) instead of
+    after a pass over each destination's row of tile sums."""
+    return 0.5 * G * ntiles * (ntiles + G) <= 1 << 20
+
+
 def exchange_bench(torch, dev, eb, K, W, Gs=(8,), i32=False):
     """The row-wise exchange's local kernels at the sizes of the skewed
     workloads split over GPUs by rows.  bucketize: the 26-table, 16384-bag
@@ -332,8 +339,9 @@ def exchange_bench(torch, dev, eb, K, W, Gs=(8,), i32=False):
                           "us_per_call": round(us, 1), "ids_per_s": idx.size / us * 1e6,
                           "algorithmic_bytes": by, "algorithmic_GBps": round(by / us / 1e3, 1),
                           "frac_of_8TBps": round(by / us / 1e3 / HBM_PEAK_GBPS, 4),
-                          # count, tile sums, (tile prefix when over 131072 tile sums,) tile scan, scatter
-                          "kernels_per_call": 4 if G * scan_tile_count(w.T, w.B) <= 131072 else 5}), flush=True)
+                          # count, tile sums, (row prefix when the fused tile scan would read
+                          # over 2^20 tile sums,) tile scan, scatter
+                          "kernels_per_call": 4 if fused_scan(G, scan_tile_count(w.T, w.B)) else 5}), flush=True)
         del out_off, ws
     del d_i, out_idx
     Gp = 8  # the partial blocks of 8 GPUs, whatever --destinations says

@@ -36,10 +36,11 @@
 //                (reduce-then-scan over tiles of up to 2048 entries made of
 //                whole count waves: tile sums from the wave totals into the
 //                workspace; each tile then adds up its row's earlier tiles,
-//                and the rows' first tiles the segments; with more than
-//                131072 tile sums one workgroup first scans them as one
-//                sequence instead); every 16th scanned entry of each row
-//                is also copied to the workspace for the scatter.
+//                and the rows' first tiles the segments; where that would
+//                read too many tile sums, a workgroup per destination first
+//                scans its row's tile sums instead); every 16th scanned
+//                entry of each row is also copied to the workspace for the
+//                scatter.
 //   3. scatter : waves of 16 bags; ids are written to segments[g] +
 //                out_offsets[g][p] + rank (a wave's first out_offsets from
 //                the workspace copy), the rank counting earlier ids of
@@ -580,6 +581,7 @@ struct ScanArgs {
     int64_t *tile_sums; // [G][ntiles]
     int64_t *segments;  // [G+1]
     int64_t *starts;    // [G][nq]: every 16th entry of each row, starts[g][q] = rows[g][16 q]
+    int64_t *row_totals; // [G]: each row's total (pass 2b only)
     const int64_t *wave_totals; // [nparts][G]: count's totals per wave (T * waves_per_table)
     int64_t nparts;
     int64_t nq;         // TB / 16 + 1
@@ -626,11 +628,16 @@ __device__ __forceinline__ ScanTile scan_tile(const ScanArgs &a, int k)
     return r;
 }
 
-// Pass 2c adds up the earlier tile sums itself (no pass 2b) while every
-// workgroup reads at most this many of them: a row's first tile reads all
-// earlier rows' sums (at most 1 MB, from L2), still far quicker than one
-// workgroup scanning them all in sequence.
-constexpr int64_t kFusedScanMax = 131072;
+// Pass 2c adds up the earlier tile sums itself (no pass 2b) while that
+// reads few of them: tile k of a row reads its row's k earlier sums and each
+// row's first tile all earlier rows' sums, G * ntiles * (ntiles + G) / 2 in
+// all.  Up to kFusedScanReads that costs less than pass 2b's launch
+// (measured on workload 3's batch: 16 and 32 destinations, 0.37 M and 0.8 M
+// reads, 2.1 and 2.8 us faster fused; 64 and 200, 1.8 M and 8.5 M reads,
+// 2.3 and 39 us slower).
+constexpr double kFusedScanReads = 1 << 20;
+
+bool fused_scan(int64_t G, int64_t ntiles) { return 0.5 * G * ntiles * (double)(ntiles + G) <= kFusedScanReads; }
 
 // The scan also keeps every kStartStride-th entry of each row in a compact
 // array, where the scatter's waves (kBagsPerWave bags each) find their first
@@ -686,55 +693,55 @@ __global__ __launch_bounds__(kBlock) void eb_scan_tile_sums(const ScanArgs a)
     }
 }
 
-// Pass 2b: the tile sums of all rows, row after row, as one sequence: its
-// exclusive scan at a row's first tile is that destination's segment start,
-// and the scan minus it is the tile's prefix within its row (written back in
-// place).  One workgroup; every thread takes a contiguous run of tiles.  Run
-// only beyond kFusedScanMax tile sums, or to fill the outputs of a batch
-// without bags.
-__global__ __launch_bounds__(kBlock) void eb_scan_tile_prefix(const ScanArgs a)
+// Pass 2b, where the fused tile scan would read too many tile sums (past
+// kFusedScanReads): one workgroup per
+// row scans the row's tile sums in place into each tile's prefix within the
+// row (exclusive), kScanTile at a time, and stores the row's total in
+// row_totals[g], from which the row's first tile takes its segment start.
+__global__ __launch_bounds__(kBlock) void eb_scan_row_prefix(const ScanArgs a)
 {
-    __shared__ int64_t seg[kMaxShards];
-    if (a.ntiles == 0) { // no bags: every destination is empty, its offsets the single 0
-        for (int g = threadIdx.x; g < a.G; g += kBlock) {
-            a.rows[g] = 0;
-            a.segments[g] = 0;
+    const int g = blockIdx.x;
+    int64_t *ts = a.tile_sums + (int64_t)g * a.ntiles;
+    int64_t carry = 0;
+    for (int64_t c0 = 0; c0 < a.ntiles; c0 += kScanTile) {
+        // thread x takes the kScanPer consecutive sums from c0 + kScanPer x
+        const int64_t lo = c0 + (int64_t)threadIdx.x * kScanPer;
+        int64_t v[kScanPer];
+#pragma unroll
+        for (int j = 0; j < kScanPer; ++j) v[j] = lo + j < a.ntiles ? ts[lo + j] : 0;
+        int64_t mine = 0;
+#pragma unroll
+        for (int j = 0; j < kScanPer; ++j) mine += v[j];
+        int64_t total;
+        int64_t run = carry + block_inclusive_scan(mine, &total) - mine;
+#pragma unroll
+        for (int j = 0; j < kScanPer; ++j) {
+            if (lo + j < a.ntiles) ts[lo + j] = run;
+            run += v[j];
         }
-        if (threadIdx.x == 0) a.segments[a.G] = 0;
-        return;
+        carry += total;
     }
-    int64_t *ts = a.tile_sums;
-    const int64_t n = (int64_t)a.G * a.ntiles;
-    const int64_t per = (n + kBlock - 1) / kBlock;
-    const int64_t lo = std::min<int64_t>(n, threadIdx.x * per);
-    const int64_t hi = std::min<int64_t>(n, lo + per);
-    int64_t sum = 0;
-    for (int64_t i = lo; i < hi; ++i) sum += ts[i];
-    int64_t total;
-    const int64_t before = block_inclusive_scan(sum, &total) - sum;
-    int64_t run = before;
-    for (int64_t i = lo; i < hi; ++i) {
-        if (i % a.ntiles == 0) seg[i / a.ntiles] = run;
-        run += ts[i];
+    if (threadIdx.x == 0) a.row_totals[g] = carry;
+}
+
+// A batch without bags: every destination is empty, its offsets the single 0.
+__global__ __launch_bounds__(kBlock) void eb_scan_empty(const ScanArgs a)
+{
+    for (int g = threadIdx.x; g < a.G; g += kBlock) {
+        a.rows[g] = 0;
+        a.segments[g] = 0;
     }
-    __syncthreads();
-    run = before;
-    for (int64_t i = lo; i < hi; ++i) {
-        const int64_t v = ts[i];
-        ts[i] = run - seg[i / a.ntiles];
-        run += v;
-    }
-    for (int g = threadIdx.x; g < a.G; g += kBlock) a.segments[g] = seg[g];
-    if (threadIdx.x == 0) a.segments[a.G] = total;
+    if (threadIdx.x == 0) a.segments[a.G] = 0;
 }
 
 // Pass 2c: scan every tile and add its prefix, in place.  The tile passes
 // through LDS so that each thread scans kScanPer consecutive counts of its
-// own and a single block-wide scan joins the threads.  Fused (few tiles in
-// all): the tile's prefix is the sum of its row's earlier tiles, and each
-// row's first tile also writes the row's segment start (the sum of all
-// earlier rows' tiles; the last row also the total), which saves pass 2b's
-// launch.
+// own and a single block-wide scan joins the threads.  Each row's first tile
+// also writes the row's segment start (the sum of all earlier rows; the last
+// row also the total).  Fused (few tiles in all): the tile's prefix is the
+// sum of its row's earlier tiles and the segment start the sum of all
+// earlier rows' tiles, which saves pass 2b's launch; else pass 2b left the
+// prefix in place of the tile's sum and the rows' totals in row_totals.
 __device__ __forceinline__ int scan_slot(int e) { return e + e / kScanPer; } // conflict-free row reads
 
 __global__ __launch_bounds__(kBlock) void eb_scan_tiles(const ScanArgs a)
@@ -776,6 +783,21 @@ __global__ __launch_bounds__(kBlock) void eb_scan_tiles(const ScanArgs a)
         }
     } else {
         carry = a.tile_sums[row0 + k];
+        if (k == 0) {
+            int64_t before = 0, all = 0;
+            for (int j = threadIdx.x; j < a.G; j += kBlock) {
+                const int64_t x = a.row_totals[j];
+                if (j < g) before += x;
+                all += x;
+            }
+            int64_t seg, total;
+            block_inclusive_scan(before, &seg);
+            block_inclusive_scan(all, &total);
+            if (threadIdx.x == 0) {
+                a.segments[g] = seg;
+                if (g == a.G - 1) a.segments[a.G] = total;
+            }
+        }
     }
 #pragma unroll
     for (int j = 0; j < kScanPer; ++j) sm[scan_slot(j * kBlock + threadIdx.x)] = v[j];
@@ -1235,11 +1257,11 @@ ScanShape scan_shape(int32_t T, int64_t B, int32_t G)
 }
 
 // Workspace entries (int64): tile sums, every 16th entry of each
-// destination's offsets, count's wave totals.
+// destination's offsets, count's wave totals, the rows' totals.
 int64_t workspace_entries(int32_t T, int64_t B, int32_t G)
 {
     const ScanShape s = scan_shape(T, B, G);
-    return (int64_t)G * (s.ntiles + start_entries((int64_t)T * B) + s.nparts);
+    return (int64_t)G * (s.ntiles + start_entries((int64_t)T * B) + s.nparts + 1);
 }
 
 // The count and scatter instantiations for G destinations (count_bags bags
@@ -1329,17 +1351,20 @@ int bucketize_impl(int32_t T, int64_t B, int32_t G, const int64_t *bounds, int32
     ba.count_blocks_per_table = (int32_t)cbpt;
     ba.count_waves_per_table = (int32_t)shape.waves_per_table;
 
-    // Workspace: tile sums [G][ntiles], starts [G][nq], wave totals [nparts][G].
+    // Workspace: tile sums [G][ntiles], starts [G][nq], wave totals [nparts][G],
+    // row totals [G].
     ScanArgs sa;
     sa.rows = out_offsets;
     sa.tile_sums = (int64_t *)workspace;
     sa.nq = start_entries(TB);
     sa.starts = sa.tile_sums + (int64_t)G * shape.ntiles;
     sa.nparts = shape.nparts;
-    sa.wave_totals = sa.starts + (int64_t)G * sa.nq;
+    int64_t *wave_totals = sa.starts + (int64_t)G * sa.nq;
+    sa.wave_totals = wave_totals;
+    sa.row_totals = wave_totals + shape.nparts * G;
     ba.starts = sa.starts;
     ba.nq = sa.nq;
-    ba.wave_totals = sa.starts + (int64_t)G * sa.nq;
+    ba.wave_totals = wave_totals;
     ba.nparts = shape.nparts;
     sa.segments = segments;
     sa.TB = TB;
@@ -1351,7 +1376,7 @@ int bucketize_impl(int32_t T, int64_t B, int32_t G, const int64_t *bounds, int32
     sa.tables_per_tile = (int32_t)shape.tables_per_tile;
     sa.waves_per_table = (int32_t)shape.waves_per_table;
     sa.bags_per_wave = cbags;
-    sa.fused = (int64_t)G * sa.ntiles <= kFusedScanMax ? 1 : 0;
+    sa.fused = fused_scan(G, sa.ntiles) ? 1 : 0;
 
     if (TB > 0) {
         void *args[] = {&ba};
@@ -1363,7 +1388,7 @@ int bucketize_impl(int32_t T, int64_t B, int32_t G, const int64_t *bounds, int32
         err = hipLaunchKernel((const void *)eb_scan_tile_sums, dim3(sa.ntiles, (G + kBlock - 1) / kBlock),
                               dim3(kBlock), sargs, 0, st);
         if (err == hipSuccess && !sa.fused)
-            err = hipLaunchKernel((const void *)eb_scan_tile_prefix, dim3(1), dim3(kBlock), sargs, 0, st);
+            err = hipLaunchKernel((const void *)eb_scan_row_prefix, dim3(G), dim3(kBlock), sargs, 0, st);
         if (err == hipSuccess)
             err = hipLaunchKernel((const void *)eb_scan_tiles, dim3(sa.ntiles, G), dim3(kBlock), sargs, 0, st);
         if (err == hipSuccess)
@@ -1373,9 +1398,8 @@ int bucketize_impl(int32_t T, int64_t B, int32_t G, const int64_t *bounds, int32
         if (err != hipSuccess) return fail(EB_ERR_HIP, "eb_bucketize: %s", hipGetErrorString(err));
     } else {
         // No bags: every destination is empty.
-        sa.ntiles = 0;
         void *sargs[] = {&sa};
-        hipError_t err = hipLaunchKernel((const void *)eb_scan_tile_prefix, dim3(1), dim3(kBlock), sargs, 0, st);
+        hipError_t err = hipLaunchKernel((const void *)eb_scan_empty, dim3(1), dim3(kBlock), sargs, 0, st);
         if (err != hipSuccess) return fail(EB_ERR_HIP, "eb_bucketize: %s", hipGetErrorString(err));
     }
     return EB_OK;

@@ -78,11 +78,12 @@ def test_bucketize_batch_tails(B, device):
 
 
 @pytest.mark.parametrize("G,T,B", [(8, 5, 5001), (3, 1, 40960), (300, 2, 14000), (1024, 2, 6000),
-                                   (1024, 1, 34817), (1024, 1, 264_193)])
+                                   (1024, 1, 34817), (1024, 1, 264_193), (1000, 3, 90_000)])
 def test_bucketize_many_scan_tiles(G, T, B, device):
-    # Many 2048-bag scan tiles with a ragged last one.  Up to 131,072 tile
-    # sums in all (destinations x tiles) the tile scan adds up the earlier
-    # tiles itself; 1024 x 130 takes the separate one-workgroup prefix pass.
+    # Many 2048-bag scan tiles with a ragged last one per table.  With few
+    # tile sums to read (the first three) the tile scan adds up the earlier
+    # tiles itself; the others take the separate pass that scans each
+    # destination's row of tile sums.
     T, B, idx, off, bounds = bucket_case(G * 7 + B, G, T=T, B=B, maxL=4 if B < 100_000 else 1)
     check_bucketize(T, B, idx, off, bounds, device)
 
