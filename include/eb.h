@@ -254,6 +254,9 @@ int eb_bucketize_workspace(int32_t T, int64_t B, int32_t G, size_t *bytes);
  *                [T*B+1] clamped into [0, nnz]; every bag sends the ids of
  *                its own clamped range, so bags whose ranges overlap, which
  *                only malformed offsets produce, send such ids once each).
+ *                A bag may send at most 2^31 - 1 ids to one destination
+ *                (each bag's count per destination is a 32-bit counter
+ *                while it is taken; nothing checks this).
  *   out_offsets  device int64 [G][T*B+1]: destination g's CSR offsets for
  *                the same T*B bags, out_offsets[g][0] = 0.
  *   out_indices  device int64 [out_capacity]: destination g's ids at
