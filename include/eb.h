@@ -316,7 +316,7 @@ int eb_bucketize_ex(int32_t T, int64_t B, int32_t G, const int64_t *bounds, int3
  * one copy on every GPU the library runs on, held until the process ends.
  * Its address on the current device is looked up on the first call there;
  * the call itself allocates nothing.  Calls whose eb_bucketize_workspace()
- * exceeds 8 MiB (for G = 8 destinations, batches of more than about two
+ * exceeds 8 MiB (for G = 8 destinations, batches of more than about 1.6
  * million bags) fail with EB_ERR_UNSUPPORTED before touching the device.
  * `stream` must belong to the current device (EB_ERR_INVALID otherwise).
  *
