@@ -267,8 +267,11 @@ constexpr int kBagsPerWave = 16;
 constexpr int kBagsPerBlock = kBagsPerWave * kWavesPerBlock;
 static_assert(kBagsPerWave <= kWave && (kBagsPerWave & (kBagsPerWave - 1)) == 0, "bags per wave");
 constexpr int64_t kCountWavesMin = 4608; // 18 per compute unit
-constexpr int kCountChunks = 4;   // 64-id chunks loaded ahead by count
-constexpr int kScatterChunks = 8; // and by scatter (measured best for each)
+// 64-id chunks loaded ahead by count: 4 with the compare trees, 8 with
+// binary search (whose longer per-id chains gain from more loads in flight),
+// and 8 by scatter (each measured best).
+template <int kOwners> constexpr int kCountChunks = kOwners == 0 ? 8 : 4;
+constexpr int kScatterChunks = 8;
 
 struct BucketArgs {
     const int64_t *bounds;   // [T][G+1]
@@ -382,8 +385,8 @@ __device__ __forceinline__ void wave_sync_lds()
 }
 
 // One pass of count's loop: the ids at k0 + u * 64 + lane, the first R of
-// them (all kCountChunks * 64 when kFull, the usual case, which then needs
-// no tail masks).
+// them (all kCountChunks<kOwners> * 64 when kFull, the usual case, which then
+// needs no tail masks).
 // kOwners: 8 (owners by the 3-bit tree), 16 (the 4-bit tree), or 0 (by
 // binary search over the bounds in LDS).
 template <typename IT, int kOwners, bool kFull>
@@ -392,12 +395,12 @@ __device__ __forceinline__ void count_pass(const BucketArgs &a, const int64_t *b
                                            int64_t k0, int R)
 {
     const IT *src = ids_of<IT>(a) + k0 + lane;
-    int64_t id[kCountChunks];
+    int64_t id[kCountChunks<kOwners>];
 #pragma unroll
-    for (int u = 0; u < kCountChunks; ++u)
+    for (int u = 0; u < kCountChunks<kOwners>; ++u)
         id[u] = (kFull || lane_bit(lanes_below(R - u * kWave))) ? (int64_t)__builtin_nontemporal_load(src + u * kWave) : 0;
 #pragma unroll
-    for (int u = 0; u < kCountChunks; ++u) {
+    for (int u = 0; u < kCountChunks<kOwners>; ++u) {
         // The bag of position k is the last one starting at or
         // before k: the bags starting by the chunk's first position,
         // plus one for each bag starting inside the chunk at or
@@ -433,7 +436,7 @@ __device__ __forceinline__ void count_chunks(const BucketArgs &a, const int64_t 
                                              const TreeBounds &tb, int *hist, int lane, int64_t s, uint64_t bags,
                                              int64_t S, int64_t E)
 {
-    constexpr int kPass = kCountChunks * kWave;
+    constexpr int kPass = kCountChunks<kOwners> * kWave;
     for (int64_t k0 = S; k0 < E; k0 += kPass) {
         const int R = __builtin_amdgcn_readfirstlane((int)min<int64_t>(E - k0, (int64_t)kPass));
         if (R == kPass)
