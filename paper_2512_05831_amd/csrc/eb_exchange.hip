@@ -20,9 +20,9 @@
 //
 // eb_bucketize runs three kernels on the caller's stream (eb_bucketize_ex the
 // same with int32 ids, offsets and scattered ids, each widened on load):
-//   1. count   : a wave takes 8 to 64 consecutive bags (for up to 16
+//   1. count   : a wave takes 16 to 64 consecutive bags (for up to 16
 //                destinations the most of 16, 32, 64 that leave at least
-//                4608 waves, else 16, and 8 beyond 64; each XCD one
+//                4608 waves, else 16; 16-bit counts beyond 64; each XCD one
 //                contiguous run of workgroups); each id's owner by
 //                comparisons with the table's block bounds (up to 16 blocks:
 //                a search tree evaluated as wave-wide lane masks) or by
@@ -262,7 +262,7 @@ __device__ __forceinline__ int owner_by_eighths(const int64_t *bnd, int G, const
 // A count wave takes 16, 32 or 64 bags up to 16 destinations (the most that
 // still leave at least kCountWavesMin waves, since count's waves are short
 // and each starts with a dependent load of its offsets, which longer waves
-// pay less often), 16 up to 64 destinations and 8 beyond (count_bags).
+// pay less often), and 16 beyond 16 destinations (count_bags).
 constexpr int kBagsPerWave = 16;
 constexpr int kBagsPerBlock = kBagsPerWave * kWavesPerBlock;
 static_assert(kBagsPerWave <= kWave && (kBagsPerWave & (kBagsPerWave - 1)) == 0, "bags per wave");
@@ -321,11 +321,20 @@ __device__ __forceinline__ int xcd_run_block(int b, int n)
 // Dynamic LDS: the table's G+1 bounds, then one area per wave.
 // count's histogram row per bag: 8 entries for up to 8 destinations and 16
 // for up to 16 (an index by shift), else G.
-__host__ __device__ constexpr int count_stride(int G) { return G <= kFewShards ? kFewShards : G <= kTreeShards ? kTreeShards : G; }
-__host__ __device__ constexpr size_t count_wave_bytes(int G, int bags) { return (size_t)4 * count_stride(G) * bags; }
-// 8-bag waves keep the histogram of the most destinations within 32 KB.
-static_assert(count_wave_bytes(kMaxShards, 8) <= 32768, "count histogram");
-__host__ __device__ inline size_t count_lds_bytes(int G, int bags) { return (size_t)(G + 1) * 8 + kWavesPerBlock * count_wave_bytes(G, bags); }
+// Beyond 64 destinations (kPacked) two counts share a 32-bit word, 16 bits
+// each: a row of (G + 1) / 2 words per bag.
+__host__ __device__ constexpr int count_stride(int G, bool packed = false)
+{
+    return packed ? (G + 1) / 2 : G <= kFewShards ? kFewShards : G <= kTreeShards ? kTreeShards : G;
+}
+__host__ __device__ constexpr size_t count_wave_bytes(int G, int bags, bool packed = false)
+{
+    return (size_t)4 * count_stride(G, packed) * bags;
+}
+// 16-bag waves of packed counts keep the histogram of the most destinations
+// within 32 KB.
+static_assert(count_wave_bytes(kMaxShards, 16, true) <= 32768, "count histogram");
+__host__ __device__ inline size_t count_lds_bytes(int G, int bags, bool packed) { return (size_t)(G + 1) * 8 + kWavesPerBlock * count_wave_bytes(G, bags, packed); }
 __host__ __device__ inline size_t scatter_lds_bytes(int G) { return (size_t)(G + 1) * 8 + (size_t)kWavesPerBlock * G * 8; }
 
 __device__ __forceinline__ int64_t shfl_down64(int64_t v, int d)
@@ -388,8 +397,8 @@ __device__ __forceinline__ void wave_sync_lds()
 // them (all kCountChunks<kOwners> * 64 when kFull, the usual case, which then
 // needs no tail masks).
 // kOwners: 8 (owners by the 3-bit tree), 16 (the 4-bit tree), or 0 (by
-// binary search over the bounds in LDS).
-template <typename IT, int kOwners, bool kFull>
+// binary search over the bounds in LDS); kPacked: 16-bit counts, two to a word.
+template <typename IT, int kOwners, bool kFull, bool kPacked>
 __device__ __forceinline__ void count_pass(const BucketArgs &a, const int64_t *bnd, const FewBounds &fb,
                                            const TreeBounds &tb, int *hist, int lane, int64_t s, uint64_t bags,
                                            int64_t k0, int R)
@@ -421,6 +430,9 @@ __device__ __forceinline__ void count_pass(const BucketArgs &a, const int64_t *b
         } else if constexpr (kOwners == kTreeShards) {
             const TreeMasks o = tree_owner_masks(tb, id[u], in);
             if (lane_bit(o.valid)) atomicAdd(&hist[l * kTreeShards + tree_bits<1>(o)], 1);
+        } else if constexpr (kPacked) {
+            const int g = owner_by_eighths(bnd, a.G, fb, id[u], in);
+            if (g >= 0) atomicAdd((unsigned *)&hist[l * count_stride(a.G, true) + (g >> 1)], 1u << ((g & 1) * 16));
         } else {
             const int g = owner_by_eighths(bnd, a.G, fb, id[u], in);
             if (g >= 0) atomicAdd(&hist[l * count_stride(a.G) + g], 1);
@@ -430,8 +442,9 @@ __device__ __forceinline__ void count_pass(const BucketArgs &a, const int64_t *b
 
 // count's loop over the wave's ids [S, E) for contiguous bags (bag l of the
 // wave starts at lane l's s; bags = lanes holding a bag): adds each id with
-// an owner to hist[bag * count_stride(G) + owner].
-template <typename IT, int kOwners>
+// an owner to hist[bag * count_stride(G) + owner] (packed: half owner & 1 of
+// word bag * count_stride(G, true) + owner / 2).
+template <typename IT, int kOwners, bool kPacked>
 __device__ __forceinline__ void count_chunks(const BucketArgs &a, const int64_t *bnd, const FewBounds &fb,
                                              const TreeBounds &tb, int *hist, int lane, int64_t s, uint64_t bags,
                                              int64_t S, int64_t E)
@@ -440,19 +453,23 @@ __device__ __forceinline__ void count_chunks(const BucketArgs &a, const int64_t 
     for (int64_t k0 = S; k0 < E; k0 += kPass) {
         const int R = __builtin_amdgcn_readfirstlane((int)min<int64_t>(E - k0, (int64_t)kPass));
         if (R == kPass)
-            count_pass<IT, kOwners, true>(a, bnd, fb, tb, hist, lane, s, bags, k0, R);
+            count_pass<IT, kOwners, true, kPacked>(a, bnd, fb, tb, hist, lane, s, bags, k0, R);
         else
-            count_pass<IT, kOwners, false>(a, bnd, fb, tb, hist, lane, s, bags, k0, R);
+            count_pass<IT, kOwners, false, kPacked>(a, bnd, fb, tb, hist, lane, s, bags, k0, R);
     }
 }
 
 // kOwners: how the instantiation finds owners (8: 3-bit compare tree, 16:
 // 4-bit tree, 0: binary search); one instantiation per method and wave size,
-// so that each keeps only its own path's registers.
-template <typename IT, int kBags, int kOwners>
+// so that each keeps only its own path's registers.  kPacked (beyond 64
+// destinations): the histogram holds 16-bit counts, two to a word, so that
+// 16-bag waves fit; a wave with a bag of 65,536 ids or more takes the
+// bag-at-a-time path instead.
+template <typename IT, int kBags, int kOwners, bool kPacked>
 __global__ __launch_bounds__(kBlock) void eb_bucket_count(const BucketArgs a)
 {
-    static_assert(kBags >= 8 && kBags <= kWave && (kBags & (kBags - 1)) == 0, "bags per count wave");
+    static_assert(kBags >= 16 && kBags <= kWave && (kBags & (kBags - 1)) == 0, "bags per count wave");
+    static_assert(!kPacked || kOwners == 0, "packed counts with binary search only");
     extern __shared__ int64_t lds[];
     const int G = a.G;
     int64_t *bnd = lds;
@@ -460,7 +477,7 @@ __global__ __launch_bounds__(kBlock) void eb_bucket_count(const BucketArgs a)
     const int t = lb / a.count_blocks_per_table;
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = threadIdx.x / kWave;
-    int *hist = (int *)((char *)(lds + G + 1) + wave * count_wave_bytes(G, kBags));
+    int *hist = (int *)((char *)(lds + G + 1) + wave * count_wave_bytes(G, kBags, kPacked));
     const int64_t b0 = (int64_t)(lb - t * a.count_blocks_per_table) * (kBags * kWavesPerBlock) + wave * kBags;
     const bool live = b0 < a.B; // the wave has bags
     const int nb = live ? (int)min<int64_t>(kBags, a.B - b0) : 0;
@@ -473,7 +490,8 @@ __global__ __launch_bounds__(kBlock) void eb_bucket_count(const BucketArgs a)
     for (int g = threadIdx.x; g <= G; g += kBlock) bnd[g] = a.bounds[(int64_t)t * (G + 1) + g];
     __syncthreads();
     if (!live) return; // no block-wide barrier follows
-    const bool contiguous = wave_bags(a, nb, lane, s, e, S, E);
+    bool contiguous = wave_bags(a, nb, lane, s, e, S, E);
+    if (kPacked && __ballot(lane < nb && e - s >= 65536) != 0) contiguous = false; // a half could overflow
     if (p0 == 0)
         for (int g = lane; g < G; g += kWave) a.out_offsets[(int64_t)g * row] = 0;
     // The wave's totals per destination (one contiguous run), for the scan's
@@ -482,15 +500,34 @@ __global__ __launch_bounds__(kBlock) void eb_bucket_count(const BucketArgs a)
 
     if (contiguous) {
         const uint64_t bags = __ballot(lane < nb);
-        for (int x = lane; x < kBags * count_stride(G); x += kWave) hist[x] = 0;
+        for (int x = lane; x < kBags * count_stride(G, kPacked); x += kWave) hist[x] = 0;
         wave_sync_lds();
         if constexpr (kOwners == kFewShards)
-            count_chunks<IT, kFewShards>(a, bnd, few_bounds(bnd, G), TreeBounds{}, hist, lane, s, bags, S, E);
+            count_chunks<IT, kFewShards, false>(a, bnd, few_bounds(bnd, G), TreeBounds{}, hist, lane, s, bags, S, E);
         else if constexpr (kOwners == kTreeShards)
-            count_chunks<IT, kTreeShards>(a, bnd, FewBounds{}, tree_bounds(bnd, G), hist, lane, s, bags, S, E);
+            count_chunks<IT, kTreeShards, false>(a, bnd, FewBounds{}, tree_bounds(bnd, G), hist, lane, s, bags, S, E);
         else
-            count_chunks<IT, 0>(a, bnd, eighth_bounds(bnd, G), TreeBounds{}, hist, lane, s, bags, S, E);
+            count_chunks<IT, 0, kPacked>(a, bnd, eighth_bounds(bnd, G), TreeBounds{}, hist, lane, s, bags, S, E);
         wave_sync_lds();
+        if constexpr (kPacked) {
+            // The counts (each taken from its half word) transposed as below;
+            // lane g + 64 r adds up destination g + 64 r's total over all bags.
+            const int stride = count_stride(G, true);
+            for (int x = lane; x < kBags * G; x += kWave) {
+                const int j = x & (kBags - 1), g = x / kBags;
+                if (j < nb)
+                    a.out_offsets[(int64_t)g * row + p0 + j + 1] =
+                        ((unsigned)hist[j * stride + (g >> 1)] >> ((g & 1) * 16)) & 0xFFFFu;
+            }
+            for (int g = lane; g < G; g += kWave) {
+                int64_t sum = 0;
+#pragma unroll
+                for (int j = 0; j < kBags; ++j)
+                    sum += j < nb ? ((unsigned)hist[j * stride + (g >> 1)] >> ((g & 1) * 16)) & 0xFFFFu : 0u;
+                totals[g] = sum;
+            }
+            return;
+        }
         // Entry x of the histogram's transpose: bag x % kBags, destination
         // x / kBags; a store covers 64 / kBags rows, kBags bags of each.
         const int stride = count_stride(G);
@@ -498,34 +535,25 @@ __global__ __launch_bounds__(kBlock) void eb_bucket_count(const BucketArgs a)
             const int j = x & (kBags - 1), g = x / kBags;
             if (j < nb) a.out_offsets[(int64_t)g * row + p0 + j + 1] = hist[j * stride + g];
         }
-        // The wave's totals: up to 64 destinations, lane q * Gp + g (Gp =
-        // G rounded up to a power of two) adds up destination g over every
-        // (64 / Gp)-th bag from bag q on, then the lanes of each destination
-        // combine; beyond 64 (8 bags), lane g + 64 r adds up destination g +
-        // 64 r over all bags.
-        if (kOwners != 0 || G <= kWave) { // the compare trees take at most 16
-            const int Gp = 1 << (32 - __builtin_clz((unsigned)(2 * G - 1)) - 1);
-            const int P = kWave / Gp, g = lane & (Gp - 1), q = lane / Gp;
-            int64_t sum = 0;
-            if (g < G) {
+        // The wave's totals (unpacked counts: at most 64 destinations): lane
+        // q * Gp + g (Gp = G rounded up to a power of two) adds up
+        // destination g over every (64 / Gp)-th bag from bag q on, then the
+        // lanes of each destination combine.
+        const int Gp = 1 << (32 - __builtin_clz((unsigned)(2 * G - 1)) - 1);
+        const int P = kWave / Gp, g = lane & (Gp - 1), q = lane / Gp;
+        int64_t sum = 0;
+        if (g < G) {
 #pragma unroll 4
-                for (int j = q; j < nb; j += P) sum += hist[j * stride + g];
-            }
-            for (int o = Gp; o < kWave; o <<= 1) sum += shfl_xor64(sum, o);
-            if (q == 0 && g < G) totals[g] = sum;
-        } else if constexpr (kOwners == 0) {
-            for (int g = lane; g < G; g += kWave) {
-                int64_t sum = 0;
-#pragma unroll
-                for (int j = 0; j < kBags; ++j) sum += j < nb ? hist[j * stride + g] : 0;
-                totals[g] = sum;
-            }
+            for (int j = q; j < nb; j += P) sum += hist[j * stride + g];
         }
+        for (int o = Gp; o < kWave; o <<= 1) sum += shfl_xor64(sum, o);
+        if (q == 0 && g < G) totals[g] = sum;
         return;
     }
     // Any offsets, any G: one bag at a time, with the running totals in the
-    // wave's LDS area after the bag's G counts (it holds 4 * count_stride(G)
-    // * kBags >= 12 G bytes, since kBags >= 8 beyond 16 destinations).
+    // wave's LDS area after the bag's G counts (it holds
+    // count_wave_bytes(G, kBags, kPacked) >= 12 G bytes: kBags >= 16, so
+    // 64 G bytes unpacked and 32 G packed).
     int64_t *run = (int64_t *)(hist + ((G + 1) & ~1));
     for (int g = lane; g < G; g += kWave) run[g] = 0;
     for (int j = 0; j < nb; ++j) {
@@ -1223,13 +1251,17 @@ __global__ __launch_bounds__(kBlock) void eb_sum_partials_scalar(const PartialAr
 // Bags per count wave for T*B bags in all and G destinations (see
 // kCountWavesMin).  Only the compare-tree paths (G <= 16, 8 or 16 histogram
 // entries per bag) gain from longer waves; 17 to 64 destinations take 16
-// bags, more take 8 (measured: 8 bags beat 16 at 200 destinations, and at
-// 1024 beat 2 or 4 even though the histograms then limit a compute unit to 4
-// waves).  Always a power of two from 8 to 64, so that it divides the scan's
+// bags, and so do more, with packed 16-bit counts (with 32-bit counts 8 bags
+// had beaten 16 at 200 destinations, and at 1024 beaten 2 or 4 even though
+// the histograms then limit a compute unit to 4 waves; packed 16-bag waves
+// write each destination's counts in 128-byte runs at the same histogram
+// size).  Always a power of two from 16 to 64, so that it divides the scan's
 // 2048-bag tiles.
+constexpr int kPackedBags = 16;
+bool packed_counts(int G) { return G > kWave; }
 int count_bags(int64_t TB, int G)
 {
-    if (G > kWave) return 8;
+    if (packed_counts(G)) return kPackedBags;
     if (G > kTreeShards) return 16;
     for (int bags = 64; bags > 16; bags /= 2)
         if (TB / bags >= kCountWavesMin) return bags;
@@ -1273,14 +1305,15 @@ template <typename IT>
 const void *count_kernel(int G, int bags)
 {
     if (G <= kFewShards)
-        return bags == 64 ? (const void *)eb_bucket_count<IT, 64, kFewShards>
-               : bags == 32 ? (const void *)eb_bucket_count<IT, 32, kFewShards>
-                            : (const void *)eb_bucket_count<IT, 16, kFewShards>;
+        return bags == 64 ? (const void *)eb_bucket_count<IT, 64, kFewShards, false>
+               : bags == 32 ? (const void *)eb_bucket_count<IT, 32, kFewShards, false>
+                            : (const void *)eb_bucket_count<IT, 16, kFewShards, false>;
     if (G <= kTreeShards)
-        return bags == 64 ? (const void *)eb_bucket_count<IT, 64, kTreeShards>
-               : bags == 32 ? (const void *)eb_bucket_count<IT, 32, kTreeShards>
-                            : (const void *)eb_bucket_count<IT, 16, kTreeShards>;
-    return bags == 16 ? (const void *)eb_bucket_count<IT, 16, 0> : (const void *)eb_bucket_count<IT, 8, 0>;
+        return bags == 64 ? (const void *)eb_bucket_count<IT, 64, kTreeShards, false>
+               : bags == 32 ? (const void *)eb_bucket_count<IT, 32, kTreeShards, false>
+                            : (const void *)eb_bucket_count<IT, 16, kTreeShards, false>;
+    return packed_counts(G) ? (const void *)eb_bucket_count<IT, kPackedBags, 0, true>
+                            : (const void *)eb_bucket_count<IT, 16, 0, false>;
 }
 
 template <typename IT>
@@ -1385,7 +1418,7 @@ int bucketize_impl(int32_t T, int64_t B, int32_t G, const int64_t *bounds, int32
         void *args[] = {&ba};
         const void *count = i32 ? count_kernel<int32_t>(G, cbags) : count_kernel<int64_t>(G, cbags);
         hipError_t err = hipLaunchKernel(count, dim3((unsigned)(T * cbpt)), dim3(kBlock), args,
-                                         count_lds_bytes(G, cbags), st);
+                                         count_lds_bytes(G, cbags, packed_counts(G)), st);
         if (err != hipSuccess) return fail(EB_ERR_HIP, "eb_bucketize: %s", hipGetErrorString(err));
         void *sargs[] = {&sa};
         err = hipLaunchKernel((const void *)eb_scan_tile_sums, dim3(sa.ntiles, (G + kBlock - 1) / kBlock),

@@ -98,6 +98,31 @@ def test_bucketize_long_bags_and_skew(device):
     check_bucketize(T, B, idx, off, bounds, device)
 
 
+@pytest.mark.parametrize("G", [65, 300])
+def test_bucketize_bags_past_16_bit_counts(G, device):
+    """Beyond 64 destinations count keeps 16-bit counts, two to a word; a
+    wave whose bags include one of 65,536 ids or more counts bag by bag
+    instead.  Bags of 65,535 ids all for one destination fill a count to
+    its limit; bags of 65,536 and 70,000 ids (one destination, or spread
+    over all) take the other path; small bags of the same waves and of
+    other waves must come out right either way."""
+    g = np.random.default_rng(G)
+    T, B, rows = 2, 40, 1_000_000
+    bounds = even_bounds([rows, rows], G)
+    L = g.integers(0, 30, T * B)
+    big = {3: 65_535, 17: 65_536, 20: 70_000, 41: 65_535, 60: 65_537}
+    for p_, n in big.items():
+        L[p_] = n
+    off = wl.offsets_from_lengths(L)
+    idx = g.integers(0, rows, int(off[-1]), dtype=np.int64)
+    # bags 3, 17 and 41 send every id to one block (the count's maximum)
+    for p_ in (3, 17, 41):
+        t = p_ // B
+        lo, hi = int(bounds[t][5]), int(bounds[t][6])
+        idx[off[p_]:off[p_ + 1]] = g.integers(lo, hi, L[p_])
+    check_bucketize(T, B, idx, off, bounds, device)
+
+
 def test_bucketize_edge_cases(device):
     # no ids at all
     off = np.zeros(2 * 5 + 1, dtype=np.int64)
