@@ -45,9 +45,11 @@
 //                out_offsets[g][p] + rank (a wave's first out_offsets from
 //                the workspace copy), the rank counting earlier ids of
 //                the bag with the same owner (per 64-id chunk: ballots of
-//                the owner's bits, three for up to 8 destinations and 4 to 6
-//                for up to 64, else a ballot per distinct owner), so the
-//                order is stable.  For ordinary CSR
+//                the owner's bits, three for up to 8 destinations, 4 to 7
+//                for up to 128 with every destination's running slot in a
+//                lane's registers, up to 10 beyond with the slots in LDS;
+//                a ballot per distinct owner for bags whose offsets are out
+//                of order), so the order is stable.  For ordinary CSR
 //                offsets one running slot per destination and wave suffices,
 //                since position order is then (bag, position) order.  Every
 //                store is checked against the capacity of out_indices (an
@@ -1018,6 +1020,59 @@ __device__ __forceinline__ void scatter_mid_pass(const BucketArgs &a, const int6
         if ((uint64_t)pos[u] < (uint64_t)a.out_cap) put_id<IT>(a, pos[u], id[u]);
 }
 
+// One pass of the scatter for contiguous bags and 65 to 128 destinations:
+// as scatter_mid_pass with 7 ballots of the owner's bits and two slots per
+// lane, lane d holding destination d's slot in slot[0] and destination d +
+// 64's in slot[1] (lbit[i] is the complement of the lane's bit i as an
+// all-ones / zero mask; bit 6 of the destination is the slot's index).
+template <typename IT, bool kFull>
+__device__ __forceinline__ void scatter_wide_pass(const BucketArgs &a, const int64_t *bnd, const FewBounds &eb, int lane,
+                                                  const uint32_t (&lbit)[6], int64_t (&slot)[2], int64_t k0, int R)
+{
+    const IT *src = ids_of<IT>(a) + k0 + lane;
+    int64_t id[kScatterChunks];
+#pragma unroll
+    for (int u = 0; u < kScatterChunks; ++u)
+        id[u] = (kFull || lane_bit(lanes_below(R - u * kWave))) ? (int64_t)__builtin_nontemporal_load(src + u * kWave) : 0;
+    int64_t pos[kScatterChunks];
+#pragma unroll
+    for (int u = 0; u < kScatterChunks; ++u) {
+        const int g = owner_by_eighths(bnd, a.G, eb, id[u], kFull ? ~0ull : lanes_below(R - u * kWave));
+        const bool ok = g >= 0;
+        const uint64_t valid = __ballot(ok);
+        uint32_t same_lo = (uint32_t)valid, same_hi = (uint32_t)(valid >> 32);
+        uint32_t own_lo[2] = {same_lo, same_lo}, own_hi[2] = {same_hi, same_hi};
+#pragma unroll
+        for (int i = 0; i < 7; ++i) {
+            const uint64_t b = __ballot(ok && ((g >> i) & 1));
+            const uint32_t n = ((g >> i) & 1) ? 0u : ~0u; // complement of this lane's owner bit
+            same_lo &= (uint32_t)b ^ n;
+            same_hi &= (uint32_t)(b >> 32) ^ n;
+#pragma unroll
+            for (int q = 0; q < 2; ++q) {
+                const uint32_t l = i < 6 ? lbit[i] : (q ? 0u : ~0u);
+                own_lo[q] &= (uint32_t)b ^ l;
+                own_hi[q] &= (uint32_t)(b >> 32) ^ l;
+            }
+        }
+        const int rank = (int)__builtin_amdgcn_mbcnt_hi(same_hi, __builtin_amdgcn_mbcnt_lo(same_lo, 0u));
+        const int from = ok ? (g & (kWave - 1)) * 4 : 0;
+        const int lo0 = __builtin_amdgcn_ds_bpermute(from, (int)(uint32_t)slot[0]);
+        const int hi0 = __builtin_amdgcn_ds_bpermute(from, (int)(slot[0] >> 32));
+        const int lo1 = __builtin_amdgcn_ds_bpermute(from, (int)(uint32_t)slot[1]);
+        const int hi1 = __builtin_amdgcn_ds_bpermute(from, (int)(slot[1] >> 32));
+        const bool upper = g >= kWave;
+        const int64_t base = ((int64_t)(upper ? hi1 : hi0) << 32) | (uint32_t)(upper ? lo1 : lo0);
+        pos[u] = ok ? base + rank : -1;
+#pragma unroll
+        for (int q = 0; q < 2; ++q) slot[q] += __popc(own_lo[q]) + __popc(own_hi[q]);
+    }
+    __builtin_amdgcn_sched_barrier(0); // keep the stores after all ranking
+#pragma unroll
+    for (int u = 0; u < kScatterChunks; ++u)
+        if ((uint64_t)pos[u] < (uint64_t)a.out_cap) put_id<IT>(a, pos[u], id[u]);
+}
+
 // One pass of the scatter for contiguous bags and more than 64 destinations:
 // owners by binary search, ranks from ballots of the owner's nbits bits, and
 // each destination's running slot in the wave's LDS array next[] (read by
@@ -1076,8 +1131,9 @@ __device__ __forceinline__ void scatter_mid(const BucketArgs &a, const int64_t *
 }
 
 // kOwners: the most destinations the instantiation ranks in one chunk's
-// ballots (8: 3-bit compare tree; 16: 4-bit tree; 32 / 64: binary search and
-// 5 / 6 bit ballots; kMaxShards: binary search, slots in LDS).  One
+// ballots (8: 3-bit compare tree; 16: 4-bit tree; 32 / 64 / 128: binary
+// search and 5 / 6 / 7 bit ballots, slots in lanes; kMaxShards: binary
+// search, slots in LDS).  One
 // instantiation per method keeps each one's registers, and so its occupancy,
 // to what its own path needs; the bag-at-a-time path for out-of-order
 // offsets is in all of them.
@@ -1101,12 +1157,17 @@ __global__ __launch_bounds__(kBlock) void eb_bucket_scatter(const BucketArgs a)
     // G <= 64: destination d's, for contiguous bags) depend on the bounds:
     // read them first, so that these loads are in flight together.
     int64_t s = 0, e = 0, S, E;
-    int64_t first_slot = 0;
+    int64_t first_slot = 0, first_slot_hi = 0; // destinations lane and lane + 64
     if (live) {
         wave_bag_loads<IT>(a, p0, nb, lane, s, e);
-        if (G <= kWave && lane < G)
+        if (G <= 2 * kWave && lane < G)
             first_slot = a.segments[lane] + (p0 % kStartStride == 0 ? a.starts[(int64_t)lane * a.nq + p0 / kStartStride]
                                                                    : a.out_offsets[(int64_t)lane * row + p0]);
+        if (kOwners == 2 * kWave && lane + kWave < G) {
+            const int d = lane + kWave;
+            first_slot_hi = a.segments[d] + (p0 % kStartStride == 0 ? a.starts[(int64_t)d * a.nq + p0 / kStartStride]
+                                                                    : a.out_offsets[(int64_t)d * row + p0]);
+        }
     }
     for (int g = threadIdx.x; g <= G; g += kBlock) bnd[g] = a.bounds[(int64_t)t * (G + 1) + g];
     __syncthreads();
@@ -1153,6 +1214,23 @@ __global__ __launch_bounds__(kBlock) void eb_bucket_scatter(const BucketArgs a)
             scatter_mid<IT, 5>(a, bnd, lane, first_slot, S, E);
         } else if constexpr (kOwners == kWave) {
             scatter_mid<IT, 6>(a, bnd, lane, first_slot, S, E);
+        }
+        return;
+    }
+    if (kOwners == 2 * kWave && contiguous) {
+        // 65 to 128 destinations: two slots per lane (scatter_wide_pass).
+        uint32_t lbit[6];
+#pragma unroll
+        for (int i = 0; i < 6; ++i) lbit[i] = (uint32_t)((lane >> i) & 1) - 1u;
+        int64_t slot[2] = {first_slot, first_slot_hi};
+        const FewBounds eb = eighth_bounds(bnd, G);
+        constexpr int kPass = kScatterChunks * kWave;
+        for (int64_t k0 = S; k0 < E; k0 += kPass) {
+            const int R = __builtin_amdgcn_readfirstlane((int)min<int64_t>(E - k0, (int64_t)kPass));
+            if (R == kPass)
+                scatter_wide_pass<IT, true>(a, bnd, eb, lane, lbit, slot, k0, R);
+            else
+                scatter_wide_pass<IT, false>(a, bnd, eb, lane, lbit, slot, k0, R);
         }
         return;
     }
@@ -1323,6 +1401,7 @@ const void *scatter_kernel(int G)
            : G <= kTreeShards ? (const void *)eb_bucket_scatter<IT, kTreeShards>
            : G <= 32          ? (const void *)eb_bucket_scatter<IT, 32>
            : G <= kWave       ? (const void *)eb_bucket_scatter<IT, kWave>
+           : G <= 2 * kWave   ? (const void *)eb_bucket_scatter<IT, 2 * kWave>
                               : (const void *)eb_bucket_scatter<IT, kMaxShards>;
 }
 

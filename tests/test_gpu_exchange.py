@@ -64,7 +64,7 @@ def check_bucketize(T, B, idx, off, bounds, device, capacity=None, index_dtype=n
         assert np.array_equal(a, b), name
 
 
-@pytest.mark.parametrize("G", [1, 2, 3, 8, 17, 64, 1024])
+@pytest.mark.parametrize("G", [1, 2, 3, 8, 17, 64, 65, 128, 129, 1024])
 @pytest.mark.parametrize("seed", range(3))
 def test_bucketize_matches_oracle(G, seed, device):
     T, B, idx, off, bounds = bucket_case(seed * 31 + G, G, uneven=(seed == 2))
@@ -260,7 +260,7 @@ def draw_bucket_case(seed):
     uneven, with empty blocks, or unsorted), ordinary or disordered offsets
     and the capacity of out_indices."""
     g = np.random.default_rng(seed)
-    G = int(g.choice([1, 2, 3, 5, 8, 9, 16, 31, 32, 33, 64, 65, 200, 1024]))
+    G = int(g.choice([1, 2, 3, 5, 8, 9, 16, 31, 32, 33, 64, 65, 128, 129, 200, 1024]))
     T = int(g.integers(1, 7))
     B = int(g.choice([1, 15, 16, 17, 300, 2048, 2049, 9000, 30000, 60000]))
     while G * T * B > 20_000_000:  # out_offsets stays under 160 MB
