@@ -24,8 +24,9 @@
 //                destinations the most of 16, 32, 64 that leave at least
 //                4608 waves, else 16; 16-bit counts beyond 64; each XCD one
 //                contiguous run of workgroups); each id's owner by
-//                comparisons with the table's block bounds (up to 16 blocks:
-//                a search tree evaluated as wave-wide lane masks) or by
+//                comparisons with the table's block bounds (up to 8 blocks:
+//                a search tree evaluated as wave-wide lane masks; up to 16
+//                the same tree over pairs of blocks and one more compare) or by
 //                binary search over them (staged in LDS); for ordinary CSR
 //                offsets the wave streams its whole id range in 64-id chunks
 //                into a [bag][destination] histogram in LDS, else it walks
@@ -168,55 +169,52 @@ __device__ __forceinline__ int few_bits(const FewMasks &o)
     return (lane_bit(o.b0) ? kScale : 0) | (lane_bit(o.b1) ? 2 * kScale : 0) | (lane_bit(o.b2) ? 4 * kScale : 0);
 }
 
-// The same search tree one level deeper, for 9 to 16 blocks: 15 inner bounds
-// (unused ones past every id) and the owner's four bits.  Level l of the tree
-// decides bit 3 - l; its 2^l candidate bound masks are those at (2p + 1) *
-// 2^(3 - l) - 1 for the 2^l values p of the bits above, and the bits already
-// decided select among them, the lowest of them first.
+// The owner among 9 to 16 blocks, as its four bits: bits 3..1 are the 3-bit
+// tree above over the bounds 2, 4, ..., 14 (h, the pair of blocks holding
+// the id; unused bounds past every id), bit 0 one more comparison, with the
+// pair's middle bound 2 h + 1, read per lane from the bounds in LDS.  For
+// non-decreasing bounds bnd[2h] <= i < bnd[2h + 2], so the owner is owner_of's
+// block.  For any bounds a valid id's owner stays below G: h reaches a pair
+// only through a right turn at its first bound, never an unused one for an
+// id below hi, so 2 h <= G - 1, and 2 h + 1 = G compares with bnd[G], which
+// no valid id reaches.
 constexpr int kTreeShards = 16;
 constexpr int kTreeBits = 4;
 
 struct TreeBounds {
-    int64_t lo, hi;
-    int64_t inner[kTreeShards - 1];
+    FewBounds even;     // lo, hi and the inner bounds 2, 4, ..., 14
+    const int64_t *bnd; // all G + 1 bounds (LDS)
+    int G;
 };
 
 __device__ __forceinline__ TreeBounds tree_bounds(const int64_t *bnd, int G)
 {
     TreeBounds b;
-    b.lo = bnd[0];
-    b.hi = bnd[G];
+    b.even.lo = bnd[0];
+    b.even.hi = bnd[G];
 #pragma unroll
-    for (int j = 1; j < kTreeShards; ++j) b.inner[j - 1] = j < G ? bnd[j] : INT64_MAX;
+    for (int k = 0; k < kFewShards - 1; ++k) b.even.inner[k] = 2 * (k + 1) < G ? bnd[2 * (k + 1)] : INT64_MAX;
+    b.bnd = bnd;
+    b.G = G;
     return b;
 }
 
 struct TreeMasks {
     uint64_t valid;        // lanes of `in` with lo <= i < hi
-    uint64_t b[kTreeBits]; // lanes whose owner has bit k set
+    uint64_t b[kTreeBits]; // lanes whose owner has bit k set (bit 0 also set on lanes outside valid)
 };
 
 __device__ __forceinline__ TreeMasks tree_owner_masks(const TreeBounds &t, int64_t i, uint64_t in)
 {
-    uint64_t m[kTreeShards - 1];
-#pragma unroll
-    for (int j = 0; j < kTreeShards - 1; ++j) m[j] = __ballot(i >= t.inner[j]);
+    const FewMasks f = few_owner_masks(t.even, i, in);
+    const int h = few_bits<1>(f);
+    const int64_t mid = t.bnd[min(2 * h + 1, t.G)]; // clamped for lanes outside valid
     TreeMasks o;
-    o.valid = in & __ballot(i >= t.lo) & __ballot(i < t.hi);
-#pragma unroll
-    for (int l = 0; l < kTreeBits; ++l) {
-        const int bit = kTreeBits - 1 - l;
-        uint64_t c[kTreeShards / 2];
-#pragma unroll
-        for (int p = 0; p < (1 << l); ++p) c[p] = m[((2 * p + 1) << bit) - 1];
-#pragma unroll
-        for (int q = 0; q < l; ++q) {
-            const uint64_t sel = o.b[bit + 1 + q];
-#pragma unroll
-            for (int p = 0; p < (1 << (l - q - 1)); ++p) c[p] = (sel & c[2 * p + 1]) | (~sel & c[2 * p]);
-        }
-        o.b[bit] = c[0];
-    }
+    o.valid = f.valid;
+    o.b[0] = __ballot(i >= mid);
+    o.b[1] = f.b0;
+    o.b[2] = f.b1;
+    o.b[3] = f.b2;
     return o;
 }
 
@@ -398,7 +396,7 @@ __device__ __forceinline__ void wave_sync_lds()
 // One pass of count's loop: the ids at k0 + u * 64 + lane, the first R of
 // them (all kCountChunks<kOwners> * 64 when kFull, the usual case, which then
 // needs no tail masks).
-// kOwners: 8 (owners by the 3-bit tree), 16 (the 4-bit tree), or 0 (by
+// kOwners: 8 (owners by the 3-bit tree), 16 (by pairs of blocks), or 0 (by
 // binary search over the bounds in LDS); kPacked: 16-bit counts, two to a word.
 template <typename IT, int kOwners, bool kFull, bool kPacked>
 __device__ __forceinline__ void count_pass(const BucketArgs &a, const int64_t *bnd, const FewBounds &fb,
@@ -462,7 +460,7 @@ __device__ __forceinline__ void count_chunks(const BucketArgs &a, const int64_t 
 }
 
 // kOwners: how the instantiation finds owners (8: 3-bit compare tree, 16:
-// 4-bit tree, 0: binary search); one instantiation per method and wave size,
+// pairs of blocks, 0: binary search); one instantiation per method and wave size,
 // so that each keeps only its own path's registers.  kPacked (beyond 64
 // destinations): the histogram holds 16-bit counts, two to a word, so that
 // 16-bag waves fit; a wave with a bag of 65,536 ids or more takes the
@@ -936,7 +934,8 @@ __device__ __forceinline__ void scatter_few_pass(const BucketArgs &a, const FewB
         if ((uint64_t)pos[u] < (uint64_t)a.out_cap) put_id<IT>(a, pos[u], id[u]);
 }
 
-// scatter_few_pass for 9 to 16 destinations: owners from the 4-bit tree.
+// scatter_few_pass for 9 to 16 destinations: owners by pairs of blocks
+// (tree_owner_masks).
 template <typename IT, bool kFull>
 __device__ __forceinline__ void scatter_tree_pass(const BucketArgs &a, const TreeBounds &tb, int lane,
                                                   const uint32_t (&lbit)[kTreeBits], int64_t &slot, int64_t k0, int R)
@@ -1131,7 +1130,7 @@ __device__ __forceinline__ void scatter_mid(const BucketArgs &a, const int64_t *
 }
 
 // kOwners: the most destinations the instantiation ranks in one chunk's
-// ballots (8: 3-bit compare tree; 16: 4-bit tree; 32 / 64 / 128: binary
+// ballots (8: 3-bit compare tree; 16: pairs of blocks; 32 / 64 / 128: binary
 // search and 5 / 6 / 7 bit ballots, slots in lanes; kMaxShards: binary
 // search, slots in LDS).  One
 // instantiation per method keeps each one's registers, and so its occupancy,
@@ -1195,7 +1194,7 @@ __global__ __launch_bounds__(kBlock) void eb_bucket_scatter(const BucketArgs a)
         // position) order is position order, so one running slot per
         // destination (lane g keeps destination g's) suffices, and ballots of
         // the owners' 4, 5 or 6 bits rank a whole chunk at once (owners by
-        // the 4-bit tree up to 16 destinations, else by binary search).
+        // pairs of blocks up to 16 destinations, else by binary search).
         if constexpr (kOwners == kTreeShards) {
             const TreeBounds tb = tree_bounds(bnd, G);
             uint32_t lbit[kTreeBits];
