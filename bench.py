@@ -298,6 +298,27 @@ def fused_scan(G, ntiles):
     return 0.5 * G * ntiles * (ntiles + G) <= 1 << 20
 
 
+def count_wave_bags(T, B, G):
+    """Bags per count wave of eb_bucketize: 16, 32 or 64 up to 16
+    destinations (the most that leave at least 4608 waves), else 16."""
+    if G <= 16:
+        for bags in (64, 32):
+            if T * B // bags >= 4608:
+                return bags
+    return 16
+
+
+def scan_kernels(G, T, B):
+    """Kernels per eb_bucketize call: count, scan and scatter, the scan in 1
+    (tiles read count's wave totals themselves: nparts * G * (ntiles + G) / 2
+    reads up to 2^16), 2 (tile sums, fused tile scan) or 3 launches."""
+    ntiles = scan_tile_count(T, B)
+    nparts = T * -(-B // count_wave_bags(T, B, G))
+    if 0.5 * nparts * G * (ntiles + G) <= 1 << 16:
+        return 3
+    return 4 if fused_scan(G, ntiles) else 5
+
+
 def exchange_bench(torch, dev, eb, K, W, Gs=(8,), i32=False):
     """The row-wise exchange's local kernels at the sizes of the skewed
     workloads split over GPUs by rows.  bucketize: the 26-table, 16384-bag
@@ -339,9 +360,10 @@ def exchange_bench(torch, dev, eb, K, W, Gs=(8,), i32=False):
                           "us_per_call": round(us, 1), "ids_per_s": idx.size / us * 1e6,
                           "algorithmic_bytes": by, "algorithmic_GBps": round(by / us / 1e3, 1),
                           "frac_of_8TBps": round(by / us / 1e3 / HBM_PEAK_GBPS, 4),
-                          # count, tile sums, (row prefix when the fused tile scan would read
-                          # over 2^20 tile sums,) tile scan, scatter
-                          "kernels_per_call": 4 if fused_scan(G, scan_tile_count(w.T, w.B)) else 5}), flush=True)
+                          # count, (tile sums unless the tile scan reads the wave totals itself,)
+                          # (row prefix when the fused tile scan would read over 2^20 tile sums,)
+                          # tile scan, scatter
+                          "kernels_per_call": scan_kernels(G, w.T, w.B)}), flush=True)
         del out_off, ws
     del d_i, out_idx
     Gp = 8  # the partial blocks of 8 GPUs, whatever --destinations says
