@@ -263,7 +263,9 @@ int eb_bucketize_workspace(int32_t T, int64_t B, int32_t G, size_t *bytes);
  *                [segments[g], segments[g+1]), in (table, bag, position)
  *                order.  They stay global ids: the receiving GPU pools them
  *                with eb_forward and its own shard range.  Positions at or
- *                past out_capacity are not written.
+ *                past out_capacity are not written; those from segments[G]
+ *                up to it hold unspecified values afterwards (the call may
+ *                use them as scratch).
  *   out_capacity entries of out_indices, >= 0.  nnz always suffices for
  *                ordinary offsets (non-decreasing within [0, nnz]).
  *   segments     device int64 [G+1]; segments[G] = ids sent, the full

@@ -123,6 +123,35 @@ def test_bucketize_bags_past_16_bit_counts(G, device):
     check_bucketize(T, B, idx, off, bounds, device)
 
 
+@pytest.mark.parametrize("G", [8, 16, 40, 100])
+@pytest.mark.parametrize("ordered", [True, False])
+def test_bucketize_counts_staged_or_in_place(G, ordered, device):
+    """count stages 32-bit counts in out_indices when out_offsets reaches
+    32 MB and out_indices has room for all G x T x B of them, else it writes
+    them into out_offsets: short bags in a batch just past that size give
+    the second with out_indices of nnz entries and the first with a larger
+    one; both must match the oracle, for ordinary and disordered offsets
+    (every count path: compare trees, pairs, binary search, packed)."""
+    g = np.random.default_rng(G + 7 * ordered)
+    T = 2
+    B = -(-(33 << 20) // (8 * G * T))  # out_offsets just over 33 MB
+    L = g.integers(0, 3, T * B)
+    off = wl.offsets_from_lengths(L)
+    if not ordered:  # some offsets moved a little: waves with bags out of order
+        nnz = int(off[-1])
+        p = g.choice(np.arange(1, T * B), 2000, replace=False)
+        off[p] = np.clip(off[p] + g.integers(-6, 7, p.size), -3, nnz + 3)
+    rows = 100_000
+    idx = g.integers(-2, rows + 2, int(off[-1]), dtype=np.int64)
+    bounds = even_bounds([rows] * T, G)
+    assert G * (T * B + 1) * 8 >= 32 << 20 and len(idx) * 8 < G * T * B * 4
+    print(f"G={G} T={T} B={B} nnz={len(idx)}", flush=True)
+    check_bucketize(T, B, idx, off, bounds, device)  # out_indices of nnz entries: counts in place
+    check_bucketize(T, B, idx, off, bounds, device, capacity=G * T * B // 2 + 1)  # staged
+    # (moved offsets can make bags overlap, sending more ids than nnz: the
+    # first call then also checks a truncating capacity)
+
+
 def test_bucketize_edge_cases(device):
     # no ids at all
     off = np.zeros(2 * 5 + 1, dtype=np.int64)
