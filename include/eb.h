@@ -277,10 +277,13 @@ int eb_bucketize_workspace(int32_t T, int64_t B, int32_t G, size_t *bytes);
  *   stream       a hipStream_t (NULL = the null stream); asynchronous.
  *
  * No allocation, no host synchronisation; calls that overlap on the same
- * workspace race.  Errors: EB_ERR_INVALID for NULL buffers (indices may be
- * NULL when nnz == 0, out_indices when out_capacity == 0), negative sizes, or
- * a workspace that is too small; EB_ERR_UNSUPPORTED for G > 1024 or a batch too large
- * for one launch; EB_ERR_HIP when a launch fails.  With non-decreasing
+ * workspace race.  out_offsets, out_indices, segments and the workspace must
+ * not overlap each other or the inputs (count may stage its results in
+ * out_indices while the ids are still being read).  Errors: EB_ERR_INVALID
+ * for NULL buffers (indices may be NULL when nnz == 0, out_indices when
+ * out_capacity == 0), negative sizes, or a workspace that is too small;
+ * EB_ERR_UNSUPPORTED for G > 1024 or a batch too large for one launch;
+ * EB_ERR_HIP when a launch fails.  With non-decreasing
  * bounds the result equals the definition above; other bounds give an
  * unspecified split but every access stays in bounds.
  */
