@@ -761,10 +761,10 @@ __global__ __launch_bounds__(kBlock) void eb_scan_tile_sums(const ScanArgs a)
 }
 
 // Pass 2b, where the fused tile scan would read too many tile sums (past
-// kFusedScanReads): one workgroup per
-// row scans the row's tile sums in place into each tile's prefix within the
-// row (exclusive), kScanTile at a time, and stores the row's total in
-// row_totals[g], from which the row's first tile takes its segment start.
+// kFusedScanReads): one workgroup per row scans the row's tile sums in place
+// into each tile's prefix within the row (exclusive), kScanTile at a time,
+// and stores the row's total in row_totals[g], from which the row's first
+// tile takes its segment start.
 __global__ __launch_bounds__(kBlock) void eb_scan_row_prefix(const ScanArgs a)
 {
     const int g = blockIdx.x;
