@@ -285,7 +285,8 @@ struct BucketArgs {
     const int64_t *starts;   // [G][nq]: out_offsets[g][16 q] (scatter pass; workspace)
     int64_t nq;
     int64_t *wave_totals;    // [nparts][G]: each count wave's ids per destination (workspace)
-    int32_t *counts32;       // or null: count's counts, [G][TB] int32, staged in out_indices
+    uint16_t *counts16;      // or null: count's counts, [G][TB] uint16, staged in out_indices
+                             // (0xFFFF: 65,535 or more, the count itself in out_offsets)
     int64_t nparts;          // T * count_waves_per_table
     int64_t out_cap;         // entries of out_indices; positions at or past it are not written
     int64_t nnz;
@@ -308,20 +309,26 @@ __device__ __forceinline__ int64_t offset_at(const BucketArgs &a, int64_t p) { r
 template <typename IT>
 __device__ __forceinline__ void put_id(const BucketArgs &a, int64_t pos, int64_t id) { ((IT *)a.out_indices)[pos] = (IT)id; }
 
-// Measured, workload 3's batch and its first 2048 bags per table, old and new
-// library in one process: staged counts 1-8% faster from 16 to 64
-// destinations (out_offsets 54-218 MB), 5% slower for the small batch (1.7 MB).
+// Measured on workload 3's batch and its first 2048 bags per table, old and
+// new library in one process: counts staged as 16 bits 2-22% faster from 64
+// to 150 destinations (out_offsets 218-511 MB), unchanged at 16 and 32; at
+// 8 destinations (27 MB) and for the small batch (1.7 MB) staging was up to
+// 5% slower.
 constexpr int64_t kStageCountsMinBytes = (int64_t)32 << 20;
 
-// count's result for destination g and position p: 32 bits in out_indices
+// count's result for destination g and position p: 16 bits in out_indices
 // (free until the scatter) where it has room for all G * T * B of them, so
-// that the scan reads half the bytes, else in place in out_offsets[g][p + 1].
+// that count writes and the scan reads a quarter of the bytes (a count of
+// 65,535 or more leaves 0xFFFF there and itself in out_offsets[g][p + 1]),
+// else in place in out_offsets[g][p + 1].
 __device__ __forceinline__ void put_count(const BucketArgs &a, int g, int64_t p, int v)
 {
-    if (a.counts32)
-        a.counts32[(int64_t)g * a.TB + p] = v;
-    else
+    if (a.counts16) {
+        a.counts16[(int64_t)g * a.TB + p] = (uint16_t)(v < 0xFFFF ? v : 0xFFFF);
+        if (v >= 0xFFFF) a.out_offsets[(int64_t)g * (a.TB + 1) + p + 1] = v;
+    } else {
         a.out_offsets[(int64_t)g * (a.TB + 1) + p + 1] = v;
+    }
 }
 
 // Workgroups are dealt to the 8 XCDs in turn (workgroup b to XCD b % 8).
@@ -643,7 +650,7 @@ struct ScanArgs {
     int32_t waves_per_table;  // count's waves holding bags, per table
     int32_t bags_per_wave;    // count's (a power of two dividing kScanTile)
     int32_t mode;       // kScanDirect, kScanFused or kScanRows (below)
-    const int32_t *counts32; // count's counts when staged in out_indices, else null (in rows)
+    const uint16_t *counts16; // count's counts when staged in out_indices (see put_count), else null
 };
 
 // How pass 2c finds a tile's prefix and the rows' segment starts: from
@@ -824,13 +831,16 @@ __global__ __launch_bounds__(kBlock) void eb_scan_tiles(const ScanArgs a)
     const int64_t lo = tl.lo;
     const int n = tl.n;
     int64_t v[kScanPer];
-    if (a.counts32) {
-        const int32_t *cnt = a.counts32 + (int64_t)g * a.TB + lo;
+    if (a.counts16) {
+        const uint16_t *cnt = a.counts16 + (int64_t)g * a.TB + lo;
 #pragma unroll
         for (int j = 0; j < kScanPer; ++j) {
             const int i = j * kBlock + threadIdx.x;
             v[j] = i < n ? cnt[i] : 0;
         }
+#pragma unroll
+        for (int j = 0; j < kScanPer; ++j) // 0xFFFF: the count is in the row
+            if (v[j] == 0xFFFF) v[j] = row[lo + j * kBlock + threadIdx.x];
     } else {
 #pragma unroll
         for (int j = 0; j < kScanPer; ++j) {
@@ -1553,14 +1563,14 @@ int bucketize_impl(int32_t T, int64_t B, int32_t G, const int64_t *bounds, int32
     ba.wave_totals = wave_totals;
     ba.nparts = shape.nparts;
     sa.segments = segments;
-    // count's results go to out_indices as int32 where it has room for them
+    // count's results go to out_indices as uint16 where it has room for them
     // and they would not stay in the L2s (at least kStageCountsMinBytes of
     // out_offsets); small batches keep them in place, where the scan finds
     // them in cache.
-    const bool stage32 = TB > 0 && (int64_t)G * (TB + 1) * 8 >= kStageCountsMinBytes &&
-                         out_capacity >= ((int64_t)G * TB * 4 + (i32 ? 3 : 7)) / (i32 ? 4 : 8);
-    ba.counts32 = stage32 ? (int32_t *)out_indices : nullptr;
-    sa.counts32 = ba.counts32;
+    const bool stage16 = TB > 0 && (int64_t)G * (TB + 1) * 8 >= kStageCountsMinBytes &&
+                         out_capacity >= ((int64_t)G * TB * 2 + (i32 ? 3 : 7)) / (i32 ? 4 : 8);
+    ba.counts16 = stage16 ? (uint16_t *)out_indices : nullptr;
+    sa.counts16 = ba.counts16;
     sa.TB = TB;
     sa.B = B;
     sa.T = T;

@@ -126,28 +126,37 @@ def test_bucketize_bags_past_16_bit_counts(G, device):
 @pytest.mark.parametrize("G", [8, 16, 40, 100])
 @pytest.mark.parametrize("ordered", [True, False])
 def test_bucketize_counts_staged_or_in_place(G, ordered, device):
-    """count stages 32-bit counts in out_indices when out_offsets reaches
+    """count stages 16-bit counts in out_indices when out_offsets reaches
     32 MB and out_indices has room for all G x T x B of them, else it writes
     them into out_offsets: short bags in a batch just past that size give
     the second with out_indices of nnz entries and the first with a larger
     one; both must match the oracle, for ordinary and disordered offsets
-    (every count path: compare trees, pairs, binary search, packed)."""
+    (every count path: compare trees, pairs, binary search, packed).  Three
+    bags send 65,534, 65,535 and 70,000 ids to one destination: counts below,
+    at and past what 16 bits hold (the last two go through out_offsets)."""
     g = np.random.default_rng(G + 7 * ordered)
     T = 2
     B = -(-(33 << 20) // (8 * G * T))  # out_offsets just over 33 MB
     L = g.integers(0, 3, T * B)
+    big = {5: 70_000, 1000: 65_535, T * B - 3: 65_534}
+    for p_, n in big.items():
+        L[p_] = n
     off = wl.offsets_from_lengths(L)
     if not ordered:  # some offsets moved a little: waves with bags out of order
         nnz = int(off[-1])
-        p = g.choice(np.arange(1, T * B), 2000, replace=False)
+        p = g.choice(np.setdiff1d(np.arange(1, T * B), [q + d for q in big for d in (0, 1)]), 2000, replace=False)
         off[p] = np.clip(off[p] + g.integers(-6, 7, p.size), -3, nnz + 3)
     rows = 100_000
-    idx = g.integers(-2, rows + 2, int(off[-1]), dtype=np.int64)
     bounds = even_bounds([rows] * T, G)
-    assert G * (T * B + 1) * 8 >= 32 << 20 and len(idx) * 8 < G * T * B * 4
+    idx = g.integers(-2, rows + 2, int(off[-1]), dtype=np.int64)
+    for p_ in big:  # every id of the big bags in one block
+        t = p_ // B
+        lo, hi = int(bounds[t][G // 2]), int(bounds[t][G // 2 + 1])
+        idx[off[p_]:off[p_ + 1]] = g.integers(lo, hi, L[p_])
+    assert G * (T * B + 1) * 8 >= 32 << 20 and len(idx) * 8 < G * T * B * 2
     print(f"G={G} T={T} B={B} nnz={len(idx)}", flush=True)
     check_bucketize(T, B, idx, off, bounds, device)  # out_indices of nnz entries: counts in place
-    check_bucketize(T, B, idx, off, bounds, device, capacity=G * T * B // 2 + 1)  # staged
+    check_bucketize(T, B, idx, off, bounds, device, capacity=G * T * B // 4 + 1)  # staged
     # (moved offsets can make bags overlap, sending more ids than nnz: the
     # first call then also checks a truncating capacity)
 
