@@ -67,6 +67,7 @@
 #include <atomic>
 #include <cstring>
 #include <limits>
+#include <type_traits>
 
 #include "../../include/eb.h"
 #include "eb_internal.h"
@@ -321,14 +322,27 @@ constexpr int64_t kStageCountsMinBytes = (int64_t)32 << 20;
 // that count writes and the scan reads a quarter of the bytes (a count of
 // 65,535 or more leaves 0xFFFF there and itself in out_offsets[g][p + 1]),
 // else in place in out_offsets[g][p + 1].
+// kStaged: a.counts16 is set (chosen per call; callers branch once, outside
+// their loops, through with_staging).
+template <bool kStaged>
 __device__ __forceinline__ void put_count(const BucketArgs &a, int g, int64_t p, int v)
 {
-    if (a.counts16) {
+    if constexpr (kStaged) {
         a.counts16[(int64_t)g * a.TB + p] = (uint16_t)(v < 0xFFFF ? v : 0xFFFF);
         if (v >= 0xFFFF) a.out_offsets[(int64_t)g * (a.TB + 1) + p + 1] = v;
     } else {
         a.out_offsets[(int64_t)g * (a.TB + 1) + p + 1] = v;
     }
+}
+
+// f(std::true_type) if the call stages its counts, else f(std::false_type).
+template <typename F>
+__device__ __forceinline__ void with_staging(const BucketArgs &a, F f)
+{
+    if (a.counts16)
+        f(std::true_type{});
+    else
+        f(std::false_type{});
 }
 
 // Workgroups are dealt to the 8 XCDs in turn (workgroup b to XCD b % 8).
@@ -539,10 +553,14 @@ __global__ __launch_bounds__(kBlock) void eb_bucket_count(const BucketArgs a)
             // The counts (each taken from its half word) transposed as below;
             // lane g + 64 r adds up destination g + 64 r's total over all bags.
             const int stride = count_stride(G, true);
-            for (int x = lane; x < kBags * G; x += kWave) {
-                const int j = x & (kBags - 1), g = x / kBags;
-                if (j < nb) put_count(a, g, p0 + j, (int)(((unsigned)hist[j * stride + (g >> 1)] >> ((g & 1) * 16)) & 0xFFFFu));
-            }
+            with_staging(a, [&](auto staged) {
+                for (int x = lane; x < kBags * G; x += kWave) {
+                    const int j = x & (kBags - 1), g = x / kBags;
+                    if (j < nb)
+                        put_count<decltype(staged)::value>(
+                            a, g, p0 + j, (int)(((unsigned)hist[j * stride + (g >> 1)] >> ((g & 1) * 16)) & 0xFFFFu));
+                }
+            });
             for (int g = lane; g < G; g += kWave) {
                 int64_t sum = 0;
 #pragma unroll
@@ -555,10 +573,12 @@ __global__ __launch_bounds__(kBlock) void eb_bucket_count(const BucketArgs a)
         // Entry x of the histogram's transpose: bag x % kBags, destination
         // x / kBags; a store covers 64 / kBags rows, kBags bags of each.
         const int stride = count_stride(G);
-        for (int x = lane; x < kBags * G; x += kWave) {
-            const int j = x & (kBags - 1), g = x / kBags;
-            if (j < nb) put_count(a, g, p0 + j, hist[j * stride + g]);
-        }
+        with_staging(a, [&](auto staged) {
+            for (int x = lane; x < kBags * G; x += kWave) {
+                const int j = x & (kBags - 1), g = x / kBags;
+                if (j < nb) put_count<decltype(staged)::value>(a, g, p0 + j, hist[j * stride + g]);
+            }
+        });
         // The wave's totals (unpacked counts: at most 64 destinations): lane
         // q * Gp + g (Gp = G rounded up to a power of two) adds up
         // destination g over every (64 / Gp)-th bag from bag q on, then the
@@ -589,10 +609,12 @@ __global__ __launch_bounds__(kBlock) void eb_bucket_count(const BucketArgs a)
             if (g >= 0) atomicAdd(&hist[g], 1);
         }
         wave_sync_lds();
-        for (int g = lane; g < G; g += kWave) {
-            put_count(a, g, p0 + j, hist[g]);
-            run[g] += hist[g];
-        }
+        with_staging(a, [&](auto staged) {
+            for (int g = lane; g < G; g += kWave) {
+                put_count<decltype(staged)::value>(a, g, p0 + j, hist[g]);
+                run[g] += hist[g];
+            }
+        });
         wave_sync_lds();
     }
     for (int g = lane; g < G; g += kWave) totals[g] = run[g];
