@@ -286,8 +286,8 @@ struct BucketArgs {
     const int64_t *starts;   // [G][nq]: out_offsets[g][16 q] (scatter pass; workspace)
     int64_t nq;
     int64_t *wave_totals;    // [nparts][G]: each count wave's ids per destination (workspace)
-    uint16_t *counts16;      // or null: count's counts, [G][TB] uint16, staged in out_indices
-                             // (0xFFFF: 65,535 or more, the count itself in out_offsets)
+    uint8_t *counts8;        // or null: count's counts, [G][TB] uint8, staged in out_indices
+                             // (0xFF: 255 or more, the count itself in out_offsets)
     int64_t nparts;          // T * count_waves_per_table
     int64_t out_cap;         // entries of out_indices; positions at or past it are not written
     int64_t nnz;
@@ -311,25 +311,26 @@ template <typename IT>
 __device__ __forceinline__ void put_id(const BucketArgs &a, int64_t pos, int64_t id) { ((IT *)a.out_indices)[pos] = (IT)id; }
 
 // Measured on workload 3's batch and its first 2048 bags per table, old and
-// new library in one process: counts staged as 16 bits 2-22% faster from 64
-// to 150 destinations (out_offsets 218-511 MB), unchanged at 16 and 32; at
-// 8 destinations (27 MB) and for the small batch (1.7 MB) staging was up to
-// 5% slower.
+// new library in one process: counts staged as bytes 1-27% faster from 32 to
+// 300 destinations (out_offsets 109-1022 MB), unchanged at 16; at 8
+// destinations (27 MB) and for the small batch (1.7 MB) staging was up to 5%
+// slower.
 constexpr int64_t kStageCountsMinBytes = (int64_t)32 << 20;
 
-// count's result for destination g and position p: 16 bits in out_indices
+// count's result for destination g and position p: one byte in out_indices
 // (free until the scatter) where it has room for all G * T * B of them, so
-// that count writes and the scan reads a quarter of the bytes (a count of
-// 65,535 or more leaves 0xFFFF there and itself in out_offsets[g][p + 1]),
-// else in place in out_offsets[g][p + 1].
-// kStaged: a.counts16 is set (chosen per call; callers branch once, outside
+// that count writes and the scan reads an eighth of the bytes (a count of
+// 255 or more, which a bag's ids seldom reach in one destination, leaves
+// 0xFF there and itself in out_offsets[g][p + 1]), else in place in
+// out_offsets[g][p + 1].
+// kStaged: a.counts8 is set (chosen per call; callers branch once, outside
 // their loops, through with_staging).
 template <bool kStaged>
 __device__ __forceinline__ void put_count(const BucketArgs &a, int g, int64_t p, int v)
 {
     if constexpr (kStaged) {
-        a.counts16[(int64_t)g * a.TB + p] = (uint16_t)(v < 0xFFFF ? v : 0xFFFF);
-        if (v >= 0xFFFF) a.out_offsets[(int64_t)g * (a.TB + 1) + p + 1] = v;
+        a.counts8[(int64_t)g * a.TB + p] = (uint8_t)(v < 0xFF ? v : 0xFF);
+        if (v >= 0xFF) a.out_offsets[(int64_t)g * (a.TB + 1) + p + 1] = v;
     } else {
         a.out_offsets[(int64_t)g * (a.TB + 1) + p + 1] = v;
     }
@@ -339,7 +340,7 @@ __device__ __forceinline__ void put_count(const BucketArgs &a, int g, int64_t p,
 template <typename F>
 __device__ __forceinline__ void with_staging(const BucketArgs &a, F f)
 {
-    if (a.counts16)
+    if (a.counts8)
         f(std::true_type{});
     else
         f(std::false_type{});
@@ -672,7 +673,7 @@ struct ScanArgs {
     int32_t waves_per_table;  // count's waves holding bags, per table
     int32_t bags_per_wave;    // count's (a power of two dividing kScanTile)
     int32_t mode;       // kScanDirect, kScanFused or kScanRows (below)
-    const uint16_t *counts16; // count's counts when staged in out_indices (see put_count), else null
+    const uint8_t *counts8; // count's counts when staged in out_indices (see put_count), else null
 };
 
 // How pass 2c finds a tile's prefix and the rows' segment starts: from
@@ -853,16 +854,16 @@ __global__ __launch_bounds__(kBlock) void eb_scan_tiles(const ScanArgs a)
     const int64_t lo = tl.lo;
     const int n = tl.n;
     int64_t v[kScanPer];
-    if (a.counts16) {
-        const uint16_t *cnt = a.counts16 + (int64_t)g * a.TB + lo;
+    if (a.counts8) {
+        const uint8_t *cnt = a.counts8 + (int64_t)g * a.TB + lo;
 #pragma unroll
         for (int j = 0; j < kScanPer; ++j) {
             const int i = j * kBlock + threadIdx.x;
             v[j] = i < n ? cnt[i] : 0;
         }
 #pragma unroll
-        for (int j = 0; j < kScanPer; ++j) // 0xFFFF: the count is in the row
-            if (v[j] == 0xFFFF) v[j] = row[lo + j * kBlock + threadIdx.x];
+        for (int j = 0; j < kScanPer; ++j) // 0xFF: the count is in the row
+            if (v[j] == 0xFF) v[j] = row[lo + j * kBlock + threadIdx.x];
     } else {
 #pragma unroll
         for (int j = 0; j < kScanPer; ++j) {
@@ -1585,14 +1586,14 @@ int bucketize_impl(int32_t T, int64_t B, int32_t G, const int64_t *bounds, int32
     ba.wave_totals = wave_totals;
     ba.nparts = shape.nparts;
     sa.segments = segments;
-    // count's results go to out_indices as uint16 where it has room for them
+    // count's results go to out_indices as bytes where it has room for them
     // and they would not stay in the L2s (at least kStageCountsMinBytes of
     // out_offsets); small batches keep them in place, where the scan finds
     // them in cache.
-    const bool stage16 = TB > 0 && (int64_t)G * (TB + 1) * 8 >= kStageCountsMinBytes &&
-                         out_capacity >= ((int64_t)G * TB * 2 + (i32 ? 3 : 7)) / (i32 ? 4 : 8);
-    ba.counts16 = stage16 ? (uint16_t *)out_indices : nullptr;
-    sa.counts16 = ba.counts16;
+    const bool stage8 = TB > 0 && (int64_t)G * (TB + 1) * 8 >= kStageCountsMinBytes &&
+                        out_capacity >= ((int64_t)G * TB + (i32 ? 3 : 7)) / (i32 ? 4 : 8);
+    ba.counts8 = stage8 ? (uint8_t *)out_indices : nullptr;
+    sa.counts8 = ba.counts8;
     sa.TB = TB;
     sa.B = B;
     sa.T = T;

@@ -126,19 +126,21 @@ def test_bucketize_bags_past_16_bit_counts(G, device):
 @pytest.mark.parametrize("G", [8, 16, 40, 100])
 @pytest.mark.parametrize("ordered", [True, False])
 def test_bucketize_counts_staged_or_in_place(G, ordered, device):
-    """count stages 16-bit counts in out_indices when out_offsets reaches
-    32 MB and out_indices has room for all G x T x B of them, else it writes
+    """count stages byte counts in out_indices when out_offsets reaches 32
+    MB and out_indices has room for all G x T x B of them, else it writes
     them into out_offsets: short bags in a batch just past that size give
     the second with out_indices of nnz entries and the first with a larger
     one; both must match the oracle, for ordinary and disordered offsets
-    (every count path: compare trees, pairs, binary search, packed).  Three
-    bags send 65,534, 65,535 and 70,000 ids to one destination: counts below,
-    at and past what 16 bits hold (the last two go through out_offsets)."""
+    (every count path: compare trees, pairs, binary search, packed).  Some
+    bags send all their ids to one destination: 254, 255 and 256 (below, at
+    and past what a byte holds: the last two go through out_offsets), 65,535
+    (the most a packed 16-bit histogram count holds) and 70,000 (a wave that
+    counts bag by bag beyond 64 destinations)."""
     g = np.random.default_rng(G + 7 * ordered)
     T = 2
     B = -(-(33 << 20) // (8 * G * T))  # out_offsets just over 33 MB
-    L = g.integers(0, 3, T * B)
-    big = {5: 70_000, 1000: 65_535, T * B - 3: 65_534}
+    L = (g.random(T * B) < 0.3).astype(np.int64)
+    big = {5: 70_000, 1000: 65_535, 3000: 254, 3001: 255, T * B - 3: 256}
     for p_, n in big.items():
         L[p_] = n
     off = wl.offsets_from_lengths(L)
@@ -153,10 +155,10 @@ def test_bucketize_counts_staged_or_in_place(G, ordered, device):
         t = p_ // B
         lo, hi = int(bounds[t][G // 2]), int(bounds[t][G // 2 + 1])
         idx[off[p_]:off[p_ + 1]] = g.integers(lo, hi, L[p_])
-    assert G * (T * B + 1) * 8 >= 32 << 20 and len(idx) * 8 < G * T * B * 2
+    assert G * (T * B + 1) * 8 >= 32 << 20 and len(idx) * 8 < G * T * B
     print(f"G={G} T={T} B={B} nnz={len(idx)}", flush=True)
     check_bucketize(T, B, idx, off, bounds, device)  # out_indices of nnz entries: counts in place
-    check_bucketize(T, B, idx, off, bounds, device, capacity=G * T * B // 4 + 1)  # staged
+    check_bucketize(T, B, idx, off, bounds, device, capacity=G * T * B // 8 + 1)  # staged
     # (moved offsets can make bags overlap, sending more ids than nnz: the
     # first call then also checks a truncating capacity)
 
