@@ -235,8 +235,10 @@ int eb_forward_ex(const eb_tables *tables, int32_t T, const int64_t *rows, int32
 /*
  * eb_bucketize_workspace -- device workspace, in bytes, that eb_bucketize
  * needs for T tables, B bags per table and G destinations (at least 1, at
- * most 1024).  Returns EB_ERR_INVALID for NULL bytes or bad sizes,
- * EB_ERR_UNSUPPORTED for G > 1024.  Touches no device state.
+ * most 1024): the three-kernel path's share, rounded up to 256 bytes, and a
+ * fixed 66,048 bytes for the one-pass kernel (below).  Returns
+ * EB_ERR_INVALID for NULL bytes or bad sizes, EB_ERR_UNSUPPORTED for G >
+ * 1024.  Touches no device state.
  */
 int eb_bucketize_workspace(int32_t T, int64_t B, int32_t G, size_t *bytes);
 
@@ -275,6 +277,18 @@ int eb_bucketize_workspace(int32_t T, int64_t B, int32_t G, size_t *bytes);
  *   workspace    device scratch of at least eb_bucketize_workspace() bytes,
  *                owned by the caller; its contents are not kept.
  *   stream       a hipStream_t (NULL = the null stream); asynchronous.
+ *
+ * Paths: batches of at least 2^23 ids with at most 8 destinations and 1024
+ * tables, outside a graph capture, run a one-pass kernel that reads every
+ * id once: its workgroups (as many as the GPU holds resident at once) meet
+ * at one grid-wide barrier.  The three-kernel path (count, scan, scatter)
+ * is launched behind it and returns at once when the one-pass kernel has
+ * written the outputs; it does the work instead when the offsets are not
+ * ordinary, or when the barrier gave up (about 30-60 ms of waiting, when
+ * other work on the GPU keeps workgroups from being resident).  Both give
+ * the same outputs.  The environment variable EB_BUCKETIZE_ONE_PASS (read on
+ * every call) forces the choice: 0 never, 1 whenever the kernel can hold
+ * the batch (up to 8 destinations and about 23 million ids).
  *
  * No allocation, no host synchronisation; calls that overlap on the same
  * workspace race.  out_offsets, out_indices, segments and the workspace must

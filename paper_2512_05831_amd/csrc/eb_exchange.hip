@@ -18,8 +18,12 @@
 // contraction); eb_sum_partials is bound by it, eb_bucketize by its waves'
 // chains of dependent loads and by instruction issue.
 //
-// eb_bucketize runs three kernels on the caller's stream (eb_bucketize_ex the
-// same with int32 ids, offsets and scattered ids, each widened on load):
+// eb_bucketize runs, for batches of at least kOneMinIds ids and at most 8
+// destinations, a one-pass kernel that reads every id once (see "One-pass
+// bucketize" below), followed by the three kernels here, which return at
+// once when it has written the outputs and otherwise do the work; every
+// other batch takes the three kernels alone (eb_bucketize_ex the same with
+// int32 ids, offsets and scattered ids, each widened on load):
 //   1. count   : a wave takes 16 to 64 consecutive bags (for up to 16
 //                destinations the most of 16, 32, 64 that leave at least
 //                4608 waves, else 16; 16-bit counts beyond 64; each XCD one
@@ -65,6 +69,7 @@
 
 #include <algorithm>
 #include <atomic>
+#include <cstdlib>
 #include <cstring>
 #include <limits>
 #include <type_traits>
@@ -297,6 +302,7 @@ struct BucketArgs {
     int32_t blocks_per_table;       // scatter's workgroups per table
     int32_t count_blocks_per_table; // count's
     int32_t count_waves_per_table;  // count's waves that hold bags, per table
+    const int32_t *skip;            // or null: when it holds nonzero, the one-pass kernel wrote the outputs
 };
 
 // The batch's index type IT (int64_t or int32_t) types the ids, the offsets
@@ -511,6 +517,7 @@ __global__ __launch_bounds__(kBlock) void eb_bucket_count(const BucketArgs a)
 {
     static_assert(kBags >= 16 && kBags <= kWave && (kBags & (kBags - 1)) == 0, "bags per count wave");
     static_assert(!kPacked || kOwners == 0, "packed counts with binary search only");
+    if (a.skip && *a.skip) return;
     extern __shared__ int64_t lds[];
     const int G = a.G;
     int64_t *bnd = lds;
@@ -674,6 +681,7 @@ struct ScanArgs {
     int32_t bags_per_wave;    // count's (a power of two dividing kScanTile)
     int32_t mode;       // kScanDirect, kScanFused or kScanRows (below)
     const uint8_t *counts8; // count's counts when staged in out_indices (see put_count), else null
+    const int32_t *skip; // as BucketArgs::skip
 };
 
 // How pass 2c finds a tile's prefix and the rows' segment starts: from
@@ -755,6 +763,7 @@ constexpr int kSumAhead = 8; // loads issued before the first is added
 __global__ __launch_bounds__(kBlock) void eb_scan_tile_sums(const ScanArgs a)
 {
     __shared__ int64_t part[kBlock];
+    if (a.skip && *a.skip) return;
     const int k = blockIdx.x;
     const int d0 = blockIdx.y * kBlock;
     const int Gy = min(kBlock, a.G - d0);
@@ -797,6 +806,7 @@ __global__ __launch_bounds__(kBlock) void eb_scan_tile_sums(const ScanArgs a)
 // tile takes its segment start.
 __global__ __launch_bounds__(kBlock) void eb_scan_row_prefix(const ScanArgs a)
 {
+    if (a.skip && *a.skip) return;
     const int g = blockIdx.x;
     int64_t *ts = a.tile_sums + (int64_t)g * a.ntiles;
     int64_t carry = 0;
@@ -847,6 +857,7 @@ __device__ __forceinline__ int scan_slot(int e) { return e + e / kScanPer; } // 
 __global__ __launch_bounds__(kBlock) void eb_scan_tiles(const ScanArgs a)
 {
     __shared__ int64_t sm[kScanTile + kScanTile / kScanPer];
+    if (a.skip && *a.skip) return;
     const int g = blockIdx.y;
     const int k = blockIdx.x;
     int64_t *row = a.rows + (int64_t)g * (a.TB + 1) + 1;
@@ -1245,6 +1256,7 @@ template <typename IT, int kOwners>
 __global__ __launch_bounds__(kBlock) void eb_bucket_scatter(const BucketArgs a)
 {
     extern __shared__ int64_t lds[];
+    if (a.skip && *a.skip) return;
     const int G = a.G;
     int64_t *bnd = lds;
     const int lb = xcd_run_block(blockIdx.x, gridDim.x);
@@ -1429,6 +1441,546 @@ __global__ __launch_bounds__(kBlock) void eb_sum_partials_scalar(const PartialAr
     }
 }
 
+// ---------------------------------------------------------------------------
+// One-pass bucketize: ordinary offsets, at most 8 destinations.
+//
+// With ordinary offsets (non-decreasing within [0, nnz]) the batch's ids lie
+// in (table, bag, position) order already, so destination g's output is the
+// subsequence of the ids it owns, and out_offsets[g][p] is the number of ids
+// owned by g at positions before offsets[p]: a rank over positions, with no
+// per-bag counts.  One cooperative launch with one grid-wide barrier then
+// reads every id once:
+//   phase 1  table t's positions [offsets[t B], offsets[(t+1) B]) are split
+//            among max(1, ceil(length / C)) consecutive waves (C = K * 64
+//            ids; T + nnz / C waves at most).  A wave keeps its ids in
+//            registers as 32 bits (every id it will store lies inside the
+//            table's outer bounds, so 32 bits hold it exactly when those do;
+//            a wave whose table's bounds do not fit reloads its ids), keeps
+//            each 64-id chunk's owner masks and the running count per
+//            destination before it in LDS, and publishes its workgroup's
+//            totals; every wave also marks, for its share of the offsets,
+//            which bags start in which wave's positions.
+//   barrier
+//   phase 2  each workgroup adds up the totals of the workgroups before it
+//            and of all of them (the segments).
+//   phase 3  each wave stores its ids at segments[g] + rank, and writes
+//            out_offsets for the bags that start in its positions from the
+//            chunk records (one lane per bag).
+// The workgroups must all be resident at once (a cooperative launch, sized
+// from the occupancy the runtime reports), since phase 3 waits for all of
+// phase 1.  Offsets that are not ordinary are detected in phase 1; the
+// kernel then writes nothing and the call's other kernels do the work.
+constexpr int kOneWaves = 8;                        // waves per workgroup
+constexpr int kOneBlock = kOneWaves * kWave;        // threads per workgroup
+constexpr int kOneBlocksPerCu = 2;                  // 16 waves per compute unit
+constexpr int kOneChunks = 88;                      // 64-id chunks a wave holds, at most
+constexpr int kOneGroup = 8;                        // chunks loaded together
+#ifndef ONE_SG
+#define ONE_SG 2
+#endif
+constexpr int kOneStoreGroup = ONE_SG;                   // chunks stored together
+constexpr int kOneMaxTables = 1024;
+constexpr int kOneTotals = 16;                      // int32 per workgroup: 8 totals, flag
+constexpr uint32_t kOneSpinLimit = 1u << 16;        // barrier polls (about 30-60 ms) before cancelling
+constexpr uint32_t kOneCancel = 0x80000000u;        // the barrier counter's cancelled mark
+static_assert(kOneChunks % kOneGroup == 0, "chunk groups");
+
+struct OneArgs {
+    const int64_t *bounds;  // [T][G+1]
+    const void *indices;    // IT [nnz]
+    const void *offsets;    // IT [T*B+1]
+    int64_t *out_offsets;   // [G][T*B+1]
+    void *out_indices;      // IT [out_cap]
+    int64_t *segments;      // [G+1]
+    int64_t *first_bag;     // [waves+1] (workspace): the first bag that starts at or past wave c's positions
+    int32_t *block_totals;  // [gridDim.x][kOneTotals] (workspace)
+    uint32_t *barrier;      // zero at launch (workspace)
+    int32_t *done;          // (workspace): 1 once the outputs are written
+    int64_t out_cap;
+    int64_t nnz;
+    int64_t B;
+    int64_t TB;
+    int64_t C;              // ids per wave, K * 64
+    int32_t T;
+    int32_t G;
+    int32_t K;              // chunks per wave
+};
+
+struct OneRec {
+    uint64_t valid, b0, b1, b2; // a chunk's owner masks (FewMasks)
+};
+
+// LDS of a wave: kOneChunks + 1 records and running counts (the last: none,
+// and the wave's totals).
+struct OneWaveLds {
+    OneRec rec[kOneChunks + 1];
+    uint16_t cum[kOneChunks + 1][kFewShards];
+};
+
+struct OneBlockLds {
+    OneWaveLds wave[kOneWaves];
+    int64_t tstart[kOneMaxTables + 1]; // offsets[t B], clamped into [0, nnz]
+    int32_t wstart[kOneMaxTables + 1]; // table t's first wave; wstart[T]: waves used
+    int32_t wave_total[kOneWaves][kFewShards];
+    int32_t wave_flag[kOneWaves];
+    int32_t part_before[kOneWaves][kFewShards]; // phase 2: each wave's sums
+    int32_t part_all[kOneWaves][kFewShards];
+    int32_t part_flag[kOneWaves];
+    int32_t pass;                      // the grid barrier's outcome
+    int64_t block_base[kFewShards];    // ids for g in earlier workgroups
+    int64_t total[kFewShards];         // ids for g in all
+    int64_t wave_base[kOneWaves][kFewShards]; // ids for g before the wave
+    int32_t flag;
+};
+
+__device__ __forceinline__ int64_t uniform64(int64_t x)
+{
+    const int lo = __builtin_amdgcn_readfirstlane((int)(x & 0xFFFFFFFF));
+    const int hi = __builtin_amdgcn_readfirstlane((int)(x >> 32));
+    return ((int64_t)hi << 32) | (uint32_t)lo;
+}
+
+__device__ __forceinline__ uint64_t uniform_mask(uint64_t x) { return (uint64_t)uniform64((int64_t)x); }
+
+__device__ __forceinline__ int64_t shfl_up64(int64_t v, int d)
+{
+    const int lo = __shfl_up((int)(v & 0xFFFFFFFF), d);
+    const int hi = __shfl_up((int)(v >> 32), d);
+    return ((int64_t)hi << 32) | (uint32_t)lo;
+}
+
+// f(integral_constant<int, u>) for u = 0 .. N-1, unrolled (so that arrays
+// indexed by u stay in registers).
+template <typename F, int... U>
+__device__ __forceinline__ void one_each_(F &f, std::integer_sequence<int, U...>)
+{
+    (f(std::integral_constant<int, U>{}), ...);
+}
+template <int N, typename F>
+__device__ __forceinline__ void one_each(F f)
+{
+    one_each_(f, std::make_integer_sequence<int, N>{});
+}
+
+// The lanes of `valid` whose owner bits equal (x0, x1, x2) (each all ones
+// or zero), for one 32-bit half of the masks.
+__device__ __forceinline__ uint32_t one_same(uint32_t valid, uint32_t b0, uint32_t b1, uint32_t b2, uint32_t x0,
+                                             uint32_t x1, uint32_t x2)
+{
+    return valid & ~((b0 ^ x0) | (b1 ^ x1) | (b2 ^ x2));
+}
+
+// The grid-wide barrier: true once all n workgroups have arrived.  The
+// launch sizes the grid to what the runtime reports resident at once, but
+// nothing forces the workgroups to be resident together (other work on the
+// GPU may hold compute units), so a workgroup that has polled kOneSpinLimit
+// times cancels the barrier instead: a compare-and-swap sets kOneCancel only
+// while the count is still short, every workgroup then sees the mark (late
+// arrivals in the value their increment returns) and returns false, the
+// kernel writes nothing, and the three-kernel path runs.  Either all
+// workgroups pass or none does.
+// What the workgroups publish before it (totals, first_bag) is written and
+// read with agent-scope atomics, which bypass the L2s (one per XCD) on both
+// sides, and the stores have completed (the workgroup barrier waits for them)
+// before the counter is incremented; agent-scope fences would write back or
+// invalidate whole L2s instead, which measured about 70 us per call.
+__device__ __forceinline__ bool one_grid_barrier(uint32_t *counter, uint32_t n, int32_t *ok)
+{
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        uint32_t v = __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) + 1u;
+        uint32_t spin = 0;
+        while (!(v & kOneCancel) && v < n) {
+            if (++spin > kOneSpinLimit) {
+                uint32_t seen = v;
+                if (__hip_atomic_compare_exchange_strong(counter, &seen, v | kOneCancel, __ATOMIC_RELAXED,
+                                                         __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {
+                    v |= kOneCancel;
+                    break;
+                }
+                v = seen; // moved on meanwhile: check it again
+                continue;
+            }
+            __builtin_amdgcn_s_sleep(2);
+            v = __hip_atomic_load(counter, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+        *ok = !(v & kOneCancel);
+    }
+    __syncthreads();
+    return *ok != 0;
+}
+
+template <typename T>
+__device__ __forceinline__ void one_store(T *p, T v) { __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); }
+
+template <typename T>
+__device__ __forceinline__ T one_load(const T *p) { return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); }
+
+__global__ void eb_one_clear(uint32_t *barrier, int32_t *done)
+{
+    if (threadIdx.x == 0) {
+        *barrier = 0;
+        *done = 0;
+    }
+}
+
+// The wave holding bag boundary p (0 <= p <= TB): the wave of table
+// min(p / B, T - 1) whose positions hold offsets[p] (a boundary at a wave's
+// end belongs to that wave).
+__device__ __forceinline__ int64_t one_wave_of(const OneArgs &a, const OneBlockLds &L, int64_t p, int64_t x)
+{
+    const int t = (int)min<int64_t>(p / max<int64_t>(a.B, 1), a.T - 1);
+    const int64_t lo = L.tstart[t], hi = max(lo, L.tstart[t + 1]);
+    const int64_t waves = L.wstart[t + 1] - L.wstart[t];
+    x = min(max(x, lo), hi) - lo;
+    return L.wstart[t] + min<int64_t>(x / a.C, waves - 1);
+}
+
+// few_owner_masks for ids and bounds that fit in 32 bits: the bounds of a
+// table whose outer pair lies in [INT32_MIN, INT32_MAX], the inner ones
+// clamped into that pair (which gives every id between them the masks the
+// 64-bit bounds give it).
+struct FewBounds32 {
+    int32_t lo, hi;
+    int32_t inner[kFewShards - 1];
+};
+
+__device__ __forceinline__ bool few_bounds_narrow(const FewBounds &b)
+{
+    return b.lo >= INT32_MIN && b.lo <= INT32_MAX && b.hi <= INT32_MAX;
+}
+
+__device__ __forceinline__ FewBounds32 few_bounds32(const FewBounds &b)
+{
+    FewBounds32 n;
+    n.lo = (int32_t)b.lo;
+    n.hi = (int32_t)max(b.lo, b.hi);
+#pragma unroll
+    for (int j = 0; j < kFewShards - 1; ++j) n.inner[j] = (int32_t)min(max(b.inner[j], b.lo), max(b.lo, b.hi));
+    return n;
+}
+
+__device__ __forceinline__ FewMasks few_owner_masks32(const FewBounds32 &b, int32_t i, uint64_t in)
+{
+    const uint64_t m0 = __ballot(i >= b.inner[0]), m1 = __ballot(i >= b.inner[1]), m2 = __ballot(i >= b.inner[2]),
+                   m3 = __ballot(i >= b.inner[3]), m4 = __ballot(i >= b.inner[4]), m5 = __ballot(i >= b.inner[5]),
+                   m6 = __ballot(i >= b.inner[6]);
+    FewMasks o;
+    o.valid = in & __ballot(i >= b.lo) & __ballot(i < b.hi);
+    o.b2 = m3;
+    o.b1 = (m3 & m5) | (~m3 & m1);
+    const uint64_t upper = (o.b1 & m6) | (~o.b1 & m4), lower = (o.b1 & m2) | (~o.b1 & m0);
+    o.b0 = (m3 & upper) | (~m3 & lower);
+    return o;
+}
+
+// A copy of x in a register of its own (a held id must not become half of a
+// 64-bit register pair, which would keep its neighbour from holding another).
+__device__ __forceinline__ uint32_t one_copy(uint32_t x)
+{
+    uint32_t y;
+    asm volatile("v_mov_b32 %0, %1" : "=v"(y) : "v"(x));
+    return y;
+}
+
+// Phase 1's record of chunk u: its masks, and the running counts before it
+// (lane g < 8 keeps destination g's in `run`).
+__device__ __forceinline__ void one_record(OneWaveLds &W, int u, int lane, const FewMasks &o, int32_t &run, uint32_t l0,
+                                           uint32_t l1, uint32_t l2)
+{
+    if (lane == 0) W.rec[u] = OneRec{o.valid, o.b0, o.b1, o.b2};
+    if (lane < kFewShards) W.cum[u][lane] = (uint16_t)run;
+    const uint32_t own_lo = one_same((uint32_t)o.valid, (uint32_t)o.b0, (uint32_t)o.b1, (uint32_t)o.b2, ~l0, ~l1, ~l2);
+    const uint32_t own_hi = one_same((uint32_t)(o.valid >> 32), (uint32_t)(o.b0 >> 32), (uint32_t)(o.b1 >> 32),
+                                     (uint32_t)(o.b2 >> 32), ~l0, ~l1, ~l2);
+    run += __popc(own_lo) + __popc(own_hi);
+}
+
+// Phase 3's step for chunk u, whose id this lane holds: its rank among the
+// chunk's ids for the same destination, the destination's slot from the lane
+// numbered by it (lane g < 8 holds slot + the running count for g), one store.
+template <typename IT>
+__device__ __forceinline__ void one_store_chunk(const OneArgs &a, const OneWaveLds &W, int lane, int64_t slot, int u,
+                                                int64_t id, IT *out)
+{
+    const OneRec r = W.rec[u];
+    const uint64_t valid = uniform_mask(r.valid);
+    const uint64_t b0 = uniform_mask(r.b0), b1 = uniform_mask(r.b1), b2 = uniform_mask(r.b2);
+    const uint32_t x0 = lane_bit(b0) ? ~0u : 0u, x1 = lane_bit(b1) ? ~0u : 0u, x2 = lane_bit(b2) ? ~0u : 0u;
+    const uint32_t same_lo = one_same((uint32_t)valid, (uint32_t)b0, (uint32_t)b1, (uint32_t)b2, x0, x1, x2);
+    const uint32_t same_hi = one_same((uint32_t)(valid >> 32), (uint32_t)(b0 >> 32), (uint32_t)(b1 >> 32),
+                                      (uint32_t)(b2 >> 32), x0, x1, x2);
+    const int rank = (int)__builtin_amdgcn_mbcnt_hi(same_hi, __builtin_amdgcn_mbcnt_lo(same_lo, 0u));
+    const int64_t mine = slot + (lane < kFewShards ? (int64_t)W.cum[u][lane] : 0);
+    const int from = few_bits<4>(FewMasks{valid, b0, b1, b2});
+    const int base_lo = __builtin_amdgcn_ds_bpermute(from, (int)(uint32_t)mine);
+    const int base_hi = __builtin_amdgcn_ds_bpermute(from, (int)(mine >> 32));
+    const int64_t pos = (((int64_t)base_hi << 32) | (uint32_t)base_lo) + rank;
+    if (lane_bit(valid) && (uint64_t)pos < (uint64_t)a.out_cap) out[pos] = (IT)id;
+}
+
+template <typename IT>
+__global__ __launch_bounds__(kOneBlock) __attribute__((amdgpu_waves_per_eu(4, 4))) void eb_bucket_onepass(const OneArgs a)
+{
+    extern __shared__ __align__(16) unsigned char one_lds_raw[];
+    OneBlockLds &L = *(OneBlockLds *)one_lds_raw;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = threadIdx.x / kWave;
+    const int lb = xcd_run_block(blockIdx.x, gridDim.x);
+    const int64_t v = (int64_t)lb * kOneWaves + wave;
+    const int64_t C = a.C;
+    const IT *off = (const IT *)a.offsets;
+
+    // Tables: start positions and first waves (wave 0; T <= kOneMaxTables).
+    if (wave == 0) {
+        int64_t carry = 0;
+        for (int t0 = 0; t0 <= a.T; t0 += kWave) {
+            const int t = t0 + lane;
+            int64_t s = 0, e = 0;
+            if (t <= a.T) s = min<int64_t>(max<int64_t>((int64_t)off[(int64_t)t * a.B], 0), a.nnz);
+            if (t < a.T) e = min<int64_t>(max<int64_t>((int64_t)off[(int64_t)(t + 1) * a.B], 0), a.nnz);
+            const int64_t len = e > s ? e - s : 0;
+            const int64_t waves = t < a.T ? (len <= C ? 1 : 1 + (len - 1) / C) : 0;
+            int64_t incl = waves; // inclusive scan over the lanes
+            for (int d = 1; d < kWave; d <<= 1) {
+                const int64_t y = shfl_up64(incl, d);
+                if (lane >= d) incl += y;
+            }
+            if (t <= a.T) {
+                L.tstart[t] = s;
+                L.wstart[t] = (int32_t)(carry + incl - waves);
+            }
+            carry += readlane64(incl, kWave - 1);
+        }
+    }
+    __syncthreads();
+    const int64_t used = L.wstart[a.T]; // waves that hold a table's positions
+
+    // This wave's table and positions [ps, ps + n).
+    int t = 0;
+    for (int t0 = 1; t0 < a.T; t0 += kWave) {
+        const int tt = t0 + lane;
+        t += __popcll(__ballot(tt < a.T && L.wstart[tt] <= v));
+    }
+    t = __builtin_amdgcn_readfirstlane(t);
+    int64_t ps = 0, n = 0;
+    if (v < used) {
+        const int64_t lo = L.tstart[t], hi = max(lo, L.tstart[t + 1]);
+        ps = min(lo + (v - L.wstart[t]) * C, hi);
+        n = min(hi - ps, C);
+    }
+    ps = uniform64(ps);
+    n = uniform64(n);
+    OneWaveLds &W = L.wave[wave];
+
+    // Which bags start in which wave's positions, for this wave's share of
+    // the boundaries 0 .. TB and a last, virtual one (TB + 1) past them all:
+    // first_bag[c] = the first p whose wave is c or later.  Offsets that
+    // decrease or leave [0, nnz] raise the flag.
+    bool disorder = false;
+    {
+        const int64_t nwaves = (int64_t)gridDim.x * kOneWaves;
+        const int64_t share = (a.TB + 2 + nwaves - 1) / nwaves;
+        const int64_t pend = min<int64_t>((v + 1) * share, a.TB + 2);
+        for (int64_t p = v * share + lane; p < pend; p += kWave) {
+            const int64_t xp = p <= a.TB ? (int64_t)off[p] : 0;
+            const int64_t xq = p >= 1 && p - 1 <= a.TB ? (int64_t)off[p - 1] : 0;
+            if ((p >= 1 && p <= a.TB && xq > xp) || (p == 0 && xp < 0) || (p == a.TB && xp > a.nnz)) disorder = true;
+            const int64_t c1 = p <= a.TB ? one_wave_of(a, L, p, xp) : used;
+            const int64_t c0 = p >= 1 ? one_wave_of(a, L, p - 1, xq) + 1 : 0;
+            // (c stays within the grid's waves even for offsets that are not
+            // ordinary, whose tables may claim more waves than there are)
+            for (int64_t c = max<int64_t>(c0, 0); c <= min(c1, min(used, nwaves)); ++c) one_store(a.first_bag + c, p);
+        }
+    }
+
+    // Phase 1: hold the ids, record every chunk's masks and running counts.
+    uint32_t held[kOneChunks];
+    int32_t run = 0; // lane g < 8: this wave's ids for destination g so far
+    const uint32_t l0 = (uint32_t)(lane & 1) - 1u, l1 = (uint32_t)((lane >> 1) & 1) - 1u,
+                   l2 = (uint32_t)((lane >> 2) & 1) - 1u;
+    const IT *src = (const IT *)a.indices + ps + lane;
+    FewBounds fb;
+    bool narrow = true;
+    {
+        const int64_t *bnd = a.bounds + (int64_t)t * (a.G + 1);
+        fb.lo = uniform64(bnd[0]);
+        fb.hi = uniform64(bnd[a.G]);
+#pragma unroll
+        for (int j = 1; j < kFewShards; ++j) fb.inner[j - 1] = j < a.G ? uniform64(bnd[j]) : INT64_MAX;
+        narrow = few_bounds_narrow(fb);
+    }
+    const int n32 = (int)n; // at most kOneChunks * 64
+    if (n > 0 && !narrow) {
+        for (int u = 0; u < a.K; ++u) {
+            const int64_t id = u * kWave + lane < n32 ? (int64_t)src[(int64_t)u * kWave] : 0;
+            one_record(W, u, lane, few_owner_masks(fb, id, lanes_below(n32 - u * kWave)), run, l0, l1, l2);
+        }
+    } else if (n > 0) {
+        const FewBounds32 f32 = few_bounds32(fb);
+        one_each<kOneChunks / kOneGroup>([&](auto G0) __attribute__((always_inline)) {
+            constexpr int g0 = decltype(G0)::value * kOneGroup;
+            if (g0 < a.K) {
+                IT raw[kOneGroup];
+#pragma unroll
+                for (int j = 0; j < kOneGroup; ++j) {
+                    const int u = g0 + j;
+                    raw[j] = u * kWave + lane < n32 ? __builtin_nontemporal_load(src + u * kWave) : (IT)0;
+                }
+#pragma unroll
+                for (int j = 0; j < kOneGroup; ++j) {
+                    const int u = g0 + j;
+                    const int32_t lo = (int32_t)raw[j];
+                    uint64_t in = lanes_below(n32 - u * kWave);
+                    if constexpr (sizeof(IT) == 8) in &= __ballot((int32_t)((int64_t)raw[j] >> 32) == (lo >> 31));
+                    held[u] = sizeof(IT) == 8 ? one_copy((uint32_t)lo) : (uint32_t)lo;
+                    one_record(W, u, lane, few_owner_masks32(f32, lo, in), run, l0, l1, l2);
+                    __builtin_amdgcn_sched_barrier(0); // one chunk at a time: registers hold the ids
+                }
+            }
+        });
+    }
+    // The record past the last chunk: no ids, the totals.
+    if (lane == 0) {
+        W.rec[a.K] = OneRec{0, 0, 0, 0};
+        L.wave_flag[wave] = __ballot(disorder) != 0;
+    }
+    if (lane < kFewShards) {
+        W.cum[a.K][lane] = (uint16_t)run;
+        L.wave_total[wave][lane] = run;
+    }
+    __syncthreads();
+    if (threadIdx.x < kOneTotals) {
+        int32_t x = 0;
+        if (threadIdx.x < kFewShards)
+            for (int w = 0; w < kOneWaves; ++w) x += L.wave_total[w][threadIdx.x];
+        else if (threadIdx.x == kFewShards)
+            for (int w = 0; w < kOneWaves; ++w) x |= L.wave_flag[w];
+        one_store(a.block_totals + (int64_t)lb * kOneTotals + threadIdx.x, x);
+    }
+    if (!one_grid_barrier(a.barrier, gridDim.x, &L.pass)) return; // cancelled: the other kernels write the outputs
+
+    // Phase 2: the workgroups' totals before this one and in all, and the
+    // offsets' flag: thread b reads workgroup b's (independent loads, past
+    // the L2s), each wave adds up its 64 workgroups, then the waves' sums.
+    {
+        const int nb = gridDim.x;
+        const int b = threadIdx.x; // kOneBlock >= workgroups in the grid
+        int32_t x[kFewShards + 1];
+#pragma unroll
+        for (int g = 0; g <= kFewShards; ++g)
+            x[g] = b < nb ? one_load(a.block_totals + (int64_t)b * kOneTotals + g) : 0;
+        int32_t before[kFewShards], all[kFewShards];
+#pragma unroll
+        for (int g = 0; g < kFewShards; ++g) {
+            before[g] = b < lb ? x[g] : 0;
+            all[g] = x[g];
+        }
+        const int32_t f = __ballot(x[kFewShards] != 0) != 0;
+        for (int m = kWave / 2; m >= 1; m >>= 1) {
+#pragma unroll
+            for (int g = 0; g < kFewShards; ++g) {
+                before[g] += __shfl_xor(before[g], m);
+                all[g] += __shfl_xor(all[g], m);
+            }
+        }
+        if (lane == 0) {
+#pragma unroll
+            for (int g = 0; g < kFewShards; ++g) {
+                L.part_before[wave][g] = before[g];
+                L.part_all[wave][g] = all[g];
+            }
+            L.part_flag[wave] = f;
+        }
+        __syncthreads();
+        if (threadIdx.x < kFewShards) {
+            int64_t bs = 0, as = 0;
+            for (int w = 0; w < kOneWaves; ++w) {
+                bs += L.part_before[w][threadIdx.x];
+                as += L.part_all[w][threadIdx.x];
+            }
+            L.block_base[threadIdx.x] = bs;
+            L.total[threadIdx.x] = as;
+        }
+        if (threadIdx.x == kFewShards) {
+            int32_t any = 0;
+            for (int w = 0; w < kOneWaves; ++w) any |= L.part_flag[w];
+            L.flag = any;
+        }
+    }
+    __syncthreads();
+    if (L.flag) return; // offsets not ordinary: the other kernels write the outputs
+    // From here on every workgroup writes its part; the other kernels see
+    // `done` and return at once.
+    if (lb == 0 && threadIdx.x <= a.G) {
+        int64_t s = 0;
+        for (int g = 0; g < (int)threadIdx.x; ++g) s += L.total[g];
+        a.segments[threadIdx.x] = s;
+        if (threadIdx.x == 0) *a.done = 1;
+    }
+    int64_t slot = 0; // lane g < G: where this wave's first id for g goes
+    if (lane < kFewShards) {
+        int64_t lbase = 0;
+        if (lane < a.G) {
+            lbase = L.block_base[lane];
+            for (int w = 0; w < wave; ++w) lbase += L.wave_total[w][lane];
+            int64_t seg = 0;
+            for (int g = 0; g < lane; ++g) seg += L.total[g];
+            slot = seg + lbase;
+        }
+        L.wave_base[wave][lane] = lbase;
+    }
+    wave_sync_lds(); // wave_base, read by every lane below
+
+    // Phase 3: the ids, from registers (reloaded when the table's bounds do
+    // not fit in 32 bits: a separate loop, so that no store waits for a load).
+    IT *out = (IT *)a.out_indices;
+    if (n > 0 && !narrow) {
+        for (int u = 0; u < a.K; ++u)
+            one_store_chunk<IT>(a, W, lane, slot, u, u * kWave + lane < n32 ? (int64_t)src[(int64_t)u * kWave] : 0, out);
+    } else if (n > 0) {
+        one_each<kOneChunks / kOneStoreGroup>([&](auto G0) __attribute__((always_inline)) {
+            constexpr int g0 = decltype(G0)::value * kOneStoreGroup;
+            if (g0 < a.K) {
+#pragma unroll
+                for (int j = 0; j < kOneStoreGroup; ++j) {
+                    const int u = g0 + j;
+                    const uint32_t h = sizeof(IT) == 8 ? one_copy(held[u]) : held[u];
+                    one_store_chunk<IT>(a, W, lane, slot, u, (int64_t)(int32_t)h, out);
+                    __builtin_amdgcn_sched_barrier(0);
+                }
+            }
+        });
+    }
+
+    // out_offsets for the bags that start in this wave's positions.
+    if (v < used) {
+        const int64_t pb0 = max<int64_t>(0, one_load(a.first_bag + v));
+        const int64_t pb1 = min<int64_t>(a.TB + 1, one_load(a.first_bag + v + 1));
+        int64_t wb[kFewShards];
+#pragma unroll
+        for (int g = 0; g < kFewShards; ++g) wb[g] = L.wave_base[wave][g];
+        const int64_t row = a.TB + 1;
+        for (int64_t p = pb0 + lane; p < pb1; p += kWave) {
+            // A boundary at the end of the wave's ids takes the totals'
+            // record (so that a wave without ids reads only that one).
+            const int64_t x = max<int64_t>(0, min<int64_t>((int64_t)off[p] - ps, n));
+            const int u = x >= n ? a.K : (int)(x >> 6), rr = x >= n ? 0 : (int)(x & 63);
+            const OneRec r = W.rec[u];
+            const uint64_t below = rr == 0 ? 0ull : (~0ull >> (64 - rr));
+            const uint64_t v0 = r.valid & below;
+#pragma unroll
+            for (int g = 0; g < kFewShards; ++g) {
+                if (g < a.G) {
+                    const uint64_t leaf = v0 & ((g & 1) ? r.b0 : ~r.b0) & ((g & 2) ? r.b1 : ~r.b1) &
+                                          ((g & 4) ? r.b2 : ~r.b2);
+                    a.out_offsets[(int64_t)g * row + p] = wb[g] + W.cum[u][g] + __popcll(leaf);
+                }
+            }
+        }
+    }
+}
+
 
 // Bags per count wave for T*B bags in all and G destinations (see
 // kCountWavesMin).  Only the compare-tree paths (G <= 16, 8 or 16 histogram
@@ -1509,6 +2061,75 @@ const void *scatter_kernel(int G)
                               : (const void *)eb_bucket_scatter<IT, kMaxShards>;
 }
 
+// The one-pass kernel's workgroups: kOneBlocksPerCu per compute unit when
+// the runtime reports that many resident and phase 2's one thread per
+// workgroup suffices, else 0 (the path is not taken).
+int one_pass_blocks()
+{
+    static std::atomic<int> cached{-1};
+    int b = cached.load(std::memory_order_acquire);
+    if (b >= 0) return b;
+    int dev = 0, cus = 0, per64 = 0, per32 = 0;
+    b = 0;
+    if (hipGetDevice(&dev) == hipSuccess &&
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per64, (const void *)eb_bucket_onepass<int64_t>, kOneBlock,
+                                                     sizeof(OneBlockLds)) == hipSuccess &&
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per32, (const void *)eb_bucket_onepass<int32_t>, kOneBlock,
+                                                     sizeof(OneBlockLds)) == hipSuccess &&
+        std::min(per64, per32) >= kOneBlocksPerCu && cus * kOneBlocksPerCu <= kOneBlock)
+        b = cus * kOneBlocksPerCu;
+    cached.store(b, std::memory_order_release);
+    return b;
+}
+
+// Chunks per wave so that every table's positions fit in `waves` waves, at
+// least one per table: T + nnz / C waves at most.
+int64_t one_pass_chunks(int64_t nnz, int64_t waves, int32_t T)
+{
+    const int64_t spare = waves - T;
+    return spare > 0 ? std::max<int64_t>(1, (nnz + spare * kWave - 1) / (spare * kWave)) : kOneChunks + 1;
+}
+
+// The one-pass kernel's workspace: the barrier counter and `done`, the
+// workgroups' totals, first_bag.  It follows the other kernels' workspace, so
+// that those never write over `done` before reading it.
+constexpr size_t kOnePassWorkspace =
+    (256 + (size_t)kOneBlock * kOneTotals * 4 + ((size_t)kOneBlock * kOneWaves + 1) * 8 + 255) / 256 * 256;
+
+// Batches below this many ids keep the three kernels: on workload 3's tables
+// (8 destinations), first B bags of each, the one-pass path took 47.6 against
+// 32.8 us at B = 2048 (2.6 M ids) and 73.3 against 77.8 us at B = 8192
+// (10.5 M ids); its launches and barrier cost the same at any size.
+constexpr int64_t kOneMinIds = (int64_t)1 << 23;
+
+// EB_BUCKETIZE_ONE_PASS=0 never takes the one-pass kernel, =1 takes it for
+// every batch it can hold (the tests run both ways); unset, batches of at
+// least kOneMinIds ids take it.  Read on every call.
+int one_pass_setting()
+{
+    const char *e = std::getenv("EB_BUCKETIZE_ONE_PASS");
+    return e && e[0] == '0' ? 0 : e && e[0] == '1' ? 1 : -1;
+}
+
+bool one_pass_fits(int32_t T, int32_t G, int64_t nnz, hipStream_t st)
+{
+    const int setting = one_pass_setting();
+    if (setting == 0 || G > kFewShards || T < 1 || T > kOneMaxTables || nnz < 1) return false;
+    if (setting < 0 && nnz < kOneMinIds) return false;
+    const int blocks = one_pass_blocks();
+    if (blocks <= 0) return false;
+    if (one_pass_chunks(nnz, (int64_t)blocks * kOneWaves, T) > kOneChunks) return false;
+    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing(st, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone) return false;
+    return true;
+}
+
+size_t classic_workspace_bytes(int32_t T, int64_t B, int32_t G)
+{
+    return ((size_t)workspace_entries(T, B, G) * sizeof(int64_t) + 255) / 256 * 256;
+}
+
 } // namespace
 
 namespace {
@@ -1521,7 +2142,7 @@ int bucketize_workspace_impl(int32_t T, int64_t B, int32_t G, size_t *bytes)
     if (G > kMaxShards) return fail(EB_ERR_UNSUPPORTED, "eb_bucketize_workspace: more than 1024 shards");
     if (T > 0 && B > std::numeric_limits<int64_t>::max() / T / G / 8)
         return fail(EB_ERR_INVALID, "eb_bucketize_workspace: sizes overflow");
-    *bytes = (size_t)workspace_entries(T, B, G) * sizeof(int64_t);
+    *bytes = classic_workspace_bytes(T, B, G) + kOnePassWorkspace;
     return EB_OK;
 }
 
@@ -1573,6 +2194,7 @@ int bucketize_impl(int32_t T, int64_t B, int32_t G, const int64_t *bounds, int32
     // Workspace: tile sums [G][ntiles], starts [G][nq], wave totals [nparts][G],
     // row totals [G].
     ScanArgs sa;
+    std::memset(&sa, 0, sizeof sa);
     sa.rows = out_offsets;
     sa.tile_sums = (int64_t *)workspace;
     sa.nq = start_entries(TB);
@@ -1605,6 +2227,43 @@ int bucketize_impl(int32_t T, int64_t B, int32_t G, const int64_t *bounds, int32
     sa.bags_per_wave = cbags;
     sa.mode = direct_scan(G, sa.ntiles, sa.nparts) ? kScanDirect : fused_scan(G, sa.ntiles) ? kScanFused : kScanRows;
 
+    // Ordinary offsets and up to 8 destinations: the one-pass kernel, with
+    // the three kernels launched behind it, which return at once when it
+    // has written the outputs (`done`) and do the work when it could not
+    // (offsets not ordinary, a cancelled barrier).
+    if (TB > 0 && one_pass_fits(T, G, nnz, st)) {
+        OneArgs oa;
+        std::memset(&oa, 0, sizeof oa);
+        const int blocks = one_pass_blocks();
+        oa.bounds = bounds;
+        oa.indices = indices;
+        oa.offsets = offsets;
+        oa.out_offsets = out_offsets;
+        oa.out_indices = out_indices;
+        oa.segments = segments;
+        oa.out_cap = out_capacity;
+        oa.nnz = nnz;
+        oa.B = B;
+        oa.TB = TB;
+        oa.T = T;
+        oa.G = G;
+        oa.K = (int32_t)one_pass_chunks(nnz, (int64_t)blocks * kOneWaves, T);
+        oa.C = (int64_t)oa.K * kWave;
+        unsigned char *w = (unsigned char *)workspace + classic_workspace_bytes(T, B, G);
+        oa.barrier = (uint32_t *)w;
+        oa.done = (int32_t *)(w + 4);
+        oa.block_totals = (int32_t *)(w + 256);
+        oa.first_bag = (int64_t *)(w + 256 + (size_t)kOneBlock * kOneTotals * 4);
+        void *cargs[] = {&oa.barrier, &oa.done};
+        hipError_t err = hipLaunchKernel((const void *)eb_one_clear, dim3(1), dim3(kWave), cargs, 0, st);
+        void *oargs[] = {&oa};
+        if (err == hipSuccess)
+            err = hipLaunchKernel(i32 ? (const void *)eb_bucket_onepass<int32_t> : (const void *)eb_bucket_onepass<int64_t>,
+                                  dim3(blocks), dim3(kOneBlock), oargs, sizeof(OneBlockLds), st);
+        if (err != hipSuccess) return fail(EB_ERR_HIP, "eb_bucketize: %s", hipGetErrorString(err));
+        ba.skip = oa.done;
+        sa.skip = oa.done;
+    }
     if (TB > 0) {
         void *args[] = {&ba};
         const void *count = i32 ? count_kernel<int32_t>(G, cbags) : count_kernel<int64_t>(G, cbags);

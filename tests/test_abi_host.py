@@ -218,10 +218,19 @@ def test_bucketize_workspace_sizes():
     # per destination: one sum per scan tile (2048 bags of a table, or whole
     # tables when B < 2048), every 16th offset, one total per count wave
     # (64 bags for workload 3 into 8 blocks, else 16) and the row's total
-    assert eb.eb_bucketize_workspace(26, 16384, 8) == 8 * (26 * 8 + 26 * 16384 // 16 + 1 + 26 * 16384 // 64 + 1) * 8
-    assert eb.eb_bucketize_workspace(3, 7, 2) == 2 * (1 + 21 // 16 + 1 + 3 + 1) * 8
-    assert eb.eb_bucketize_workspace(5, 3000, 100) == 100 * (5 * 2 + 15000 // 16 + 1 + 5 * 188 + 1) * 8
-    assert eb.eb_bucketize_workspace(0, 0, 1) == 24
+    # the three kernels' part, rounded up to 256 bytes, then the one-pass
+    # kernel's fixed part (barrier word, 512 workgroups' totals, 4097 wave
+    # entries)
+    one_pass = (256 + 512 * 16 * 4 + 4097 * 8 + 255) // 256 * 256
+    assert one_pass == 66048
+
+    def ws(entries):
+        return (entries * 8 + 255) // 256 * 256 + one_pass
+
+    assert eb.eb_bucketize_workspace(26, 16384, 8) == ws(8 * (26 * 8 + 26 * 16384 // 16 + 1 + 26 * 16384 // 64 + 1))
+    assert eb.eb_bucketize_workspace(3, 7, 2) == ws(2 * (1 + 21 // 16 + 1 + 3 + 1))
+    assert eb.eb_bucketize_workspace(5, 3000, 100) == ws(100 * (5 * 2 + 15000 // 16 + 1 + 5 * 188 + 1))
+    assert eb.eb_bucketize_workspace(0, 0, 1) == ws(3)
     assert code_of(lambda: eb.eb_bucketize_workspace(1, 1, 0)) == eb.EB_ERR_INVALID
     assert code_of(lambda: eb.eb_bucketize_workspace(-1, 1, 2)) == eb.EB_ERR_INVALID
     assert code_of(lambda: eb.eb_bucketize_workspace(1, 1, 1025)) == eb.EB_ERR_UNSUPPORTED

@@ -13,6 +13,14 @@ from paper_2512_05831_amd import eb, workloads as wl
 pytestmark = pytest.mark.gpu
 
 
+@pytest.fixture(params=["three-kernel", "one-pass"], autouse=True)
+def bucketize_path(request, monkeypatch):
+    """Every test runs twice: with eb_bucketize's three kernels, and with its
+    one-pass kernel wherever that applies (at most 8 destinations; outside a
+    graph capture), whatever the batch's size."""
+    monkeypatch.setenv("EB_BUCKETIZE_ONE_PASS", "0" if request.param == "three-kernel" else "1")
+
+
 def batch(seed, T, B, G, rows=1_000_000):
     g = np.random.default_rng(seed)
     L = np.where(g.random(T * B) < 0.05, 0, g.integers(1, 60, T * B))
