@@ -1473,17 +1473,14 @@ __global__ __launch_bounds__(kBlock) void eb_sum_partials_scalar(const PartialAr
 constexpr int kOneWaves = 8;                        // waves per workgroup
 constexpr int kOneBlock = kOneWaves * kWave;        // threads per workgroup
 constexpr int kOneBlocksPerCu = 2;                  // 16 waves per compute unit
-constexpr int kOneChunks = 88;                      // 64-id chunks a wave holds, at most
+constexpr int kOneChunks = 84;                      // 64-id chunks a wave holds, at most (128 VGPRs)
+constexpr int kOneChunksSmall = 48;                 // the kernel walking fewer, for smaller batches
 constexpr int kOneGroup = 8;                        // chunks loaded together
-#ifndef ONE_SG
-#define ONE_SG 2
-#endif
-constexpr int kOneStoreGroup = ONE_SG;                   // chunks stored together
+constexpr int kOneStoreGroup = 2;                   // chunks stored together (phase 3)
 constexpr int kOneMaxTables = 1024;
 constexpr int kOneTotals = 16;                      // int32 per workgroup: 8 totals, flag
 constexpr uint32_t kOneSpinLimit = 1u << 16;        // barrier polls (about 30-60 ms) before cancelling
 constexpr uint32_t kOneCancel = 0x80000000u;        // the barrier counter's cancelled mark
-static_assert(kOneChunks % kOneGroup == 0, "chunk groups");
 
 struct OneArgs {
     const int64_t *bounds;  // [T][G+1]
@@ -1719,9 +1716,29 @@ __device__ __forceinline__ void one_store_chunk(const OneArgs &a, const OneWaveL
     if (lane_bit(valid) && (uint64_t)pos < (uint64_t)a.out_cap) out[pos] = (IT)id;
 }
 
+// A buffer resource over n bytes from p: loads past n return 0 without
+// touching memory, so every lane may load and no branch skips a load.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t one_rsrc(const void *p, int n)
+{
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), (short)0, n, 0x00020000);
+}
+
 template <typename IT>
+__device__ __forceinline__ IT one_buffer_load(__amdgpu_buffer_rsrc_t r, int byte_offset)
+{
+    if constexpr (sizeof(IT) == 8) {
+        const uint2 v = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(r, byte_offset, 0, 2));
+        return (IT)(((uint64_t)v.y << 32) | v.x);
+    } else {
+        return (IT)__builtin_amdgcn_raw_buffer_load_b32(r, byte_offset, 0, 2);
+    }
+}
+
+// kChunks: the chunks phase 1 walks (K of them hold ids); 48 or kOneChunks.
+template <typename IT, int kChunks>
 __global__ __launch_bounds__(kOneBlock) __attribute__((amdgpu_waves_per_eu(4, 4))) void eb_bucket_onepass(const OneArgs a)
 {
+    static_assert(kChunks % kOneStoreGroup == 0 && kChunks <= kOneChunks, "chunks");
     extern __shared__ __align__(16) unsigned char one_lds_raw[];
     OneBlockLds &L = *(OneBlockLds *)one_lds_raw;
     const int lane = threadIdx.x & (kWave - 1);
@@ -1795,7 +1812,7 @@ __global__ __launch_bounds__(kOneBlock) __attribute__((amdgpu_waves_per_eu(4, 4)
     }
 
     // Phase 1: hold the ids, record every chunk's masks and running counts.
-    uint32_t held[kOneChunks];
+    uint32_t held[kChunks];
     int32_t run = 0; // lane g < 8: this wave's ids for destination g so far
     const uint32_t l0 = (uint32_t)(lane & 1) - 1u, l1 = (uint32_t)((lane >> 1) & 1) - 1u,
                    l2 = (uint32_t)((lane >> 2) & 1) - 1u;
@@ -1817,27 +1834,26 @@ __global__ __launch_bounds__(kOneBlock) __attribute__((amdgpu_waves_per_eu(4, 4)
             one_record(W, u, lane, few_owner_masks(fb, id, lanes_below(n32 - u * kWave)), run, l0, l1, l2);
         }
     } else if (n > 0) {
+        // A rolling pipeline over all kChunks chunks, straight-line code:
+        // chunk u's register, once processed, loads chunk u + kOneGroup, so
+        // that kOneGroup loads stay in flight while the wave works and each
+        // wait covers only the oldest.  Chunks past the wave's ids load 0
+        // (the buffer's size) and record no ids.
         const FewBounds32 f32 = few_bounds32(fb);
-        one_each<kOneChunks / kOneGroup>([&](auto G0) __attribute__((always_inline)) {
-            constexpr int g0 = decltype(G0)::value * kOneGroup;
-            if (g0 < a.K) {
-                IT raw[kOneGroup];
+        const __amdgpu_buffer_rsrc_t rs = one_rsrc((const IT *)a.indices + ps, n32 * (int)sizeof(IT));
+        IT raw[kOneGroup];
 #pragma unroll
-                for (int j = 0; j < kOneGroup; ++j) {
-                    const int u = g0 + j;
-                    raw[j] = u * kWave + lane < n32 ? __builtin_nontemporal_load(src + u * kWave) : (IT)0;
-                }
-#pragma unroll
-                for (int j = 0; j < kOneGroup; ++j) {
-                    const int u = g0 + j;
-                    const int32_t lo = (int32_t)raw[j];
-                    uint64_t in = lanes_below(n32 - u * kWave);
-                    if constexpr (sizeof(IT) == 8) in &= __ballot((int32_t)((int64_t)raw[j] >> 32) == (lo >> 31));
-                    held[u] = sizeof(IT) == 8 ? one_copy((uint32_t)lo) : (uint32_t)lo;
-                    one_record(W, u, lane, few_owner_masks32(f32, lo, in), run, l0, l1, l2);
-                    __builtin_amdgcn_sched_barrier(0); // one chunk at a time: registers hold the ids
-                }
-            }
+        for (int j = 0; j < kOneGroup; ++j) raw[j] = one_buffer_load<IT>(rs, (j * kWave + lane) * (int)sizeof(IT));
+        one_each<kChunks>([&](auto U) __attribute__((always_inline)) {
+            constexpr int u = decltype(U)::value, j = u % kOneGroup;
+            const int32_t lo = (int32_t)raw[j];
+            uint64_t in = lanes_below(n32 - u * kWave);
+            if constexpr (sizeof(IT) == 8) in &= __ballot((int32_t)((int64_t)raw[j] >> 32) == (lo >> 31));
+            held[u] = sizeof(IT) == 8 ? one_copy((uint32_t)lo) : (uint32_t)lo;
+            one_record(W, u, lane, few_owner_masks32(f32, lo, in), run, l0, l1, l2);
+            if constexpr (u + kOneGroup < kChunks)
+                raw[j] = one_buffer_load<IT>(rs, ((u + kOneGroup) * kWave + lane) * (int)sizeof(IT));
+            __builtin_amdgcn_sched_barrier(0); // one chunk at a time: registers hold the ids
         });
     }
     // The record past the last chunk: no ids, the totals.
@@ -1939,7 +1955,7 @@ __global__ __launch_bounds__(kOneBlock) __attribute__((amdgpu_waves_per_eu(4, 4)
         for (int u = 0; u < a.K; ++u)
             one_store_chunk<IT>(a, W, lane, slot, u, u * kWave + lane < n32 ? (int64_t)src[(int64_t)u * kWave] : 0, out);
     } else if (n > 0) {
-        one_each<kOneChunks / kOneStoreGroup>([&](auto G0) __attribute__((always_inline)) {
+        one_each<kChunks / kOneStoreGroup>([&](auto G0) __attribute__((always_inline)) {
             constexpr int g0 = decltype(G0)::value * kOneStoreGroup;
             if (g0 < a.K) {
 #pragma unroll
@@ -2061,6 +2077,17 @@ const void *scatter_kernel(int G)
                               : (const void *)eb_bucket_scatter<IT, kMaxShards>;
 }
 
+template <typename IT, int kChunks>
+const void *one_pass_kernel() { return (const void *)eb_bucket_onepass<IT, kChunks>; }
+
+template <typename IT, int kChunks>
+int one_pass_occupancy()
+{
+    int per = 0;
+    return hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, one_pass_kernel<IT, kChunks>(), kOneBlock,
+                                                        sizeof(OneBlockLds)) == hipSuccess ? per : 0;
+}
+
 // The one-pass kernel's workgroups: kOneBlocksPerCu per compute unit when
 // the runtime reports that many resident and phase 2's one thread per
 // workgroup suffices, else 0 (the path is not taken).
@@ -2069,15 +2096,14 @@ int one_pass_blocks()
     static std::atomic<int> cached{-1};
     int b = cached.load(std::memory_order_acquire);
     if (b >= 0) return b;
-    int dev = 0, cus = 0, per64 = 0, per32 = 0;
+    int dev = 0, cus = 0;
     b = 0;
     if (hipGetDevice(&dev) == hipSuccess &&
         hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
-        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per64, (const void *)eb_bucket_onepass<int64_t>, kOneBlock,
-                                                     sizeof(OneBlockLds)) == hipSuccess &&
-        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per32, (const void *)eb_bucket_onepass<int32_t>, kOneBlock,
-                                                     sizeof(OneBlockLds)) == hipSuccess &&
-        std::min(per64, per32) >= kOneBlocksPerCu && cus * kOneBlocksPerCu <= kOneBlock)
+        std::min({one_pass_occupancy<int64_t, kOneChunksSmall>(), one_pass_occupancy<int64_t, kOneChunks>(),
+                  one_pass_occupancy<int32_t, kOneChunksSmall>(), one_pass_occupancy<int32_t, kOneChunks>()}) >=
+            kOneBlocksPerCu &&
+        cus * kOneBlocksPerCu <= kOneBlock)
         b = cus * kOneBlocksPerCu;
     cached.store(b, std::memory_order_release);
     return b;
@@ -2258,7 +2284,9 @@ int bucketize_impl(int32_t T, int64_t B, int32_t G, const int64_t *bounds, int32
         hipError_t err = hipLaunchKernel((const void *)eb_one_clear, dim3(1), dim3(kWave), cargs, 0, st);
         void *oargs[] = {&oa};
         if (err == hipSuccess)
-            err = hipLaunchKernel(i32 ? (const void *)eb_bucket_onepass<int32_t> : (const void *)eb_bucket_onepass<int64_t>,
+            err = hipLaunchKernel(oa.K <= kOneChunksSmall
+                                      ? (i32 ? one_pass_kernel<int32_t, kOneChunksSmall>() : one_pass_kernel<int64_t, kOneChunksSmall>())
+                                      : (i32 ? one_pass_kernel<int32_t, kOneChunks>() : one_pass_kernel<int64_t, kOneChunks>()),
                                   dim3(blocks), dim3(kOneBlock), oargs, sizeof(OneBlockLds), st);
         if (err != hipSuccess) return fail(EB_ERR_HIP, "eb_bucketize: %s", hipGetErrorString(err));
         ba.skip = oa.done;
