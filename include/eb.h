@@ -236,7 +236,7 @@ int eb_forward_ex(const eb_tables *tables, int32_t T, const int64_t *rows, int32
  * eb_bucketize_workspace -- device workspace, in bytes, that eb_bucketize
  * needs for T tables, B bags per table and G destinations (at least 1, at
  * most 1024): the three-kernel path's share, rounded up to 256 bytes, and a
- * fixed 66,048 bytes for the one-pass kernel (below).  Returns
+ * fixed 51,456 bytes for the one-pass kernel (below).  Returns
  * EB_ERR_INVALID for NULL bytes or bad sizes, EB_ERR_UNSUPPORTED for G >
  * 1024.  Touches no device state.
  */

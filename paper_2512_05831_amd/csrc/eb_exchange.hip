@@ -1478,7 +1478,8 @@ constexpr int kOneChunksSmall = 48;                 // the kernel walking fewer,
 constexpr int kOneGroup = 8;                        // chunks loaded together
 constexpr int kOneStoreGroup = 2;                   // chunks stored together (phase 3)
 constexpr int kOneMaxTables = 1024;
-constexpr int kOneTotals = 16;                      // int32 per workgroup: 8 totals, flag
+constexpr int kOneGoStride = 32;                    // int32: one 128-byte line per XCD's release word
+constexpr size_t kOneHeader = 2048;                 // workspace bytes before the workgroups' totals
 constexpr uint32_t kOneSpinLimit = 1u << 16;        // barrier polls (about 30-60 ms) before cancelling
 constexpr uint32_t kOneCancel = 0x80000000u;        // the barrier counter's cancelled mark
 
@@ -1490,9 +1491,11 @@ struct OneArgs {
     void *out_indices;      // IT [out_cap]
     int64_t *segments;      // [G+1]
     int64_t *first_bag;     // [waves+1] (workspace): the first bag that starts at or past wave c's positions
-    int32_t *block_totals;  // [gridDim.x][kOneTotals] (workspace)
-    uint32_t *barrier;      // zero at launch (workspace)
-    int32_t *done;          // (workspace): 1 once the outputs are written
+    int32_t *block_totals;  // [gridDim.x][8] (workspace): each workgroup's ids per destination
+    uint32_t *barrier;      // (workspace, zero at launch): workgroups arrived, or kOneCancel
+    int32_t *done;          // (workspace, zero at launch): 1 once the outputs are written
+    int32_t *disorder;      // (workspace, zero at launch): nonzero when the offsets are not ordinary
+    int32_t *go;            // (workspace, zero at launch): [kXcds][kOneGoStride]: 1 pass, 2 cancelled
     int64_t out_cap;
     int64_t nnz;
     int64_t B;
@@ -1522,7 +1525,6 @@ struct OneBlockLds {
     int32_t wave_flag[kOneWaves];
     int32_t part_before[kOneWaves][kFewShards]; // phase 2: each wave's sums
     int32_t part_all[kOneWaves][kFewShards];
-    int32_t part_flag[kOneWaves];
     int32_t pass;                      // the grid barrier's outcome
     int64_t block_base[kFewShards];    // ids for g in earlier workgroups
     int64_t total[kFewShards];         // ids for g in all
@@ -1568,40 +1570,57 @@ __device__ __forceinline__ uint32_t one_same(uint32_t valid, uint32_t b0, uint32
 }
 
 // The grid-wide barrier: true once all n workgroups have arrived.  The
-// launch sizes the grid to what the runtime reports resident at once, but
-// nothing forces the workgroups to be resident together (other work on the
-// GPU may hold compute units), so a workgroup that has polled kOneSpinLimit
-// times cancels the barrier instead: a compare-and-swap sets kOneCancel only
-// while the count is still short, every workgroup then sees the mark (late
-// arrivals in the value their increment returns) and returns false, the
-// kernel writes nothing, and the three-kernel path runs.  Either all
-// workgroups pass or none does.
-// What the workgroups publish before it (totals, first_bag) is written and
-// read with agent-scope atomics, which bypass the L2s (one per XCD) on both
-// sides, and the stores have completed (the workgroup barrier waits for them)
-// before the counter is incremented; agent-scope fences would write back or
-// invalidate whole L2s instead, which measured about 70 us per call.
-__device__ __forceinline__ bool one_grid_barrier(uint32_t *counter, uint32_t n, int32_t *ok)
+// workgroup whose increment completes the count sets every XCD's release
+// word (one 128-byte line each, so that each XCD's workgroups poll their own
+// line); the others poll theirs.  The launch sizes the grid to what the
+// runtime reports resident at once, but nothing forces the workgroups to be
+// resident together (other work on the GPU may hold compute units), so a
+// workgroup that has polled kOneSpinLimit times cancels the barrier instead:
+// a compare-and-swap sets kOneCancel on the count only while it is still
+// short, and the release words then say cancelled; late arrivals see the
+// mark in the value their increment returns.  Either all workgroups pass or
+// none does, and then the kernel writes nothing and the three-kernel path
+// runs.
+// What the workgroups publish before it (totals, first_bag, the disorder
+// flag) is written and read with agent-scope atomics or loads that bypass
+// the L2s (one per XCD) on both sides, and the stores have completed (the
+// workgroup barrier waits for them) before the count is incremented;
+// agent-scope fences would write back or invalidate whole L2s instead, which
+// measured about 70 us per call.
+__device__ __forceinline__ bool one_grid_barrier(const OneArgs &a, uint32_t n, int32_t *ok)
 {
     __syncthreads();
     if (threadIdx.x == 0) {
-        uint32_t v = __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) + 1u;
-        uint32_t spin = 0;
-        while (!(v & kOneCancel) && v < n) {
-            if (++spin > kOneSpinLimit) {
-                uint32_t seen = v;
-                if (__hip_atomic_compare_exchange_strong(counter, &seen, v | kOneCancel, __ATOMIC_RELAXED,
-                                                         __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {
-                    v |= kOneCancel;
-                    break;
+        const uint32_t v = __hip_atomic_fetch_add(a.barrier, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) + 1u;
+        int32_t r = 0;
+        if (v & kOneCancel) {
+            r = 2;
+        } else if (v == n) {
+            for (int x = 0; x < kXcds; ++x)
+                __hip_atomic_store(a.go + x * kOneGoStride, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            r = 1;
+        } else {
+            const int32_t *mine = a.go + (blockIdx.x % kXcds) * kOneGoStride;
+            for (uint32_t spin = 0;; ++spin) {
+                r = __hip_atomic_load(mine, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                if (r) break;
+                if (spin > kOneSpinLimit) {
+                    uint32_t seen = __hip_atomic_load(a.barrier, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    if (!(seen & kOneCancel) && seen < n &&
+                        __hip_atomic_compare_exchange_strong(a.barrier, &seen, seen | kOneCancel, __ATOMIC_RELAXED,
+                                                             __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {
+                        for (int x = 0; x < kXcds; ++x)
+                            __hip_atomic_store(a.go + x * kOneGoStride, 2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                        r = 2;
+                        break;
+                    }
+                    // else complete or cancelled meanwhile (its release word
+                    // follows), or one more arrival: try again at the next poll
                 }
-                v = seen; // moved on meanwhile: check it again
-                continue;
+                __builtin_amdgcn_s_sleep(2);
             }
-            __builtin_amdgcn_s_sleep(2);
-            v = __hip_atomic_load(counter, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
-        *ok = !(v & kOneCancel);
+        *ok = r == 1;
     }
     __syncthreads();
     return *ok != 0;
@@ -1613,12 +1632,16 @@ __device__ __forceinline__ void one_store(T *p, T v) { __hip_atomic_store(p, v, 
 template <typename T>
 __device__ __forceinline__ T one_load(const T *p) { return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); }
 
-__global__ void eb_one_clear(uint32_t *barrier, int32_t *done)
+// Zeroes the one-pass kernel's barrier count, `done`, the disorder flag and
+// the release words (kernel stores: a memset node in a graph is avoided).
+__global__ void eb_one_clear(OneArgs a)
 {
     if (threadIdx.x == 0) {
-        *barrier = 0;
-        *done = 0;
+        *a.barrier = 0;
+        *a.done = 0;
+        *a.disorder = 0;
     }
+    if (threadIdx.x < kXcds) a.go[threadIdx.x * kOneGoStride] = 0;
 }
 
 // The wave holding bag boundary p (0 <= p <= TB): the wave of table
@@ -1866,33 +1889,41 @@ __global__ __launch_bounds__(kOneBlock) __attribute__((amdgpu_waves_per_eu(4, 4)
         L.wave_total[wave][lane] = run;
     }
     __syncthreads();
-    if (threadIdx.x < kOneTotals) {
+    if (threadIdx.x < kFewShards) {
         int32_t x = 0;
-        if (threadIdx.x < kFewShards)
-            for (int w = 0; w < kOneWaves; ++w) x += L.wave_total[w][threadIdx.x];
-        else if (threadIdx.x == kFewShards)
-            for (int w = 0; w < kOneWaves; ++w) x |= L.wave_flag[w];
-        one_store(a.block_totals + (int64_t)lb * kOneTotals + threadIdx.x, x);
+        for (int w = 0; w < kOneWaves; ++w) x += L.wave_total[w][threadIdx.x];
+        one_store(a.block_totals + (int64_t)lb * kFewShards + threadIdx.x, x);
+    } else if (threadIdx.x == kFewShards) {
+        int32_t f = 0;
+        for (int w = 0; w < kOneWaves; ++w) f |= L.wave_flag[w];
+        if (f) __hip_atomic_fetch_or(a.disorder, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
-    if (!one_grid_barrier(a.barrier, gridDim.x, &L.pass)) return; // cancelled: the other kernels write the outputs
+    if (!one_grid_barrier(a, gridDim.x, &L.pass)) return; // cancelled: the other kernels write the outputs
 
     // Phase 2: the workgroups' totals before this one and in all, and the
-    // offsets' flag: thread b reads workgroup b's (independent loads, past
-    // the L2s), each wave adds up its 64 workgroups, then the waves' sums.
+    // offsets' flag: thread b reads workgroup b's 32-byte record (two loads
+    // past the L2s), each wave adds up its 64 workgroups, then the waves' sums.
     {
         const int nb = gridDim.x;
         const int b = threadIdx.x; // kOneBlock >= workgroups in the grid
-        int32_t x[kFewShards + 1];
+        int32_t x[kFewShards];
+        if (b < nb) {
+            typedef int v4i __attribute__((ext_vector_type(4)));
+            const __amdgpu_buffer_rsrc_t rt = one_rsrc(a.block_totals, nb * kFewShards * 4);
+            const v4i p = __builtin_bit_cast(v4i, __builtin_amdgcn_raw_buffer_load_b128(rt, b * 32, 0, 16));
+            const v4i q = __builtin_bit_cast(v4i, __builtin_amdgcn_raw_buffer_load_b128(rt, b * 32 + 16, 0, 16));
+            x[0] = p.x; x[1] = p.y; x[2] = p.z; x[3] = p.w;
+            x[4] = q.x; x[5] = q.y; x[6] = q.z; x[7] = q.w;
+        } else {
 #pragma unroll
-        for (int g = 0; g <= kFewShards; ++g)
-            x[g] = b < nb ? one_load(a.block_totals + (int64_t)b * kOneTotals + g) : 0;
+            for (int g = 0; g < kFewShards; ++g) x[g] = 0;
+        }
         int32_t before[kFewShards], all[kFewShards];
 #pragma unroll
         for (int g = 0; g < kFewShards; ++g) {
             before[g] = b < lb ? x[g] : 0;
             all[g] = x[g];
         }
-        const int32_t f = __ballot(x[kFewShards] != 0) != 0;
         for (int m = kWave / 2; m >= 1; m >>= 1) {
 #pragma unroll
             for (int g = 0; g < kFewShards; ++g) {
@@ -1906,7 +1937,6 @@ __global__ __launch_bounds__(kOneBlock) __attribute__((amdgpu_waves_per_eu(4, 4)
                 L.part_before[wave][g] = before[g];
                 L.part_all[wave][g] = all[g];
             }
-            L.part_flag[wave] = f;
         }
         __syncthreads();
         if (threadIdx.x < kFewShards) {
@@ -1918,11 +1948,7 @@ __global__ __launch_bounds__(kOneBlock) __attribute__((amdgpu_waves_per_eu(4, 4)
             L.block_base[threadIdx.x] = bs;
             L.total[threadIdx.x] = as;
         }
-        if (threadIdx.x == kFewShards) {
-            int32_t any = 0;
-            for (int w = 0; w < kOneWaves; ++w) any |= L.part_flag[w];
-            L.flag = any;
-        }
+        if (threadIdx.x == kFewShards) L.flag = one_load(a.disorder);
     }
     __syncthreads();
     if (L.flag) return; // offsets not ordinary: the other kernels write the outputs
@@ -2121,7 +2147,7 @@ int64_t one_pass_chunks(int64_t nnz, int64_t waves, int32_t T)
 // workgroups' totals, first_bag.  It follows the other kernels' workspace, so
 // that those never write over `done` before reading it.
 constexpr size_t kOnePassWorkspace =
-    (256 + (size_t)kOneBlock * kOneTotals * 4 + ((size_t)kOneBlock * kOneWaves + 1) * 8 + 255) / 256 * 256;
+    (kOneHeader + (size_t)kOneBlock * kFewShards * 4 + ((size_t)kOneBlock * kOneWaves + 1) * 8 + 255) / 256 * 256;
 
 // Batches below this many ids keep the three kernels: on workload 3's tables
 // (8 destinations), first B bags of each, the one-pass path took 47.6 against
@@ -2278,11 +2304,12 @@ int bucketize_impl(int32_t T, int64_t B, int32_t G, const int64_t *bounds, int32
         unsigned char *w = (unsigned char *)workspace + classic_workspace_bytes(T, B, G);
         oa.barrier = (uint32_t *)w;
         oa.done = (int32_t *)(w + 4);
-        oa.block_totals = (int32_t *)(w + 256);
-        oa.first_bag = (int64_t *)(w + 256 + (size_t)kOneBlock * kOneTotals * 4);
-        void *cargs[] = {&oa.barrier, &oa.done};
-        hipError_t err = hipLaunchKernel((const void *)eb_one_clear, dim3(1), dim3(kWave), cargs, 0, st);
+        oa.disorder = (int32_t *)(w + 8);
+        oa.go = (int32_t *)(w + 1024);
+        oa.block_totals = (int32_t *)(w + kOneHeader);
+        oa.first_bag = (int64_t *)(w + kOneHeader + (size_t)kOneBlock * kFewShards * 4);
         void *oargs[] = {&oa};
+        hipError_t err = hipLaunchKernel((const void *)eb_one_clear, dim3(1), dim3(kWave), oargs, 0, st);
         if (err == hipSuccess)
             err = hipLaunchKernel(oa.K <= kOneChunksSmall
                                       ? (i32 ? one_pass_kernel<int32_t, kOneChunksSmall>() : one_pass_kernel<int64_t, kOneChunksSmall>())

@@ -219,10 +219,10 @@ def test_bucketize_workspace_sizes():
     # tables when B < 2048), every 16th offset, one total per count wave
     # (64 bags for workload 3 into 8 blocks, else 16) and the row's total
     # the three kernels' part, rounded up to 256 bytes, then the one-pass
-    # kernel's fixed part (barrier word, 512 workgroups' totals, 4097 wave
-    # entries)
-    one_pass = (256 + 512 * 16 * 4 + 4097 * 8 + 255) // 256 * 256
-    assert one_pass == 66048
+    # kernel's fixed part (2 KiB of barrier words, 512 workgroups' totals of
+    # 8 int32, 4097 wave entries)
+    one_pass = (2048 + 512 * 8 * 4 + 4097 * 8 + 255) // 256 * 256
+    assert one_pass == 51456
 
     def ws(entries):
         return (entries * 8 + 255) // 256 * 256 + one_pass
