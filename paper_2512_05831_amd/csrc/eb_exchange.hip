@@ -1474,7 +1474,9 @@ constexpr int kOneWaves = 8;                        // waves per workgroup
 constexpr int kOneBlock = kOneWaves * kWave;        // threads per workgroup
 constexpr int kOneBlocksPerCu = 2;                  // 16 waves per compute unit
 constexpr int kOneChunks = 84;                      // 64-id chunks a wave holds, at most (128 VGPRs)
-constexpr int kOneChunksSmall = 48;                 // the kernel walking fewer, for smaller batches
+// Phase 1 walks a fixed number of chunks (straight-line code); smaller
+// batches take a kernel walking fewer: the first of these that holds K.
+constexpr int kOneChunkSizes[] = {16, 32, 48};
 constexpr int kOneGroup = 8;                        // chunks loaded together
 constexpr int kOneStoreGroup = 2;                   // chunks stored together (phase 3)
 constexpr int kOneMaxTables = 1024;
@@ -1757,7 +1759,8 @@ __device__ __forceinline__ IT one_buffer_load(__amdgpu_buffer_rsrc_t r, int byte
     }
 }
 
-// kChunks: the chunks phase 1 walks (K of them hold ids); 48 or kOneChunks.
+// kChunks: the chunks phase 1 walks (K of them hold ids): one of
+// kOneChunkSizes or kOneChunks.
 template <typename IT, int kChunks>
 __global__ __launch_bounds__(kOneBlock) __attribute__((amdgpu_waves_per_eu(4, 4))) void eb_bucket_onepass(const OneArgs a)
 {
@@ -2106,6 +2109,14 @@ const void *scatter_kernel(int G)
 template <typename IT, int kChunks>
 const void *one_pass_kernel() { return (const void *)eb_bucket_onepass<IT, kChunks>; }
 
+template <typename IT>
+const void *one_pass_kernel_for(int K)
+{
+    static_assert(kOneChunkSizes[0] == 16 && kOneChunkSizes[1] == 32 && kOneChunkSizes[2] == 48, "sizes");
+    return K <= 16 ? one_pass_kernel<IT, 16>() : K <= 32 ? one_pass_kernel<IT, 32>()
+           : K <= 48 ? one_pass_kernel<IT, 48>() : one_pass_kernel<IT, kOneChunks>();
+}
+
 template <typename IT, int kChunks>
 int one_pass_occupancy()
 {
@@ -2126,8 +2137,10 @@ int one_pass_blocks()
     b = 0;
     if (hipGetDevice(&dev) == hipSuccess &&
         hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
-        std::min({one_pass_occupancy<int64_t, kOneChunksSmall>(), one_pass_occupancy<int64_t, kOneChunks>(),
-                  one_pass_occupancy<int32_t, kOneChunksSmall>(), one_pass_occupancy<int32_t, kOneChunks>()}) >=
+        std::min({one_pass_occupancy<int64_t, 16>(), one_pass_occupancy<int64_t, 32>(),
+                  one_pass_occupancy<int64_t, 48>(), one_pass_occupancy<int64_t, kOneChunks>(),
+                  one_pass_occupancy<int32_t, 16>(), one_pass_occupancy<int32_t, 32>(),
+                  one_pass_occupancy<int32_t, 48>(), one_pass_occupancy<int32_t, kOneChunks>()}) >=
             kOneBlocksPerCu &&
         cus * kOneBlocksPerCu <= kOneBlock)
         b = cus * kOneBlocksPerCu;
@@ -2150,10 +2163,11 @@ constexpr size_t kOnePassWorkspace =
     (kOneHeader + (size_t)kOneBlock * kFewShards * 4 + ((size_t)kOneBlock * kOneWaves + 1) * 8 + 255) / 256 * 256;
 
 // Batches below this many ids keep the three kernels: on workload 3's tables
-// (8 destinations), first B bags of each, the one-pass path took 47.6 against
-// 32.8 us at B = 2048 (2.6 M ids) and 73.3 against 77.8 us at B = 8192
-// (10.5 M ids); its launches and barrier cost the same at any size.
-constexpr int64_t kOneMinIds = (int64_t)1 << 23;
+// (8 destinations), first B bags of each, the one-pass path took 33.0 / 35.9
+// / 38.1 / 45.5 / 49.2 us against 25.7 / 32.8 / 40.4 / 48.7 / 62.5 us for B =
+// 1024 / 2048 / 3072 / 4096 / 6144 (1.3 to 7.9 M ids), one process each; its
+// launches, barrier and set-up cost about the same at any size.
+constexpr int64_t kOneMinIds = (int64_t)7 << 19; // 3.67 M
 
 // EB_BUCKETIZE_ONE_PASS=0 never takes the one-pass kernel, =1 takes it for
 // every batch it can hold (the tests run both ways); unset, batches of at
@@ -2311,13 +2325,15 @@ int bucketize_impl(int32_t T, int64_t B, int32_t G, const int64_t *bounds, int32
         void *oargs[] = {&oa};
         hipError_t err = hipLaunchKernel((const void *)eb_one_clear, dim3(1), dim3(kWave), oargs, 0, st);
         if (err == hipSuccess)
-            err = hipLaunchKernel(oa.K <= kOneChunksSmall
-                                      ? (i32 ? one_pass_kernel<int32_t, kOneChunksSmall>() : one_pass_kernel<int64_t, kOneChunksSmall>())
-                                      : (i32 ? one_pass_kernel<int32_t, kOneChunks>() : one_pass_kernel<int64_t, kOneChunks>()),
+            err = hipLaunchKernel(i32 ? one_pass_kernel_for<int32_t>(oa.K) : one_pass_kernel_for<int64_t>(oa.K),
                                   dim3(blocks), dim3(kOneBlock), oargs, sizeof(OneBlockLds), st);
         if (err != hipSuccess) return fail(EB_ERR_HIP, "eb_bucketize: %s", hipGetErrorString(err));
         ba.skip = oa.done;
         sa.skip = oa.done;
+        // Behind the one-pass kernel the scan runs as one kernel (its direct
+        // mode, correct at any size and slower only when it does the work):
+        // each kernel launched costs about 2 us even when it returns at once.
+        sa.mode = kScanDirect;
     }
     if (TB > 0) {
         void *args[] = {&ba};
