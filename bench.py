@@ -308,10 +308,16 @@ def count_wave_bags(T, B, G):
     return 16
 
 
-def scan_kernels(G, T, B):
-    """Kernels per eb_bucketize call: count, scan and scatter, the scan in 1
-    (tiles read count's wave totals themselves: nparts * G * (ntiles + G) / 2
-    reads up to 2^16), 2 (tile sums, fused tile scan) or 3 launches."""
+def scan_kernels(G, T, B, nnz=0):
+    """Kernels per eb_bucketize call.  Up to 8 destinations and from 3.67 M
+    ids (unless EB_BUCKETIZE_ONE_PASS says otherwise): the clear kernel, the
+    one-pass kernel, and count, the one-kernel scan and scatter behind it (5).
+    Otherwise count, scan and scatter, the scan in 1 (tiles read count's wave
+    totals themselves: nparts * G * (ntiles + G) / 2 reads up to 2^16), 2
+    (tile sums, fused tile scan) or 3 launches."""
+    setting = os.environ.get("EB_BUCKETIZE_ONE_PASS", "")
+    if G <= 8 and T * B > 0 and setting != "0" and (nnz >= 7 << 19 or setting == "1"):
+        return 5
     ntiles = scan_tile_count(T, B)
     nparts = T * -(-B // count_wave_bags(T, B, G))
     if 0.5 * nparts * G * (ntiles + G) <= 1 << 16:
@@ -363,7 +369,7 @@ def exchange_bench(torch, dev, eb, K, W, Gs=(8,), i32=False):
                           # count, (tile sums unless the tile scan reads the wave totals itself,)
                           # (row prefix when the fused tile scan would read over 2^20 tile sums,)
                           # tile scan, scatter
-                          "kernels_per_call": scan_kernels(G, w.T, w.B)}), flush=True)
+                          "kernels_per_call": scan_kernels(G, w.T, w.B, int(idx.size))}), flush=True)
         del out_off, ws
     del d_i, out_idx
     Gp = 8  # the partial blocks of 8 GPUs, whatever --destinations says
