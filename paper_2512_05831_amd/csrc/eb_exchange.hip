@@ -1648,14 +1648,15 @@ __global__ void eb_one_clear(OneArgs a)
 
 // The wave holding bag boundary p (0 <= p <= TB): the wave of table
 // min(p / B, T - 1) whose positions hold offsets[p] (a boundary at a wave's
-// end belongs to that wave).
-__device__ __forceinline__ int64_t one_wave_of(const OneArgs &a, const OneBlockLds &L, int64_t p, int64_t x)
+// end belongs to that wave).  32-bit divisions: the path takes T * B < 2^31
+// and nnz < 2^31, and x is clamped into the table's positions first.
+__device__ __forceinline__ int one_wave_of(const OneArgs &a, const OneBlockLds &L, uint32_t p, int64_t x)
 {
-    const int t = (int)min<int64_t>(p / max<int64_t>(a.B, 1), a.T - 1);
+    const int t = (int)min<uint32_t>(p / (uint32_t)a.B, (uint32_t)(a.T - 1));
     const int64_t lo = L.tstart[t], hi = max(lo, L.tstart[t + 1]);
-    const int64_t waves = L.wstart[t + 1] - L.wstart[t];
-    x = min(max(x, lo), hi) - lo;
-    return L.wstart[t] + min<int64_t>(x / a.C, waves - 1);
+    const uint32_t waves = (uint32_t)(L.wstart[t + 1] - L.wstart[t]);
+    const uint32_t xr = (uint32_t)(min(max(x, lo), hi) - lo);
+    return L.wstart[t] + (int)min<uint32_t>(xr / (uint32_t)a.C, waves - 1);
 }
 
 // few_owner_masks for ids and bounds that fit in 32 bits: the bounds of a
@@ -1782,8 +1783,8 @@ __global__ __launch_bounds__(kOneBlock) __attribute__((amdgpu_waves_per_eu(4, 4)
             int64_t s = 0, e = 0;
             if (t <= a.T) s = min<int64_t>(max<int64_t>((int64_t)off[(int64_t)t * a.B], 0), a.nnz);
             if (t < a.T) e = min<int64_t>(max<int64_t>((int64_t)off[(int64_t)(t + 1) * a.B], 0), a.nnz);
-            const int64_t len = e > s ? e - s : 0;
-            const int64_t waves = t < a.T ? (len <= C ? 1 : 1 + (len - 1) / C) : 0;
+            const int64_t len = e > s ? e - s : 0; // at most nnz < 2^31
+            const int64_t waves = t < a.T ? (len <= C ? 1 : 1 + (int64_t)((uint32_t)(len - 1) / (uint32_t)C)) : 0;
             int64_t incl = waves; // inclusive scan over the lanes
             for (int d = 1; d < kWave; d <<= 1) {
                 const int64_t y = shfl_up64(incl, d);
@@ -1825,15 +1826,25 @@ __global__ __launch_bounds__(kOneBlock) __attribute__((amdgpu_waves_per_eu(4, 4)
         const int64_t nwaves = (int64_t)gridDim.x * kOneWaves;
         const int64_t share = (a.TB + 2 + nwaves - 1) / nwaves;
         const int64_t pend = min<int64_t>((v + 1) * share, a.TB + 2);
-        for (int64_t p = v * share + lane; p < pend; p += kWave) {
-            const int64_t xp = p <= a.TB ? (int64_t)off[p] : 0;
-            const int64_t xq = p >= 1 && p - 1 <= a.TB ? (int64_t)off[p - 1] : 0;
+        for (int64_t p0 = v * share; p0 < pend; p0 += kWave) {
+            const int64_t p = p0 + lane;
+            const bool in = p < pend;
+            const int64_t xp = in && p <= a.TB ? (int64_t)off[p] : 0;
+            const int c1 = !in ? 0 : p <= a.TB ? one_wave_of(a, L, (uint32_t)p, xp) : (int)used;
+            // The previous boundary's offset and wave: lane - 1's (lane 0
+            // finds its own).
+            int64_t xq = shfl_up64(xp, 1);
+            int c0 = __shfl_up(c1, 1);
+            if (lane == 0 && p >= 1) {
+                xq = (int64_t)off[p - 1];
+                c0 = one_wave_of(a, L, (uint32_t)(p - 1), xq);
+            }
+            if (!in) continue;
             if ((p >= 1 && p <= a.TB && xq > xp) || (p == 0 && xp < 0) || (p == a.TB && xp > a.nnz)) disorder = true;
-            const int64_t c1 = p <= a.TB ? one_wave_of(a, L, p, xp) : used;
-            const int64_t c0 = p >= 1 ? one_wave_of(a, L, p - 1, xq) + 1 : 0;
             // (c stays within the grid's waves even for offsets that are not
             // ordinary, whose tables may claim more waves than there are)
-            for (int64_t c = max<int64_t>(c0, 0); c <= min(c1, min(used, nwaves)); ++c) one_store(a.first_bag + c, p);
+            const int64_t last = min<int64_t>(c1, min(used, nwaves));
+            for (int64_t c = p >= 1 ? c0 + 1 : 0; c <= last; ++c) one_store(a.first_bag + c, p);
         }
     }
 
@@ -2178,10 +2189,11 @@ int one_pass_setting()
     return e && e[0] == '0' ? 0 : e && e[0] == '1' ? 1 : -1;
 }
 
-bool one_pass_fits(int32_t T, int32_t G, int64_t nnz, hipStream_t st)
+bool one_pass_fits(int32_t T, int64_t B, int32_t G, int64_t nnz, hipStream_t st)
 {
     const int setting = one_pass_setting();
     if (setting == 0 || G > kFewShards || T < 1 || T > kOneMaxTables || nnz < 1) return false;
+    if ((int64_t)T * B >= ((int64_t)1 << 31) - 2 || nnz >= ((int64_t)1 << 31)) return false; // 32-bit positions
     if (setting < 0 && nnz < kOneMinIds) return false;
     const int blocks = one_pass_blocks();
     if (blocks <= 0) return false;
@@ -2297,7 +2309,7 @@ int bucketize_impl(int32_t T, int64_t B, int32_t G, const int64_t *bounds, int32
     // the three kernels launched behind it, which return at once when it
     // has written the outputs (`done`) and do the work when it could not
     // (offsets not ordinary, a cancelled barrier).
-    if (TB > 0 && one_pass_fits(T, G, nnz, st)) {
+    if (TB > 0 && one_pass_fits(T, B, G, nnz, st)) {
         OneArgs oa;
         std::memset(&oa, 0, sizeof oa);
         const int blocks = one_pass_blocks();
