@@ -279,7 +279,8 @@ int eb_bucketize_workspace(int32_t T, int64_t B, int32_t G, size_t *bytes);
  *   stream       a hipStream_t (NULL = the null stream); asynchronous.
  *
  * Paths: batches of at least 3,670,016 ids with at most 8 destinations and 1024
- * tables, outside a graph capture, run a one-pass kernel that reads every
+ * tables (and, inside a graph capture, once an eager call has run on the
+ * process's device) run a one-pass kernel that reads every
  * id once: its workgroups (as many as the GPU holds resident at once) meet
  * at one grid-wide barrier.  The three-kernel path (count, scan, scatter)
  * is launched behind it and returns at once when the one-pass kernel has

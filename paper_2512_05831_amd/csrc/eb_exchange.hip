@@ -2139,9 +2139,11 @@ int one_pass_occupancy()
 // The one-pass kernel's workgroups: kOneBlocksPerCu per compute unit when
 // the runtime reports that many resident and phase 2's one thread per
 // workgroup suffices, else 0 (the path is not taken).
+std::atomic<int> g_one_pass_blocks{-1}; // -1 until the first eager call has asked the runtime
+
 int one_pass_blocks()
 {
-    static std::atomic<int> cached{-1};
+    std::atomic<int> &cached = g_one_pass_blocks;
     int b = cached.load(std::memory_order_acquire);
     if (b >= 0) return b;
     int dev = 0, cus = 0;
@@ -2195,12 +2197,16 @@ bool one_pass_fits(int32_t T, int64_t B, int32_t G, int64_t nnz, hipStream_t st)
     if (setting == 0 || G > kFewShards || T < 1 || T > kOneMaxTables || nnz < 1) return false;
     if ((int64_t)T * B >= ((int64_t)1 << 31) - 2 || nnz >= ((int64_t)1 << 31)) return false; // 32-bit positions
     if (setting < 0 && nnz < kOneMinIds) return false;
+    // Under a graph capture the kernels record like any others (the clear
+    // kernel resets the barrier words on every replay), but the occupancy
+    // query is not made there: a capture before any eager call keeps the
+    // three kernels.
+    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing(st, &cs) != hipSuccess) return false;
+    if (cs != hipStreamCaptureStatusNone && g_one_pass_blocks.load(std::memory_order_acquire) < 0) return false;
     const int blocks = one_pass_blocks();
     if (blocks <= 0) return false;
-    if (one_pass_chunks(nnz, (int64_t)blocks * kOneWaves, T) > kOneChunks) return false;
-    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
-    if (hipStreamIsCapturing(st, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone) return false;
-    return true;
+    return one_pass_chunks(nnz, (int64_t)blocks * kOneWaves, T) <= kOneChunks;
 }
 
 size_t classic_workspace_bytes(int32_t T, int64_t B, int32_t G)
