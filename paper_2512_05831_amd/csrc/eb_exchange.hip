@@ -1506,6 +1506,7 @@ struct OneArgs {
     int32_t T;
     int32_t G;
     int32_t K;              // chunks per wave
+    uint32_t spin_limit;    // barrier polls before cancelling (kOneSpinLimit)
 };
 
 struct OneRec {
@@ -1606,7 +1607,7 @@ __device__ __forceinline__ bool one_grid_barrier(const OneArgs &a, uint32_t n, i
             for (uint32_t spin = 0;; ++spin) {
                 r = __hip_atomic_load(mine, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 if (r) break;
-                if (spin > kOneSpinLimit) {
+                if (spin > a.spin_limit) {
                     uint32_t seen = __hip_atomic_load(a.barrier, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                     if (!(seen & kOneCancel) && seen < n &&
                         __hip_atomic_compare_exchange_strong(a.barrier, &seen, seen | kOneCancel, __ATOMIC_RELAXED,
@@ -2332,6 +2333,10 @@ int bucketize_impl(int32_t T, int64_t B, int32_t G, const int64_t *bounds, int32
         oa.T = T;
         oa.G = G;
         oa.K = (int32_t)one_pass_chunks(nnz, (int64_t)blocks * kOneWaves, T);
+        // EB_BUCKETIZE_SPIN_LIMIT (tests only) shortens the barrier's wait,
+        // so that a test can make it cancel and the fallback run.
+        const char *spin = std::getenv("EB_BUCKETIZE_SPIN_LIMIT");
+        oa.spin_limit = spin && *spin ? (uint32_t)std::strtoul(spin, nullptr, 10) : kOneSpinLimit;
         oa.C = (int64_t)oa.K * kWave;
         unsigned char *w = (unsigned char *)workspace + classic_workspace_bytes(T, B, G);
         oa.barrier = (uint32_t *)w;

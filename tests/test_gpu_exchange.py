@@ -396,6 +396,69 @@ def test_bucketize_dlrm_batch(device):
     check_bucketize(w.T, w.B, idx, off, bounds, device)
 
 
+
+def one_pass_case(seed, G, layout, T=4, B=600):
+    """Ordinary offsets in layouts the one-pass kernel's wave ranges must
+    handle: offsets starting above 0 and ending before nnz (ids in no bag),
+    empty tables (first, middle, last), one bag holding most ids (a bag across
+    many waves), and a plain batch (used with a short out_indices)."""
+    g = np.random.default_rng(seed)
+    rows = [int(g.integers(1000, 50_000)) for _ in range(T)]
+    L = g.integers(0, 40, T * B)
+    if layout == "empty-tables":
+        for t in (0, T // 2, T - 1):
+            L[t * B:(t + 1) * B] = 0
+    if layout == "huge-bag":
+        L[B + 7] = 300_000
+    off = wl.offsets_from_lengths(L)
+    lead, tail = (37, 55) if layout == "inner-offsets" else (0, 0)
+    off = off + lead
+    nnz = int(off[-1]) + tail
+    idx = np.empty(nnz, dtype=np.int64)
+    idx[:lead] = g.integers(0, rows[0], lead)
+    idx[nnz - tail:] = g.integers(0, rows[-1], tail)
+    for t in range(T):
+        s0, s1 = int(off[t * B]), int(off[(t + 1) * B])
+        idx[s0:s1] = g.integers(-3, rows[t] + 3, s1 - s0)
+    return T, B, idx, off, even_bounds(rows, G)
+
+
+@pytest.mark.parametrize("G", [1, 5, 8])
+@pytest.mark.parametrize("layout", ["inner-offsets", "empty-tables", "huge-bag", "short-capacity"])
+def test_bucketize_one_pass_layouts(G, layout, device):
+    T, B, idx, off, bounds = one_pass_case(G * 7 + len(layout), G, layout)
+    cap = None
+    if layout == "short-capacity":
+        n = oracle.bucketize(bounds, idx, off, T, B)[2][-1]
+        cap = int(n) // 2
+    check_bucketize(T, B, idx, off, bounds, device, capacity=cap)
+
+
+@pytest.mark.parametrize("nnz", [4_150_000, 4_400_000])
+def test_bucketize_one_pass_kernel_sizes(nnz, device):
+    """Batches on either side of the 16-chunk kernel's capacity (with 4096
+    resident waves: 16 x 64 ids per wave), one in each kernel size."""
+    g = np.random.default_rng(nnz)
+    T, B, rows = 3, 40_000, 900_000
+    L = g.multinomial(nnz, np.full(T * B, 1.0 / (T * B)))
+    off = wl.offsets_from_lengths(L)
+    idx = g.integers(0, rows, int(off[-1]), dtype=np.int64)
+    check_bucketize(T, B, idx, off, even_bounds([rows] * T, 8), device)
+
+
+@pytest.mark.parametrize("G", [2, 8])
+def test_bucketize_cancelled_barrier(G, device, monkeypatch):
+    """With the barrier's wait cut to no polls (a test-only setting), the
+    workgroups that find it incomplete cancel it: the one-pass kernel then
+    writes nothing and the three kernels behind it do the work, or, when
+    every workgroup has arrived first, the kernel finishes as usual.  Either
+    way the outputs must be the oracle's, call after call."""
+    monkeypatch.setenv("EB_BUCKETIZE_SPIN_LIMIT", "0")
+    for seed in range(3):
+        T, B, idx, off, bounds = one_pass_case(seed, G, "plain", T=5, B=3000)
+        check_bucketize(T, B, idx, off, bounds, device)
+
+
 def run_sum_partials(parts, B, T, D, mean_off, nnz, device, out=None):
     d_p = torch.from_numpy(np.ascontiguousarray(parts, dtype=np.float32)).to(device)
     d_m = None if mean_off is None else torch.from_numpy(np.asarray(mean_off, np.int64)).to(device)
