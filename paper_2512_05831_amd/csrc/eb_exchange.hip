@@ -1448,8 +1448,8 @@ __global__ __launch_bounds__(kBlock) void eb_sum_partials_scalar(const PartialAr
 // in (table, bag, position) order already, so destination g's output is the
 // subsequence of the ids it owns, and out_offsets[g][p] is the number of ids
 // owned by g at positions before offsets[p]: a rank over positions, with no
-// per-bag counts.  One cooperative launch with one grid-wide barrier then
-// reads every id once:
+// per-bag counts.  One launch with one grid-wide barrier then reads every id
+// once:
 //   phase 1  table t's positions [offsets[t B], offsets[(t+1) B]) are split
 //            among max(1, ceil(length / C)) consecutive waves (C = K * 64
 //            ids; T + nnz / C waves at most).  A wave keeps its ids in
@@ -1466,10 +1466,12 @@ __global__ __launch_bounds__(kBlock) void eb_sum_partials_scalar(const PartialAr
 //   phase 3  each wave stores its ids at segments[g] + rank, and writes
 //            out_offsets for the bags that start in its positions from the
 //            chunk records (one lane per bag).
-// The workgroups must all be resident at once (a cooperative launch, sized
-// from the occupancy the runtime reports), since phase 3 waits for all of
-// phase 1.  Offsets that are not ordinary are detected in phase 1; the
-// kernel then writes nothing and the call's other kernels do the work.
+// The workgroups must all be resident at once, since phase 3 waits for all
+// of phase 1: the grid is sized from the occupancy the runtime reports, and
+// the barrier gives up (and the kernel writes nothing) when they are not
+// (see one_grid_barrier).  Offsets that are not ordinary are detected in
+// phase 1, and the kernel then writes nothing either; in both cases the
+// count, scan and scatter kernels launched behind it do the work.
 constexpr int kOneWaves = 8;                        // waves per workgroup
 constexpr int kOneBlock = kOneWaves * kWave;        // threads per workgroup
 constexpr int kOneBlocksPerCu = 2;                  // 16 waves per compute unit
@@ -1477,12 +1479,12 @@ constexpr int kOneChunks = 84;                      // 64-id chunks a wave holds
 // Phase 1 walks a fixed number of chunks (straight-line code); smaller
 // batches take a kernel walking fewer: the first of these that holds K.
 constexpr int kOneChunkSizes[] = {16, 32, 48};
-constexpr int kOneGroup = 8;                        // chunks loaded together
+constexpr int kOneGroup = 8;                        // phase 1's loads in flight per wave
 constexpr int kOneStoreGroup = 2;                   // chunks stored together (phase 3)
 constexpr int kOneMaxTables = 1024;
 constexpr int kOneGoStride = 32;                    // int32: one 128-byte line per XCD's release word
 constexpr size_t kOneHeader = 2048;                 // workspace bytes before the workgroups' totals
-constexpr uint32_t kOneSpinLimit = 1u << 16;        // barrier polls (about 30-60 ms) before cancelling
+constexpr uint32_t kOneSpinLimit = 1u << 16;        // barrier polls (tens of milliseconds) before cancelling
 constexpr uint32_t kOneCancel = 0x80000000u;        // the barrier counter's cancelled mark
 
 struct OneArgs {
@@ -1894,10 +1896,13 @@ __global__ __launch_bounds__(kOneBlock) __attribute__((amdgpu_waves_per_eu(4, 4)
             __builtin_amdgcn_sched_barrier(0); // one chunk at a time: registers hold the ids
         });
     }
-    // The record past the last chunk: no ids, the totals.
+    // The record past the last chunk: no ids, the totals.  (The ballot is
+    // taken by the whole wave: any lane may have found the offsets out of
+    // order.)
+    const bool wave_disorder = __ballot(disorder) != 0;
     if (lane == 0) {
         W.rec[a.K] = OneRec{0, 0, 0, 0};
-        L.wave_flag[wave] = __ballot(disorder) != 0;
+        L.wave_flag[wave] = wave_disorder;
     }
     if (lane < kFewShards) {
         W.cum[a.K][lane] = (uint16_t)run;

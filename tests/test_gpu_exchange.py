@@ -446,6 +446,21 @@ def test_bucketize_one_pass_kernel_sizes(nnz, device):
     check_bucketize(T, B, idx, off, even_bounds([rows] * T, 8), device)
 
 
+@pytest.mark.parametrize("where", [12_345, 200_001, 333_333])
+def test_bucketize_one_decreasing_offset(where, device):
+    """Ordinary offsets but for a single one that decreases, in a batch with
+    many bags per wave of the one-pass kernel's offset checks (so that most
+    offsets are checked by lanes other than the first): it must be found,
+    and the output is then that of the offsets as given."""
+    g = np.random.default_rng(where)
+    T, B, rows = 4, 100_000, 50_000
+    L = g.integers(0, 12, T * B)
+    off = wl.offsets_from_lengths(L)
+    off[where] = off[where + 1] + 3  # offsets[where] > offsets[where + 1]
+    idx = g.integers(0, rows, int(off[-1]), dtype=np.int64)
+    check_bucketize(T, B, idx, off, even_bounds([rows] * T, 8), device)
+
+
 @pytest.mark.parametrize("G", [2, 8])
 def test_bucketize_cancelled_barrier(G, device, monkeypatch):
     """With the barrier's wait cut to no polls (a test-only setting), the
