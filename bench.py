@@ -309,14 +309,14 @@ def count_wave_bags(T, B, G):
 
 
 def scan_kernels(G, T, B, nnz=0):
-    """Kernels per eb_bucketize call.  Up to 8 destinations and from 3.67 M
+    """Kernels per eb_bucketize call.  Up to 16 destinations and from 3.67 M
     ids (unless EB_BUCKETIZE_ONE_PASS says otherwise): the clear kernel, the
     one-pass kernel, and count, the one-kernel scan and scatter behind it (5).
     Otherwise count, scan and scatter, the scan in 1 (tiles read count's wave
     totals themselves: nparts * G * (ntiles + G) / 2 reads up to 2^16), 2
     (tile sums, fused tile scan) or 3 launches."""
     setting = os.environ.get("EB_BUCKETIZE_ONE_PASS", "")
-    if G <= 8 and T * B > 0 and setting != "0" and (nnz >= 7 << 19 or setting == "1"):
+    if G <= 16 and T * B > 0 and setting != "0" and (nnz >= 7 << 19 or setting == "1"):
         return 5
     ntiles = scan_tile_count(T, B)
     nparts = T * -(-B // count_wave_bags(T, B, G))

@@ -278,7 +278,7 @@ int eb_bucketize_workspace(int32_t T, int64_t B, int32_t G, size_t *bytes);
  *                owned by the caller; its contents are not kept.
  *   stream       a hipStream_t (NULL = the null stream); asynchronous.
  *
- * Paths: batches of at least 3,670,016 ids with at most 8 destinations and 1024
+ * Paths: batches of at least 3,670,016 ids with at most 16 destinations and 1024
  * tables (and, inside a graph capture, once an eager call has run on the
  * process's device) run a one-pass kernel that reads every
  * id once: its workgroups (as many as the GPU holds resident at once) meet
@@ -289,7 +289,7 @@ int eb_bucketize_workspace(int32_t T, int64_t B, int32_t G, size_t *bytes);
  * other work on the GPU keeps workgroups from being resident).  Both give
  * the same outputs.  The environment variable EB_BUCKETIZE_ONE_PASS (read on
  * every call) forces the choice: 0 never, 1 whenever the kernel can hold
- * the batch (up to 8 destinations and about 23 million ids).
+ * the batch (up to 16 destinations and about 23 million ids).
  *
  * No allocation, no host synchronisation; calls that overlap on the same
  * workspace race.  out_offsets, out_indices, segments and the workspace must

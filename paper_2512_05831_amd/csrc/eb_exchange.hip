@@ -18,7 +18,7 @@
 // contraction); eb_sum_partials is bound by it, eb_bucketize by its waves'
 // chains of dependent loads and by instruction issue.
 //
-// eb_bucketize runs, for batches of at least kOneMinIds ids and at most 8
+// eb_bucketize runs, for batches of at least kOneMinIds ids and at most 16
 // destinations, a one-pass kernel that reads every id once (see "One-pass
 // bucketize" below), followed by the three kernels here, which return at
 // once when it has written the outputs and otherwise do the work; every
@@ -1442,7 +1442,7 @@ __global__ __launch_bounds__(kBlock) void eb_sum_partials_scalar(const PartialAr
 }
 
 // ---------------------------------------------------------------------------
-// One-pass bucketize: ordinary offsets, at most 8 destinations.
+// One-pass bucketize: ordinary offsets, at most 16 destinations.
 //
 // With ordinary offsets (non-decreasing within [0, nnz]) the batch's ids lie
 // in (table, bag, position) order already, so destination g's output is the
@@ -1495,7 +1495,7 @@ struct OneArgs {
     void *out_indices;      // IT [out_cap]
     int64_t *segments;      // [G+1]
     int64_t *first_bag;     // [waves+1] (workspace): the first bag that starts at or past wave c's positions
-    int32_t *block_totals;  // [gridDim.x][8] (workspace): each workgroup's ids per destination
+    int32_t *block_totals;  // [gridDim.x][kD / 2] (workspace): each workgroup's ids per destination, 16 bits each
     uint32_t *barrier;      // (workspace, zero at launch): workgroups arrived, or kOneCancel
     int32_t *done;          // (workspace, zero at launch): 1 once the outputs are written
     int32_t *disorder;      // (workspace, zero at launch): nonzero when the offsets are not ordinary
@@ -1511,29 +1511,41 @@ struct OneArgs {
     uint32_t spin_limit;    // barrier polls before cancelling (kOneSpinLimit)
 };
 
+// A chunk's owner masks: the valid lanes and one mask per bit of the owner
+// (kBits = 3 up to 8 destinations, 4 up to 16).
+struct OneMasks {
+    uint64_t valid;
+    uint64_t b[4];
+};
+
+template <int kBits>
 struct OneRec {
-    uint64_t valid, b0, b1, b2; // a chunk's owner masks (FewMasks)
+    uint64_t valid;
+    uint64_t b[kBits];
 };
 
 // LDS of a wave: kOneChunks + 1 records and running counts (the last: none,
 // and the wave's totals).
+template <int kBits>
 struct OneWaveLds {
-    OneRec rec[kOneChunks + 1];
-    uint16_t cum[kOneChunks + 1][kFewShards];
+    OneRec<kBits> rec[kOneChunks + 1];
+    uint16_t cum[kOneChunks + 1][1 << kBits];
 };
 
+template <int kBits>
 struct OneBlockLds {
-    OneWaveLds wave[kOneWaves];
+    static constexpr int kD = 1 << kBits;
+    OneWaveLds<kBits> wave[kOneWaves];
     int64_t tstart[kOneMaxTables + 1]; // offsets[t B], clamped into [0, nnz]
     int32_t wstart[kOneMaxTables + 1]; // table t's first wave; wstart[T]: waves used
-    int32_t wave_total[kOneWaves][kFewShards];
+    int32_t wave_total[kOneWaves][kD];
     int32_t wave_flag[kOneWaves];
-    int32_t part_before[kOneWaves][kFewShards]; // phase 2: each wave's sums
-    int32_t part_all[kOneWaves][kFewShards];
+    int32_t part_before[kOneWaves][kD]; // phase 2: each wave's sums
+    int32_t part_all[kOneWaves][kD];
     int32_t pass;                      // the grid barrier's outcome
-    int64_t block_base[kFewShards];    // ids for g in earlier workgroups
-    int64_t total[kFewShards];         // ids for g in all
-    int64_t wave_base[kOneWaves][kFewShards]; // ids for g before the wave
+    int64_t block_base[kD];            // ids for g in earlier workgroups
+    int64_t total[kD];                 // ids for g in all
+    int64_t wave_base[kOneWaves][kD];  // ids for g before the wave
     int32_t flag;
 };
 
@@ -1653,7 +1665,8 @@ __global__ void eb_one_clear(OneArgs a)
 // min(p / B, T - 1) whose positions hold offsets[p] (a boundary at a wave's
 // end belongs to that wave).  32-bit divisions: the path takes T * B < 2^31
 // and nnz < 2^31, and x is clamped into the table's positions first.
-__device__ __forceinline__ int one_wave_of(const OneArgs &a, const OneBlockLds &L, uint32_t p, int64_t x)
+template <typename LdsT>
+__device__ __forceinline__ int one_wave_of(const OneArgs &a, const LdsT &L, uint32_t p, int64_t x)
 {
     const int t = (int)min<uint32_t>(p / (uint32_t)a.B, (uint32_t)(a.T - 1));
     const int64_t lo = L.tstart[t], hi = max(lo, L.tstart[t + 1]);
@@ -1709,36 +1722,62 @@ __device__ __forceinline__ uint32_t one_copy(uint32_t x)
     return y;
 }
 
-// Phase 1's record of chunk u: its masks, and the running counts before it
-// (lane g < 8 keeps destination g's in `run`).
-__device__ __forceinline__ void one_record(OneWaveLds &W, int u, int lane, const FewMasks &o, int32_t &run, uint32_t l0,
-                                           uint32_t l1, uint32_t l2)
+// The lanes of `valid` whose owner bits equal x[k] (each all ones or zero)
+// for every k < kBits, for one 32-bit half (hi) of the masks.
+template <int kBits>
+__device__ __forceinline__ uint32_t one_same_n(const OneMasks &o, const uint32_t (&x)[4], bool hi)
 {
-    if (lane == 0) W.rec[u] = OneRec{o.valid, o.b0, o.b1, o.b2};
-    if (lane < kFewShards) W.cum[u][lane] = (uint16_t)run;
-    const uint32_t own_lo = one_same((uint32_t)o.valid, (uint32_t)o.b0, (uint32_t)o.b1, (uint32_t)o.b2, ~l0, ~l1, ~l2);
-    const uint32_t own_hi = one_same((uint32_t)(o.valid >> 32), (uint32_t)(o.b0 >> 32), (uint32_t)(o.b1 >> 32),
-                                     (uint32_t)(o.b2 >> 32), ~l0, ~l1, ~l2);
-    run += __popc(own_lo) + __popc(own_hi);
+    uint32_t d = 0;
+#pragma unroll
+    for (int k = 0; k < kBits; ++k) d |= (uint32_t)(o.b[k] >> (hi ? 32 : 0)) ^ x[k];
+    return (uint32_t)(o.valid >> (hi ? 32 : 0)) & ~d;
+}
+
+// Phase 1's record of chunk u: its masks, and the running counts before it
+// (lane g < 2^kBits keeps destination g's in `run`; mine[k] is all ones
+// where the lane's bit k is set).
+template <int kBits>
+__device__ __forceinline__ void one_record(OneWaveLds<kBits> &W, int u, int lane, const OneMasks &o, int32_t &run,
+                                           const uint32_t (&mine)[4])
+{
+    if (lane == 0) {
+        OneRec<kBits> r;
+        r.valid = o.valid;
+#pragma unroll
+        for (int k = 0; k < kBits; ++k) r.b[k] = o.b[k];
+        W.rec[u] = r;
+    }
+    if (lane < (1 << kBits)) W.cum[u][lane] = (uint16_t)run;
+    run += __popc(one_same_n<kBits>(o, mine, false)) + __popc(one_same_n<kBits>(o, mine, true));
+}
+
+__device__ __forceinline__ OneMasks one_masks(const FewMasks &f)
+{
+    return OneMasks{f.valid, {f.b0, f.b1, f.b2, 0}};
 }
 
 // Phase 3's step for chunk u, whose id this lane holds: its rank among the
 // chunk's ids for the same destination, the destination's slot from the lane
 // numbered by it (lane g < 8 holds slot + the running count for g), one store.
-template <typename IT>
-__device__ __forceinline__ void one_store_chunk(const OneArgs &a, const OneWaveLds &W, int lane, int64_t slot, int u,
-                                                int64_t id, IT *out)
+template <typename IT, int kBits>
+__device__ __forceinline__ void one_store_chunk(const OneArgs &a, const OneWaveLds<kBits> &W, int lane, int64_t slot,
+                                                int u, int64_t id, IT *out)
 {
-    const OneRec r = W.rec[u];
-    const uint64_t valid = uniform_mask(r.valid);
-    const uint64_t b0 = uniform_mask(r.b0), b1 = uniform_mask(r.b1), b2 = uniform_mask(r.b2);
-    const uint32_t x0 = lane_bit(b0) ? ~0u : 0u, x1 = lane_bit(b1) ? ~0u : 0u, x2 = lane_bit(b2) ? ~0u : 0u;
-    const uint32_t same_lo = one_same((uint32_t)valid, (uint32_t)b0, (uint32_t)b1, (uint32_t)b2, x0, x1, x2);
-    const uint32_t same_hi = one_same((uint32_t)(valid >> 32), (uint32_t)(b0 >> 32), (uint32_t)(b1 >> 32),
-                                      (uint32_t)(b2 >> 32), x0, x1, x2);
-    const int rank = (int)__builtin_amdgcn_mbcnt_hi(same_hi, __builtin_amdgcn_mbcnt_lo(same_lo, 0u));
-    const int64_t mine = slot + (lane < kFewShards ? (int64_t)W.cum[u][lane] : 0);
-    const int from = few_bits<4>(FewMasks{valid, b0, b1, b2});
+    const OneRec<kBits> r = W.rec[u];
+    OneMasks o;
+    o.valid = uniform_mask(r.valid);
+    uint32_t x[4];
+    int from = 0; // 4 x this lane's owner: the lane holding its slot, as a byte offset
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        o.b[k] = k < kBits ? uniform_mask(r.b[k < kBits ? k : 0]) : 0;
+        x[k] = k < kBits && lane_bit(o.b[k]) ? ~0u : 0u;
+        from |= k < kBits && lane_bit(o.b[k]) ? 4 << k : 0;
+    }
+    const int rank = (int)__builtin_amdgcn_mbcnt_hi(one_same_n<kBits>(o, x, true),
+                                                    __builtin_amdgcn_mbcnt_lo(one_same_n<kBits>(o, x, false), 0u));
+    const int64_t mine = slot + (lane < (1 << kBits) ? (int64_t)W.cum[u][lane] : 0);
+    const uint64_t valid = o.valid;
     const int base_lo = __builtin_amdgcn_ds_bpermute(from, (int)(uint32_t)mine);
     const int base_hi = __builtin_amdgcn_ds_bpermute(from, (int)(mine >> 32));
     const int64_t pos = (((int64_t)base_hi << 32) | (uint32_t)base_lo) + rank;
@@ -1764,13 +1803,17 @@ __device__ __forceinline__ IT one_buffer_load(__amdgpu_buffer_rsrc_t r, int byte
 }
 
 // kChunks: the chunks phase 1 walks (K of them hold ids): one of
-// kOneChunkSizes or kOneChunks.
-template <typename IT, int kChunks>
+// kOneChunkSizes or kOneChunks.  kBits: the owner's bits, 3 up to 8
+// destinations, 4 up to 16 (the compare tree over every second bound picks
+// the pair of blocks, one compare with the pair's middle bound the block).
+template <typename IT, int kChunks, int kBits>
 __global__ __launch_bounds__(kOneBlock) __attribute__((amdgpu_waves_per_eu(4, 4))) void eb_bucket_onepass(const OneArgs a)
 {
     static_assert(kChunks % kOneStoreGroup == 0 && kChunks <= kOneChunks, "chunks");
     extern __shared__ __align__(16) unsigned char one_lds_raw[];
-    OneBlockLds &L = *(OneBlockLds *)one_lds_raw;
+    OneBlockLds<kBits> &L = *(OneBlockLds<kBits> *)one_lds_raw;
+    constexpr int kD = 1 << kBits;
+    constexpr int kGroup = kOneGroup;
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = threadIdx.x / kWave;
     const int lb = xcd_run_block(blockIdx.x, gridDim.x);
@@ -1818,7 +1861,7 @@ __global__ __launch_bounds__(kOneBlock) __attribute__((amdgpu_waves_per_eu(4, 4)
     }
     ps = uniform64(ps);
     n = uniform64(n);
-    OneWaveLds &W = L.wave[wave];
+    OneWaveLds<kBits> &W = L.wave[wave];
 
     // Which bags start in which wave's positions, for this wave's share of
     // the boundaries 0 .. TB and a last, virtual one (TB + 1) past them all:
@@ -1853,46 +1896,71 @@ __global__ __launch_bounds__(kOneBlock) __attribute__((amdgpu_waves_per_eu(4, 4)
 
     // Phase 1: hold the ids, record every chunk's masks and running counts.
     uint32_t held[kChunks];
-    int32_t run = 0; // lane g < 8: this wave's ids for destination g so far
-    const uint32_t l0 = (uint32_t)(lane & 1) - 1u, l1 = (uint32_t)((lane >> 1) & 1) - 1u,
-                   l2 = (uint32_t)((lane >> 2) & 1) - 1u;
+    int32_t run = 0; // lane g < kD: this wave's ids for destination g so far
+    uint32_t mine[4];  // all ones where this lane's bit k is set
+#pragma unroll
+    for (int k = 0; k < 4; ++k) mine[k] = ((lane >> k) & 1) ? ~0u : 0u;
     const IT *src = (const IT *)a.indices + ps + lane;
+    // The table's bounds: for kBits = 3 all inner ones; for 4 every second
+    // one (the pairs), with the odd ones (the pairs' middles, clamped to
+    // bounds[G]) on lanes 0..7.
     FewBounds fb;
     bool narrow = true;
+    const int64_t *bnd = a.bounds + (int64_t)t * (a.G + 1);
     {
-        const int64_t *bnd = a.bounds + (int64_t)t * (a.G + 1);
+        constexpr int kStep = kBits == 3 ? 1 : 2;
         fb.lo = uniform64(bnd[0]);
         fb.hi = uniform64(bnd[a.G]);
 #pragma unroll
-        for (int j = 1; j < kFewShards; ++j) fb.inner[j - 1] = j < a.G ? uniform64(bnd[j]) : INT64_MAX;
+        for (int j = 1; j < kFewShards; ++j) fb.inner[j - 1] = kStep * j < a.G ? uniform64(bnd[kStep * j]) : INT64_MAX;
         narrow = few_bounds_narrow(fb);
+    }
+    int32_t odd32 = 0;
+    if (kBits == 4 && lane < kFewShards) {
+        const int64_t m = bnd[min(2 * lane + 1, a.G)];
+        odd32 = (int32_t)min(max(m, fb.lo), max(fb.lo, fb.hi)); // used only when narrow
     }
     const int n32 = (int)n; // at most kOneChunks * 64
     if (n > 0 && !narrow) {
         for (int u = 0; u < a.K; ++u) {
             const int64_t id = u * kWave + lane < n32 ? (int64_t)src[(int64_t)u * kWave] : 0;
-            one_record(W, u, lane, few_owner_masks(fb, id, lanes_below(n32 - u * kWave)), run, l0, l1, l2);
+            const uint64_t in = lanes_below(n32 - u * kWave);
+            OneMasks o;
+            if constexpr (kBits == 3) {
+                o = one_masks(few_owner_masks(fb, id, in));
+            } else {
+                const TreeMasks tm = tree_owner_masks(TreeBounds{fb, bnd, a.G}, id, in);
+                o = OneMasks{tm.valid, {tm.b[0], tm.b[1], tm.b[2], tm.b[3]}};
+            }
+            one_record<kBits>(W, u, lane, o, run, mine);
         }
     } else if (n > 0) {
         // A rolling pipeline over all kChunks chunks, straight-line code:
-        // chunk u's register, once processed, loads chunk u + kOneGroup, so
-        // that kOneGroup loads stay in flight while the wave works and each
+        // chunk u's register, once processed, loads chunk u + kGroup, so
+        // that kGroup loads stay in flight while the wave works and each
         // wait covers only the oldest.  Chunks past the wave's ids load 0
         // (the buffer's size) and record no ids.
         const FewBounds32 f32 = few_bounds32(fb);
         const __amdgpu_buffer_rsrc_t rs = one_rsrc((const IT *)a.indices + ps, n32 * (int)sizeof(IT));
-        IT raw[kOneGroup];
+        IT raw[kGroup];
 #pragma unroll
-        for (int j = 0; j < kOneGroup; ++j) raw[j] = one_buffer_load<IT>(rs, (j * kWave + lane) * (int)sizeof(IT));
+        for (int j = 0; j < kGroup; ++j) raw[j] = one_buffer_load<IT>(rs, (j * kWave + lane) * (int)sizeof(IT));
         one_each<kChunks>([&](auto U) __attribute__((always_inline)) {
-            constexpr int u = decltype(U)::value, j = u % kOneGroup;
+            constexpr int u = decltype(U)::value, j = u % kGroup;
             const int32_t lo = (int32_t)raw[j];
             uint64_t in = lanes_below(n32 - u * kWave);
             if constexpr (sizeof(IT) == 8) in &= __ballot((int32_t)((int64_t)raw[j] >> 32) == (lo >> 31));
             held[u] = sizeof(IT) == 8 ? one_copy((uint32_t)lo) : (uint32_t)lo;
-            one_record(W, u, lane, few_owner_masks32(f32, lo, in), run, l0, l1, l2);
-            if constexpr (u + kOneGroup < kChunks)
-                raw[j] = one_buffer_load<IT>(rs, ((u + kOneGroup) * kWave + lane) * (int)sizeof(IT));
+            const FewMasks f = few_owner_masks32(f32, lo, in);
+            if constexpr (kBits == 3) {
+                one_record<kBits>(W, u, lane, one_masks(f), run, mine);
+            } else {
+                // the pair's middle bound, from the lane numbered by the pair
+                const int32_t mid = __builtin_amdgcn_ds_bpermute(few_bits<4>(f), odd32);
+                one_record<kBits>(W, u, lane, OneMasks{f.valid, {__ballot(lo >= mid), f.b0, f.b1, f.b2}}, run, mine);
+            }
+            if constexpr (u + kGroup < kChunks)
+                raw[j] = one_buffer_load<IT>(rs, ((u + kGroup) * kWave + lane) * (int)sizeof(IT));
             __builtin_amdgcn_sched_barrier(0); // one chunk at a time: registers hold the ids
         });
     }
@@ -1901,19 +1969,24 @@ __global__ __launch_bounds__(kOneBlock) __attribute__((amdgpu_waves_per_eu(4, 4)
     // order.)
     const bool wave_disorder = __ballot(disorder) != 0;
     if (lane == 0) {
-        W.rec[a.K] = OneRec{0, 0, 0, 0};
+        W.rec[a.K] = OneRec<kBits>{};
         L.wave_flag[wave] = wave_disorder;
     }
-    if (lane < kFewShards) {
+    if (lane < kD) {
         W.cum[a.K][lane] = (uint16_t)run;
         L.wave_total[wave][lane] = run;
     }
     __syncthreads();
-    if (threadIdx.x < kFewShards) {
-        int32_t x = 0;
-        for (int w = 0; w < kOneWaves; ++w) x += L.wave_total[w][threadIdx.x];
-        one_store(a.block_totals + (int64_t)lb * kFewShards + threadIdx.x, x);
-    } else if (threadIdx.x == kFewShards) {
+    // (a workgroup holds at most 8 waves x kOneChunks x 64 ids: 16 bits)
+    static_assert(kOneWaves * kOneChunks * kWave < 65536, "16-bit workgroup totals");
+    if (threadIdx.x < kD / 2) {
+        int32_t x0 = 0, x1 = 0;
+        for (int w = 0; w < kOneWaves; ++w) {
+            x0 += L.wave_total[w][2 * threadIdx.x];
+            x1 += L.wave_total[w][2 * threadIdx.x + 1];
+        }
+        one_store(a.block_totals + (int64_t)lb * (kD / 2) + threadIdx.x, x0 | (x1 << 16));
+    } else if (threadIdx.x == kD) {
         int32_t f = 0;
         for (int w = 0; w < kOneWaves; ++w) f |= L.wave_flag[w];
         if (f) __hip_atomic_fetch_or(a.disorder, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -1921,45 +1994,48 @@ __global__ __launch_bounds__(kOneBlock) __attribute__((amdgpu_waves_per_eu(4, 4)
     if (!one_grid_barrier(a, gridDim.x, &L.pass)) return; // cancelled: the other kernels write the outputs
 
     // Phase 2: the workgroups' totals before this one and in all, and the
-    // offsets' flag: thread b reads workgroup b's 32-byte record (two loads
-    // past the L2s), each wave adds up its 64 workgroups, then the waves' sums.
+    // offsets' flag: thread b reads workgroup b's record (16-byte loads past
+    // the L2s, 8 destinations each), each wave adds up its 64 workgroups,
+    // then the waves' sums.
     {
         const int nb = gridDim.x;
         const int b = threadIdx.x; // kOneBlock >= workgroups in the grid
-        int32_t x[kFewShards];
-        if (b < nb) {
-            typedef int v4i __attribute__((ext_vector_type(4)));
-            const __amdgpu_buffer_rsrc_t rt = one_rsrc(a.block_totals, nb * kFewShards * 4);
-            const v4i p = __builtin_bit_cast(v4i, __builtin_amdgcn_raw_buffer_load_b128(rt, b * 32, 0, 16));
-            const v4i q = __builtin_bit_cast(v4i, __builtin_amdgcn_raw_buffer_load_b128(rt, b * 32 + 16, 0, 16));
-            x[0] = p.x; x[1] = p.y; x[2] = p.z; x[3] = p.w;
-            x[4] = q.x; x[5] = q.y; x[6] = q.z; x[7] = q.w;
-        } else {
+        typedef int v4i __attribute__((ext_vector_type(4)));
+        const __amdgpu_buffer_rsrc_t rt = one_rsrc(a.block_totals, nb * kD * 2);
+#pragma unroll 1
+        for (int h = 0; h < kD / kFewShards; ++h) { // (a loop: the held ids leave registers for one half)
+            int32_t x[kFewShards];
+            if (b < nb) {
+                const v4i p = __builtin_bit_cast(v4i, __builtin_amdgcn_raw_buffer_load_b128(rt, b * kD * 2 + h * 16, 0, 16));
+                x[0] = p.x & 0xFFFF; x[1] = (uint32_t)p.x >> 16; x[2] = p.y & 0xFFFF; x[3] = (uint32_t)p.y >> 16;
+                x[4] = p.z & 0xFFFF; x[5] = (uint32_t)p.z >> 16; x[6] = p.w & 0xFFFF; x[7] = (uint32_t)p.w >> 16;
+            } else {
 #pragma unroll
-            for (int g = 0; g < kFewShards; ++g) x[g] = 0;
-        }
-        int32_t before[kFewShards], all[kFewShards];
-#pragma unroll
-        for (int g = 0; g < kFewShards; ++g) {
-            before[g] = b < lb ? x[g] : 0;
-            all[g] = x[g];
-        }
-        for (int m = kWave / 2; m >= 1; m >>= 1) {
-#pragma unroll
-            for (int g = 0; g < kFewShards; ++g) {
-                before[g] += __shfl_xor(before[g], m);
-                all[g] += __shfl_xor(all[g], m);
+                for (int g = 0; g < kFewShards; ++g) x[g] = 0;
             }
-        }
-        if (lane == 0) {
+            int32_t before[kFewShards], all[kFewShards];
 #pragma unroll
             for (int g = 0; g < kFewShards; ++g) {
-                L.part_before[wave][g] = before[g];
-                L.part_all[wave][g] = all[g];
+                before[g] = b < lb ? x[g] : 0;
+                all[g] = x[g];
+            }
+            for (int m = kWave / 2; m >= 1; m >>= 1) {
+#pragma unroll
+                for (int g = 0; g < kFewShards; ++g) {
+                    before[g] += __shfl_xor(before[g], m);
+                    all[g] += __shfl_xor(all[g], m);
+                }
+            }
+            if (lane == 0) {
+#pragma unroll
+                for (int g = 0; g < kFewShards; ++g) {
+                    L.part_before[wave][h * kFewShards + g] = before[g];
+                    L.part_all[wave][h * kFewShards + g] = all[g];
+                }
             }
         }
         __syncthreads();
-        if (threadIdx.x < kFewShards) {
+        if (threadIdx.x < kD) {
             int64_t bs = 0, as = 0;
             for (int w = 0; w < kOneWaves; ++w) {
                 bs += L.part_before[w][threadIdx.x];
@@ -1968,7 +2044,7 @@ __global__ __launch_bounds__(kOneBlock) __attribute__((amdgpu_waves_per_eu(4, 4)
             L.block_base[threadIdx.x] = bs;
             L.total[threadIdx.x] = as;
         }
-        if (threadIdx.x == kFewShards) L.flag = one_load(a.disorder);
+        if (threadIdx.x == kD) L.flag = one_load(a.disorder);
     }
     __syncthreads();
     if (L.flag) return; // offsets not ordinary: the other kernels write the outputs
@@ -1981,7 +2057,7 @@ __global__ __launch_bounds__(kOneBlock) __attribute__((amdgpu_waves_per_eu(4, 4)
         if (threadIdx.x == 0) *a.done = 1;
     }
     int64_t slot = 0; // lane g < G: where this wave's first id for g goes
-    if (lane < kFewShards) {
+    if (lane < kD) {
         int64_t lbase = 0;
         if (lane < a.G) {
             lbase = L.block_base[lane];
@@ -1999,7 +2075,7 @@ __global__ __launch_bounds__(kOneBlock) __attribute__((amdgpu_waves_per_eu(4, 4)
     IT *out = (IT *)a.out_indices;
     if (n > 0 && !narrow) {
         for (int u = 0; u < a.K; ++u)
-            one_store_chunk<IT>(a, W, lane, slot, u, u * kWave + lane < n32 ? (int64_t)src[(int64_t)u * kWave] : 0, out);
+            one_store_chunk<IT, kBits>(a, W, lane, slot, u, u * kWave + lane < n32 ? (int64_t)src[(int64_t)u * kWave] : 0, out);
     } else if (n > 0) {
         one_each<kChunks / kOneStoreGroup>([&](auto G0) __attribute__((always_inline)) {
             constexpr int g0 = decltype(G0)::value * kOneStoreGroup;
@@ -2008,7 +2084,7 @@ __global__ __launch_bounds__(kOneBlock) __attribute__((amdgpu_waves_per_eu(4, 4)
                 for (int j = 0; j < kOneStoreGroup; ++j) {
                     const int u = g0 + j;
                     const uint32_t h = sizeof(IT) == 8 ? one_copy(held[u]) : held[u];
-                    one_store_chunk<IT>(a, W, lane, slot, u, (int64_t)(int32_t)h, out);
+                    one_store_chunk<IT, kBits>(a, W, lane, slot, u, (int64_t)(int32_t)h, out);
                     __builtin_amdgcn_sched_barrier(0);
                 }
             }
@@ -2019,23 +2095,24 @@ __global__ __launch_bounds__(kOneBlock) __attribute__((amdgpu_waves_per_eu(4, 4)
     if (v < used) {
         const int64_t pb0 = max<int64_t>(0, one_load(a.first_bag + v));
         const int64_t pb1 = min<int64_t>(a.TB + 1, one_load(a.first_bag + v + 1));
-        int64_t wb[kFewShards];
+        int64_t wb[kD];
 #pragma unroll
-        for (int g = 0; g < kFewShards; ++g) wb[g] = L.wave_base[wave][g];
+        for (int g = 0; g < kD; ++g) wb[g] = L.wave_base[wave][g];
         const int64_t row = a.TB + 1;
         for (int64_t p = pb0 + lane; p < pb1; p += kWave) {
             // A boundary at the end of the wave's ids takes the totals'
             // record (so that a wave without ids reads only that one).
             const int64_t x = max<int64_t>(0, min<int64_t>((int64_t)off[p] - ps, n));
             const int u = x >= n ? a.K : (int)(x >> 6), rr = x >= n ? 0 : (int)(x & 63);
-            const OneRec r = W.rec[u];
+            const OneRec<kBits> r = W.rec[u];
             const uint64_t below = rr == 0 ? 0ull : (~0ull >> (64 - rr));
             const uint64_t v0 = r.valid & below;
 #pragma unroll
-            for (int g = 0; g < kFewShards; ++g) {
+            for (int g = 0; g < kD; ++g) {
                 if (g < a.G) {
-                    const uint64_t leaf = v0 & ((g & 1) ? r.b0 : ~r.b0) & ((g & 2) ? r.b1 : ~r.b1) &
-                                          ((g & 4) ? r.b2 : ~r.b2);
+                    uint64_t leaf = v0;
+#pragma unroll
+                    for (int k = 0; k < kBits; ++k) leaf &= ((g >> k) & 1) ? r.b[k] : ~r.b[k];
                     a.out_offsets[(int64_t)g * row + p] = wb[g] + W.cum[u][g] + __popcll(leaf);
                 }
             }
@@ -2123,23 +2200,30 @@ const void *scatter_kernel(int G)
                               : (const void *)eb_bucket_scatter<IT, kMaxShards>;
 }
 
-template <typename IT, int kChunks>
-const void *one_pass_kernel() { return (const void *)eb_bucket_onepass<IT, kChunks>; }
+template <typename IT, int kChunks, int kBits>
+const void *one_pass_kernel() { return (const void *)eb_bucket_onepass<IT, kChunks, kBits>; }
 
-template <typename IT>
+template <typename IT, int kBits>
 const void *one_pass_kernel_for(int K)
 {
     static_assert(kOneChunkSizes[0] == 16 && kOneChunkSizes[1] == 32 && kOneChunkSizes[2] == 48, "sizes");
-    return K <= 16 ? one_pass_kernel<IT, 16>() : K <= 32 ? one_pass_kernel<IT, 32>()
-           : K <= 48 ? one_pass_kernel<IT, 48>() : one_pass_kernel<IT, kOneChunks>();
+    return K <= 16 ? one_pass_kernel<IT, 16, kBits>() : K <= 32 ? one_pass_kernel<IT, 32, kBits>()
+           : K <= 48 ? one_pass_kernel<IT, 48, kBits>() : one_pass_kernel<IT, kOneChunks, kBits>();
 }
 
-template <typename IT, int kChunks>
+template <typename IT, int kChunks, int kBits>
 int one_pass_occupancy()
 {
     int per = 0;
-    return hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, one_pass_kernel<IT, kChunks>(), kOneBlock,
-                                                        sizeof(OneBlockLds)) == hipSuccess ? per : 0;
+    return hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, one_pass_kernel<IT, kChunks, kBits>(), kOneBlock,
+                                                        sizeof(OneBlockLds<kBits>)) == hipSuccess ? per : 0;
+}
+
+template <typename IT, int kBits>
+int one_pass_occupancy_all()
+{
+    return std::min({one_pass_occupancy<IT, 16, kBits>(), one_pass_occupancy<IT, 32, kBits>(),
+                     one_pass_occupancy<IT, 48, kBits>(), one_pass_occupancy<IT, kOneChunks, kBits>()});
 }
 
 // The one-pass kernel's workgroups: kOneBlocksPerCu per compute unit when
@@ -2156,11 +2240,8 @@ int one_pass_blocks()
     b = 0;
     if (hipGetDevice(&dev) == hipSuccess &&
         hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
-        std::min({one_pass_occupancy<int64_t, 16>(), one_pass_occupancy<int64_t, 32>(),
-                  one_pass_occupancy<int64_t, 48>(), one_pass_occupancy<int64_t, kOneChunks>(),
-                  one_pass_occupancy<int32_t, 16>(), one_pass_occupancy<int32_t, 32>(),
-                  one_pass_occupancy<int32_t, 48>(), one_pass_occupancy<int32_t, kOneChunks>()}) >=
-            kOneBlocksPerCu &&
+        std::min({one_pass_occupancy_all<int64_t, 3>(), one_pass_occupancy_all<int32_t, 3>(),
+                  one_pass_occupancy_all<int64_t, 4>(), one_pass_occupancy_all<int32_t, 4>()}) >= kOneBlocksPerCu &&
         cus * kOneBlocksPerCu <= kOneBlock)
         b = cus * kOneBlocksPerCu;
     cached.store(b, std::memory_order_release);
@@ -2200,7 +2281,7 @@ int one_pass_setting()
 bool one_pass_fits(int32_t T, int64_t B, int32_t G, int64_t nnz, hipStream_t st)
 {
     const int setting = one_pass_setting();
-    if (setting == 0 || G > kFewShards || T < 1 || T > kOneMaxTables || nnz < 1) return false;
+    if (setting == 0 || G > kTreeShards || T < 1 || T > kOneMaxTables || nnz < 1) return false;
     if ((int64_t)T * B >= ((int64_t)1 << 31) - 2 || nnz >= ((int64_t)1 << 31)) return false; // 32-bit positions
     if (setting < 0 && nnz < kOneMinIds) return false;
     // Under a graph capture the kernels record like any others (the clear
@@ -2317,7 +2398,7 @@ int bucketize_impl(int32_t T, int64_t B, int32_t G, const int64_t *bounds, int32
     sa.bags_per_wave = cbags;
     sa.mode = direct_scan(G, sa.ntiles, sa.nparts) ? kScanDirect : fused_scan(G, sa.ntiles) ? kScanFused : kScanRows;
 
-    // Ordinary offsets and up to 8 destinations: the one-pass kernel, with
+    // Ordinary offsets and up to 16 destinations: the one-pass kernel, with
     // the three kernels launched behind it, which return at once when it
     // has written the outputs (`done`) and do the work when it could not
     // (offsets not ordinary, a cancelled barrier).
@@ -2353,8 +2434,11 @@ int bucketize_impl(int32_t T, int64_t B, int32_t G, const int64_t *bounds, int32
         void *oargs[] = {&oa};
         hipError_t err = hipLaunchKernel((const void *)eb_one_clear, dim3(1), dim3(kWave), oargs, 0, st);
         if (err == hipSuccess)
-            err = hipLaunchKernel(i32 ? one_pass_kernel_for<int32_t>(oa.K) : one_pass_kernel_for<int64_t>(oa.K),
-                                  dim3(blocks), dim3(kOneBlock), oargs, sizeof(OneBlockLds), st);
+            err = G <= kFewShards
+                      ? hipLaunchKernel(i32 ? one_pass_kernel_for<int32_t, 3>(oa.K) : one_pass_kernel_for<int64_t, 3>(oa.K),
+                                        dim3(blocks), dim3(kOneBlock), oargs, sizeof(OneBlockLds<3>), st)
+                      : hipLaunchKernel(i32 ? one_pass_kernel_for<int32_t, 4>(oa.K) : one_pass_kernel_for<int64_t, 4>(oa.K),
+                                        dim3(blocks), dim3(kOneBlock), oargs, sizeof(OneBlockLds<4>), st);
         if (err != hipSuccess) return fail(EB_ERR_HIP, "eb_bucketize: %s", hipGetErrorString(err));
         ba.skip = oa.done;
         sa.skip = oa.done;

@@ -21,7 +21,7 @@ pytestmark = pytest.mark.gpu
 @pytest.fixture(params=["three-kernel", "one-pass"], autouse=True)
 def bucketize_path(request, monkeypatch):
     """Every test runs twice: with eb_bucketize's three kernels, and with its
-    one-pass kernel wherever that applies (at most 8 destinations, also in a
+    one-pass kernel wherever that applies (at most 16 destinations, also in a
     graph capture once an eager call has run), whatever the batch's size."""
     monkeypatch.setenv("EB_BUCKETIZE_ONE_PASS", "0" if request.param == "three-kernel" else "1")
 
@@ -72,7 +72,7 @@ def check_bucketize(T, B, idx, off, bounds, device, capacity=None, index_dtype=n
         assert np.array_equal(a, b), name
 
 
-@pytest.mark.parametrize("G", [1, 2, 3, 8, 17, 64, 65, 128, 129, 1024])
+@pytest.mark.parametrize("G", [1, 2, 3, 8, 9, 16, 17, 64, 65, 128, 129, 1024])
 @pytest.mark.parametrize("seed", range(3))
 def test_bucketize_matches_oracle(G, seed, device):
     T, B, idx, off, bounds = bucket_case(seed * 31 + G, G, uneven=(seed == 2))
@@ -423,7 +423,7 @@ def one_pass_case(seed, G, layout, T=4, B=600):
     return T, B, idx, off, even_bounds(rows, G)
 
 
-@pytest.mark.parametrize("G", [1, 5, 8])
+@pytest.mark.parametrize("G", [1, 5, 8, 12, 16])
 @pytest.mark.parametrize("layout", ["inner-offsets", "empty-tables", "huge-bag", "short-capacity"])
 def test_bucketize_one_pass_layouts(G, layout, device):
     T, B, idx, off, bounds = one_pass_case(G * 7 + len(layout), G, layout)
@@ -434,8 +434,9 @@ def test_bucketize_one_pass_layouts(G, layout, device):
     check_bucketize(T, B, idx, off, bounds, device, capacity=cap)
 
 
+@pytest.mark.parametrize("G", [8, 16])
 @pytest.mark.parametrize("nnz", [4_150_000, 4_400_000])
-def test_bucketize_one_pass_kernel_sizes(nnz, device):
+def test_bucketize_one_pass_kernel_sizes(nnz, G, device):
     """Batches on either side of the 16-chunk kernel's capacity (with 4096
     resident waves: 16 x 64 ids per wave), one in each kernel size."""
     g = np.random.default_rng(nnz)
@@ -443,7 +444,7 @@ def test_bucketize_one_pass_kernel_sizes(nnz, device):
     L = g.multinomial(nnz, np.full(T * B, 1.0 / (T * B)))
     off = wl.offsets_from_lengths(L)
     idx = g.integers(0, rows, int(off[-1]), dtype=np.int64)
-    check_bucketize(T, B, idx, off, even_bounds([rows] * T, 8), device)
+    check_bucketize(T, B, idx, off, even_bounds([rows] * T, G), device)
 
 
 @pytest.mark.parametrize("where", [12_345, 200_001, 333_333])
@@ -461,7 +462,7 @@ def test_bucketize_one_decreasing_offset(where, device):
     check_bucketize(T, B, idx, off, even_bounds([rows] * T, 8), device)
 
 
-@pytest.mark.parametrize("G", [2, 8])
+@pytest.mark.parametrize("G", [2, 8, 16])
 def test_bucketize_cancelled_barrier(G, device, monkeypatch):
     """With the barrier's wait cut to no polls (a test-only setting), the
     workgroups that find it incomplete cancel it: the one-pass kernel then

@@ -16,7 +16,7 @@ pytestmark = pytest.mark.gpu
 @pytest.fixture(params=["three-kernel", "one-pass"], autouse=True)
 def bucketize_path(request, monkeypatch):
     """Every test runs twice: with eb_bucketize's three kernels, and with its
-    one-pass kernel wherever that applies (at most 8 destinations, also in a
+    one-pass kernel wherever that applies (at most 16 destinations, also in a
     graph capture once an eager call has run), whatever the batch's size."""
     monkeypatch.setenv("EB_BUCKETIZE_ONE_PASS", "0" if request.param == "three-kernel" else "1")
 
