@@ -2266,7 +2266,9 @@ constexpr size_t kOnePassWorkspace =
 // (8 destinations), first B bags of each, the one-pass path took 33.0 / 35.9
 // / 38.1 / 45.5 / 49.2 us against 25.7 / 32.8 / 40.4 / 48.7 / 62.5 us for B =
 // 1024 / 2048 / 3072 / 4096 / 6144 (1.3 to 7.9 M ids), one process each; its
-// launches, barrier and set-up cost about the same at any size.
+// launches, barrier and set-up cost about the same at any size.  At 16
+// destinations: 39.8 / 43.6 / 45.7 against 29.0 / 39.6 / 49.1 us for B = 1024
+// / 2048 / 3072, at 12: 39.3 / 42.7 / 45.6 against 28.7 / 37.9 / 45.5 us.
 constexpr int64_t kOneMinIds = (int64_t)7 << 19; // 3.67 M
 
 // EB_BUCKETIZE_ONE_PASS=0 never takes the one-pass kernel, =1 takes it for
