@@ -447,6 +447,31 @@ def test_bucketize_one_pass_kernel_sizes(nnz, G, device):
     check_bucketize(T, B, idx, off, even_bounds([rows] * T, G), device)
 
 
+@pytest.mark.parametrize("T", [300, 1024, 1025])
+def test_bucketize_many_tables(T, device):
+    """More tables than a wave has lanes: the one-pass kernel lays out the
+    tables' waves 64 tables at a time (a running carry) and finds each
+    wave's table the same way; 1024 tables is its maximum (1025 takes the
+    three kernels); some tables are empty."""
+    g = np.random.default_rng(T)
+    B = 30
+    rows = [int(g.integers(100, 20_000)) for _ in range(T)]
+    L = g.integers(0, 30, T * B)
+    L[g.choice(T, T // 10, replace=False)[:, None] * B + np.arange(B)] = 0
+    off = wl.offsets_from_lengths(L)
+    idx = np.concatenate([g.integers(-2, rows[t] + 2, int(off[(t + 1) * B] - off[t * B])) for t in range(T)])
+    check_bucketize(T, B, idx.astype(np.int64), off, even_bounds(rows, 8), device)
+
+
+def test_bucketize_dlrm_batch_int32(device):
+    # the 26-table, 16384-bag, Zipf(1.05) batch as int32 ids and offsets
+    # (eb_bucketize_ex), split over 8 GPUs by rows
+    w = wl.config(3)
+    off = w.offsets()
+    idx = w.indices(off)
+    check_bucketize(w.T, w.B, idx, off, even_bounds([w.rows] * w.T, 8), device, index_dtype=np.int32)
+
+
 @pytest.mark.parametrize("where", [12_345, 200_001, 333_333])
 def test_bucketize_one_decreasing_offset(where, device):
     """Ordinary offsets but for a single one that decreases, in a batch with
