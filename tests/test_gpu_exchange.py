@@ -447,6 +447,32 @@ def test_bucketize_one_pass_kernel_sizes(nnz, G, device):
     check_bucketize(T, B, idx, off, even_bounds([rows] * T, G), device)
 
 
+@pytest.mark.parametrize("seed", range(24))
+def test_bucketize_random_layouts(seed, device):
+    """Random batches over the shapes the one-pass kernel lays out: 1 to 16
+    destinations, 1 to 200 tables, runs of empty bags and tables, offsets
+    that may start above 0 and end before nnz, even or uneven bounds, int64
+    or int32 ids; against the oracle."""
+    g = np.random.default_rng(1000 + seed)
+    G = int(g.integers(1, 17))
+    T = int(g.integers(1, 201))
+    B = int(g.integers(1, 2001 // max(1, T // 20)))
+    rows = [int(g.integers(1, 200_000)) for _ in range(T)]
+    L = g.integers(0, int(g.integers(1, 80)), T * B)
+    L[g.random(T * B) < g.random() * 0.5] = 0
+    off = wl.offsets_from_lengths(L)
+    lead, tail = (int(g.integers(0, 50)), int(g.integers(0, 50))) if seed % 3 == 0 else (0, 0)
+    off = off + lead
+    nnz = int(off[-1]) + tail
+    idx = g.integers(-5, max(rows) + 5, nnz).astype(np.int64)
+    if seed % 2:
+        bounds = np.sort(g.integers(0, max(rows) + 1, (T, G + 1)), axis=1)
+    else:
+        bounds = even_bounds(rows, G)
+    i32 = seed % 4 == 1
+    check_bucketize(T, B, idx, off, bounds, device, index_dtype=np.int32 if i32 else np.int64)
+
+
 @pytest.mark.parametrize("T", [300, 1024, 1025])
 def test_bucketize_many_tables(T, device):
     """More tables than a wave has lanes: the one-pass kernel lays out the
