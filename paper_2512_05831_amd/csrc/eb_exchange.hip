@@ -1578,14 +1578,6 @@ __device__ __forceinline__ void one_each(F f)
     one_each_(f, std::make_integer_sequence<int, N>{});
 }
 
-// The lanes of `valid` whose owner bits equal (x0, x1, x2) (each all ones
-// or zero), for one 32-bit half of the masks.
-__device__ __forceinline__ uint32_t one_same(uint32_t valid, uint32_t b0, uint32_t b1, uint32_t b2, uint32_t x0,
-                                             uint32_t x1, uint32_t x2)
-{
-    return valid & ~((b0 ^ x0) | (b1 ^ x1) | (b2 ^ x2));
-}
-
 // The grid-wide barrier: true once all n workgroups have arrived.  The
 // workgroup whose increment completes the count sets every XCD's release
 // word (one 128-byte line each, so that each XCD's workgroups poll their own
