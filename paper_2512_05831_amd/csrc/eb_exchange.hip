@@ -2221,22 +2221,32 @@ int one_pass_occupancy_all()
 // The one-pass kernel's workgroups: kOneBlocksPerCu per compute unit when
 // the runtime reports that many resident and phase 2's one thread per
 // workgroup suffices, else 0 (the path is not taken).
-std::atomic<int> g_one_pass_blocks{-1}; // -1 until the first eager call has asked the runtime
+// Per device: 0 until the first eager call on it has asked the runtime, then
+// the workgroups + 1.
+constexpr int kOneMaxDevices = 64;
+std::atomic<int> g_one_pass_blocks[kOneMaxDevices];
+
+int current_device()
+{
+    int dev = -1;
+    return hipGetDevice(&dev) == hipSuccess && dev >= 0 && dev < kOneMaxDevices ? dev : -1;
+}
 
 int one_pass_blocks()
 {
-    std::atomic<int> &cached = g_one_pass_blocks;
+    const int dev = current_device();
+    if (dev < 0) return 0;
+    std::atomic<int> &cached = g_one_pass_blocks[dev];
     int b = cached.load(std::memory_order_acquire);
-    if (b >= 0) return b;
-    int dev = 0, cus = 0;
+    if (b > 0) return b - 1;
+    int cus = 0;
     b = 0;
-    if (hipGetDevice(&dev) == hipSuccess &&
-        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
         std::min({one_pass_occupancy_all<int64_t, 3>(), one_pass_occupancy_all<int32_t, 3>(),
                   one_pass_occupancy_all<int64_t, 4>(), one_pass_occupancy_all<int32_t, 4>()}) >= kOneBlocksPerCu &&
         cus * kOneBlocksPerCu <= kOneBlock)
         b = cus * kOneBlocksPerCu;
-    cached.store(b, std::memory_order_release);
+    cached.store(b + 1, std::memory_order_release);
     return b;
 }
 
@@ -2284,7 +2294,10 @@ bool one_pass_fits(int32_t T, int64_t B, int32_t G, int64_t nnz, hipStream_t st)
     // three kernels.
     hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
     if (hipStreamIsCapturing(st, &cs) != hipSuccess) return false;
-    if (cs != hipStreamCaptureStatusNone && g_one_pass_blocks.load(std::memory_order_acquire) < 0) return false;
+    if (cs != hipStreamCaptureStatusNone) {
+        const int dev = current_device();
+        if (dev < 0 || g_one_pass_blocks[dev].load(std::memory_order_acquire) == 0) return false;
+    }
     const int blocks = one_pass_blocks();
     if (blocks <= 0) return false;
     return one_pass_chunks(nnz, (int64_t)blocks * kOneWaves, T) <= kOneChunks;
